@@ -1,0 +1,302 @@
+"""Plain CPU oracle of TreeFlash drafting (arXiv 2606.03819).
+
+TEST INFRASTRUCTURE ONLY.  This module is imported by the tests, by the smoke
+check of the entry module and by the CPU-baseline leg of the benchmark.  The
+HIP library never imports, links or calls it, and it shares no code with the
+library: it uses nothing but NumPy and the Python standard library.
+
+What it computes (paper: Method section, "AR-Approximation", Eq. 1, and
+Appendix B, the "AR-approximated OPT-Tree Construction" algorithm):
+
+Part 1 -- AR-approximated distributions
+  * stage 1: ``q_{t+i} = LMHead(h_{t+i})`` for every draft depth i, and the
+    top-M candidate tokens of each depth;
+  * one conditional row per (depth, previous token) pair of the M-ary tree:
+    depth 1 is conditioned on the root token x_t, depth i >= 2 on each of the
+    M candidates of depth i-1 (so 1 + (gamma-1)*M rows per sequence);
+  * Eq. 1: ``h' = h + SwiGLU(norm(h) :: norm(Embd(prev)))`` followed by the
+    LM head and a log-softmax over the whole vocabulary.
+Part 2 -- OPT-Tree selection
+  * best-first pops of the candidate with the highest path probability until
+    the tree holds B nodes besides the root; a popped node contributes its
+    children only when its token is one of the M candidates of its depth.
+
+Arithmetic is float64 throughout, with the following readings where the paper
+is silent (each is listed in the design doc):
+  * "normalized" is RMSNorm with its own gain, eps = 1e-6;
+  * SwiGLU(x) = W_down (silu(W_gate x) * (W_up x)), no biases, x = [h~ ; e~];
+  * the LM head is a plain product with the [V, d] output embedding; logits are
+    multiplied by the inverse drafter temperature before the softmax;
+  * for bf16 workloads the oracle rounds to bf16 exactly where a bf16 operand
+    is formed for a matrix product: x, the SwiGLU activation a, and h'
+    ("mirror" rounding points); all else stays float64;
+  * path scores are float32 running sums of float32 row log-probabilities, so
+    a tree is reproducible bit for bit from the same rows;
+  * ties: top-k lists order by (value desc, token asc); tree candidates order by
+    (score desc, depth asc, rank path lexicographic asc), where the rank path
+    lists each node's position in its parent's sorted row, root to node.
+"""
+from __future__ import annotations
+
+import heapq
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+__all__ = [
+    "bf16_round", "rms_norm", "silu", "log_softmax", "topk_sorted",
+    "marginal_stage", "row_table", "previous_tokens", "ar_approximator",
+    "conditional_stage", "build_tree", "draft", "RMS_EPS",
+]
+
+RMS_EPS = 1e-6
+
+
+# ---------------------------------------------------------------- elementwise
+
+def bf16_round(x) -> np.ndarray:
+    """Round to the nearest bfloat16 value, ties to even.
+
+    bfloat16 keeps 8 significant bits.  Writing x = f * 2**e with
+    0.5 <= |f| < 1, the rounded value is round_half_even(f * 2**8) * 2**(e-8).
+    Valid for the normal bfloat16 range (|x| >= 2**-126) and for zero.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    f, e = np.frexp(x)
+    return np.ldexp(np.round(np.ldexp(f, 8)), e - 8)
+
+
+def rms_norm(x: np.ndarray, gain: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+    """x / sqrt(mean(x**2) + eps) * gain over the last axis (Method, Eq. 1)."""
+    x = np.asarray(x, dtype=np.float64)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * np.asarray(gain, dtype=np.float64)
+
+
+def silu(g: np.ndarray) -> np.ndarray:
+    """SiLU(g) = g * sigmoid(g) = g / (1 + exp(-g))."""
+    g = np.asarray(g, dtype=np.float64)
+    return g / (1.0 + np.exp(-g))
+
+
+def log_softmax(z: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Log-softmax over the last axis; returns (log-probs, log-sum-exp)."""
+    z = np.asarray(z, dtype=np.float64)
+    m = np.max(z, axis=-1, keepdims=True)
+    lse = m + np.log(np.sum(np.exp(z - m), axis=-1, keepdims=True))
+    return z - lse, lse[..., 0]
+
+
+def topk_sorted(values: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k largest entries per row, ordered (value desc, index asc).
+
+    A stable sort of the negated values keeps equal values in ascending index
+    order, which is the tie rule.
+    """
+    order = np.argsort(-np.asarray(values, dtype=np.float64), axis=-1, kind="stable")
+    return order[..., :k]
+
+
+# ------------------------------------------------------------------- Part 1
+
+def marginal_stage(h: np.ndarray, lm_head: np.ndarray, k: int,
+                   inv_temperature: float = 1.0) -> Dict[str, np.ndarray]:
+    """Stage 1 (Appendix B, Part 1, first loop): LM head on every depth, top-M.
+
+    h: [b, gamma, d]; lm_head: [V, d] (row v is the output embedding of v).
+    Returns logits z [b, gamma, V] (temperature applied), log-probs, the top-k
+    ids [b, gamma, k] and their log-probs.
+    """
+    h = np.asarray(h, dtype=np.float64)
+    w = np.asarray(lm_head, dtype=np.float64)
+    z = inv_temperature * np.matmul(h, w.T)
+    lp, lse = log_softmax(z)
+    idx = topk_sorted(z, k)
+    return {
+        "logits": z,
+        "logprob": lp,
+        "lse": lse,
+        "topk_idx": idx.astype(np.int32),
+        "topk_logprob": np.take_along_axis(lp, idx, axis=-1),
+    }
+
+
+def row_table(gamma: int, M: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Rows of the conditional table (Appendix B, Part 1, second block).
+
+    Row 0 is depth 1 conditioned on the root token.  For depth i = 2..gamma and
+    candidate m = 0..M-1 the row is 1 + (i-2)*M + m, conditioned on the m-th
+    candidate of depth i-1.  Returns (depth [R], candidate slot [R]; -1 = root).
+    """
+    depth = [1]
+    slot = [-1]
+    for i in range(2, gamma + 1):
+        for m in range(M):
+            depth.append(i)
+            slot.append(m)
+    return np.asarray(depth, dtype=np.int64), np.asarray(slot, dtype=np.int64)
+
+
+def previous_tokens(root: int, topk_idx_seq: np.ndarray, gamma: int, M: int) -> np.ndarray:
+    """Token each conditional row is conditioned on (the previous token)."""
+    depth, slot = row_table(gamma, M)
+    prev = np.empty(depth.shape[0], dtype=np.int64)
+    for r in range(depth.shape[0]):
+        if slot[r] < 0:
+            prev[r] = int(root)
+        else:
+            # candidate slot[r] of depth depth[r]-1 (1-based) = index depth[r]-2
+            prev[r] = int(topk_idx_seq[depth[r] - 2, slot[r]])
+    return prev
+
+
+def ar_approximator(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
+                    emb: np.ndarray, norm_h_gain: np.ndarray, norm_e_gain: np.ndarray,
+                    w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
+                    eps: float = RMS_EPS, mirror_bf16: bool = False) -> np.ndarray:
+    """Eq. 1 for every conditional row of one sequence.
+
+    h_seq: [gamma, d] drafter states; prev/depth: [R] from row_table.
+    h'_r = h_{depth_r} + W_down( silu(W_gate x_r) * (W_up x_r) ),
+    x_r = [ rms(h_{depth_r}) ; rms(Embd(prev_r)) ].
+    With mirror_bf16, x, the activation and h' are rounded to bf16.
+    """
+    hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
+    e = np.asarray(emb, dtype=np.float64)[np.asarray(prev)]
+    x = np.concatenate([rms_norm(hd, norm_h_gain, eps), rms_norm(e, norm_e_gain, eps)], axis=-1)
+    if mirror_bf16:
+        x = bf16_round(x)
+    g = x @ np.asarray(w_gate, dtype=np.float64).T
+    u = x @ np.asarray(w_up, dtype=np.float64).T
+    a = silu(g) * u
+    if mirror_bf16:
+        a = bf16_round(a)
+    hp = hd + a @ np.asarray(w_down, dtype=np.float64).T
+    if mirror_bf16:
+        hp = bf16_round(hp)
+    return hp
+
+
+def conditional_stage(hp: np.ndarray, lm_head: np.ndarray, topk2: int,
+                      inv_temperature: float = 1.0, keep_full: bool = False
+                      ) -> Dict[str, np.ndarray]:
+    """LM head + log-softmax on every conditional row (Appendix B, Part 1).
+
+    hp: [..., R, d].  Keeps the top-topk2 entries of each row in (log-prob
+    desc, token asc) order; log-probs are handed on as float32, the precision
+    of the tree's path sums.  Each full row must sum to one.
+    """
+    z = inv_temperature * np.matmul(np.asarray(hp, dtype=np.float64),
+                                    np.asarray(lm_head, dtype=np.float64).T)
+    lp, lse = log_softmax(z)
+    total = np.sum(np.exp(lp), axis=-1)
+    if not np.all(np.abs(total - 1.0) < 1e-12):
+        raise AssertionError("conditional row does not sum to one")
+    idx = topk_sorted(lp, topk2)
+    out = {
+        "cond_idx": idx.astype(np.int32),
+        "cond_logprob": np.take_along_axis(lp, idx, axis=-1).astype(np.float32),
+        "cond_lse": lse,
+    }
+    if keep_full:
+        out["logprob"] = lp
+    return out
+
+
+# ------------------------------------------------------------------- Part 2
+
+def build_tree(cond_idx: np.ndarray, cond_logprob: np.ndarray, topk_idx_seq: np.ndarray,
+               gamma: int, M: int, B: int) -> Dict[str, np.ndarray]:
+    """OPT-Tree selection for one sequence (Appendix B, Part 2).
+
+    cond_idx / cond_logprob: [R, K] rows sorted (log-prob desc, token asc);
+    K is the full vocabulary or any K >= B (the truncated rows give the same
+    tree).  topk_idx_seq: [gamma, M] stage-1 candidates.
+
+    The queue starts with every child of the root (row 0).  Each pop appends
+    the best candidate to the tree; when the popped token is candidate m of its
+    depth and the depth is below gamma, every entry of row 1+(depth-1)*M+m is
+    queued as its child.  Pops stop when the tree holds B nodes besides the
+    root.  Returns per node, in pop order: token, parent (-1 = root), depth,
+    score (float32 path log-probability), child_row (-1 if not expandable)
+    and rank (position in the parent's row).
+    """
+    cond_idx = np.asarray(cond_idx)
+    lp32 = np.asarray(cond_logprob, dtype=np.float32)
+    K = cond_idx.shape[1]
+    heap: List[tuple] = []
+
+    def push_row(row: int, parent: int, parent_score: np.float32, depth: int, path: tuple):
+        for c in range(K):
+            s = np.float32(parent_score + lp32[row, c])        # float32 add
+            heapq.heappush(heap, (-float(s), depth, path + (c,), parent, row, c))
+
+    push_row(0, -1, np.float32(0.0), 1, ())
+    token, parent, depth_o, score, child_row, rank = [], [], [], [], [], []
+    while len(token) < B:
+        if not heap:
+            raise ValueError("draft budget exceeds the number of admissible nodes")
+        negs, dep, path, par, row, c = heapq.heappop(heap)
+        tok = int(cond_idx[row, c])
+        crow = -1
+        if dep < gamma:
+            hits = np.nonzero(np.asarray(topk_idx_seq[dep - 1]) == tok)[0]
+            if hits.size:
+                crow = 1 + (dep - 1) * M + int(hits[0])
+        token.append(tok)
+        parent.append(par)
+        depth_o.append(dep)
+        score.append(np.float32(-negs))
+        child_row.append(crow)
+        rank.append(c)
+        if crow >= 0:
+            push_row(crow, len(token) - 1, np.float32(-negs), dep + 1, path)
+    return {
+        "token": np.asarray(token, dtype=np.int32),
+        "parent": np.asarray(parent, dtype=np.int32),
+        "depth": np.asarray(depth_o, dtype=np.int32),
+        "score": np.asarray(score, dtype=np.float32),
+        "child_row": np.asarray(child_row, dtype=np.int32),
+        "rank": np.asarray(rank, dtype=np.int32),
+    }
+
+
+# ------------------------------------------------------------- whole step
+
+def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
+          inv_temperature: float = 1.0, mirror_bf16: bool = False,
+          topk2: Optional[int] = None, eps: float = RMS_EPS,
+          keep_full: bool = False, sequences: Optional[List[int]] = None
+          ) -> Dict[str, object]:
+    """One drafting step for every sequence: Part 1 then Part 2.
+
+    ``inputs`` holds float64/int64 numpy arrays: h [b, gamma, d], root [b],
+    lm_head, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down.
+    ``sequences`` restricts the work to a subset of the batch (the sequences
+    are independent).
+    """
+    h = inputs["h"]
+    b = h.shape[0]
+    V = inputs["lm_head"].shape[0]
+    K2 = min(B, V) if topk2 is None else topk2
+    seqs = list(range(b)) if sequences is None else list(sequences)
+    depth, _ = row_table(gamma, k)
+    out = {"stage1": [], "rows": [], "hprime": [], "tree": [], "prev": []}
+    for s in seqs:
+        st1 = marginal_stage(h[s:s + 1], inputs["lm_head"], k, inv_temperature)
+        st1 = {key: val[0] for key, val in st1.items()}
+        prev = previous_tokens(int(inputs["root"][s]), st1["topk_idx"], gamma, k)
+        hp = ar_approximator(h[s], prev, depth, inputs["emb"], inputs["norm_h_gain"],
+                             inputs["norm_e_gain"], inputs["w_gate"], inputs["w_up"],
+                             inputs["w_down"], eps=eps, mirror_bf16=mirror_bf16)
+        rows = conditional_stage(hp, inputs["lm_head"], K2, inv_temperature, keep_full=keep_full)
+        tree = build_tree(rows["cond_idx"], rows["cond_logprob"], st1["topk_idx"], gamma, k, B)
+        if not keep_full:
+            st1.pop("logits")
+            st1.pop("logprob")
+        out["stage1"].append(st1)
+        out["rows"].append(rows)
+        out["hprime"].append(hp)
+        out["tree"].append(tree)
+        out["prev"].append(prev)
+    return out
