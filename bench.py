@@ -1,0 +1,175 @@
+#!/usr/bin/env python3
+"""Throughput of one TreeFlash drafting step on one MI355X.
+
+A step is the whole hot path for one batch: stage 1 (marginal LM head and
+top-M), the AR approximator on every conditional row, the stage-2 LM head with
+log-softmax and top-K2, and the best-first tree.  Inputs are synthetic
+(seeded, drawn on the GPU) and resident in HBM before timing starts; several
+independent weight copies rotate between steps so that no step finds its
+weights in the 256 MB last-level cache.
+
+Prints ONE JSON line: draft trees/s (value), rows/s, per-stage times, the
+roofline of the dominant kernel (the stage-2 LM head), and the CPU oracle
+timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import torch
+
+from paper_2606_03819_amd import binding, synth
+
+METRIC = "draft trees/sec (+ conditional rows/sec) at Qwen3-8B shape; HBM GB/s or MFMA % of peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector/MFMA
+RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen3-8b-shape", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--copies", type=int, default=4, help="independent weight copies rotated per step")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=30.0, help="rough cap on the CPU baseline's work")
+    return ap.parse_args()
+
+
+def make_copies(w, n):
+    dev = torch.device("cuda", 0)
+    copies = []
+    for i in range(n):
+        wi = w.replace(weight_seed=w.weight_seed + 1000 * i)
+        device = synth.default_device_for(w)
+        ws = synth.make_weights(wi, device)
+        copies.append({k: v.to(dev) for k, v in ws.items()})
+    states = synth.make_states(w, synth.default_device_for(w))
+    return copies, {k: v.to(dev) for k, v in states.items()}
+
+
+def cpu_baseline(w, weights, states, budget_s):
+    """The oracle, untuned, on one sequence's full step (one draft tree)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    import oracle
+
+    inputs = {k: synth.to_numpy64(v) for k, v in weights.items()}
+    inputs["h"] = synth.to_numpy64(states["h"][:1])
+    inputs["root"] = synth.to_numpy64(states["root"][:1])
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    t0 = time.perf_counter()
+    oracle.draft(inputs, w.gamma, w.k, w.B, w.inv_temperature, mirror_bf16=(w.dtype == "bf16"))
+    dt = time.perf_counter() - t0
+    return {"value": 1.0 / dt, "unit": "trees/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one sequence's full drafting step (stage 1, {w.rows} conditional rows, tree); "
+                      f"{dt:.2f} s in NumPy float64 on this host",
+            "seconds": dt}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(2)
+    w = synth.get_workload(args.workload)
+    torch.cuda.set_device(0)
+    binding.lib()
+    copies, st = make_copies(w, max(1, args.copies))
+    dev = torch.device("cuda", 0)
+    d, V, R, b = w.d, w.V, w.rows, w.b
+    dr = binding.Drafter(copies[0], b, w.gamma, w.k, w.B, w.inv_temperature)
+    hp = torch.empty((b, R, d), dtype=w.torch_dtype, device=dev)
+    h, root = st["h"], st["root"]
+
+    def step(i, ev=None):
+        wt = copies[i % len(copies)]
+        if ev is not None:
+            ev[0].record()
+        binding.treeflash_marginal_topk(h, wt["lm_head"], w.k, w.inv_temperature, dr.workspace, dr.topk_idx,
+                                        dr.topk_lp)
+        if ev is not None:
+            ev[1].record()
+        binding.treeflash_arapprox_hidden(h, root, dr.topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
+                                          wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, dr.workspace, hp, V)
+        if ev is not None:
+            ev[2].record()
+        binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
+                                        dr.cond_idx, dr.cond_lp, dr.cond_lse)
+        if ev is not None:
+            ev[3].record()
+        binding.treeflash_build_tree(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
+        if ev is not None:
+            ev[4].record()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    stage_ms = {"stage1_lmhead_topk": 0.0, "arapprox_mlp": 0.0, "stage2_lmhead_topk": 0.0, "tree": 0.0}
+    names = list(stage_ms)
+    for e in evs:
+        for j, n in enumerate(names):
+            stage_ms[n] += e[j].elapsed_time(e[j + 1])
+    stage_us = {n: 1000.0 * v / args.steps for n, v in stage_ms.items()}
+    ms_per_step = 1000.0 * elapsed / args.steps
+    trees_per_s = b * args.steps / elapsed
+    rows = b * R
+
+    # dominant kernel: the stage-2 LM head (split-vocabulary GEMM + per-row merge)
+    es = 2 if w.dtype == "bf16" else 4
+    t_lm = stage_us["stage2_lmhead_topk"] * 1e-6
+    alg_bytes = V * d * es + rows * d * es + rows * dr.topk2 * 8 + rows * 4
+    alg_flops = 2.0 * rows * V * d
+    if w.dtype == "bf16" and rows > RIDGE:
+        roof = {"bound": "mfma", "achieved": alg_flops / t_lm / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    elif w.dtype == "bf16":
+        roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = "stage-2 LM head: lmhead GEMM + merge_topk, events around treeflash_marginal_topk on h'"
+    roof["alg_bytes_per_launch"] = alg_bytes
+    roof["alg_flops_per_launch"] = alg_flops
+
+    # whole-step roofline context
+    mlp_bytes = (2 * w.I * 2 * d + d * w.I) * es
+    step_bytes = 2 * V * d * es + mlp_bytes
+    out = {
+        "metric": METRIC, "value": trees_per_s, "unit": "trees/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "b": b, "d": d, "V": V, "gamma": w.gamma, "k": w.k, "B": w.B, "I": w.I,
+                   "inv_temperature": w.inv_temperature, "conditional_rows": rows, "gamma_k_b": w.gamma * w.k * b,
+                   "weight_copies": len(copies)},
+        "rows_per_s": rows * args.steps / elapsed,
+        "stage_us": stage_us,
+        "step_hbm_frac": step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, copies[0], st, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,169 @@
+/*
+ * treeflash.h -- C ABI of the TreeFlash drafting library for AMD MI355X (gfx950).
+ *
+ * TreeFlash (arXiv 2606.03819) drafts a speculative-decoding tree from a
+ * one-shot block drafter in two stages (Appendix B, "AR-approximated OPT-Tree
+ * Construction"):
+ *
+ *   Part 1 (treeflash_marginal_topk + treeflash_arapprox_expand)
+ *     stage 1: q_{t+i} = LMHead(h_{t+i}) for every draft depth i, top-M ids;
+ *     stage 2: for depth 1 (conditioned on the root token x_t) and for every
+ *              (depth i >= 2, candidate m of depth i-1) pair, Eq. 1
+ *                h' = h_i + SwiGLU( rms(h_i) :: rms(Embd(prev)) )
+ *              then the LM head, a log-softmax and the best entries per row.
+ *   Part 2 (treeflash_build_tree)
+ *     best-first (OPT-Tree) selection of B nodes by path probability; a node
+ *     is expanded only when its token is one of the M candidates of its depth.
+ *
+ * Conventions shared by every call
+ *   - Every tensor pointer is a DEVICE pointer to a dense row-major array owned
+ *     by the caller; the library never allocates, frees or keeps a pointer
+ *     after the call returns.  h, h', lm_head, w_gate, w_up, w_down and the
+ *     workspace must be 16-byte aligned (they are read with 16-byte loads);
+ *     every other array needs 4-byte alignment.
+ *   - Calls are asynchronous and ordered on `stream` (0 = the null stream).
+ *     They never synchronise the device.  Arguments are validated before any
+ *     HIP call; an invalid argument returns an error and launches nothing.
+ *     After launching, the library checks hipGetLastError and maps a failure
+ *     to TF_ERR_HIP.  Nothing is thrown or aborted across the ABI.
+ *   - `dt` is the element type of h, the embedding, the gains and every weight
+ *     matrix: TF_BF16 (bf16 operands, fp32 accumulation, bf16 rounding of the
+ *     x, SwiGLU-activation and h' operands) or TF_F32 (fp32 throughout).
+ *   - Shapes: b sequences, hidden size d, vocabulary V, draft depth gamma,
+ *     M = k stage-1 candidates per depth, SwiGLU width I, draft budget B.
+ *     R = 1 + (gamma-1)*k conditional rows per sequence.  Row 0 is depth 1
+ *     conditioned on the root token; row 1 + (i-2)*k + m is depth i (2..gamma)
+ *     conditioned on candidate m of depth i-1.
+ *   - Requirements (else TF_ERR_INVALID_ARG): b >= 1, gamma >= 1, 1 <= k <= V,
+ *     k <= 1024, d >= 16 and d % 16 == 0, I >= 16 and I % 16 == 0,
+ *     inv_temperature > 0 and finite.  b*gamma*... products must fit in int32.
+ *   - Ordering: every top-k list is sorted by (value desc, token id asc).
+ *   - Non-finite inputs give unspecified (but memory-safe) results.
+ *   - Calls that share a workspace must not overlap in time.
+ */
+#ifndef TREEFLASH_H
+#define TREEFLASH_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TF_OK = 0,
+    TF_ERR_INVALID_ARG = 1,  /* a NULL required pointer, a bad shape or parameter */
+    TF_ERR_UNSUPPORTED = 2,  /* valid request outside what this build implements  */
+    TF_ERR_WORKSPACE = 3,    /* workspace NULL or smaller than required           */
+    TF_ERR_HIP = 4           /* a HIP launch or runtime error                     */
+} tf_status_t;
+
+typedef enum { TF_F32 = 0, TF_BF16 = 1 } tf_dtype_t;
+
+/* Bytes of device workspace the two Part-1 calls need for these shapes (the
+ * larger of the two).  `topk2` is the stage-2 list length (see below).
+ * Returns 0 if the shapes are invalid.  The first 64 bytes of the workspace
+ * hold diagnostic counters: int32 at byte offset 0 counts the (row, vocabulary
+ * slice) pairs the last call re-evaluated on its exact slow path. */
+size_t treeflash_workspace_bytes(int b, int gamma, int d, int I, int V, int k, int topk2,
+                                 tf_dtype_t dt);
+
+/* Part 1, stage 1 (Appendix B, first loop of Part 1): marginal LM head and top-k.
+ *   h             [b, gamma, d]  drafter hidden states h_{t+1..t+gamma}
+ *   lm_head       [V, d]         output embedding; row v belongs to token v
+ *   inv_temperature              logits are multiplied by it before the softmax
+ *   topk_idx      out [b, gamma, k] int32: the k best ids per depth (logit desc, id asc)
+ *   topk_logprob  out [b, gamma, k] fp32 log-softmax values of those ids; may be NULL
+ *   lse           out [b, gamma] fp32 log-sum-exp of the scaled logits; may be NULL
+ * The [b*gamma, V] logits are never written to memory.  The operation is the
+ * same for any set of rows: called on h' viewed as [b, R, d] with k = topk2 it
+ * is the LM-head half of the conditional stage (here `gamma` only counts rows
+ * and may exceed 255). */
+tf_status_t treeflash_marginal_topk(const void *h, const void *lm_head,
+                                    int b, int gamma, int d, int V, int k,
+                                    float inv_temperature, tf_dtype_t dt,
+                                    int32_t *topk_idx, float *topk_logprob, float *lse,
+                                    void *workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
+/* Part 1, stage 2, first half (Method, Eq. 1): the AR-approximated hidden
+ * state of every conditional row,
+ *   h'_r = h_{depth(r)} + W_down( silu(W_gate x_r) * (W_up x_r) ),
+ *   x_r  = [ rms(h_{depth(r)}) * norm_h_gain ; rms(Embd(prev_r)) * norm_e_gain ].
+ * Arguments as in treeflash_arapprox_expand below;
+ *   hprime        out [b, R, d] (dtype dt; bf16 values are rounded to nearest even)
+ * The workspace must be sized by treeflash_workspace_bytes. */
+tf_status_t treeflash_arapprox_hidden(const void *h, const int32_t *root_token,
+                                      const int32_t *topk_idx, const void *emb,
+                                      const void *norm_h_gain, const void *norm_e_gain,
+                                      const void *w_gate, const void *w_up, const void *w_down,
+                                      int b, int gamma, int d, int I, int V, int k,
+                                      float rms_eps, tf_dtype_t dt, void *hprime,
+                                      void *workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/* Part 1, stage 2 (Method, Eq. 1; Appendix B, rest of Part 1): AR approximation
+ * of every conditional row, LM head, log-softmax, top-topk2.  Equivalent to
+ * treeflash_arapprox_hidden followed by treeflash_marginal_topk on h'.
+ *   h             [b, gamma, d]  drafter hidden states
+ *   root_token    [b] int32      x_t, the token that conditions depth 1
+ *   topk_idx      [b, gamma, k]  int32 stage-1 candidates (ids must be < V)
+ *   emb           [V, d]         input embedding Embd
+ *   norm_h_gain   [d] or NULL    RMSNorm gain applied to h (NULL = ones)
+ *   norm_e_gain   [d] or NULL    RMSNorm gain applied to Embd(prev) (NULL = ones)
+ *   w_gate, w_up  [I, 2d]        SwiGLU input projections; columns 0..d-1 act on
+ *                                the normalised h, columns d..2d-1 on the
+ *                                normalised embedding
+ *   w_down        [d, I]         SwiGLU output projection
+ *   lm_head       [V, d]         output embedding (as in stage 1)
+ *   topk2                        entries kept per row; min(B, V) <= topk2 <= V,
+ *                                topk2 <= 1024.  topk2 >= min(B, V) makes the
+ *                                tree of Part 2 equal to the tree of full rows.
+ *   rms_eps                      RMSNorm epsilon (the paper's models use 1e-6), >= 0
+ *   cond_idx      out [b, R, topk2] int32 best ids per row (log-prob desc, id asc)
+ *   cond_logprob  out [b, R, topk2] fp32 log-softmax of those ids
+ *   cond_lse      out [b, R] fp32 log-sum-exp of the scaled logits, or NULL
+ * The [b*R, V] logits are never written to memory. */
+tf_status_t treeflash_arapprox_expand(const void *h, const int32_t *root_token,
+                                      const int32_t *topk_idx, const void *emb,
+                                      const void *norm_h_gain, const void *norm_e_gain,
+                                      const void *w_gate, const void *w_up,
+                                      const void *w_down, const void *lm_head,
+                                      int b, int gamma, int d, int I, int V, int k, int topk2,
+                                      float inv_temperature, float rms_eps, tf_dtype_t dt,
+                                      int32_t *cond_idx, float *cond_logprob, float *cond_lse,
+                                      void *workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/* Part 2 (Appendix B): OPT-Tree selection.  Needs no workspace.
+ *   cond_idx, cond_logprob  [b, R, topk2] rows as produced by the call above
+ *                           (each row sorted by log-prob desc, id asc; log-probs <= 0)
+ *   topk_idx                [b, gamma, k] stage-1 candidates
+ *   B                       draft budget: nodes besides the root, 1 <= B <= 4095,
+ *                           B <= V * (1 + k + ... + k^(gamma-1)), and topk2 >= min(B, V)
+ * Outputs, per sequence, in pop order (best first), arrays [b, B]:
+ *   node_token      token id
+ *   node_parent     index of the parent node in the same array, -1 = the root x_t
+ *   node_depth      1..gamma
+ *   node_score      fp32 path log-probability: parent score + row log-prob, added in fp32
+ *   node_child_row  row (0..R-1) holding this node's children, -1 if it is not
+ *                   expandable (depth gamma, or not a stage-1 candidate); may be NULL
+ * Ties in path score go to the shallower node, then to the lexicographically
+ * smaller path of row ranks (rank = position in the parent's sorted row). */
+tf_status_t treeflash_build_tree(const int32_t *cond_idx, const float *cond_logprob,
+                                 const int32_t *topk_idx,
+                                 int b, int gamma, int k, int topk2, int B,
+                                 int32_t *node_token, int32_t *node_parent, int32_t *node_depth,
+                                 float *node_score, int32_t *node_child_row,
+                                 hipStream_t stream);
+
+/* Static description of a status code. */
+const char *treeflash_status_string(tf_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREEFLASH_H */

@@ -1,0 +1,193 @@
+// C ABI of the TreeFlash drafting library: argument checks, workspace layout,
+// launches.  Every argument is checked before the first HIP call.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/treeflash.h"
+#include "launch.hpp"
+#include "plan.hpp"
+
+namespace tf {
+size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks);
+}
+
+namespace {
+
+using namespace tf;
+
+constexpr long long kMaxRows = 1 << 20;
+
+// Operands read with 16-byte vector loads (activations, weights, h', the
+// workspace) must be 16-byte aligned; every other array only needs the
+// alignment of its 4-byte elements.
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+bool dtype_ok(tf_dtype_t dt) { return dt == TF_F32 || dt == TF_BF16; }
+
+// `gamma` is a draft depth (at most 255) unless `rows_only`, where it only
+// counts rows per sequence (the LM-head call on h' viewed as [b, R, d]).
+bool common_shapes_ok(int b, int gamma, int d, int V, int k, bool rows_only = false) {
+    if (b < 1 || gamma < 1 || (!rows_only && gamma > 255) || V < 1 || k < 1 || k > V || k > kMaxTopk) return false;
+    if (d < 16 || d % 16 != 0) return false;
+    if ((long long)b * gamma > kMaxRows) return false;
+    if (!rows_only && (long long)b * (1 + (long long)(gamma - 1) * k) > kMaxRows) return false;
+    if ((long long)V * d >= (1ll << 40)) return false;
+    return true;
+}
+
+size_t stage1_bytes(int b, int gamma, int V, bool bf16) {
+    const LmPlan p = lm_plan(b * gamma, V, bf16);
+    return 256 + align256((size_t)b * gamma * p.nsplit * kPartStride * 4);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t treeflash_workspace_bytes(int b, int gamma, int d, int I, int V, int k, int topk2, tf_dtype_t dt) {
+    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k)) return 0;
+    if (I < 16 || I % 16 != 0 || topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return 0;
+    return workspace_layout(b, gamma, d, I, V, k, dt == TF_BF16).total;
+}
+
+tf_status_t treeflash_marginal_topk(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
+                                    float inv_temperature, tf_dtype_t dt, int32_t* topk_idx,
+                                    float* topk_logprob, float* lse, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+    if (h == nullptr || lm_head == nullptr || topk_idx == nullptr) return TF_ERR_INVALID_ARG;
+    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k, true)) return TF_ERR_INVALID_ARG;
+    if (!(inv_temperature > 0.f) || !isfinite(inv_temperature)) return TF_ERR_INVALID_ARG;
+    if (!aligned16(h) || !aligned16(lm_head) || !aligned4(topk_idx) ||
+        (topk_logprob != nullptr && !aligned4(topk_logprob)) || (lse != nullptr && !aligned4(lse)))
+        return TF_ERR_INVALID_ARG;
+    const bool bf16 = dt == TF_BF16;
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < stage1_bytes(b, gamma, V, bf16))
+        return TF_ERR_WORKSPACE;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    int* diag = reinterpret_cast<int*>(ws);
+    float* part = reinterpret_cast<float*>(ws + 256);
+    const hipError_t e = launch_lmhead_topk(h, d, lm_head, b * gamma, d, V, k, inv_temperature, bf16, part,
+                                            topk_idx, topk_logprob, lse, diag, stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+}  // extern "C"
+
+namespace {
+
+tf_status_t check_hidden_args(const void* h, const int32_t* root_token, const int32_t* topk_idx, const void* emb,
+                              const void* norm_h_gain, const void* norm_e_gain, const void* w_gate,
+                              const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
+                              float rms_eps, tf_dtype_t dt) {
+    if (h == nullptr || root_token == nullptr || topk_idx == nullptr || emb == nullptr || w_gate == nullptr ||
+        w_up == nullptr || w_down == nullptr)
+        return TF_ERR_INVALID_ARG;
+    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k)) return TF_ERR_INVALID_ARG;
+    if (I < 16 || I % 16 != 0) return TF_ERR_INVALID_ARG;
+    if (!(rms_eps >= 0.f) || !isfinite(rms_eps)) return TF_ERR_INVALID_ARG;
+    const void* vec[] = {h, w_gate, w_up, w_down};
+    for (const void* p : vec)
+        if (!aligned16(p)) return TF_ERR_INVALID_ARG;
+    if (!aligned4(root_token) || !aligned4(topk_idx) || !aligned4(emb)) return TF_ERR_INVALID_ARG;
+    if ((norm_h_gain != nullptr && !aligned4(norm_h_gain)) || (norm_e_gain != nullptr && !aligned4(norm_e_gain)))
+        return TF_ERR_INVALID_ARG;
+    return TF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, const int32_t* topk_idx,
+                                      const void* emb, const void* norm_h_gain, const void* norm_e_gain,
+                                      const void* w_gate, const void* w_up, const void* w_down, int b, int gamma,
+                                      int d, int I, int V, int k, float rms_eps, tf_dtype_t dt, void* hprime,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
+                                              w_down, b, gamma, d, I, V, k, rms_eps, dt);
+    if (chk != TF_OK) return chk;
+    if (hprime == nullptr || !aligned16(hprime)) return TF_ERR_INVALID_ARG;
+    const bool bf16 = dt == TF_BF16;
+    const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16);
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    const hipError_t e = launch_arapprox(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
+                                         w_down, b, gamma, d, I, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et,
+                                         ws + lay.act, hprime, reinterpret_cast<int*>(ws + lay.diag), stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, const int32_t* topk_idx,
+                                      const void* emb, const void* norm_h_gain, const void* norm_e_gain,
+                                      const void* w_gate, const void* w_up, const void* w_down,
+                                      const void* lm_head, int b, int gamma, int d, int I, int V, int k, int topk2,
+                                      float inv_temperature, float rms_eps, tf_dtype_t dt, int32_t* cond_idx,
+                                      float* cond_logprob, float* cond_lse, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream) {
+    const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
+                                              w_down, b, gamma, d, I, V, k, rms_eps, dt);
+    if (chk != TF_OK) return chk;
+    if (lm_head == nullptr || cond_idx == nullptr || cond_logprob == nullptr) return TF_ERR_INVALID_ARG;
+    if (topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return TF_ERR_INVALID_ARG;
+    if (!(inv_temperature > 0.f) || !isfinite(inv_temperature)) return TF_ERR_INVALID_ARG;
+    if (!aligned16(lm_head) || !aligned4(cond_idx) || !aligned4(cond_logprob) ||
+        (cond_lse != nullptr && !aligned4(cond_lse)))
+        return TF_ERR_INVALID_ARG;
+    const bool bf16 = dt == TF_BF16;
+    const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16);
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    int* diag = reinterpret_cast<int*>(ws + lay.diag);
+    hipError_t e = launch_arapprox(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down, b,
+                                   gamma, d, I, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et, ws + lay.act,
+                                   ws + lay.hp, diag, stream);
+    if (e != hipSuccess) return TF_ERR_HIP;
+    const int rows = b * (1 + (gamma - 1) * k);
+    e = launch_lmhead_topk(ws + lay.hp, d, lm_head, rows, d, V, topk2, inv_temperature, bf16,
+                           reinterpret_cast<float*>(ws + lay.part), cond_idx, cond_logprob, cond_lse, diag, stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+tf_status_t treeflash_build_tree(const int32_t* cond_idx, const float* cond_logprob, const int32_t* topk_idx, int b,
+                                 int gamma, int k, int topk2, int B, int32_t* node_token, int32_t* node_parent,
+                                 int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                                 hipStream_t stream) {
+    if (cond_idx == nullptr || cond_logprob == nullptr || topk_idx == nullptr || node_token == nullptr ||
+        node_parent == nullptr || node_depth == nullptr || node_score == nullptr)
+        return TF_ERR_INVALID_ARG;
+    if (b < 1 || gamma < 1 || gamma > 255 || k < 1 || k > kMaxTopk || topk2 < 1 || topk2 > 4096) return TF_ERR_INVALID_ARG;
+    if (B < 1 || B > kMaxBudget) return TF_ERR_INVALID_ARG;
+    const long long Rs = 1 + (long long)(gamma - 1) * k;
+    if ((long long)b * Rs > kMaxRows) return TF_ERR_INVALID_ARG;
+    if (topk2 < B) {
+        // Rows shorter than B are only meaningful when they are full rows
+        // (topk2 == V); then the tree can hold topk2 * (1 + k + ... + k^(gamma-1)) nodes.
+        long long cap = 0, pw = 1;
+        for (int j = 0; j < gamma && cap < B; ++j) {
+            cap += pw * topk2;
+            pw = pw * k > (1ll << 40) ? (1ll << 40) : pw * k;
+        }
+        if (cap < B) return TF_ERR_INVALID_ARG;
+    }
+    const void* ptrs[] = {cond_idx, cond_logprob, topk_idx, node_token, node_parent, node_depth, node_score};
+    for (const void* p : ptrs)
+        if (!aligned4(p)) return TF_ERR_INVALID_ARG;
+    if (node_child_row != nullptr && !aligned4(node_child_row)) return TF_ERR_INVALID_ARG;
+    if (tree_lds_bytes(B, gamma, k, (int)Rs, topk2, nullptr) == 0) return TF_ERR_UNSUPPORTED;
+    const hipError_t e = launch_build_tree(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, node_token,
+                                           node_parent, node_depth, node_score, node_child_row, stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+const char* treeflash_status_string(tf_status_t status) {
+    switch (status) {
+        case TF_OK: return "success";
+        case TF_ERR_INVALID_ARG: return "invalid argument";
+        case TF_ERR_UNSUPPORTED: return "unsupported configuration";
+        case TF_ERR_WORKSPACE: return "workspace missing or too small";
+        case TF_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

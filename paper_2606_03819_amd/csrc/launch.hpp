@@ -1,0 +1,28 @@
+// Host launchers of the TreeFlash kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tf {
+
+// LM head over `rows` activation rows [rows, d] (row stride ldx elements),
+// followed by the per-row merge: top-K ids and log-probs, log-sum-exp.
+hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
+                              float inv_t, bool bf16, float* part, int32_t* out_idx, float* out_lp,
+                              float* out_lse, int* diag, hipStream_t stream);
+
+// Eq. 1 for every conditional row: RMSNorm of h and of the previous token's
+// embedding, SwiGLU, residual.  Writes h' [b*R, d] into `hp`.
+hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
+                           const void* gain_h, const void* gain_e, const void* w_gate, const void* w_up,
+                           const void* w_down, int b, int gamma, int d, int I, int V, int k, float eps,
+                           bool bf16, void* ht, void* et, void* act, void* hp, int* diag, hipStream_t stream);
+
+// Best-first tree selection, one workgroup per sequence.
+hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, const int32_t* topk_idx, int b,
+                             int gamma, int k, int topk2, int B, int32_t* node_token, int32_t* node_parent,
+                             int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                             hipStream_t stream);
+
+}  // namespace tf

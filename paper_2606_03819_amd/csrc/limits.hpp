@@ -1,0 +1,13 @@
+// Compile-time constants shared by host planning code and device kernels.
+#pragma once
+
+namespace tf {
+
+// Entries each (row, vocabulary slice) partial keeps, and the partial layout:
+// [max, sum, bound, count, val[kKeep], idx[kKeep]] (raw, unscaled logits).
+constexpr int kKeep = 8;
+constexpr int kPartStride = 4 + 2 * kKeep;
+// Per-lane running list length inside the LM-head epilogue.
+constexpr int kLane = 4;
+
+}  // namespace tf

@@ -1,0 +1,447 @@
+// LM head with online log-sum-exp and top-k (Appendix B, Part 1: q = LMHead(h),
+// TopM, and the conditional rows q').  The [rows, V] logits never reach
+// memory: each workgroup reduces its vocabulary slice to a (row, slice)
+// partial, and one merge workgroup per row turns the partials into the row's
+// log-sum-exp and exact top-k.
+#include "common.hpp"
+#include "launch.hpp"
+#include "plan.hpp"
+#include "stream_gemm.hpp"
+
+namespace tf {
+
+// ------------------------------------------------------------ bf16 / MFMA
+
+template <int WM, int NT>
+__global__ __launch_bounds__(256) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
+                                                          const uint16_t* __restrict__ w, GemmShape sh,
+                                                          int V, float sl2, float* __restrict__ part,
+                                                          int* __restrict__ diag) {
+    using Tr = GemmTraits<WM, NT>;
+    using E = EpiLmHead<WM, NT>;
+    constexpr int SMEM = Tr::XS_BYTES > E::MERGE_BYTES ? Tr::XS_BYTES : E::MERGE_BYTES;
+    __shared__ __align__(16) unsigned char smem[SMEM];
+    if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
+    WRowsPlain ws{w, V, sh.K};
+    XRowsPlain xs{x, ldx};
+    E epi{part, V, sl2};
+    stream_gemm_body<WM, NT>(ws, xs, epi, sh, smem);
+}
+
+// ------------------------------------------------------------ fp32 / SIMT
+//
+// The fp32 workloads are small; this kernel keeps the same partial format
+// with plain FMA: a workgroup holds 32 activation rows, each thread one
+// vocabulary row of the current 256-row step, and every (row, 1/8 of the
+// step) pair is one contributor list.
+__global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict__ x, long ldx,
+                                                         const float* __restrict__ w, GemmShape sh,
+                                                         int V, float sl2, float* __restrict__ part,
+                                                         int* __restrict__ diag) {
+    __shared__ float xs[32][65];
+    __shared__ float lt[32][257];
+    if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
+    const int tid = threadIdx.x;
+    const int L = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int split = L / sh.nrb;
+    const int rb = L - split * sh.nrb;
+    const int row0 = rb * 32;
+    const int t0 = (int)(((long long)split * sh.ntiles) / sh.nsplit);
+    const int t1 = (int)(((long long)(split + 1) * sh.ntiles) / sh.nsplit);
+    const int vend = min(V, t1 * 32);
+    const int srow = tid >> 3, sub = tid & 7;
+
+    float m = neg_inf(), s = 0.f;
+    float lv[kLane];
+    int li[kLane];
+#pragma unroll
+    for (int q = 0; q < kLane; ++q) {
+        lv[q] = neg_inf();
+        li[q] = -1;
+    }
+    int seen = 0;
+
+    for (int ct = t0; ct < t1; ct += 8) {
+        const int v = ct * 32 + tid;
+        const bool vok = v < vend;
+        float acc[32];
+#pragma unroll
+        for (int r = 0; r < 32; ++r) acc[r] = 0.f;
+        for (int k0 = 0; k0 < sh.K; k0 += 64) {
+            __syncthreads();
+            for (int i = 0; i < 8; ++i) {
+                const int e = tid + 256 * i;
+                const int r = e >> 6, c = e & 63;
+                const int gr = row0 + r, k = k0 + c;
+                xs[r][c] = (gr < sh.R && k < sh.K) ? x[(size_t)gr * ldx + k] : 0.f;
+            }
+            __syncthreads();
+            if (vok) {
+                const float* wr = w + (size_t)v * sh.K + k0;
+                const int kn = min(64, sh.K - k0);
+                for (int c = 0; c < kn; ++c) {
+                    const float wv = wr[c];
+#pragma unroll
+                    for (int r = 0; r < 32; ++r) acc[r] = fmaf(wv, xs[r][c], acc[r]);
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 32; ++r) lt[r][tid] = acc[r];
+        __syncthreads();
+        float cm = neg_inf();
+        int nv = 0;
+        for (int j = 0; j < 32; ++j) {
+            const int vv = ct * 32 + sub + 8 * j;
+            if (vv < vend) {
+                cm = fmaxf(cm, lt[srow][sub + 8 * j]);
+                ++nv;
+            }
+        }
+        if (nv > 0) {
+            seen += nv;
+            const float mn = fmaxf(m, cm);
+            float sum = s * exp2f((m - mn) * sl2);
+            for (int j = 0; j < 32; ++j) {
+                const int vv = ct * 32 + sub + 8 * j;
+                if (vv >= vend) continue;
+                float cv = lt[srow][sub + 8 * j];
+                sum += exp2f((cv - mn) * sl2);
+                if (cv > lv[kLane - 1]) {
+                    int ci = vv;
+#pragma unroll
+                    for (int q = 0; q < kLane; ++q) {
+                        const bool sw = cv > lv[q];
+                        const float tv = sw ? lv[q] : cv;
+                        const int ti = sw ? li[q] : ci;
+                        lv[q] = sw ? cv : lv[q];
+                        li[q] = sw ? ci : li[q];
+                        cv = tv;
+                        ci = ti;
+                    }
+                }
+            }
+            s = sum;
+            m = mn;
+        }
+    }
+    __syncthreads();
+    constexpr int W = 3 + 2 * kLane;
+    float* cmrg = &lt[0][0];   // [32 rows][8 contributors][W]
+    float* c = cmrg + (srow * 8 + sub) * W;
+    c[0] = m;
+    c[1] = s;
+    c[2] = seen > kLane ? lv[kLane - 1] : neg_inf();
+#pragma unroll
+    for (int e = 0; e < kLane; ++e) {
+        c[3 + e] = lv[e];
+        c[3 + kLane + e] = __int_as_float(li[e]);
+    }
+    __syncthreads();
+    lm_merge_contributors(cmrg, 32, row0, split, sl2, part, sh);
+}
+
+// ------------------------------------------------------------------ merge
+
+struct MergeArgs {
+    const float* part;
+    int nsplit, ntiles, K, V, d;
+    float inv_t, sl2;
+    int32_t* out_idx;
+    float* out_lp;
+    float* out_lse;
+    const void* x;   // activation rows (slow path)
+    long ldx;
+    const void* w;   // LM head (slow path)
+    int* diag;
+};
+
+__device__ __forceinline__ float dot_row(const uint16_t* a, const uint16_t* b, int d) {
+    float acc = 0.f;
+    for (int k = 0; k < d; k += 8) {
+        const u32x4 av = *reinterpret_cast<const u32x4*>(a + k);
+        const u32x4 bv = *reinterpret_cast<const u32x4*>(b + k);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc = fmaf(bf16_bits_to_f32(av[q] & 0xffffu), bf16_bits_to_f32(bv[q] & 0xffffu), acc);
+            acc = fmaf(bf16_bits_to_f32(av[q] >> 16), bf16_bits_to_f32(bv[q] >> 16), acc);
+        }
+    }
+    return acc;
+}
+__device__ __forceinline__ float dot_row(const float* a, const float* b, int d) {
+    float acc = 0.f;
+    for (int k = 0; k < d; ++k) acc = fmaf(a[k], b[k], acc);
+    return acc;
+}
+
+__device__ __forceinline__ float block_max(float v, float* red) {
+    v = wave_max(v);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+__device__ __forceinline__ float block_sum(float v, float* red) {
+    v = wave_sum(v);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// One workgroup per row.  The candidates are the rows' slice lists; a radix
+// select over 64-bit keys (value, then inverted id) finds the k-th best, the
+// selected entries are bitonic-sorted, and every slice whose bound reaches the
+// k-th value is re-evaluated exactly (dot products straight from memory), so
+// the result is the exact top-k of the row whatever the data.
+template <class T>
+__global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
+    constexpr int NPT = kMaxSplits * kKeep / 256;
+    __shared__ float red[4];
+    __shared__ unsigned hist[256];
+    __shared__ int s_digit, s_krem, s_count, s_nflag, s_ncand;
+    __shared__ float sel_v[kMaxTopk];
+    __shared__ int sel_i[kMaxTopk];
+    __shared__ int s_flag[kMaxSplits];
+    __shared__ float cand_v[256];
+    __shared__ int cand_i[256];
+
+    const int row = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int K = a.K;
+    const float* P = a.part + (size_t)row * a.nsplit * kPartStride;
+
+    // log-sum-exp of the row from the slice (max, sum) pairs
+    float M = neg_inf();
+    for (int s = tid; s < a.nsplit; s += 256) M = fmaxf(M, P[s * kPartStride]);
+    M = block_max(M, red);
+    float S = 0.f;
+    for (int s = tid; s < a.nsplit; s += 256) {
+        const float ms = P[s * kPartStride];
+        if (ms != neg_inf()) S += P[s * kPartStride + 1] * exp2f((ms - M) * a.sl2);
+    }
+    S = block_sum(S, red);
+    const float logS = logf(S);
+
+    // candidate keys: (order-preserving value bits << 32) | ~id; 0 = empty
+    const int N = a.nsplit * kKeep;
+    unsigned long long key[NPT];
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+        const int e = tid + 256 * i;
+        key[i] = 0ull;
+        if (e < N) {
+            const int s = e / kKeep, j = e - s * kKeep;
+            const int id = __float_as_int(P[s * kPartStride + 4 + kKeep + j]);
+            if (id >= 0)
+                key[i] = ((unsigned long long)f32_key(P[s * kPartStride + 4 + j]) << 32) | (unsigned)(~id);
+        }
+    }
+
+    // radix select of the K-th largest key, 8 bits at a time
+    unsigned long long prefix = 0ull, mask = 0ull;
+    int krem = K;
+    bool insufficient = false;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        hist[tid] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < NPT; ++i)
+            if (key[i] != 0ull && (key[i] & mask) == prefix) atomicAdd(&hist[(key[i] >> shift) & 255u], 1u);
+        __syncthreads();
+        if (wave == 0) {
+            unsigned c[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) c[q] = hist[255 - 4 * lane - q];
+            const unsigned loc = c[0] + c[1] + c[2] + c[3];
+            unsigned inc = loc;
+            for (int o = 1; o < 64; o <<= 1) {
+                const unsigned t = __shfl_up(inc, o);
+                if (lane >= o) inc += t;
+            }
+            const unsigned exc = inc - loc;
+            if (exc < (unsigned)krem && (unsigned)krem <= inc) {
+                unsigned run = exc;
+                for (int q = 0; q < 4; ++q) {
+                    if (run + c[q] >= (unsigned)krem) {
+                        s_digit = 255 - 4 * lane - q;
+                        s_krem = krem - (int)run;
+                        break;
+                    }
+                    run += c[q];
+                }
+            }
+            if (lane == 63 && inc < (unsigned)krem) s_digit = -1;
+        }
+        __syncthreads();
+        const int dg = s_digit;
+        if (dg < 0) {
+            insufficient = true;
+            break;
+        }
+        krem = s_krem;
+        prefix |= (unsigned long long)dg << shift;
+        mask |= 0xffull << shift;
+        __syncthreads();
+    }
+
+    if (tid == 0) {
+        s_count = 0;
+        s_nflag = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+        if (key[i] != 0ull && (insufficient || key[i] >= prefix)) {
+            const int pos = atomicAdd(&s_count, 1);
+            if (pos < K) {   // keys are unique, so at most K entries qualify
+                sel_v[pos] = key_f32((unsigned)(key[i] >> 32));
+                sel_i[pos] = (int)(~(unsigned)key[i]);
+            }
+        }
+    }
+    const float tval = insufficient ? neg_inf() : key_f32((unsigned)(prefix >> 32));
+    for (int s = tid; s < a.nsplit; s += 256) {
+        const float U = P[s * kPartStride + 2];
+        if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = s;
+    }
+    __syncthreads();
+    int cnt = min(s_count, K);
+
+    // bitonic sort of the selected entries, best first
+    int pw = 1;
+    while (pw < cnt) pw <<= 1;
+    for (int i = cnt + tid; i < pw; i += 256) {
+        sel_v[i] = neg_inf();
+        sel_i[i] = 0x7fffffff;
+    }
+    __syncthreads();
+    for (int size = 2; size <= pw; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = tid; i < (pw >> 1); i += 256) {
+                const int lo = 2 * i - (i & (stride - 1));
+                const int hi = lo + stride;
+                const bool up = (lo & size) == 0;
+                const float vl = sel_v[lo], vh = sel_v[hi];
+                const int il = sel_i[lo], ih = sel_i[hi];
+                const bool sw = up ? better(vh, ih, vl, il) : better(vl, il, vh, ih);
+                if (sw) {
+                    sel_v[lo] = vh;
+                    sel_i[lo] = ih;
+                    sel_v[hi] = vl;
+                    sel_i[hi] = il;
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    // exact slow path for slices that may hide a qualifying logit
+    const int nflag = s_nflag;
+    if (nflag > 0) {
+        const T* xr = reinterpret_cast<const T*>(a.x) + (size_t)row * a.ldx;
+        const T* wb = reinterpret_cast<const T*>(a.w);
+        for (int f = 0; f < nflag; ++f) {
+            const int s = s_flag[f];
+            const int t0 = (int)(((long long)s * a.ntiles) / a.nsplit);
+            const int t1 = (int)(((long long)(s + 1) * a.ntiles) / a.nsplit);
+            const int v0 = t0 * 32, v1 = min(a.V, t1 * 32);
+            for (int vb = v0; vb < v1; vb += 256) {
+                if (tid == 0) s_ncand = 0;
+                __syncthreads();
+                const int v = vb + tid;
+                if (v < v1) {
+                    const float val = dot_row(xr, wb + (size_t)v * a.d, a.d);
+                    bool take = cnt < K || better(val, v, sel_v[K - 1], sel_i[K - 1]);
+                    if (take)
+                        for (int j = 0; j < cnt; ++j)
+                            if (sel_i[j] == v) {
+                                take = false;
+                                break;
+                            }
+                    if (take) {
+                        const int p = atomicAdd(&s_ncand, 1);
+                        cand_v[p] = val;
+                        cand_i[p] = v;
+                    }
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    int c = cnt;
+                    for (int q = 0; q < s_ncand; ++q) {
+                        const float cv = cand_v[q];
+                        const int ci = cand_i[q];
+                        int pos;
+                        if (c < K) {
+                            pos = c++;
+                        } else if (better(cv, ci, sel_v[K - 1], sel_i[K - 1])) {
+                            pos = K - 1;
+                        } else {
+                            continue;
+                        }
+                        while (pos > 0 && better(cv, ci, sel_v[pos - 1], sel_i[pos - 1])) {
+                            sel_v[pos] = sel_v[pos - 1];
+                            sel_i[pos] = sel_i[pos - 1];
+                            --pos;
+                        }
+                        sel_v[pos] = cv;
+                        sel_i[pos] = ci;
+                    }
+                    s_count = c;
+                }
+                __syncthreads();
+                cnt = s_count;
+            }
+        }
+        if (tid == 0 && a.diag != nullptr) atomicAdd(a.diag, nflag);
+    }
+
+    for (int j = tid; j < K; j += 256) {
+        const bool ok = j < cnt;
+        a.out_idx[(size_t)row * K + j] = ok ? sel_i[j] : -1;
+        if (a.out_lp != nullptr)
+            a.out_lp[(size_t)row * K + j] = ok ? a.inv_t * (sel_v[j] - M) - logS : neg_inf();
+    }
+    if (a.out_lse != nullptr && tid == 0) a.out_lse[row] = a.inv_t * M + logS;
+}
+
+// ------------------------------------------------------------------ launchers
+
+template <int WM, int NT>
+static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, int V,
+                           float sl2, float* part, int* diag, hipStream_t st) {
+    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT>), dim3(sh.nsplit * sh.nrb), dim3(256), 0, st, x, ldx, w, sh,
+                       V, sl2, part, diag);
+}
+
+hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
+                              float inv_t, bool bf16, float* part, int32_t* out_idx, float* out_lp,
+                              float* out_lse, int* diag, hipStream_t stream) {
+    const LmPlan p = lm_plan(rows, V, bf16);
+    GemmShape sh{rows, d, p.ntiles, p.nsplit, p.nrb};
+    const float sl2 = inv_t * kLog2e;
+    if (bf16) {
+        const uint16_t* xb = static_cast<const uint16_t*>(x);
+        const uint16_t* wb = static_cast<const uint16_t*>(w);
+        switch (p.NT) {
+            case 1: launch_lm_bf16<2, 1>(xb, ldx, wb, sh, V, sl2, part, diag, stream); break;
+            case 2: launch_lm_bf16<2, 2>(xb, ldx, wb, sh, V, sl2, part, diag, stream); break;
+            default: launch_lm_bf16<2, 4>(xb, ldx, wb, sh, V, sl2, part, diag, stream); break;
+        }
+    } else {
+        hipLaunchKernelGGL(lmhead_f32_kernel, dim3(sh.nsplit * sh.nrb), dim3(256), 0, stream,
+                           static_cast<const float*>(x), ldx, static_cast<const float*>(w), sh, V, sl2, part,
+                           diag);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    MergeArgs ma{part, p.nsplit, p.ntiles, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
+    if (bf16)
+        hipLaunchKernelGGL(merge_topk_kernel<uint16_t>, dim3(rows), dim3(256), 0, stream, ma);
+    else
+        hipLaunchKernelGGL(merge_topk_kernel<float>, dim3(rows), dim3(256), 0, stream, ma);
+    return hipGetLastError();
+}
+
+}  // namespace tf

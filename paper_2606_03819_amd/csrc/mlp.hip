@@ -1,0 +1,195 @@
+// The AR approximator of Eq. 1 for every conditional row:
+//   h'_r = h_{depth(r)} + W_down( silu(W_gate x_r) * (W_up x_r) ),
+//   x_r  = [ rms(h_{depth(r)}) * g_h ; rms(Embd(prev_r)) * g_e ].
+// Rows follow Appendix B: row 0 is depth 1 conditioned on the root token,
+// row 1 + (i-2)*M + m is depth i conditioned on candidate m of depth i-1.
+#include "common.hpp"
+#include "launch.hpp"
+#include "plan.hpp"
+#include "stream_gemm.hpp"
+
+namespace tf {
+
+__device__ __forceinline__ float load_elem(const uint16_t* p, size_t i) { return bf16_bits_to_f32(p[i]); }
+__device__ __forceinline__ float load_elem(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ void store_elem(uint16_t* p, size_t i, float v) { p[i] = (uint16_t)f32_to_bf16_bits(v); }
+__device__ __forceinline__ void store_elem(float* p, size_t i, float v) { p[i] = v; }
+
+__device__ __forceinline__ int row_depth(int rl, int M) { return rl == 0 ? 1 : 2 + (rl - 1) / M; }
+
+// RMSNorm of the b*gamma drafter states (into ht) and of the b*R previous-token
+// embeddings (into et); one workgroup per row.  bf16 outputs are rounded to
+// nearest even: they are the bf16 operand x of the SwiGLU products.
+template <class T>
+__global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__ h, const int32_t* __restrict__ root,
+                                                           const int32_t* __restrict__ topk,
+                                                           const T* __restrict__ emb, const T* __restrict__ gh,
+                                                           const T* __restrict__ ge, int b, int gamma, int d, int V,
+                                                           int M, int Rs, float eps, T* __restrict__ ht,
+                                                           T* __restrict__ et, int* __restrict__ diag) {
+    __shared__ float red[4];
+    if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
+    const int row = blockIdx.x;
+    const T* src;
+    const T* gain;
+    T* dst;
+    if (row < b * gamma) {
+        src = h + (size_t)row * d;
+        gain = gh;
+        dst = ht + (size_t)row * d;
+    } else {
+        const int rr = row - b * gamma;
+        const int s = rr / Rs;
+        const int rl = rr - s * Rs;
+        int prev;
+        if (rl == 0) {
+            prev = root[s];
+        } else {
+            const int depth = row_depth(rl, M);
+            prev = topk[((size_t)s * gamma + (depth - 2)) * M + (rl - 1) % M];
+        }
+        prev = min(max(prev, 0), V - 1);   // ids are documented to be < V; never read out of bounds
+        src = emb + (size_t)prev * d;
+        gain = ge;
+        dst = et + (size_t)rr * d;
+    }
+    float ss = 0.f;
+    for (int k = threadIdx.x; k < d; k += 256) {
+        const float x = load_elem(src, k);
+        ss = fmaf(x, x, ss);
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    ss = (red[0] + red[1]) + (red[2] + red[3]);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+    for (int k = threadIdx.x; k < d; k += 256) {
+        float y = load_elem(src, k) * inv;
+        if (gain != nullptr) y *= load_elem(gain, k);
+        store_elem(dst, k, y);
+    }
+}
+
+// ------------------------------------------------------------------ bf16
+
+template <int WM, int NT>
+__global__ __launch_bounds__(256) void gateup_bf16_kernel(WRowsGateUp ws, XRowsConcat xs, GemmShape sh,
+                                                          uint16_t* __restrict__ act, int I) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::XS_BYTES];
+    EpiSwiGLU<WM, NT> epi{act, I};
+    stream_gemm_body<WM, NT>(ws, xs, epi, sh, smem);
+}
+
+template <int WM, int NT>
+__global__ __launch_bounds__(256) void down_bf16_kernel(WRowsPlain ws, XRowsPlain xs, GemmShape sh,
+                                                        uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
+                                                        int d, int Rs, int gamma, int M) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::XS_BYTES];
+    EpiResidual<WM, NT> epi{hp, h, d, Rs, gamma, M};
+    stream_gemm_body<WM, NT>(ws, xs, epi, sh, smem);
+}
+
+// ------------------------------------------------------------------ fp32
+
+__global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ wg, const float* __restrict__ wu,
+                                                         const float* __restrict__ ht, const float* __restrict__ et,
+                                                         int rows, int d, int I, int Rs, int gamma, int M,
+                                                         float* __restrict__ act) {
+    const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
+    const int i = blockIdx.x * 64 + (threadIdx.x & 63);
+    if (r >= rows || i >= I) return;
+    const int s = r / Rs;
+    const int rl = r - s * Rs;
+    const float* hr = ht + (size_t)(s * gamma + row_depth(rl, M) - 1) * d;
+    const float* er = et + (size_t)r * d;
+    const float* g_row = wg + (size_t)i * 2 * d;
+    const float* u_row = wu + (size_t)i * 2 * d;
+    float g = 0.f, u = 0.f;
+    for (int k = 0; k < d; ++k) {
+        g = fmaf(hr[k], g_row[k], g);
+        u = fmaf(hr[k], u_row[k], u);
+    }
+    for (int k = 0; k < d; ++k) {
+        g = fmaf(er[k], g_row[d + k], g);
+        u = fmaf(er[k], u_row[d + k], u);
+    }
+    act[(size_t)r * I + i] = g / (1.0f + expf(-g)) * u;
+}
+
+__global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__ wd, const float* __restrict__ act,
+                                                       const float* __restrict__ h, int rows, int d, int I, int Rs,
+                                                       int gamma, int M, float* __restrict__ hp) {
+    const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
+    const int n = blockIdx.x * 64 + (threadIdx.x & 63);
+    if (r >= rows || n >= d) return;
+    const int s = r / Rs;
+    const int rl = r - s * Rs;
+    const float* ar = act + (size_t)r * I;
+    const float* wr = wd + (size_t)n * I;
+    float y = 0.f;
+    for (int i = 0; i < I; ++i) y = fmaf(ar[i], wr[i], y);
+    hp[(size_t)r * d + n] = h[(size_t)(s * gamma + row_depth(rl, M) - 1) * d + n] + y;
+}
+
+// ------------------------------------------------------------------ launcher
+
+template <int WM, int NT>
+static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
+                            const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
+                            int I, int Rs, int gamma, int M, const LmPlan& pg, const LmPlan& pd, hipStream_t st) {
+    WRowsGateUp wgu{wg, wu, I, 2 * d};
+    XRowsConcat xc{ht, et, d, Rs, gamma, M};
+    GemmShape shg{rows, 2 * d, pg.ntiles, pg.nsplit, pg.nrb};
+    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT>), dim3(pg.nsplit * pg.nrb), dim3(256), 0, st, wgu, xc, shg, act,
+                       I);
+    WRowsPlain wdn{wd, d, I};
+    XRowsPlain xa{act, (long)I};
+    GemmShape shd{rows, I, pd.ntiles, pd.nsplit, pd.nrb};
+    hipLaunchKernelGGL((down_bf16_kernel<WM, NT>), dim3(pd.nsplit * pd.nrb), dim3(256), 0, st, wdn, xa, shd, hp, h,
+                       d, Rs, gamma, M);
+}
+
+hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
+                           const void* gain_h, const void* gain_e, const void* w_gate, const void* w_up,
+                           const void* w_down, int b, int gamma, int d, int I, int V, int k, float eps,
+                           bool bf16, void* ht, void* et, void* act, void* hp, int* diag, hipStream_t stream) {
+    const int Rs = 1 + (gamma - 1) * k;
+    const int rows = b * Rs;
+    const int nrows = b * gamma + rows;
+    if (bf16) {
+        hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),
+                           static_cast<const uint16_t*>(gain_h), static_cast<const uint16_t*>(gain_e), b, gamma, d,
+                           V, k, Rs, eps, static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag);
+        const LmPlan pg = mlp_plan(rows, cdiv(I, 16));
+        const LmPlan pd = mlp_plan(rows, cdiv(d, 32));
+        const uint16_t* hb = static_cast<const uint16_t*>(h);
+        const uint16_t* wg = static_cast<const uint16_t*>(w_gate);
+        const uint16_t* wu = static_cast<const uint16_t*>(w_up);
+        const uint16_t* wd = static_cast<const uint16_t*>(w_down);
+        const uint16_t* htb = static_cast<const uint16_t*>(ht);
+        const uint16_t* etb = static_cast<const uint16_t*>(et);
+        uint16_t* actb = static_cast<uint16_t*>(act);
+        uint16_t* hpb = static_cast<uint16_t*>(hp);
+        switch (pg.NT) {
+            case 1: launch_mlp_bf16<2, 1>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma, k, pg, pd, stream); break;
+            case 2: launch_mlp_bf16<2, 2>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma, k, pg, pd, stream); break;
+            default: launch_mlp_bf16<2, 4>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma, k, pg, pd, stream); break;
+        }
+    } else {
+        hipLaunchKernelGGL(rmsnorm_rows_kernel<float>, dim3(nrows), dim3(256), 0, stream,
+                           static_cast<const float*>(h), root, topk_idx, static_cast<const float*>(emb),
+                           static_cast<const float*>(gain_h), static_cast<const float*>(gain_e), b, gamma, d, V, k,
+                           Rs, eps, static_cast<float*>(ht), static_cast<float*>(et), diag);
+        hipLaunchKernelGGL(gateup_f32_kernel, dim3(cdiv(I, 64), cdiv(rows, 4)), dim3(256), 0, stream,
+                           static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
+                           static_cast<const float*>(ht), static_cast<const float*>(et), rows, d, I, Rs, gamma, k,
+                           static_cast<float*>(act));
+        hipLaunchKernelGGL(down_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
+                           static_cast<const float*>(w_down), static_cast<const float*>(act),
+                           static_cast<const float*>(h), rows, d, I, Rs, gamma, k, static_cast<float*>(hp));
+    }
+    return hipGetLastError();
+}
+
+}  // namespace tf

@@ -114,17 +114,21 @@ def _normal(shape, std, g, device, dtype):
     return x.to(dtype)
 
 
-def make_weights(w: Workload, device="cpu") -> Dict[str, torch.Tensor]:
-    """Weights in draw order: LM head, embedding, gate, up, down, then gains."""
+def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> Dict[str, torch.Tensor]:
+    """Weights in draw order: LM head, embedding, gate, up, down, then gains.
+
+    ``weight_std`` other than 0.02 is only used by tests that want sharper
+    distributions on small shapes.
+    """
     device = torch.device(device)
     dt = w.torch_dtype
     g = _generator(device, w.weight_seed)
     out = {}
-    out["lm_head"] = _normal((w.V, w.d), WEIGHT_STD, g, device, dt)
-    out["emb"] = _normal((w.V, w.d), WEIGHT_STD, g, device, dt)
-    out["w_gate"] = _normal((w.I, 2 * w.d), WEIGHT_STD, g, device, dt)
-    out["w_up"] = _normal((w.I, 2 * w.d), WEIGHT_STD, g, device, dt)
-    out["w_down"] = _normal((w.d, w.I), WEIGHT_STD, g, device, dt)
+    out["lm_head"] = _normal((w.V, w.d), weight_std, g, device, dt)
+    out["emb"] = _normal((w.V, w.d), weight_std, g, device, dt)
+    out["w_gate"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
+    out["w_up"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
+    out["w_down"] = _normal((w.d, w.I), weight_std, g, device, dt)
     out["norm_h_gain"] = torch.ones(w.d, device=device, dtype=dt)
     out["norm_e_gain"] = torch.ones(w.d, device=device, dtype=dt)
     return out
@@ -149,10 +153,11 @@ def default_device_for(w: Workload) -> str:
     return "cpu" if w.V * w.d <= (1 << 22) else "cuda"
 
 
-def make_inputs(w: Workload, device: Optional[str] = None) -> Dict[str, torch.Tensor]:
+def make_inputs(w: Workload, device: Optional[str] = None,
+                weight_std: float = WEIGHT_STD) -> Dict[str, torch.Tensor]:
     """All inputs of one workload, drawn on ``device`` (default per workload)."""
     device = device or default_device_for(w)
-    out = make_weights(w, device)
+    out = make_weights(w, device, weight_std)
     out.update(make_states(w, device))
     return out
 

@@ -1,0 +1,132 @@
+"""Comparators between the HIP path and the CPU oracle.
+
+* ``check_topk``: a GPU top-k list passes when its ids are distinct, the
+  oracle value of the GPU id at position j is within tol of the oracle's own
+  j-th best value, and the GPU value is within tol of the oracle value of the
+  same id.  This forces equal ids wherever the oracle's neighbouring values
+  are more than tol apart, and admits any order inside a cluster of near-ties.
+* ``check_tree_exact``: the tree kernel fed the oracle's rows must reproduce
+  the oracle tree bit for bit.
+* ``replay_tree``: end to end, every GPU pop must be an admissible candidate
+  whose oracle path score is within tol of the best admissible oracle score,
+  and whose GPU score is within tol of its oracle score.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2606_03819_amd import synth
+
+
+def np64(t):
+    return synth.to_numpy64(t)
+
+
+def oracle_inputs(inputs):
+    """float64/int64 numpy copies of every input tensor."""
+    return {k: np64(v) for k, v in inputs.items()}
+
+
+def topk_values_sorted(full: np.ndarray, k: int) -> np.ndarray:
+    """The k largest values of each row, descending."""
+    V = full.shape[-1]
+    part = np.partition(full, V - k, axis=-1)[..., V - k:]
+    return -np.sort(-part, axis=-1)
+
+
+def check_topk(gpu_idx, gpu_val, oracle_full, tol, what=""):
+    """P1 comparator; gpu_idx/gpu_val [n, k], oracle_full [n, V] in the same units."""
+    gpu_idx = np.asarray(gpu_idx).reshape(-1, np.asarray(gpu_idx).shape[-1]).astype(np.int64)
+    gpu_val = np.asarray(gpu_val, dtype=np.float64).reshape(gpu_idx.shape)
+    full = np.asarray(oracle_full, dtype=np.float64).reshape(gpu_idx.shape[0], -1)
+    n, k = gpu_idx.shape
+    V = full.shape[1]
+    assert np.all((gpu_idx >= 0) & (gpu_idx < V)), f"{what}: ids out of range"
+    for r in range(n):
+        assert len(set(gpu_idx[r].tolist())) == k, f"{what}: duplicate ids in row {r}"
+    ref = topk_values_sorted(full, k)
+    o_of_gpu = np.take_along_axis(full, gpu_idx, axis=1)
+    err_rank = np.abs(o_of_gpu - ref)
+    err_val = np.abs(gpu_val - o_of_gpu)
+    worst_rank = float(err_rank.max())
+    worst_val = float(err_val.max())
+    assert worst_rank <= tol, f"{what}: GPU list departs from the oracle order by {worst_rank:.3g} > {tol}"
+    assert worst_val <= tol, f"{what}: GPU values differ from the oracle by {worst_val:.3g} > {tol}"
+    return {"max_rank_err": worst_rank, "max_val_err": worst_val,
+            "exact_ids": float(np.mean(gpu_idx == np.argsort(-full, axis=1, kind="stable")[:, :k]))}
+
+
+def check_tree_exact(gpu_tree, ref_tree, what=""):
+    for f in ("token", "parent", "depth", "score", "child_row"):
+        g = np.asarray(gpu_tree[f])
+        o = np.asarray(ref_tree[f])
+        assert np.array_equal(g, o), f"{what}: tree field {f} differs\nGPU {g}\noracle {o}"
+
+
+def replay_tree(gpu_tree, row_lp, topk_seq, gamma, M, B, tol, what=""):
+    """End-to-end tree check against oracle rows.
+
+    gpu_tree: dict of numpy arrays for one sequence; row_lp: dict row -> full
+    oracle log-prob row (float64, length V) for every row the replay needs;
+    topk_seq: [gamma, M] stage-1 candidates the rows were conditioned on.
+    """
+    tok = np.asarray(gpu_tree["token"])
+    par = np.asarray(gpu_tree["parent"])
+    dep = np.asarray(gpu_tree["depth"])
+    gsc = np.asarray(gpu_tree["score"], dtype=np.float64)
+    osc = np.zeros(B)
+    children = {-1: set()}
+    rowof = {-1: 0}
+    order = {}
+    worst = 0.0
+
+    def best_child(p):
+        lp = row_lp[rowof[p]]
+        if p not in order:
+            order[p] = np.argsort(-lp, kind="stable")
+        for t in order[p]:
+            if int(t) not in children[p]:
+                return (osc[p] if p >= 0 else 0.0) + lp[t]
+        return -np.inf
+
+    for j in range(B):
+        p = int(par[j])
+        assert -1 <= p < j, f"{what}: node {j} has parent {p}"
+        assert p in rowof, f"{what}: node {j} hangs below a node that is not expandable"
+        assert dep[j] == (1 if p < 0 else dep[p] + 1), f"{what}: node {j} depth"
+        assert int(tok[j]) not in children[p], f"{what}: node {j} duplicates a sibling"
+        best = max(best_child(q) for q in rowof)
+        lp = row_lp[rowof[p]]
+        osc[j] = (osc[p] if p >= 0 else 0.0) + lp[int(tok[j])]
+        gap = best - osc[j]
+        worst = max(worst, gap, abs(gsc[j] - osc[j]))
+        assert gap <= tol, f"{what}: pop {j} is {gap:.3g} below the best admissible candidate"
+        assert abs(gsc[j] - osc[j]) <= tol, f"{what}: pop {j} score {gsc[j]} vs oracle {osc[j]}"
+        children[p].add(int(tok[j]))
+        children[j] = set()
+        if dep[j] < gamma:
+            hits = np.nonzero(np.asarray(topk_seq[dep[j] - 1]) == tok[j])[0]
+            if hits.size:
+                rowof[j] = 1 + (dep[j] - 1) * M + int(hits[0])
+                assert int(gpu_tree["child_row"][j]) == rowof[j], f"{what}: node {j} child_row"
+            else:
+                assert int(gpu_tree["child_row"][j]) == -1
+        else:
+            assert int(gpu_tree["child_row"][j]) == -1
+    return worst
+
+
+def rows_needed(gpu_tree, B):
+    """Rows whose entries appear in the tree (the root row and expanded nodes' rows)."""
+    need = {0}
+    for j in range(B):
+        c = int(gpu_tree["child_row"][j])
+        if c >= 0:
+            need.add(c)
+    return sorted(need)
+
+
+def to_cpu_tree(tree, s):
+    return {k: v[s].cpu().numpy() for k, v in tree.items()}

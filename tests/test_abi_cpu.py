@@ -1,0 +1,153 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments before touching HIP."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_03819_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "treeflash.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIB_PATH), reason="libtreeflash.so not built")
+
+FAKE = 0x10000          # 16-byte aligned non-null dummy pointers: never dereferenced
+FAKE2 = 0x20000
+BF16, F32 = binding.TF_BF16, binding.TF_F32
+INVALID, UNSUPPORTED, WORKSPACE = 1, 2, 3
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(treeflash_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(binding.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported():
+    lib = binding.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for s in range(5):
+        assert binding.status_string(s) and binding.status_string(s) != "unknown status"
+    assert binding.status_string(99) == "unknown status"
+
+
+def test_workspace_size_is_monotone_and_rejects_bad_shapes():
+    f = binding.lib().treeflash_workspace_bytes
+    small = f(1, 16, 4096, 4096, 151936, 8, 32, BF16)
+    big = f(16, 16, 4096, 4096, 151936, 8, 32, BF16)
+    assert 0 < small < big
+    assert f(1, 8, 256, 256, 4096, 4, 16, F32) > 0
+    assert f(0, 16, 4096, 4096, 151936, 8, 32, BF16) == 0         # b < 1
+    assert f(1, 16, 4100, 4096, 151936, 8, 32, BF16) == 0         # d % 16
+    assert f(1, 16, 4096, 4096, 151936, 8, 151937, BF16) == 0     # topk2 > V
+    assert f(1, 16, 4096, 4096, 8, 9, 8, BF16) == 0               # k > V
+    assert f(1, 16, 4096, 4096, 151936, 8, 32, 7) == 0            # dtype
+
+
+def _marginal(**over):
+    a = dict(h=FAKE, w=FAKE, b=1, gamma=16, d=4096, V=151936, k=8, it=1.0, dt=BF16, idx=FAKE2, lp=None,
+             lse=None, ws=FAKE, wsb=1 << 40, st=None)
+    a.update(over)
+    return binding.lib().treeflash_marginal_topk(a["h"], a["w"], a["b"], a["gamma"], a["d"], a["V"], a["k"],
+                                                 a["it"], a["dt"], a["idx"], a["lp"], a["lse"], a["ws"], a["wsb"],
+                                                 a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(h=None), INVALID), (dict(w=None), INVALID), (dict(idx=None), INVALID),
+    (dict(b=0), INVALID), (dict(gamma=0), INVALID), (dict(d=4090), INVALID), (dict(d=0), INVALID),
+    (dict(k=0), INVALID), (dict(k=151937), INVALID), (dict(k=2000), INVALID), (dict(V=0), INVALID),
+    (dict(it=0.0), INVALID), (dict(it=-1.0), INVALID), (dict(it=float("inf")), INVALID),
+    (dict(it=float("nan")), INVALID), (dict(dt=5), INVALID), (dict(h=FAKE + 4), INVALID),
+    (dict(lp=FAKE + 2), INVALID), (dict(lse=FAKE + 1), INVALID), (dict(w=FAKE + 4), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws=FAKE + 8), WORKSPACE),
+    (dict(wsb=1024), WORKSPACE),
+])
+def test_marginal_topk_rejects(over, code):
+    assert _marginal(**over) == code
+
+
+def _expand(**over):
+    a = dict(h=FAKE, root=FAKE, topk=FAKE, emb=FAKE, gh=None, ge=None, wg=FAKE, wu=FAKE, wd=FAKE, lm=FAKE,
+             b=1, gamma=16, d=4096, I=4096, V=151936, k=8, topk2=32, it=1.0, eps=1e-6, dt=BF16,
+             ci=FAKE2, cl=FAKE2, lse=None, ws=FAKE, wsb=1 << 40, st=None)
+    a.update(over)
+    return binding.lib().treeflash_arapprox_expand(
+        a["h"], a["root"], a["topk"], a["emb"], a["gh"], a["ge"], a["wg"], a["wu"], a["wd"], a["lm"], a["b"],
+        a["gamma"], a["d"], a["I"], a["V"], a["k"], a["topk2"], a["it"], a["eps"], a["dt"], a["ci"], a["cl"],
+        a["lse"], a["ws"], a["wsb"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(h=None), INVALID), (dict(root=None), INVALID), (dict(topk=None), INVALID), (dict(emb=None), INVALID),
+    (dict(wg=None), INVALID), (dict(wu=None), INVALID), (dict(wd=None), INVALID), (dict(lm=None), INVALID),
+    (dict(ci=None), INVALID), (dict(cl=None), INVALID), (dict(I=0), INVALID), (dict(I=100), INVALID),
+    (dict(topk2=0), INVALID), (dict(topk2=151937), INVALID), (dict(topk2=2048), INVALID),
+    (dict(eps=-1.0), INVALID), (dict(eps=float("nan")), INVALID), (dict(it=0.0), INVALID),
+    (dict(gh=FAKE + 2), INVALID), (dict(lse=FAKE + 2), INVALID), (dict(gamma=300), INVALID),
+    (dict(wd=FAKE + 4), INVALID), (dict(lm=FAKE + 8), INVALID), (dict(ci=FAKE + 1), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(wsb=4096), WORKSPACE),
+])
+def test_arapprox_expand_rejects(over, code):
+    assert _expand(**over) == code
+
+
+def _hidden(**over):
+    a = dict(h=FAKE, root=FAKE, topk=FAKE, emb=FAKE, gh=None, ge=None, wg=FAKE, wu=FAKE, wd=FAKE,
+             b=1, gamma=16, d=4096, I=4096, V=151936, k=8, eps=1e-6, dt=BF16, hp=FAKE2, ws=FAKE, wsb=1 << 40,
+             st=None)
+    a.update(over)
+    return binding.lib().treeflash_arapprox_hidden(
+        a["h"], a["root"], a["topk"], a["emb"], a["gh"], a["ge"], a["wg"], a["wu"], a["wd"], a["b"], a["gamma"],
+        a["d"], a["I"], a["V"], a["k"], a["eps"], a["dt"], a["hp"], a["ws"], a["wsb"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(h=None), INVALID), (dict(root=None), INVALID), (dict(topk=None), INVALID), (dict(emb=None), INVALID),
+    (dict(wg=None), INVALID), (dict(wu=None), INVALID), (dict(wd=None), INVALID), (dict(hp=None), INVALID),
+    (dict(hp=FAKE2 + 2), INVALID), (dict(I=24), INVALID), (dict(eps=float("inf")), INVALID),
+    (dict(k=0), INVALID), (dict(ws=None), WORKSPACE), (dict(wsb=100), WORKSPACE),
+])
+def test_arapprox_hidden_rejects(over, code):
+    assert _hidden(**over) == code
+
+
+def _tree(**over):
+    a = dict(ci=FAKE, cl=FAKE, tk=FAKE, b=1, gamma=16, k=8, topk2=32, B=32, tok=FAKE2, par=FAKE2, dep=FAKE2,
+             sc=FAKE2, cr=None, st=None)
+    a.update(over)
+    return binding.lib().treeflash_build_tree(a["ci"], a["cl"], a["tk"], a["b"], a["gamma"], a["k"], a["topk2"],
+                                              a["B"], a["tok"], a["par"], a["dep"], a["sc"], a["cr"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(ci=None), INVALID), (dict(cl=None), INVALID), (dict(tk=None), INVALID), (dict(tok=None), INVALID),
+    (dict(par=None), INVALID), (dict(dep=None), INVALID), (dict(sc=None), INVALID), (dict(B=0), INVALID),
+    (dict(B=5000), INVALID), (dict(b=0), INVALID), (dict(k=0), INVALID), (dict(topk2=0), INVALID),
+    (dict(cr=FAKE + 2), INVALID), (dict(tk=FAKE + 1), INVALID),
+    # rows shorter than B must be full rows able to hold B nodes: 4 * (1 + 2) = 12 < 13
+    (dict(gamma=2, k=2, topk2=4, B=13), INVALID),
+    # the frontier and node arrays of a very large budget do not fit in LDS
+    (dict(gamma=200, k=200, topk2=4000, B=4000), UNSUPPORTED),
+])
+def test_build_tree_rejects(over, code):
+    assert _tree(**over) == code
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    h = torch.zeros(1, 2, 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        binding.treeflash_marginal_topk(h, torch.zeros(8, 16, dtype=torch.bfloat16), 2,
+                                        workspace=torch.zeros(1 << 16, dtype=torch.uint8),
+                                        topk_idx=torch.zeros(1, 2, 2, dtype=torch.int32),
+                                        topk_logprob=torch.zeros(1, 2, 2))
