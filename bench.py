@@ -22,7 +22,11 @@ import time
 
 import torch
 
-from paper_2606_03819_amd import binding, synth
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2606_03819_amd import binding, synth  # noqa: E402
 
 METRIC = "draft trees/sec (+ conditional rows/sec) at Qwen3-8B shape; HBM GB/s or MFMA % of peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E

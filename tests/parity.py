@@ -130,3 +130,75 @@ def rows_needed(gpu_tree, B):
 
 def to_cpu_tree(tree, s):
     return {k: v[s].cpu().numpy() for k, v in tree.items()}
+
+
+def _oracle_rows(o_in, w, topk_seq, s):
+    depth, _ = oracle.row_table(w.gamma, w.k)
+    prev = oracle.previous_tokens(int(o_in["root"][s]), topk_seq, w.gamma, w.k)
+    hp = oracle.ar_approximator(o_in["h"][s], prev, depth, o_in["emb"], o_in["norm_h_gain"], o_in["norm_e_gain"],
+                                o_in["w_gate"], o_in["w_up"], o_in["w_down"], mirror_bf16=(w.dtype == "bf16"))
+    return oracle.conditional_stage(hp, o_in["lm_head"], w.topk2, w.inv_temperature, keep_full=True)
+
+
+def check_draft(w, g, o_in, seqs, tol, log=print):
+    """Whole-path parity for the sequences ``seqs`` of workload ``w``.
+
+    g: GPU input tensors; o_in: float64 numpy copies of the same inputs.
+    1. stage 1 (GPU) against the oracle's marginal rows;
+    2. stage 2 and the tree on the GPU, fed the oracle's stage-1 candidates,
+       against the oracle's conditional rows (top-k lists, log-sum-exp, tree
+       replay);
+    3. the tree kernel fed the oracle's own rows reproduces the oracle tree
+       bit for bit;
+    4. the GPU's own end-to-end step equals the teacher-forced GPU outputs
+       whenever its stage-1 candidates equal the oracle's (else the sequence
+       sits on a stage-1 near-tie and only steps 1-3 apply).
+    The oracle never consumes a HIP-path output.
+    """
+    from paper_2606_03819_amd import binding
+    dr = binding.Drafter(g, w.b, w.gamma, w.k, w.B, w.inv_temperature)
+    idx1, lp1 = dr.stage1(g["h"])
+    gpu_topk = idx1.cpu().numpy()
+    gpu_lp1 = lp1.cpu().numpy()
+    o_topk = np.zeros_like(gpu_topk)
+    stats = {}
+    for s in seqs:
+        st1 = oracle.marginal_stage(o_in["h"][s:s + 1], o_in["lm_head"], w.k, w.inv_temperature)
+        r = check_topk(gpu_topk[s], gpu_lp1[s], st1["logprob"][0], tol, f"{w.name} stage 1 seq {s}")
+        stats[f"stage1_seq{s}"] = r
+        o_topk[s] = st1["topk_idx"][0]
+    # teacher forcing: the oracle's candidates for the sampled sequences (the
+    # others keep the GPU's, they are not checked)
+    forced = gpu_topk.copy()
+    forced[list(seqs)] = o_topk[list(seqs)]
+    forced_t = torch.from_numpy(forced).to(torch.int32).cuda()
+    ci, cl, lse = dr.stage2(g["h"], g["root"], topk_idx=forced_t)
+    tree_tf = dr.tree_build(topk_idx=forced_t)
+    ci, cl, lse = ci.cpu().numpy(), cl.cpu().numpy(), lse.cpu().numpy()
+    tree_tf = {k: v.cpu().numpy() for k, v in tree_tf.items()}
+    for s in seqs:
+        rows = _oracle_rows(o_in, w, o_topk[s], s)
+        stats[f"stage2_seq{s}"] = check_topk(ci[s], cl[s], rows["logprob"], tol, f"{w.name} stage 2 seq {s}")
+        lse_err = float(np.max(np.abs(lse[s] - rows["cond_lse"])))
+        assert lse_err <= tol, f"{w.name}: log-sum-exp off by {lse_err}"
+        t = {k: v[s] for k, v in tree_tf.items()}
+        rl = {r: rows["logprob"][r] for r in rows_needed(t, w.B)}
+        stats[f"tree_replay_seq{s}"] = replay_tree(t, rl, o_topk[s], w.gamma, w.k, w.B, tol, f"{w.name} tree seq {s}")
+        gt = binding.treeflash_build_tree(torch.from_numpy(rows["cond_idx"][None]).cuda(),
+                                          torch.from_numpy(rows["cond_logprob"][None]).cuda(),
+                                          torch.from_numpy(o_topk[s][None]).to(torch.int32).cuda(), w.B)
+        ref = oracle.build_tree(rows["cond_idx"], rows["cond_logprob"], o_topk[s], w.gamma, w.k, w.B)
+        check_tree_exact(to_cpu_tree(gt, 0), ref, f"{w.name} tree kernel seq {s}")
+    # end to end
+    full = {k: v.clone() for k, v in dr.step(g["h"], g["root"]).items()}
+    e2e_ci, e2e_cl = dr.cond_idx.cpu().numpy(), dr.cond_lp.cpu().numpy()
+    same = 0
+    for s in seqs:
+        if np.array_equal(gpu_topk[s], o_topk[s]):
+            same += 1
+            assert np.array_equal(e2e_ci[s], ci[s]) and np.array_equal(e2e_cl[s], cl[s])
+            for k in tree_tf:
+                assert np.array_equal(full[k][s].cpu().numpy(), tree_tf[k][s]), f"{w.name}: e2e tree {k}"
+    stats["e2e_sequences_equal_to_forced"] = same
+    log(f"[parity] {w.name}: {stats}")
+    return stats

@@ -1,0 +1,30 @@
+"""Parity at the full Qwen3-shaped sizes, in the launch configuration the
+benchmark times (same plans, same kernels), on sampled sequences: stage 1 on
+every depth, stage 2 on every conditional row, the tree replay and the
+bit-exact tree kernel check.  Weights are drawn on the GPU and copied to the
+host as float64 for the oracle."""
+import gc
+
+import pytest
+import torch
+
+from paper_2606_03819_amd import synth
+from parity import check_draft, oracle_inputs
+
+pytestmark = pytest.mark.gpu
+
+FULL = [("qwen3-4b-shape", [0]), ("qwen3-8b-shape", [0]), ("qwen3-8b-shape-k16-b64", [0]),
+        ("qwen3-8b-shape-batch16", [0, 15])]
+
+
+@pytest.mark.parametrize("name,seqs", FULL, ids=[f[0] for f in FULL])
+def test_full_size_parity(name, seqs):
+    w = synth.get_workload(name)
+    print(f"[fullsize] {name}: drawing inputs on the GPU", flush=True)
+    g = synth.make_inputs(w, "cuda")
+    o_in = oracle_inputs(g)
+    print(f"[fullsize] {name}: oracle inputs ready; checking sequences {seqs}", flush=True)
+    check_draft(w, g, o_in, seqs, 2e-2, log=lambda m: print(m, flush=True))
+    del g, o_in
+    gc.collect()
+    torch.cuda.empty_cache()

@@ -12,8 +12,7 @@ import torch
 
 import oracle
 from paper_2606_03819_amd import binding, synth
-from parity import (check_topk, check_tree_exact, np64, oracle_inputs, replay_tree, rows_needed,
-                    to_cpu_tree)
+from parity import _oracle_rows, check_draft, check_topk, oracle_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -41,58 +40,11 @@ def to_gpu(inputs):
     return {k: v.cuda() for k, v in inputs.items()}
 
 
-def run_oracle_rows(o_in, w, topk_seq, s, rows=None):
-    """Oracle h' and full conditional log-prob rows of sequence s, given candidates."""
-    depth, _ = oracle.row_table(w.gamma, w.k)
-    prev = oracle.previous_tokens(int(o_in["root"][s]), topk_seq, w.gamma, w.k)
-    hp = oracle.ar_approximator(o_in["h"][s], prev, depth, o_in["emb"], o_in["norm_h_gain"], o_in["norm_e_gain"],
-                                o_in["w_gate"], o_in["w_up"], o_in["w_down"], mirror_bf16=(w.dtype == "bf16"))
-    sel = np.arange(hp.shape[0]) if rows is None else np.asarray(rows)
-    st = oracle.conditional_stage(hp[sel], o_in["lm_head"], w.topk2, w.inv_temperature, keep_full=True)
-    return st, sel
-
-
 @pytest.mark.parametrize("w,std", CASES, ids=[c[0].name for c in CASES])
 def test_draft_matches_oracle(w, std):
     print(f"[parity] case={w.name} shape=b{w.b} d{w.d} V{w.V} g{w.gamma} k{w.k} B{w.B}", flush=True)
     cpu = synth.make_inputs(w, "cpu", weight_std=std)
-    g = to_gpu(cpu)
-    o_in = oracle_inputs(cpu)
-    tol = tol_for(w)
-    dr = binding.Drafter(g, w.b, w.gamma, w.k, w.B, w.inv_temperature)
-
-    # stage 1
-    idx1, lp1 = dr.stage1(g["h"])
-    st1 = oracle.marginal_stage(o_in["h"], o_in["lm_head"], w.k, w.inv_temperature)
-    check_topk(idx1.cpu().numpy(), lp1.cpu().numpy(), st1["logprob"], tol, f"{w.name} stage 1")
-    gpu_topk = idx1.cpu().numpy()
-
-    # stage 2 teacher-forced on the oracle's candidates
-    o_topk = torch.from_numpy(st1["topk_idx"]).to(torch.int32).cuda()
-    ci, cl, lse = dr.stage2(g["h"], g["root"], topk_idx=o_topk)
-    ci, cl, lse = ci.cpu().numpy(), cl.cpu().numpy(), lse.cpu().numpy()
-    for s in range(w.b):
-        st, _ = run_oracle_rows(o_in, w, st1["topk_idx"][s], s)
-        check_topk(ci[s], cl[s], st["logprob"], tol, f"{w.name} stage 2 seq {s}")
-        assert np.max(np.abs(lse[s] - st["cond_lse"])) <= tol, f"{w.name}: log-sum-exp"
-        # tree kernel on the oracle's own rows: bit-exact
-        tree_in = (torch.from_numpy(st["cond_idx"][None]).cuda(), torch.from_numpy(st["cond_logprob"][None]).cuda(),
-                   torch.from_numpy(st1["topk_idx"][s][None]).to(torch.int32).cuda())
-        gt = binding.treeflash_build_tree(*tree_in, w.B)
-        ref = oracle.build_tree(st["cond_idx"], st["cond_logprob"], st1["topk_idx"][s], w.gamma, w.k, w.B)
-        check_tree_exact(to_cpu_tree(gt, 0), ref, f"{w.name} tree seq {s}")
-
-    # end to end on the GPU's own candidates
-    tree = dr.step(g["h"], g["root"])
-    assert np.array_equal(dr.topk_idx.cpu().numpy(), gpu_topk)
-    ci, cl = dr.cond_idx.cpu().numpy(), dr.cond_lp.cpu().numpy()
-    for s in range(w.b):
-        st, _ = run_oracle_rows(o_in, w, gpu_topk[s], s)
-        check_topk(ci[s], cl[s], st["logprob"], tol, f"{w.name} e2e rows seq {s}")
-        t = to_cpu_tree(tree, s)
-        rl = {r: st["logprob"][r] for r in rows_needed(t, w.B)}
-        worst = replay_tree(t, rl, gpu_topk[s], w.gamma, w.k, w.B, tol, f"{w.name} e2e tree seq {s}")
-        print(f"[parity] {w.name} seq {s}: worst tree score gap {worst:.2e}", flush=True)
+    check_draft(w, to_gpu(cpu), oracle_inputs(cpu), range(w.b), tol_for(w))
 
 
 def test_repeatable_and_stream_ordered():
@@ -128,7 +80,7 @@ def test_exact_ties_take_smaller_ids_and_use_the_slow_path():
     st1 = oracle.marginal_stage(o_in["h"], o_in["lm_head"], w.k, 1.0)
     assert np.array_equal(idx.cpu().numpy(), st1["topk_idx"])   # ties at the boundary go to smaller ids
     dr.stage2(g["h"], g["root"])
-    st, _ = run_oracle_rows(o_in, w, idx.cpu().numpy()[0], 0)
+    st = _oracle_rows(o_in, w, st1["topk_idx"][0], 0)
     check_topk(dr.cond_idx.cpu().numpy()[0], dr.cond_lp.cpu().numpy()[0], st["logprob"], 2e-2, "ties stage 2")
 
 
