@@ -36,8 +36,8 @@ bool common_shapes_ok(int b, int gamma, int d, int V, int k, bool rows_only = fa
 }
 
 size_t stage1_bytes(int b, int gamma, int V, bool bf16) {
-    const LmPlan p = lm_plan(b * gamma, V, bf16);
-    return 256 + align256((size_t)b * gamma * p.nsplit * kPartStride * 4);
+    const GemmPlan p = lm_plan(b * gamma, V, bf16);
+    return 256 + align256((size_t)b * gamma * p.nchunks * kPartStride * 4);
 }
 
 }  // namespace
@@ -113,7 +113,9 @@ tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, 
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     const hipError_t e = launch_arapprox(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
                                          w_down, b, gamma, d, I, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et,
-                                         ws + lay.act, hprime, reinterpret_cast<int*>(ws + lay.diag), stream);
+                                         ws + lay.act, hprime, reinterpret_cast<float*>(ws + lay.mlp_part),
+                                         reinterpret_cast<int*>(ws + lay.counters), reinterpret_cast<int*>(ws + lay.diag),
+                                         stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
@@ -140,7 +142,8 @@ tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, 
     int* diag = reinterpret_cast<int*>(ws + lay.diag);
     hipError_t e = launch_arapprox(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down, b,
                                    gamma, d, I, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et, ws + lay.act,
-                                   ws + lay.hp, diag, stream);
+                                   ws + lay.hp, reinterpret_cast<float*>(ws + lay.mlp_part),
+                                   reinterpret_cast<int*>(ws + lay.counters), diag, stream);
     if (e != hipSuccess) return TF_ERR_HIP;
     const int rows = b * (1 + (gamma - 1) * k);
     e = launch_lmhead_topk(ws + lay.hp, d, lm_head, rows, d, V, topk2, inv_temperature, bf16,

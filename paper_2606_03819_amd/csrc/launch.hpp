@@ -17,7 +17,8 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
 hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
                            const void* gain_h, const void* gain_e, const void* w_gate, const void* w_up,
                            const void* w_down, int b, int gamma, int d, int I, int V, int k, float eps,
-                           bool bf16, void* ht, void* et, void* act, void* hp, int* diag, hipStream_t stream);
+                           bool bf16, void* ht, void* et, void* act, void* hp, float* mlp_partial, int* counters,
+                           int* diag, hipStream_t stream);
 
 // Best-first tree selection, one workgroup per sequence.
 hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, const int32_t* topk_idx, int b,

@@ -5,7 +5,7 @@ namespace tf {
 
 // Entries each (row, vocabulary slice) partial keeps, and the partial layout:
 // [max, sum, bound, count, val[kKeep], idx[kKeep]] (raw, unscaled logits).
-constexpr int kKeep = 8;
+constexpr int kKeep = 4;
 constexpr int kPartStride = 4 + 2 * kKeep;
 // Per-lane running list length inside the LM-head epilogue.
 constexpr int kLane = 4;

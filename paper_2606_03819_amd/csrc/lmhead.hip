@@ -12,20 +12,24 @@ namespace tf {
 
 // ------------------------------------------------------------ bf16 / MFMA
 
-template <int WM, int NT>
-__global__ __launch_bounds__(256) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
+#ifndef TF_LM_MIN_BLOCKS
+#define TF_LM_MIN_BLOCKS 2
+#endif
+
+template <int WM, int NT, int PIPE, bool WNT>
+__global__ __launch_bounds__(256, TF_LM_MIN_BLOCKS) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
                                                           const uint16_t* __restrict__ w, GemmShape sh,
                                                           int V, float sl2, float* __restrict__ part,
                                                           int* __restrict__ diag) {
     using Tr = GemmTraits<WM, NT>;
     using E = EpiLmHead<WM, NT>;
-    constexpr int SMEM = Tr::XS_BYTES > E::MERGE_BYTES ? Tr::XS_BYTES : E::MERGE_BYTES;
+    constexpr int SMEM = Tr::SMEM_BYTES > E::MERGE_BYTES ? Tr::SMEM_BYTES : E::MERGE_BYTES;
     __shared__ __align__(16) unsigned char smem[SMEM];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     WRowsPlain ws{w, V, sh.K};
     XRowsPlain xs{x, ldx};
     E epi{part, V, sl2};
-    stream_gemm_body<WM, NT>(ws, xs, epi, sh, smem);
+    stream_gemm_body<WM, NT, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
 // ------------------------------------------------------------ fp32 / SIMT
@@ -46,8 +50,8 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
     const int split = L / sh.nrb;
     const int rb = L - split * sh.nrb;
     const int row0 = rb * 32;
-    const int t0 = (int)(((long long)split * sh.ntiles) / sh.nsplit);
-    const int t1 = (int)(((long long)(split + 1) * sh.ntiles) / sh.nsplit);
+    const int t0 = split * 8;
+    const int t1 = min(t0 + 8, sh.ntiles);
     const int vend = min(V, t1 * 32);
     const int srow = tid >> 3, sub = tid & 7;
 
@@ -138,14 +142,14 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
         c[3 + kLane + e] = __int_as_float(li[e]);
     }
     __syncthreads();
-    lm_merge_contributors(cmrg, 32, row0, split, sl2, part, sh);
+    lm_merge_contributors(cmrg, 32, row0, split, sh.nchunks, sh.R, sl2, part);
 }
 
 // ------------------------------------------------------------------ merge
 
 struct MergeArgs {
     const float* part;
-    int nsplit, ntiles, K, V, d;
+    int nsplit, chunk_tiles, ntiles, K, V, d;
     float inv_t, sl2;
     int32_t* out_idx;
     float* out_lp;
@@ -190,131 +194,85 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
     return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// One workgroup per row.  The candidates are the rows' slice lists; a radix
-// select over 64-bit keys (value, then inverted id) finds the k-th best, the
-// selected entries are bitonic-sorted, and every slice whose bound reaches the
-// k-th value is re-evaluated exactly (dot products straight from memory), so
-// the result is the exact top-k of the row whatever the data.
+// Descending bitonic sort of one value per lane across a wave.
+__device__ __forceinline__ float wave_sort_desc(float v, int lane) {
+    for (int k = 2; k <= 64; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const float o = __shfl_xor(v, j);
+            const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
+            v = keep_max ? fmaxf(v, o) : fminf(v, o);
+        }
+    return v;
+}
+
+constexpr int kMergeCap = kMaxSplits * kKeep;   // candidate buffer: every slice entry fits
+
+// One workgroup per row.
+//  1. log-sum-exp of the row from the slices' (max, sum) pairs;
+//  2. a lower bound t0 on the row's k-th best value: within a wave, sort the
+//     lanes' best slice heads; k distinct slices reach the k-th of them, so
+//     at least k candidates are >= it (k <= 64; otherwise t0 = -inf);
+//  3. every slice entry >= t0 goes to LDS, is bitonic-sorted, and the first k
+//     are the row's top-k among the candidates;
+//  4. a slice whose bound (everything it dropped is <= bound) reaches the k-th
+//     value is re-evaluated exactly from memory, so the result is the exact
+//     top-k of the row for any data, ties included.
 template <class T>
 __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
-    constexpr int NPT = kMaxSplits * kKeep / 256;
     __shared__ float red[4];
-    __shared__ unsigned hist[256];
-    __shared__ int s_digit, s_krem, s_count, s_nflag, s_ncand;
-    __shared__ float sel_v[kMaxTopk];
-    __shared__ int sel_i[kMaxTopk];
+    __shared__ float s_bound[4];
+    __shared__ int s_count, s_nflag, s_ncand;
+    __shared__ float cand_v[kMergeCap];
+    __shared__ int cand_i[kMergeCap];
     __shared__ int s_flag[kMaxSplits];
-    __shared__ float cand_v[256];
-    __shared__ int cand_i[256];
 
     const int row = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int K = a.K;
     const float* P = a.part + (size_t)row * a.nsplit * kPartStride;
 
-    // log-sum-exp of the row from the slice (max, sum) pairs
     float M = neg_inf();
     for (int s = tid; s < a.nsplit; s += 256) M = fmaxf(M, P[s * kPartStride]);
     M = block_max(M, red);
     float S = 0.f;
+    float head = neg_inf();
     for (int s = tid; s < a.nsplit; s += 256) {
         const float ms = P[s * kPartStride];
         if (ms != neg_inf()) S += P[s * kPartStride + 1] * exp2f((ms - M) * a.sl2);
+        if (__float_as_int(P[s * kPartStride + 3]) > 0) head = fmaxf(head, P[s * kPartStride + 4]);
     }
     S = block_sum(S, red);
     const float logS = logf(S);
 
-    // candidate keys: (order-preserving value bits << 32) | ~id; 0 = empty
-    const int N = a.nsplit * kKeep;
-    unsigned long long key[NPT];
-#pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-        const int e = tid + 256 * i;
-        key[i] = 0ull;
-        if (e < N) {
-            const int s = e / kKeep, j = e - s * kKeep;
-            const int id = __float_as_int(P[s * kPartStride + 4 + kKeep + j]);
-            if (id >= 0)
-                key[i] = ((unsigned long long)f32_key(P[s * kPartStride + 4 + j]) << 32) | (unsigned)(~id);
-        }
-    }
-
-    // radix select of the K-th largest key, 8 bits at a time
-    unsigned long long prefix = 0ull, mask = 0ull;
-    int krem = K;
-    bool insufficient = false;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-        hist[tid] = 0u;
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < NPT; ++i)
-            if (key[i] != 0ull && (key[i] & mask) == prefix) atomicAdd(&hist[(key[i] >> shift) & 255u], 1u);
-        __syncthreads();
-        if (wave == 0) {
-            unsigned c[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) c[q] = hist[255 - 4 * lane - q];
-            const unsigned loc = c[0] + c[1] + c[2] + c[3];
-            unsigned inc = loc;
-            for (int o = 1; o < 64; o <<= 1) {
-                const unsigned t = __shfl_up(inc, o);
-                if (lane >= o) inc += t;
-            }
-            const unsigned exc = inc - loc;
-            if (exc < (unsigned)krem && (unsigned)krem <= inc) {
-                unsigned run = exc;
-                for (int q = 0; q < 4; ++q) {
-                    if (run + c[q] >= (unsigned)krem) {
-                        s_digit = 255 - 4 * lane - q;
-                        s_krem = krem - (int)run;
-                        break;
-                    }
-                    run += c[q];
-                }
-            }
-            if (lane == 63 && inc < (unsigned)krem) s_digit = -1;
-        }
-        __syncthreads();
-        const int dg = s_digit;
-        if (dg < 0) {
-            insufficient = true;
-            break;
-        }
-        krem = s_krem;
-        prefix |= (unsigned long long)dg << shift;
-        mask |= 0xffull << shift;
-        __syncthreads();
-    }
-
+    // lower bound on the k-th best value
+    const float sorted = wave_sort_desc(head, lane);
+    const float wb = K <= 64 ? __shfl(sorted, K - 1) : neg_inf();
+    if (lane == 0) s_bound[wave] = wb;
     if (tid == 0) {
         s_count = 0;
         s_nflag = 0;
     }
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-        if (key[i] != 0ull && (insufficient || key[i] >= prefix)) {
+    const float t0 = fmaxf(fmaxf(s_bound[0], s_bound[1]), fmaxf(s_bound[2], s_bound[3]));
+
+    for (int s = tid; s < a.nsplit; s += 256) {
+        const float* ps = P + s * kPartStride;
+        const int n = __float_as_int(ps[3]);
+        for (int e = 0; e < n; ++e) {
+            const float v = ps[4 + e];
+            if (!(v >= t0)) break;   // lists are sorted
             const int pos = atomicAdd(&s_count, 1);
-            if (pos < K) {   // keys are unique, so at most K entries qualify
-                sel_v[pos] = key_f32((unsigned)(key[i] >> 32));
-                sel_i[pos] = (int)(~(unsigned)key[i]);
-            }
+            cand_v[pos] = v;
+            cand_i[pos] = __float_as_int(ps[4 + kKeep + e]);
         }
     }
-    const float tval = insufficient ? neg_inf() : key_f32((unsigned)(prefix >> 32));
-    for (int s = tid; s < a.nsplit; s += 256) {
-        const float U = P[s * kPartStride + 2];
-        if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = s;
-    }
     __syncthreads();
-    int cnt = min(s_count, K);
-
-    // bitonic sort of the selected entries, best first
+    const int c = s_count;
     int pw = 1;
-    while (pw < cnt) pw <<= 1;
-    for (int i = cnt + tid; i < pw; i += 256) {
-        sel_v[i] = neg_inf();
-        sel_i[i] = 0x7fffffff;
+    while (pw < c) pw <<= 1;
+    for (int i = c + tid; i < pw; i += 256) {
+        cand_v[i] = neg_inf();
+        cand_i[i] = 0x7fffffff;
     }
     __syncthreads();
     for (int size = 2; size <= pw; size <<= 1) {
@@ -323,30 +281,42 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
                 const int lo = 2 * i - (i & (stride - 1));
                 const int hi = lo + stride;
                 const bool up = (lo & size) == 0;
-                const float vl = sel_v[lo], vh = sel_v[hi];
-                const int il = sel_i[lo], ih = sel_i[hi];
+                const float vl = cand_v[lo], vh = cand_v[hi];
+                const int il = cand_i[lo], ih = cand_i[hi];
                 const bool sw = up ? better(vh, ih, vl, il) : better(vl, il, vh, ih);
                 if (sw) {
-                    sel_v[lo] = vh;
-                    sel_i[lo] = ih;
-                    sel_v[hi] = vl;
-                    sel_i[hi] = il;
+                    cand_v[lo] = vh;
+                    cand_i[lo] = ih;
+                    cand_v[hi] = vl;
+                    cand_i[hi] = il;
                 }
             }
             __syncthreads();
         }
     }
+    int cnt = min(c, K);
+    float* sel_v = cand_v;   // the best cnt entries, sorted
+    int* sel_i = cand_i;
+
+    const float tval = cnt == K ? sel_v[K - 1] : neg_inf();
+    for (int s = tid; s < a.nsplit; s += 256) {
+        const float U = P[s * kPartStride + 2];
+        if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = s;
+    }
+    __syncthreads();
 
     // exact slow path for slices that may hide a qualifying logit
     const int nflag = s_nflag;
     if (nflag > 0) {
+        float* buf_v = cand_v + kMergeCap - 256;   // scratch past the sorted head (K <= kMaxTopk)
+        int* buf_i = cand_i + kMergeCap - 256;
         const T* xr = reinterpret_cast<const T*>(a.x) + (size_t)row * a.ldx;
         const T* wb = reinterpret_cast<const T*>(a.w);
         for (int f = 0; f < nflag; ++f) {
             const int s = s_flag[f];
-            const int t0 = (int)(((long long)s * a.ntiles) / a.nsplit);
-            const int t1 = (int)(((long long)(s + 1) * a.ntiles) / a.nsplit);
-            const int v0 = t0 * 32, v1 = min(a.V, t1 * 32);
+            const int t0s = s * a.chunk_tiles;
+            const int t1s = min(t0s + a.chunk_tiles, a.ntiles);
+            const int v0 = t0s * 32, v1 = min(a.V, t1s * 32);
             for (int vb = v0; vb < v1; vb += 256) {
                 if (tid == 0) s_ncand = 0;
                 __syncthreads();
@@ -362,19 +332,19 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
                             }
                     if (take) {
                         const int p = atomicAdd(&s_ncand, 1);
-                        cand_v[p] = val;
-                        cand_i[p] = v;
+                        buf_v[p] = val;
+                        buf_i[p] = v;
                     }
                 }
                 __syncthreads();
                 if (tid == 0) {
-                    int c = cnt;
+                    int cc = cnt;
                     for (int q = 0; q < s_ncand; ++q) {
-                        const float cv = cand_v[q];
-                        const int ci = cand_i[q];
+                        const float cv = buf_v[q];
+                        const int ci = buf_i[q];
                         int pos;
-                        if (c < K) {
-                            pos = c++;
+                        if (cc < K) {
+                            pos = cc++;
                         } else if (better(cv, ci, sel_v[K - 1], sel_i[K - 1])) {
                             pos = K - 1;
                         } else {
@@ -388,7 +358,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
                         sel_v[pos] = cv;
                         sel_i[pos] = ci;
                     }
-                    s_count = c;
+                    s_count = cc;
                 }
                 __syncthreads();
                 cnt = s_count;
@@ -408,35 +378,44 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 
 // ------------------------------------------------------------------ launchers
 
-template <int WM, int NT>
-static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, int V,
+template <int WM, int NT, int PIPE, bool WNT>
+static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, int blocks, int V,
                            float sl2, float* part, int* diag, hipStream_t st) {
-    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT>), dim3(sh.nsplit * sh.nrb), dim3(256), 0, st, x, ldx, w, sh,
-                       V, sl2, part, diag);
+    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, PIPE, WNT>), dim3(blocks), dim3(256), 0, st, x, ldx, w, sh, V,
+                       sl2, part, diag);
+}
+
+// tile shape and pipeline variants the plans can ask for
+static void dispatch_lm_bf16(const GemmPlan& p, const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
+                             int V, float sl2, float* part, int* diag, hipStream_t st) {
+    const int blocks = p.blocks();
+    if (p.NT == 1)
+        launch_lm_bf16<TF_LM_WM_NT1, 1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+    else if (p.NT == 2)
+        launch_lm_bf16<TF_LM_WM_NT2, 2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+    else if (p.wnt)
+        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+    else
+        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
 }
 
 hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
                               float inv_t, bool bf16, float* part, int32_t* out_idx, float* out_lp,
                               float* out_lse, int* diag, hipStream_t stream) {
-    const LmPlan p = lm_plan(rows, V, bf16);
-    GemmShape sh{rows, d, p.ntiles, p.nsplit, p.nrb};
+    const GemmPlan p = lm_plan(rows, V, bf16);
+    if (p.nchunks > kMaxSplits) return hipErrorInvalidValue;
+    GemmShape sh{rows, d, p.ntiles, p.nchunks, 1, p.nrb};
     const float sl2 = inv_t * kLog2e;
     if (bf16) {
-        const uint16_t* xb = static_cast<const uint16_t*>(x);
-        const uint16_t* wb = static_cast<const uint16_t*>(w);
-        switch (p.NT) {
-            case 1: launch_lm_bf16<2, 1>(xb, ldx, wb, sh, V, sl2, part, diag, stream); break;
-            case 2: launch_lm_bf16<2, 2>(xb, ldx, wb, sh, V, sl2, part, diag, stream); break;
-            default: launch_lm_bf16<2, 4>(xb, ldx, wb, sh, V, sl2, part, diag, stream); break;
-        }
+        dispatch_lm_bf16(p, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w), sh, V, sl2, part,
+                         diag, stream);
     } else {
-        hipLaunchKernelGGL(lmhead_f32_kernel, dim3(sh.nsplit * sh.nrb), dim3(256), 0, stream,
-                           static_cast<const float*>(x), ldx, static_cast<const float*>(w), sh, V, sl2, part,
-                           diag);
+        hipLaunchKernelGGL(lmhead_f32_kernel, dim3(p.blocks()), dim3(256), 0, stream, static_cast<const float*>(x),
+                           ldx, static_cast<const float*>(w), sh, V, sl2, part, diag);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    MergeArgs ma{part, p.nsplit, p.ntiles, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
+    MergeArgs ma{part, p.nchunks, p.chunk, p.ntiles, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
     if (bf16)
         hipLaunchKernelGGL(merge_topk_kernel<uint16_t>, dim3(rows), dim3(256), 0, stream, ma);
     else

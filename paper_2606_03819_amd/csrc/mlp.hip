@@ -26,9 +26,12 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
                                                            const T* __restrict__ emb, const T* __restrict__ gh,
                                                            const T* __restrict__ ge, int b, int gamma, int d, int V,
                                                            int M, int Rs, float eps, T* __restrict__ ht,
-                                                           T* __restrict__ et, int* __restrict__ diag) {
+                                                           T* __restrict__ et, int* __restrict__ diag,
+                                                           int* __restrict__ counters, int ncounters) {
     __shared__ float red[4];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
+    if (blockIdx.x == 0)   // split-K arrival counters of the SwiGLU products that follow on this stream
+        for (int i = threadIdx.x; i < ncounters; i += 256) counters[i] = 0;
     const int row = blockIdx.x;
     const T* src;
     const T* gain;
@@ -72,21 +75,23 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
 
 // ------------------------------------------------------------------ bf16
 
-template <int WM, int NT>
-__global__ __launch_bounds__(256) void gateup_bf16_kernel(WRowsGateUp ws, XRowsConcat xs, GemmShape sh,
-                                                          uint16_t* __restrict__ act, int I) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::XS_BYTES];
-    EpiSwiGLU<WM, NT> epi{act, I};
-    stream_gemm_body<WM, NT>(ws, xs, epi, sh, smem);
+template <int WM, int NT, int PIPE, bool WNT>
+__global__ __launch_bounds__(256, 2) void gateup_bf16_kernel(WRowsGateUp ws, XRowsConcat xs, GemmShape sh,
+                                                             uint16_t* __restrict__ act, int I, float* partial,
+                                                             int* counter) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::SMEM_BYTES];
+    EpiSplitK<WM, NT, EpiSwiGLU<WM, NT>> epi{EpiSwiGLU<WM, NT>{act, I}, partial, counter};
+    stream_gemm_body<WM, NT, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
-template <int WM, int NT>
-__global__ __launch_bounds__(256) void down_bf16_kernel(WRowsPlain ws, XRowsPlain xs, GemmShape sh,
-                                                        uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
-                                                        int d, int Rs, int gamma, int M) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::XS_BYTES];
-    EpiResidual<WM, NT> epi{hp, h, d, Rs, gamma, M};
-    stream_gemm_body<WM, NT>(ws, xs, epi, sh, smem);
+template <int WM, int NT, int PIPE, bool WNT>
+__global__ __launch_bounds__(256, 2) void down_bf16_kernel(WRowsPlain ws, XRowsPlain xs, GemmShape sh,
+                                                           uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
+                                                           int d, int Rs, int gamma, int M, float* partial,
+                                                           int* counter) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::SMEM_BYTES];
+    EpiSplitK<WM, NT, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, Rs, gamma, M}, partial, counter};
+    stream_gemm_body<WM, NT, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
 // ------------------------------------------------------------------ fp32
@@ -133,36 +138,40 @@ __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__
 
 // ------------------------------------------------------------------ launcher
 
-template <int WM, int NT>
+template <int WM, int NT, int PIPE, bool WNT>
 static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                             const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
-                            int I, int Rs, int gamma, int M, const LmPlan& pg, const LmPlan& pd, hipStream_t st) {
+                            int I, int Rs, int gamma, int M, const GemmPlan& pg, const GemmPlan& pd, float* partial,
+                            int* counters, hipStream_t st) {
     WRowsGateUp wgu{wg, wu, I, 2 * d};
     XRowsConcat xc{ht, et, d, Rs, gamma, M};
-    GemmShape shg{rows, 2 * d, pg.ntiles, pg.nsplit, pg.nrb};
-    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT>), dim3(pg.nsplit * pg.nrb), dim3(256), 0, st, wgu, xc, shg, act,
-                       I);
+    GemmShape shg{rows, 2 * d, pg.ntiles, pg.nchunks, pg.nkp, pg.nrb};
+    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, PIPE, WNT>), dim3(pg.blocks()), dim3(256), 0, st, wgu, xc, shg, act, I,
+                       partial, counters);
     WRowsPlain wdn{wd, d, I};
     XRowsPlain xa{act, (long)I};
-    GemmShape shd{rows, I, pd.ntiles, pd.nsplit, pd.nrb};
-    hipLaunchKernelGGL((down_bf16_kernel<WM, NT>), dim3(pd.nsplit * pd.nrb), dim3(256), 0, st, wdn, xa, shd, hp, h,
-                       d, Rs, gamma, M);
+    GemmShape shd{rows, I, pd.ntiles, pd.nchunks, pd.nkp, pd.nrb};
+    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, PIPE, WNT>), dim3(pd.blocks()), dim3(256), 0, st, wdn, xa, shd, hp, h, d, Rs,
+                       gamma, M, partial, counters + pg.nchunks * pg.nrb);
 }
 
 hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
                            const void* gain_h, const void* gain_e, const void* w_gate, const void* w_up,
                            const void* w_down, int b, int gamma, int d, int I, int V, int k, float eps,
-                           bool bf16, void* ht, void* et, void* act, void* hp, int* diag, hipStream_t stream) {
+                           bool bf16, void* ht, void* et, void* act, void* hp, float* mlp_partial, int* counters,
+                           int* diag, hipStream_t stream) {
     const int Rs = 1 + (gamma - 1) * k;
     const int rows = b * Rs;
     const int nrows = b * gamma + rows;
     if (bf16) {
+        const GemmPlan pg = mlp_plan(rows, cdiv(I, 16), 2 * d);
+        const GemmPlan pd = mlp_plan(rows, cdiv(d, 32), I);
+        const int ncounters = pg.nchunks * pg.nrb + pd.nchunks * pd.nrb;
         hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
                            static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),
                            static_cast<const uint16_t*>(gain_h), static_cast<const uint16_t*>(gain_e), b, gamma, d,
-                           V, k, Rs, eps, static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag);
-        const LmPlan pg = mlp_plan(rows, cdiv(I, 16));
-        const LmPlan pd = mlp_plan(rows, cdiv(d, 32));
+                           V, k, Rs, eps, static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag, counters,
+                           ncounters);
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         const uint16_t* wg = static_cast<const uint16_t*>(w_gate);
         const uint16_t* wu = static_cast<const uint16_t*>(w_up);
@@ -171,16 +180,26 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
         const uint16_t* etb = static_cast<const uint16_t*>(et);
         uint16_t* actb = static_cast<uint16_t*>(act);
         uint16_t* hpb = static_cast<uint16_t*>(hp);
-        switch (pg.NT) {
-            case 1: launch_mlp_bf16<2, 1>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma, k, pg, pd, stream); break;
-            case 2: launch_mlp_bf16<2, 2>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma, k, pg, pd, stream); break;
-            default: launch_mlp_bf16<2, 4>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma, k, pg, pd, stream); break;
-        }
+        // both products of one call share the row blocking (same rows)
+        if (pg.NT == 1)
+            launch_mlp_bf16<2, 1, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I,
+                                                                       Rs, gamma, k, pg, pd, mlp_partial, counters,
+                                                                       stream);
+        else if (pg.NT == 2)
+            launch_mlp_bf16<2, 2, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I,
+                                                                       Rs, gamma, k, pg, pd, mlp_partial, counters,
+                                                                       stream);
+        else if (pg.wnt)
+            launch_mlp_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma,
+                                                            k, pg, pd, mlp_partial, counters, stream);
+        else
+            launch_mlp_bf16<1, 4, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma,
+                                                          k, pg, pd, mlp_partial, counters, stream);
     } else {
         hipLaunchKernelGGL(rmsnorm_rows_kernel<float>, dim3(nrows), dim3(256), 0, stream,
                            static_cast<const float*>(h), root, topk_idx, static_cast<const float*>(emb),
                            static_cast<const float*>(gain_h), static_cast<const float*>(gain_e), b, gamma, d, V, k,
-                           Rs, eps, static_cast<float*>(ht), static_cast<float*>(et), diag);
+                           Rs, eps, static_cast<float*>(ht), static_cast<float*>(et), diag, counters, 0);
         hipLaunchKernelGGL(gateup_f32_kernel, dim3(cdiv(I, 64), cdiv(rows, 4)), dim3(256), 0, stream,
                            static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
                            static_cast<const float*>(ht), static_cast<const float*>(et), rows, d, I, Rs, gamma, k,
