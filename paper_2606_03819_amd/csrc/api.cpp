@@ -35,9 +35,8 @@ bool common_shapes_ok(int b, int gamma, int d, int V, int k, bool rows_only = fa
     return true;
 }
 
-size_t stage1_bytes(int b, int gamma, int V, bool bf16) {
-    const GemmPlan p = lm_plan(b * gamma, V, bf16);
-    return 256 + align256((size_t)b * gamma * p.nchunks * kPartStride * 4);
+size_t stage1_bytes(int b, int gamma, int d, int V, bool bf16) {
+    return 256 + lm_layout(b * gamma, V, d, bf16).total;
 }
 
 }  // namespace
@@ -61,12 +60,11 @@ tf_status_t treeflash_marginal_topk(const void* h, const void* lm_head, int b, i
         (topk_logprob != nullptr && !aligned4(topk_logprob)) || (lse != nullptr && !aligned4(lse)))
         return TF_ERR_INVALID_ARG;
     const bool bf16 = dt == TF_BF16;
-    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < stage1_bytes(b, gamma, V, bf16))
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < stage1_bytes(b, gamma, d, V, bf16))
         return TF_ERR_WORKSPACE;
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     int* diag = reinterpret_cast<int*>(ws);
-    float* part = reinterpret_cast<float*>(ws + 256);
-    const hipError_t e = launch_lmhead_topk(h, d, lm_head, b * gamma, d, V, k, inv_temperature, bf16, part,
+    const hipError_t e = launch_lmhead_topk(h, d, lm_head, b * gamma, d, V, k, inv_temperature, bf16, ws + 256,
                                             topk_idx, topk_logprob, lse, diag, stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
@@ -146,8 +144,8 @@ tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, 
                                    reinterpret_cast<int*>(ws + lay.counters), diag, stream);
     if (e != hipSuccess) return TF_ERR_HIP;
     const int rows = b * (1 + (gamma - 1) * k);
-    e = launch_lmhead_topk(ws + lay.hp, d, lm_head, rows, d, V, topk2, inv_temperature, bf16,
-                           reinterpret_cast<float*>(ws + lay.part), cond_idx, cond_logprob, cond_lse, diag, stream);
+    e = launch_lmhead_topk(ws + lay.hp, d, lm_head, rows, d, V, topk2, inv_temperature, bf16, ws + lay.lm,
+                           cond_idx, cond_logprob, cond_lse, diag, stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 

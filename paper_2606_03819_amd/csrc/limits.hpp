@@ -7,7 +7,9 @@ namespace tf {
 // [max, sum, bound, count, val[kKeep], idx[kKeep]] (raw, unscaled logits).
 constexpr int kKeep = 4;
 constexpr int kPartStride = 4 + 2 * kKeep;
-// Per-lane running list length inside the LM-head epilogue.
+// Per-thread running list lengths inside the LM-head epilogues (SIMT fp32
+// kernel, MFMA bf16 kernel).
 constexpr int kLane = 4;
+constexpr int kLaneMfma = 2;
 
 }  // namespace tf

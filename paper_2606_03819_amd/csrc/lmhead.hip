@@ -12,24 +12,25 @@ namespace tf {
 
 // ------------------------------------------------------------ bf16 / MFMA
 
-#ifndef TF_LM_MIN_BLOCKS
-#define TF_LM_MIN_BLOCKS 2
-#endif
-
-template <int WM, int NT, int PIPE, bool WNT>
-__global__ __launch_bounds__(256, TF_LM_MIN_BLOCKS) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
-                                                          const uint16_t* __restrict__ w, GemmShape sh,
-                                                          int V, float sl2, float* __restrict__ part,
-                                                          int* __restrict__ diag) {
-    using Tr = GemmTraits<WM, NT>;
-    using E = EpiLmHead<WM, NT>;
+template <int WM, int NT, int NW, int PIPE, bool WNT>
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
+                                                                 const uint16_t* __restrict__ w, GemmShape sh,
+                                                                 int V, float sl2, float* __restrict__ part,
+                                                                 float* __restrict__ fix, int* __restrict__ counters,
+                                                                 int* __restrict__ diag) {
+    using Tr = GemmTraits<WM, NT, NW>;
+    using E = EpiLmHead<WM, NT, NW>;
     constexpr int SMEM = Tr::SMEM_BYTES > E::MERGE_BYTES ? Tr::SMEM_BYTES : E::MERGE_BYTES;
     __shared__ __align__(16) unsigned char smem[SMEM];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     WRowsPlain ws{w, V, sh.K};
     XRowsPlain xs{x, ldx};
-    E epi{part, V, sl2};
-    stream_gemm_body<WM, NT, PIPE, WNT>(ws, xs, epi, sh, smem);
+    EpiFixup<WM, NT, NW, E> epi{E{part, V, sl2}, fix, counters};
+    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
+}
+
+__global__ void zero_ints_kernel(int* __restrict__ p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
 // ------------------------------------------------------------ fp32 / SIMT
@@ -142,7 +143,7 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
         c[3 + kLane + e] = __int_as_float(li[e]);
     }
     __syncthreads();
-    lm_merge_contributors(cmrg, 32, row0, split, sh.nchunks, sh.R, sl2, part);
+    lm_merge_contributors<8, kLane>(cmrg, 32, row0, split, sh.nchunks, sh.R, sl2, part);
 }
 
 // ------------------------------------------------------------------ merge
@@ -379,36 +380,44 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 // ------------------------------------------------------------------ launchers
 
 template <int WM, int NT, int PIPE, bool WNT>
-static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, int blocks, int V,
-                           float sl2, float* part, int* diag, hipStream_t st) {
-    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, PIPE, WNT>), dim3(blocks), dim3(256), 0, st, x, ldx, w, sh, V,
-                       sl2, part, diag);
+static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, int V, float sl2,
+                           float* part, float* fix, int* counters, int* diag, hipStream_t st) {
+    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(sh.G), dim3(64 * TF_NW), 0, st, x, ldx,
+                       w, sh, V, sl2, part, fix, counters, diag);
 }
 
 // tile shape and pipeline variants the plans can ask for
 static void dispatch_lm_bf16(const GemmPlan& p, const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
-                             int V, float sl2, float* part, int* diag, hipStream_t st) {
-    const int blocks = p.blocks();
+                             int V, float sl2, float* part, float* fix, int* counters, int* diag, hipStream_t st) {
     if (p.NT == 1)
-        launch_lm_bf16<TF_LM_WM_NT1, 1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+        launch_lm_bf16<2, 1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
     else if (p.NT == 2)
-        launch_lm_bf16<TF_LM_WM_NT2, 2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+        launch_lm_bf16<1, 2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
     else if (p.wnt)
-        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+        launch_lm_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
     else
-        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, blocks, V, sl2, part, diag, st);
+        launch_lm_bf16<1, 4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
 }
 
 hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
-                              float inv_t, bool bf16, float* part, int32_t* out_idx, float* out_lp,
+                              float inv_t, bool bf16, unsigned char* lm_ws, int32_t* out_idx, float* out_lp,
                               float* out_lse, int* diag, hipStream_t stream) {
-    const GemmPlan p = lm_plan(rows, V, bf16);
+    const GemmPlan p = lm_plan(rows, V, d, bf16);
     if (p.nchunks > kMaxSplits) return hipErrorInvalidValue;
-    GemmShape sh{rows, d, p.ntiles, p.nchunks, 1, p.nrb};
+    const LmLayout lay = lm_layout(rows, V, d, bf16);
+    float* part = reinterpret_cast<float*>(lm_ws + lay.part);
+    const GemmShape sh = p.shape(rows, d);
     const float sl2 = inv_t * kLog2e;
     if (bf16) {
+        float* fix = reinterpret_cast<float*>(lm_ws + lay.fix);
+        int* counters = reinterpret_cast<int*>(lm_ws + lay.counters);
+        if (p.pieces) {
+            const int n = (int)p.counter_ints();
+            hipLaunchKernelGGL(zero_ints_kernel, dim3(cdiv(n, 256) < 64 ? cdiv(n, 256) : 64), dim3(256), 0, stream,
+                               counters, n);
+        }
         dispatch_lm_bf16(p, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w), sh, V, sl2, part,
-                         diag, stream);
+                         fix, counters, diag, stream);
     } else {
         hipLaunchKernelGGL(lmhead_f32_kernel, dim3(p.blocks()), dim3(256), 0, stream, static_cast<const float*>(x),
                            ldx, static_cast<const float*>(w), sh, V, sl2, part, diag);

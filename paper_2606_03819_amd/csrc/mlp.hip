@@ -30,7 +30,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
                                                            int* __restrict__ counters, int ncounters) {
     __shared__ float red[4];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
-    if (blockIdx.x == 0)   // split-K arrival counters of the SwiGLU products that follow on this stream
+    if (blockIdx.x == 0)   // arrival counters of the SwiGLU products that follow on this stream
         for (int i = threadIdx.x; i < ncounters; i += 256) counters[i] = 0;
     const int row = blockIdx.x;
     const T* src;
@@ -75,23 +75,23 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
 
 // ------------------------------------------------------------------ bf16
 
-template <int WM, int NT, int PIPE, bool WNT>
-__global__ __launch_bounds__(256, 2) void gateup_bf16_kernel(WRowsGateUp ws, XRowsConcat xs, GemmShape sh,
-                                                             uint16_t* __restrict__ act, int I, float* partial,
-                                                             int* counter) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::SMEM_BYTES];
-    EpiSplitK<WM, NT, EpiSwiGLU<WM, NT>> epi{EpiSwiGLU<WM, NT>{act, I}, partial, counter};
-    stream_gemm_body<WM, NT, PIPE, WNT>(ws, xs, epi, sh, smem);
+template <int WM, int NT, int NW, int PIPE, bool WNT>
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void gateup_bf16_kernel(WRowsGateUp ws, XRowsConcat xs, GemmShape sh,
+                                                                 uint16_t* __restrict__ act, int I, float* partial,
+                                                                 int* counter) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
+    EpiFixup<WM, NT, NW, EpiSwiGLU<WM, NT>> epi{EpiSwiGLU<WM, NT>{act, I}, partial, counter};
+    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
-template <int WM, int NT, int PIPE, bool WNT>
-__global__ __launch_bounds__(256, 2) void down_bf16_kernel(WRowsPlain ws, XRowsPlain xs, GemmShape sh,
-                                                           uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
-                                                           int d, int Rs, int gamma, int M, float* partial,
-                                                           int* counter) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT>::SMEM_BYTES];
-    EpiSplitK<WM, NT, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, Rs, gamma, M}, partial, counter};
-    stream_gemm_body<WM, NT, PIPE, WNT>(ws, xs, epi, sh, smem);
+template <int WM, int NT, int NW, int PIPE, bool WNT>
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void down_bf16_kernel(WRowsPlain ws, XRowsPlain xs, GemmShape sh,
+                                                               uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
+                                                               int d, int Rs, int gamma, int M, float* partial,
+                                                               int* counter) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
+    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, Rs, gamma, M}, partial, counter};
+    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
 // ------------------------------------------------------------------ fp32
@@ -145,14 +145,14 @@ static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_
                             int* counters, hipStream_t st) {
     WRowsGateUp wgu{wg, wu, I, 2 * d};
     XRowsConcat xc{ht, et, d, Rs, gamma, M};
-    GemmShape shg{rows, 2 * d, pg.ntiles, pg.nchunks, pg.nkp, pg.nrb};
-    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, PIPE, WNT>), dim3(pg.blocks()), dim3(256), 0, st, wgu, xc, shg, act, I,
-                       partial, counters);
+    const GemmShape shg = pg.shape(rows, 2 * d);
+    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(shg.G), dim3(64 * TF_NW), 0, st, wgu, xc,
+                       shg, act, I, partial, counters);
     WRowsPlain wdn{wd, d, I};
     XRowsPlain xa{act, (long)I};
-    GemmShape shd{rows, I, pd.ntiles, pd.nchunks, pd.nkp, pd.nrb};
-    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, PIPE, WNT>), dim3(pd.blocks()), dim3(256), 0, st, wdn, xa, shd, hp, h, d, Rs,
-                       gamma, M, partial, counters + pg.nchunks * pg.nrb);
+    const GemmShape shd = pd.shape(rows, I);
+    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(shd.G), dim3(64 * TF_NW), 0, st, wdn, xa,
+                       shd, hp, h, d, Rs, gamma, M, partial, counters + pg.counter_ints());
 }
 
 hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
@@ -166,7 +166,7 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
     if (bf16) {
         const GemmPlan pg = mlp_plan(rows, cdiv(I, 16), 2 * d);
         const GemmPlan pd = mlp_plan(rows, cdiv(d, 32), I);
-        const int ncounters = pg.nchunks * pg.nrb + pd.nchunks * pd.nrb;
+        const int ncounters = (int)(pg.counter_ints() + pd.counter_ints());
         hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
                            static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),
                            static_cast<const uint16_t*>(gain_h), static_cast<const uint16_t*>(gain_e), b, gamma, d,
@@ -186,7 +186,7 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
                                                                        Rs, gamma, k, pg, pd, mlp_partial, counters,
                                                                        stream);
         else if (pg.NT == 2)
-            launch_mlp_bf16<2, 2, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I,
+            launch_mlp_bf16<1, 2, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I,
                                                                        Rs, gamma, k, pg, pd, mlp_partial, counters,
                                                                        stream);
         else if (pg.wnt)

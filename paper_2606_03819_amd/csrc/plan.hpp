@@ -7,31 +7,31 @@
 #include <stdint.h>
 
 #include "limits.hpp"
+#include "work.hpp"
 
 namespace tf {
 
 constexpr int kMaxSplits = 2048;       // vocabulary slices (partials per row); kMaxSplits*kKeep <= merge capacity
-constexpr int kTargetWorkgroups = 512; // two 256-thread workgroups per CU on 256 CUs
 constexpr int kMaxTopk = 1024;         // longest top-k list the merge kernel sorts
 constexpr int kMaxBudget = 4095;       // tree nodes per sequence
-constexpr int kMaxSplitK = 8;          // k-parts of a SwiGLU product
+constexpr int kNumCUs = 256;           // compute units of an MI355X
 
-inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
-
-struct GemmPlan {
-    int NT;       // 32-row activation tiles per workgroup
-    int WM;       // 32-row weight tiles per wave (bf16)
-    int chunk;    // weight tiles per workgroup
-    int nrb;      // activation-row blocks
-    int ntiles;   // 32-row weight tiles
-    int nchunks;  // workgroup chunks of weight tiles (= vocabulary slices for the LM head)
-    int nkp;      // k-parts
-    bool wnt;     // non-temporal weight loads (weights read by one row block only)
-    int blocks() const { return nchunks * nkp * nrb; }
-};
-
+// Waves per workgroup of the bf16 streaming products; one such workgroup
+// fills a CU's register file at two waves per SIMD.
+#ifndef TF_NW
+#define TF_NW 8
+#endif
+// Workgroups of the LM head when a single row block is cut evenly.
+#ifndef TF_LM_WORKGROUPS
+#define TF_LM_WORKGROUPS 256
+#endif
+// Workgroups of the SwiGLU products when a single row block leaves the
+// weight tiles too few to occupy every CU (their k-range is then cut).
+#ifndef TF_MLP_WORKGROUPS
+#define TF_MLP_WORKGROUPS 256
+#endif
 // Pipeline depth (k-chunks of loads in flight per wave) when a single row
-// block reads each weight once at NT = 4, and otherwise; the launchers pick
+// block streams the weights once at NT = 4, and otherwise; the launchers pick
 // the kernel instance from NT and wnt.
 #ifndef TF_PIPE_SINGLE_NT4
 #define TF_PIPE_SINGLE_NT4 3
@@ -43,84 +43,127 @@ struct GemmPlan {
 #define TF_MLP_WNT 0
 #endif
 
+inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+struct GemmPlan {
+    int NT;       // 32-row activation tiles per workgroup
+    int WM;       // 32-row weight tiles per wave (bf16)
+    int NW;       // waves per workgroup
+    int chunk;    // weight tiles per chunk (NW * WM)
+    int nrb;      // activation-row blocks
+    int ntiles;   // 32-row weight tiles
+    int nchunks;  // chunks (= vocabulary slices for the LM head)
+    int nk;       // 64-wide k-chunks
+    int G;        // workgroups
+    bool wnt;     // non-temporal weight loads (weights read by one row block only)
+    bool pieces;  // some item is cut between workgroups
+    int items() const { return nchunks * nrb; }
+    int blocks() const { return G; }
+    GemmShape shape(int R, int K) const { return GemmShape{R, K, ntiles, nchunks, nrb, nk, G}; }
+    // accumulators of one workgroup, in floats
+    size_t part_floats() const { return (size_t)NW * WM * NT * 16 * 64; }
+    // partial sums of cut items: two slots per workgroup
+    size_t fix_floats() const { return pieces ? 2 * (size_t)G * part_floats() : 0; }
+    size_t counter_ints() const { return pieces ? (size_t)items() : 0; }
+};
+
 inline int plan_nt(int rows) { return rows <= 32 ? 1 : (rows <= 64 ? 2 : 4); }
-// one weight tile per wave at NT = 4 keeps two workgroups per CU
-inline int plan_wm(int NT) { return NT == 4 ? 1 : 2; }
+// two weight tiles per wave at NT = 1; one otherwise keeps the accumulators,
+// the load pipeline and the epilogue within 256 registers
+inline int plan_wm(int NT) { return NT == 1 ? 2 : 1; }
 
-// LM-head tile shape (weight tiles per wave) per activation-tile count.
-#ifndef TF_LM_WM_NT1
-#define TF_LM_WM_NT1 2
-#endif
-#ifndef TF_LM_WM_NT2
-#define TF_LM_WM_NT2 2
-#endif
-#ifndef TF_LM_WM_NT4
-#define TF_LM_WM_NT4 1
-#endif
-inline int lm_wm(int NT) { return NT == 1 ? TF_LM_WM_NT1 : (NT == 2 ? TF_LM_WM_NT2 : TF_LM_WM_NT4); }
-
-// LM head: one chunk of the vocabulary per workgroup, so every workgroup
-// streams the same bytes.  fp32: 32 rows and 8 tiles (256 tokens) per workgroup.
-inline GemmPlan lm_plan(int rows, int V, bool bf16) {
-    GemmPlan p;
-    p.NT = bf16 ? plan_nt(rows) : 1;
-    p.WM = bf16 ? lm_wm(p.NT) : 2;
-    p.chunk = 4 * p.WM;
-    p.nrb = cdiv(rows, 32 * p.NT);
-    p.ntiles = cdiv(V, 32);
-    p.nchunks = cdiv(p.ntiles, p.chunk);
-    p.nkp = 1;
-    p.wnt = p.nrb == 1;
-    return p;
-}
-
-// SwiGLU products (bf16): few weight tiles, so the reduction is split over
-// up to kMaxSplitK workgroups until about kTargetWorkgroups are in flight.
-inline GemmPlan mlp_plan(int rows, int ntiles, int K) {
+// bf16 product of `rows` activation rows with `ntiles` weight tiles over K.
+// One row block: the units are cut evenly over `wg_single` workgroups.
+// Several row blocks: one item per workgroup, the row blocks of a chunk on
+// consecutive workgroups so that they share the chunk through L2.
+inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
     GemmPlan p;
     p.NT = plan_nt(rows);
     p.WM = plan_wm(p.NT);
-    p.chunk = 4 * p.WM;
+    p.NW = TF_NW;
+    p.chunk = p.NW * p.WM;
     p.nrb = cdiv(rows, 32 * p.NT);
     p.ntiles = ntiles;
     p.nchunks = cdiv(ntiles, p.chunk);
-    int nkp = kTargetWorkgroups / (p.nchunks * p.nrb);
-    const int nkc = cdiv(K, 64);
-    if (nkp > kMaxSplitK) nkp = kMaxSplitK;
-    if (nkp > nkc) nkp = nkc;
-    if (nkp < 1) nkp = 1;
-    p.nkp = nkp;
+    p.nk = cdiv(K, 64);
+    if (p.nrb == 1) {
+        const long long units = (long long)p.nchunks * p.nk;
+        p.G = (int)(units < wg_single ? units : wg_single);
+    } else {
+        p.G = p.items();
+    }
+    p.wnt = p.nrb == 1;
+    p.pieces = gemm_has_pieces(p.shape(rows, K));
+    return p;
+}
+
+// LM head over [rows, d] x [V, d].  bf16: the vocabulary slices are the
+// chunks.  fp32 (small workloads, SIMT kernel): 32 rows and 8 tiles (256
+// tokens) per workgroup, never cut.
+inline GemmPlan lm_plan(int rows, int V, int d, bool bf16) {
+    if (bf16) return gemm_plan(rows, cdiv(V, 32), d, TF_LM_WORKGROUPS);
+    GemmPlan p;
+    p.NT = 1;
+    p.WM = 2;
+    p.NW = 4;
+    p.chunk = 8;
+    p.nrb = cdiv(rows, 32);
+    p.ntiles = cdiv(V, 32);
+    p.nchunks = cdiv(p.ntiles, p.chunk);
+    p.nk = cdiv(d, 64);
+    p.G = p.items();
+    p.wnt = false;
+    p.pieces = false;
+    return p;
+}
+
+// SwiGLU products (bf16).
+inline GemmPlan mlp_plan(int rows, int ntiles, int K) {
+    GemmPlan p = gemm_plan(rows, ntiles, K, TF_MLP_WORKGROUPS);
     p.wnt = TF_MLP_WNT && p.nrb == 1;
     return p;
 }
 
-inline size_t mlp_partial_floats(const GemmPlan& p) {
-    if (p.nkp == 1) return 0;
-    return (size_t)p.nchunks * p.nrb * p.nkp * (4 * p.WM * p.NT * 16 * 64);
-}
-
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// LM-head scratch: [(row, slice) partials | partial sums of cut items |
+// arrival counters of the items].
+struct LmLayout {
+    size_t part, fix, counters, total;
+};
+inline LmLayout lm_layout(int rows, int V, int d, bool bf16) {
+    const GemmPlan p = lm_plan(rows, V, d, bf16);
+    LmLayout l;
+    size_t off = 0;
+    l.part = off;
+    off += align256((size_t)rows * p.nchunks * kPartStride * 4);
+    l.fix = off;
+    off += align256(p.fix_floats() * 4);
+    l.counters = off;
+    off += align256(p.counter_ints() * 4);
+    l.total = off;
+    return l;
+}
+
 struct Workspace {
-    size_t diag, part, ht, et, act, hp, mlp_part, counters, total;
+    size_t diag, lm, ht, et, act, hp, mlp_part, counters, total;
     int ncounters;
 };
 
-// Layout: [diag counters | LM-head partials | normalised h | normalised
-// embeddings | SwiGLU activation | h' | split-K partials | split-K counters].
-// Stage 1 uses the first two only.
+// Layout: [diag counters | LM-head scratch (stage 1 or stage 2) | normalised
+// h | normalised embeddings | SwiGLU activation | h' | SwiGLU partial sums |
+// SwiGLU arrival counters].  Stage 1 uses the first two only.
 inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, bool bf16) {
     const int R = 1 + (gamma - 1) * k;
     const size_t es = bf16 ? 2 : 4;
     const int rows1 = b * gamma, rows2 = b * R;
-    const GemmPlan p1 = lm_plan(rows1, V, bf16), p2 = lm_plan(rows2, V, bf16);
-    const size_t part1 = (size_t)rows1 * p1.nchunks, part2 = (size_t)rows2 * p2.nchunks;
+    const size_t lm1 = lm_layout(rows1, V, d, bf16).total, lm2 = lm_layout(rows2, V, d, bf16).total;
     Workspace w;
     size_t off = 0;
     w.diag = off;
     off += 256;
-    w.part = off;
-    off += align256((part1 > part2 ? part1 : part2) * kPartStride * 4);
+    w.lm = off;
+    off += lm1 > lm2 ? lm1 : lm2;
     w.ht = off;
     off += align256((size_t)rows1 * d * es);
     w.et = off;
@@ -133,9 +176,9 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     w.ncounters = 0;
     if (bf16) {
         const GemmPlan pg = mlp_plan(rows2, cdiv(I, 16), 2 * d), pd = mlp_plan(rows2, cdiv(d, 32), I);
-        const size_t a = mlp_partial_floats(pg), c = mlp_partial_floats(pd);
+        const size_t a = pg.fix_floats(), c = pd.fix_floats();
         mp = a > c ? a : c;
-        w.ncounters = pg.nchunks * pg.nrb + pd.nchunks * pd.nrb;
+        w.ncounters = (int)(pg.counter_ints() + pd.counter_ints());
     }
     w.mlp_part = off;
     off += align256(mp * 4);

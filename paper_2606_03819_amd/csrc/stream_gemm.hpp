@@ -9,12 +9,13 @@
 // reductions over the vocabulary (max, sum-exp, running top-k) stay inside a
 // lane.
 //
-// Work decomposition: a workgroup (4 waves) owns one chunk of 4*WM weight
-// tiles (WM per wave), one block of 32*NT activation rows and one k-range
-// (split-K for the short SwiGLU matrices; the LM head never splits K).  Every
-// workgroup therefore streams the same amount of weights.  Per 64-wide
+// Work decomposition (see work.hpp): a workgroup of NW waves streams chunks
+// of NW*WM weight tiles (WM per wave) against blocks of 32*NT activation rows,
+// one k-range at a time; the units of a single row block are cut evenly over
+// the workgroups, so every workgroup streams the same bytes.  Per 64-wide
 // k-chunk the activation tile [32*NT x 64] is staged in LDS (double buffered,
-// rows padded to 144 B so the 16-byte fragment reads are bank-conflict free).
+// rows padded to 144 B so the 16-byte fragment reads are bank-conflict free)
+// and shared by all NW*WM weight tiles of the workgroup.
 // Each wave streams its own weight rows with fully coalesced loads -- one
 // instruction covers 8 rows x 128 B, i.e. whole cache lines -- several
 // k-chunks ahead of the MFMAs, and transposes them into fragment order through a
@@ -25,64 +26,65 @@
 #pragma once
 
 #include "common.hpp"
+#include "work.hpp"
 
 namespace tf {
 
-struct GemmShape {
-    int R;        // activation rows
-    int K;        // reduction length (multiple of 16)
-    int ntiles;   // 32-row weight tiles
-    int nchunks;  // workgroup chunks along the weight tiles
-    int nkp;      // k-parts (split-K); each a whole number of 64-wide k-chunks
-    int nrb;      // activation-row blocks
-};
-
-struct WorkItem {
-    int chunk, kp, rb;
+// One contiguous k-range of one item, computed by one workgroup.
+struct Segment {
+    int g;         // workgroup (logical id)
+    int item, chunk, rb;
     int t0, t1;    // weight tiles [t0, t1)
     int kc0, kc1;  // 64-wide k-chunks [kc0, kc1)
     int row0;      // first activation row
+    int gfirst;    // first workgroup holding a piece of the item
+    int npieces;   // workgroups holding a piece of the item
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs of an MI355X.
 // Renumber them so consecutive logical ids share an XCD (and its L2): the
-// row blocks of one weight chunk then read the same weight tiles through the
-// same L2.
+// row blocks of one weight chunk, and the pieces of a cut item, then meet in
+// the same L2.
 __device__ __forceinline__ int xcd_logical_id(int bid, int nblocks) {
     if ((nblocks & 7) != 0) return bid;
     return (bid & 7) * (nblocks >> 3) + (bid >> 3);
 }
 
-template <int WM, int NT>
+template <int WM, int NT, int NW>
 struct GemmTraits {
     static constexpr int TR = 32 * NT;           // activation rows per workgroup
     static constexpr int KC = 64;                // k per LDS stage
     static constexpr int LDSW = KC + 8;          // padded LDS row, bf16 elements
     static constexpr int XS_BYTES = 2 * TR * LDSW * 2;
     static constexpr int WROWS = 32 * WM;        // weight rows per wave
-    static constexpr int WS_BYTES = 4 * WROWS * KC * 2;   // wave-private weight tiles
+    static constexpr int WS_BYTES = NW * WROWS * KC * 2;   // wave-private weight tiles
     static constexpr int SMEM_BYTES = XS_BYTES + WS_BYTES;
     static constexpr int NWL = WROWS / 8;        // coalesced weight loads per wave per k-chunk
-    static constexpr int CHUNK = 4 * WM;         // weight tiles per workgroup
-    static constexpr int PART_FLOATS = 4 * WM * NT * 16 * 64;   // one workgroup's accumulators
+    static constexpr int CHUNK = NW * WM;        // weight tiles per chunk
+    static constexpr int NTHREADS = 64 * NW;
+    static constexpr int XPIECES = TR * 8;       // 16-byte pieces of an activation tile
+    static constexpr int XPT = (XPIECES + NTHREADS - 1) / NTHREADS;
+    static constexpr int PART_FLOATS = NW * WM * NT * 16 * 64;   // one workgroup's accumulators
 };
 
-template <int WM, int NT>
-__device__ __forceinline__ WorkItem work_item(const GemmShape& sh) {
-    using T = GemmTraits<WM, NT>;
-    WorkItem w;
-    const int L = xcd_logical_id(blockIdx.x, gridDim.x);
-    w.rb = L % sh.nrb;
-    const int rest = L / sh.nrb;
-    w.kp = rest % sh.nkp;
-    w.chunk = rest / sh.nkp;
-    w.t0 = w.chunk * T::CHUNK;
-    w.t1 = min(w.t0 + T::CHUNK, sh.ntiles);
-    const int nkc = (sh.K + T::KC - 1) / T::KC;
-    w.kc0 = (int)(((long long)w.kp * nkc) / sh.nkp);
-    w.kc1 = (int)(((long long)(w.kp + 1) * nkc) / sh.nkp);
-    w.row0 = w.rb * T::TR;
-    return w;
+// The segment of workgroup g that starts at unit u (u < end of g's range).
+template <int WM, int NT, int NW>
+__device__ __forceinline__ Segment make_segment(const GemmShape& sh, int g, long long u, long long u_end) {
+    using T = GemmTraits<WM, NT, NW>;
+    Segment s;
+    s.g = g;
+    s.item = (int)(u / sh.nk);
+    s.chunk = s.item / sh.nrb;
+    s.rb = s.item - s.chunk * sh.nrb;
+    const long long ib = (long long)s.item * sh.nk;
+    s.kc0 = (int)(u - ib);
+    s.kc1 = (int)((u_end - ib) < sh.nk ? (u_end - ib) : sh.nk);
+    s.t0 = s.chunk * T::CHUNK;
+    s.t1 = min(s.t0 + T::CHUNK, sh.ntiles);
+    s.row0 = s.rb * T::TR;
+    s.gfirst = unit_owner(sh, ib);
+    s.npieces = unit_owner(sh, ib + sh.nk - 1) - s.gfirst + 1;
+    return s;
 }
 
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
@@ -101,22 +103,22 @@ __device__ __forceinline__ int wswz(int row) { return (row >> 1) & 7; }
 // waited for before the barrier.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// PIPE: k-chunks of loads in flight per wave.  WNT: weight loads carry the
-// non-temporal hint, for weights that one workgroup alone reads (a single
-// activation row block), so they do not evict the activations that every
-// workgroup re-reads from L2.
-template <int WM, int NT, int PIPE, bool WNT, class WSrc, class XSrc, class Epi>
-__device__ __forceinline__ void stream_gemm_body(const WSrc& wsrc, const XSrc& xsrc, Epi& epi,
-                                                 const GemmShape& sh, unsigned char* smem) {
-    using T = GemmTraits<WM, NT>;
-    constexpr int TR = T::TR, KC = T::KC, LDSW = T::LDSW, NWL = T::NWL;
+// Accumulate one segment: acc[mt][nt] = X[rows of nt] . W[tiles of mt] over
+// the segment's k-chunks.  PIPE: k-chunks of loads in flight per wave.  WNT:
+// weight loads carry the non-temporal hint, for weights that one workgroup
+// alone reads (a single activation row block), so they do not evict the
+// activations that every workgroup re-reads from L2.
+template <int WM, int NT, int NW, int PIPE, bool WNT, class WSrc, class XSrc>
+__device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc, const GemmShape& sh,
+                                             const Segment& it, f32x16 (&acc)[WM][NT], unsigned char* smem) {
+    using T = GemmTraits<WM, NT, NW>;
+    constexpr int TR = T::TR, KC = T::KC, LDSW = T::LDSW, NWL = T::NWL, NTH = T::NTHREADS, XPT = T::XPT;
     uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     uint16_t* wl = reinterpret_cast<uint16_t*>(smem + T::XS_BYTES) + wave * T::WROWS * KC;
-    const WorkItem it = work_item<WM, NT>(sh);
     const int nk = it.kc1 - it.kc0;
     const int slot = lane & 7;          // 16-byte slot of a 128-byte row segment this lane loads
 
@@ -134,7 +136,6 @@ __device__ __forceinline__ void stream_gemm_body(const WSrc& wsrc, const XSrc& x
         const uint16_t* p = (tile < it.t1) ? wsrc.row(tile, row & 31) : nullptr;
         gw[q] = p != nullptr ? p : wsrc.row(0, 0);
     }
-    f32x16 acc[WM][NT];
 #pragma unroll
     for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
@@ -144,22 +145,28 @@ __device__ __forceinline__ void stream_gemm_body(const WSrc& wsrc, const XSrc& x
 
     // activation rows of this thread's 16-byte pieces (clamped into [0, R))
     const int kmax = sh.K - 8;
-    auto load_x = [&](u32x4 (&xr)[NT], int kc) {
+    // activation pieces p = tid + NTH*i: row p / 8, 16-byte slot p % 8
+    constexpr bool XFULL = T::XPIECES % NTH == 0;
+    auto load_x = [&](u32x4 (&xr)[XPT], int kc) {
 #pragma unroll
-        for (int i = 0; i < NT; ++i) {
-            const int p = tid + 256 * i;
-            const int gr = min(it.row0 + (p >> 3), sh.R - 1);
-            const int k = min(kc * KC + (p & 7) * 8, kmax);
-            xr[i] = *reinterpret_cast<const u32x4*>(xsrc.ptr(gr, k));
+        for (int i = 0; i < XPT; ++i) {
+            const int p = tid + NTH * i;
+            if (XFULL || p < T::XPIECES) {
+                const int gr = min(it.row0 + (p >> 3), sh.R - 1);
+                const int k = min(kc * KC + (p & 7) * 8, kmax);
+                xr[i] = *reinterpret_cast<const u32x4*>(xsrc.ptr(gr, k));
+            }
         }
     };
-    auto store_x = [&](const u32x4 (&xr)[NT], int buf, int kc) {
+    auto store_x = [&](const u32x4 (&xr)[XPT], int buf, int kc) {
 #pragma unroll
-        for (int i = 0; i < NT; ++i) {
-            const int p = tid + 256 * i;
-            const bool ok = it.row0 + (p >> 3) < sh.R && kc * KC + (p & 7) * 8 < sh.K;
-            *reinterpret_cast<u32x4*>(xs + buf * TR * LDSW + (p >> 3) * LDSW + (p & 7) * 8) =
-                ok ? xr[i] : u32x4{0u, 0u, 0u, 0u};
+        for (int i = 0; i < XPT; ++i) {
+            const int p = tid + NTH * i;
+            if (XFULL || p < T::XPIECES) {
+                const bool ok = it.row0 + (p >> 3) < sh.R && kc * KC + (p & 7) * 8 < sh.K;
+                *reinterpret_cast<u32x4*>(xs + buf * TR * LDSW + (p >> 3) * LDSW + (p & 7) * 8) =
+                    ok ? xr[i] : u32x4{0u, 0u, 0u, 0u};
+            }
         }
     };
     auto load_w = [&](u32x4 (&w)[NWL], int kc) {
@@ -187,7 +194,7 @@ __device__ __forceinline__ void stream_gemm_body(const WSrc& wsrc, const XSrc& x
     // loads of the chunk they store (loads return in order), leaving the
     // later chunks in flight.
     static_assert(PIPE >= 2 && PIPE <= 4, "pipeline depth");
-    u32x4 xr[PIPE][NT];
+    u32x4 xr[PIPE][XPT];
     u32x4 wr[PIPE][NWL];
     // MFMAs of k-chunk i from LDS (activation buffer i & 1, the wave's weight tile)
     auto compute = [&](int i) {
@@ -257,8 +264,25 @@ __device__ __forceinline__ void stream_gemm_body(const WSrc& wsrc, const XSrc& x
             }
         }
     }
-    __syncthreads();  // LDS tiles no longer needed: the epilogue may reuse them
-    epi.apply(acc, it, wave, lane, smem, sh);
+}
+
+// Every segment of this workgroup: accumulate, then hand the accumulators to
+// the epilogue (which may reuse the LDS tiles).
+template <int WM, int NT, int NW, int PIPE, bool WNT, class WSrc, class XSrc, class Epi>
+__device__ __forceinline__ void stream_gemm(const WSrc& wsrc, const XSrc& xsrc, Epi& epi, const GemmShape& sh,
+                                            unsigned char* smem) {
+    const int g = xcd_logical_id(blockIdx.x, gridDim.x);
+    const long long u_end = unit_start(sh, g + 1);
+    long long u = unit_start(sh, g);
+    while (u < u_end) {
+        const Segment seg = make_segment<WM, NT, NW>(sh, g, u, u_end);
+        f32x16 acc[WM][NT];
+        gemm_segment<WM, NT, NW, PIPE, WNT>(wsrc, xsrc, sh, seg, acc, smem);
+        __syncthreads();  // LDS tiles no longer needed
+        epi.apply(acc, seg, smem, sh);
+        u = (long long)(seg.item + 1) * sh.nk;
+        if (u < u_end) __syncthreads();  // the epilogue's LDS use ends before the next tiles land
+    }
 }
 
 // ----------------------------------------------------------- weight sources
@@ -311,42 +335,44 @@ struct XRowsConcat {
 
 // ------------------------------------------------------------------ epilogues
 
-// Merge the 8 contributor lists of each activation row (written to `cm` as
-// [rows][8][3 + 2*kLane] = max, sum, bound, values, ids) into the row's
+// Merge the NC contributor lists of each activation row (written to `cm` as
+// [rows][NC][3 + 2*KL] = max, sum, bound, KL values, KL ids; `bound` is at
+// least every value the contributor saw but did not list) into the row's
 // (row, slice) partial.  One thread per row.
+template <int NC, int KL>
 __device__ inline void lm_merge_contributors(const float* cm, int rows, int row0, int split, int nsplit, int R,
                                              float sl2, float* part) {
-    constexpr int W = 3 + 2 * kLane;
+    constexpr int W = 3 + 2 * KL;
     const int tid = threadIdx.x;
     if (tid >= rows) return;
     const int grow = row0 + tid;
     if (grow >= R) return;
-    const float* c = cm + tid * 8 * W;
+    const float* c = cm + tid * NC * W;
     float M = neg_inf(), U = neg_inf();
 #pragma unroll
-    for (int p = 0; p < 8; ++p) {
+    for (int p = 0; p < NC; ++p) {
         M = fmaxf(M, c[p * W + 0]);
         U = fmaxf(U, c[p * W + 2]);
     }
     float S = 0.f;
 #pragma unroll
-    for (int p = 0; p < 8; ++p) {
+    for (int p = 0; p < NC; ++p) {
         const float mp = c[p * W + 0];
         S += (mp == neg_inf()) ? 0.f : c[p * W + 1] * exp2f((mp - M) * sl2);
     }
     float* out = part + ((size_t)grow * nsplit + split) * kPartStride;
-    int ptr[8];
+    int ptr[NC];
 #pragma unroll
-    for (int p = 0; p < 8; ++p) ptr[p] = 0;
+    for (int p = 0; p < NC; ++p) ptr[p] = 0;
     int cnt = 0;
     for (int e = 0; e <= kKeep; ++e) {
         float bv = neg_inf();
         int bi = -1, bp = -1;
 #pragma unroll
-        for (int p = 0; p < 8; ++p) {
-            if (ptr[p] < kLane) {
+        for (int p = 0; p < NC; ++p) {
+            if (ptr[p] < KL) {
                 const float v = c[p * W + 3 + ptr[p]];
-                const int i = __float_as_int(c[p * W + 3 + kLane + ptr[p]]);
+                const int i = __float_as_int(c[p * W + 3 + KL + ptr[p]]);
                 if (i >= 0 && (bp < 0 || better(v, i, bv, bi))) {
                     bv = v;
                     bi = i;
@@ -360,7 +386,7 @@ __device__ inline void lm_merge_contributors(const float* cm, int rows, int row0
             break;
         }
 #pragma unroll
-        for (int p = 0; p < 8; ++p) ptr[p] += (p == bp) ? 1 : 0;
+        for (int p = 0; p < NC; ++p) ptr[p] += (p == bp) ? 1 : 0;
         out[4 + e] = bv;
         out[4 + kKeep + e] = __int_as_float(bi);
         ++cnt;
@@ -375,157 +401,185 @@ __device__ inline void lm_merge_contributors(const float* cm, int rows, int row0
     out[3] = __int_as_float(cnt);
 }
 
-// LM head: online log-sum-exp and a top-kLane list per lane and row, merged
-// per workgroup into a (row, slice) partial of kKeep entries; the slice is the
-// workgroup's chunk of the vocabulary.
+// LM head: per lane and row, the maximum, the sum of exponentials, the two
+// best logits with their token ids and a bound on the rest (the largest logit
+// the lane drops); merged per workgroup into a (row, slice) partial of kKeep
+// entries, the slice being the workgroup's chunk of the vocabulary.
 //
 // The partial's `bound` is an upper bound on every logit of the slice that is
-// not in its list: a lane drops only values no larger than its kLane-th entry,
-// and the workgroup merge drops only values no larger than the (kKeep+1)-th
-// entry of the union.  The merge kernel uses it to prove the global top-k
-// exact, or to re-evaluate the slice when it cannot.
-template <int WM, int NT>
+// not in its list: a lane drops only values no larger than its bound, and the
+// workgroup merge drops only values no larger than the (kKeep+1)-th entry of
+// the union.  The merge kernel uses it to prove the global top-k exact, or to
+// re-evaluate the slice when it cannot.  Two entries per lane keep this pass
+// cheap (it runs on the vector ALUs after every item); a slice is re-evaluated
+// only if one lane holds three of the row's best k logits.
+template <int WM, int NT, int NW>
 struct EpiLmHead {
     float* part;     // [R, nchunks, kPartStride]
     int V;
     float sl2;       // inv_temperature * log2(e)
-    static constexpr int MERGE_WORDS = 3 + 2 * kLane;
-    static constexpr int MERGE_BYTES = 32 * NT * 8 * MERGE_WORDS * 4;
+    static constexpr int KL = kLaneMfma;
+    static constexpr int NC = 2 * NW;             // contributor lists per row
+    static constexpr int MERGE_WORDS = 3 + 2 * KL;
+    static constexpr int MERGE_BYTES = 32 * NT * NC * MERGE_WORDS * 4;
 
-    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const WorkItem& it, int wave, int lane,
-                                          unsigned char* smem, const GemmShape& sh) {
-        float* cm = reinterpret_cast<float*>(smem);   // [32*NT rows][8 contributors][MERGE_WORDS]
-        const int q = wave * 2 + (lane >> 5);
-        int vbase[WM];
-        bool tv[WM];
-#pragma unroll
-        for (int mt = 0; mt < WM; ++mt) {
-            const int tile = it.t0 + wave * WM + mt;
-            tv[mt] = tile < it.t1;
-            vbase[mt] = tile * 32 + 4 * (lane >> 5);
-        }
-        int seen = 0;
+    // One row (accumulator column nt) of this lane; tokens past the
+    // vocabulary count as -inf.
+    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NT], int nt, const int (&vbase)[WM],
+                                             float* c) const {
+        float x[WM][16];
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-            for (int j = 0; j < 16; ++j) seen += (tv[mt] && vbase[mt] + 8 * (j >> 2) + (j & 3) < V) ? 1 : 0;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            float m = neg_inf();
-#pragma unroll
-            for (int mt = 0; mt < WM; ++mt)
-#pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const bool ok = tv[mt] && vbase[mt] + 8 * (j >> 2) + (j & 3) < V;
-                    m = ok ? fmaxf(m, acc[mt][nt][j]) : m;
-                }
-            float s = 0.f;
-            float lv[kLane];
-            int li[kLane];
-#pragma unroll
-            for (int e = 0; e < kLane; ++e) {
-                lv[e] = neg_inf();
-                li[e] = -1;
+            for (int j = 0; j < 16; ++j) {
+                const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
+                x[mt][j] = v < V ? acc[mt][nt][j] : neg_inf();
             }
-            // running top-kLane, visited in increasing token id so that equal
-            // values keep the smaller id first
+        float m = neg_inf();
 #pragma unroll
-            for (int mt = 0; mt < WM; ++mt)
+        for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
-                    const bool ok = tv[mt] && v < V;
-                    float cv = acc[mt][nt][j];
-                    s += ok ? exp2f((cv - m) * sl2) : 0.f;
-                    if (ok && cv > lv[kLane - 1]) {
-                        int ci = v;
+            for (int j = 0; j < 16; ++j) m = fmaxf(m, x[mt][j]);
+        const float ms = m * sl2;
+        float s = 0.f;
+        float l0 = neg_inf(), l1 = neg_inf(), rest = neg_inf();
+        int i0 = -1, i1 = -1;
+        // visited in increasing token id, so a tie keeps the smaller id first
 #pragma unroll
-                        for (int e = 0; e < kLane; ++e) {
-                            const bool sw = cv > lv[e];
-                            const float tvv = sw ? lv[e] : cv;
-                            const int tii = sw ? li[e] : ci;
-                            lv[e] = sw ? cv : lv[e];
-                            li[e] = sw ? ci : li[e];
-                            cv = tvv;
-                            ci = tii;
-                        }
-                    }
-                }
-            float* c = cm + ((nt * 32 + (lane & 31)) * 8 + q) * MERGE_WORDS;
-            c[0] = m;
-            c[1] = seen > 0 ? s : 0.f;
-            c[2] = seen > kLane ? lv[kLane - 1] : neg_inf();
+        for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-            for (int e = 0; e < kLane; ++e) {
-                c[3 + e] = lv[e];
-                c[3 + kLane + e] = __int_as_float(li[e]);
+            for (int j = 0; j < 16; ++j) {
+                const float xv = x[mt][j];
+                const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
+                s += exp2f(fmaf(xv, sl2, -ms));
+                const bool c0 = xv > l0, c1 = xv > l1;
+                rest = fmaxf(rest, c1 ? l1 : xv);
+                const float nl1 = c0 ? l0 : (c1 ? xv : l1);
+                const int ni1 = c0 ? i0 : (c1 ? v : i1);
+                l0 = c0 ? xv : l0;
+                i0 = c0 ? v : i0;
+                l1 = nl1;
+                i1 = ni1;
             }
-        }
+        c[0] = m;
+        c[1] = m == neg_inf() ? 0.f : s;
+        c[2] = rest;
+        c[3] = l0;
+        c[4] = l1;
+        c[5] = __int_as_float(i0);
+        c[6] = __int_as_float(i1);
+    }
+
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char* smem,
+                                          const GemmShape& sh) {
+        static_assert(KL == 2, "lane lists hold two entries");
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
+        float* cm = reinterpret_cast<float*>(smem);   // [32*NT rows][NC contributors][MERGE_WORDS]
+        const int q = wave * 2 + (lane >> 5);
+        const int tw = it.t0 + wave * WM;            // this wave's first tile
+        int vbase[WM];
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt) vbase[mt] = (tw + mt < it.t1 ? tw + mt : 0x3fffffff / 32) * 32 + 4 * (lane >> 5);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            lane_row(acc, nt, vbase, cm + ((nt * 32 + (lane & 31)) * NC + q) * MERGE_WORDS);
         __syncthreads();
-        lm_merge_contributors(cm, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
+        lm_merge_contributors<NC, KL>(cm, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
 };
 
-// Split-K: each workgroup stores its accumulators, and the last of the nkp
-// workgroups of a (chunk, row block) sums them in k-part order (so the result
-// does not depend on arrival order) and runs the real epilogue.  The counters
-// are zeroed before the first product of every call and reset by their last
-// user.
-template <int WM, int NT, class Inner>
-struct EpiSplitK {
-    Inner inner;
-    float* partial;   // [nchunks * nrb][nkp][PART_FLOATS]
-    int* counter;     // [nchunks * nrb]
+// Cut items: every workgroup holding a piece stores its accumulators, and
+// the last one to arrive sums the pieces in workgroup order (so the result
+// does not depend on arrival order) and runs the real epilogue.  The arrival
+// counters are zeroed before the product starts.
+//
+// The pieces may sit on different XCDs, whose L2 caches are not coherent
+// with each other.  A device-scope fence would write back and invalidate the
+// whole L2 of the XCD (stalling every workgroup there), so only this
+// traffic is made device-coherent: the partial sums are written and read with
+// device-scope relaxed atomics (write-through stores and loads that do not
+// hit stale lines), the writer waits for its stores to complete before it
+// bumps the counter, and the reader loads only after seeing the count.
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// every memory operation of this thread issued so far has completed
+__device__ __forceinline__ void wait_memory() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
-    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const WorkItem& it, int wave, int lane,
-                                          unsigned char* smem, const GemmShape& sh) {
-        if (sh.nkp == 1) {
-            inner.apply(acc, it, wave, lane, sh);
-            return;
-        }
-        constexpr int PF = GemmTraits<WM, NT>::PART_FLOATS;
-        const int slotid = it.chunk * sh.nrb + it.rb;
-        float* base = partial + (size_t)slotid * sh.nkp * PF;
-        auto idx = [&](int mt, int nt, int j4) {
-            return ((((wave * WM + mt) * NT + nt) * 4 + j4) * 64 + lane) * 4;
-        };
+template <int WM, int NT, int NW, class Inner>
+struct EpiFixup {
+    Inner inner;
+    float* partial;   // [2 * G][PART_FLOATS]
+    int* counter;     // [items]
+
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char* smem,
+                                          const GemmShape& sh) {
+        if (it.npieces > 1 && !combine(acc, it, smem, sh)) return;
+        inner.apply(acc, it, smem, sh);
+    }
+
+    // Store this piece; if it is the last to arrive, replace acc by the sum
+    // of all pieces and return true.
+    __device__ __forceinline__ bool combine(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char* smem,
+                                         const GemmShape& sh) {
+        constexpr int PF = GemmTraits<WM, NT, NW>::PART_FLOATS;
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
+        // register j of accumulator (mt, nt) of all 64 lanes: one 256-byte row
+        auto idx = [&](int mt, int nt, int j) { return (((wave * WM + mt) * NT + nt) * 16 + j) * 64 + lane; };
+        float* mine = partial + (size_t)piece_slot(sh, it.g, it.item) * PF;
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                for (int j4 = 0; j4 < 4; ++j4)
-                    *reinterpret_cast<float4*>(base + (size_t)it.kp * PF + idx(mt, nt, j4)) =
-                        float4{acc[mt][nt][4 * j4], acc[mt][nt][4 * j4 + 1], acc[mt][nt][4 * j4 + 2],
-                               acc[mt][nt][4 * j4 + 3]};
-        __threadfence();
-        __syncthreads();
+                for (int j = 0; j < 16; ++j) store_coherent(mine + idx(mt, nt, j), acc[mt][nt][j]);
+        wait_memory();
+        __syncthreads();   // every thread's piece is stored
         int* flag = reinterpret_cast<int*>(smem);
-        if (threadIdx.x == 0) flag[0] = (atomicAdd(counter + slotid, 1) == sh.nkp - 1) ? 1 : 0;
+        if (threadIdx.x == 0)
+            flag[0] = (__hip_atomic_fetch_add(counter + it.item, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                       it.npieces - 1)
+                          ? 1
+                          : 0;
         __syncthreads();
-        if (flag[0] == 0) return;
-        __threadfence();
+        const bool last = flag[0] != 0;
+        __syncthreads();   // flag read by all before the epilogue reuses the LDS
+        if (!last) return false;
+        // pieces in workgroup order (this workgroup's own one re-read from
+        // memory, so every sum is the same chain of additions); the loads of
+        // one piece are independent, so each piece costs one round trip
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                for (int j4 = 0; j4 < 4; ++j4) {
-                    float4 sum = float4{0.f, 0.f, 0.f, 0.f};
-                    for (int p = 0; p < sh.nkp; ++p) {
-                        const float4 v = *reinterpret_cast<const float4*>(base + (size_t)p * PF + idx(mt, nt, j4));
-                        sum.x += v.x;
-                        sum.y += v.y;
-                        sum.z += v.z;
-                        sum.w += v.w;
-                    }
-                    acc[mt][nt][4 * j4] = sum.x;
-                    acc[mt][nt][4 * j4 + 1] = sum.y;
-                    acc[mt][nt][4 * j4 + 2] = sum.z;
-                    acc[mt][nt][4 * j4 + 3] = sum.w;
-                }
-        if (threadIdx.x == 0) counter[slotid] = 0;
-        inner.apply(acc, it, wave, lane, sh);
+                for (int j = 0; j < 16; ++j) acc[mt][nt][j] = 0.f;
+        for (int pc = 0; pc < it.npieces; ++pc) {
+            const float* src = partial + (size_t)piece_slot(sh, it.gfirst + pc, it.item) * PF;
+            f32x16 v[WM][NT];
+#pragma unroll
+            for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) v[mt][nt][j] = load_coherent(src + idx(mt, nt, j));
+#pragma unroll
+            for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) acc[mt][nt][j] += v[mt][nt][j];
+        }
+        return true;
     }
 };
 
@@ -534,8 +588,10 @@ template <int WM, int NT>
 struct EpiSwiGLU {
     uint16_t* out;   // [R, I]
     int I;
-    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const WorkItem& it, int wave, int lane,
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char*,
                                           const GemmShape& sh) {
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt) {
             const int tile = it.t0 + wave * WM + mt;
@@ -577,8 +633,10 @@ struct EpiResidual {
     uint16_t* out;        // [R, d]
     const uint16_t* h;    // [b, gamma, d]
     int d, Rs, gamma, M;
-    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const WorkItem& it, int wave, int lane,
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char*,
                                           const GemmShape& sh) {
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             const int r = it.row0 + nt * 32 + (lane & 31);
