@@ -164,8 +164,8 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
     const int rows = b * Rs;
     const int nrows = b * gamma + rows;
     if (bf16) {
-        const GemmPlan pg = mlp_plan(rows, cdiv(I, 16), 2 * d);
-        const GemmPlan pd = mlp_plan(rows, cdiv(d, 32), I);
+        const GemmPlan pg = gateup_plan(rows, d, I);
+        const GemmPlan pd = down_plan(rows, d, I);
         const int ncounters = (int)(pg.counter_ints() + pd.counter_ints());
         hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
                            static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),

@@ -25,10 +25,15 @@ constexpr int kNumCUs = 256;           // compute units of an MI355X
 #ifndef TF_LM_WORKGROUPS
 #define TF_LM_WORKGROUPS 256
 #endif
-// Workgroups of the SwiGLU products when a single row block leaves the
-// weight tiles too few to occupy every CU (their k-range is then cut).
+// Workgroups of the SwiGLU gate/up and down products when a single row
+// block leaves too few weight tiles to occupy every CU (their k-range is
+// then cut; every cut adds a partial-sum round trip, so the smaller down
+// product uses fewer workgroups).
 #ifndef TF_MLP_WORKGROUPS
 #define TF_MLP_WORKGROUPS 256
+#endif
+#ifndef TF_DOWN_WORKGROUPS
+#define TF_DOWN_WORKGROUPS 128
 #endif
 // Pipeline depth (k-chunks of loads in flight per wave) when a single row
 // block streams the weights once at NT = 4, and otherwise; the launchers pick
@@ -118,11 +123,13 @@ inline GemmPlan lm_plan(int rows, int V, int d, bool bf16) {
 }
 
 // SwiGLU products (bf16).
-inline GemmPlan mlp_plan(int rows, int ntiles, int K) {
-    GemmPlan p = gemm_plan(rows, ntiles, K, TF_MLP_WORKGROUPS);
+inline GemmPlan mlp_plan(int rows, int ntiles, int K, int wg_single) {
+    GemmPlan p = gemm_plan(rows, ntiles, K, wg_single);
     p.wnt = TF_MLP_WNT && p.nrb == 1;
     return p;
 }
+inline GemmPlan gateup_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(I, 16), 2 * d, TF_MLP_WORKGROUPS); }
+inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d, 32), I, TF_DOWN_WORKGROUPS); }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -175,7 +182,7 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     size_t mp = 0;
     w.ncounters = 0;
     if (bf16) {
-        const GemmPlan pg = mlp_plan(rows2, cdiv(I, 16), 2 * d), pd = mlp_plan(rows2, cdiv(d, 32), I);
+        const GemmPlan pg = gateup_plan(rows2, d, I), pd = down_plan(rows2, d, I);
         const size_t a = pg.fix_floats(), c = pd.fix_floats();
         mp = a > c ? a : c;
         w.ncounters = (int)(pg.counter_ints() + pd.counter_ints());
