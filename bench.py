@@ -9,14 +9,24 @@ independent weight copies rotate between steps so that no step finds its
 weights in the 256 MB last-level cache.
 
 Prints ONE JSON line: draft trees/s (value), rows/s, per-stage times, the
-roofline of the dominant kernel (the stage-2 LM head), and the CPU oracle
-timed on a bounded sample on this host.
+roofline of the dominant kernel (the stage-2 LM-head GEMM, timed alone with HIP
+events recorded around its launch), and the CPU oracle timed on a bounded
+sample on this host.
+
+Offline helpers (no GPU): --summarize-trace and --summarize-pmc turn
+rocprofv3 output into the text summaries kept under profiles/; the HBM traffic
+summary is read back into roofline.traffic while the kernel sources are
+unchanged since the counters were taken.
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
+import sqlite3
 import sys
 import time
 
@@ -33,6 +43,45 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector/MFMA
 RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+PROFILES = os.path.join(ROOT, "profiles")
+# sources that define the LM-head GEMM kernel; counters taken on another
+# version of them say nothing about this one
+KERNEL_SOURCES = ["lmhead.hip", "stream_gemm.hpp", "work.hpp", "plan.hpp", "common.hpp", "limits.hpp"]
+COPY_BYTES = 1 << 30      # plain copy used to scale the traffic counters
+
+
+def kernel_source_digest() -> str:
+    hsh = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_03819_amd", "csrc", name), "rb") as f:
+            hsh.update(name.encode() + b"\0" + f.read())
+    return hsh.hexdigest()
+
+
+def lm_kernel_prefix(rows: int) -> str:
+    """Name prefix of the bf16 LM-head kernel instance the plan picks for `rows` rows."""
+    nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
+    wm = 2 if nt == 1 else 1
+    return f"lmhead_bf16_kernel<{wm}, {nt}, "
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(PROFILES, f"lmhead_stage2_{workload}_hbm_traffic.md")
+
+
+def read_traffic(workload: str):
+    """HBM bytes per launch of the stage-2 LM-head kernel from the committed counter summary,
+    or None when there is none or the kernel sources changed since it was taken."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha256") != kernel_source_digest() or rec.get("workload") != workload:
+        return None
+    return rec["traffic_bytes"]
 
 
 def parse():
@@ -44,6 +93,13 @@ def parse():
     ap.add_argument("--copies", type=int, default=4, help="independent weight copies rotated per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=30.0, help="rough cap on the CPU baseline's work")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, copy 1 GiB three times (torch.neg, read 1 GiB + write 1 GiB) "
+                         "for counter calibration")
+    ap.add_argument("--summarize-trace", metavar="DIR", help="print a kernel-trace summary of a rocprofv3 run")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the HBM traffic summary from FETCH_SIZE and WRITE_SIZE rocprofv3 runs")
+    ap.add_argument("--command", default="", help="command line recorded in a summary")
     return ap.parse_args()
 
 
@@ -78,8 +134,88 @@ def cpu_baseline(w, weights, states, budget_s):
             "seconds": dt}
 
 
+def _db(path):
+    dbs = sorted(glob.glob(os.path.join(path, "**", "*.db"), recursive=True))
+    if not dbs:
+        raise SystemExit(f"no rocprofv3 database under {path}")
+    return sqlite3.connect(dbs[0])
+
+
+def summarize_trace(args):
+    """Markdown table of per-kernel durations from a rocprofv3 --kernel-trace run."""
+    cur = _db(args.summarize_trace).cursor()
+    rows = cur.execute("select name, count(*), avg(duration), min(duration), max(duration), sum(duration) "
+                       "from kernels group by name order by sum(duration) desc").fetchall()
+    print(f"# Kernel trace: TreeFlash drafting step, {args.workload}\n")
+    print(f"Command (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
+    print("| kernel | calls | avg us | min us | max us | total ms |\n|---|---|---|---|---|---|")
+    for name, n, avg, mn, mx, tot in rows:
+        short = name.split("(")[0].replace("void ", "")
+        print(f"| `{short}` | {n} | {avg / 1e3:.1f} | {mn / 1e3:.1f} | {mx / 1e3:.1f} | {tot / 1e6:.2f} |")
+
+
+def summarize_pmc(args):
+    """HBM traffic of the stage-2 LM-head kernel, scaled by a plain copy of known size."""
+    w = synth.get_workload(args.workload)
+    prefix = lm_kernel_prefix(w.rows * w.b)
+
+    def per_kernel(path, counter):
+        cur = _db(path).cursor()
+        out = {}
+        for name, v, n in cur.execute("select name, avg(counter_value), count(*) from pmc_events "
+                                      "where counter_name = ? group by name", (counter,)):
+            out[name] = (v, n)
+        return out
+
+    fetch, write = per_kernel(args.summarize_pmc[0], "FETCH_SIZE"), per_kernel(args.summarize_pmc[1], "WRITE_SIZE")
+
+    def pick(d, pred):
+        hits = [(k, v) for k, v in d.items() if pred(k)]
+        if not hits:
+            raise SystemExit("kernel not found in the counter runs")
+        return max(hits, key=lambda kv: kv[1][0])
+
+    lm_f = pick(fetch, lambda k: k.replace("void tf::", "").startswith(prefix))
+    lm_w = pick(write, lambda k: k.replace("void tf::", "").startswith(prefix))
+    cp_f = pick(fetch, lambda k: "neg" in k.lower())
+    cp_w = pick(write, lambda k: "neg" in k.lower())
+    kib = COPY_BYTES / 1024.0
+    f_fac, w_fac = kib / cp_f[1][0], kib / cp_w[1][0]
+    read_b = lm_f[1][0] * 1024.0 * f_fac
+    write_b = lm_w[1][0] * 1024.0 * w_fac
+    es = 2 if w.dtype == "bf16" else 4
+    alg = w.V * w.d * es + w.rows * w.b * w.d * es
+    rec = {"workload": w.name, "kernel": lm_f[0].split("(")[0], "dispatches": lm_f[1][1],
+           "fetch_size_kib": lm_f[1][0], "write_size_kib": lm_w[1][0],
+           "copy_kernel": cp_f[0].split("(")[0][:120], "copy_bytes": COPY_BYTES,
+           "copy_fetch_size_kib": cp_f[1][0], "copy_write_size_kib": cp_w[1][0],
+           "fetch_factor": f_fac, "write_factor": w_fac, "read_bytes": read_b, "write_bytes": write_b,
+           "traffic_bytes": read_b + write_b, "algorithmic_bytes": alg,
+           "traffic_over_algorithmic": (read_b + write_b) / alg, "source_sha256": kernel_source_digest()}
+    print(f"# HBM traffic of the stage-2 LM-head kernel, {w.name}\n")
+    print("Two rocprofv3 counter runs of the same bench command, one counter each; the 1 GiB copy "
+          "(torch.neg over float32) that `--copy-calibration` adds gives the factor that turns each "
+          "counter into bytes. "
+          "`bench.py` reports `traffic_bytes` as `roofline.traffic` while the kernel sources hash to "
+          "`source_sha256`.\n")
+    print(f"Commands (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
+    print(f"- LM-head kernel `{rec['kernel']}`: FETCH_SIZE {rec['fetch_size_kib']:.0f} KiB, "
+          f"WRITE_SIZE {rec['write_size_kib']:.0f} KiB per dispatch ({rec['dispatches']} dispatches)")
+    print(f"- copy of {COPY_BYTES} B: FETCH_SIZE {rec['copy_fetch_size_kib']:.0f} KiB, WRITE_SIZE "
+          f"{rec['copy_write_size_kib']:.0f} KiB -> factors {f_fac:.3f} (read), {w_fac:.3f} (write)")
+    print(f"- traffic {rec['traffic_bytes'] / 1e6:.1f} MB per launch = {rec['traffic_over_algorithmic']:.3f} x the "
+          f"algorithmic {alg / 1e6:.1f} MB (lm_head + activation rows)\n")
+    print("```json\n" + json.dumps(rec, indent=1) + "\n```")
+
+
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
                           "n_gpus": args.gpus}))
@@ -110,7 +246,8 @@ def main():
         if ev is not None:
             ev[2].record()
         binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
-                                        dr.cond_idx, dr.cond_lp, dr.cond_lse)
+                                        dr.cond_idx, dr.cond_lp, dr.cond_lse,
+                                        events=None if ev is None else (ev[5].cuda_event, ev[6].cuda_event))
         if ev is not None:
             ev[3].record()
         binding.treeflash_build_tree(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
@@ -120,7 +257,12 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # events 0..4 bracket the four calls; 5, 6 bracket the stage-2 LM-head GEMM kernel
+    # (recorded inside the library on this stream); recording once creates them
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+    for e in evs:
+        for x in e:
+            x.record()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -134,26 +276,41 @@ def main():
         for j, n in enumerate(names):
             stage_ms[n] += e[j].elapsed_time(e[j + 1])
     stage_us = {n: 1000.0 * v / args.steps for n, v in stage_ms.items()}
+    gemm_us = sorted(1000.0 * e[5].elapsed_time(e[6]) for e in evs)
+    gemm = {"mean": sum(gemm_us) / len(gemm_us), "median": gemm_us[len(gemm_us) // 2],
+            "p10": gemm_us[len(gemm_us) // 10], "p90": gemm_us[(9 * len(gemm_us)) // 10]}
+    if args.copy_calibration:
+        # an elementwise kernel that reads COPY_BYTES and writes COPY_BYTES (torch's
+        # same-dtype copy_ goes to the runtime's blit kernel, shared with other copies)
+        a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        c = torch.empty_like(a)
+        for _ in range(3):
+            torch.neg(a, out=c)
+        torch.cuda.synchronize()
+        del a, c
     ms_per_step = 1000.0 * elapsed / args.steps
     trees_per_s = b * args.steps / elapsed
     rows = b * R
 
-    # dominant kernel: the stage-2 LM head (split-vocabulary GEMM + per-row merge)
+    # dominant kernel: the stage-2 LM-head GEMM (the per-row merge is a separate kernel);
+    # algorithmic bytes per launch: lm_head [V, d] once plus the activation rows h' [rows, d]
     es = 2 if w.dtype == "bf16" else 4
-    t_lm = stage_us["stage2_lmhead_topk"] * 1e-6
-    alg_bytes = V * d * es + rows * d * es + rows * dr.topk2 * 8 + rows * 4
+    t_lm = gemm["mean"] * 1e-6
+    alg_bytes = V * d * es + rows * d * es
     alg_flops = 2.0 * rows * V * d
     if w.dtype == "bf16" and rows > RIDGE:
         roof = {"bound": "mfma", "achieved": alg_flops / t_lm / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-    elif w.dtype == "bf16":
-        roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     else:
         roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
-    roof["kernel"] = "stage-2 LM head: lmhead GEMM + merge_topk, events around treeflash_marginal_topk on h'"
+    roof["traffic"] = read_traffic(w.name)
+    roof["kernel"] = lm_kernel_prefix(rows).rstrip(", ") + " (stage-2 LM head on h')" if w.dtype == "bf16" \
+        else "lmhead_f32_kernel (stage-2 LM head on h')"
+    roof["kernel_us"] = gemm
     roof["alg_bytes_per_launch"] = alg_bytes
     roof["alg_flops_per_launch"] = alg_flops
+    roof["hbm_frac"] = alg_bytes / t_lm / 1e9 / HBM_PEAK_GBS
+    roof["mfma_frac"] = alg_flops / t_lm / 1e12 / BF16_PEAK_TFLOPS
 
     # whole-step roofline context
     mlp_bytes = (2 * w.I * 2 * d + d * w.I) * es

@@ -88,6 +88,21 @@ tf_status_t treeflash_marginal_topk(const void *h, const void *lm_head,
                                     void *workspace, size_t workspace_bytes,
                                     hipStream_t stream);
 
+/* treeflash_marginal_topk with its LM-head product timed: `ev_begin` and
+ * `ev_end` (events created by the caller; either may be NULL) are recorded on
+ * `stream` right before and right after the kernel that streams lm_head, so
+ * the per-row merge kernel that follows lies outside the pair.  For callers
+ * that measure that kernel's bandwidth; arguments, results and errors are
+ * otherwise those of treeflash_marginal_topk (on an invalid argument nothing
+ * is recorded). */
+tf_status_t treeflash_marginal_topk_timed(const void *h, const void *lm_head,
+                                          int b, int gamma, int d, int V, int k,
+                                          float inv_temperature, tf_dtype_t dt,
+                                          int32_t *topk_idx, float *topk_logprob, float *lse,
+                                          void *workspace, size_t workspace_bytes,
+                                          hipStream_t stream, hipEvent_t ev_begin,
+                                          hipEvent_t ev_end);
+
 /* Part 1, stage 2, first half (Method, Eq. 1): the AR-approximated hidden
  * state of every conditional row,
  *   h'_r = h_{depth(r)} + W_down( silu(W_gate x_r) * (W_up x_r) ),

@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(HERE, "libtreeflash.so")
 
 TF_F32, TF_BF16 = 0, 1
 STATUS = {0: "TF_OK", 1: "TF_ERR_INVALID_ARG", 2: "TF_ERR_UNSUPPORTED", 3: "TF_ERR_WORKSPACE", 4: "TF_ERR_HIP"}
-EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_arapprox_hidden",
-            "treeflash_arapprox_expand", "treeflash_build_tree", "treeflash_status_string")
+EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_marginal_topk_timed",
+            "treeflash_arapprox_hidden", "treeflash_arapprox_expand", "treeflash_build_tree",
+            "treeflash_status_string")
 
 _lib = None
 
@@ -44,6 +45,8 @@ def lib() -> ctypes.CDLL:
     L.treeflash_workspace_bytes.restype = S
     L.treeflash_marginal_topk.argtypes = [P, P, I, I, I, I, I, F, I, P, P, P, P, S, P]
     L.treeflash_marginal_topk.restype = I
+    L.treeflash_marginal_topk_timed.argtypes = [P, P, I, I, I, I, I, F, I, P, P, P, P, S, P, P, P]
+    L.treeflash_marginal_topk_timed.restype = I
     L.treeflash_arapprox_hidden.argtypes = [P, P, P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, P, S, P]
     L.treeflash_arapprox_hidden.restype = I
     L.treeflash_arapprox_expand.argtypes = [P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, F, F, I,
@@ -106,8 +109,12 @@ def alloc_workspace(nbytes: int, device) -> torch.Tensor:
 
 def treeflash_marginal_topk(h: torch.Tensor, lm_head: torch.Tensor, k: int, inv_temperature: float = 1.0,
                             workspace: Optional[torch.Tensor] = None, topk_idx: Optional[torch.Tensor] = None,
-                            topk_logprob: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None):
-    """Stage 1: top-k ids and log-probs of LMHead(h) per draft depth (any [b, rows, d])."""
+                            topk_logprob: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                            events: Optional[tuple] = None):
+    """Stage 1: top-k ids and log-probs of LMHead(h) per draft depth (any [b, rows, d]).
+
+    `events`: optional pair of raw hipEvent_t handles recorded around the
+    LM-head kernel (treeflash_marginal_topk_timed)."""
     b, gamma, d = h.shape
     V = lm_head.shape[0]
     dev = h.device
@@ -120,12 +127,14 @@ def treeflash_marginal_topk(h: torch.Tensor, lm_head: torch.Tensor, k: int, inv_
         topk_logprob = torch.empty((b, gamma, k), dtype=torch.float32, device=dev)
     if workspace is None:
         workspace = alloc_workspace(treeflash_workspace_bytes(b, gamma, d, 16, V, k, min(k, V), dt), dev)
-    st = lib().treeflash_marginal_topk(
-        _ptr(h, "h", device=dev), _ptr(lm_head, "lm_head", h.dtype, dev), b, gamma, d, V, k,
-        float(inv_temperature), dt, _ptr(topk_idx, "topk_idx", torch.int32, dev),
-        _ptr(topk_logprob, "topk_logprob", torch.float32, dev), _ptr(lse, "lse", torch.float32, dev),
-        _ptr(workspace, "workspace", device=dev), workspace.numel() * workspace.element_size(), _stream(dev))
-    _check("treeflash_marginal_topk", st)
+    args = (_ptr(h, "h", device=dev), _ptr(lm_head, "lm_head", h.dtype, dev), b, gamma, d, V, k,
+            float(inv_temperature), dt, _ptr(topk_idx, "topk_idx", torch.int32, dev),
+            _ptr(topk_logprob, "topk_logprob", torch.float32, dev), _ptr(lse, "lse", torch.float32, dev),
+            _ptr(workspace, "workspace", device=dev), workspace.numel() * workspace.element_size(), _stream(dev))
+    if events is None:
+        _check("treeflash_marginal_topk", lib().treeflash_marginal_topk(*args))
+    else:
+        _check("treeflash_marginal_topk_timed", lib().treeflash_marginal_topk_timed(*args, events[0], events[1]))
     return topk_idx, topk_logprob
 
 

@@ -36,7 +36,7 @@ bool common_shapes_ok(int b, int gamma, int d, int V, int k, bool rows_only = fa
 }
 
 size_t stage1_bytes(int b, int gamma, int d, int V, bool bf16) {
-    return 256 + lm_layout(b * gamma, V, d, bf16).total;
+    return 256 + lm_scratch_bytes(b * gamma, V, d, bf16);
 }
 
 }  // namespace
@@ -49,10 +49,10 @@ size_t treeflash_workspace_bytes(int b, int gamma, int d, int I, int V, int k, i
     return workspace_layout(b, gamma, d, I, V, k, dt == TF_BF16).total;
 }
 
-tf_status_t treeflash_marginal_topk(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
-                                    float inv_temperature, tf_dtype_t dt, int32_t* topk_idx,
-                                    float* topk_logprob, float* lse, void* workspace, size_t workspace_bytes,
-                                    hipStream_t stream) {
+static tf_status_t marginal_topk(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
+                                 float inv_temperature, tf_dtype_t dt, int32_t* topk_idx, float* topk_logprob,
+                                 float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 hipEvent_t ev_begin, hipEvent_t ev_end) {
     if (h == nullptr || lm_head == nullptr || topk_idx == nullptr) return TF_ERR_INVALID_ARG;
     if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k, true)) return TF_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.f) || !isfinite(inv_temperature)) return TF_ERR_INVALID_ARG;
@@ -65,8 +65,25 @@ tf_status_t treeflash_marginal_topk(const void* h, const void* lm_head, int b, i
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     int* diag = reinterpret_cast<int*>(ws);
     const hipError_t e = launch_lmhead_topk(h, d, lm_head, b * gamma, d, V, k, inv_temperature, bf16, ws + 256,
-                                            topk_idx, topk_logprob, lse, diag, stream);
+                                            topk_idx, topk_logprob, lse, diag, stream, ev_begin, ev_end);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+tf_status_t treeflash_marginal_topk(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
+                                    float inv_temperature, tf_dtype_t dt, int32_t* topk_idx,
+                                    float* topk_logprob, float* lse, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+    return marginal_topk(h, lm_head, b, gamma, d, V, k, inv_temperature, dt, topk_idx, topk_logprob, lse, workspace,
+                         workspace_bytes, stream, nullptr, nullptr);
+}
+
+tf_status_t treeflash_marginal_topk_timed(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
+                                          float inv_temperature, tf_dtype_t dt, int32_t* topk_idx,
+                                          float* topk_logprob, float* lse, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream, hipEvent_t ev_begin,
+                                          hipEvent_t ev_end) {
+    return marginal_topk(h, lm_head, b, gamma, d, V, k, inv_temperature, dt, topk_idx, topk_logprob, lse, workspace,
+                         workspace_bytes, stream, ev_begin, ev_end);
 }
 
 }  // extern "C"

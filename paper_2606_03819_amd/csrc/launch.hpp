@@ -8,10 +8,11 @@ namespace tf {
 
 // LM head over `rows` activation rows [rows, d] (row stride ldx elements),
 // followed by the per-row merge: top-K ids and log-probs, log-sum-exp.
-// `lm_ws` holds lm_layout(rows, V, d, bf16).total bytes.
+// `lm_ws` holds lm_scratch_bytes(rows, V, d, bf16) bytes.
 hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
                               float inv_t, bool bf16, unsigned char* lm_ws, int32_t* out_idx, float* out_lp,
-                              float* out_lse, int* diag, hipStream_t stream);
+                              float* out_lse, int* diag, hipStream_t stream, hipEvent_t ev_begin = nullptr,
+                              hipEvent_t ev_end = nullptr);
 
 // Eq. 1 for every conditional row: RMSNorm of h and of the previous token's
 // embedding, SwiGLU, residual.  Writes h' [b*R, d] into `hp`.

@@ -12,12 +12,14 @@ namespace tf {
 
 // ------------------------------------------------------------ bf16 / MFMA
 
+// One workgroup per (tile range, row block): the range's rounds in turn, each
+// a full pass over K reduced to a (row, slice) partial.
 template <int WM, int NT, int NW, int PIPE, bool WNT>
 __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
-                                                                 const uint16_t* __restrict__ w, GemmShape sh,
-                                                                 int V, float sl2, float* __restrict__ part,
-                                                                 float* __restrict__ fix, int* __restrict__ counters,
-                                                                 int* __restrict__ diag) {
+                                                                               const uint16_t* __restrict__ w,
+                                                                               GemmShape sh, SliceMap map, int V,
+                                                                               float sl2, float* __restrict__ part,
+                                                                               int* __restrict__ diag) {
     using Tr = GemmTraits<WM, NT, NW>;
     using E = EpiLmHead<WM, NT, NW>;
     constexpr int SMEM = Tr::SMEM_BYTES > E::MERGE_BYTES ? Tr::SMEM_BYTES : E::MERGE_BYTES;
@@ -25,12 +27,40 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void lmhead_bf16_kernel(c
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     WRowsPlain ws{w, V, sh.K};
     XRowsPlain xs{x, ldx};
-    EpiFixup<WM, NT, NW, E> epi{E{part, V, sl2}, fix, counters};
-    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
-}
-
-__global__ void zero_ints_kernel(int* __restrict__ p, int n) {
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+    E epi{part, V, sl2};
+    const int L = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int rb = L % sh.nrb;
+    const int g = L / sh.nrb;
+    GemmShape se = sh;   // the epilogue indexes partials by slice
+    se.nchunks = map.G * map.rmax;
+    for (int r = 0; r < map.rmax; ++r) {
+        Segment seg;
+        seg.g = L;
+        seg.item = seg.chunk = g * map.rmax + r;
+        seg.rb = rb;
+        slice_tiles(map, seg.chunk, seg.t0, seg.t1);
+        seg.kc0 = 0;
+        seg.kc1 = sh.nk;
+        seg.row0 = rb * Tr::TR;
+        seg.gfirst = L;
+        seg.npieces = 1;
+        if (seg.t0 == seg.t1) {   // empty slice: a partial the merge skips
+            const int t = threadIdx.x;
+            if (t < Tr::TR && seg.row0 + t < sh.R) {
+                float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * kPartStride;
+                o[0] = neg_inf();
+                o[1] = 0.f;
+                o[2] = neg_inf();
+                o[3] = __int_as_float(0);
+            }
+            continue;
+        }
+        f32x16 acc[WM][NT];
+        gemm_segment<WM, NT, NW, PIPE, WNT>(ws, xs, sh, seg, acc, smem);
+        __syncthreads();  // LDS tiles no longer needed
+        epi.apply(acc, seg, smem, se);
+        __syncthreads();  // the epilogue's LDS use ends before the next round's tiles land
+    }
 }
 
 // ------------------------------------------------------------ fp32 / SIMT
@@ -40,7 +70,7 @@ __global__ void zero_ints_kernel(int* __restrict__ p, int n) {
 // vocabulary row of the current 256-row step, and every (row, 1/8 of the
 // step) pair is one contributor list.
 __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict__ x, long ldx,
-                                                         const float* __restrict__ w, GemmShape sh,
+                                                         const float* __restrict__ w, GemmShape sh, SliceMap map,
                                                          int V, float sl2, float* __restrict__ part,
                                                          int* __restrict__ diag) {
     __shared__ float xs[32][65];
@@ -48,11 +78,11 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     const int tid = threadIdx.x;
     const int L = xcd_logical_id(blockIdx.x, gridDim.x);
-    const int split = L / sh.nrb;
+    const int split = L / sh.nrb;   // one tile range of at most 8 tiles, one slice (rmax = 1)
     const int rb = L - split * sh.nrb;
     const int row0 = rb * 32;
-    const int t0 = split * 8;
-    const int t1 = min(t0 + 8, sh.ntiles);
+    int t0, t1;
+    slice_tiles(map, split, t0, t1);
     const int vend = min(V, t1 * 32);
     const int srow = tid >> 3, sub = tid & 7;
 
@@ -150,7 +180,9 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
 
 struct MergeArgs {
     const float* part;
-    int nsplit, chunk_tiles, ntiles, K, V, d;
+    int nsplit;
+    SliceMap map;
+    int K, V, d;
     float inv_t, sl2;
     int32_t* out_idx;
     float* out_lp;
@@ -315,8 +347,8 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
         const T* wb = reinterpret_cast<const T*>(a.w);
         for (int f = 0; f < nflag; ++f) {
             const int s = s_flag[f];
-            const int t0s = s * a.chunk_tiles;
-            const int t1s = min(t0s + a.chunk_tiles, a.ntiles);
+            int t0s, t1s;
+            slice_tiles(a.map, s, t0s, t1s);
             const int v0 = t0s * 32, v1 = min(a.V, t1s * 32);
             for (int vb = v0; vb < v1; vb += 256) {
                 if (tid == 0) s_ncand = 0;
@@ -380,51 +412,47 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 // ------------------------------------------------------------------ launchers
 
 template <int WM, int NT, int PIPE, bool WNT>
-static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, int V, float sl2,
-                           float* part, float* fix, int* counters, int* diag, hipStream_t st) {
-    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(sh.G), dim3(64 * TF_NW), 0, st, x, ldx,
-                       w, sh, V, sl2, part, fix, counters, diag);
+static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, const SliceMap& map,
+                           int blocks, int V, float sl2, float* part, int* diag, hipStream_t st) {
+    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(blocks), dim3(64 * TF_NW), 0, st, x, ldx,
+                       w, sh, map, V, sl2, part, diag);
 }
 
 // tile shape and pipeline variants the plans can ask for
-static void dispatch_lm_bf16(const GemmPlan& p, const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
-                             int V, float sl2, float* part, float* fix, int* counters, int* diag, hipStream_t st) {
+static void dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
+                             int V, float sl2, float* part, int* diag, hipStream_t st) {
+    const int nb = p.blocks();
     if (p.NT == 1)
-        launch_lm_bf16<2, 1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
+        launch_lm_bf16<2, 1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     else if (p.NT == 2)
-        launch_lm_bf16<1, 2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
+        launch_lm_bf16<1, 2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     else if (p.wnt)
-        launch_lm_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
+        launch_lm_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     else
-        launch_lm_bf16<1, 4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, V, sl2, part, fix, counters, diag, st);
+        launch_lm_bf16<1, 4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
 }
 
 hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
                               float inv_t, bool bf16, unsigned char* lm_ws, int32_t* out_idx, float* out_lp,
-                              float* out_lse, int* diag, hipStream_t stream) {
-    const GemmPlan p = lm_plan(rows, V, d, bf16);
-    if (p.nchunks > kMaxSplits) return hipErrorInvalidValue;
-    const LmLayout lay = lm_layout(rows, V, d, bf16);
-    float* part = reinterpret_cast<float*>(lm_ws + lay.part);
-    const GemmShape sh = p.shape(rows, d);
+                              float* out_lse, int* diag, hipStream_t stream, hipEvent_t ev_begin,
+                              hipEvent_t ev_end) {
+    const LmPlan p = lm_plan(rows, V, d, bf16);
+    if (p.nsplit() > kMaxSplits) return hipErrorInvalidValue;
+    float* part = reinterpret_cast<float*>(lm_ws);
+    // the LM kernels read R, K, ntiles, nrb and nk; G counts workgroups
+    const GemmShape sh{rows, d, p.ntiles, p.map.G, p.nrb, p.nk, p.blocks()};
     const float sl2 = inv_t * kLog2e;
-    if (bf16) {
-        float* fix = reinterpret_cast<float*>(lm_ws + lay.fix);
-        int* counters = reinterpret_cast<int*>(lm_ws + lay.counters);
-        if (p.pieces) {
-            const int n = (int)p.counter_ints();
-            hipLaunchKernelGGL(zero_ints_kernel, dim3(cdiv(n, 256) < 64 ? cdiv(n, 256) : 64), dim3(256), 0, stream,
-                               counters, n);
-        }
+    if (ev_begin != nullptr && hipEventRecord(ev_begin, stream) != hipSuccess) return hipErrorInvalidHandle;
+    if (bf16)
         dispatch_lm_bf16(p, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w), sh, V, sl2, part,
-                         fix, counters, diag, stream);
-    } else {
+                         diag, stream);
+    else
         hipLaunchKernelGGL(lmhead_f32_kernel, dim3(p.blocks()), dim3(256), 0, stream, static_cast<const float*>(x),
-                           ldx, static_cast<const float*>(w), sh, V, sl2, part, diag);
-    }
+                           ldx, static_cast<const float*>(w), sh, p.map, V, sl2, part, diag);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    MergeArgs ma{part, p.nchunks, p.chunk, p.ntiles, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
+    if (ev_end != nullptr && hipEventRecord(ev_end, stream) != hipSuccess) return hipErrorInvalidHandle;
+    MergeArgs ma{part, p.nsplit(), p.map, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
     if (bf16)
         hipLaunchKernelGGL(merge_topk_kernel<uint16_t>, dim3(rows), dim3(256), 0, stream, ma);
     else

@@ -21,7 +21,8 @@ constexpr int kNumCUs = 256;           // compute units of an MI355X
 #ifndef TF_NW
 #define TF_NW 8
 #endif
-// Workgroups of the LM head when a single row block is cut evenly.
+// Tile ranges (workgroups) of the LM head when a single row block streams
+// the whole vocabulary.
 #ifndef TF_LM_WORKGROUPS
 #define TF_LM_WORKGROUPS 256
 #endif
@@ -102,23 +103,43 @@ inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
     return p;
 }
 
-// LM head over [rows, d] x [V, d].  bf16: the vocabulary slices are the
-// chunks.  fp32 (small workloads, SIMT kernel): 32 rows and 8 tiles (256
-// tokens) per workgroup, never cut.
-inline GemmPlan lm_plan(int rows, int V, int d, bool bf16) {
-    if (bf16) return gemm_plan(rows, cdiv(V, 32), d, TF_LM_WORKGROUPS);
-    GemmPlan p;
-    p.NT = 1;
-    p.WM = 2;
-    p.NW = 4;
-    p.chunk = 8;
-    p.nrb = cdiv(rows, 32);
+// LM head over [rows, d] x [V, d]: vocabulary slices (see SliceMap), one
+// workgroup per (tile range, row block).  A single row block spreads the
+// tiles over TF_LM_WORKGROUPS ranges; several row blocks use one chunk per
+// range, the row blocks of a range on consecutive workgroups so that they
+// share its tiles through L2.  fp32 (small workloads, SIMT kernel): 32 rows
+// and at most 8 tiles (256 tokens) per workgroup.
+struct LmPlan {
+    int NT, WM, NW, chunk, nrb, ntiles, nk;
+    SliceMap map;
+    bool wnt;
+    int nsplit() const { return map.G * map.rmax; }
+    int blocks() const { return map.G * nrb; }
+};
+
+inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
+    LmPlan p;
     p.ntiles = cdiv(V, 32);
-    p.nchunks = cdiv(p.ntiles, p.chunk);
     p.nk = cdiv(d, 64);
-    p.G = p.items();
-    p.wnt = false;
-    p.pieces = false;
+    if (bf16) {
+        p.NT = plan_nt(rows);
+        p.WM = plan_wm(p.NT);
+        p.NW = TF_NW;
+        p.chunk = p.NW * p.WM;
+        p.nrb = cdiv(rows, 32 * p.NT);
+        const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)
+                                 : cdiv(p.ntiles, p.chunk);
+        p.map = make_slice_map(p.ntiles, G, p.chunk);
+        p.wnt = p.nrb == 1;
+    } else {
+        p.NT = 1;
+        p.WM = 2;
+        p.NW = 4;
+        p.chunk = 8;
+        p.nrb = cdiv(rows, 32);
+        p.map = make_slice_map(p.ntiles, cdiv(p.ntiles, p.chunk), p.chunk);
+        p.wnt = false;
+    }
     return p;
 }
 
@@ -133,23 +154,10 @@ inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// LM-head scratch: [(row, slice) partials | partial sums of cut items |
-// arrival counters of the items].
-struct LmLayout {
-    size_t part, fix, counters, total;
-};
-inline LmLayout lm_layout(int rows, int V, int d, bool bf16) {
-    const GemmPlan p = lm_plan(rows, V, d, bf16);
-    LmLayout l;
-    size_t off = 0;
-    l.part = off;
-    off += align256((size_t)rows * p.nchunks * kPartStride * 4);
-    l.fix = off;
-    off += align256(p.fix_floats() * 4);
-    l.counters = off;
-    off += align256(p.counter_ints() * 4);
-    l.total = off;
-    return l;
+// LM-head scratch: the (row, slice) partials.
+inline size_t lm_scratch_bytes(int rows, int V, int d, bool bf16) {
+    const LmPlan p = lm_plan(rows, V, d, bf16);
+    return align256((size_t)rows * p.nsplit() * kPartStride * 4);
 }
 
 struct Workspace {
@@ -164,7 +172,7 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     const int R = 1 + (gamma - 1) * k;
     const size_t es = bf16 ? 2 : 4;
     const int rows1 = b * gamma, rows2 = b * R;
-    const size_t lm1 = lm_layout(rows1, V, d, bf16).total, lm2 = lm_layout(rows2, V, d, bf16).total;
+    const size_t lm1 = lm_scratch_bytes(rows1, V, d, bf16), lm2 = lm_scratch_bytes(rows2, V, d, bf16);
     Workspace w;
     size_t off = 0;
     w.diag = off;

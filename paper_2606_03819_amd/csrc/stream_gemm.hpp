@@ -121,6 +121,10 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
     uint16_t* wl = reinterpret_cast<uint16_t*>(smem + T::XS_BYTES) + wave * T::WROWS * KC;
     const int nk = it.kc1 - it.kc0;
     const int slot = lane & 7;          // 16-byte slot of a 128-byte row segment this lane loads
+    // wave-uniform: does this wave own a weight tile of the segment?  Idle
+    // waves (a segment narrower than the workgroup) still stage activations
+    // and meet the barriers, but load no weights and issue no MFMAs.
+    const bool wact = it.t0 + wave * WM < it.t1;
 
     // Coalesced weight loads: instruction q covers wave rows 8q..8q+7.  Every
     // load is unconditional and in bounds: rows past the matrix read its first
@@ -170,6 +174,7 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
         }
     };
     auto load_w = [&](u32x4 (&w)[NWL], int kc) {
+        if (!wact) return;
         const int k = min(kc * KC + slot * 8, kmax);
 #pragma unroll
         for (int q = 0; q < NWL; ++q) {
@@ -181,6 +186,7 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
         }
     };
     auto store_w = [&](const u32x4 (&w)[NWL]) {
+        if (!wact) return;
 #pragma unroll
         for (int q = 0; q < NWL; ++q) {
             const int row = 8 * q + (lane >> 3);
@@ -198,6 +204,7 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
     u32x4 wr[PIPE][NWL];
     // MFMAs of k-chunk i from LDS (activation buffer i & 1, the wave's weight tile)
     auto compute = [&](int i) {
+        if (!wact) return;
         const uint16_t* xb = xs + (i & 1) * TR * LDSW;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {

@@ -1,7 +1,8 @@
 // Work split of a weight-streaming product, shared by the host plans and the
 // kernels so both derive the same pieces from the same shape.
 //
-// The weight tiles (32 rows each) are grouped into chunks, the activation rows
+// SwiGLU products (few weight tiles): the k-range is cut.  The weight tiles
+// (32 rows each) are grouped into chunks, the activation rows
 // into row blocks.  An item is one (chunk, row block) pair; a unit is one
 // 64-wide k-chunk of an item.  The U = items * nk units are ordered item-major
 // (row block fastest within a chunk, then k) and workgroup g owns the
@@ -51,6 +52,45 @@ inline bool gemm_has_pieces(const GemmShape& s) {
     for (int g = 1; g < s.G; ++g)
         if (unit_start(s, g) % s.nk != 0) return true;
     return false;
+}
+
+// LM head (many weight tiles): the vocabulary is cut instead.
+//
+// Vocabulary slices of the LM head.  The T weight tiles are cut into G
+// contiguous ranges of floor(T/G) or ceil(T/G) tiles (one per workgroup
+// column); range g is streamed in rounds(g) = ceil(n_g / chunk) near-equal
+// rounds of at most `chunk` tiles, each a full pass over K.  Slice g*rmax + r
+// is round r of range g and is empty when r >= rounds(g).  Every workgroup
+// thus streams the same number of weight tiles (up to one), and no slice
+// needs partial sums from another workgroup.
+struct SliceMap {
+    int T;       // weight tiles
+    int G;       // tile ranges
+    int chunk;   // most tiles per round
+    int rmax;    // slices per range
+};
+
+__host__ __device__ inline int slice_range_begin(const SliceMap& m, int g) {
+    return (int)((long long)g * m.T / m.G);
+}
+
+// tiles [t0, t1) of slice s (t0 == t1 for an empty slice)
+__host__ __device__ inline void slice_tiles(const SliceMap& m, int s, int& t0, int& t1) {
+    const int g = s / m.rmax, r = s - g * m.rmax;
+    const int a = slice_range_begin(m, g);
+    const int n = slice_range_begin(m, g + 1) - a;
+    const int rounds = (n + m.chunk - 1) / m.chunk;
+    if (r >= rounds) {
+        t0 = t1 = a;
+        return;
+    }
+    t0 = a + (int)((long long)r * n / rounds);
+    t1 = a + (int)((long long)(r + 1) * n / rounds);
+}
+
+inline SliceMap make_slice_map(int T, int G, int chunk) {
+    const int per = (T + G - 1) / G;
+    return SliceMap{T, G, chunk, (per + chunk - 1) / chunk};
 }
 
 }  // namespace tf

@@ -54,13 +54,15 @@ def test_workspace_size_covers_the_buffers_and_rejects_bad_shapes():
     assert f(1, 16, 4096, 4096, 151936, 8, 32, 7) == 0            # dtype
 
 
-def _marginal(**over):
+def _marginal(timed=False, **over):
     a = dict(h=FAKE, w=FAKE, b=1, gamma=16, d=4096, V=151936, k=8, it=1.0, dt=BF16, idx=FAKE2, lp=None,
              lse=None, ws=FAKE, wsb=1 << 40, st=None)
     a.update(over)
-    return binding.lib().treeflash_marginal_topk(a["h"], a["w"], a["b"], a["gamma"], a["d"], a["V"], a["k"],
-                                                 a["it"], a["dt"], a["idx"], a["lp"], a["lse"], a["ws"], a["wsb"],
-                                                 a["st"])
+    args = (a["h"], a["w"], a["b"], a["gamma"], a["d"], a["V"], a["k"], a["it"], a["dt"], a["idx"], a["lp"],
+            a["lse"], a["ws"], a["wsb"], a["st"])
+    if timed:   # events are never touched when validation fails
+        return binding.lib().treeflash_marginal_topk_timed(*args, FAKE, FAKE)
+    return binding.lib().treeflash_marginal_topk(*args)
 
 
 @pytest.mark.parametrize("over,code", [
@@ -73,8 +75,9 @@ def _marginal(**over):
     (dict(ws=None), WORKSPACE), (dict(ws=FAKE + 8), WORKSPACE),
     (dict(wsb=1024), WORKSPACE),
 ])
-def test_marginal_topk_rejects(over, code):
-    assert _marginal(**over) == code
+@pytest.mark.parametrize("timed", [False, True])
+def test_marginal_topk_rejects(over, code, timed):
+    assert _marginal(timed, **over) == code
 
 
 def _expand(**over):

@@ -64,6 +64,23 @@ def test_repeatable_and_stream_ordered():
         assert torch.equal(x, y)
 
 
+def test_timed_entry_point_matches_and_times_the_lm_head():
+    w = CASES[3][0]
+    cpu = synth.make_inputs(w, "cpu", weight_std=0.08)
+    g = to_gpu(cpu)
+    ws = binding.alloc_workspace(binding.treeflash_workspace_bytes(w.b, w.gamma, w.d, w.I, w.V, w.k, w.k,
+                                                                   w.torch_dtype), g["h"].device)
+    idx_a, lp_a = binding.treeflash_marginal_topk(g["h"], g["lm_head"], w.k, w.inv_temperature, ws)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for e in ev:
+        e.record()   # creates the events
+    idx_b, lp_b = binding.treeflash_marginal_topk(g["h"], g["lm_head"], w.k, w.inv_temperature, ws,
+                                                  events=(ev[0].cuda_event, ev[1].cuda_event))
+    torch.cuda.synchronize()
+    assert torch.equal(idx_a, idx_b) and torch.equal(lp_a, lp_b)
+    assert ev[0].elapsed_time(ev[1]) > 0.0
+
+
 def test_exact_ties_take_smaller_ids_and_use_the_slow_path():
     """Duplicated LM-head rows give exactly equal logits; the (value desc, id
     asc) order must hold and the exact slow path must be exercised."""
