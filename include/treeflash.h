@@ -157,7 +157,10 @@ tf_status_t treeflash_arapprox_expand(const void *h, const int32_t *root_token,
  *                           (each row sorted by log-prob desc, id asc; log-probs <= 0)
  *   topk_idx                [b, gamma, k] stage-1 candidates
  *   B                       draft budget: nodes besides the root, 1 <= B <= 4095,
- *                           B <= V * (1 + k + ... + k^(gamma-1)), and topk2 >= min(B, V)
+ *                           B <= V * (1 + k + ... + k^(gamma-1)), and topk2 >= min(B, V);
+ *                           TF_ERR_UNSUPPORTED when the node table and frontier
+ *                           (44*B + 20 + 4*gamma*k bytes) exceed the kernel's 144 KiB of
+ *                           LDS, i.e. from about B = 3300 on
  * Outputs, per sequence, in pop order (best first), arrays [b, B]:
  *   node_token      token id
  *   node_parent     index of the parent node in the same array, -1 = the root x_t

@@ -1,12 +1,19 @@
-// OPT-Tree selection (Appendix B, Part 2) on the GPU, one wave per sequence.
+// OPT-Tree selection (Appendix B, Part 2) on the GPU, one workgroup per
+// sequence: every wave preloads the sequence's rows into LDS, then one wave
+// selects.
 //
 // The paper's queue holds every child of every expanded node.  Because each
 // conditional row arrives sorted, a node's children are popped in row order,
 // so the frontier only needs each expanded node's best child not yet popped:
 // slot 0 holds the root's next child, slot n+1 node n's next child.  A pop is
-// an argmax over at most B+1 slots (a 64-lane butterfly), then the popped
-// slot advances to its next sibling and, if the popped token is a stage-1
-// candidate of its depth, slot n+1 opens on the first entry of its row.
+// an argmax over at most B+1 slots, then the popped slot advances to its next
+// sibling and, if the popped token is a stage-1 candidate of its depth, slot
+// n+1 opens on the first entry of its row.
+//
+// Up to 1024 slots the frontier lives in registers (slot s in lane s % 64)
+// and the argmax is a DPP maximum of the lanes' score keys; only an exact
+// score tie between lanes runs the full comparison.  Larger budgets keep the
+// frontier in LDS.
 //
 // Candidate order: path score (fp32 running sum) desc, depth asc, then the
 // lexicographic order of the rank paths (ranks of the nodes in their parents'
@@ -18,7 +25,11 @@
 
 namespace tf {
 
-constexpr int kTreeLdsBudget = 64 * 1024;
+// LDS for the node table, the frontier and the cached leading ranks of every
+// row (gfx950 gives a workgroup up to 160 KB).
+constexpr int kTreeLdsBudget = 144 * 1024;
+constexpr int kTreeThreads = 1024;  // all waves preload; wave 0 alone selects
+constexpr int kTreeRegSlots = 16;   // frontier slots per lane held in registers
 
 struct TreeArgs {
     const int32_t* cond_idx;
@@ -93,22 +104,209 @@ __device__ __forceinline__ bool cand_before(const Cand& x, const Cand& y, const 
     return rx < ry;
 }
 
-__global__ __launch_bounds__(64) void build_tree_kernel(TreeArgs a) {
+// Orders this wave's LDS accesses (the selection runs in one wave, whose LDS
+// operations complete in issue order).
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Rows of this sequence's leading ranks and its stage-1 candidates into LDS,
+// every thread with several independent loads in flight.
+__device__ __forceinline__ void tree_preload(const TreeArgs& a, const TreeLds& t, int seq, const float* rlp,
+                                             const int32_t* ridx) {
+    const int tid = threadIdx.x;
+    for (int s = tid; s <= a.B; s += kTreeThreads) t.f_depth[s] = 0;
+    for (int e = tid; e < a.gamma * a.M; e += kTreeThreads) t.tk[e] = a.topk[(size_t)seq * a.gamma * a.M + e];
+    const int ncache = a.Rs * a.P;
+    for (int e0 = tid; e0 < ncache; e0 += 4 * kTreeThreads) {
+        float lp[4];
+        int ix[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * kTreeThreads;
+            const int r = e / a.P, c = e - r * a.P;
+            const size_t gi = e < ncache ? (size_t)r * a.K2 + c : 0;
+            lp[u] = rlp[gi];
+            ix[u] = ridx[gi];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * kTreeThreads;
+            if (e < ncache) {
+                t.c_lp[e] = lp[u];
+                t.c_idx[e] = ix[u];
+            }
+        }
+    }
+}
+
+// Child row of a popped node: 1 + (depth-1)*M + m if its token is candidate m
+// of its depth, else -1 (uniform across the wave).
+__device__ __forceinline__ int tree_child_row(const TreeArgs& a, const TreeLds& t, int depth, int tok, int lane) {
+    if (depth >= a.gamma) return -1;
+    for (int m0 = 0; m0 < a.M; m0 += 64) {
+        const int m = m0 + lane;
+        const bool hit = m < a.M && t.tk[(depth - 1) * a.M + m] == tok;
+        const unsigned long long bal = __ballot(hit);
+        if (bal != 0ull) return 1 + (depth - 1) * a.M + m0 + (__ffsll((long long)bal) - 1);
+    }
+    return -1;
+}
+
+// Node table -> outputs (slots past the last pop get the empty values).
+__device__ __forceinline__ void tree_store(const TreeArgs& a, const TreeLds& t, int seq, int n, int lane) {
+    const size_t o = (size_t)seq * a.B;
+    for (int i = lane; i < a.B; i += 64) {
+        const bool ok = i < n;
+        a.tok[o + i] = ok ? t.n_tok[i] : -1;
+        a.par[o + i] = ok ? t.n_par[i] : -1;
+        a.dep[o + i] = ok ? t.n_dep[i] : 0;
+        a.score[o + i] = ok ? t.n_score[i] : neg_inf();
+        if (a.crow != nullptr) a.crow[o + i] = ok ? t.n_crow[i] : -1;
+    }
+}
+
+// Wave maximum through DPP: quad swaps, half-row and row mirrors give every
+// lane its 16-lane row maximum; four readlanes combine the rows.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));  // row_mirror
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+
+// Best candidate of the wave under the full order (butterfly).
+__device__ __forceinline__ Cand wave_best(Cand best, const TreeLds& t) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        Cand other{__shfl_xor(best.score, o), (uint32_t)__shfl_xor((int)best.meta, o)};
+        if (cand_before(other, best, t)) best = other;
+    }
+    return best;
+}
+
+// Frontier in registers: slot s = lane + 64*j, j < FS (B + 1 <= 64*FS).
+template <int FS>
+__global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a) {
     extern __shared__ __align__(16) unsigned char dyn[];
     const TreeLds t = tree_lds(dyn, a);
     const int seq = blockIdx.x;
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & 63;
     const int32_t* ridx = a.cond_idx + (size_t)seq * a.Rs * a.K2;
     const float* rlp = a.cond_lp + (size_t)seq * a.Rs * a.K2;
-
-    for (int s = lane; s <= a.B; s += 64) t.f_depth[s] = 0;
-    for (int e = lane; e < a.gamma * a.M; e += 64) t.tk[e] = a.topk[(size_t)seq * a.gamma * a.M + e];
-    for (int e = lane; e < a.Rs * a.P; e += 64) {
-        const int r = e / a.P, c = e - r * a.P;
-        t.c_lp[e] = rlp[(size_t)r * a.K2 + c];
-        t.c_idx[e] = ridx[(size_t)r * a.K2 + c];
-    }
+    tree_preload(a, t, seq, rlp, ridx);
     __syncthreads();
+    if (threadIdx.x >= 64) return;
+    auto get_lp = [&](int r, int c) -> float {
+        return c < a.P ? t.c_lp[r * a.P + c] : rlp[(size_t)r * a.K2 + c];
+    };
+    auto get_idx = [&](int r, int c) -> int {
+        return c < a.P ? t.c_idx[r * a.P + c] : ridx[(size_t)r * a.K2 + c];
+    };
+    float f_score[FS], f_pscore[FS];
+    int f_depth[FS], f_rank[FS], f_row[FS];
+#pragma unroll
+    for (int j = 0; j < FS; ++j) {
+        f_score[j] = f_pscore[j] = 0.f;
+        f_depth[j] = f_rank[j] = f_row[j] = 0;
+    }
+    {
+        const float first = get_lp(0, 0);
+        if (lane == 0) {
+            f_depth[0] = 1;
+            f_score[0] = first;
+        }
+    }
+
+    int n = 0;
+    for (; n < a.B; ++n) {
+        Cand lb{0.f, 0u};
+#pragma unroll
+        for (int j = 0; j < FS; ++j)
+            if (f_depth[j] > 0) {
+                const Cand c{f_score[j],
+                             ((uint32_t)f_depth[j] << 24) | ((uint32_t)(lane + 64 * j) << 12) | (uint32_t)f_rank[j]};
+                if (cand_before(c, lb, t)) lb = c;
+            }
+        const uint32_t key = c_depth(lb.meta) != 0 ? f32_key(lb.score) : 0u;
+        const uint32_t mx = wave_max_u32(key);
+        if (mx == 0u) break;   // frontier exhausted (excluded by argument checks)
+        const unsigned long long tied = __ballot(key == mx);
+        Cand best;
+        if (__popcll(tied) == 1) {
+            const int wl = __ffsll((long long)tied) - 1;
+            best.score = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lb.score), wl));
+            best.meta = (uint32_t)__builtin_amdgcn_readlane((int)lb.meta, wl);
+        } else {   // exact score tie between lanes: the full order decides
+            best = wave_best(key == mx ? lb : Cand{0.f, 0u}, t);
+        }
+        const int depth = c_depth(best.meta), slot = c_slot(best.meta), rank = c_rank(best.meta);
+        const int owner = slot & 63, js = slot >> 6;
+        int my_row = 0;
+        float my_ps = 0.f;
+#pragma unroll
+        for (int j = 0; j < FS; ++j)
+            if (j == js) {
+                my_row = f_row[j];
+                my_ps = f_pscore[j];
+            }
+        const int row = __builtin_amdgcn_readlane(my_row, owner);
+        const float pscore = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_ps), owner));
+        const int tok = get_idx(row, rank);
+        const int child_row = tree_child_row(a, t, depth, tok, lane);
+        if (lane == 0) {
+            t.n_tok[n] = tok;
+            t.n_par[n] = slot - 1;
+            t.n_rank[n] = rank;
+            t.n_dep[n] = depth;
+            t.n_score[n] = best.score;
+            t.n_crow[n] = child_row;
+        }
+        // the popped slot moves to its next sibling (owner lane)
+        const bool more = rank + 1 < a.K2;
+        const float next_lp = more ? get_lp(row, rank + 1) : 0.f;
+        if (lane == owner) {
+#pragma unroll
+            for (int j = 0; j < FS; ++j)
+                if (j == js) {
+                    f_rank[j] = rank + 1;
+                    f_score[j] = pscore + next_lp;
+                    f_depth[j] = more ? f_depth[j] : 0;
+                }
+        }
+        // an expandable node opens slot n + 1 on the first entry of its row
+        if (child_row >= 0) {
+            const float first = get_lp(child_row, 0);
+            const int jn = (n + 1) >> 6;
+            if (lane == ((n + 1) & 63)) {
+#pragma unroll
+                for (int j = 0; j < FS; ++j)
+                    if (j == jn) {
+                        f_depth[j] = depth + 1;
+                        f_rank[j] = 0;
+                        f_row[j] = child_row;
+                        f_pscore[j] = best.score;
+                        f_score[j] = best.score + first;
+                    }
+            }
+        }
+        wave_lds_sync();   // node n is in LDS before a later tie walk reads it
+    }
+    tree_store(a, t, seq, n, lane);
+}
+
+// Frontier in LDS, for budgets beyond the register frontier.
+__global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
+    extern __shared__ __align__(16) unsigned char dyn[];
+    const TreeLds t = tree_lds(dyn, a);
+    const int seq = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int32_t* ridx = a.cond_idx + (size_t)seq * a.Rs * a.K2;
+    const float* rlp = a.cond_lp + (size_t)seq * a.Rs * a.K2;
+    tree_preload(a, t, seq, rlp, ridx);
+    __syncthreads();
+    if (threadIdx.x >= 64) return;
     auto get_lp = [&](int r, int c) -> float {
         return c < a.P ? t.c_lp[r * a.P + c] : rlp[(size_t)r * a.K2 + c];
     };
@@ -122,7 +320,7 @@ __global__ __launch_bounds__(64) void build_tree_kernel(TreeArgs a) {
         t.f_pscore[0] = 0.f;
         t.f_score[0] = 0.f + get_lp(0, 0);
     }
-    __syncthreads();
+    wave_lds_sync();
 
     int n = 0;
     for (; n < a.B; ++n) {
@@ -134,29 +332,14 @@ __global__ __launch_bounds__(64) void build_tree_kernel(TreeArgs a) {
                 if (cand_before(c, best, t)) best = c;
             }
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            Cand other{__shfl_xor(best.score, o), (uint32_t)__shfl_xor((int)best.meta, o)};
-            if (cand_before(other, best, t)) best = other;
-        }
+        best = wave_best(best, t);
         const int depth = c_depth(best.meta);
         if (depth == 0) break;   // frontier exhausted (excluded by argument checks)
         const int slot = c_slot(best.meta), rank = c_rank(best.meta);
         const int row = t.f_row[slot];
         const int tok = get_idx(row, rank);
-        int child_row = -1;
-        if (depth < a.gamma) {
-            for (int m0 = 0; m0 < a.M; m0 += 64) {
-                const int m = m0 + lane;
-                const bool hit = m < a.M && t.tk[(depth - 1) * a.M + m] == tok;
-                const unsigned long long bal = __ballot(hit);
-                if (bal != 0ull) {
-                    child_row = 1 + (depth - 1) * a.M + m0 + (__ffsll((long long)bal) - 1);
-                    break;
-                }
-            }
-        }
-        __syncthreads();   // every lane has read the frontier before it changes
+        const int child_row = tree_child_row(a, t, depth, tok, lane);
+        wave_lds_sync();   // every lane has read the frontier before it changes
         if (lane == 0) {
             t.n_tok[n] = tok;
             t.n_par[n] = slot - 1;
@@ -178,17 +361,9 @@ __global__ __launch_bounds__(64) void build_tree_kernel(TreeArgs a) {
                 t.f_score[n + 1] = best.score + get_lp(child_row, 0);
             }
         }
-        __syncthreads();
+        wave_lds_sync();
     }
-    const size_t o = (size_t)seq * a.B;
-    for (int i = lane; i < a.B; i += 64) {
-        const bool ok = i < n;
-        a.tok[o + i] = ok ? t.n_tok[i] : -1;
-        a.par[o + i] = ok ? t.n_par[i] : -1;
-        a.dep[o + i] = ok ? t.n_dep[i] : 0;
-        a.score[o + i] = ok ? t.n_score[i] : neg_inf();
-        if (a.crow != nullptr) a.crow[o + i] = ok ? t.n_crow[i] : -1;
-    }
+    tree_store(a, t, seq, n, lane);
 }
 
 size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks) {
@@ -210,7 +385,25 @@ hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, cons
     if (lds == 0) return hipErrorInvalidValue;
     TreeArgs a{cond_idx, cond_lp, topk_idx, gamma, k, topk2, B, Rs, P,
                node_token, node_parent, node_depth, node_score, node_child_row};
-    hipLaunchKernelGGL(build_tree_kernel, dim3(b), dim3(64), lds, stream, a);
+    const void* fn;
+    if (B + 1 <= 64)
+        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<1>);
+    else if (B + 1 <= 128)
+        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<2>);
+    else if (B + 1 <= 256)
+        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<4>);
+    else if (B + 1 <= 512)
+        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<8>);
+    else if (B + 1 <= 64 * kTreeRegSlots)
+        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<kTreeRegSlots>);
+    else
+        fn = reinterpret_cast<const void*>(build_tree_kernel);
+    // dynamic LDS beyond the 64 KiB default
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kTreeLdsBudget) != hipSuccess)
+        return hipErrorInvalidValue;
+    void* args[] = {&a};
+    const hipError_t e = hipLaunchKernel(fn, dim3(b), dim3(kTreeThreads), args, lds, stream);
+    if (e != hipSuccess) return e;
     return hipGetLastError();
 }
 
