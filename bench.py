@@ -58,11 +58,11 @@ def kernel_source_digest() -> str:
     return hsh.hexdigest()
 
 
-def lm_kernel_prefix(rows: int) -> str:
-    """Name prefix of the bf16 LM-head kernel instance the plan picks for `rows` rows."""
+def lm_kernel_pattern(rows: int) -> str:
+    """Regex for the bf16 LM-head kernel instance the plan picks for `rows` rows
+    (template arguments: weight tiles per wave, activation tiles, waves, ...)."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
-    wm = 2 if nt == 1 else 1
-    return f"lmhead_bf16_kernel<{wm}, {nt}, "
+    return rf"lmhead_bf16_kernel<\d+, {nt}, "
 
 
 def traffic_file(workload: str) -> str:
@@ -157,7 +157,7 @@ def summarize_trace(args):
 def summarize_pmc(args):
     """HBM traffic of the stage-2 LM-head kernel, scaled by a plain copy of known size."""
     w = synth.get_workload(args.workload)
-    prefix = lm_kernel_prefix(w.rows * w.b)
+    pattern = lm_kernel_pattern(w.rows * w.b)
 
     def per_kernel(path, counter):
         cur = _db(path).cursor()
@@ -175,8 +175,8 @@ def summarize_pmc(args):
             raise SystemExit("kernel not found in the counter runs")
         return max(hits, key=lambda kv: kv[1][0])
 
-    lm_f = pick(fetch, lambda k: k.replace("void tf::", "").startswith(prefix))
-    lm_w = pick(write, lambda k: k.replace("void tf::", "").startswith(prefix))
+    lm_f = pick(fetch, lambda k: re.search(pattern, k) is not None)
+    lm_w = pick(write, lambda k: re.search(pattern, k) is not None)
     cp_f = pick(fetch, lambda k: "neg" in k.lower())
     cp_w = pick(write, lambda k: "neg" in k.lower())
     kib = COPY_BYTES / 1024.0
@@ -304,7 +304,7 @@ def main():
         roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = read_traffic(w.name)
-    roof["kernel"] = lm_kernel_prefix(rows).rstrip(", ") + " (stage-2 LM head on h')" if w.dtype == "bf16" \
+    roof["kernel"] = "lmhead_bf16_kernel (stage-2 LM head on h')" if w.dtype == "bf16" \
         else "lmhead_f32_kernel (stage-2 LM head on h')"
     roof["kernel_us"] = gemm
     roof["alg_bytes_per_launch"] = alg_bytes

@@ -15,7 +15,7 @@ namespace tf {
 // One workgroup per (tile range, row block): the range's rounds in turn, each
 // a full pass over K reduced to a (row, slice) partial.
 template <int WM, int NT, int NW, int PIPE, bool WNT>
-__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
+__global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
                                                                                const uint16_t* __restrict__ w,
                                                                                GemmShape sh, SliceMap map, int V,
                                                                                float sl2, float* __restrict__ part,
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
         c[3 + kLane + e] = __int_as_float(li[e]);
     }
     __syncthreads();
-    lm_merge_contributors<8, kLane>(cmrg, 32, row0, split, sh.nchunks, sh.R, sl2, part);
+    lm_merge_contributors<8, kLane>(cmrg, 8 * W, 32, row0, split, sh.nchunks, sh.R, sl2, part);
 }
 
 // ------------------------------------------------------------------ merge
@@ -411,11 +411,11 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 
 // ------------------------------------------------------------------ launchers
 
-template <int WM, int NT, int PIPE, bool WNT>
+template <int WM, int NT, int NW, int PIPE, bool WNT>
 static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, const SliceMap& map,
                            int blocks, int V, float sl2, float* part, int* diag, hipStream_t st) {
-    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(blocks), dim3(64 * TF_NW), 0, st, x, ldx,
-                       w, sh, map, V, sl2, part, diag);
+    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(blocks), dim3(64 * NW), 0, st, x, ldx, w, sh,
+                       map, V, sl2, part, diag);
 }
 
 // tile shape and pipeline variants the plans can ask for
@@ -423,13 +423,17 @@ static void dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const
                              int V, float sl2, float* part, int* diag, hipStream_t st) {
     const int nb = p.blocks();
     if (p.NT == 1)
-        launch_lm_bf16<2, 1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+                                                                           diag, st);
     else if (p.NT == 2)
-        launch_lm_bf16<1, 2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        launch_lm_bf16<TF_LM_WM_NT2, 2, TF_LM_NW_NT2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+                                                                           diag, st);
     else if (p.wnt)
-        launch_lm_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, p.map, nb, V, sl2,
+                                                                              part, diag, st);
     else
-        launch_lm_bf16<1, 4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+                                                                            diag, st);
 }
 
 hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,

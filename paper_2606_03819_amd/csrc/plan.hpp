@@ -117,14 +117,38 @@ struct LmPlan {
     int blocks() const { return map.G * nrb; }
 };
 
+// LM-head tile shape per activation-tile count: waves per workgroup and
+// weight tiles per wave (one wave per SIMD when NW = 4, so that a wave may
+// hold 128 accumulator registers).
+#ifndef TF_LM_NW_NT1
+#define TF_LM_NW_NT1 4
+#endif
+#ifndef TF_LM_WM_NT1
+#define TF_LM_WM_NT1 4
+#endif
+#ifndef TF_LM_NW_NT2
+#define TF_LM_NW_NT2 8
+#endif
+#ifndef TF_LM_WM_NT2
+#define TF_LM_WM_NT2 1
+#endif
+#ifndef TF_LM_NW_NT4
+#define TF_LM_NW_NT4 8
+#endif
+#ifndef TF_LM_WM_NT4
+#define TF_LM_WM_NT4 1
+#endif
+inline int lm_nw(int NT) { return NT == 1 ? TF_LM_NW_NT1 : (NT == 2 ? TF_LM_NW_NT2 : TF_LM_NW_NT4); }
+inline int lm_wm(int NT) { return NT == 1 ? TF_LM_WM_NT1 : (NT == 2 ? TF_LM_WM_NT2 : TF_LM_WM_NT4); }
+
 inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     LmPlan p;
     p.ntiles = cdiv(V, 32);
     p.nk = cdiv(d, 64);
     if (bf16) {
         p.NT = plan_nt(rows);
-        p.WM = plan_wm(p.NT);
-        p.NW = TF_NW;
+        p.WM = lm_wm(p.NT);
+        p.NW = lm_nw(p.NT);
         p.chunk = p.NW * p.WM;
         p.nrb = cdiv(rows, 32 * p.NT);
         const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)

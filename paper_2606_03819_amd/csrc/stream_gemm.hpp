@@ -10,19 +10,25 @@
 // lane.
 //
 // Work decomposition (see work.hpp): a workgroup of NW waves streams chunks
-// of NW*WM weight tiles (WM per wave) against blocks of 32*NT activation rows,
-// one k-range at a time; the units of a single row block are cut evenly over
-// the workgroups, so every workgroup streams the same bytes.  Per 64-wide
-// k-chunk the activation tile [32*NT x 64] is staged in LDS (double buffered,
-// rows padded to 144 B so the 16-byte fragment reads are bank-conflict free)
-// and shared by all NW*WM weight tiles of the workgroup.
+// of NW*WM weight tiles (WM per wave) against blocks of 32*NT activation rows.
+// The LM head cuts the vocabulary into equal tile ranges, one per workgroup,
+// streamed in rounds; the small SwiGLU products cut their k-range instead.
+// Per 64-wide k-chunk the activation tile [32*NT x 64] is staged in LDS
+// (double buffered, rows padded to 144 B so the 16-byte fragment reads are
+// bank-conflict free) and shared by all NW*WM weight tiles of the workgroup.
 // Each wave streams its own weight rows with fully coalesced loads -- one
 // instruction covers 8 rows x 128 B, i.e. whole cache lines -- several
-// k-chunks ahead of the MFMAs, and transposes them into fragment order through a
-// wave-private LDS tile whose 16-byte slots are XOR-swizzled by row (see
-// wswz), so both the writes and the fragment reads are conflict free.  (Loading fragments
-// directly -- 32 rows x 32 B per instruction -- measured ~17% less HBM
-// bandwidth on MI355X.)
+// k-chunks ahead of the MFMAs, and transposes them into fragment order
+// through a wave-private LDS tile whose 16-byte slots are XOR-swizzled by
+// row (see wswz), so both the writes and the fragment reads are conflict
+// free.  (Loading fragments directly -- 32 rows x 32 B per instruction --
+// measured ~17% less HBM bandwidth on MI355X.)
+//
+// What bounds these kernels on MI355X is the vector-memory path of each CU:
+// weight bytes (from HBM) plus activation bytes (re-read from L2 once per
+// round of a workgroup) together top out near 6.5-7 TB/s, the rate of a
+// plain streaming read.  The activation share therefore shrinks with more
+// weight tiles per round (more accumulators per CU).
 #pragma once
 
 #include "common.hpp"
@@ -50,11 +56,12 @@ __device__ __forceinline__ int xcd_logical_id(int bid, int nblocks) {
     return (bid & 7) * (nblocks >> 3) + (bid >> 3);
 }
 
+
 template <int WM, int NT, int NW>
 struct GemmTraits {
     static constexpr int TR = 32 * NT;           // activation rows per workgroup
     static constexpr int KC = 64;                // k per LDS stage
-    static constexpr int LDSW = KC + 8;          // padded LDS row, bf16 elements
+    static constexpr int LDSW = KC + 8;          // padded LDS row (144 B), bf16 elements
     static constexpr int XS_BYTES = 2 * TR * LDSW * 2;
     static constexpr int WROWS = 32 * WM;        // weight rows per wave
     static constexpr int WS_BYTES = NW * WROWS * KC * 2;   // wave-private weight tiles
@@ -104,20 +111,21 @@ __device__ __forceinline__ int wswz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Accumulate one segment: acc[mt][nt] = X[rows of nt] . W[tiles of mt] over
-// the segment's k-chunks.  PIPE: k-chunks of loads in flight per wave.  WNT:
-// weight loads carry the non-temporal hint, for weights that one workgroup
-// alone reads (a single activation row block), so they do not evict the
-// activations that every workgroup re-reads from L2.
+// the segment's 64-wide k-chunks.  PIPE: k-chunks of loads in flight per
+// wave.  WNT: weight loads carry the non-temporal hint, for weights that one
+// workgroup alone reads (a single activation row block), so they do not
+// evict the activations that every workgroup re-reads from L2.
 template <int WM, int NT, int NW, int PIPE, bool WNT, class WSrc, class XSrc>
 __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc, const GemmShape& sh,
                                              const Segment& it, f32x16 (&acc)[WM][NT], unsigned char* smem) {
     using T = GemmTraits<WM, NT, NW>;
     constexpr int TR = T::TR, KC = T::KC, LDSW = T::LDSW, NWL = T::NWL, NTH = T::NTHREADS, XPT = T::XPT;
-    uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
+    uint16_t* xs = reinterpret_cast<uint16_t*>(smem);   // [2 buffers][TR][LDSW]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    // this wave's weight tile: [WROWS][KC]
     uint16_t* wl = reinterpret_cast<uint16_t*>(smem + T::XS_BYTES) + wave * T::WROWS * KC;
     const int nk = it.kc1 - it.kc0;
     const int slot = lane & 7;          // 16-byte slot of a 128-byte row segment this lane loads
@@ -162,13 +170,15 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
             }
         }
     };
+    // chunk kc into activation buffer `buf`; zero outside the matrix
     auto store_x = [&](const u32x4 (&xr)[XPT], int buf, int kc) {
+        uint16_t* dst = xs + buf * TR * LDSW;
 #pragma unroll
         for (int i = 0; i < XPT; ++i) {
             const int p = tid + NTH * i;
             if (XFULL || p < T::XPIECES) {
                 const bool ok = it.row0 + (p >> 3) < sh.R && kc * KC + (p & 7) * 8 < sh.K;
-                *reinterpret_cast<u32x4*>(xs + buf * TR * LDSW + (p >> 3) * LDSW + (p & 7) * 8) =
+                *reinterpret_cast<u32x4*>(dst + (p >> 3) * LDSW + (p & 7) * 8) =
                     ok ? xr[i] : u32x4{0u, 0u, 0u, 0u};
             }
         }
@@ -194,14 +204,19 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
         }
     };
 
-    // Software pipeline of depth PIPE: the loads of k-chunk j are issued at the
-    // end of step j-PIPE and stored to LDS at the end of step j-1, so each load
-    // has PIPE-1 steps to arrive.  Within a step the stores wait only for the
-    // loads of the chunk they store (loads return in order), leaving the
+    // Software pipeline of depth PIPE: the loads of k-chunk j are issued at
+    // the start of step j-PIPE+1 (their register set held chunk j-PIPE+1,
+    // already in LDS), so they run under that step's MFMAs, and are stored
+    // to LDS at the end of step j-1.  Within a step the stores wait only for
+    // the loads of the chunk they store (loads return in order), leaving the
     // later chunks in flight.
     static_assert(PIPE >= 2 && PIPE <= 4, "pipeline depth");
     u32x4 xr[PIPE][XPT];
     u32x4 wr[PIPE][NWL];
+    auto load_step = [&](int r, int i) {
+        load_x(xr[r], it.kc0 + i);
+        load_w(wr[r], it.kc0 + i);
+    };
     // MFMAs of k-chunk i from LDS (activation buffer i & 1, the wave's weight tile)
     auto compute = [&](int i) {
         if (!wact) return;
@@ -217,8 +232,8 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
             }
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
-                bfr[nt] = *reinterpret_cast<const u32x4*>(xb + (nt * 32 + (lane & 31)) * LDSW + ks * 16 +
-                                                          (lane >> 5) * 8);
+                bfr[nt] = *reinterpret_cast<const u32x4*>(
+                    xb + (nt * 32 + (lane & 31)) * LDSW + (2 * ks + (lane >> 5)) * 8);
 #pragma unroll
             for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
@@ -226,48 +241,44 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
                     acc[mt][nt] = mfma_32x32x16_bf16(afr[mt], bfr[nt], acc[mt][nt]);
         }
     };
-    // store register set s (k-chunk i) into LDS after this wave's reads of the
+    // store register set r (k-chunk i) into LDS after this wave's reads of the
     // previous chunk (LDS operations of a wave complete in order)
-    auto stage = [&](int s, int i) {
+    auto stage = [&](int r, int i) {
         compiler_fence();
-        store_w(wr[s]);
-        store_x(xr[s], i & 1, it.kc0 + i);
+        store_w(wr[r]);
+        store_x(xr[r], i & 1, it.kc0 + i);
         compiler_fence();
     };
-    if (nk > 0) {
+    const int nsteps = nk;
+    if (nsteps > 0) {
 #pragma unroll
         for (int j = 0; j < PIPE; ++j)
-            if (j < nk) {
-                load_x(xr[j], it.kc0 + j);
-                load_w(wr[j], it.kc0 + j);
-            }
+            if (j < nsteps) load_step(j, j);
         stage(0, 0);
         int i0 = 0;
-        // steady state, branch free: every step computes, stages the next
-        // chunk and issues the loads PIPE chunks ahead
-        for (; i0 + 2 * PIPE <= nk; i0 += PIPE) {
+        // steady state, branch free: every step refills the register set it
+        // freed, computes, and stages the next chunk
+        for (; i0 + 2 * PIPE <= nsteps; i0 += PIPE) {
 #pragma unroll
             for (int u = 0; u < PIPE; ++u) {
                 const int i = i0 + u;
-                lds_barrier();  // chunk i visible; the other activation buffer is free
+                // register set u held step i, already in LDS: refill it first,
+                // so the loads run under this step's MFMAs
+                load_step(u, i + PIPE);
+                lds_barrier();  // step i visible; the other activation buffer is free
                 compute(i);
                 stage((u + 1) % PIPE, i + 1);
-                load_x(xr[u], it.kc0 + i + PIPE);
-                load_w(wr[u], it.kc0 + i + PIPE);
             }
         }
-        // tail: fewer than 2*PIPE chunks left
+        // tail: fewer than 2*PIPE steps left
 #pragma unroll
         for (int u = 0; u < 2 * PIPE; ++u) {
             const int i = i0 + u;
-            if (i < nk) {
+            if (i < nsteps) {
+                if (i + PIPE < nsteps) load_step(u % PIPE, i + PIPE);
                 lds_barrier();
                 compute(i);
-                if (i + 1 < nk) stage((u + 1) % PIPE, i + 1);
-                if (i + PIPE < nk) {
-                    load_x(xr[u % PIPE], it.kc0 + i + PIPE);
-                    load_w(wr[u % PIPE], it.kc0 + i + PIPE);
-                }
+                if (i + 1 < nsteps) stage((u + 1) % PIPE, i + 1);
             }
         }
     }
@@ -347,14 +358,14 @@ struct XRowsConcat {
 // least every value the contributor saw but did not list) into the row's
 // (row, slice) partial.  One thread per row.
 template <int NC, int KL>
-__device__ inline void lm_merge_contributors(const float* cm, int rows, int row0, int split, int nsplit, int R,
-                                             float sl2, float* part) {
+__device__ inline void lm_merge_contributors(const float* cm, int rstride, int rows, int row0, int split, int nsplit,
+                                             int R, float sl2, float* part) {
     constexpr int W = 3 + 2 * KL;
     const int tid = threadIdx.x;
     if (tid >= rows) return;
     const int grow = row0 + tid;
     if (grow >= R) return;
-    const float* c = cm + tid * NC * W;
+    const float* c = cm + tid * rstride;
     float M = neg_inf(), U = neg_inf();
 #pragma unroll
     for (int p = 0; p < NC; ++p) {
@@ -428,7 +439,9 @@ struct EpiLmHead {
     static constexpr int KL = kLaneMfma;
     static constexpr int NC = 2 * NW;             // contributor lists per row
     static constexpr int MERGE_WORDS = 3 + 2 * KL;
-    static constexpr int MERGE_BYTES = 32 * NT * NC * MERGE_WORDS * 4;
+    // odd row stride: the lanes of a wave (consecutive rows) hit distinct banks
+    static constexpr int RSTRIDE = NC * MERGE_WORDS + 1;
+    static constexpr int MERGE_BYTES = 32 * NT * RSTRIDE * 4;
 
     // One row (accumulator column nt) of this lane; tokens past the
     // vocabulary count as -inf.
@@ -482,7 +495,7 @@ struct EpiLmHead {
         static_assert(KL == 2, "lane lists hold two entries");
         const int lane = threadIdx.x & 63;
         const int wave = threadIdx.x >> 6;
-        float* cm = reinterpret_cast<float*>(smem);   // [32*NT rows][NC contributors][MERGE_WORDS]
+        float* cm = reinterpret_cast<float*>(smem);   // [32*NT rows, stride RSTRIDE][NC contributors][MERGE_WORDS]
         const int q = wave * 2 + (lane >> 5);
         const int tw = it.t0 + wave * WM;            // this wave's first tile
         int vbase[WM];
@@ -490,9 +503,9 @@ struct EpiLmHead {
         for (int mt = 0; mt < WM; ++mt) vbase[mt] = (tw + mt < it.t1 ? tw + mt : 0x3fffffff / 32) * 32 + 4 * (lane >> 5);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
-            lane_row(acc, nt, vbase, cm + ((nt * 32 + (lane & 31)) * NC + q) * MERGE_WORDS);
+            lane_row(acc, nt, vbase, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
         __syncthreads();
-        lm_merge_contributors<NC, KL>(cm, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
+        lm_merge_contributors<NC, KL>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
 };
 
