@@ -145,9 +145,11 @@ def summarize_trace(args):
     """Markdown table of per-kernel durations from a rocprofv3 --kernel-trace run."""
     cur = _db(args.summarize_trace).cursor()
     rows = cur.execute("select name, count(*), avg(duration), min(duration), max(duration), sum(duration) "
-                       "from kernels group by name order by sum(duration) desc").fetchall()
+                       "from kernels where name like '%tf::%' group by name order by sum(duration) desc").fetchall()
     print(f"# Kernel trace: TreeFlash drafting step, {args.workload}\n")
     print(f"Command (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
+    print("The library's kernels only (the PyTorch kernels that draw the synthetic inputs are left out); "
+          "each bench step runs every kernel once, the merge twice (stage 1 and stage 2).\n")
     print("| kernel | calls | avg us | min us | max us | total ms |\n|---|---|---|---|---|---|")
     for name, n, avg, mn, mx, tot in rows:
         short = name.split("(")[0].replace("void ", "")
