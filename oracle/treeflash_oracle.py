@@ -20,6 +20,10 @@ Part 2 -- OPT-Tree selection
   * best-first pops of the candidate with the highest path probability until
     the tree holds B nodes besides the root; a popped node contributes its
     children only when its token is one of the M candidates of its depth.
+Marginal baseline (the paper's DDTree comparison, Related Work and Appendix C)
+  * the same selection on the marginal distributions alone: every node above
+    the last depth expands into the marginal row of the next depth, so all
+    paths share one child ranking (a nested tree).
 
 Arithmetic is float64 throughout, with the following readings where the paper
 is silent (each is listed in DESIGN.md):
@@ -46,7 +50,7 @@ import numpy as np
 __all__ = [
     "bf16_round", "rms_norm", "silu", "log_softmax", "topk_sorted",
     "marginal_stage", "row_table", "previous_tokens", "ar_approximator",
-    "conditional_stage", "build_tree", "draft", "RMS_EPS",
+    "conditional_stage", "build_tree", "draft", "build_marginal_tree", "draft_marginal", "RMS_EPS",
 ]
 
 RMS_EPS = 1e-6
@@ -261,6 +265,53 @@ def build_tree(cond_idx: np.ndarray, cond_logprob: np.ndarray, topk_idx_seq: np.
     }
 
 
+def build_marginal_tree(marg_idx: np.ndarray, marg_logprob: np.ndarray, gamma: int,
+                        B: int) -> Dict[str, np.ndarray]:
+    """OPT-Tree selection on the marginal distributions (the DDTree baseline).
+
+    marg_idx / marg_logprob: [gamma, K] stage-1 rows sorted (log-prob desc,
+    token asc), row i-1 being depth i; K >= min(B, V) gives the tree of full
+    rows.  Every node of depth d < gamma takes its children from row d (the
+    marginal of depth d+1), whatever its token; the root's children come from
+    row 0.  Pops, scores (float32 running sums) and ties follow build_tree.
+    Returns the same fields as build_tree; child_row is the row a node expands
+    into (-1 at depth gamma).
+    """
+    marg_idx = np.asarray(marg_idx)
+    lp32 = np.asarray(marg_logprob, dtype=np.float32)
+    K = marg_idx.shape[1]
+    heap: List[tuple] = []
+
+    def push_row(row: int, parent: int, parent_score: np.float32, depth: int, path: tuple):
+        for c in range(K):
+            s = np.float32(parent_score + lp32[row, c])        # float32 add
+            heapq.heappush(heap, (-float(s), depth, path + (c,), parent, row, c))
+
+    push_row(0, -1, np.float32(0.0), 1, ())
+    token, parent, depth_o, score, child_row, rank = [], [], [], [], [], []
+    while len(token) < B:
+        if not heap:
+            raise ValueError("draft budget exceeds the number of admissible nodes")
+        negs, dep, path, par, row, c = heapq.heappop(heap)
+        crow = dep if dep < gamma else -1
+        token.append(int(marg_idx[row, c]))
+        parent.append(par)
+        depth_o.append(dep)
+        score.append(np.float32(-negs))
+        child_row.append(crow)
+        rank.append(c)
+        if crow >= 0:
+            push_row(crow, len(token) - 1, np.float32(-negs), dep + 1, path)
+    return {
+        "token": np.asarray(token, dtype=np.int32),
+        "parent": np.asarray(parent, dtype=np.int32),
+        "depth": np.asarray(depth_o, dtype=np.int32),
+        "score": np.asarray(score, dtype=np.float32),
+        "child_row": np.asarray(child_row, dtype=np.int32),
+        "rank": np.asarray(rank, dtype=np.int32),
+    }
+
+
 # ------------------------------------------------------------- whole step
 
 def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
@@ -299,4 +350,24 @@ def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
         out["hprime"].append(hp)
         out["tree"].append(tree)
         out["prev"].append(prev)
+    return out
+
+
+def draft_marginal(inputs: Dict[str, np.ndarray], gamma: int, B: int, inv_temperature: float = 1.0,
+                   K: Optional[int] = None, sequences: Optional[List[int]] = None) -> Dict[str, object]:
+    """The marginal baseline for every sequence: stage 1 with K = min(B, V)
+    entries per depth, then build_marginal_tree."""
+    h = inputs["h"]
+    V = inputs["lm_head"].shape[0]
+    K = min(B, V) if K is None else K
+    seqs = list(range(h.shape[0])) if sequences is None else list(sequences)
+    out = {"stage1": [], "tree": []}
+    for s in seqs:
+        st1 = marginal_stage(h[s:s + 1], inputs["lm_head"], K, inv_temperature)
+        st1 = {key: val[0] for key, val in st1.items()}
+        tree = build_marginal_tree(st1["topk_idx"], st1["topk_logprob"], gamma, B)
+        st1.pop("logits")
+        st1.pop("logprob")
+        out["stage1"].append(st1)
+        out["tree"].append(tree)
     return out

@@ -111,3 +111,42 @@ def check_tree_invariants(tree, cond_idx, cond_logprob, topk_idx_seq, gamma, M, 
         keys.append((-float(sc[i]), int(dep[i])))
     for a, b in zip(keys, keys[1:]):
         assert a <= b, "pops must come in non-increasing candidate order"
+
+
+def brute_force_marginal_tree(marg_idx, marg_logprob, gamma, B):
+    """Every token path of length 1..gamma over the marginal rows (depth d uses
+    row d-1), float32 left-to-right sums, sorted by the candidate order; the
+    best B.  Independent of the oracle's heap."""
+    marg_idx = np.asarray(marg_idx)
+    lp = np.asarray(marg_logprob, dtype=np.float32)
+    K = marg_idx.shape[1]
+    found = []
+    stack = [(1, np.float32(0.0), ())]
+    while stack:
+        dep, s_par, path = stack.pop()
+        for c in range(K):
+            s = np.float32(s_par + lp[dep - 1, c])
+            p = path + (c,)
+            found.append((_key(s, dep, p), s, int(marg_idx[dep - 1, c])))
+            if dep < gamma:
+                stack.append((dep + 1, s, p))
+    if len(found) < B:
+        raise ValueError("budget exceeds admissible nodes")
+    found.sort(key=lambda t: t[0])
+    top = found[:B]
+    pos = {t[0][2]: i for i, t in enumerate(top)}
+    out = {k: [] for k in ("token", "parent", "depth", "score", "rank")}
+    for key, s, tok in top:
+        path = key[2]
+        out["token"].append(tok)
+        out["parent"].append(pos[path[:-1]] if len(path) > 1 else -1)
+        out["depth"].append(key[1])
+        out["score"].append(s)
+        out["rank"].append(path[-1])
+    return {
+        "token": np.asarray(out["token"], dtype=np.int32),
+        "parent": np.asarray(out["parent"], dtype=np.int32),
+        "depth": np.asarray(out["depth"], dtype=np.int32),
+        "score": np.asarray(out["score"], dtype=np.float32),
+        "rank": np.asarray(out["rank"], dtype=np.int32),
+    }
