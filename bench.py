@@ -294,6 +294,25 @@ def main():
     trees_per_s = b * args.steps / elapsed
     rows = b * R
 
+    # the marginal baseline (DDTree: stage 1 with K = min(B, V), marginal tree) on the
+    # same workload and weight rotation, for the cost of AR-approximation
+    md = binding.MarginalDrafter(copies[0]["lm_head"], b, w.gamma, w.B, w.inv_temperature)
+    for i in range(args.warmup):
+        md.step(h, copies[i % len(copies)]["lm_head"])
+    mevs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(args.steps):
+        mevs[i][0].record()
+        md.step(h, copies[i % len(copies)]["lm_head"])
+        mevs[i][1].record()
+    torch.cuda.synchronize()
+    m_elapsed = time.perf_counter() - t1
+    ddtree = {"trees_per_s": b * args.steps / m_elapsed, "ms_per_step": 1000.0 * m_elapsed / args.steps,
+              "gpu_us_per_step": 1000.0 * sum(e[0].elapsed_time(e[1]) for e in mevs) / args.steps,
+              "K": md.K, "what": "stage 1 with K = min(B, V) entries per depth + marginal OPT-Tree"}
+    del md
+
     # dominant kernel: the stage-2 LM-head GEMM (the per-row merge is a separate kernel);
     # algorithmic bytes per launch: lm_head [V, d] once plus the activation rows h' [rows, d]
     es = 2 if w.dtype == "bf16" else 4
@@ -328,6 +347,7 @@ def main():
         "stage_us": stage_us,
         "step_hbm_frac": step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": roof,
+        "ddtree_baseline": ddtree,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, copies[0], st, args.cpu_seconds)

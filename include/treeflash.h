@@ -177,6 +177,28 @@ tf_status_t treeflash_build_tree(const int32_t *cond_idx, const float *cond_logp
                                  float *node_score, int32_t *node_child_row,
                                  hipStream_t stream);
 
+/* The marginal OPT-Tree (the paper's DDTree comparison, Related Work;
+ * Appendix C): the same best-first selection on the drafter's marginal
+ * distributions alone.  Every node above depth gamma expands into the
+ * marginal row of the next depth, so all paths share one child ranking.
+ * Needs no workspace.
+ *   marg_idx, marg_logprob  [b, gamma, K] stage-1 lists from
+ *                           treeflash_marginal_topk with k = K (row i-1 is
+ *                           depth i, sorted by log-prob desc, id asc)
+ *   K                       list length, 1 <= K <= 4096; K >= min(B, V) gives
+ *                           the tree of full rows
+ *   B                       1 <= B <= 4095 and B <= K + K^2 + ... + K^gamma;
+ *                           TF_ERR_UNSUPPORTED past the kernel's LDS, as for
+ *                           treeflash_build_tree
+ * Outputs as for treeflash_build_tree; node_child_row is the row a node
+ * expands into (its depth, 0-based row of depth+1) or -1 at depth gamma.
+ * Ties: as for treeflash_build_tree. */
+tf_status_t treeflash_build_tree_marginal(const int32_t *marg_idx, const float *marg_logprob,
+                                          int b, int gamma, int K, int B,
+                                          int32_t *node_token, int32_t *node_parent,
+                                          int32_t *node_depth, float *node_score,
+                                          int32_t *node_child_row, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *treeflash_status_string(tf_status_t status);
 

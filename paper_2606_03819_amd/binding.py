@@ -21,7 +21,7 @@ TF_F32, TF_BF16 = 0, 1
 STATUS = {0: "TF_OK", 1: "TF_ERR_INVALID_ARG", 2: "TF_ERR_UNSUPPORTED", 3: "TF_ERR_WORKSPACE", 4: "TF_ERR_HIP"}
 EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_marginal_topk_timed",
             "treeflash_arapprox_hidden", "treeflash_arapprox_expand", "treeflash_build_tree",
-            "treeflash_status_string")
+            "treeflash_build_tree_marginal", "treeflash_status_string")
 
 _lib = None
 
@@ -54,6 +54,8 @@ def lib() -> ctypes.CDLL:
     L.treeflash_arapprox_expand.restype = I
     L.treeflash_build_tree.argtypes = [P, P, P, I, I, I, I, I, P, P, P, P, P, P]
     L.treeflash_build_tree.restype = I
+    L.treeflash_build_tree_marginal.argtypes = [P, P, I, I, I, I, P, P, P, P, P, P]
+    L.treeflash_build_tree_marginal.restype = I
     L.treeflash_status_string.argtypes = [I]
     L.treeflash_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -218,6 +220,57 @@ def treeflash_build_tree(cond_idx, cond_logprob, topk_idx, B: int, out: Optional
         _ptr(out.get("child_row"), "child_row", torch.int32, dev), _stream(dev))
     _check("treeflash_build_tree", st)
     return out
+
+
+def _tree_buffers(b: int, B: int, dev) -> Dict[str, torch.Tensor]:
+    return {
+        "token": torch.empty((b, B), dtype=torch.int32, device=dev),
+        "parent": torch.empty((b, B), dtype=torch.int32, device=dev),
+        "depth": torch.empty((b, B), dtype=torch.int32, device=dev),
+        "score": torch.empty((b, B), dtype=torch.float32, device=dev),
+        "child_row": torch.empty((b, B), dtype=torch.int32, device=dev),
+    }
+
+
+def treeflash_build_tree_marginal(marg_idx, marg_logprob, B: int, out: Optional[Dict[str, torch.Tensor]] = None):
+    """Marginal OPT-Tree (the DDTree baseline) from stage-1 lists [b, gamma, K]."""
+    b, gamma, K = marg_idx.shape
+    dev = marg_idx.device
+    if out is None:
+        out = _tree_buffers(b, B, dev)
+    st = lib().treeflash_build_tree_marginal(
+        _ptr(marg_idx, "marg_idx", torch.int32, dev), _ptr(marg_logprob, "marg_logprob", torch.float32, dev),
+        b, gamma, K, B, _ptr(out["token"], "token", torch.int32, dev),
+        _ptr(out["parent"], "parent", torch.int32, dev), _ptr(out["depth"], "depth", torch.int32, dev),
+        _ptr(out["score"], "score", torch.float32, dev), _ptr(out.get("child_row"), "child_row", torch.int32, dev),
+        _stream(dev))
+    _check("treeflash_build_tree_marginal", st)
+    return out
+
+
+class MarginalDrafter:
+    """The marginal baseline over resident weights: stage 1 with K = min(B, V)
+    entries per depth, then the marginal OPT-Tree.  Allocates nothing per step."""
+
+    def __init__(self, lm_head: torch.Tensor, b: int, gamma: int, B: int, inv_temperature: float = 1.0):
+        self.lm_head = lm_head
+        self.dev = lm_head.device
+        self.V, self.d = lm_head.shape
+        self.b, self.gamma, self.B = b, gamma, B
+        self.K = min(B, self.V)
+        self.inv_t = inv_temperature
+        nbytes = treeflash_workspace_bytes(b, gamma, self.d, 16, self.V, self.K, self.K, lm_head.dtype)
+        if nbytes == 0:
+            raise ValueError("invalid drafting shapes")
+        self.workspace = alloc_workspace(nbytes, self.dev)
+        self.idx = torch.empty((b, gamma, self.K), dtype=torch.int32, device=self.dev)
+        self.lp = torch.empty((b, gamma, self.K), dtype=torch.float32, device=self.dev)
+        self.tree = _tree_buffers(b, B, self.dev)
+
+    def step(self, h, lm_head=None):
+        treeflash_marginal_topk(h, self.lm_head if lm_head is None else lm_head, self.K, self.inv_t,
+                                self.workspace, self.idx, self.lp)
+        return treeflash_build_tree_marginal(self.idx, self.lp, self.B, self.tree)
 
 
 class Drafter:

@@ -7,10 +7,6 @@
 #include "launch.hpp"
 #include "plan.hpp"
 
-namespace tf {
-size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks);
-}
-
 namespace {
 
 using namespace tf;
@@ -192,7 +188,34 @@ tf_status_t treeflash_build_tree(const int32_t* cond_idx, const float* cond_logp
         if (!aligned4(p)) return TF_ERR_INVALID_ARG;
     if (node_child_row != nullptr && !aligned4(node_child_row)) return TF_ERR_INVALID_ARG;
     if (tree_lds_bytes(B, gamma, k, (int)Rs, topk2, nullptr) == 0) return TF_ERR_UNSUPPORTED;
-    const hipError_t e = launch_build_tree(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, node_token,
+    const hipError_t e = launch_build_tree(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, false,
+                                           node_token, node_parent, node_depth, node_score, node_child_row, stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+tf_status_t treeflash_build_tree_marginal(const int32_t* marg_idx, const float* marg_logprob, int b, int gamma,
+                                          int K, int B, int32_t* node_token, int32_t* node_parent,
+                                          int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                                          hipStream_t stream) {
+    if (marg_idx == nullptr || marg_logprob == nullptr || node_token == nullptr || node_parent == nullptr ||
+        node_depth == nullptr || node_score == nullptr)
+        return TF_ERR_INVALID_ARG;
+    if (b < 1 || gamma < 1 || gamma > 255 || K < 1 || K > 4096 || B < 1 || B > kMaxBudget)
+        return TF_ERR_INVALID_ARG;
+    if ((long long)b * gamma > kMaxRows) return TF_ERR_INVALID_ARG;
+    // every path of length 1..gamma over the rows is a node: K + K^2 + ... + K^gamma of them
+    long long cap = 0, pw = K;
+    for (int j = 0; j < gamma && cap < B; ++j) {
+        cap += pw;
+        pw = pw * K > (1ll << 40) ? (1ll << 40) : pw * K;
+    }
+    if (cap < B) return TF_ERR_INVALID_ARG;
+    const void* ptrs[] = {marg_idx, marg_logprob, node_token, node_parent, node_depth, node_score};
+    for (const void* p : ptrs)
+        if (!aligned4(p)) return TF_ERR_INVALID_ARG;
+    if (node_child_row != nullptr && !aligned4(node_child_row)) return TF_ERR_INVALID_ARG;
+    if (tree_lds_bytes(B, gamma, 0, gamma, K, nullptr) == 0) return TF_ERR_UNSUPPORTED;
+    const hipError_t e = launch_build_tree(marg_idx, marg_logprob, nullptr, b, gamma, 0, K, B, true, node_token,
                                            node_parent, node_depth, node_score, node_child_row, stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }

@@ -22,10 +22,13 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
                            bool bf16, void* ht, void* et, void* act, void* hp, float* mlp_partial, int* counters,
                            int* diag, hipStream_t stream);
 
-// Best-first tree selection, one workgroup per sequence.
+// Best-first tree selection, one workgroup per sequence.  `marginal`: the
+// rows are the gamma marginal rows [b, gamma, topk2] and every node above
+// depth gamma expands into the next depth's row (topk_idx and k unused).
 hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, const int32_t* topk_idx, int b,
-                             int gamma, int k, int topk2, int B, int32_t* node_token, int32_t* node_parent,
-                             int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                             int gamma, int k, int topk2, int B, bool marginal, int32_t* node_token,
+                             int32_t* node_parent, int32_t* node_depth, float* node_score, int32_t* node_child_row,
                              hipStream_t stream);
+size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks);
 
 }  // namespace tf

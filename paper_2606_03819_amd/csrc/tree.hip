@@ -36,6 +36,7 @@ struct TreeArgs {
     const float* cond_lp;
     const int32_t* topk;
     int gamma, M, K2, B, Rs, P;   // P = leading ranks of each row cached in LDS
+    int marginal;                 // 1: rows are the gamma marginal rows, every node above depth gamma expands
     int32_t* tok;
     int32_t* par;
     int32_t* dep;
@@ -114,7 +115,8 @@ __device__ __forceinline__ void tree_preload(const TreeArgs& a, const TreeLds& t
                                              const int32_t* ridx) {
     const int tid = threadIdx.x;
     for (int s = tid; s <= a.B; s += kTreeThreads) t.f_depth[s] = 0;
-    for (int e = tid; e < a.gamma * a.M; e += kTreeThreads) t.tk[e] = a.topk[(size_t)seq * a.gamma * a.M + e];
+    if (!a.marginal)
+        for (int e = tid; e < a.gamma * a.M; e += kTreeThreads) t.tk[e] = a.topk[(size_t)seq * a.gamma * a.M + e];
     const int ncache = a.Rs * a.P;
     for (int e0 = tid; e0 < ncache; e0 += 4 * kTreeThreads) {
         float lp[4];
@@ -139,9 +141,11 @@ __device__ __forceinline__ void tree_preload(const TreeArgs& a, const TreeLds& t
 }
 
 // Child row of a popped node: 1 + (depth-1)*M + m if its token is candidate m
-// of its depth, else -1 (uniform across the wave).
+// of its depth, else -1; in marginal mode the marginal row of the next depth
+// (row `depth`) for every node above depth gamma.  Uniform across the wave.
 __device__ __forceinline__ int tree_child_row(const TreeArgs& a, const TreeLds& t, int depth, int tok, int lane) {
     if (depth >= a.gamma) return -1;
+    if (a.marginal) return depth;
     for (int m0 = 0; m0 < a.M; m0 += 64) {
         const int m = m0 + lane;
         const bool hit = m < a.M && t.tk[(depth - 1) * a.M + m] == tok;
@@ -376,14 +380,15 @@ size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks
 }
 
 hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, const int32_t* topk_idx, int b,
-                             int gamma, int k, int topk2, int B, int32_t* node_token, int32_t* node_parent,
-                             int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                             int gamma, int k, int topk2, int B, bool marginal, int32_t* node_token,
+                             int32_t* node_parent, int32_t* node_depth, float* node_score, int32_t* node_child_row,
                              hipStream_t stream) {
-    const int Rs = 1 + (gamma - 1) * k;
+    const int M = marginal ? 0 : k;
+    const int Rs = marginal ? gamma : 1 + (gamma - 1) * k;
     int P = 0;
-    const size_t lds = tree_lds_bytes(B, gamma, k, Rs, topk2, &P);
+    const size_t lds = tree_lds_bytes(B, gamma, M, Rs, topk2, &P);
     if (lds == 0) return hipErrorInvalidValue;
-    TreeArgs a{cond_idx, cond_lp, topk_idx, gamma, k, topk2, B, Rs, P,
+    TreeArgs a{cond_idx, cond_lp, topk_idx, gamma, M, topk2, B, Rs, P, marginal ? 1 : 0,
                node_token, node_parent, node_depth, node_score, node_child_row};
     const void* fn;
     if (B + 1 <= 64)

@@ -155,3 +155,23 @@ def test_binding_refuses_cpu_tensors():
                                         workspace=torch.zeros(1 << 16, dtype=torch.uint8),
                                         topk_idx=torch.zeros(1, 2, 2, dtype=torch.int32),
                                         topk_logprob=torch.zeros(1, 2, 2))
+
+
+def _margtree(**over):
+    a = dict(idx=FAKE, lp=FAKE2, b=1, gamma=16, K=32, B=32, tok=FAKE, par=FAKE, dep=FAKE, sc=FAKE2, crow=None,
+             st=None)
+    a.update(over)
+    return binding.lib().treeflash_build_tree_marginal(a["idx"], a["lp"], a["b"], a["gamma"], a["K"], a["B"],
+                                                       a["tok"], a["par"], a["dep"], a["sc"], a["crow"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(idx=None), INVALID), (dict(lp=None), INVALID), (dict(tok=None), INVALID), (dict(sc=None), INVALID),
+    (dict(b=0), INVALID), (dict(gamma=0), INVALID), (dict(gamma=256), INVALID), (dict(K=0), INVALID),
+    (dict(K=5000), INVALID), (dict(B=0), INVALID), (dict(B=4096), INVALID),
+    (dict(gamma=2, K=2, B=7), INVALID),          # only 2 + 4 paths exist
+    (dict(idx=FAKE + 2), INVALID), (dict(crow=FAKE + 1), INVALID),
+    (dict(gamma=200, K=4000, B=4000), UNSUPPORTED),
+])
+def test_build_tree_marginal_rejects(over, code):
+    assert _margtree(**over) == code
