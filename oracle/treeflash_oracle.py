@@ -20,6 +20,11 @@ Part 2 -- OPT-Tree selection
   * best-first pops of the candidate with the highest path probability until
     the tree holds B nodes besides the root; a popped node contributes its
     children only when its token is one of the M candidates of its depth.
+Verification hand-off (Method, "Inference": equality-check verification;
+Experiments, "Metrics": block efficiency)
+  * the tree laid out for a verifier pass with tree attention (root first,
+    positions = depths, ancestor mask) and the greedy acceptance walk that
+    turns the verifier's per-node next tokens into accepted nodes and tau.
 Marginal baseline (the paper's DDTree comparison, Related Work and Appendix C)
   * the same selection on the marginal distributions alone: every node above
     the last depth expands into the marginal row of the next depth, so all
@@ -50,7 +55,8 @@ import numpy as np
 __all__ = [
     "bf16_round", "rms_norm", "silu", "log_softmax", "topk_sorted",
     "marginal_stage", "row_table", "previous_tokens", "ar_approximator",
-    "conditional_stage", "build_tree", "draft", "build_marginal_tree", "draft_marginal", "RMS_EPS",
+    "conditional_stage", "build_tree", "draft", "build_marginal_tree", "draft_marginal",
+    "verification_inputs", "acceptance_walk", "RMS_EPS",
 ]
 
 RMS_EPS = 1e-6
@@ -371,3 +377,55 @@ def draft_marginal(inputs: Dict[str, np.ndarray], gamma: int, B: int, inv_temper
         out["stage1"].append(st1)
         out["tree"].append(tree)
     return out
+
+
+# ------------------------------------------------------- verification hand-off
+
+def verification_inputs(root_token: int, token: np.ndarray, parent: np.ndarray,
+                        depth: np.ndarray) -> Dict[str, np.ndarray]:
+    """The draft tree as one verifier input with tree attention.
+
+    Position 0 is the root token x_t; position 1 + j is node j of the tree (pop
+    order).  Returns tokens [B+1], positions [B+1] (the depth: 0 for the root)
+    and mask [B+1, B+1] (bool): mask[i, j] is true when position j is position
+    i or one of its ancestors, i.e. the tokens position i may attend to.
+    """
+    B = len(token)
+    tokens = np.concatenate([[root_token], np.asarray(token)]).astype(np.int32)
+    positions = np.concatenate([[0], np.asarray(depth)]).astype(np.int32)
+    mask = np.zeros((B + 1, B + 1), dtype=bool)
+    mask[0, 0] = True
+    for j in range(B):
+        i = 1 + j
+        mask[i, i] = True
+        mask[i, 0] = True
+        p = int(parent[j])
+        while p >= 0:
+            mask[i, 1 + p] = True
+            p = int(parent[p])
+    return {"tokens": tokens, "positions": positions, "mask": mask}
+
+
+def acceptance_walk(token: np.ndarray, parent: np.ndarray, target: np.ndarray) -> Dict[str, object]:
+    """Greedy equality verification of one draft tree.
+
+    target[0] is the verifier's next token after the root, target[1 + j] its
+    next token after the path ending at node j.  From the root, move to the
+    child whose token equals the current position's target, as long as there
+    is one (siblings carry distinct tokens).  Returns the accepted node ids in
+    order, tau = accepted + 1 (the verifier's own next token after the last
+    accepted node is always gained) and that bonus token.
+    """
+    token = np.asarray(token)
+    parent = np.asarray(parent)
+    accepted: List[int] = []
+    cur = -1
+    while True:
+        want = int(target[1 + cur])
+        hit = [j for j in range(len(token)) if parent[j] == cur and token[j] == want]
+        if not hit:
+            break
+        cur = hit[0]
+        accepted.append(cur)
+    return {"accepted": accepted, "tau": len(accepted) + 1, "bonus": int(target[1 + cur])}
+
