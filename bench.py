@@ -294,6 +294,36 @@ def main():
     trees_per_s = b * args.steps / elapsed
     rows = b * R
 
+    # verification hand-off on the last step's trees: tree-attention inputs and the
+    # acceptance walk for a synthetic verifier that agrees with the drafter's best
+    # child at every position (so tau is the depth of the greedy path + 1)
+    tree_cpu = {f: dr.tree[f].cpu() for f in ("token", "parent")}
+    target = torch.full((b, w.B + 1), -1, dtype=torch.int32)
+    for s in range(b):
+        seen = set()
+        for j in range(w.B):
+            p = int(tree_cpu["parent"][s, j])
+            if p not in seen:
+                seen.add(p)
+                target[s, p + 1] = tree_cpu["token"][s, j]
+    target = target.to(dev)
+    vi = binding.treeflash_tree_attention_inputs(root, dr.tree)
+    acc = binding.treeflash_accept(dr.tree, target, w.gamma)
+    vevs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        vevs[i][0].record()
+        binding.treeflash_tree_attention_inputs(root, dr.tree, vi)
+        vevs[i][1].record()
+        binding.treeflash_accept(dr.tree, target, w.gamma, acc)
+        vevs[i][2].record()
+    torch.cuda.synchronize()
+    handoff = {"tree_attention_inputs_us": 1000.0 * sum(e[0].elapsed_time(e[1]) for e in vevs) / args.steps,
+               "accept_us": 1000.0 * sum(e[1].elapsed_time(e[2]) for e in vevs) / args.steps,
+               "tau_greedy_verifier": float(acc["accept_len"].float().mean().item()) + 1.0,
+               "what": "verifier input (tokens, positions, ancestor mask) and the greedy acceptance walk; "
+                       "synthetic verifier = the drafter's best child at every position"}
+
     # the marginal baseline (DDTree: stage 1 with K = min(B, V), marginal tree) on the
     # same workload and weight rotation, for the cost of AR-approximation
     md = binding.MarginalDrafter(copies[0]["lm_head"], b, w.gamma, w.B, w.inv_temperature)
@@ -348,6 +378,7 @@ def main():
         "step_hbm_frac": step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": roof,
         "ddtree_baseline": ddtree,
+        "verify_handoff": handoff,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, copies[0], st, args.cpu_seconds)

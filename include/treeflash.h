@@ -199,6 +199,45 @@ tf_status_t treeflash_build_tree_marginal(const int32_t *marg_idx, const float *
                                           int32_t *node_depth, float *node_score,
                                           int32_t *node_child_row, hipStream_t stream);
 
+/* Verification hand-off, part 1 (Method, "Inference": the draft is verified
+ * in one verifier pass with tree attention and an equality check): the tree
+ * as that pass's input.  Position 0 is the root token x_t, position 1 + j is
+ * node j of the tree (pop order, as produced by treeflash_build_tree or
+ * treeflash_build_tree_marginal).  Needs no workspace.
+ *   root_token      [b] int32
+ *   node_token, node_parent, node_depth  [b, B] int32 (a parent precedes its
+ *                   child; parent -1 = the root)
+ *   tokens          out [b, B+1] int32: root token, then the node tokens
+ *   positions       out [b, B+1] int32: depth of each position (root 0); add
+ *                   the root's sequence position for absolute positions
+ *   mask            out [b, B+1, B+1] uint8: mask[i][j] = 1 when position j
+ *                   is position i or one of its ancestors (what i attends to
+ *                   inside the tree), else 0
+ * Requirements: 1 <= B <= 4095; int32 arrays 4-byte aligned. */
+tf_status_t treeflash_tree_attention_inputs(const int32_t *root_token, const int32_t *node_token,
+                                            const int32_t *node_parent, const int32_t *node_depth,
+                                            int b, int B, int32_t *tokens, int32_t *positions,
+                                            uint8_t *mask, hipStream_t stream);
+
+/* Verification hand-off, part 2 (Method, "Inference"; Experiments, "Metrics":
+ * block efficiency tau = accepted tokens + the verifier's residual token):
+ * the greedy equality walk.  Needs no workspace.
+ *   node_token, node_parent  [b, B] int32, as above
+ *   target          [b, B+1] int32: the verifier's next token at every
+ *                   position of the tree input above (position 0 = after the
+ *                   root)
+ *   gamma           longest acceptable path (the draft depth), 1..255
+ *   accepted        out [b, gamma] int32: accepted node ids, root to leaf,
+ *                   then -1
+ *   accept_len      out [b] int32: number of accepted nodes; tau = accept_len + 1
+ *   bonus           out [b] int32: the verifier's token after the last
+ *                   accepted node (the residual token)
+ * From the root, the walk moves to the child whose token equals the current
+ * position's target while there is one (siblings carry distinct tokens). */
+tf_status_t treeflash_accept(const int32_t *node_token, const int32_t *node_parent, const int32_t *target,
+                             int b, int B, int gamma, int32_t *accepted, int32_t *accept_len,
+                             int32_t *bonus, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *treeflash_status_string(tf_status_t status);
 

@@ -21,7 +21,8 @@ TF_F32, TF_BF16 = 0, 1
 STATUS = {0: "TF_OK", 1: "TF_ERR_INVALID_ARG", 2: "TF_ERR_UNSUPPORTED", 3: "TF_ERR_WORKSPACE", 4: "TF_ERR_HIP"}
 EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_marginal_topk_timed",
             "treeflash_arapprox_hidden", "treeflash_arapprox_expand", "treeflash_build_tree",
-            "treeflash_build_tree_marginal", "treeflash_status_string")
+            "treeflash_build_tree_marginal", "treeflash_tree_attention_inputs", "treeflash_accept",
+            "treeflash_status_string")
 
 _lib = None
 
@@ -56,6 +57,10 @@ def lib() -> ctypes.CDLL:
     L.treeflash_build_tree.restype = I
     L.treeflash_build_tree_marginal.argtypes = [P, P, I, I, I, I, P, P, P, P, P, P]
     L.treeflash_build_tree_marginal.restype = I
+    L.treeflash_tree_attention_inputs.argtypes = [P, P, P, P, I, I, P, P, P, P]
+    L.treeflash_tree_attention_inputs.restype = I
+    L.treeflash_accept.argtypes = [P, P, P, I, I, I, P, P, P, P]
+    L.treeflash_accept.restype = I
     L.treeflash_status_string.argtypes = [I]
     L.treeflash_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -245,6 +250,42 @@ def treeflash_build_tree_marginal(marg_idx, marg_logprob, B: int, out: Optional[
         _ptr(out["score"], "score", torch.float32, dev), _ptr(out.get("child_row"), "child_row", torch.int32, dev),
         _stream(dev))
     _check("treeflash_build_tree_marginal", st)
+    return out
+
+
+def treeflash_tree_attention_inputs(root_token, tree: Dict[str, torch.Tensor], out: Optional[dict] = None):
+    """Verifier input of each draft tree: tokens, positions [b, B+1], ancestor mask [b, B+1, B+1] (uint8)."""
+    b, B = tree["token"].shape
+    dev = tree["token"].device
+    if out is None:
+        out = {"tokens": torch.empty((b, B + 1), dtype=torch.int32, device=dev),
+               "positions": torch.empty((b, B + 1), dtype=torch.int32, device=dev),
+               "mask": torch.empty((b, B + 1, B + 1), dtype=torch.uint8, device=dev)}
+    st = lib().treeflash_tree_attention_inputs(
+        _ptr(root_token, "root_token", torch.int32, dev), _ptr(tree["token"], "token", torch.int32, dev),
+        _ptr(tree["parent"], "parent", torch.int32, dev), _ptr(tree["depth"], "depth", torch.int32, dev), b, B,
+        _ptr(out["tokens"], "tokens", torch.int32, dev), _ptr(out["positions"], "positions", torch.int32, dev),
+        _ptr(out["mask"], "mask", torch.uint8, dev), _stream(dev))
+    _check("treeflash_tree_attention_inputs", st)
+    return out
+
+
+def treeflash_accept(tree: Dict[str, torch.Tensor], target: torch.Tensor, gamma: int, out: Optional[dict] = None):
+    """Greedy equality walk given the verifier's next token at every position [b, B+1]."""
+    b, B = tree["token"].shape
+    dev = tree["token"].device
+    if target.shape != (b, B + 1):
+        raise ValueError("target must be [b, B+1]")
+    if out is None:
+        out = {"accepted": torch.empty((b, gamma), dtype=torch.int32, device=dev),
+               "accept_len": torch.empty((b,), dtype=torch.int32, device=dev),
+               "bonus": torch.empty((b,), dtype=torch.int32, device=dev)}
+    st = lib().treeflash_accept(
+        _ptr(tree["token"], "token", torch.int32, dev), _ptr(tree["parent"], "parent", torch.int32, dev),
+        _ptr(target, "target", torch.int32, dev), b, B, gamma,
+        _ptr(out["accepted"], "accepted", torch.int32, dev), _ptr(out["accept_len"], "accept_len", torch.int32, dev),
+        _ptr(out["bonus"], "bonus", torch.int32, dev), _stream(dev))
+    _check("treeflash_accept", st)
     return out
 
 

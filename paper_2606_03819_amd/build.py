@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_NAME = "libtreeflash.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["lmhead.hip", "mlp.hip", "tree.hip", "api.cpp"]
+SOURCES = ["lmhead.hip", "mlp.hip", "tree.hip", "verify.hip", "api.cpp"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

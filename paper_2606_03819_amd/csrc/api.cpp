@@ -220,6 +220,37 @@ tf_status_t treeflash_build_tree_marginal(const int32_t* marg_idx, const float* 
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
+tf_status_t treeflash_tree_attention_inputs(const int32_t* root_token, const int32_t* node_token,
+                                            const int32_t* node_parent, const int32_t* node_depth, int b, int B,
+                                            int32_t* tokens, int32_t* positions, uint8_t* mask,
+                                            hipStream_t stream) {
+    if (root_token == nullptr || node_token == nullptr || node_parent == nullptr || node_depth == nullptr ||
+        tokens == nullptr || positions == nullptr || mask == nullptr)
+        return TF_ERR_INVALID_ARG;
+    if (b < 1 || B < 1 || B > kMaxBudget || (long long)b * (B + 1) * (B + 1) > (1ll << 40)) return TF_ERR_INVALID_ARG;
+    const void* ptrs[] = {root_token, node_token, node_parent, node_depth, tokens, positions};
+    for (const void* p : ptrs)
+        if (!aligned4(p)) return TF_ERR_INVALID_ARG;
+    const hipError_t e = launch_tree_inputs(root_token, node_token, node_parent, node_depth, b, B, tokens,
+                                            positions, mask, stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+tf_status_t treeflash_accept(const int32_t* node_token, const int32_t* node_parent, const int32_t* target, int b,
+                             int B, int gamma, int32_t* accepted, int32_t* accept_len, int32_t* bonus,
+                             hipStream_t stream) {
+    if (node_token == nullptr || node_parent == nullptr || target == nullptr || accepted == nullptr ||
+        accept_len == nullptr || bonus == nullptr)
+        return TF_ERR_INVALID_ARG;
+    if (b < 1 || B < 1 || B > kMaxBudget || gamma < 1 || gamma > 255) return TF_ERR_INVALID_ARG;
+    const void* ptrs[] = {node_token, node_parent, target, accepted, accept_len, bonus};
+    for (const void* p : ptrs)
+        if (!aligned4(p)) return TF_ERR_INVALID_ARG;
+    const hipError_t e = launch_accept(node_token, node_parent, target, b, B, gamma, accepted, accept_len, bonus,
+                                       stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
 const char* treeflash_status_string(tf_status_t status) {
     switch (status) {
         case TF_OK: return "success";

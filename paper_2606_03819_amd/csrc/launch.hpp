@@ -31,4 +31,15 @@ hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, cons
                              hipStream_t stream);
 size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks);
 
+// Verifier input of a draft tree: tokens and positions [b, B+1], ancestor
+// mask [b, B+1, B+1] (uint8).
+hipError_t launch_tree_inputs(const int32_t* root_token, const int32_t* node_token, const int32_t* node_parent,
+                              const int32_t* node_depth, int b, int B, int32_t* tokens, int32_t* positions,
+                              uint8_t* mask, hipStream_t stream);
+
+// Greedy acceptance walk: accepted node ids [b, max_depth], lengths and the
+// verifier's bonus token per sequence.
+hipError_t launch_accept(const int32_t* node_token, const int32_t* node_parent, const int32_t* target, int b, int B,
+                         int max_depth, int32_t* accepted, int32_t* accept_len, int32_t* bonus, hipStream_t stream);
+
 }  // namespace tf

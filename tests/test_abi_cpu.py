@@ -175,3 +175,35 @@ def _margtree(**over):
 ])
 def test_build_tree_marginal_rejects(over, code):
     assert _margtree(**over) == code
+
+
+def _attn(**over):
+    a = dict(root=FAKE, tok=FAKE, par=FAKE, dep=FAKE, b=1, B=32, otok=FAKE2, opos=FAKE2, mask=FAKE2, st=None)
+    a.update(over)
+    return binding.lib().treeflash_tree_attention_inputs(a["root"], a["tok"], a["par"], a["dep"], a["b"], a["B"],
+                                                         a["otok"], a["opos"], a["mask"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(root=None), INVALID), (dict(tok=None), INVALID), (dict(par=None), INVALID), (dict(dep=None), INVALID),
+    (dict(otok=None), INVALID), (dict(mask=None), INVALID), (dict(b=0), INVALID), (dict(B=0), INVALID),
+    (dict(B=4096), INVALID), (dict(par=FAKE + 2), INVALID), (dict(opos=FAKE2 + 1), INVALID),
+])
+def test_tree_attention_inputs_rejects(over, code):
+    assert _attn(**over) == code
+
+
+def _accept(**over):
+    a = dict(tok=FAKE, par=FAKE, tgt=FAKE, b=1, B=32, gamma=16, acc=FAKE2, alen=FAKE2, bonus=FAKE2, st=None)
+    a.update(over)
+    return binding.lib().treeflash_accept(a["tok"], a["par"], a["tgt"], a["b"], a["B"], a["gamma"], a["acc"],
+                                          a["alen"], a["bonus"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(tok=None), INVALID), (dict(tgt=None), INVALID), (dict(acc=None), INVALID), (dict(bonus=None), INVALID),
+    (dict(b=0), INVALID), (dict(B=0), INVALID), (dict(B=5000), INVALID), (dict(gamma=0), INVALID),
+    (dict(gamma=256), INVALID), (dict(tgt=FAKE + 2), INVALID),
+])
+def test_accept_rejects(over, code):
+    assert _accept(**over) == code
