@@ -100,6 +100,9 @@ def parse():
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the HBM traffic summary from FETCH_SIZE and WRITE_SIZE rocprofv3 runs")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
+    ap.add_argument("--sweep", action="store_true",
+                    help="drafting cost over budgets B = 16..512 (M = 8) and branchings M = 4..64 (B = 32) "
+                         "at the workload's shape; prints one JSON line of its own")
     return ap.parse_args()
 
 
@@ -210,6 +213,63 @@ def summarize_pmc(args):
     print("```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
+def time_steps(w, copies, h, root, steps, warmup):
+    """Mean GPU time per stage of the drafting step for workload w (events around each call)."""
+    dev = torch.device("cuda", 0)
+    dr = binding.Drafter(copies[0], w.b, w.gamma, w.k, w.B, w.inv_temperature)
+    hp = torch.empty((w.b, w.rows, w.d), dtype=w.torch_dtype, device=dev)
+
+    def step(i, ev=None):
+        wt = copies[i % len(copies)]
+        if ev is not None:
+            ev[0].record()
+        binding.treeflash_marginal_topk(h, wt["lm_head"], w.k, w.inv_temperature, dr.workspace, dr.topk_idx,
+                                        dr.topk_lp)
+        if ev is not None:
+            ev[1].record()
+        binding.treeflash_arapprox_hidden(h, root, dr.topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
+                                          wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, dr.workspace, hp, w.V)
+        if ev is not None:
+            ev[2].record()
+        binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
+                                        dr.cond_idx, dr.cond_lp, dr.cond_lse)
+        if ev is not None:
+            ev[3].record()
+        binding.treeflash_build_tree(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
+        if ev is not None:
+            ev[4].record()
+
+    for i in range(warmup):
+        step(i)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    names = ["stage1_lmhead_topk", "arapprox_mlp", "stage2_lmhead_topk", "tree"]
+    us = {n: 1000.0 * sum(e[j].elapsed_time(e[j + 1]) for e in evs) / steps for j, n in enumerate(names)}
+    us["step"] = sum(us.values())
+    return us
+
+
+def sweep(args):
+    """Drafting cost over budgets and branchings at the workload's shape (the paper's
+    B and M sweeps, as a systems curve)."""
+    base = synth.get_workload(args.workload)
+    copies, st = make_copies(base, max(1, args.copies))
+    h, root = st["h"], st["root"]
+    out = []
+    points = [("B", B, base.replace(name=f"{base.name}-B{B}", B=B)) for B in (16, 32, 64, 128, 256, 512)]
+    points += [("M", M, base.replace(name=f"{base.name}-M{M}", k=M)) for M in (4, 8, 16, 32, 64)]
+    for axis, val, w in points:
+        us = time_steps(w, copies, h, root, args.steps, args.warmup)
+        out.append({"axis": axis, "value": val, "B": w.B, "M": w.k, "conditional_rows": w.rows * w.b,
+                    "trees_per_s": w.b * 1e6 / us["step"], "stage_us": us})
+    print(json.dumps({"metric": "drafting cost over draft budget B and branching M", "unit": "us",
+                      "workload": base.name, "steps": args.steps, "warmup": args.warmup, "sweep": out}),
+          flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_trace:
@@ -225,9 +285,12 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(2)
-    w = synth.get_workload(args.workload)
     torch.cuda.set_device(0)
     binding.lib()
+    if args.sweep:
+        sweep(args)
+        return
+    w = synth.get_workload(args.workload)
     copies, st = make_copies(w, max(1, args.copies))
     dev = torch.device("cuda", 0)
     d, V, R, b = w.d, w.V, w.rows, w.b

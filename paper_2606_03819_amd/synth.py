@@ -89,6 +89,11 @@ WORKLOADS: Dict[str, Workload] = {
                  "Qwen3-8B-shaped bf16, batch 1, M=16 candidates, budget 64"),
         Workload("qwen3-8b-shape-batch16", 16, 4096, 151936, 16, 8, 32, 4096, "bf16", 1.0, 3, 1500,
                  "Qwen3-8B-shaped bf16, 16 independent sequences: MFMA-bound"),
+        # ends of the budget and branching sweeps (drafting cost only)
+        Workload("qwen3-8b-shape-b512", 1, 4096, 151936, 16, 8, 512, 4096, "bf16", 1.0, 3, 13,
+                 "Qwen3-8B-shaped bf16, batch 1, budget 512 (512-entry stage-2 lists)"),
+        Workload("qwen3-8b-shape-m64", 1, 4096, 151936, 16, 64, 32, 4096, "bf16", 1.0, 3, 13,
+                 "Qwen3-8B-shaped bf16, batch 1, M=64 candidates (961 conditional rows)"),
     ]
 }
 
