@@ -56,7 +56,7 @@ __all__ = [
     "bf16_round", "rms_norm", "silu", "log_softmax", "topk_sorted",
     "marginal_stage", "row_table", "previous_tokens", "ar_approximator",
     "conditional_stage", "build_tree", "draft", "build_marginal_tree", "draft_marginal",
-    "verification_inputs", "acceptance_walk", "RMS_EPS",
+    "verification_inputs", "acceptance_walk", "ar_approximator_linear", "RMS_EPS",
 ]
 
 RMS_EPS = 1e-6
@@ -182,6 +182,26 @@ def ar_approximator(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
     if mirror_bf16:
         a = bf16_round(a)
     hp = hd + a @ np.asarray(w_down, dtype=np.float64).T
+    if mirror_bf16:
+        hp = bf16_round(hp)
+    return hp
+
+
+def ar_approximator_linear(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
+                           emb: np.ndarray, norm_h_gain: np.ndarray, norm_e_gain: np.ndarray,
+                           w_lin: np.ndarray, eps: float = RMS_EPS, mirror_bf16: bool = False) -> np.ndarray:
+    """The paper's "w/ Linear" ablation (Ablations, Model Design): the SwiGLU of
+    Eq. 1 replaced by one linear layer on the same normalised input,
+    h'_r = h_{depth_r} + W_lin x_r, x_r = [ rms(h_{depth_r}) ; rms(Embd(prev_r)) ],
+    W_lin [d, 2d] with no bias; its e-half is the previous-token-conditioned
+    shift the paper describes.  With mirror_bf16, x and h' are rounded to bf16.
+    """
+    hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
+    e = np.asarray(emb, dtype=np.float64)[np.asarray(prev)]
+    x = np.concatenate([rms_norm(hd, norm_h_gain, eps), rms_norm(e, norm_e_gain, eps)], axis=-1)
+    if mirror_bf16:
+        x = bf16_round(x)
+    hp = hd + x @ np.asarray(w_lin, dtype=np.float64).T
     if mirror_bf16:
         hp = bf16_round(hp)
     return hp
