@@ -213,6 +213,16 @@ def summarize_pmc(args):
     print("```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
+def approx_hidden(wt, h, root, topk_idx, workspace, hp, V):
+    """Stage 2's first half: Eq. 1's SwiGLU, or the w/ Linear layer when the weights hold one."""
+    if "w_lin" in wt:
+        binding.treeflash_arapprox_linear_hidden(h, root, topk_idx, wt["emb"], wt["norm_h_gain"],
+                                                 wt["norm_e_gain"], wt["w_lin"], 1e-6, workspace, hp, V)
+    else:
+        binding.treeflash_arapprox_hidden(h, root, topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
+                                          wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, workspace, hp, V)
+
+
 def time_steps(w, copies, h, root, steps, warmup):
     """Mean GPU time per stage of the drafting step for workload w (events around each call)."""
     dev = torch.device("cuda", 0)
@@ -227,8 +237,7 @@ def time_steps(w, copies, h, root, steps, warmup):
                                         dr.topk_lp)
         if ev is not None:
             ev[1].record()
-        binding.treeflash_arapprox_hidden(h, root, dr.topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
-                                          wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, dr.workspace, hp, w.V)
+        approx_hidden(wt, h, root, dr.topk_idx, dr.workspace, hp, w.V)
         if ev is not None:
             ev[2].record()
         binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
@@ -306,8 +315,7 @@ def main():
                                         dr.topk_lp)
         if ev is not None:
             ev[1].record()
-        binding.treeflash_arapprox_hidden(h, root, dr.topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
-                                          wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, dr.workspace, hp, V)
+        approx_hidden(wt, h, root, dr.topk_idx, dr.workspace, hp, V)
         if ev is not None:
             ev[2].record()
         binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
@@ -427,14 +435,14 @@ def main():
     roof["mfma_frac"] = alg_flops / t_lm / 1e12 / BF16_PEAK_TFLOPS
 
     # whole-step roofline context
-    mlp_bytes = (2 * w.I * 2 * d + d * w.I) * es
+    mlp_bytes = (2 * d * d if w.approximator == "linear" else 2 * w.I * 2 * d + d * w.I) * es
     step_bytes = 2 * V * d * es + mlp_bytes
     out = {
         "metric": METRIC, "value": trees_per_s, "unit": "trees/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "b": b, "d": d, "V": V, "gamma": w.gamma, "k": w.k, "B": w.B, "I": w.I,
-                   "inv_temperature": w.inv_temperature, "conditional_rows": rows, "gamma_k_b": w.gamma * w.k * b,
+                   "approximator": w.approximator, "inv_temperature": w.inv_temperature, "conditional_rows": rows, "gamma_k_b": w.gamma * w.k * b,
                    "weight_copies": len(copies)},
         "rows_per_s": rows * args.steps / elapsed,
         "stage_us": stage_us,

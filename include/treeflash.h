@@ -119,6 +119,23 @@ tf_status_t treeflash_arapprox_hidden(const void *h, const int32_t *root_token,
                                       void *workspace, size_t workspace_bytes,
                                       hipStream_t stream);
 
+/* The paper's "w/ Linear" ablation (Ablations, Model Design): the SwiGLU of
+ * Eq. 1 replaced by one linear layer on the same normalised input,
+ *   h'_r = h_{depth(r)} + W_lin x_r,  x_r as above,
+ *   w_lin  [d, 2d] (columns 0..d-1 act on the normalised h, d..2d-1 on the
+ *          normalised embedding; no bias)
+ * Other arguments as in treeflash_arapprox_hidden (no SwiGLU width); bf16
+ * rounds x and h'.  The workspace must hold
+ * treeflash_workspace_bytes(b, gamma, d, 16, V, k, topk2, dt) bytes for any
+ * valid topk2 (the SwiGLU width does not enter). */
+tf_status_t treeflash_arapprox_linear_hidden(const void *h, const int32_t *root_token,
+                                             const int32_t *topk_idx, const void *emb,
+                                             const void *norm_h_gain, const void *norm_e_gain,
+                                             const void *w_lin, int b, int gamma, int d, int V, int k,
+                                             float rms_eps, tf_dtype_t dt, void *hprime,
+                                             void *workspace, size_t workspace_bytes,
+                                             hipStream_t stream);
+
 /* Part 1, stage 2 (Method, Eq. 1; Appendix B, rest of Part 1): AR approximation
  * of every conditional row, LM head, log-softmax, top-topk2.  Equivalent to
  * treeflash_arapprox_hidden followed by treeflash_marginal_topk on h'.

@@ -348,7 +348,8 @@ def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
     """One drafting step for every sequence: Part 1 then Part 2.
 
     ``inputs`` holds float64/int64 numpy arrays: h [b, gamma, d], root [b],
-    lm_head, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down.
+    lm_head, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down (or w_lin
+    for the w/ Linear ablation, which then replaces Eq. 1's SwiGLU).
     ``sequences`` restricts the work to a subset of the batch (the sequences
     are independent).
     """
@@ -363,9 +364,14 @@ def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
         st1 = marginal_stage(h[s:s + 1], inputs["lm_head"], k, inv_temperature)
         st1 = {key: val[0] for key, val in st1.items()}
         prev = previous_tokens(int(inputs["root"][s]), st1["topk_idx"], gamma, k)
-        hp = ar_approximator(h[s], prev, depth, inputs["emb"], inputs["norm_h_gain"],
-                             inputs["norm_e_gain"], inputs["w_gate"], inputs["w_up"],
-                             inputs["w_down"], eps=eps, mirror_bf16=mirror_bf16)
+        if "w_lin" in inputs:
+            hp = ar_approximator_linear(h[s], prev, depth, inputs["emb"], inputs["norm_h_gain"],
+                                        inputs["norm_e_gain"], inputs["w_lin"], eps=eps,
+                                        mirror_bf16=mirror_bf16)
+        else:
+            hp = ar_approximator(h[s], prev, depth, inputs["emb"], inputs["norm_h_gain"],
+                                 inputs["norm_e_gain"], inputs["w_gate"], inputs["w_up"],
+                                 inputs["w_down"], eps=eps, mirror_bf16=mirror_bf16)
         rows = conditional_stage(hp, inputs["lm_head"], K2, inv_temperature, keep_full=keep_full)
         tree = build_tree(rows["cond_idx"], rows["cond_logprob"], st1["topk_idx"], gamma, k, B)
         if not keep_full:

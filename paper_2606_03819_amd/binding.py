@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(HERE, "libtreeflash.so")
 TF_F32, TF_BF16 = 0, 1
 STATUS = {0: "TF_OK", 1: "TF_ERR_INVALID_ARG", 2: "TF_ERR_UNSUPPORTED", 3: "TF_ERR_WORKSPACE", 4: "TF_ERR_HIP"}
 EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_marginal_topk_timed",
-            "treeflash_arapprox_hidden", "treeflash_arapprox_expand", "treeflash_build_tree",
+            "treeflash_arapprox_hidden", "treeflash_arapprox_linear_hidden", "treeflash_arapprox_expand",
+            "treeflash_build_tree",
             "treeflash_build_tree_marginal", "treeflash_tree_attention_inputs", "treeflash_accept",
             "treeflash_status_string")
 
@@ -50,6 +51,8 @@ def lib() -> ctypes.CDLL:
     L.treeflash_marginal_topk_timed.restype = I
     L.treeflash_arapprox_hidden.argtypes = [P, P, P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, P, S, P]
     L.treeflash_arapprox_hidden.restype = I
+    L.treeflash_arapprox_linear_hidden.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, I, P, P, S, P]
+    L.treeflash_arapprox_linear_hidden.restype = I
     L.treeflash_arapprox_expand.argtypes = [P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, F, F, I,
                                             P, P, P, P, S, P]
     L.treeflash_arapprox_expand.restype = I
@@ -168,6 +171,31 @@ def treeflash_arapprox_hidden(h, root_token, topk_idx, emb, norm_h_gain, norm_e_
         b, gamma, d, I, V, k, float(rms_eps), dt, _ptr(hprime, "hprime", h.dtype, dev),
         _ptr(workspace, "workspace", device=dev), workspace.numel() * workspace.element_size(), _stream(dev))
     _check("treeflash_arapprox_hidden", st)
+    return hprime
+
+
+def treeflash_arapprox_linear_hidden(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_lin,
+                                     rms_eps: float = 1e-6, workspace: Optional[torch.Tensor] = None,
+                                     hprime: Optional[torch.Tensor] = None, V: Optional[int] = None):
+    """The w/ Linear approximator for every conditional row: h' [b, R, d]."""
+    b, gamma, d = h.shape
+    k = topk_idx.shape[2]
+    V = emb.shape[0] if V is None else V
+    R = 1 + (gamma - 1) * k
+    dev = h.device
+    dt = _dtype_code(h)
+    if hprime is None:
+        hprime = torch.empty((b, R, d), dtype=h.dtype, device=dev)
+    if workspace is None:
+        workspace = alloc_workspace(treeflash_workspace_bytes(b, gamma, d, 16, V, k, 1, dt), dev)
+    st = lib().treeflash_arapprox_linear_hidden(
+        _ptr(h, "h", device=dev), _ptr(root_token, "root_token", torch.int32, dev),
+        _ptr(topk_idx, "topk_idx", torch.int32, dev), _ptr(emb, "emb", h.dtype, dev),
+        _ptr(norm_h_gain, "norm_h_gain", h.dtype, dev), _ptr(norm_e_gain, "norm_e_gain", h.dtype, dev),
+        _ptr(w_lin, "w_lin", h.dtype, dev), b, gamma, d, V, k, float(rms_eps), dt,
+        _ptr(hprime, "hprime", h.dtype, dev), _ptr(workspace, "workspace", device=dev),
+        workspace.numel() * workspace.element_size(), _stream(dev))
+    _check("treeflash_arapprox_linear_hidden", st)
     return hprime
 
 
@@ -318,6 +346,9 @@ class Drafter:
     """One drafting step over resident weights: the three C calls in order.
 
     Holds the workspace and output buffers so repeated steps allocate nothing.
+    With a ``w_lin`` weight (the w/ Linear approximator) stage 2 is
+    treeflash_arapprox_linear_hidden into a held h' buffer followed by
+    treeflash_marginal_topk on its rows.
     """
 
     def __init__(self, weights: Dict[str, torch.Tensor], b: int, gamma: int, k: int, B: int,
@@ -326,7 +357,8 @@ class Drafter:
         lm = weights["lm_head"]
         self.dev = lm.device
         self.V, self.d = lm.shape
-        self.I = weights["w_gate"].shape[0]
+        self.linear = "w_lin" in weights
+        self.I = 16 if self.linear else weights["w_gate"].shape[0]
         self.b, self.gamma, self.k, self.B = b, gamma, k, B
         self.topk2 = min(B, self.V) if topk2 is None else topk2
         self.inv_t, self.eps = inv_temperature, rms_eps
@@ -342,6 +374,7 @@ class Drafter:
         self.cond_idx = torch.empty((b, self.R, self.topk2), dtype=torch.int32, **z)
         self.cond_lp = torch.empty((b, self.R, self.topk2), dtype=torch.float32, **z)
         self.cond_lse = torch.empty((b, self.R), dtype=torch.float32, **z)
+        self.hprime = torch.empty((b, self.R, self.d), dtype=dt, **z) if self.linear else None
         self.tree = {
             "token": torch.empty((b, B), dtype=torch.int32, **z),
             "parent": torch.empty((b, B), dtype=torch.int32, **z),
@@ -357,6 +390,13 @@ class Drafter:
 
     def stage2(self, h, root, weights=None, topk_idx=None):
         w = weights or self.w
+        tk = self.topk_idx if topk_idx is None else topk_idx
+        if self.linear:
+            treeflash_arapprox_linear_hidden(h, root, tk, w["emb"], w["norm_h_gain"], w["norm_e_gain"], w["w_lin"],
+                                             self.eps, self.workspace, self.hprime, self.V)
+            treeflash_marginal_topk(self.hprime, w["lm_head"], self.topk2, self.inv_t, self.workspace,
+                                    self.cond_idx, self.cond_lp, self.cond_lse)
+            return self.cond_idx, self.cond_lp, self.cond_lse
         return treeflash_arapprox_expand(
             h, root, self.topk_idx if topk_idx is None else topk_idx, w["emb"], w["norm_h_gain"],
             w["norm_e_gain"], w["w_gate"], w["w_up"], w["w_down"], w["lm_head"], self.topk2, self.inv_t,

@@ -130,6 +130,28 @@ tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, 
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
+tf_status_t treeflash_arapprox_linear_hidden(const void* h, const int32_t* root_token, const int32_t* topk_idx,
+                                             const void* emb, const void* norm_h_gain, const void* norm_e_gain,
+                                             const void* w_lin, int b, int gamma, int d, int V, int k, float rms_eps,
+                                             tf_dtype_t dt, void* hprime, void* workspace, size_t workspace_bytes,
+                                             hipStream_t stream) {
+    // the SwiGLU checks with w_lin standing in for the three projections and the smallest width
+    const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_lin, w_lin,
+                                              w_lin, b, gamma, d, 16, V, k, rms_eps, dt);
+    if (chk != TF_OK) return chk;
+    if (hprime == nullptr || !aligned16(hprime)) return TF_ERR_INVALID_ARG;
+    const bool bf16 = dt == TF_BF16;
+    const Workspace lay = workspace_layout(b, gamma, d, 16, V, k, bf16);
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    const hipError_t e = launch_arapprox_linear(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_lin, b,
+                                                gamma, d, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et, hprime,
+                                                reinterpret_cast<float*>(ws + lay.mlp_part),
+                                                reinterpret_cast<int*>(ws + lay.counters),
+                                                reinterpret_cast<int*>(ws + lay.diag), stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
 tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, const int32_t* topk_idx,
                                       const void* emb, const void* norm_h_gain, const void* norm_e_gain,
                                       const void* w_gate, const void* w_up, const void* w_down,

@@ -22,6 +22,13 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
                            bool bf16, void* ht, void* et, void* act, void* hp, float* mlp_partial, int* counters,
                            int* diag, hipStream_t stream);
 
+// The "w/ Linear" approximator for every conditional row: RMSNorm of h and
+// of the previous token's embedding, h' = h + W_lin [h~ ; e~].
+hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
+                                  const void* gain_h, const void* gain_e, const void* w_lin, int b, int gamma, int d,
+                                  int V, int k, float eps, bool bf16, void* ht, void* et, void* hp,
+                                  float* mlp_partial, int* counters, int* diag, hipStream_t stream);
+
 // Best-first tree selection, one workgroup per sequence.  `marginal`: the
 // rows are the gamma marginal rows [b, gamma, topk2] and every node above
 // depth gamma expands into the next depth's row (topk_idx and k unused).

@@ -94,6 +94,19 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void down_bf16_kernel(WRo
     stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
+// The linear approximator: h' = h + W_lin [h~ ; e~].
+template <int WM, int NT, int NW, int PIPE, bool WNT>
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void linear_bf16_kernel(WRowsPlain ws, XRowsConcat xs,
+                                                                              GemmShape sh,
+                                                                              uint16_t* __restrict__ hp,
+                                                                              const uint16_t* __restrict__ h, int d,
+                                                                              int Rs, int gamma, int M,
+                                                                              float* partial, int* counter) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
+    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, Rs, gamma, M}, partial, counter};
+    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
+}
+
 // ------------------------------------------------------------------ fp32
 
 __global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ wg, const float* __restrict__ wu,
@@ -134,6 +147,25 @@ __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__
     float y = 0.f;
     for (int i = 0; i < I; ++i) y = fmaf(ar[i], wr[i], y);
     hp[(size_t)r * d + n] = h[(size_t)(s * gamma + row_depth(rl, M) - 1) * d + n] + y;
+}
+
+__global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict__ wl, const float* __restrict__ ht,
+                                                         const float* __restrict__ et, const float* __restrict__ h,
+                                                         int rows, int d, int Rs, int gamma, int M,
+                                                         float* __restrict__ hp) {
+    const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
+    const int n = blockIdx.x * 64 + (threadIdx.x & 63);
+    if (r >= rows || n >= d) return;
+    const int s = r / Rs;
+    const int rl = r - s * Rs;
+    const int hrow = s * gamma + row_depth(rl, M) - 1;
+    const float* hr = ht + (size_t)hrow * d;
+    const float* er = et + (size_t)r * d;
+    const float* w = wl + (size_t)n * 2 * d;
+    float y = 0.f;
+    for (int k = 0; k < d; ++k) y = fmaf(hr[k], w[k], y);
+    for (int k = 0; k < d; ++k) y = fmaf(er[k], w[d + k], y);
+    hp[(size_t)r * d + n] = h[(size_t)hrow * d + n] + y;
 }
 
 // ------------------------------------------------------------------ launcher
@@ -207,6 +239,47 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
         hipLaunchKernelGGL(down_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
                            static_cast<const float*>(w_down), static_cast<const float*>(act),
                            static_cast<const float*>(h), rows, d, I, Rs, gamma, k, static_cast<float*>(hp));
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
+                                  const void* gain_h, const void* gain_e, const void* w_lin, int b, int gamma, int d,
+                                  int V, int k, float eps, bool bf16, void* ht, void* et, void* hp,
+                                  float* mlp_partial, int* counters, int* diag, hipStream_t stream) {
+    const int Rs = 1 + (gamma - 1) * k;
+    const int rows = b * Rs;
+    const int nrows = b * gamma + rows;
+    if (bf16) {
+        const GemmPlan pl = linear_plan(rows, d);
+        hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),
+                           static_cast<const uint16_t*>(gain_h), static_cast<const uint16_t*>(gain_e), b, gamma, d,
+                           V, k, Rs, eps, static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag, counters,
+                           (int)pl.counter_ints());
+        WRowsPlain wr{static_cast<const uint16_t*>(w_lin), d, 2 * d};
+        XRowsConcat xc{static_cast<const uint16_t*>(ht), static_cast<const uint16_t*>(et), d, Rs, gamma, k};
+        const GemmShape sh = pl.shape(rows, 2 * d);
+        uint16_t* hpb = static_cast<uint16_t*>(hp);
+        const uint16_t* hb = static_cast<const uint16_t*>(h);
+        if (pl.NT == 1)
+            hipLaunchKernelGGL((linear_bf16_kernel<2, 1, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
+                               0, stream, wr, xc, sh, hpb, hb, d, Rs, gamma, k, mlp_partial, counters);
+        else if (pl.NT == 2)
+            hipLaunchKernelGGL((linear_bf16_kernel<1, 2, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
+                               0, stream, wr, xc, sh, hpb, hb, d, Rs, gamma, k, mlp_partial, counters);
+        else
+            hipLaunchKernelGGL((linear_bf16_kernel<1, 4, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
+                               0, stream, wr, xc, sh, hpb, hb, d, Rs, gamma, k, mlp_partial, counters);
+    } else {
+        hipLaunchKernelGGL(rmsnorm_rows_kernel<float>, dim3(nrows), dim3(256), 0, stream,
+                           static_cast<const float*>(h), root, topk_idx, static_cast<const float*>(emb),
+                           static_cast<const float*>(gain_h), static_cast<const float*>(gain_e), b, gamma, d, V, k,
+                           Rs, eps, static_cast<float*>(ht), static_cast<float*>(et), diag, counters, 0);
+        hipLaunchKernelGGL(linear_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
+                           static_cast<const float*>(w_lin), static_cast<const float*>(ht),
+                           static_cast<const float*>(et), static_cast<const float*>(h), rows, d, Rs, gamma, k,
+                           static_cast<float*>(hp));
     }
     return hipGetLastError();
 }

@@ -175,6 +175,8 @@ inline GemmPlan mlp_plan(int rows, int ntiles, int K, int wg_single) {
 }
 inline GemmPlan gateup_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(I, 16), 2 * d, TF_MLP_WORKGROUPS); }
 inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d, 32), I, TF_DOWN_WORKGROUPS); }
+// the linear approximator: [rows, 2d] x [d, 2d]^T
+inline GemmPlan linear_plan(int rows, int d) { return mlp_plan(rows, cdiv(d, 32), 2 * d, TF_DOWN_WORKGROUPS); }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -214,10 +216,12 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     size_t mp = 0;
     w.ncounters = 0;
     if (bf16) {
-        const GemmPlan pg = gateup_plan(rows2, d, I), pd = down_plan(rows2, d, I);
-        const size_t a = pg.fix_floats(), c = pd.fix_floats();
+        const GemmPlan pg = gateup_plan(rows2, d, I), pd = down_plan(rows2, d, I), pl = linear_plan(rows2, d);
+        const size_t a = pg.fix_floats(), c = pd.fix_floats(), l = pl.fix_floats();
         mp = a > c ? a : c;
-        w.ncounters = (int)(pg.counter_ints() + pd.counter_ints());
+        mp = mp > l ? mp : l;
+        const size_t nc = pg.counter_ints() + pd.counter_ints();
+        w.ncounters = (int)(nc > pl.counter_ints() ? nc : pl.counter_ints());
     }
     w.mlp_part = off;
     off += align256(mp * 4);

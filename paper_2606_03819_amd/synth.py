@@ -12,6 +12,8 @@ checkpoints and evaluation prompts that are not available here):
   fp32 and rounded to bf16 (round-to-nearest-even) for the bf16 workloads;
   the tiny workload stays fp32;
 * drafter hidden states ``h[b, gamma, d]`` ~ N(0, 1);
+* the w/ Linear workloads draw ``W_lin [d, 2d]`` from N(0, 0.02) in place of
+  the three SwiGLU matrices;
 * both RMSNorm gains are ones (no biases anywhere);
 * the root token of each sequence is uniform over the vocabulary.
 
@@ -58,6 +60,7 @@ class Workload:
     weight_seed: int
     state_seed: int       # per-sequence seed = state_seed + s when b > 1
     description: str = ""
+    approximator: str = "swiglu"   # "swiglu" (Eq. 1) or "linear" (the w/ Linear ablation)
 
     @property
     def rows(self) -> int:
@@ -94,6 +97,16 @@ WORKLOADS: Dict[str, Workload] = {
                  "Qwen3-8B-shaped bf16, batch 1, budget 512 (512-entry stage-2 lists)"),
         Workload("qwen3-8b-shape-m64", 1, 4096, 151936, 16, 64, 32, 4096, "bf16", 1.0, 3, 13,
                  "Qwen3-8B-shaped bf16, batch 1, M=64 candidates (961 conditional rows)"),
+        # the AR approximator at the width the paper's parameter counts imply
+        # (5*d*I = +125M / +251M: the target models' MLP widths)
+        Workload("qwen3-4b-shape-i9728", 1, 2560, 151936, 16, 8, 32, 9728, "bf16", 1.0 / 0.7, 2, 12,
+                 "Qwen3-4B-shaped bf16, SwiGLU width 9728 (the paper's AR-approximator size)"),
+        Workload("qwen3-8b-shape-i12288", 1, 4096, 151936, 16, 8, 32, 12288, "bf16", 1.0, 3, 13,
+                 "Qwen3-8B-shaped bf16, SwiGLU width 12288 (the paper's AR-approximator size)"),
+        # the w/ Linear ablation: one [d, 2d] layer in place of the SwiGLU
+        # (I is unused); same LM head, embedding and states as qwen3-8b-shape
+        Workload("qwen3-8b-shape-linear", 1, 4096, 151936, 16, 8, 32, 0, "bf16", 1.0, 3, 13,
+                 "Qwen3-8B-shaped bf16, w/ Linear approximator", "linear"),
     ]
 }
 
@@ -120,7 +133,8 @@ def _normal(shape, std, g, device, dtype):
 
 
 def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> Dict[str, torch.Tensor]:
-    """Weights in draw order: LM head, embedding, gate, up, down, then gains.
+    """Weights in draw order: LM head, embedding, gate, up, down (or, for the
+    linear approximator, W_lin [d, 2d] in their place), then gains.
 
     ``weight_std`` other than 0.02 is only used by tests that want sharper
     distributions on small shapes.
@@ -131,9 +145,12 @@ def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> D
     out = {}
     out["lm_head"] = _normal((w.V, w.d), weight_std, g, device, dt)
     out["emb"] = _normal((w.V, w.d), weight_std, g, device, dt)
-    out["w_gate"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
-    out["w_up"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
-    out["w_down"] = _normal((w.d, w.I), weight_std, g, device, dt)
+    if w.approximator == "linear":
+        out["w_lin"] = _normal((w.d, 2 * w.d), weight_std, g, device, dt)
+    else:
+        out["w_gate"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
+        out["w_up"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
+        out["w_down"] = _normal((w.d, w.I), weight_std, g, device, dt)
     out["norm_h_gain"] = torch.ones(w.d, device=device, dtype=dt)
     out["norm_e_gain"] = torch.ones(w.d, device=device, dtype=dt)
     return out

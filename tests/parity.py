@@ -135,8 +135,13 @@ def to_cpu_tree(tree, s):
 def _oracle_rows(o_in, w, topk_seq, s):
     depth, _ = oracle.row_table(w.gamma, w.k)
     prev = oracle.previous_tokens(int(o_in["root"][s]), topk_seq, w.gamma, w.k)
-    hp = oracle.ar_approximator(o_in["h"][s], prev, depth, o_in["emb"], o_in["norm_h_gain"], o_in["norm_e_gain"],
-                                o_in["w_gate"], o_in["w_up"], o_in["w_down"], mirror_bf16=(w.dtype == "bf16"))
+    if "w_lin" in o_in:
+        hp = oracle.ar_approximator_linear(o_in["h"][s], prev, depth, o_in["emb"], o_in["norm_h_gain"],
+                                           o_in["norm_e_gain"], o_in["w_lin"], mirror_bf16=(w.dtype == "bf16"))
+    else:
+        hp = oracle.ar_approximator(o_in["h"][s], prev, depth, o_in["emb"], o_in["norm_h_gain"],
+                                    o_in["norm_e_gain"], o_in["w_gate"], o_in["w_up"], o_in["w_down"],
+                                    mirror_bf16=(w.dtype == "bf16"))
     return oracle.conditional_stage(hp, o_in["lm_head"], w.topk2, w.inv_temperature, keep_full=True)
 
 

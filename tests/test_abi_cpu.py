@@ -125,6 +125,37 @@ def test_arapprox_hidden_rejects(over, code):
     assert _hidden(**over) == code
 
 
+def _linear(**over):
+    a = dict(h=FAKE, root=FAKE, topk=FAKE, emb=FAKE, gh=None, ge=None, wl=FAKE,
+             b=1, gamma=16, d=4096, V=151936, k=8, eps=1e-6, dt=BF16, hp=FAKE2, ws=FAKE, wsb=1 << 40, st=None)
+    a.update(over)
+    return binding.lib().treeflash_arapprox_linear_hidden(
+        a["h"], a["root"], a["topk"], a["emb"], a["gh"], a["ge"], a["wl"], a["b"], a["gamma"], a["d"], a["V"],
+        a["k"], a["eps"], a["dt"], a["hp"], a["ws"], a["wsb"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(h=None), INVALID), (dict(root=None), INVALID), (dict(topk=None), INVALID), (dict(emb=None), INVALID),
+    (dict(wl=None), INVALID), (dict(wl=FAKE + 8), INVALID), (dict(hp=None), INVALID), (dict(hp=FAKE2 + 2), INVALID),
+    (dict(d=24), INVALID), (dict(eps=float("inf")), INVALID), (dict(k=0), INVALID), (dict(k=2000), INVALID),
+    (dict(gamma=300), INVALID), (dict(dt=7), INVALID), (dict(gh=FAKE + 2), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws=FAKE + 8), WORKSPACE), (dict(wsb=100), WORKSPACE),
+])
+def test_arapprox_linear_hidden_rejects(over, code):
+    assert _linear(**over) == code
+
+
+def test_linear_workspace_fits_in_the_swiglu_one():
+    # the linear variant's workspace (any SwiGLU width stands in) never exceeds
+    # what treeflash_workspace_bytes gives for the smallest width
+    for (b, gamma, d, V, k) in [(1, 16, 4096, 151936, 8), (16, 16, 4096, 151936, 8), (1, 4, 64, 1000, 3),
+                                (4, 7, 2560, 151936, 32)]:
+        n16 = binding.lib().treeflash_workspace_bytes(b, gamma, d, 16, V, k, 8, BF16)
+        assert n16 > 0
+        # one byte short of it is refused before any launch
+        assert _linear(b=b, gamma=gamma, d=d, V=V, k=k, wsb=n16 - 1) == WORKSPACE
+
+
 def _tree(**over):
     a = dict(ci=FAKE, cl=FAKE, tk=FAKE, b=1, gamma=16, k=8, topk2=32, B=32, tok=FAKE2, par=FAKE2, dep=FAKE2,
              sc=FAKE2, cr=None, st=None)

@@ -14,7 +14,8 @@ from parity import check_draft, oracle_inputs
 pytestmark = pytest.mark.gpu
 
 FULL = [("qwen3-4b-shape", [0]), ("qwen3-8b-shape", [0]), ("qwen3-8b-shape-k16-b64", [0]),
-        ("qwen3-8b-shape-batch16", [0, 15]), ("qwen3-8b-shape-b512", [0]), ("qwen3-8b-shape-m64", [0])]
+        ("qwen3-8b-shape-batch16", [0, 15]), ("qwen3-8b-shape-b512", [0]), ("qwen3-8b-shape-m64", [0]),
+        ("qwen3-4b-shape-i9728", [0]), ("qwen3-8b-shape-i12288", [0]), ("qwen3-8b-shape-linear", [0])]
 
 
 @pytest.mark.parametrize("name,seqs", FULL, ids=[f[0] for f in FULL])
