@@ -25,6 +25,11 @@ Experiments, "Metrics": block efficiency)
   * the tree laid out for a verifier pass with tree attention (root first,
     positions = depths, ancestor mask) and the greedy acceptance walk that
     turns the verifier's per-node next tokens into accepted nodes and tau.
+The w/ Linear and w/ 2-prev ablations (Ablations, Model Design)
+  * one linear layer in place of the SwiGLU of Eq. 1;
+  * the previous bigram instead of one previous token: 1 + M + (gamma-2)*M^2
+    conditional rows, and a tree whose nodes expand into the row of their
+    (parent token, own token) pair.
 Marginal baseline (the paper's DDTree comparison, Related Work and Appendix C)
   * the same selection on the marginal distributions alone: every node above
     the last depth expands into the marginal row of the next depth, so all
@@ -57,6 +62,7 @@ __all__ = [
     "marginal_stage", "row_table", "previous_tokens", "ar_approximator",
     "conditional_stage", "build_tree", "draft", "build_marginal_tree", "draft_marginal",
     "verification_inputs", "acceptance_walk", "ar_approximator_linear", "RMS_EPS",
+    "row_table_2prev", "previous_pairs", "ar_approximator_2prev", "build_tree_2prev", "draft_2prev",
 ]
 
 RMS_EPS = 1e-6
@@ -401,6 +407,167 @@ def draft_marginal(inputs: Dict[str, np.ndarray], gamma: int, B: int, inv_temper
         st1.pop("logits")
         st1.pop("logprob")
         out["stage1"].append(st1)
+        out["tree"].append(tree)
+    return out
+
+
+# ------------------------------------------------- the w/ 2-prev ablation
+#
+# Ablations, Model Design: the AR approximator reads the two previous tokens
+# (the previous bigram) instead of one.  Readings (the paper gives no more):
+#   * x_r = [ rms(h_{depth_r}) ; rms(Embd(prev1_r)) ; rms(Embd(prev2_r)) ], the
+#     embedding RMSNorm (one gain) applied to each token, prev1 the token
+#     right before the drafted position, prev2 the one before it; W_gate and
+#     W_up are [I, 3d], W_down [d, I];
+#   * depth 1 reads (x_{t-1}, x_t): the context token before the root and the
+#     root; depth 2 reads (x_t, candidate m of depth 1); depth i >= 3 reads
+#     (candidate m2 of depth i-2, candidate m1 of depth i-1): M^2 rows;
+#   * a node expands when its token is a candidate of its depth and, below
+#     depth 1, its parent's token is one of the parent depth (which holds for
+#     every node whose parent was expanded).
+
+def row_table_2prev(gamma: int, M: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Rows of the bigram-conditioned table: row 0 is depth 1, rows 1..M depth
+    2 (candidate m1 = row-1 of depth 1), then for depth i >= 3 the M^2 rows
+    1 + M + (i-3)*M^2 + m2*M + m1.  Returns (depth, slot1, slot2) [R]: the
+    candidate indices of prev1 (depth-1 list) and prev2 (depth-2 list); -1
+    marks the root token, -2 the context token before the root."""
+    depth, slot1, slot2 = [1], [-1], [-2]
+    if gamma >= 2:
+        for m1 in range(M):
+            depth.append(2)
+            slot1.append(m1)
+            slot2.append(-1)
+    for i in range(3, gamma + 1):
+        for m2 in range(M):
+            for m1 in range(M):
+                depth.append(i)
+                slot1.append(m1)
+                slot2.append(m2)
+    return (np.asarray(depth, dtype=np.int64), np.asarray(slot1, dtype=np.int64),
+            np.asarray(slot2, dtype=np.int64))
+
+
+def previous_pairs(context: int, root: int, topk_idx_seq: np.ndarray, gamma: int,
+                   M: int) -> Tuple[np.ndarray, np.ndarray]:
+    """(prev1, prev2) tokens of every row of row_table_2prev."""
+    depth, slot1, slot2 = row_table_2prev(gamma, M)
+
+    def token(d_list: int, slot: int) -> int:
+        if slot == -1:
+            return int(root)
+        if slot == -2:
+            return int(context)
+        return int(topk_idx_seq[d_list - 1, slot])
+
+    prev1 = np.array([token(depth[r] - 1, slot1[r]) for r in range(depth.shape[0])], dtype=np.int64)
+    prev2 = np.array([token(depth[r] - 2, slot2[r]) for r in range(depth.shape[0])], dtype=np.int64)
+    return prev1, prev2
+
+
+def ar_approximator_2prev(h_seq: np.ndarray, prev1: np.ndarray, prev2: np.ndarray, depth: np.ndarray,
+                          emb: np.ndarray, norm_h_gain: np.ndarray, norm_e_gain: np.ndarray,
+                          w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
+                          eps: float = RMS_EPS, mirror_bf16: bool = False) -> np.ndarray:
+    """Eq. 1 with the bigram input x_r = [h~ ; e~(prev1) ; e~(prev2)] (3d wide).
+    With mirror_bf16, x, the activation and h' are rounded to bf16."""
+    hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
+    E = np.asarray(emb, dtype=np.float64)
+    x = np.concatenate([rms_norm(hd, norm_h_gain, eps), rms_norm(E[np.asarray(prev1)], norm_e_gain, eps),
+                        rms_norm(E[np.asarray(prev2)], norm_e_gain, eps)], axis=-1)
+    if mirror_bf16:
+        x = bf16_round(x)
+    g = x @ np.asarray(w_gate, dtype=np.float64).T
+    u = x @ np.asarray(w_up, dtype=np.float64).T
+    a = silu(g) * u
+    if mirror_bf16:
+        a = bf16_round(a)
+    hp = hd + a @ np.asarray(w_down, dtype=np.float64).T
+    if mirror_bf16:
+        hp = bf16_round(hp)
+    return hp
+
+
+def build_tree_2prev(cond_idx: np.ndarray, cond_logprob: np.ndarray, topk_idx_seq: np.ndarray,
+                     gamma: int, M: int, B: int) -> Dict[str, np.ndarray]:
+    """OPT-Tree selection over the bigram-conditioned rows.
+
+    Pops, scores and ties as in build_tree.  A popped node of depth i < gamma
+    whose token is candidate m1 of depth i expands into row 1 + m1 when i = 1,
+    else into row 1 + M + (i-2)*M^2 + m2*M + m1, m2 being its parent's
+    candidate index at depth i-1.  Returns build_tree's fields.
+    """
+    cond_idx = np.asarray(cond_idx)
+    lp32 = np.asarray(cond_logprob, dtype=np.float32)
+    K = cond_idx.shape[1]
+    heap: List[tuple] = []
+
+    def push_row(row: int, parent: int, parent_score: np.float32, depth: int, path: tuple):
+        for c in range(K):
+            s = np.float32(parent_score + lp32[row, c])        # float32 add
+            heapq.heappush(heap, (-float(s), depth, path + (c,), parent, row, c))
+
+    push_row(0, -1, np.float32(0.0), 1, ())
+    token, parent, depth_o, score, child_row, rank, slot = [], [], [], [], [], [], []
+    while len(token) < B:
+        if not heap:
+            raise ValueError("draft budget exceeds the number of admissible nodes")
+        negs, dep, path, par, row, c = heapq.heappop(heap)
+        tok = int(cond_idx[row, c])
+        hits = np.nonzero(np.asarray(topk_idx_seq[dep - 1]) == tok)[0]
+        m1 = int(hits[0]) if hits.size else -1
+        crow = -1
+        if dep < gamma and m1 >= 0:
+            if dep == 1:
+                crow = 1 + m1
+            else:
+                crow = 1 + M + (dep - 2) * M * M + slot[par] * M + m1
+        token.append(tok)
+        parent.append(par)
+        depth_o.append(dep)
+        score.append(np.float32(-negs))
+        child_row.append(crow)
+        rank.append(c)
+        slot.append(m1)
+        if crow >= 0:
+            push_row(crow, len(token) - 1, np.float32(-negs), dep + 1, path)
+    return {
+        "token": np.asarray(token, dtype=np.int32),
+        "parent": np.asarray(parent, dtype=np.int32),
+        "depth": np.asarray(depth_o, dtype=np.int32),
+        "score": np.asarray(score, dtype=np.float32),
+        "child_row": np.asarray(child_row, dtype=np.int32),
+        "rank": np.asarray(rank, dtype=np.int32),
+    }
+
+
+def draft_2prev(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
+                inv_temperature: float = 1.0, mirror_bf16: bool = False,
+                topk2: Optional[int] = None, eps: float = RMS_EPS,
+                keep_full: bool = False, sequences: Optional[List[int]] = None) -> Dict[str, object]:
+    """One w/ 2-prev drafting step: ``inputs`` as for draft plus ``context``
+    [b] (the token before each root); w_gate and w_up are [I, 3d]."""
+    h = inputs["h"]
+    V = inputs["lm_head"].shape[0]
+    K2 = min(B, V) if topk2 is None else topk2
+    seqs = list(range(h.shape[0])) if sequences is None else list(sequences)
+    depth, _, _ = row_table_2prev(gamma, k)
+    out = {"stage1": [], "rows": [], "hprime": [], "tree": []}
+    for s in seqs:
+        st1 = marginal_stage(h[s:s + 1], inputs["lm_head"], k, inv_temperature)
+        st1 = {key: val[0] for key, val in st1.items()}
+        p1, p2 = previous_pairs(int(inputs["context"][s]), int(inputs["root"][s]), st1["topk_idx"], gamma, k)
+        hp = ar_approximator_2prev(h[s], p1, p2, depth, inputs["emb"], inputs["norm_h_gain"],
+                                   inputs["norm_e_gain"], inputs["w_gate"], inputs["w_up"], inputs["w_down"],
+                                   eps=eps, mirror_bf16=mirror_bf16)
+        rows = conditional_stage(hp, inputs["lm_head"], K2, inv_temperature, keep_full=keep_full)
+        tree = build_tree_2prev(rows["cond_idx"], rows["cond_logprob"], st1["topk_idx"], gamma, k, B)
+        if not keep_full:
+            st1.pop("logits")
+            st1.pop("logprob")
+        out["stage1"].append(st1)
+        out["rows"].append(rows)
+        out["hprime"].append(hp)
         out["tree"].append(tree)
     return out
 

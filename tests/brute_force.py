@@ -150,3 +150,58 @@ def brute_force_marginal_tree(marg_idx, marg_logprob, gamma, B):
         "score": np.asarray(out["score"], dtype=np.float32),
         "rank": np.asarray(out["rank"], dtype=np.int32),
     }
+
+
+def brute_force_tree_2prev(cond_idx, cond_logprob, topk_idx_seq, gamma, M, B, context=-2, root=-1):
+    """Every admissible node of the bigram-conditioned tree, best B by the
+    candidate order.  Rows are found by their (depth, token two back, previous
+    token) key, enumerated here in the table's stated order: depth 1 is
+    (context, root), depth 2 (root, candidate m of depth 1), depth i >= 3
+    (candidate m2 of depth i-2, candidate m1 of depth i-1) with m1 fastest.
+    ``context`` and ``root`` only need to differ from every candidate token."""
+    cond_idx = np.asarray(cond_idx)
+    lp = np.asarray(cond_logprob, dtype=np.float32)
+    K = cond_idx.shape[1]
+    cands = [list(np.asarray(topk_idx_seq[i]).tolist()) for i in range(gamma)]
+    key_row = {}
+    r = 0
+    key_row[(1, context, root)] = r
+    r += 1
+    if gamma >= 2:
+        for t1 in cands[0]:
+            key_row[(2, root, t1)] = r
+            r += 1
+    for dep in range(3, gamma + 1):
+        for t2 in cands[dep - 3]:
+            for t1 in cands[dep - 2]:
+                key_row[(dep, t2, t1)] = r
+                r += 1
+    found = []
+    # (row, depth of the row's tokens, parent score, rank path, token two back, previous token)
+    stack = [(0, 1, np.float32(0.0), (), context, root)]
+    while stack:
+        row, dep, s_par, path, t2, t1 = stack.pop()
+        for c in range(K):
+            s = np.float32(s_par + lp[row, c])
+            p = path + (c,)
+            tok = int(cond_idx[row, c])
+            found.append((_key(s, dep, p), s, tok))
+            nxt = key_row.get((dep + 1, t1, tok))
+            if dep < gamma and nxt is not None and tok in cands[dep - 1]:
+                stack.append((nxt, dep + 1, s, p, t1, tok))
+    if len(found) < B:
+        raise ValueError("budget exceeds admissible nodes")
+    found.sort(key=lambda t: t[0])
+    top = found[:B]
+    pos = {t[0][2]: i for i, t in enumerate(top)}
+    out = {k: [] for k in ("token", "parent", "depth", "score", "rank")}
+    for key, s, tok in top:
+        path = key[2]
+        out["token"].append(tok)
+        out["parent"].append(pos[path[:-1]] if len(path) > 1 else -1)
+        out["depth"].append(key[1])
+        out["score"].append(s)
+        out["rank"].append(path[-1])
+    res = {k: np.asarray(v, dtype=np.float32 if k == "score" else np.int32) for k, v in out.items()}
+    res["admissible"] = len(found)
+    return res
