@@ -127,9 +127,11 @@ def cpu_baseline(w, weights, states, budget_s):
     inputs = {k: synth.to_numpy64(v) for k, v in weights.items()}
     inputs["h"] = synth.to_numpy64(states["h"][:1])
     inputs["root"] = synth.to_numpy64(states["root"][:1])
+    inputs["context"] = synth.to_numpy64(states["context"][:1])
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    draft = oracle.draft_2prev if w.approximator == "2prev" else oracle.draft
     t0 = time.perf_counter()
-    oracle.draft(inputs, w.gamma, w.k, w.B, w.inv_temperature, mirror_bf16=(w.dtype == "bf16"))
+    draft(inputs, w.gamma, w.k, w.B, w.inv_temperature, mirror_bf16=(w.dtype == "bf16"))
     dt = time.perf_counter() - t0
     return {"value": 1.0 / dt, "unit": "trees/s", "cores": int(threads), "kind": "oracle",
             "sample": f"one sequence's full drafting step (stage 1, {w.rows} conditional rows, tree); "
@@ -213,20 +215,39 @@ def summarize_pmc(args):
     print("```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
-def approx_hidden(wt, h, root, topk_idx, workspace, hp, V):
-    """Stage 2's first half: Eq. 1's SwiGLU, or the w/ Linear layer when the weights hold one."""
+def make_drafter(w, weights):
+    """The drafter of the workload's approximator (its buffers and workspace)."""
+    cls = binding.Drafter2Prev if w.approximator == "2prev" else binding.Drafter
+    return cls(weights, w.b, w.gamma, w.k, w.B, w.inv_temperature)
+
+
+def approx_hidden(wt, h, root, context, topk_idx, workspace, hp, V):
+    """Stage 2's first half: Eq. 1's SwiGLU, the w/ Linear layer when the weights
+    hold one, or the w/ 2-prev SwiGLU when gate/up read three d-blocks."""
+    d = h.shape[2]
     if "w_lin" in wt:
         binding.treeflash_arapprox_linear_hidden(h, root, topk_idx, wt["emb"], wt["norm_h_gain"],
                                                  wt["norm_e_gain"], wt["w_lin"], 1e-6, workspace, hp, V)
+    elif wt["w_gate"].shape[1] == 3 * d:
+        binding.treeflash_arapprox_2prev_hidden(h, context, root, topk_idx, wt["emb"], wt["norm_h_gain"],
+                                                wt["norm_e_gain"], wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6,
+                                                workspace, hp, V)
     else:
         binding.treeflash_arapprox_hidden(h, root, topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
                                           wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, workspace, hp, V)
 
 
-def time_steps(w, copies, h, root, steps, warmup):
+def build_tree(w, dr):
+    if w.approximator == "2prev":
+        binding.treeflash_build_tree_2prev(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
+    else:
+        binding.treeflash_build_tree(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
+
+
+def time_steps(w, copies, h, root, steps, warmup, context=None):
     """Mean GPU time per stage of the drafting step for workload w (events around each call)."""
     dev = torch.device("cuda", 0)
-    dr = binding.Drafter(copies[0], w.b, w.gamma, w.k, w.B, w.inv_temperature)
+    dr = make_drafter(w, copies[0])
     hp = torch.empty((w.b, w.rows, w.d), dtype=w.torch_dtype, device=dev)
 
     def step(i, ev=None):
@@ -237,14 +258,14 @@ def time_steps(w, copies, h, root, steps, warmup):
                                         dr.topk_lp)
         if ev is not None:
             ev[1].record()
-        approx_hidden(wt, h, root, dr.topk_idx, dr.workspace, hp, w.V)
+        approx_hidden(wt, h, root, context, dr.topk_idx, dr.workspace, hp, w.V)
         if ev is not None:
             ev[2].record()
         binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
                                         dr.cond_idx, dr.cond_lp, dr.cond_lse)
         if ev is not None:
             ev[3].record()
-        binding.treeflash_build_tree(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
+        build_tree(w, dr)
         if ev is not None:
             ev[4].record()
 
@@ -266,12 +287,12 @@ def sweep(args):
     B and M sweeps, as a systems curve)."""
     base = synth.get_workload(args.workload)
     copies, st = make_copies(base, max(1, args.copies))
-    h, root = st["h"], st["root"]
+    h, root, context = st["h"], st["root"], st["context"]
     out = []
     points = [("B", B, base.replace(name=f"{base.name}-B{B}", B=B)) for B in (16, 32, 64, 128, 256, 512)]
     points += [("M", M, base.replace(name=f"{base.name}-M{M}", k=M)) for M in (4, 8, 16, 32, 64)]
     for axis, val, w in points:
-        us = time_steps(w, copies, h, root, args.steps, args.warmup)
+        us = time_steps(w, copies, h, root, args.steps, args.warmup, context)
         out.append({"axis": axis, "value": val, "B": w.B, "M": w.k, "conditional_rows": w.rows * w.b,
                     "trees_per_s": w.b * 1e6 / us["step"], "stage_us": us})
     print(json.dumps({"metric": "drafting cost over draft budget B and branching M", "unit": "us",
@@ -303,9 +324,9 @@ def main():
     copies, st = make_copies(w, max(1, args.copies))
     dev = torch.device("cuda", 0)
     d, V, R, b = w.d, w.V, w.rows, w.b
-    dr = binding.Drafter(copies[0], b, w.gamma, w.k, w.B, w.inv_temperature)
+    dr = make_drafter(w, copies[0])
     hp = torch.empty((b, R, d), dtype=w.torch_dtype, device=dev)
-    h, root = st["h"], st["root"]
+    h, root, context = st["h"], st["root"], st["context"]
 
     def step(i, ev=None):
         wt = copies[i % len(copies)]
@@ -315,7 +336,7 @@ def main():
                                         dr.topk_lp)
         if ev is not None:
             ev[1].record()
-        approx_hidden(wt, h, root, dr.topk_idx, dr.workspace, hp, V)
+        approx_hidden(wt, h, root, context, dr.topk_idx, dr.workspace, hp, V)
         if ev is not None:
             ev[2].record()
         binding.treeflash_marginal_topk(hp, wt["lm_head"], dr.topk2, w.inv_temperature, dr.workspace,
@@ -323,7 +344,7 @@ def main():
                                         events=None if ev is None else (ev[5].cuda_event, ev[6].cuda_event))
         if ev is not None:
             ev[3].record()
-        binding.treeflash_build_tree(dr.cond_idx, dr.cond_lp, dr.topk_idx, w.B, dr.tree)
+        build_tree(w, dr)
         if ev is not None:
             ev[4].record()
 
@@ -435,7 +456,8 @@ def main():
     roof["mfma_frac"] = alg_flops / t_lm / 1e12 / BF16_PEAK_TFLOPS
 
     # whole-step roofline context
-    mlp_bytes = (2 * d * d if w.approximator == "linear" else 2 * w.I * 2 * d + d * w.I) * es
+    kin = 3 * d if w.approximator == "2prev" else 2 * d
+    mlp_bytes = (2 * d * d if w.approximator == "linear" else 2 * w.I * kin + d * w.I) * es
     step_bytes = 2 * V * d * es + mlp_bytes
     out = {
         "metric": METRIC, "value": trees_per_s, "unit": "trees/s", "n_gpus": 1, "steps": args.steps,

@@ -28,7 +28,8 @@
  *     to TF_ERR_HIP.  Nothing is thrown or aborted across the ABI.
  *   - `dt` is the element type of h, the embedding, the gains and every weight
  *     matrix: TF_BF16 (bf16 operands, fp32 accumulation, bf16 rounding of the
- *     x, SwiGLU-activation and h' operands) or TF_F32 (fp32 throughout).
+ *     x and h' operands; the SwiGLU activation enters the down projection as
+ *     a bf16 hi/lo pair, about 16 significant bits) or TF_F32 (fp32 throughout).
  *   - Shapes: b sequences, hidden size d, vocabulary V, draft depth gamma,
  *     M = k stage-1 candidates per depth, SwiGLU width I, draft budget B.
  *     R = 1 + (gamma-1)*k conditional rows per sequence.  Row 0 is depth 1
@@ -193,6 +194,48 @@ tf_status_t treeflash_build_tree(const int32_t *cond_idx, const float *cond_logp
                                  int32_t *node_token, int32_t *node_parent, int32_t *node_depth,
                                  float *node_score, int32_t *node_child_row,
                                  hipStream_t stream);
+
+/* The paper's "w/ 2-prev" ablation (Ablations, Model Design): the AR
+ * approximator reads the previous bigram instead of one token.
+ *   R2 = 1 + k + (gamma-2)*k*k conditional rows per sequence (1 when gamma = 1):
+ *   row 0: depth 1, previous tokens (context_token, root_token);
+ *   rows 1..k: depth 2, (root_token, candidate m of depth 1), row 1 + m;
+ *   depth i >= 3: (candidate m2 of depth i-2, candidate m1 of depth i-1),
+ *   row 1 + k + (i-3)*k*k + m2*k + m1.
+ * x_r = [ rms(h)*g_h ; rms(Embd(prev1))*g_e ; rms(Embd(prev2))*g_e ] with prev1
+ * the token right before the drafted position, then Eq. 1's SwiGLU and
+ * residual.  b*R2 must not exceed 2^20. */
+
+/* Workspace bytes of treeflash_arapprox_2prev_hidden and of the LM-head call
+ * on its rows (treeflash_marginal_topk on h' viewed as [b, R2, d] with k =
+ * topk2); 0 for invalid shapes. */
+size_t treeflash_workspace_bytes_2prev(int b, int gamma, int d, int I, int V, int k, int topk2,
+                                       tf_dtype_t dt);
+
+/* h' of every bigram row.
+ *   context_token [b] int32: the token before each root (x_{t-1})
+ *   w_gate, w_up  [I, 3d]  (columns: h~, then e~(prev1), then e~(prev2))
+ *   w_down        [d, I]
+ *   hprime        out [b, R2, d]
+ * Other arguments, rounding and errors as treeflash_arapprox_hidden. */
+tf_status_t treeflash_arapprox_2prev_hidden(const void *h, const int32_t *context_token,
+                                            const int32_t *root_token, const int32_t *topk_idx,
+                                            const void *emb, const void *norm_h_gain,
+                                            const void *norm_e_gain, const void *w_gate,
+                                            const void *w_up, const void *w_down, int b, int gamma,
+                                            int d, int I, int V, int k, float rms_eps, tf_dtype_t dt,
+                                            void *hprime, void *workspace, size_t workspace_bytes,
+                                            hipStream_t stream);
+
+/* OPT-Tree selection over the bigram rows [b, R2, topk2]: as treeflash_build_tree,
+ * except that a node of depth i < gamma whose token is candidate m1 of its
+ * depth expands into row 1 + m1 (i = 1) or 1 + k + (i-2)*k*k + m2*k + m1,
+ * m2 being its parent's candidate index. */
+tf_status_t treeflash_build_tree_2prev(const int32_t *cond_idx, const float *cond_logprob,
+                                       const int32_t *topk_idx, int b, int gamma, int k, int topk2,
+                                       int B, int32_t *node_token, int32_t *node_parent,
+                                       int32_t *node_depth, float *node_score,
+                                       int32_t *node_child_row, hipStream_t stream);
 
 /* The marginal OPT-Tree (the paper's DDTree comparison, Related Work;
  * Appendix C): the same best-first selection on the drafter's marginal

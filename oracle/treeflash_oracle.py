@@ -42,8 +42,9 @@ is silent (each is listed in DESIGN.md):
   * the LM head is a plain product with the [V, d] output embedding; logits are
     multiplied by the inverse drafter temperature before the softmax;
   * for bf16 workloads the oracle rounds to bf16 exactly where a bf16 operand
-    is formed for a matrix product: x, the SwiGLU activation a, and h'
-    ("mirror" rounding points); all else stays float64;
+    is formed for a matrix product: x and h' ("mirror" rounding points); the
+    SwiGLU activation a enters the down projection as a bf16 hi/lo pair, about
+    16 significant bits, which float64 stands in for; all else stays float64;
   * path scores are float32 running sums of float32 row log-probabilities, so
     a tree is reproducible bit for bit from the same rows;
   * ties: top-k lists order by (value desc, token asc); tree candidates order by
@@ -175,7 +176,7 @@ def ar_approximator(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
     h_seq: [gamma, d] drafter states; prev/depth: [R] from row_table.
     h'_r = h_{depth_r} + W_down( silu(W_gate x_r) * (W_up x_r) ),
     x_r = [ rms(h_{depth_r}) ; rms(Embd(prev_r)) ].
-    With mirror_bf16, x, the activation and h' are rounded to bf16.
+    With mirror_bf16, x and h' are rounded to bf16 (the activation is not).
     """
     hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
     e = np.asarray(emb, dtype=np.float64)[np.asarray(prev)]
@@ -185,8 +186,6 @@ def ar_approximator(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
     g = x @ np.asarray(w_gate, dtype=np.float64).T
     u = x @ np.asarray(w_up, dtype=np.float64).T
     a = silu(g) * u
-    if mirror_bf16:
-        a = bf16_round(a)
     hp = hd + a @ np.asarray(w_down, dtype=np.float64).T
     if mirror_bf16:
         hp = bf16_round(hp)
@@ -470,7 +469,7 @@ def ar_approximator_2prev(h_seq: np.ndarray, prev1: np.ndarray, prev2: np.ndarra
                           w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
                           eps: float = RMS_EPS, mirror_bf16: bool = False) -> np.ndarray:
     """Eq. 1 with the bigram input x_r = [h~ ; e~(prev1) ; e~(prev2)] (3d wide).
-    With mirror_bf16, x, the activation and h' are rounded to bf16."""
+    With mirror_bf16, x and h' are rounded to bf16 (the activation is not)."""
     hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
     E = np.asarray(emb, dtype=np.float64)
     x = np.concatenate([rms_norm(hd, norm_h_gain, eps), rms_norm(E[np.asarray(prev1)], norm_e_gain, eps),
@@ -480,8 +479,6 @@ def ar_approximator_2prev(h_seq: np.ndarray, prev1: np.ndarray, prev2: np.ndarra
     g = x @ np.asarray(w_gate, dtype=np.float64).T
     u = x @ np.asarray(w_up, dtype=np.float64).T
     a = silu(g) * u
-    if mirror_bf16:
-        a = bf16_round(a)
     hp = hd + a @ np.asarray(w_down, dtype=np.float64).T
     if mirror_bf16:
         hp = bf16_round(hp)

@@ -23,6 +23,7 @@ EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_m
             "treeflash_arapprox_hidden", "treeflash_arapprox_linear_hidden", "treeflash_arapprox_expand",
             "treeflash_build_tree",
             "treeflash_build_tree_marginal", "treeflash_tree_attention_inputs", "treeflash_accept",
+            "treeflash_workspace_bytes_2prev", "treeflash_arapprox_2prev_hidden", "treeflash_build_tree_2prev",
             "treeflash_status_string")
 
 _lib = None
@@ -64,6 +65,12 @@ def lib() -> ctypes.CDLL:
     L.treeflash_tree_attention_inputs.restype = I
     L.treeflash_accept.argtypes = [P, P, P, I, I, I, P, P, P, P]
     L.treeflash_accept.restype = I
+    L.treeflash_workspace_bytes_2prev.argtypes = [I, I, I, I, I, I, I, I]
+    L.treeflash_workspace_bytes_2prev.restype = S
+    L.treeflash_arapprox_2prev_hidden.argtypes = [P, P, P, P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, P, S, P]
+    L.treeflash_arapprox_2prev_hidden.restype = I
+    L.treeflash_build_tree_2prev.argtypes = [P, P, P, I, I, I, I, I, P, P, P, P, P, P]
+    L.treeflash_build_tree_2prev.restype = I
     L.treeflash_status_string.argtypes = [I]
     L.treeflash_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -96,6 +103,13 @@ def _ptr(t: Optional[torch.Tensor], name: str, dtype=None, device=None) -> Optio
     if dtype is not None and t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
     return t.data_ptr()
+
+
+def _shapes(func: str, **want):
+    """Raise unless every tensor has the shape the library will read it with."""
+    for name, (t, shape) in want.items():
+        if t is not None and tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{func}: {name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
 def _stream(device) -> int:
@@ -136,7 +150,8 @@ def treeflash_marginal_topk(h: torch.Tensor, lm_head: torch.Tensor, k: int, inv_
     if topk_logprob is None:
         topk_logprob = torch.empty((b, gamma, k), dtype=torch.float32, device=dev)
     if workspace is None:
-        workspace = alloc_workspace(treeflash_workspace_bytes(b, gamma, d, 16, V, k, min(k, V), dt), dev)
+        # stage-1 scratch for b * gamma rows (gamma may count more rows than a draft depth)
+        workspace = alloc_workspace(treeflash_workspace_bytes(b * gamma, 1, d, 16, V, k, min(k, V), dt), dev)
     args = (_ptr(h, "h", device=dev), _ptr(lm_head, "lm_head", h.dtype, dev), b, gamma, d, V, k,
             float(inv_temperature), dt, _ptr(topk_idx, "topk_idx", torch.int32, dev),
             _ptr(topk_logprob, "topk_logprob", torch.float32, dev), _ptr(lse, "lse", torch.float32, dev),
@@ -157,6 +172,9 @@ def treeflash_arapprox_hidden(h, root_token, topk_idx, emb, norm_h_gain, norm_e_
     V = emb.shape[0] if V is None else V
     I = w_gate.shape[0]
     R = 1 + (gamma - 1) * k
+    _shapes("treeflash_arapprox_hidden", root_token=(root_token, (b,)), topk_idx=(topk_idx, (b, gamma, k)),
+            emb=(emb, (V, d)), w_gate=(w_gate, (I, 2 * d)), w_up=(w_up, (I, 2 * d)), w_down=(w_down, (d, I)),
+            hprime=(hprime, (b, R, d)))
     dev = h.device
     dt = _dtype_code(h)
     if hprime is None:
@@ -182,6 +200,8 @@ def treeflash_arapprox_linear_hidden(h, root_token, topk_idx, emb, norm_h_gain, 
     k = topk_idx.shape[2]
     V = emb.shape[0] if V is None else V
     R = 1 + (gamma - 1) * k
+    _shapes("treeflash_arapprox_linear_hidden", root_token=(root_token, (b,)), topk_idx=(topk_idx, (b, gamma, k)),
+            emb=(emb, (V, d)), w_lin=(w_lin, (d, 2 * d)), hprime=(hprime, (b, R, d)))
     dev = h.device
     dt = _dtype_code(h)
     if hprime is None:
@@ -199,6 +219,41 @@ def treeflash_arapprox_linear_hidden(h, root_token, topk_idx, emb, norm_h_gain, 
     return hprime
 
 
+def treeflash_workspace_bytes_2prev(b, gamma, d, I, V, k, topk2, dtype) -> int:
+    code = dtype if isinstance(dtype, int) else (TF_BF16 if dtype == torch.bfloat16 else TF_F32)
+    return int(lib().treeflash_workspace_bytes_2prev(b, gamma, d, I, V, k, topk2, code))
+
+
+def treeflash_arapprox_2prev_hidden(h, context_token, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate,
+                                    w_up, w_down, rms_eps: float = 1e-6, workspace: Optional[torch.Tensor] = None,
+                                    hprime: Optional[torch.Tensor] = None, V: Optional[int] = None):
+    """The w/ 2-prev approximator for every bigram row: h' [b, R2, d]."""
+    b, gamma, d = h.shape
+    k = topk_idx.shape[2]
+    V = emb.shape[0] if V is None else V
+    I = w_gate.shape[0]
+    R = 1 if gamma == 1 else 1 + k + (gamma - 2) * k * k
+    _shapes("treeflash_arapprox_2prev_hidden", context_token=(context_token, (b,)), root_token=(root_token, (b,)),
+            topk_idx=(topk_idx, (b, gamma, k)), emb=(emb, (V, d)), w_gate=(w_gate, (I, 3 * d)),
+            w_up=(w_up, (I, 3 * d)), w_down=(w_down, (d, I)), hprime=(hprime, (b, R, d)))
+    dev = h.device
+    dt = _dtype_code(h)
+    if hprime is None:
+        hprime = torch.empty((b, R, d), dtype=h.dtype, device=dev)
+    if workspace is None:
+        workspace = alloc_workspace(treeflash_workspace_bytes_2prev(b, gamma, d, I, V, k, 1, dt), dev)
+    st = lib().treeflash_arapprox_2prev_hidden(
+        _ptr(h, "h", device=dev), _ptr(context_token, "context_token", torch.int32, dev),
+        _ptr(root_token, "root_token", torch.int32, dev), _ptr(topk_idx, "topk_idx", torch.int32, dev),
+        _ptr(emb, "emb", h.dtype, dev), _ptr(norm_h_gain, "norm_h_gain", h.dtype, dev),
+        _ptr(norm_e_gain, "norm_e_gain", h.dtype, dev), _ptr(w_gate, "w_gate", h.dtype, dev),
+        _ptr(w_up, "w_up", h.dtype, dev), _ptr(w_down, "w_down", h.dtype, dev), b, gamma, d, I, V, k,
+        float(rms_eps), dt, _ptr(hprime, "hprime", h.dtype, dev), _ptr(workspace, "workspace", device=dev),
+        workspace.numel() * workspace.element_size(), _stream(dev))
+    _check("treeflash_arapprox_2prev_hidden", st)
+    return hprime
+
+
 def treeflash_arapprox_expand(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down,
                               lm_head, topk2: int, inv_temperature: float = 1.0, rms_eps: float = 1e-6,
                               workspace: Optional[torch.Tensor] = None, cond_idx=None, cond_logprob=None,
@@ -209,6 +264,9 @@ def treeflash_arapprox_expand(h, root_token, topk_idx, emb, norm_h_gain, norm_e_
     V = lm_head.shape[0]
     I = w_gate.shape[0]
     R = 1 + (gamma - 1) * k
+    _shapes("treeflash_arapprox_expand", root_token=(root_token, (b,)), topk_idx=(topk_idx, (b, gamma, k)),
+            emb=(emb, (V, d)), w_gate=(w_gate, (I, 2 * d)), w_up=(w_up, (I, 2 * d)), w_down=(w_down, (d, I)),
+            lm_head=(lm_head, (V, d)), cond_idx=(cond_idx, (b, R, topk2)), cond_logprob=(cond_logprob, (b, R, topk2)))
     dev = h.device
     dt = _dtype_code(h)
     if cond_idx is None:
@@ -232,27 +290,35 @@ def treeflash_arapprox_expand(h, root_token, topk_idx, emb, norm_h_gain, norm_e_
     return cond_idx, cond_logprob, cond_lse
 
 
-def treeflash_build_tree(cond_idx, cond_logprob, topk_idx, B: int, out: Optional[Dict[str, torch.Tensor]] = None):
-    """Part 2: best-first selection of B nodes per sequence (pop order)."""
+def _build_tree(func: str, rows_of, cond_idx, cond_logprob, topk_idx, B, out):
     b, R, topk2 = cond_idx.shape
     gamma, k = topk_idx.shape[1], topk_idx.shape[2]
+    if R != rows_of(gamma, k) or cond_logprob.shape != cond_idx.shape or topk_idx.shape[0] != b:
+        raise ValueError(f"{func}: rows {tuple(cond_idx.shape)} do not match candidates {tuple(topk_idx.shape)}")
     dev = cond_idx.device
     if out is None:
-        out = {
-            "token": torch.empty((b, B), dtype=torch.int32, device=dev),
-            "parent": torch.empty((b, B), dtype=torch.int32, device=dev),
-            "depth": torch.empty((b, B), dtype=torch.int32, device=dev),
-            "score": torch.empty((b, B), dtype=torch.float32, device=dev),
-            "child_row": torch.empty((b, B), dtype=torch.int32, device=dev),
-        }
-    st = lib().treeflash_build_tree(
+        out = _tree_buffers(b, B, dev)
+    st = getattr(lib(), func)(
         _ptr(cond_idx, "cond_idx", torch.int32, dev), _ptr(cond_logprob, "cond_logprob", torch.float32, dev),
         _ptr(topk_idx, "topk_idx", torch.int32, dev), b, gamma, k, topk2, B,
         _ptr(out["token"], "token", torch.int32, dev), _ptr(out["parent"], "parent", torch.int32, dev),
         _ptr(out["depth"], "depth", torch.int32, dev), _ptr(out["score"], "score", torch.float32, dev),
         _ptr(out.get("child_row"), "child_row", torch.int32, dev), _stream(dev))
-    _check("treeflash_build_tree", st)
+    _check(func, st)
     return out
+
+
+def treeflash_build_tree(cond_idx, cond_logprob, topk_idx, B: int, out: Optional[Dict[str, torch.Tensor]] = None):
+    """Part 2: best-first selection of B nodes per sequence (pop order)."""
+    return _build_tree("treeflash_build_tree", lambda g, k: 1 + (g - 1) * k, cond_idx, cond_logprob, topk_idx, B,
+                       out)
+
+
+def treeflash_build_tree_2prev(cond_idx, cond_logprob, topk_idx, B: int,
+                               out: Optional[Dict[str, torch.Tensor]] = None):
+    """Part 2 over the bigram rows of the w/ 2-prev approximator."""
+    return _build_tree("treeflash_build_tree_2prev", lambda g, k: 1 if g == 1 else 1 + k + (g - 2) * k * k,
+                       cond_idx, cond_logprob, topk_idx, B, out)
 
 
 def _tree_buffers(b: int, B: int, dev) -> Dict[str, torch.Tensor]:
@@ -416,3 +482,60 @@ class Drafter:
     def diagnostics(self) -> int:
         """Slices the last call re-evaluated on the exact slow path (synchronises)."""
         return int(self.workspace[:4].view(torch.int32).item())
+
+
+class Drafter2Prev(Drafter):
+    """A drafting step of the w/ 2-prev approximator (bigram rows): stage 1,
+    treeflash_arapprox_2prev_hidden into a held h' buffer, the LM head on its
+    rows, treeflash_build_tree_2prev.  The weights' w_gate / w_up are [I, 3d]."""
+
+    def __init__(self, weights: Dict[str, torch.Tensor], b: int, gamma: int, k: int, B: int,
+                 inv_temperature: float = 1.0, rms_eps: float = 1e-6, topk2: Optional[int] = None):
+        lm = weights["lm_head"]
+        V, d = lm.shape
+        I = weights["w_gate"].shape[0]
+        if weights["w_gate"].shape[1] != 3 * d:
+            raise ValueError("w_gate must be [I, 3d] for the 2-prev approximator")
+        self.w = weights
+        self.dev = lm.device
+        self.V, self.d, self.I = V, d, I
+        self.linear = False
+        self.b, self.gamma, self.k, self.B = b, gamma, k, B
+        self.topk2 = min(B, V) if topk2 is None else topk2
+        self.inv_t, self.eps = inv_temperature, rms_eps
+        self.R = 1 if gamma == 1 else 1 + k + (gamma - 2) * k * k
+        nbytes = treeflash_workspace_bytes_2prev(b, gamma, d, I, V, k, self.topk2, lm.dtype)
+        if nbytes == 0:
+            raise ValueError("invalid drafting shapes")
+        self.workspace = alloc_workspace(nbytes, self.dev)
+        z = dict(device=self.dev)
+        self.topk_idx = torch.empty((b, gamma, k), dtype=torch.int32, **z)
+        self.topk_lp = torch.empty((b, gamma, k), dtype=torch.float32, **z)
+        self.cond_idx = torch.empty((b, self.R, self.topk2), dtype=torch.int32, **z)
+        self.cond_lp = torch.empty((b, self.R, self.topk2), dtype=torch.float32, **z)
+        self.cond_lse = torch.empty((b, self.R), dtype=torch.float32, **z)
+        self.hprime = torch.empty((b, self.R, d), dtype=lm.dtype, **z)
+        self.tree = _tree_buffers(b, B, self.dev)
+        self.context = None
+
+    def stage2(self, h, root, weights=None, topk_idx=None, context=None):
+        w = weights or self.w
+        ctx = self.context if context is None else context
+        if ctx is None:
+            raise ValueError("the 2-prev rows need the context token before each root")
+        tk = self.topk_idx if topk_idx is None else topk_idx
+        treeflash_arapprox_2prev_hidden(h, ctx, root, tk, w["emb"], w["norm_h_gain"], w["norm_e_gain"], w["w_gate"],
+                                        w["w_up"], w["w_down"], self.eps, self.workspace, self.hprime, self.V)
+        treeflash_marginal_topk(self.hprime, w["lm_head"], self.topk2, self.inv_t, self.workspace,
+                                self.cond_idx, self.cond_lp, self.cond_lse)
+        return self.cond_idx, self.cond_lp, self.cond_lse
+
+    def tree_build(self, cond_idx=None, cond_lp=None, topk_idx=None):
+        return treeflash_build_tree_2prev(self.cond_idx if cond_idx is None else cond_idx,
+                                          self.cond_lp if cond_lp is None else cond_lp,
+                                          self.topk_idx if topk_idx is None else topk_idx, self.B, self.tree)
+
+    def step(self, h, root, weights=None, context=None):
+        if context is not None:
+            self.context = context
+        return super().step(h, root, weights)

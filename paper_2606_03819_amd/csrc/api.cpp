@@ -122,11 +122,43 @@ tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, 
     const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16);
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
     unsigned char* ws = static_cast<unsigned char*>(workspace);
-    const hipError_t e = launch_arapprox(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
-                                         w_down, b, gamma, d, I, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et,
+    const hipError_t e = launch_arapprox(h, root_token, nullptr, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate,
+                                         w_up, w_down, b, gamma, d, I, V, k, false, rms_eps, bf16, ws + lay.ht, ws + lay.et,
                                          ws + lay.act, hprime, reinterpret_cast<float*>(ws + lay.mlp_part),
                                          reinterpret_cast<int*>(ws + lay.counters), reinterpret_cast<int*>(ws + lay.diag),
                                          stream);
+    return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+size_t treeflash_workspace_bytes_2prev(int b, int gamma, int d, int I, int V, int k, int topk2, tf_dtype_t dt) {
+    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k)) return 0;
+    if (I < 16 || I % 16 != 0 || topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return 0;
+    if ((long long)b * cond_rows(gamma, k, 1) > kMaxRows) return 0;
+    return workspace_layout(b, gamma, d, I, V, k, dt == TF_BF16, true).total;
+}
+
+tf_status_t treeflash_arapprox_2prev_hidden(const void* h, const int32_t* context_token, const int32_t* root_token,
+                                            const int32_t* topk_idx, const void* emb, const void* norm_h_gain,
+                                            const void* norm_e_gain, const void* w_gate, const void* w_up,
+                                            const void* w_down, int b, int gamma, int d, int I, int V, int k,
+                                            float rms_eps, tf_dtype_t dt, void* hprime, void* workspace,
+                                            size_t workspace_bytes, hipStream_t stream) {
+    const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
+                                              w_down, b, gamma, d, I, V, k, rms_eps, dt);
+    if (chk != TF_OK) return chk;
+    if (context_token == nullptr || !aligned4(context_token)) return TF_ERR_INVALID_ARG;
+    if ((long long)b * cond_rows(gamma, k, 1) > kMaxRows) return TF_ERR_INVALID_ARG;
+    if (hprime == nullptr || !aligned16(hprime)) return TF_ERR_INVALID_ARG;
+    const bool bf16 = dt == TF_BF16;
+    const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16, true);
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    const hipError_t e = launch_arapprox(h, root_token, context_token, topk_idx, emb, norm_h_gain, norm_e_gain,
+                                         w_gate, w_up, w_down, b, gamma, d, I, V, k, true, rms_eps, bf16,
+                                         ws + lay.ht, ws + lay.et, ws + lay.act, hprime,
+                                         reinterpret_cast<float*>(ws + lay.mlp_part),
+                                         reinterpret_cast<int*>(ws + lay.counters),
+                                         reinterpret_cast<int*>(ws + lay.diag), stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
@@ -173,8 +205,9 @@ tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, 
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     int* diag = reinterpret_cast<int*>(ws + lay.diag);
-    hipError_t e = launch_arapprox(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down, b,
-                                   gamma, d, I, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et, ws + lay.act,
+    hipError_t e = launch_arapprox(h, root_token, nullptr, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
+                                   w_down, b, gamma, d, I, V, k, false, rms_eps, bf16, ws + lay.ht, ws + lay.et,
+                                   ws + lay.act,
                                    ws + lay.hp, reinterpret_cast<float*>(ws + lay.mlp_part),
                                    reinterpret_cast<int*>(ws + lay.counters), diag, stream);
     if (e != hipSuccess) return TF_ERR_HIP;
@@ -184,16 +217,21 @@ tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, 
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
-tf_status_t treeflash_build_tree(const int32_t* cond_idx, const float* cond_logprob, const int32_t* topk_idx, int b,
-                                 int gamma, int k, int topk2, int B, int32_t* node_token, int32_t* node_parent,
-                                 int32_t* node_depth, float* node_score, int32_t* node_child_row,
-                                 hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The selection over single-token or bigram conditional rows.
+tf_status_t build_tree_rows(const int32_t* cond_idx, const float* cond_logprob, const int32_t* topk_idx, int b,
+                            int gamma, int k, int topk2, int B, bool bigram, int32_t* node_token,
+                            int32_t* node_parent, int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                            hipStream_t stream) {
     if (cond_idx == nullptr || cond_logprob == nullptr || topk_idx == nullptr || node_token == nullptr ||
         node_parent == nullptr || node_depth == nullptr || node_score == nullptr)
         return TF_ERR_INVALID_ARG;
     if (b < 1 || gamma < 1 || gamma > 255 || k < 1 || k > kMaxTopk || topk2 < 1 || topk2 > 4096) return TF_ERR_INVALID_ARG;
     if (B < 1 || B > kMaxBudget) return TF_ERR_INVALID_ARG;
-    const long long Rs = 1 + (long long)(gamma - 1) * k;
+    const long long Rs = cond_rows(gamma, k, bigram ? 1 : 0);
     if ((long long)b * Rs > kMaxRows) return TF_ERR_INVALID_ARG;
     if (topk2 < B) {
         // Rows shorter than B are only meaningful when they are full rows
@@ -210,9 +248,29 @@ tf_status_t treeflash_build_tree(const int32_t* cond_idx, const float* cond_logp
         if (!aligned4(p)) return TF_ERR_INVALID_ARG;
     if (node_child_row != nullptr && !aligned4(node_child_row)) return TF_ERR_INVALID_ARG;
     if (tree_lds_bytes(B, gamma, k, (int)Rs, topk2, nullptr) == 0) return TF_ERR_UNSUPPORTED;
-    const hipError_t e = launch_build_tree(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, false,
+    const hipError_t e = launch_build_tree(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, bigram ? 2 : 0,
                                            node_token, node_parent, node_depth, node_score, node_child_row, stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+tf_status_t treeflash_build_tree(const int32_t* cond_idx, const float* cond_logprob, const int32_t* topk_idx, int b,
+                                 int gamma, int k, int topk2, int B, int32_t* node_token, int32_t* node_parent,
+                                 int32_t* node_depth, float* node_score, int32_t* node_child_row,
+                                 hipStream_t stream) {
+    return build_tree_rows(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, false, node_token, node_parent,
+                           node_depth, node_score, node_child_row, stream);
+}
+
+tf_status_t treeflash_build_tree_2prev(const int32_t* cond_idx, const float* cond_logprob, const int32_t* topk_idx,
+                                       int b, int gamma, int k, int topk2, int B, int32_t* node_token,
+                                       int32_t* node_parent, int32_t* node_depth, float* node_score,
+                                       int32_t* node_child_row, hipStream_t stream) {
+    return build_tree_rows(cond_idx, cond_logprob, topk_idx, b, gamma, k, topk2, B, true, node_token, node_parent,
+                           node_depth, node_score, node_child_row, stream);
 }
 
 tf_status_t treeflash_build_tree_marginal(const int32_t* marg_idx, const float* marg_logprob, int b, int gamma,
@@ -237,7 +295,7 @@ tf_status_t treeflash_build_tree_marginal(const int32_t* marg_idx, const float* 
         if (!aligned4(p)) return TF_ERR_INVALID_ARG;
     if (node_child_row != nullptr && !aligned4(node_child_row)) return TF_ERR_INVALID_ARG;
     if (tree_lds_bytes(B, gamma, 0, gamma, K, nullptr) == 0) return TF_ERR_UNSUPPORTED;
-    const hipError_t e = launch_build_tree(marg_idx, marg_logprob, nullptr, b, gamma, 0, K, B, true, node_token,
+    const hipError_t e = launch_build_tree(marg_idx, marg_logprob, nullptr, b, gamma, 0, K, B, 1, node_token,
                                            node_parent, node_depth, node_score, node_child_row, stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }

@@ -15,12 +15,14 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
                               hipEvent_t ev_end = nullptr);
 
 // Eq. 1 for every conditional row: RMSNorm of h and of the previous token's
-// embedding, SwiGLU, residual.  Writes h' [b*R, d] into `hp`.
-hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
-                           const void* gain_h, const void* gain_e, const void* w_gate, const void* w_up,
-                           const void* w_down, int b, int gamma, int d, int I, int V, int k, float eps,
-                           bool bf16, void* ht, void* et, void* act, void* hp, float* mlp_partial, int* counters,
-                           int* diag, hipStream_t stream);
+// embedding, SwiGLU, residual.  Writes h' [b*R, d] into `hp`.  `bigram`: the
+// w/ 2-prev rows (rows.hpp), x = [h~ ; e~(prev1) ; e~(prev2)], W_gate/W_up
+// [I, 3d], `context` [b] the token before each root (unused otherwise).
+hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* context, const int32_t* topk_idx,
+                           const void* emb, const void* gain_h, const void* gain_e, const void* w_gate,
+                           const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
+                           bool bigram, float eps, bool bf16, void* ht, void* et, void* act, void* hp,
+                           float* mlp_partial, int* counters, int* diag, hipStream_t stream);
 
 // The "w/ Linear" approximator for every conditional row: RMSNorm of h and
 // of the previous token's embedding, h' = h + W_lin [h~ ; e~].
@@ -29,11 +31,12 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
                                   int V, int k, float eps, bool bf16, void* ht, void* et, void* hp,
                                   float* mlp_partial, int* counters, int* diag, hipStream_t stream);
 
-// Best-first tree selection, one workgroup per sequence.  `marginal`: the
-// rows are the gamma marginal rows [b, gamma, topk2] and every node above
-// depth gamma expands into the next depth's row (topk_idx and k unused).
+// Best-first tree selection, one workgroup per sequence.  `mode` 0: the
+// single-token rows; 1: the rows are the gamma marginal rows [b, gamma,
+// topk2] and every node above depth gamma expands into the next depth's row
+// (topk_idx and k unused); 2: the bigram rows of the w/ 2-prev ablation.
 hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, const int32_t* topk_idx, int b,
-                             int gamma, int k, int topk2, int B, bool marginal, int32_t* node_token,
+                             int gamma, int k, int topk2, int B, int mode, int32_t* node_token,
                              int32_t* node_parent, int32_t* node_depth, float* node_score, int32_t* node_child_row,
                              hipStream_t stream);
 size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks);

@@ -1,11 +1,13 @@
 // The AR approximator of Eq. 1 for every conditional row:
 //   h'_r = h_{depth(r)} + W_down( silu(W_gate x_r) * (W_up x_r) ),
-//   x_r  = [ rms(h_{depth(r)}) * g_h ; rms(Embd(prev_r)) * g_e ].
-// Rows follow Appendix B: row 0 is depth 1 conditioned on the root token,
-// row 1 + (i-2)*M + m is depth i conditioned on candidate m of depth i-1.
+//   x_r  = [ rms(h_{depth(r)}) * g_h ; rms(Embd(prev_r)) * g_e ],
+// the w/ Linear ablation h'_r = h_{depth(r)} + W_lin x_r, and the w/ 2-prev
+// ablation whose x_r appends the normalised embedding of the token before
+// prev_r (Ablations, Model Design).  Rows follow the tables in rows.hpp.
 #include "common.hpp"
 #include "launch.hpp"
 #include "plan.hpp"
+#include "rows.hpp"
 #include "stream_gemm.hpp"
 
 namespace tf {
@@ -15,46 +17,40 @@ __device__ __forceinline__ float load_elem(const float* p, size_t i) { return p[
 __device__ __forceinline__ void store_elem(uint16_t* p, size_t i, float v) { p[i] = (uint16_t)f32_to_bf16_bits(v); }
 __device__ __forceinline__ void store_elem(float* p, size_t i, float v) { p[i] = v; }
 
-__device__ __forceinline__ int row_depth(int rl, int M) { return rl == 0 ? 1 : 2 + (rl - 1) / M; }
-
-// RMSNorm of the b*gamma drafter states (into ht) and of the b*R previous-token
-// embeddings (into et); one workgroup per row.  bf16 outputs are rounded to
-// nearest even: they are the bf16 operand x of the SwiGLU products.
+// RMSNorm of the b*gamma drafter states (into ht) and of the npre previous-
+// token embeddings of each of the b*R rows (into et, [b*R, npre*d], the
+// nearer token first); one workgroup per vector.  bf16 outputs are rounded to
+// nearest even: they are the bf16 operand x of the products that follow.
 template <class T>
 __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__ h, const int32_t* __restrict__ root,
+                                                           const int32_t* __restrict__ context,
                                                            const int32_t* __restrict__ topk,
                                                            const T* __restrict__ emb, const T* __restrict__ gh,
-                                                           const T* __restrict__ ge, int b, int gamma, int d, int V,
-                                                           int M, int Rs, float eps, T* __restrict__ ht,
+                                                           const T* __restrict__ ge, int b, int d, int V, RowTable rt,
+                                                           int npre, float eps, T* __restrict__ ht,
                                                            T* __restrict__ et, int* __restrict__ diag,
                                                            int* __restrict__ counters, int ncounters) {
     __shared__ float red[4];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
-    if (blockIdx.x == 0)   // arrival counters of the SwiGLU products that follow on this stream
+    if (blockIdx.x == 0)   // arrival counters of the products that follow on this stream
         for (int i = threadIdx.x; i < ncounters; i += 256) counters[i] = 0;
     const int row = blockIdx.x;
     const T* src;
     const T* gain;
     T* dst;
-    if (row < b * gamma) {
+    if (row < b * rt.gamma) {
         src = h + (size_t)row * d;
         gain = gh;
         dst = ht + (size_t)row * d;
     } else {
-        const int rr = row - b * gamma;
-        const int s = rr / Rs;
-        const int rl = rr - s * Rs;
-        int prev;
-        if (rl == 0) {
-            prev = root[s];
-        } else {
-            const int depth = row_depth(rl, M);
-            prev = topk[((size_t)s * gamma + (depth - 2)) * M + (rl - 1) % M];
-        }
+        const int e = row - b * rt.gamma;
+        const int rr = e / npre, which = e - rr * npre;
+        const int s = rr / rt.Rs;
+        int prev = rt.prev_token(s, rr - s * rt.Rs, which, root, context, topk);
         prev = min(max(prev, 0), V - 1);   // ids are documented to be < V; never read out of bounds
         src = emb + (size_t)prev * d;
         gain = ge;
-        dst = et + (size_t)rr * d;
+        dst = et + (size_t)rr * npre * d + (size_t)which * d;
     }
     float ss = 0.f;
     for (int k = threadIdx.x; k < d; k += 256) {
@@ -85,12 +81,11 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void gateup_bf16_kernel(W
 }
 
 template <int WM, int NT, int NW, int PIPE, bool WNT>
-__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void down_bf16_kernel(WRowsPlain ws, XRowsPlain xs, GemmShape sh,
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void down_bf16_kernel(WRowsPairedK ws, XRowsPlain xs, GemmShape sh,
                                                                uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
-                                                               int d, int Rs, int gamma, int M, float* partial,
-                                                               int* counter) {
+                                                               int d, RowTable rt, float* partial, int* counter) {
     __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
-    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, Rs, gamma, M}, partial, counter};
+    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, rt}, partial, counter};
     stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
@@ -100,34 +95,36 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void linear_bf16_kernel(W
                                                                               GemmShape sh,
                                                                               uint16_t* __restrict__ hp,
                                                                               const uint16_t* __restrict__ h, int d,
-                                                                              int Rs, int gamma, int M,
-                                                                              float* partial, int* counter) {
+                                                                              RowTable rt, float* partial,
+                                                                              int* counter) {
     __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
-    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, Rs, gamma, M}, partial, counter};
+    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, rt}, partial, counter};
     stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
 // ------------------------------------------------------------------ fp32
 
+// x_r = [ht(depth) ; et(r)] is K = d + ew wide.
 __global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ wg, const float* __restrict__ wu,
                                                          const float* __restrict__ ht, const float* __restrict__ et,
-                                                         int rows, int d, int I, int Rs, int gamma, int M,
+                                                         int rows, int d, int ew, int I, RowTable rt,
                                                          float* __restrict__ act) {
     const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
     const int i = blockIdx.x * 64 + (threadIdx.x & 63);
     if (r >= rows || i >= I) return;
-    const int s = r / Rs;
-    const int rl = r - s * Rs;
-    const float* hr = ht + (size_t)(s * gamma + row_depth(rl, M) - 1) * d;
-    const float* er = et + (size_t)r * d;
-    const float* g_row = wg + (size_t)i * 2 * d;
-    const float* u_row = wu + (size_t)i * 2 * d;
+    const int s = r / rt.Rs;
+    const int rl = r - s * rt.Rs;
+    const int K = d + ew;
+    const float* hr = ht + (size_t)(s * rt.gamma + rt.depth(rl) - 1) * d;
+    const float* er = et + (size_t)r * ew;
+    const float* g_row = wg + (size_t)i * K;
+    const float* u_row = wu + (size_t)i * K;
     float g = 0.f, u = 0.f;
     for (int k = 0; k < d; ++k) {
         g = fmaf(hr[k], g_row[k], g);
         u = fmaf(hr[k], u_row[k], u);
     }
-    for (int k = 0; k < d; ++k) {
+    for (int k = 0; k < ew; ++k) {
         g = fmaf(er[k], g_row[d + k], g);
         u = fmaf(er[k], u_row[d + k], u);
     }
@@ -135,30 +132,29 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict
 }
 
 __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__ wd, const float* __restrict__ act,
-                                                       const float* __restrict__ h, int rows, int d, int I, int Rs,
-                                                       int gamma, int M, float* __restrict__ hp) {
+                                                       const float* __restrict__ h, int rows, int d, int I,
+                                                       RowTable rt, float* __restrict__ hp) {
     const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
     const int n = blockIdx.x * 64 + (threadIdx.x & 63);
     if (r >= rows || n >= d) return;
-    const int s = r / Rs;
-    const int rl = r - s * Rs;
+    const int s = r / rt.Rs;
+    const int rl = r - s * rt.Rs;
     const float* ar = act + (size_t)r * I;
     const float* wr = wd + (size_t)n * I;
     float y = 0.f;
     for (int i = 0; i < I; ++i) y = fmaf(ar[i], wr[i], y);
-    hp[(size_t)r * d + n] = h[(size_t)(s * gamma + row_depth(rl, M) - 1) * d + n] + y;
+    hp[(size_t)r * d + n] = h[(size_t)(s * rt.gamma + rt.depth(rl) - 1) * d + n] + y;
 }
 
 __global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict__ wl, const float* __restrict__ ht,
                                                          const float* __restrict__ et, const float* __restrict__ h,
-                                                         int rows, int d, int Rs, int gamma, int M,
-                                                         float* __restrict__ hp) {
+                                                         int rows, int d, RowTable rt, float* __restrict__ hp) {
     const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
     const int n = blockIdx.x * 64 + (threadIdx.x & 63);
     if (r >= rows || n >= d) return;
-    const int s = r / Rs;
-    const int rl = r - s * Rs;
-    const int hrow = s * gamma + row_depth(rl, M) - 1;
+    const int s = r / rt.Rs;
+    const int rl = r - s * rt.Rs;
+    const int hrow = s * rt.gamma + rt.depth(rl) - 1;
     const float* hr = ht + (size_t)hrow * d;
     const float* er = et + (size_t)r * d;
     const float* w = wl + (size_t)n * 2 * d;
@@ -173,37 +169,48 @@ __global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict
 template <int WM, int NT, int PIPE, bool WNT>
 static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                             const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
-                            int I, int Rs, int gamma, int M, const GemmPlan& pg, const GemmPlan& pd, float* partial,
-                            int* counters, hipStream_t st) {
-    WRowsGateUp wgu{wg, wu, I, 2 * d};
-    XRowsConcat xc{ht, et, d, Rs, gamma, M};
-    const GemmShape shg = pg.shape(rows, 2 * d);
+                            int ew, int I, const RowTable& rt, const GemmPlan& pg, const GemmPlan& pd,
+                            float* partial, int* counters, hipStream_t st) {
+    WRowsGateUp wgu{wg, wu, I, d + ew};
+    XRowsConcat xc{ht, et, d, ew, rt};
+    const GemmShape shg = pg.shape(rows, d + ew);
     hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(shg.G), dim3(64 * TF_NW), 0, st, wgu, xc,
                        shg, act, I, partial, counters);
-    WRowsPlain wdn{wd, d, I};
-    XRowsPlain xa{act, (long)I};
-    const GemmShape shd = pd.shape(rows, I);
+    // the activation is [rows, 2I] bf16 hi/lo pairs
+    WRowsPairedK wdn{wd, d, I};
+    XRowsPlain xa{act, 2l * I};
+    const GemmShape shd = pd.shape(rows, 2 * I);
     hipLaunchKernelGGL((down_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(shd.G), dim3(64 * TF_NW), 0, st, wdn, xa,
-                       shd, hp, h, d, Rs, gamma, M, partial, counters + pg.counter_ints());
+                       shd, hp, h, d, rt, partial, counters + pg.counter_ints());
 }
 
-hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
-                           const void* gain_h, const void* gain_e, const void* w_gate, const void* w_up,
-                           const void* w_down, int b, int gamma, int d, int I, int V, int k, float eps,
-                           bool bf16, void* ht, void* et, void* act, void* hp, float* mlp_partial, int* counters,
-                           int* diag, hipStream_t stream) {
-    const int Rs = 1 + (gamma - 1) * k;
-    const int rows = b * Rs;
-    const int nrows = b * gamma + rows;
+template <class T>
+static void launch_norms(const void* h, const int32_t* root, const int32_t* context, const int32_t* topk,
+                         const void* emb, const void* gh, const void* ge, int b, int d, int V, const RowTable& rt,
+                         int npre, float eps, void* ht, void* et, int* diag, int* counters, int ncounters,
+                         hipStream_t stream) {
+    const int nvec = b * rt.gamma + b * rt.Rs * npre;
+    hipLaunchKernelGGL(rmsnorm_rows_kernel<T>, dim3(nvec), dim3(256), 0, stream, static_cast<const T*>(h), root,
+                       context, topk, static_cast<const T*>(emb), static_cast<const T*>(gh),
+                       static_cast<const T*>(ge), b, d, V, rt, npre, eps, static_cast<T*>(ht), static_cast<T*>(et),
+                       diag, counters, ncounters);
+}
+
+hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* context, const int32_t* topk_idx,
+                           const void* emb, const void* gain_h, const void* gain_e, const void* w_gate,
+                           const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
+                           bool bigram, float eps, bool bf16, void* ht, void* et, void* act, void* hp,
+                           float* mlp_partial, int* counters, int* diag, hipStream_t stream) {
+    const RowTable rt = make_row_table(gamma, k, bigram ? 1 : 0);
+    const int npre = bigram ? 2 : 1;
+    const int ew = npre * d;
+    const int rows = b * rt.Rs;
     if (bf16) {
-        const GemmPlan pg = gateup_plan(rows, d, I);
+        const GemmPlan pg = gateup_plan(rows, d + ew, I);
         const GemmPlan pd = down_plan(rows, d, I);
         const int ncounters = (int)(pg.counter_ints() + pd.counter_ints());
-        hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
-                           static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),
-                           static_cast<const uint16_t*>(gain_h), static_cast<const uint16_t*>(gain_e), b, gamma, d,
-                           V, k, Rs, eps, static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag, counters,
-                           ncounters);
+        launch_norms<uint16_t>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
+                               counters, ncounters, stream);
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         const uint16_t* wg = static_cast<const uint16_t*>(w_gate);
         const uint16_t* wu = static_cast<const uint16_t*>(w_up);
@@ -214,31 +221,27 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* to
         uint16_t* hpb = static_cast<uint16_t*>(hp);
         // both products of one call share the row blocking (same rows)
         if (pg.NT == 1)
-            launch_mlp_bf16<2, 1, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I,
-                                                                       Rs, gamma, k, pg, pd, mlp_partial, counters,
-                                                                       stream);
+            launch_mlp_bf16<2, 1, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew,
+                                                                       I, rt, pg, pd, mlp_partial, counters, stream);
         else if (pg.NT == 2)
-            launch_mlp_bf16<1, 2, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I,
-                                                                       Rs, gamma, k, pg, pd, mlp_partial, counters,
-                                                                       stream);
+            launch_mlp_bf16<1, 2, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew,
+                                                                       I, rt, pg, pd, mlp_partial, counters, stream);
         else if (pg.wnt)
-            launch_mlp_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma,
-                                                            k, pg, pd, mlp_partial, counters, stream);
+            launch_mlp_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg,
+                                                            pd, mlp_partial, counters, stream);
         else
-            launch_mlp_bf16<1, 4, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, I, Rs, gamma,
-                                                          k, pg, pd, mlp_partial, counters, stream);
+            launch_mlp_bf16<1, 4, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg,
+                                                          pd, mlp_partial, counters, stream);
     } else {
-        hipLaunchKernelGGL(rmsnorm_rows_kernel<float>, dim3(nrows), dim3(256), 0, stream,
-                           static_cast<const float*>(h), root, topk_idx, static_cast<const float*>(emb),
-                           static_cast<const float*>(gain_h), static_cast<const float*>(gain_e), b, gamma, d, V, k,
-                           Rs, eps, static_cast<float*>(ht), static_cast<float*>(et), diag, counters, 0);
+        launch_norms<float>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
+                            counters, 0, stream);
         hipLaunchKernelGGL(gateup_f32_kernel, dim3(cdiv(I, 64), cdiv(rows, 4)), dim3(256), 0, stream,
                            static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
-                           static_cast<const float*>(ht), static_cast<const float*>(et), rows, d, I, Rs, gamma, k,
+                           static_cast<const float*>(ht), static_cast<const float*>(et), rows, d, ew, I, rt,
                            static_cast<float*>(act));
         hipLaunchKernelGGL(down_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
                            static_cast<const float*>(w_down), static_cast<const float*>(act),
-                           static_cast<const float*>(h), rows, d, I, Rs, gamma, k, static_cast<float*>(hp));
+                           static_cast<const float*>(h), rows, d, I, rt, static_cast<float*>(hp));
     }
     return hipGetLastError();
 }
@@ -247,38 +250,32 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
                                   const void* gain_h, const void* gain_e, const void* w_lin, int b, int gamma, int d,
                                   int V, int k, float eps, bool bf16, void* ht, void* et, void* hp,
                                   float* mlp_partial, int* counters, int* diag, hipStream_t stream) {
-    const int Rs = 1 + (gamma - 1) * k;
-    const int rows = b * Rs;
-    const int nrows = b * gamma + rows;
+    const RowTable rt = make_row_table(gamma, k, 0);
+    const int rows = b * rt.Rs;
     if (bf16) {
         const GemmPlan pl = linear_plan(rows, d);
-        hipLaunchKernelGGL(rmsnorm_rows_kernel<uint16_t>, dim3(nrows), dim3(256), 0, stream,
-                           static_cast<const uint16_t*>(h), root, topk_idx, static_cast<const uint16_t*>(emb),
-                           static_cast<const uint16_t*>(gain_h), static_cast<const uint16_t*>(gain_e), b, gamma, d,
-                           V, k, Rs, eps, static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag, counters,
-                           (int)pl.counter_ints());
+        launch_norms<uint16_t>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
+                               counters, (int)pl.counter_ints(), stream);
         WRowsPlain wr{static_cast<const uint16_t*>(w_lin), d, 2 * d};
-        XRowsConcat xc{static_cast<const uint16_t*>(ht), static_cast<const uint16_t*>(et), d, Rs, gamma, k};
+        XRowsConcat xc{static_cast<const uint16_t*>(ht), static_cast<const uint16_t*>(et), d, d, rt};
         const GemmShape sh = pl.shape(rows, 2 * d);
         uint16_t* hpb = static_cast<uint16_t*>(hp);
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         if (pl.NT == 1)
             hipLaunchKernelGGL((linear_bf16_kernel<2, 1, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
-                               0, stream, wr, xc, sh, hpb, hb, d, Rs, gamma, k, mlp_partial, counters);
+                               0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
         else if (pl.NT == 2)
             hipLaunchKernelGGL((linear_bf16_kernel<1, 2, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
-                               0, stream, wr, xc, sh, hpb, hb, d, Rs, gamma, k, mlp_partial, counters);
+                               0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
         else
             hipLaunchKernelGGL((linear_bf16_kernel<1, 4, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
-                               0, stream, wr, xc, sh, hpb, hb, d, Rs, gamma, k, mlp_partial, counters);
+                               0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
     } else {
-        hipLaunchKernelGGL(rmsnorm_rows_kernel<float>, dim3(nrows), dim3(256), 0, stream,
-                           static_cast<const float*>(h), root, topk_idx, static_cast<const float*>(emb),
-                           static_cast<const float*>(gain_h), static_cast<const float*>(gain_e), b, gamma, d, V, k,
-                           Rs, eps, static_cast<float*>(ht), static_cast<float*>(et), diag, counters, 0);
+        launch_norms<float>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
+                            counters, 0, stream);
         hipLaunchKernelGGL(linear_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
                            static_cast<const float*>(w_lin), static_cast<const float*>(ht),
-                           static_cast<const float*>(et), static_cast<const float*>(h), rows, d, Rs, gamma, k,
+                           static_cast<const float*>(et), static_cast<const float*>(h), rows, d, rt,
                            static_cast<float*>(hp));
     }
     return hipGetLastError();

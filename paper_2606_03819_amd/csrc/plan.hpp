@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "limits.hpp"
+#include "rows.hpp"
 #include "work.hpp"
 
 namespace tf {
@@ -173,8 +174,10 @@ inline GemmPlan mlp_plan(int rows, int ntiles, int K, int wg_single) {
     p.wnt = TF_MLP_WNT && p.nrb == 1;
     return p;
 }
-inline GemmPlan gateup_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(I, 16), 2 * d, TF_MLP_WORKGROUPS); }
-inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d, 32), I, TF_DOWN_WORKGROUPS); }
+// gate/up over x = [h~ ; e~], K = 2d (3d for the bigram rows)
+inline GemmPlan gateup_plan(int rows, int K, int I) { return mlp_plan(rows, cdiv(I, 16), K, TF_MLP_WORKGROUPS); }
+// down projection over the activation's bf16 hi/lo pairs: K = 2I
+inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d, 32), 2 * I, TF_DOWN_WORKGROUPS); }
 // the linear approximator: [rows, 2d] x [d, 2d]^T
 inline GemmPlan linear_plan(int rows, int d) { return mlp_plan(rows, cdiv(d, 32), 2 * d, TF_DOWN_WORKGROUPS); }
 
@@ -193,9 +196,11 @@ struct Workspace {
 
 // Layout: [diag counters | LM-head scratch (stage 1 or stage 2) | normalised
 // h | normalised embeddings | SwiGLU activation | h' | SwiGLU partial sums |
-// SwiGLU arrival counters].  Stage 1 uses the first two only.
-inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, bool bf16) {
-    const int R = 1 + (gamma - 1) * k;
+// SwiGLU arrival counters].  Stage 1 uses the first two only.  `bigram`
+// sizes the w/ 2-prev rows (two embeddings per row, a 3d-wide input).
+inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, bool bf16, bool bigram = false) {
+    const int R = (int)cond_rows(gamma, k, bigram ? 1 : 0);
+    const int npre = bigram ? 2 : 1;
     const size_t es = bf16 ? 2 : 4;
     const int rows1 = b * gamma, rows2 = b * R;
     const size_t lm1 = lm_scratch_bytes(rows1, V, d, bf16), lm2 = lm_scratch_bytes(rows2, V, d, bf16);
@@ -208,15 +213,16 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     w.ht = off;
     off += align256((size_t)rows1 * d * es);
     w.et = off;
-    off += align256((size_t)rows2 * d * es);
+    off += align256((size_t)rows2 * npre * d * es);
     w.act = off;
-    off += align256((size_t)rows2 * I * es);
+    off += align256((size_t)rows2 * I * es * (bf16 ? 2 : 1));   // bf16: hi/lo pairs
     w.hp = off;
     off += align256((size_t)rows2 * d * es);
     size_t mp = 0;
     w.ncounters = 0;
     if (bf16) {
-        const GemmPlan pg = gateup_plan(rows2, d, I), pd = down_plan(rows2, d, I), pl = linear_plan(rows2, d);
+        const GemmPlan pg = gateup_plan(rows2, (1 + npre) * d, I), pd = down_plan(rows2, d, I),
+                       pl = linear_plan(rows2, d);
         const size_t a = pg.fix_floats(), c = pd.fix_floats(), l = pl.fix_floats();
         mp = a > c ? a : c;
         mp = mp > l ? mp : l;

@@ -32,6 +32,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "rows.hpp"
 #include "work.hpp"
 
 namespace tf {
@@ -188,7 +189,7 @@ __device__ __forceinline__ void gemm_segment(const WSrc& wsrc, const XSrc& xsrc,
         const int k = min(kc * KC + slot * 8, kmax);
 #pragma unroll
         for (int q = 0; q < NWL; ++q) {
-            const u32x4* src = reinterpret_cast<const u32x4*>(gw[q] + k);
+            const u32x4* src = reinterpret_cast<const u32x4*>(gw[q] + wsrc.kcol(k));
             if constexpr (WNT)
                 w[q] = __builtin_nontemporal_load(src);
             else
@@ -313,6 +314,23 @@ struct WRowsPlain {
         const int n = tile * 32 + r;
         return n < N ? w + (size_t)n * K : nullptr;
     }
+    __device__ __forceinline__ int kcol(int k) const { return k; }
+};
+
+// Weight rows [N, K] read against an activation stored as bf16 hi/lo pairs
+// interleaved by 8 (activation column k' holds the hi part of element
+// (k'/16)*8 + k'%8 when (k'/8) is even, the lo part when odd): reduction
+// column k' reads weight column kcol(k').  The two lanes that load the hi
+// and lo columns of the same 8 weights read the same 16 bytes, so the weight
+// bytes fetched do not change.
+struct WRowsPairedK {
+    const uint16_t* w;
+    int N, K;   // K: weight columns (half the activation width)
+    __device__ __forceinline__ const uint16_t* row(int tile, int r) const {
+        const int n = tile * 32 + r;
+        return n < N ? w + (size_t)n * K : nullptr;
+    }
+    __device__ __forceinline__ int kcol(int k) const { return ((k >> 4) << 3) | (k & 7); }
 };
 
 // SwiGLU input projections: tile rows 0..15 are gate rows 16*tile.., tile
@@ -327,6 +345,7 @@ struct WRowsGateUp {
         if (i >= I) return nullptr;
         return (r < 16 ? gate : up) + (size_t)i * K;
     }
+    __device__ __forceinline__ int kcol(int k) const { return k; }
 };
 
 // -------------------------------------------------------- activation sources
@@ -337,17 +356,19 @@ struct XRowsPlain {
     __device__ __forceinline__ const uint16_t* ptr(int r, int k) const { return x + (size_t)r * ld + k; }
 };
 
-// Input of the SwiGLU: row r is [ h~(depth of r) ; e~(r) ] (Eq. 1).
+// Input of the SwiGLU (or linear layer): row r is [ h~(depth of r) ; e~(r) ]
+// (Eq. 1), where e~(r) holds the normalised embeddings of the row's previous
+// token(s): ew = d for one token, 2d for the bigram of the w/ 2-prev rows.
 struct XRowsConcat {
     const uint16_t* ht;   // [b*gamma, d] normalised drafter states
-    const uint16_t* et;   // [b*R, d] normalised embeddings of the previous tokens
-    int d, Rs, gamma, M;
+    const uint16_t* et;   // [b*R, ew] normalised embeddings of the previous tokens
+    int d, ew;
+    RowTable t;
     __device__ __forceinline__ const uint16_t* ptr(int r, int k) const {
-        if (k >= d) return et + (size_t)r * d + (k - d);
-        const int s = r / Rs;
-        const int rl = r - s * Rs;
-        const int depth = rl == 0 ? 1 : 2 + (rl - 1) / M;
-        return ht + (size_t)(s * gamma + depth - 1) * d + k;
+        if (k >= d) return et + (size_t)r * ew + (k - d);
+        const int s = r / t.Rs;
+        const int rl = r - s * t.Rs;
+        return ht + (size_t)(s * t.gamma + t.depth(rl) - 1) * d + k;
     }
 };
 
@@ -606,7 +627,10 @@ struct EpiFixup {
 // SwiGLU activation: a[r, i] = bf16( silu(g) * u ).
 template <int WM, int NT>
 struct EpiSwiGLU {
-    uint16_t* out;   // [R, I]
+    // [R, 2I]: a = silu(g) * u as bf16 pairs, hi = bf16(a), lo = bf16(a - hi),
+    // interleaved by 8 (hi of elements 8j..8j+7, then their lo), so the down
+    // projection reads the activation at about 16 significant bits
+    uint16_t* out;
     int I;
     __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char*,
                                           const GemmShape& sh) {
@@ -624,23 +648,24 @@ struct EpiSwiGLU {
                 for (int jg = 0; jg < 2; ++jg) {
                     const int i = tile * 16 + 8 * jg + 4 * (lane >> 5);
                     if (i >= I) continue;
-                    uint32_t packed[2];
+                    uint32_t hi2[2], lo2[2];
 #pragma unroll
                     for (int q = 0; q < 2; ++q) {
-                        uint32_t lo, hi;
-                        {
-                            const float g = acc[mt][nt][4 * jg + 2 * q];
-                            const float u = acc[mt][nt][4 * jg + 2 * q + 8];
-                            lo = f32_to_bf16_bits(g / (1.0f + __expf(-g)) * u);
+                        uint32_t h[2], l[2];
+#pragma unroll
+                        for (int e = 0; e < 2; ++e) {
+                            const float g = acc[mt][nt][4 * jg + 2 * q + e];
+                            const float u = acc[mt][nt][4 * jg + 2 * q + e + 8];
+                            const float a = g / (1.0f + __expf(-g)) * u;
+                            h[e] = f32_to_bf16_bits(a);
+                            l[e] = f32_to_bf16_bits(a - bf16_bits_to_f32(h[e]));
                         }
-                        {
-                            const float g = acc[mt][nt][4 * jg + 2 * q + 1];
-                            const float u = acc[mt][nt][4 * jg + 2 * q + 9];
-                            hi = f32_to_bf16_bits(g / (1.0f + __expf(-g)) * u);
-                        }
-                        packed[q] = lo | (hi << 16);
+                        hi2[q] = h[0] | (h[1] << 16);
+                        lo2[q] = l[0] | (l[1] << 16);
                     }
-                    *reinterpret_cast<uint2*>(out + (size_t)r * I + i) = uint2{packed[0], packed[1]};
+                    uint16_t* o = out + (size_t)r * 2 * I + (size_t)(i >> 3) * 16 + (i & 7);
+                    *reinterpret_cast<uint2*>(o) = uint2{hi2[0], hi2[1]};
+                    *reinterpret_cast<uint2*>(o + 8) = uint2{lo2[0], lo2[1]};
                 }
             }
         }
@@ -652,7 +677,8 @@ template <int WM, int NT>
 struct EpiResidual {
     uint16_t* out;        // [R, d]
     const uint16_t* h;    // [b, gamma, d]
-    int d, Rs, gamma, M;
+    int d;
+    RowTable t;
     __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char*,
                                           const GemmShape& sh) {
         const int lane = threadIdx.x & 63;
@@ -661,10 +687,9 @@ struct EpiResidual {
         for (int nt = 0; nt < NT; ++nt) {
             const int r = it.row0 + nt * 32 + (lane & 31);
             if (r >= sh.R) continue;
-            const int s = r / Rs;
-            const int rl = r - s * Rs;
-            const int depth = rl == 0 ? 1 : 2 + (rl - 1) / M;
-            const uint16_t* hrow = h + (size_t)(s * gamma + depth - 1) * d;
+            const int s = r / t.Rs;
+            const int rl = r - s * t.Rs;
+            const uint16_t* hrow = h + (size_t)(s * t.gamma + t.depth(rl) - 1) * d;
 #pragma unroll
             for (int mt = 0; mt < WM; ++mt) {
                 const int tile = it.t0 + wave * WM + mt;

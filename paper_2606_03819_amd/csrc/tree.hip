@@ -22,6 +22,7 @@
 #include "common.hpp"
 #include "launch.hpp"
 #include "plan.hpp"
+#include "rows.hpp"
 
 namespace tf {
 
@@ -31,12 +32,21 @@ constexpr int kTreeLdsBudget = 144 * 1024;
 constexpr int kTreeThreads = 1024;  // all waves preload; wave 0 alone selects
 constexpr int kTreeRegSlots = 16;   // frontier slots per lane held in registers
 
+// Row tables the selection expands into.  Single: a node whose token is
+// candidate m of its depth i expands into row 1 + (i-1)*M + m.  Marginal:
+// every node above depth gamma expands into the marginal row of the next
+// depth.  Bigram (w/ 2-prev): row 1 + m at depth 1, else
+// 1 + M + (i-2)*M*M + m2*M + m with m2 the parent's candidate index.
+constexpr int kTreeSingle = 0;
+constexpr int kTreeMarginal = 1;
+constexpr int kTreeBigram = 2;
+
 struct TreeArgs {
     const int32_t* cond_idx;
     const float* cond_lp;
     const int32_t* topk;
     int gamma, M, K2, B, Rs, P;   // P = leading ranks of each row cached in LDS
-    int marginal;                 // 1: rows are the gamma marginal rows, every node above depth gamma expands
+    int mode;                     // kTreeSingle, kTreeMarginal or kTreeBigram
     int32_t* tok;
     int32_t* par;
     int32_t* dep;
@@ -115,7 +125,7 @@ __device__ __forceinline__ void tree_preload(const TreeArgs& a, const TreeLds& t
                                              const int32_t* ridx) {
     const int tid = threadIdx.x;
     for (int s = tid; s <= a.B; s += kTreeThreads) t.f_depth[s] = 0;
-    if (!a.marginal)
+    if (a.mode != kTreeMarginal)
         for (int e = tid; e < a.gamma * a.M; e += kTreeThreads) t.tk[e] = a.topk[(size_t)seq * a.gamma * a.M + e];
     const int ncache = a.Rs * a.P;
     for (int e0 = tid; e0 < ncache; e0 += 4 * kTreeThreads) {
@@ -140,17 +150,25 @@ __device__ __forceinline__ void tree_preload(const TreeArgs& a, const TreeLds& t
     }
 }
 
-// Child row of a popped node: 1 + (depth-1)*M + m if its token is candidate m
-// of its depth, else -1; in marginal mode the marginal row of the next depth
-// (row `depth`) for every node above depth gamma.  Uniform across the wave.
-__device__ __forceinline__ int tree_child_row(const TreeArgs& a, const TreeLds& t, int depth, int tok, int lane) {
+// Child row of a node popped from row `row` (see the row tables above), -1
+// if it does not expand.  In bigram mode the parent's candidate index is read
+// off `row`: a depth-2 row 1 + m2, a deeper row 1 + M + ... + m2*M + m1 whose
+// last index is the parent's.  Uniform across the wave.
+__device__ __forceinline__ int tree_child_row(const TreeArgs& a, const TreeLds& t, int depth, int tok, int row,
+                                              int lane) {
     if (depth >= a.gamma) return -1;
-    if (a.marginal) return depth;
+    if (a.mode == kTreeMarginal) return depth;
     for (int m0 = 0; m0 < a.M; m0 += 64) {
         const int m = m0 + lane;
         const bool hit = m < a.M && t.tk[(depth - 1) * a.M + m] == tok;
         const unsigned long long bal = __ballot(hit);
-        if (bal != 0ull) return 1 + (depth - 1) * a.M + m0 + (__ffsll((long long)bal) - 1);
+        if (bal != 0ull) {
+            const int mc = m0 + (__ffsll((long long)bal) - 1);
+            if (a.mode == kTreeSingle) return 1 + (depth - 1) * a.M + mc;
+            if (depth == 1) return 1 + mc;
+            const int mp = depth == 2 ? row - 1 : (row - 1 - a.M) % a.M;
+            return 1 + a.M + (depth - 2) * a.M * a.M + mp * a.M + mc;
+        }
     }
     return -1;
 }
@@ -258,7 +276,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a
         const int row = __builtin_amdgcn_readlane(my_row, owner);
         const float pscore = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_ps), owner));
         const int tok = get_idx(row, rank);
-        const int child_row = tree_child_row(a, t, depth, tok, lane);
+        const int child_row = tree_child_row(a, t, depth, tok, row, lane);
         if (lane == 0) {
             t.n_tok[n] = tok;
             t.n_par[n] = slot - 1;
@@ -342,7 +360,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
         const int slot = c_slot(best.meta), rank = c_rank(best.meta);
         const int row = t.f_row[slot];
         const int tok = get_idx(row, rank);
-        const int child_row = tree_child_row(a, t, depth, tok, lane);
+        const int child_row = tree_child_row(a, t, depth, tok, row, lane);
         wave_lds_sync();   // every lane has read the frontier before it changes
         if (lane == 0) {
             t.n_tok[n] = tok;
@@ -380,15 +398,15 @@ size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks
 }
 
 hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, const int32_t* topk_idx, int b,
-                             int gamma, int k, int topk2, int B, bool marginal, int32_t* node_token,
+                             int gamma, int k, int topk2, int B, int mode, int32_t* node_token,
                              int32_t* node_parent, int32_t* node_depth, float* node_score, int32_t* node_child_row,
                              hipStream_t stream) {
-    const int M = marginal ? 0 : k;
-    const int Rs = marginal ? gamma : 1 + (gamma - 1) * k;
+    const int M = mode == kTreeMarginal ? 0 : k;
+    const int Rs = mode == kTreeMarginal ? gamma : (int)cond_rows(gamma, k, mode == kTreeBigram ? 1 : 0);
     int P = 0;
     const size_t lds = tree_lds_bytes(B, gamma, M, Rs, topk2, &P);
     if (lds == 0) return hipErrorInvalidValue;
-    TreeArgs a{cond_idx, cond_lp, topk_idx, gamma, M, topk2, B, Rs, P, marginal ? 1 : 0,
+    TreeArgs a{cond_idx, cond_lp, topk_idx, gamma, M, topk2, B, Rs, P, mode,
                node_token, node_parent, node_depth, node_score, node_child_row};
     const void* fn;
     if (B + 1 <= 64)

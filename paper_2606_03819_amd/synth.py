@@ -13,9 +13,11 @@ checkpoints and evaluation prompts that are not available here):
   the tiny workload stays fp32;
 * drafter hidden states ``h[b, gamma, d]`` ~ N(0, 1);
 * the w/ Linear workloads draw ``W_lin [d, 2d]`` from N(0, 0.02) in place of
-  the three SwiGLU matrices;
+  the three SwiGLU matrices; the w/ 2-prev workloads draw gate and up as
+  ``[I, 3d]``;
 * both RMSNorm gains are ones (no biases anywhere);
-* the root token of each sequence is uniform over the vocabulary.
+* the root token of each sequence, and the context token before it, are
+  uniform over the vocabulary.
 
 Weights use one seed per model shape (tiny 1, 4B-shaped 2, 8B-shaped 3), so the
 three 8B-shaped workloads share weights.  Hidden states use one seed per
@@ -60,11 +62,16 @@ class Workload:
     weight_seed: int
     state_seed: int       # per-sequence seed = state_seed + s when b > 1
     description: str = ""
-    approximator: str = "swiglu"   # "swiglu" (Eq. 1) or "linear" (the w/ Linear ablation)
+    # "swiglu" (Eq. 1), "linear" (the w/ Linear ablation) or "2prev" (the
+    # w/ 2-prev ablation: SwiGLU on [h~; e~(prev1); e~(prev2)])
+    approximator: str = "swiglu"
 
     @property
     def rows(self) -> int:
-        """Conditional rows per sequence: one for depth 1, k per deeper depth."""
+        """Conditional rows per sequence: one for depth 1, k per deeper depth
+        (2prev: one, then k at depth 2 and k*k per deeper depth)."""
+        if self.approximator == "2prev":
+            return 1 if self.gamma == 1 else 1 + self.k + (self.gamma - 2) * self.k * self.k
         return 1 + (self.gamma - 1) * self.k
 
     @property
@@ -105,6 +112,9 @@ WORKLOADS: Dict[str, Workload] = {
                  "Qwen3-8B-shaped bf16, SwiGLU width 12288 (the paper's AR-approximator size)"),
         # the w/ Linear ablation: one [d, 2d] layer in place of the SwiGLU
         # (I is unused); same LM head, embedding and states as qwen3-8b-shape
+        # the w/ 2-prev ablation: bigram rows (1 + 8 + 14*64 = 905 per sequence)
+        Workload("qwen3-8b-shape-2prev", 1, 4096, 151936, 16, 8, 32, 4096, "bf16", 1.0, 3, 13,
+                 "Qwen3-8B-shaped bf16, w/ 2-prev approximator (905 bigram rows)", "2prev"),
         Workload("qwen3-8b-shape-linear", 1, 4096, 151936, 16, 8, 32, 0, "bf16", 1.0, 3, 13,
                  "Qwen3-8B-shaped bf16, w/ Linear approximator", "linear"),
     ]
@@ -148,8 +158,9 @@ def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> D
     if w.approximator == "linear":
         out["w_lin"] = _normal((w.d, 2 * w.d), weight_std, g, device, dt)
     else:
-        out["w_gate"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
-        out["w_up"] = _normal((w.I, 2 * w.d), weight_std, g, device, dt)
+        kin = 3 * w.d if w.approximator == "2prev" else 2 * w.d
+        out["w_gate"] = _normal((w.I, kin), weight_std, g, device, dt)
+        out["w_up"] = _normal((w.I, kin), weight_std, g, device, dt)
         out["w_down"] = _normal((w.d, w.I), weight_std, g, device, dt)
     out["norm_h_gain"] = torch.ones(w.d, device=device, dtype=dt)
     out["norm_e_gain"] = torch.ones(w.d, device=device, dtype=dt)
@@ -157,17 +168,20 @@ def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> D
 
 
 def make_states(w: Workload, device="cpu") -> Dict[str, torch.Tensor]:
-    """Drafter hidden states h[b, gamma, d] ~ N(0,1) and root tokens [b]."""
+    """Drafter hidden states h[b, gamma, d] ~ N(0,1), root tokens [b] and the
+    context token before each root [b] (read by the 2-prev rows only)."""
     device = torch.device(device)
-    hs, roots = [], []
+    hs, roots, ctx = [], [], []
     for s in range(w.b):
         seed = w.state_seed + s if w.b > 1 else w.state_seed
         g = _generator(device, seed)
         hs.append(_normal((w.gamma, w.d), 1.0, g, device, w.torch_dtype))
         roots.append(torch.randint(0, w.V, (1,), generator=g, device=device, dtype=torch.int64))
+        ctx.append(torch.randint(0, w.V, (1,), generator=g, device=device, dtype=torch.int64))
     h = torch.stack(hs, 0).contiguous()
     root = torch.cat(roots).to(torch.int32)
-    return {"h": h, "root": root}
+    context = torch.cat(ctx).to(torch.int32)
+    return {"h": h, "root": root, "context": context}
 
 
 def default_device_for(w: Workload) -> str:

@@ -65,12 +65,14 @@ def check_tree_exact(gpu_tree, ref_tree, what=""):
         assert np.array_equal(g, o), f"{what}: tree field {f} differs\nGPU {g}\noracle {o}"
 
 
-def replay_tree(gpu_tree, row_lp, topk_seq, gamma, M, B, tol, what=""):
+def replay_tree(gpu_tree, row_lp, topk_seq, gamma, M, B, tol, what="", bigram=False):
     """End-to-end tree check against oracle rows.
 
     gpu_tree: dict of numpy arrays for one sequence; row_lp: dict row -> full
     oracle log-prob row (float64, length V) for every row the replay needs;
     topk_seq: [gamma, M] stage-1 candidates the rows were conditioned on.
+    bigram: the rows are the w/ 2-prev table (a node's row depends on its own
+    and its parent's candidate index).
     """
     tok = np.asarray(gpu_tree["token"])
     par = np.asarray(gpu_tree["parent"])
@@ -79,6 +81,7 @@ def replay_tree(gpu_tree, row_lp, topk_seq, gamma, M, B, tol, what=""):
     osc = np.zeros(B)
     children = {-1: set()}
     rowof = {-1: 0}
+    slot = {-1: -1}
     order = {}
     worst = 0.0
 
@@ -106,10 +109,16 @@ def replay_tree(gpu_tree, row_lp, topk_seq, gamma, M, B, tol, what=""):
         assert abs(gsc[j] - osc[j]) <= tol, f"{what}: pop {j} score {gsc[j]} vs oracle {osc[j]}"
         children[p].add(int(tok[j]))
         children[j] = set()
+        hits = np.nonzero(np.asarray(topk_seq[dep[j] - 1]) == tok[j])[0]
+        slot[j] = int(hits[0]) if hits.size else -1
         if dep[j] < gamma:
-            hits = np.nonzero(np.asarray(topk_seq[dep[j] - 1]) == tok[j])[0]
             if hits.size:
-                rowof[j] = 1 + (dep[j] - 1) * M + int(hits[0])
+                if not bigram:
+                    rowof[j] = 1 + (dep[j] - 1) * M + slot[j]
+                elif dep[j] == 1:
+                    rowof[j] = 1 + slot[j]
+                else:
+                    rowof[j] = 1 + M + (dep[j] - 2) * M * M + slot[p] * M + slot[j]
                 assert int(gpu_tree["child_row"][j]) == rowof[j], f"{what}: node {j} child_row"
             else:
                 assert int(gpu_tree["child_row"][j]) == -1
@@ -133,6 +142,13 @@ def to_cpu_tree(tree, s):
 
 
 def _oracle_rows(o_in, w, topk_seq, s):
+    if w.approximator == "2prev":
+        depth, _, _ = oracle.row_table_2prev(w.gamma, w.k)
+        p1, p2 = oracle.previous_pairs(int(o_in["context"][s]), int(o_in["root"][s]), topk_seq, w.gamma, w.k)
+        hp = oracle.ar_approximator_2prev(o_in["h"][s], p1, p2, depth, o_in["emb"], o_in["norm_h_gain"],
+                                          o_in["norm_e_gain"], o_in["w_gate"], o_in["w_up"], o_in["w_down"],
+                                          mirror_bf16=(w.dtype == "bf16"))
+        return oracle.conditional_stage(hp, o_in["lm_head"], w.topk2, w.inv_temperature, keep_full=True)
     depth, _ = oracle.row_table(w.gamma, w.k)
     prev = oracle.previous_tokens(int(o_in["root"][s]), topk_seq, w.gamma, w.k)
     if "w_lin" in o_in:
@@ -161,7 +177,14 @@ def check_draft(w, g, o_in, seqs, tol, log=print):
     The oracle never consumes a HIP-path output.
     """
     from paper_2606_03819_amd import binding
-    dr = binding.Drafter(g, w.b, w.gamma, w.k, w.B, w.inv_temperature)
+    bigram = w.approximator == "2prev"
+    if bigram:
+        dr = binding.Drafter2Prev(g, w.b, w.gamma, w.k, w.B, w.inv_temperature)
+        dr.context = g["context"]
+        gpu_tree_fn, oracle_tree_fn = binding.treeflash_build_tree_2prev, oracle.build_tree_2prev
+    else:
+        dr = binding.Drafter(g, w.b, w.gamma, w.k, w.B, w.inv_temperature)
+        gpu_tree_fn, oracle_tree_fn = binding.treeflash_build_tree, oracle.build_tree
     idx1, lp1 = dr.stage1(g["h"])
     gpu_topk = idx1.cpu().numpy()
     gpu_lp1 = lp1.cpu().numpy()
@@ -188,11 +211,12 @@ def check_draft(w, g, o_in, seqs, tol, log=print):
         assert lse_err <= tol, f"{w.name}: log-sum-exp off by {lse_err}"
         t = {k: v[s] for k, v in tree_tf.items()}
         rl = {r: rows["logprob"][r] for r in rows_needed(t, w.B)}
-        stats[f"tree_replay_seq{s}"] = replay_tree(t, rl, o_topk[s], w.gamma, w.k, w.B, tol, f"{w.name} tree seq {s}")
-        gt = binding.treeflash_build_tree(torch.from_numpy(rows["cond_idx"][None]).cuda(),
-                                          torch.from_numpy(rows["cond_logprob"][None]).cuda(),
-                                          torch.from_numpy(o_topk[s][None]).to(torch.int32).cuda(), w.B)
-        ref = oracle.build_tree(rows["cond_idx"], rows["cond_logprob"], o_topk[s], w.gamma, w.k, w.B)
+        stats[f"tree_replay_seq{s}"] = replay_tree(t, rl, o_topk[s], w.gamma, w.k, w.B, tol, f"{w.name} tree seq {s}",
+                                                   bigram=bigram)
+        gt = gpu_tree_fn(torch.from_numpy(rows["cond_idx"][None]).cuda(),
+                         torch.from_numpy(rows["cond_logprob"][None]).cuda(),
+                         torch.from_numpy(o_topk[s][None]).to(torch.int32).cuda(), w.B)
+        ref = oracle_tree_fn(rows["cond_idx"], rows["cond_logprob"], o_topk[s], w.gamma, w.k, w.B)
         check_tree_exact(to_cpu_tree(gt, 0), ref, f"{w.name} tree kernel seq {s}")
     # end to end
     full = {k: v.clone() for k, v in dr.step(g["h"], g["root"]).items()}

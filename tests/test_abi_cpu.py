@@ -156,6 +156,67 @@ def test_linear_workspace_fits_in_the_swiglu_one():
         assert _linear(b=b, gamma=gamma, d=d, V=V, k=k, wsb=n16 - 1) == WORKSPACE
 
 
+def _hidden2(**over):
+    a = dict(h=FAKE, ctx=FAKE, root=FAKE, topk=FAKE, emb=FAKE, gh=None, ge=None, wg=FAKE, wu=FAKE, wd=FAKE,
+             b=1, gamma=16, d=4096, I=4096, V=151936, k=8, eps=1e-6, dt=BF16, hp=FAKE2, ws=FAKE, wsb=1 << 40,
+             st=None)
+    a.update(over)
+    return binding.lib().treeflash_arapprox_2prev_hidden(
+        a["h"], a["ctx"], a["root"], a["topk"], a["emb"], a["gh"], a["ge"], a["wg"], a["wu"], a["wd"], a["b"],
+        a["gamma"], a["d"], a["I"], a["V"], a["k"], a["eps"], a["dt"], a["hp"], a["ws"], a["wsb"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(h=None), INVALID), (dict(ctx=None), INVALID), (dict(ctx=FAKE + 2), INVALID), (dict(root=None), INVALID),
+    (dict(topk=None), INVALID), (dict(emb=None), INVALID), (dict(wg=None), INVALID), (dict(wu=FAKE + 8), INVALID),
+    (dict(hp=None), INVALID), (dict(I=24), INVALID), (dict(k=0), INVALID), (dict(gamma=256), INVALID),
+    # 32 * (1 + 64 + 14 * 64 * 64) bigram rows exceed the 2^20 row limit
+    (dict(b=32, k=64), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(wsb=4096), WORKSPACE),
+])
+def test_arapprox_2prev_hidden_rejects(over, code):
+    assert _hidden2(**over) == code
+
+
+def test_workspace_2prev_covers_the_bigram_rows():
+    lib = binding.lib()
+    for (b, gamma, d, I, V, k) in [(1, 16, 4096, 4096, 151936, 8), (2, 5, 96, 64, 1000, 3), (3, 1, 64, 32, 300, 2)]:
+        two = lib.treeflash_workspace_bytes_2prev(b, gamma, d, I, V, k, 8, BF16)
+        assert two > 0
+        assert _hidden2(b=b, gamma=gamma, d=d, I=I, V=V, k=k, wsb=two - 1) == WORKSPACE
+    assert lib.treeflash_workspace_bytes_2prev(32, 16, 4096, 4096, 151936, 64, 8, BF16) == 0
+
+
+def _tree2(**over):
+    a = dict(ci=FAKE, cl=FAKE, tk=FAKE, b=1, gamma=16, k=8, topk2=32, B=32, tok=FAKE2, par=FAKE2, dep=FAKE2,
+             sc=FAKE2, cr=None, st=None)
+    a.update(over)
+    return binding.lib().treeflash_build_tree_2prev(a["ci"], a["cl"], a["tk"], a["b"], a["gamma"], a["k"],
+                                                    a["topk2"], a["B"], a["tok"], a["par"], a["dep"], a["sc"],
+                                                    a["cr"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(ci=None), INVALID), (dict(tk=None), INVALID), (dict(sc=None), INVALID), (dict(B=0), INVALID),
+    (dict(B=5000), INVALID), (dict(k=0), INVALID), (dict(cr=FAKE + 2), INVALID),
+    (dict(b=32, k=64), INVALID),
+    (dict(gamma=2, k=2, topk2=4, B=13), INVALID),
+])
+def test_build_tree_2prev_rejects(over, code):
+    assert _tree2(**over) == code
+
+
+def test_binding_checks_row_counts_before_calling():
+    # [1, R, topk2] rows that do not match the candidates are refused in Python
+    import torch
+    ci = torch.zeros((1, 7, 4), dtype=torch.int32)
+    tk = torch.zeros((1, 3, 2), dtype=torch.int32)
+    with pytest.raises(ValueError):
+        binding.treeflash_build_tree(ci, ci.float(), tk, 4)
+    with pytest.raises(ValueError):
+        binding.treeflash_build_tree_2prev(ci, ci.float(), tk, 4)
+
+
 def _tree(**over):
     a = dict(ci=FAKE, cl=FAKE, tk=FAKE, b=1, gamma=16, k=8, topk2=32, B=32, tok=FAKE2, par=FAKE2, dep=FAKE2,
              sc=FAKE2, cr=None, st=None)

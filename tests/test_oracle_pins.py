@@ -102,9 +102,7 @@ def pin_ar_closed_form(rng, d=12, mirror=False):
     if mirror:
         hn = hn.to(torch.float32).to(torch.bfloat16).to(torch.float64)
         en = en.to(torch.float32).to(torch.bfloat16).to(torch.float64)
-    a = F.silu(hn[:, perm]) * en
-    if mirror:
-        a = a.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    a = F.silu(hn[:, perm]) * en          # the activation is not a rounding point
     want = th + a
     if mirror:
         want = want.to(torch.float32).to(torch.bfloat16).to(torch.float64)
