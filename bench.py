@@ -46,7 +46,7 @@ RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
 PROFILES = os.path.join(ROOT, "profiles")
 # sources that define the LM-head GEMM kernel; counters taken on another
 # version of them say nothing about this one
-KERNEL_SOURCES = ["lmhead.hip", "stream_gemm.hpp", "work.hpp", "plan.hpp", "common.hpp", "limits.hpp"]
+KERNEL_SOURCES = ["lmhead.hip", "stream_gemm.hpp", "work.hpp", "plan.hpp", "rows.hpp", "common.hpp", "limits.hpp"]
 COPY_BYTES = 1 << 30      # plain copy used to scale the traffic counters
 
 
@@ -58,10 +58,13 @@ def kernel_source_digest() -> str:
     return hsh.hexdigest()
 
 
-def lm_kernel_pattern(rows: int) -> str:
+def lm_kernel_pattern(rows: int, d: int) -> str:
     """Regex for the bf16 LM-head kernel instance the plan picks for `rows` rows
-    (template arguments: weight tiles per wave, activation tiles, waves, ...)."""
+    (template arguments: weight tiles per wave, activation tiles, waves, ...):
+    128-row tiles with d a multiple of 64 go to the LDS-DMA kernel."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
+    if nt == 4 and d % 64 == 0:
+        return r"lmhead_dma_kernel<\d+, 4, "
     return rf"lmhead_bf16_kernel<\d+, {nt}, "
 
 
@@ -164,7 +167,7 @@ def summarize_trace(args):
 def summarize_pmc(args):
     """HBM traffic of the stage-2 LM-head kernel, scaled by a plain copy of known size."""
     w = synth.get_workload(args.workload)
-    pattern = lm_kernel_pattern(w.rows * w.b)
+    pattern = lm_kernel_pattern(w.rows * w.b, w.d)
 
     def per_kernel(path, counter):
         cur = _db(path).cursor()
@@ -447,8 +450,8 @@ def main():
         roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = read_traffic(w.name)
-    roof["kernel"] = "lmhead_bf16_kernel (stage-2 LM head on h')" if w.dtype == "bf16" \
-        else "lmhead_f32_kernel (stage-2 LM head on h')"
+    roof["kernel"] = ("stage-2 LM head on h': " + lm_kernel_pattern(rows, d).split("<")[0]) if w.dtype == "bf16" \
+        else "stage-2 LM head on h': lmhead_f32_kernel"
     roof["kernel_us"] = gemm
     roof["alg_bytes_per_launch"] = alg_bytes
     roof["alg_flops_per_launch"] = alg_flops

@@ -63,6 +63,201 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
     }
 }
 
+// ------------------------------------------------ bf16 / MFMA, LDS DMA
+//
+// The same vocabulary slices with the weight and activation tiles copied
+// from memory straight into LDS (global_load_lds_dwordx4, no register
+// staging), so that the registers go to accumulators: NW waves of WM weight
+// tiles each.  k advances KC at a time through a ring of S LDS stages; every
+// stage holds each wave's WM weight tiles ([32 rows][KC]) and the activation
+// tile ([32*NT rows][KC]).  One DMA instruction fills 1 KiB: 1024 / (2 KC)
+// whole rows, lane l taking 16-byte slot l % (KC / 8) of row l / (KC / 8).
+// Slots are XOR-swizzled per row so that the 16 rows one quarter-wave reads
+// at one logical slot cover all 64 banks.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+
+template <int WM, int NT, int NW, int KC, int S>
+struct DmaTraits {
+    static constexpr int ROWB = KC * 2;                       // bytes of one tile row in one stage
+    static constexpr int SLOTS = KC / 8;                      // 16-byte slots per row
+    static constexpr int RPI = 1024 / ROWB;                   // rows per DMA instruction
+    static constexpr int WTILE = 32 * ROWB;                   // one weight tile of one stage
+    static constexpr int WINSTR = 32 / RPI;                   // DMA instructions per weight tile
+    static constexpr int WBYTES = NW * WM * WTILE;            // all waves' weight tiles
+    static constexpr int XBYTES = 32 * NT * ROWB;             // the activation tile
+    static constexpr int STAGE = WBYTES + XBYTES;
+    static constexpr int RING = S * STAGE;
+    static constexpr int XLOADS = XBYTES / 1024 / NW;         // activation DMA instructions per wave
+    static constexpr int LPS = WINSTR * WM + XLOADS;          // DMA instructions per wave per step
+    static_assert(KC == 32 || KC == 64, "k step");
+    static_assert(XBYTES % (1024 * NW) == 0, "every wave copies the same share of the activation tile");
+    static_assert(LPS * (S - 2) < 64, "vmcnt range");
+    // byte offset of 16-byte logical slot `ls` of row `r`
+    __device__ static __forceinline__ int slot(int r, int ls) {
+        const int sw = KC == 32 ? ((r >> 2) & 3) : ((r >> 1) & 7);
+        return r * ROWB + ((ls ^ sw) << 4);
+    }
+};
+
+// wait until at most N of this wave's memory loads are outstanding (also a
+// compiler barrier for memory operations)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+    asm volatile("" ::: "memory");
+}
+
+// wait for the loads of the step about to be computed: `ahead` later steps
+// (0 .. S-2) may still be in flight
+template <int LPS, int S>
+__device__ __forceinline__ void wait_steps_ahead(int ahead) {
+    if constexpr (S >= 4) {
+        if (ahead >= 2) {
+            wait_vmcnt<2 * LPS>();
+            return;
+        }
+    }
+    if (ahead >= 1)
+        wait_vmcnt<LPS>();
+    else
+        wait_vmcnt<0>();
+}
+
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int WM, int NT, int NW, int KC, int S>
+__global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,
+                                                                const uint16_t* __restrict__ w, GemmShape sh,
+                                                                SliceMap map, int V, float sl2,
+                                                                float* __restrict__ part, int* __restrict__ diag) {
+    using T = DmaTraits<WM, NT, NW, KC, S>;
+    using E = EpiLmHead<WM, NT, NW>;
+    static_assert(E::MERGE_BYTES <= T::RING, "the epilogue reuses the ring");
+    extern __shared__ __align__(16) unsigned char dyn[];
+    if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    E epi{part, V, sl2};
+    const int L = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int rb = L % sh.nrb;
+    const int g = L / sh.nrb;
+    GemmShape se = sh;   // the epilogue indexes partials by slice
+    se.nchunks = map.G * map.rmax;
+    const int nsteps = sh.K / KC;
+    // this lane's piece of every 1 KiB DMA block
+    const int lrow = lane / T::SLOTS;
+    const int lphys = lane % T::SLOTS;
+
+    for (int r = 0; r < map.rmax; ++r) {
+        Segment seg;
+        seg.g = L;
+        seg.item = seg.chunk = g * map.rmax + r;
+        seg.rb = rb;
+        slice_tiles(map, seg.chunk, seg.t0, seg.t1);
+        seg.kc0 = 0;
+        seg.kc1 = sh.nk;
+        seg.row0 = rb * 32 * NT;
+        seg.gfirst = L;
+        seg.npieces = 1;
+        if (seg.t0 == seg.t1) {   // empty slice: a partial the merge skips
+            const int t = threadIdx.x;
+            if (t < 32 * NT && seg.row0 + t < sh.R) {
+                float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * kPartStride;
+                o[0] = neg_inf();
+                o[1] = 0.f;
+                o[2] = neg_inf();
+                o[3] = __int_as_float(0);
+            }
+            continue;
+        }
+        // global sources of this lane's DMA pieces (k offset added per step):
+        // the piece landing at physical slot lphys of row `row` is logical
+        // slot lphys ^ swizzle(row).  Tiles past the slice repeat its last
+        // tile and vocabulary rows past V repeat row V-1, so every load stays
+        // inside w; the epilogue masks those products.  (They are computed
+        // anyway: a per-tile branch in the k loop costs more in MFMA-bound
+        // launches, whose slices are all full, than the spare products cost
+        // in the memory-bound ones.)
+        const int tw = seg.t0 + wave * WM;
+        const uint16_t* wsrc[WM][T::WINSTR];
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+            for (int hb = 0; hb < T::WINSTR; ++hb) {
+                const int row = T::RPI * hb + lrow;
+                const int tile = min(tw + mt, seg.t1 - 1);
+                const int v = min(tile * 32 + row, V - 1);
+                wsrc[mt][hb] = w + (size_t)v * sh.K + (T::slot(row, lphys) - row * T::ROWB) / 2;
+            }
+        const uint16_t* xsrc[T::XLOADS];
+#pragma unroll
+        for (int i = 0; i < T::XLOADS; ++i) {
+            const int blk = wave + NW * i;   // block of RPI activation rows
+            const int row = T::RPI * blk + lrow;
+            const int gr = min(seg.row0 + row, sh.R - 1);
+            xsrc[i] = x + (size_t)gr * ldx + (T::slot(row, lphys) - row * T::ROWB) / 2;
+        }
+        auto issue = [&](int step) {
+            unsigned char* st = dyn + (step % S) * T::STAGE;
+            const int k0 = step * KC;
+#pragma unroll
+            for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+                for (int hb = 0; hb < T::WINSTR; ++hb)
+                    __builtin_amdgcn_global_load_lds((global_void_t*)(wsrc[mt][hb] + k0),
+                                                     (lds_void_t*)(st + (wave * WM + mt) * T::WTILE + hb * 1024), 16,
+                                                     0, 0);
+#pragma unroll
+            for (int i = 0; i < T::XLOADS; ++i)
+                __builtin_amdgcn_global_load_lds((global_void_t*)(xsrc[i] + k0),
+                                                 (lds_void_t*)(st + T::WBYTES + (wave + NW * i) * 1024), 16, 0, 0);
+        };
+        f32x16 acc[WM][NT];
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) acc[mt][nt][j] = 0.f;
+
+#pragma unroll
+        for (int p = 0; p < S - 1; ++p)
+            if (p < nsteps) issue(p);
+        for (int j = 0; j < nsteps; ++j) {
+            // this wave's copies of step j have landed; the other waves' too after the barrier
+            const int ahead = nsteps - 1 - j;
+            wait_steps_ahead<T::LPS, S>(ahead < S - 2 ? ahead : S - 2);
+            block_barrier();
+            // the stage of step j - 1 is free: every wave has finished reading it
+            if (j + S - 1 < nsteps) issue(j + S - 1);
+            const unsigned char* st = dyn + (j % S) * T::STAGE;
+            const unsigned char* wt = st + wave * WM * T::WTILE;
+            const unsigned char* xt = st + T::WBYTES;
+#pragma unroll
+            for (int ks = 0; ks < KC / 16; ++ks) {
+                const int ls = 2 * ks + (lane >> 5);
+                u32x4 afr[WM], bfr[NT];
+#pragma unroll
+                for (int mt = 0; mt < WM; ++mt)
+                    afr[mt] = *reinterpret_cast<const u32x4*>(wt + mt * T::WTILE + T::slot(lane & 31, ls));
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    bfr[nt] = *reinterpret_cast<const u32x4*>(xt + T::slot(nt * 32 + (lane & 31), ls));
+#pragma unroll
+                for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_32x32x16_bf16(afr[mt], bfr[nt], acc[mt][nt]);
+            }
+        }
+        __syncthreads();  // ring reads done before the epilogue reuses the LDS
+        epi.apply(acc, seg, dyn, se);
+        __syncthreads();  // the epilogue's LDS use ends before the next round's copies land
+    }
+}
+
 // ------------------------------------------------------------ fp32 / SIMT
 //
 // The fp32 workloads are small; this kernel keeps the same partial format
@@ -419,9 +614,20 @@ static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const
 }
 
 // tile shape and pipeline variants the plans can ask for
-static void dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
-                             int V, float sl2, float* part, int* diag, hipStream_t st) {
+static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const uint16_t* w,
+                                   const GemmShape& sh, int V, float sl2, float* part, int* diag, hipStream_t st) {
     const int nb = p.blocks();
+    if (p.dma) {
+        using T = DmaTraits<TF_LM_DMA_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
+        auto kern = lmhead_dma_kernel<TF_LM_DMA_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
+        // dynamic LDS beyond the 64 KiB default
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3(nb), dim3(64 * TF_LM_DMA_NW), T::RING, st, x, ldx, w, sh, p.map, V, sl2, part,
+                           diag);
+        return hipSuccess;
+    }
     if (p.NT == 1)
         launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
                                                                            diag, st);
@@ -434,6 +640,7 @@ static void dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const
     else
         launch_lm_bf16<TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, p.map, nb, V, sl2, part,
                                                                             diag, st);
+    return hipSuccess;
 }
 
 hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, int d, int V, int K,
@@ -447,10 +654,11 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
     const GemmShape sh{rows, d, p.ntiles, p.map.G, p.nrb, p.nk, p.blocks()};
     const float sl2 = inv_t * kLog2e;
     if (ev_begin != nullptr && hipEventRecord(ev_begin, stream) != hipSuccess) return hipErrorInvalidHandle;
-    if (bf16)
-        dispatch_lm_bf16(p, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w), sh, V, sl2, part,
-                         diag, stream);
-    else
+    if (bf16) {
+        const hipError_t de = dispatch_lm_bf16(p, static_cast<const uint16_t*>(x), ldx,
+                                               static_cast<const uint16_t*>(w), sh, V, sl2, part, diag, stream);
+        if (de != hipSuccess) return de;
+    } else
         hipLaunchKernelGGL(lmhead_f32_kernel, dim3(p.blocks()), dim3(256), 0, stream, static_cast<const float*>(x),
                            ldx, static_cast<const float*>(w), sh, p.map, V, sl2, part, diag);
     hipError_t e = hipGetLastError();

@@ -114,6 +114,7 @@ struct LmPlan {
     int NT, WM, NW, chunk, nrb, ntiles, nk;
     SliceMap map;
     bool wnt;
+    bool dma;   // the LDS-DMA kernel (TF_LM_DMA_NW waves of TF_LM_DMA_WM tiles, k in steps of 32)
     int nsplit() const { return map.G * map.rmax; }
     int blocks() const { return map.G * nrb; }
 };
@@ -139,6 +140,21 @@ struct LmPlan {
 #ifndef TF_LM_WM_NT4
 #define TF_LM_WM_NT4 1
 #endif
+#ifndef TF_LM_DMA_WM
+#define TF_LM_DMA_WM 2
+#endif
+#ifndef TF_LM_DMA_NW
+#define TF_LM_DMA_NW 4
+#endif
+#ifndef TF_LM_DMA_KC
+#define TF_LM_DMA_KC 64
+#endif
+#ifndef TF_LM_DMA_STAGES
+#define TF_LM_DMA_STAGES 3
+#endif
+#ifndef TF_LM_DMA
+#define TF_LM_DMA 1
+#endif
 inline int lm_nw(int NT) { return NT == 1 ? TF_LM_NW_NT1 : (NT == 2 ? TF_LM_NW_NT2 : TF_LM_NW_NT4); }
 inline int lm_wm(int NT) { return NT == 1 ? TF_LM_WM_NT1 : (NT == 2 ? TF_LM_WM_NT2 : TF_LM_WM_NT4); }
 
@@ -146,10 +162,13 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     LmPlan p;
     p.ntiles = cdiv(V, 32);
     p.nk = cdiv(d, 64);
+    p.dma = false;
     if (bf16) {
         p.NT = plan_nt(rows);
-        p.WM = lm_wm(p.NT);
-        p.NW = lm_nw(p.NT);
+        // 128-row activation tiles with k in whole 32-wide steps: the DMA kernel
+        p.dma = TF_LM_DMA && p.NT == 4 && d % TF_LM_DMA_KC == 0;
+        p.WM = p.dma ? TF_LM_DMA_WM : lm_wm(p.NT);
+        p.NW = p.dma ? TF_LM_DMA_NW : lm_nw(p.NT);
         p.chunk = p.NW * p.WM;
         p.nrb = cdiv(rows, 32 * p.NT);
         const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)
