@@ -154,14 +154,19 @@ def summarize_trace(args):
     cur = _db(args.summarize_trace).cursor()
     rows = cur.execute("select name, count(*), avg(duration), min(duration), max(duration), sum(duration) "
                        "from kernels where name like '%tf::%' group by name order by sum(duration) desc").fetchall()
+    durs = {}
+    for name, dur in cur.execute("select name, duration from kernels where name like '%tf::%'"):
+        durs.setdefault(name, []).append(dur)
+    med = {k: sorted(v)[len(v) // 2] for k, v in durs.items()}
     print(f"# Kernel trace: TreeFlash drafting step, {args.workload}\n")
     print(f"Command (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
     print("The library's kernels only (the PyTorch kernels that draw the synthetic inputs are left out); "
           "each bench step runs every kernel once, the merge twice (stage 1 and stage 2).\n")
-    print("| kernel | calls | avg us | min us | max us | total ms |\n|---|---|---|---|---|---|")
+    print("| kernel | calls | avg us | median us | min us | max us | total ms |\n|---|---|---|---|---|---|---|")
     for name, n, avg, mn, mx, tot in rows:
         short = name.split("(")[0].replace("void ", "")
-        print(f"| `{short}` | {n} | {avg / 1e3:.1f} | {mn / 1e3:.1f} | {mx / 1e3:.1f} | {tot / 1e6:.2f} |")
+        print(f"| `{short}` | {n} | {avg / 1e3:.1f} | {med[name] / 1e3:.1f} | {mn / 1e3:.1f} | {mx / 1e3:.1f} | "
+              f"{tot / 1e6:.2f} |")
 
 
 def summarize_pmc(args):
