@@ -69,6 +69,82 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
     }
 }
 
+// bf16 with every row 16-byte aligned: one wave per vector; each lane keeps
+// its 16-byte pieces (pieces lane, lane + 64, ...; at most MAXC of them) in
+// registers between the sum of squares and the scaling, so the vector is
+// read once and the reduction needs no barrier.
+template <int MAXC>
+__global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const uint16_t* __restrict__ h,
+                                                                const int32_t* __restrict__ root,
+                                                                const int32_t* __restrict__ context,
+                                                                const int32_t* __restrict__ topk,
+                                                                const uint16_t* __restrict__ emb,
+                                                                const uint16_t* __restrict__ gh,
+                                                                const uint16_t* __restrict__ ge, int b, int d, int V,
+                                                                RowTable rt, int npre, float eps,
+                                                                uint16_t* __restrict__ ht, uint16_t* __restrict__ et,
+                                                                int* __restrict__ diag, int* __restrict__ counters,
+                                                                int ncounters) {
+    if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
+    if (blockIdx.x == 0)   // arrival counters of the products that follow on this stream
+        for (int i = threadIdx.x; i < ncounters; i += 256) counters[i] = 0;
+    const int lane = threadIdx.x & 63;
+    const int vec = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int nvec = b * rt.gamma + b * rt.Rs * npre;
+    if (vec >= nvec) return;
+    const uint16_t* src;
+    const uint16_t* gain;
+    uint16_t* dst;
+    if (vec < b * rt.gamma) {
+        src = h + (size_t)vec * d;
+        gain = gh;
+        dst = ht + (size_t)vec * d;
+    } else {
+        const int e = vec - b * rt.gamma;
+        const int rr = e / npre, which = e - rr * npre;
+        const int s = rr / rt.Rs;
+        int prev = rt.prev_token(s, rr - s * rt.Rs, which, root, context, topk);
+        prev = min(max(prev, 0), V - 1);   // ids are documented to be < V; never read out of bounds
+        src = emb + (size_t)prev * d;
+        gain = ge;
+        dst = et + (size_t)rr * npre * d + (size_t)which * d;
+    }
+    const int npc = d >> 3;   // 16-byte pieces
+    u32x4 v[MAXC];
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        const int pc = lane + 64 * c;
+        if (pc < npc) {
+            v[c] = *reinterpret_cast<const u32x4*>(src + 8 * pc);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu), hi = bf16_bits_to_f32(v[c][q] >> 16);
+                ss = fmaf(lo, lo, ss);
+                ss = fmaf(hi, hi, ss);
+            }
+        }
+    }
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        const int pc = lane + 64 * c;
+        if (pc < npc) {
+            u32x4 gv = u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};   // bf16 ones
+            if (gain != nullptr) gv = *reinterpret_cast<const u32x4*>(gain + 8 * pc);
+            u32x4 o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu) * inv * bf16_bits_to_f32(gv[q] & 0xffffu);
+                const float hi = bf16_bits_to_f32(v[c][q] >> 16) * inv * bf16_bits_to_f32(gv[q] >> 16);
+                o[q] = f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+            }
+            *reinterpret_cast<u32x4*>(dst + 8 * pc) = o;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ bf16
 
 template <int WM, int NT, int NW, int PIPE, bool WNT>
@@ -184,12 +260,28 @@ static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_
                        shd, hp, h, d, rt, partial, counters + pg.counter_ints());
 }
 
+static bool aligned16p(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 template <class T>
 static void launch_norms(const void* h, const int32_t* root, const int32_t* context, const int32_t* topk,
                          const void* emb, const void* gh, const void* ge, int b, int d, int V, const RowTable& rt,
                          int npre, float eps, void* ht, void* et, int* diag, int* counters, int ncounters,
                          hipStream_t stream) {
     const int nvec = b * rt.gamma + b * rt.Rs * npre;
+    constexpr int kMaxPieces = 16;   // d <= 16 * 64 * 8 = 8192 in registers
+    if constexpr (sizeof(T) == 2) {
+        // h rows are 16-byte aligned (checked at the boundary); the embedding and gains are only
+        // required to be 4-byte aligned, so this path is taken when they happen to be 16-byte aligned
+        if (d <= kMaxPieces * 64 * 8 && aligned16p(emb) && (gh == nullptr || aligned16p(gh)) &&
+            (ge == nullptr || aligned16p(ge))) {
+            hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel<kMaxPieces>, dim3(cdiv(nvec, 4)), dim3(256), 0, stream,
+                               static_cast<const uint16_t*>(h), root, context, topk,
+                               static_cast<const uint16_t*>(emb), static_cast<const uint16_t*>(gh),
+                               static_cast<const uint16_t*>(ge), b, d, V, rt, npre, eps,
+                               static_cast<uint16_t*>(ht), static_cast<uint16_t*>(et), diag, counters, ncounters);
+            return;
+        }
+    }
     hipLaunchKernelGGL(rmsnorm_rows_kernel<T>, dim3(nvec), dim3(256), 0, stream, static_cast<const T*>(h), root,
                        context, topk, static_cast<const T*>(emb), static_cast<const T*>(gh),
                        static_cast<const T*>(ge), b, d, V, rt, npre, eps, static_cast<T*>(ht), static_cast<T*>(et),
