@@ -68,12 +68,16 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
 // The same vocabulary slices with the weight and activation tiles copied
 // from memory straight into LDS (global_load_lds_dwordx4, no register
 // staging), so that the registers go to accumulators: NW waves of WM weight
-// tiles each.  k advances KC at a time through a ring of S LDS stages; every
-// stage holds each wave's WM weight tiles ([32 rows][KC]) and the activation
-// tile ([32*NT rows][KC]).  One DMA instruction fills 1 KiB: 1024 / (2 KC)
-// whole rows, lane l taking 16-byte slot l % (KC / 8) of row l / (KC / 8).
-// Slots are XOR-swizzled per row so that the 16 rows one quarter-wave reads
-// at one logical slot cover all 64 banks.
+// tiles each.  k advances KC at a time.  The weight tiles ([32 rows][KC] per
+// tile, each wave its own WM) go through a ring of S stages, copied S - 1
+// steps ahead; the activation tile ([32*NT rows][KC], shared) through a ring
+// of two, copied one step ahead from L2.  Each step a wave issues its
+// activation copies first, so waiting for them (all but the step's weight
+// copies retired, in issue order) also retires the older weight copies.  One
+// DMA instruction fills 1 KiB: 1024 / (2 KC) whole rows, lane l taking
+// 16-byte slot l % (KC / 8) of row l / (KC / 8).  Slots are XOR-swizzled per
+// row so that the 16 rows one quarter-wave reads at one logical slot cover
+// all 64 banks.
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void global_void_t;
 
@@ -84,15 +88,16 @@ struct DmaTraits {
     static constexpr int RPI = 1024 / ROWB;                   // rows per DMA instruction
     static constexpr int WTILE = 32 * ROWB;                   // one weight tile of one stage
     static constexpr int WINSTR = 32 / RPI;                   // DMA instructions per weight tile
-    static constexpr int WBYTES = NW * WM * WTILE;            // all waves' weight tiles
-    static constexpr int XBYTES = 32 * NT * ROWB;             // the activation tile
-    static constexpr int STAGE = WBYTES + XBYTES;
-    static constexpr int RING = S * STAGE;
-    static constexpr int XLOADS = XBYTES / 1024 / NW;         // activation DMA instructions per wave
-    static constexpr int LPS = WINSTR * WM + XLOADS;          // DMA instructions per wave per step
+    static constexpr int WSTAGE = NW * WM * WTILE;            // all waves' weight tiles of one stage
+    static constexpr int XSTAGE = 32 * NT * ROWB;             // the activation tile of one stage
+    static constexpr int XINSTR = XSTAGE / 1024;              // its DMA instructions, spread over the waves
+    static constexpr int XOFF = S * WSTAGE;                   // activation ring after the weight ring
+    static constexpr int RING = S * WSTAGE + 2 * XSTAGE;
+    static constexpr int WPS = WINSTR * WM;                   // weight DMA instructions per wave per step
     static_assert(KC == 32 || KC == 64, "k step");
-    static_assert(XBYTES % (1024 * NW) == 0, "every wave copies the same share of the activation tile");
-    static_assert(LPS * (S - 2) < 64, "vmcnt range");
+    // S >= 3: weight step j is issued at step j - S + 1 <= j - 2, before the
+    // activation step j (issued at step j - 1), so waiting for the latter retires it
+    static_assert(S >= 3 && WPS < 64, "ring depth, vmcnt range");
     // byte offset of 16-byte logical slot `ls` of row `r`
     __device__ static __forceinline__ int slot(int r, int ls) {
         const int sw = KC == 32 ? ((r >> 2) & 3) : ((r >> 1) & 7);
@@ -110,22 +115,6 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("" ::: "memory");
 }
 
-// wait for the loads of the step about to be computed: `ahead` later steps
-// (0 .. S-2) may still be in flight
-template <int LPS, int S>
-__device__ __forceinline__ void wait_steps_ahead(int ahead) {
-    if constexpr (S >= 4) {
-        if (ahead >= 2) {
-            wait_vmcnt<2 * LPS>();
-            return;
-        }
-    }
-    if (ahead >= 1)
-        wait_vmcnt<LPS>();
-    else
-        wait_vmcnt<0>();
-}
-
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <int WM, int NT, int NW, int KC, int S>
@@ -135,7 +124,7 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* 
                                                                 float* __restrict__ part, int* __restrict__ diag) {
     using T = DmaTraits<WM, NT, NW, KC, S>;
     using E = EpiLmHead<WM, NT, NW>;
-    static_assert(E::MERGE_BYTES <= T::RING, "the epilogue reuses the ring");
+    static_assert(E::MERGE_BYTES <= T::RING, "the epilogue reuses the rings");
     extern __shared__ __align__(16) unsigned char dyn[];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     const int lane = threadIdx.x & 63;
@@ -192,16 +181,17 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* 
                 const int v = min(tile * 32 + row, V - 1);
                 wsrc[mt][hb] = w + (size_t)v * sh.K + (T::slot(row, lphys) - row * T::ROWB) / 2;
             }
-        const uint16_t* xsrc[T::XLOADS];
+        constexpr int XPW = (T::XINSTR + NW - 1) / NW;   // activation instructions of this wave (at most)
+        const uint16_t* xsrc[XPW];
 #pragma unroll
-        for (int i = 0; i < T::XLOADS; ++i) {
-            const int blk = wave + NW * i;   // block of RPI activation rows
+        for (int i = 0; i < XPW; ++i) {
+            const int blk = min(wave + NW * i, T::XINSTR - 1);   // block of RPI activation rows
             const int row = T::RPI * blk + lrow;
             const int gr = min(seg.row0 + row, sh.R - 1);
             xsrc[i] = x + (size_t)gr * ldx + (T::slot(row, lphys) - row * T::ROWB) / 2;
         }
-        auto issue = [&](int step) {
-            unsigned char* st = dyn + (step % S) * T::STAGE;
+        auto issue_w = [&](int step) {
+            unsigned char* st = dyn + (step % S) * T::WSTAGE;
             const int k0 = step * KC;
 #pragma unroll
             for (int mt = 0; mt < WM; ++mt)
@@ -210,10 +200,15 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* 
                     __builtin_amdgcn_global_load_lds((global_void_t*)(wsrc[mt][hb] + k0),
                                                      (lds_void_t*)(st + (wave * WM + mt) * T::WTILE + hb * 1024), 16,
                                                      0, 0);
+        };
+        auto issue_x = [&](int step) {
+            unsigned char* st = dyn + T::XOFF + (step & 1) * T::XSTAGE;
+            const int k0 = step * KC;
 #pragma unroll
-            for (int i = 0; i < T::XLOADS; ++i)
-                __builtin_amdgcn_global_load_lds((global_void_t*)(xsrc[i] + k0),
-                                                 (lds_void_t*)(st + T::WBYTES + (wave + NW * i) * 1024), 16, 0, 0);
+            for (int i = 0; i < XPW; ++i)
+                if (wave + NW * i < T::XINSTR)   // uniform per wave
+                    __builtin_amdgcn_global_load_lds((global_void_t*)(xsrc[i] + k0),
+                                                     (lds_void_t*)(st + (wave + NW * i) * 1024), 16, 0, 0);
         };
         f32x16 acc[WM][NT];
 #pragma unroll
@@ -223,19 +218,26 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* 
 #pragma unroll
                 for (int j = 0; j < 16; ++j) acc[mt][nt][j] = 0.f;
 
+        // prologue: the first S - 1 weight steps, then activation step 0
+        // (waiting for it then retires them all)
 #pragma unroll
         for (int p = 0; p < S - 1; ++p)
-            if (p < nsteps) issue(p);
+            if (p < nsteps) issue_w(p);
+        issue_x(0);
         for (int j = 0; j < nsteps; ++j) {
-            // this wave's copies of step j have landed; the other waves' too after the barrier
-            const int ahead = nsteps - 1 - j;
-            wait_steps_ahead<T::LPS, S>(ahead < S - 2 ? ahead : S - 2);
+            // this wave's copies of step j have landed (issued in order, only
+            // weight step j + S - 2 may still be out); the other waves' too
+            // after the barrier
+            if (j >= 1 && j + S - 2 < nsteps)
+                wait_vmcnt<T::WPS>();
+            else
+                wait_vmcnt<0>();
             block_barrier();
-            // the stage of step j - 1 is free: every wave has finished reading it
-            if (j + S - 1 < nsteps) issue(j + S - 1);
-            const unsigned char* st = dyn + (j % S) * T::STAGE;
-            const unsigned char* wt = st + wave * WM * T::WTILE;
-            const unsigned char* xt = st + T::WBYTES;
+            // the stages read in step j - 1 are free now
+            if (j + 1 < nsteps) issue_x(j + 1);
+            if (j + S - 1 < nsteps) issue_w(j + S - 1);
+            const unsigned char* wt = dyn + (j % S) * T::WSTAGE + wave * WM * T::WTILE;
+            const unsigned char* xt = dyn + T::XOFF + (j & 1) * T::XSTAGE;
 #pragma unroll
             for (int ks = 0; ks < KC / 16; ++ks) {
                 const int ls = 2 * ks + (lane >> 5);
@@ -613,20 +615,28 @@ static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const
                        map, V, sl2, part, diag);
 }
 
+template <int WM, int NW>
+static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
+                                const SliceMap& map, int blocks, int V, float sl2, float* part, int* diag,
+                                hipStream_t st) {
+    using T = DmaTraits<WM, 4, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
+    auto kern = lmhead_dma_kernel<WM, 4, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
+    // dynamic LDS beyond the 64 KiB default
+    const hipError_t e =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), T::RING, st, x, ldx, w, sh, map, V, sl2, part, diag);
+    return hipSuccess;
+}
+
 // tile shape and pipeline variants the plans can ask for
 static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const uint16_t* w,
                                    const GemmShape& sh, int V, float sl2, float* part, int* diag, hipStream_t st) {
     const int nb = p.blocks();
-    if (p.dma) {
-        using T = DmaTraits<TF_LM_DMA_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
-        auto kern = lmhead_dma_kernel<TF_LM_DMA_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
-        // dynamic LDS beyond the 64 KiB default
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, dim3(nb), dim3(64 * TF_LM_DMA_NW), T::RING, st, x, ldx, w, sh, p.map, V, sl2, part,
-                           diag);
-        return hipSuccess;
+    if (p.dma) {   // the two wave counts the plans use (see lm_plan)
+        if (p.NW == TF_LM_DMA_NW_SINGLE)
+            return launch_lm_dma<TF_LM_DMA_WM, TF_LM_DMA_NW_SINGLE>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        return launch_lm_dma<TF_LM_DMA_WM, TF_LM_DMA_NW>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     }
     if (p.NT == 1)
         launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,

@@ -143,6 +143,13 @@ struct LmPlan {
 #ifndef TF_LM_DMA_WM
 #define TF_LM_DMA_WM 2
 #endif
+// waves of the DMA kernel: five for a single row block (ten tiles per round,
+// so the 256 ranges of the Qwen vocabularies take two rounds instead of three;
+// memory-bound, the fifth wave's SIMD does twice the MFMA work unnoticed),
+// four for several row blocks (MFMA-bound: one wave per SIMD)
+#ifndef TF_LM_DMA_NW_SINGLE
+#define TF_LM_DMA_NW_SINGLE 5
+#endif
 #ifndef TF_LM_DMA_NW
 #define TF_LM_DMA_NW 4
 #endif
@@ -168,9 +175,9 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
         // 128-row activation tiles with k in whole 32-wide steps: the DMA kernel
         p.dma = TF_LM_DMA && p.NT == 4 && d % TF_LM_DMA_KC == 0;
         p.WM = p.dma ? TF_LM_DMA_WM : lm_wm(p.NT);
-        p.NW = p.dma ? TF_LM_DMA_NW : lm_nw(p.NT);
-        p.chunk = p.NW * p.WM;
         p.nrb = cdiv(rows, 32 * p.NT);
+        p.NW = p.dma ? (p.nrb == 1 ? TF_LM_DMA_NW_SINGLE : TF_LM_DMA_NW) : lm_nw(p.NT);
+        p.chunk = p.NW * p.WM;
         const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)
                                  : cdiv(p.ntiles, p.chunk);
         p.map = make_slice_map(p.ntiles, G, p.chunk);
