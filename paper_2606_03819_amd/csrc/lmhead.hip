@@ -68,7 +68,8 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
 // The same vocabulary slices with the weight and activation tiles copied
 // from memory straight into LDS (global_load_lds_dwordx4, no register
 // staging), so that the registers go to accumulators: NW waves of WM weight
-// tiles each.  k advances KC at a time.  The weight tiles ([32 rows][KC] per
+// tiles each (WNT: the weight copies carry the non-temporal hint).  k
+// advances KC at a time.  The weight tiles ([32 rows][KC] per
 // tile, each wave its own WM) go through a ring of S stages, copied S - 1
 // steps ahead; the activation tile ([32*NT rows][KC], shared) through a ring
 // of two, copied one step ahead from L2.  Each step a wave issues its
@@ -79,6 +80,10 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
 // row so that the 16 rows one quarter-wave reads at one logical slot cover
 // all 64 banks.
 typedef __attribute__((address_space(3))) void lds_void_t;
+// cache-policy bit of a non-temporal load (weights that one workgroup alone
+// streams: a single activation row block); several row blocks share each
+// weight tile through L2 and load it normally
+constexpr int kCpolNt = 2;
 typedef __attribute__((address_space(1))) void global_void_t;
 
 template <int WM, int NT, int NW, int KC, int S>
@@ -117,7 +122,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int WM, int NT, int NW, int KC, int S>
+template <int WM, int NT, int NW, int KC, int S, bool WNT>
 __global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,
                                                                 const uint16_t* __restrict__ w, GemmShape sh,
                                                                 SliceMap map, int V, float sl2,
@@ -199,7 +204,7 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* 
                 for (int hb = 0; hb < T::WINSTR; ++hb)
                     __builtin_amdgcn_global_load_lds((global_void_t*)(wsrc[mt][hb] + k0),
                                                      (lds_void_t*)(st + (wave * WM + mt) * T::WTILE + hb * 1024), 16,
-                                                     0, 0);
+                                                     0, WNT ? kCpolNt : 0);
         };
         auto issue_x = [&](int step) {
             unsigned char* st = dyn + T::XOFF + (step & 1) * T::XSTAGE;
@@ -615,12 +620,12 @@ static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const
                        map, V, sl2, part, diag);
 }
 
-template <int WM, int NW>
+template <int WM, int NT, int NW, bool WNT>
 static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
                                 const SliceMap& map, int blocks, int V, float sl2, float* part, int* diag,
                                 hipStream_t st) {
-    using T = DmaTraits<WM, 4, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
-    auto kern = lmhead_dma_kernel<WM, 4, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
+    using T = DmaTraits<WM, NT, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
+    auto kern = lmhead_dma_kernel<WM, NT, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES, WNT>;
     // dynamic LDS beyond the 64 KiB default
     const hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
@@ -633,10 +638,16 @@ static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, 
 static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const uint16_t* w,
                                    const GemmShape& sh, int V, float sl2, float* part, int* diag, hipStream_t st) {
     const int nb = p.blocks();
-    if (p.dma) {   // the two wave counts the plans use (see lm_plan)
-        if (p.NW == TF_LM_DMA_NW_SINGLE)
-            return launch_lm_dma<TF_LM_DMA_WM, TF_LM_DMA_NW_SINGLE>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
-        return launch_lm_dma<TF_LM_DMA_WM, TF_LM_DMA_NW>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+    if (p.dma) {   // the shapes the plans use (see lm_plan)
+#if TF_LM_DMA_NT1
+        if (p.NT == 1)
+            return launch_lm_dma<TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+                                                                              diag, st);
+#endif
+        if (p.wnt)   // a single row block
+            return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+                                                                             diag, st);
+        return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW, false>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     }
     if (p.NT == 1)
         launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,

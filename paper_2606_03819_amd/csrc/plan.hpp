@@ -162,6 +162,16 @@ struct LmPlan {
 #ifndef TF_LM_DMA
 #define TF_LM_DMA 1
 #endif
+// the DMA kernel for 32-row tiles too (stage 1)
+#ifndef TF_LM_DMA_NT1
+#define TF_LM_DMA_NT1 0
+#endif
+#ifndef TF_LM_DMA_NT1_WM
+#define TF_LM_DMA_NT1_WM 2
+#endif
+#ifndef TF_LM_DMA_NT1_NW
+#define TF_LM_DMA_NT1_NW 5
+#endif
 inline int lm_nw(int NT) { return NT == 1 ? TF_LM_NW_NT1 : (NT == 2 ? TF_LM_NW_NT2 : TF_LM_NW_NT4); }
 inline int lm_wm(int NT) { return NT == 1 ? TF_LM_WM_NT1 : (NT == 2 ? TF_LM_WM_NT2 : TF_LM_WM_NT4); }
 
@@ -173,10 +183,18 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     if (bf16) {
         p.NT = plan_nt(rows);
         // 128-row activation tiles with k in whole 32-wide steps: the DMA kernel
-        p.dma = TF_LM_DMA && p.NT == 4 && d % TF_LM_DMA_KC == 0;
-        p.WM = p.dma ? TF_LM_DMA_WM : lm_wm(p.NT);
+        p.dma = TF_LM_DMA && (p.NT == 4 || (TF_LM_DMA_NT1 && p.NT == 1)) && d % TF_LM_DMA_KC == 0;
         p.nrb = cdiv(rows, 32 * p.NT);
-        p.NW = p.dma ? (p.nrb == 1 ? TF_LM_DMA_NW_SINGLE : TF_LM_DMA_NW) : lm_nw(p.NT);
+        if (p.dma && p.NT == 1) {
+            p.WM = TF_LM_DMA_NT1_WM;
+            p.NW = TF_LM_DMA_NT1_NW;
+        } else if (p.dma) {
+            p.WM = TF_LM_DMA_WM;
+            p.NW = p.nrb == 1 ? TF_LM_DMA_NW_SINGLE : TF_LM_DMA_NW;
+        } else {
+            p.WM = lm_wm(p.NT);
+            p.NW = lm_nw(p.NT);
+        }
         p.chunk = p.NW * p.WM;
         const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)
                                  : cdiv(p.ntiles, p.chunk);
