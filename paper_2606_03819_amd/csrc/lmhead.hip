@@ -395,19 +395,75 @@ struct MergeArgs {
     int* diag;
 };
 
-__device__ __forceinline__ float dot_row(const uint16_t* a, const uint16_t* b, int d) {
-    float acc = 0.f;
-    for (int k = 0; k < d; k += 8) {
-        const u32x4 av = *reinterpret_cast<const u32x4*>(a + k);
-        const u32x4 bv = *reinterpret_cast<const u32x4*>(b + k);
+// Exact logits of one activation row with the 32 vocabulary rows of each of
+// NTL tiles (ids 32t .. 32t+31; ids past V repeat row V-1), computed as the
+// bf16 LM-head kernels compute them: one chain per logit, an MFMA 32x32x16
+// per 16-wide k block in increasing k from zero, the weights as the A
+// operand and the activation as B, so that every value is bit for bit the
+// one the fast path saw (exact ties order the same way on both paths).  The
+// row fills all 32 B columns, so every lane holds the logits of ids
+// 32t + acc_row(j, lane) in acc[j].  Loads go in batches of P k blocks, two
+// batches in flight: one lands while the other feeds the MFMAs (a batch
+// reaching past d re-reads the last block and is not used).
+template <int NTL, int P>
+__device__ __forceinline__ void tile_logits_mfma(const uint16_t* xr, const uint16_t* w, int d, int V,
+                                                 const int (&t)[NTL], f32x16 (&acc)[NTL]) {
+    const int lane = threadIdx.x & 63;
+    const int h8 = 8 * (lane >> 5);
+    const uint16_t* wp[NTL];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            acc = fmaf(bf16_bits_to_f32(av[q] & 0xffffu), bf16_bits_to_f32(bv[q] & 0xffffu), acc);
-            acc = fmaf(bf16_bits_to_f32(av[q] >> 16), bf16_bits_to_f32(bv[q] >> 16), acc);
-        }
+    for (int i = 0; i < NTL; ++i) {
+        wp[i] = w + (size_t)min(t[i] * 32 + (lane & 31), V - 1) * d + h8;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[i][j] = 0.f;
     }
-    return acc;
+    const uint16_t* xp = xr + h8;
+    const int nblk = d / 16;
+    auto load = [&](int blk, u32x4 (&xv)[P], u32x4 (&wv)[NTL][P]) {
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int k0 = min(blk + p, nblk - 1) * 16;
+            xv[p] = *reinterpret_cast<const u32x4*>(xp + k0);
+#pragma unroll
+            for (int i = 0; i < NTL; ++i) wv[i][p] = *reinterpret_cast<const u32x4*>(wp[i] + k0);
+        }
+    };
+    auto mma = [&](int blk, const u32x4 (&xv)[P], const u32x4 (&wv)[NTL][P]) {
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            if (blk + p < nblk)
+#pragma unroll
+                for (int i = 0; i < NTL; ++i) acc[i] = mfma_32x32x16_bf16(wv[i][p], xv[p], acc[i]);
+    };
+    u32x4 xa[P], wa[NTL][P], xb[P], wb[NTL][P];
+    load(0, xa, wa);
+    for (int blk = 0; blk < nblk; blk += 2 * P) {
+        load(blk + P, xb, wb);
+        mma(blk, xa, wa);
+        if (blk + 2 * P < nblk) load(blk + 2 * P, xa, wa);
+        mma(blk + P, xb, wb);
+    }
 }
+
+// Logits of tiles [tg, tend) (at most 16) into colv[(t - tg) * 32 + m]: wave
+// w takes tiles tg + w + 4i, i < NTL; a slot past tend repeats the last tile
+// and is not read.
+template <int NTL>
+__device__ __forceinline__ void slice_logits(const uint16_t* xr, const uint16_t* w, int d, int V, int tg, int tend,
+                                             float* colv) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int tl[NTL];
+#pragma unroll
+    for (int i = 0; i < NTL; ++i) tl[i] = min(tg + wave + 4 * i, tend - 1);
+    f32x16 lg[NTL];
+    tile_logits_mfma<NTL, (NTL >= 4 ? 2 : 3)>(xr, w, d, V, tl, lg);
+    if ((lane & 31) == 0)
+#pragma unroll
+        for (int i = 0; i < NTL; ++i)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) colv[(wave + 4 * i) * 32 + acc_row(j, lane)] = lg[i][j];
+}
+
 __device__ __forceinline__ float dot_row(const float* a, const float* b, int d) {
     float acc = 0.f;
     for (int k = 0; k < d; ++k) acc = fmaf(a[k], b[k], acc);
@@ -460,6 +516,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     __shared__ float cand_v[kMergeCap];
     __shared__ int cand_i[kMergeCap];
     __shared__ int s_flag[kMaxSplits];
+    __shared__ float s_colv[512];   // logits of a re-evaluated group of 16 tiles (bf16)
 
     const int row = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -551,52 +608,71 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
             const int s = s_flag[f];
             int t0s, t1s;
             slice_tiles(a.map, s, t0s, t1s);
-            const int v0 = t0s * 32, v1 = min(a.V, t1s * 32);
-            for (int vb = v0; vb < v1; vb += 256) {
-                if (tid == 0) s_ncand = 0;
-                __syncthreads();
-                const int v = vb + tid;
-                if (v < v1) {
-                    const float val = dot_row(xr, wb + (size_t)v * a.d, a.d);
-                    bool take = cnt < K || better(val, v, sel_v[K - 1], sel_i[K - 1]);
-                    if (take)
-                        for (int j = 0; j < cnt; ++j)
-                            if (sel_i[j] == v) {
-                                take = false;
-                                break;
+            // groups of 16 tiles (every slice the plans make is one group)
+            for (int tg = t0s; tg < t1s; tg += 16) {
+                const int tend = min(t1s, tg + 16);
+                const int v0 = tg * 32, v1 = min(a.V, tend * 32);
+                if constexpr (sizeof(T) == 2) {
+                    const int ntl = (tend - tg + 3) / 4;   // tiles per wave
+                    if (ntl == 1)
+                        slice_logits<1>(xr, wb, a.d, a.V, tg, tend, s_colv);
+                    else if (ntl == 2)
+                        slice_logits<2>(xr, wb, a.d, a.V, tg, tend, s_colv);
+                    else if (ntl == 3)
+                        slice_logits<3>(xr, wb, a.d, a.V, tg, tend, s_colv);
+                    else
+                        slice_logits<4>(xr, wb, a.d, a.V, tg, tend, s_colv);
+                }
+                for (int vb = v0; vb < v1; vb += 256) {
+                    if (tid == 0) s_ncand = 0;
+                    __syncthreads();
+                    const int v = vb + tid;
+                    if (v < v1) {
+                        float val;
+                        if constexpr (sizeof(T) == 2)
+                            val = s_colv[v - v0];
+                        else   // the fp32 kernel's chain: fmaf over k in increasing order
+                            val = dot_row(xr, wb + (size_t)v * a.d, a.d);
+                        bool take = cnt < K || better(val, v, sel_v[K - 1], sel_i[K - 1]);
+                        if (take)
+                            for (int j = 0; j < cnt; ++j)
+                                if (sel_i[j] == v) {
+                                    take = false;
+                                    break;
+                                }
+                        if (take) {
+                            const int p = atomicAdd(&s_ncand, 1);
+                            buf_v[p] = val;
+                            buf_i[p] = v;
+                        }
+                    }
+                    __syncthreads();
+                    if (tid == 0) {
+                        int cc = cnt;
+                        for (int q = 0; q < s_ncand; ++q) {
+                            const float cv = buf_v[q];
+                            const int ci = buf_i[q];
+                            int pos;
+                            if (cc < K) {
+                                pos = cc++;
+                            } else if (better(cv, ci, sel_v[K - 1], sel_i[K - 1])) {
+                                pos = K - 1;
+                            } else {
+                                continue;
                             }
-                    if (take) {
-                        const int p = atomicAdd(&s_ncand, 1);
-                        buf_v[p] = val;
-                        buf_i[p] = v;
-                    }
-                }
-                __syncthreads();
-                if (tid == 0) {
-                    int cc = cnt;
-                    for (int q = 0; q < s_ncand; ++q) {
-                        const float cv = buf_v[q];
-                        const int ci = buf_i[q];
-                        int pos;
-                        if (cc < K) {
-                            pos = cc++;
-                        } else if (better(cv, ci, sel_v[K - 1], sel_i[K - 1])) {
-                            pos = K - 1;
-                        } else {
-                            continue;
+                            while (pos > 0 && better(cv, ci, sel_v[pos - 1], sel_i[pos - 1])) {
+                                sel_v[pos] = sel_v[pos - 1];
+                                sel_i[pos] = sel_i[pos - 1];
+                                --pos;
+                            }
+                            sel_v[pos] = cv;
+                            sel_i[pos] = ci;
                         }
-                        while (pos > 0 && better(cv, ci, sel_v[pos - 1], sel_i[pos - 1])) {
-                            sel_v[pos] = sel_v[pos - 1];
-                            sel_i[pos] = sel_i[pos - 1];
-                            --pos;
-                        }
-                        sel_v[pos] = cv;
-                        sel_i[pos] = ci;
+                        s_count = cc;
                     }
-                    s_count = cc;
+                    __syncthreads();
+                    cnt = s_count;
                 }
-                __syncthreads();
-                cnt = s_count;
             }
         }
         if (tid == 0 && a.diag != nullptr) atomicAdd(a.diag, nflag);
@@ -620,12 +696,12 @@ static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const
                        map, V, sl2, part, diag);
 }
 
-template <int WM, int NT, int NW, bool WNT>
+template <int WM, int NT, int NW, int KC, bool WNT>
 static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
                                 const SliceMap& map, int blocks, int V, float sl2, float* part, int* diag,
                                 hipStream_t st) {
-    using T = DmaTraits<WM, NT, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES>;
-    auto kern = lmhead_dma_kernel<WM, NT, NW, TF_LM_DMA_KC, TF_LM_DMA_STAGES, WNT>;
+    using T = DmaTraits<WM, NT, NW, KC, TF_LM_DMA_STAGES>;
+    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT>;
     // dynamic LDS beyond the 64 KiB default
     const hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
@@ -641,13 +717,14 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
     if (p.dma) {   // the shapes the plans use (see lm_plan)
 #if TF_LM_DMA_NT1
         if (p.NT == 1)
-            return launch_lm_dma<TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
-                                                                              diag, st);
+            return launch_lm_dma<TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb,
+                                                                                            V, sl2, part, diag, st);
 #endif
         if (p.wnt)   // a single row block
-            return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
-                                                                             diag, st);
-        return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW, false>(x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+            return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb, V,
+                                                                                           sl2, part, diag, st);
+        return launch_lm_dma<TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false>(x, ldx, w, sh, p.map, nb,
+                                                                                             V, sl2, part, diag, st);
     }
     if (p.NT == 1)
         launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,

@@ -153,6 +153,13 @@ struct LmPlan {
 #ifndef TF_LM_DMA_NW
 #define TF_LM_DMA_NW 4
 #endif
+// several row blocks: weight tiles per wave and k step
+#ifndef TF_LM_DMA_MULTI_WM
+#define TF_LM_DMA_MULTI_WM 2
+#endif
+#ifndef TF_LM_DMA_MULTI_KC
+#define TF_LM_DMA_MULTI_KC 64
+#endif
 #ifndef TF_LM_DMA_KC
 #define TF_LM_DMA_KC 64
 #endif
@@ -183,14 +190,18 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     if (bf16) {
         p.NT = plan_nt(rows);
         // 128-row activation tiles with k in whole 32-wide steps: the DMA kernel
-        p.dma = TF_LM_DMA && (p.NT == 4 || (TF_LM_DMA_NT1 && p.NT == 1)) && d % TF_LM_DMA_KC == 0;
         p.nrb = cdiv(rows, 32 * p.NT);
+        const int kc = p.NT == 4 && p.nrb > 1 ? TF_LM_DMA_MULTI_KC : TF_LM_DMA_KC;
+        p.dma = TF_LM_DMA && (p.NT == 4 || (TF_LM_DMA_NT1 && p.NT == 1)) && d % kc == 0;
         if (p.dma && p.NT == 1) {
             p.WM = TF_LM_DMA_NT1_WM;
             p.NW = TF_LM_DMA_NT1_NW;
-        } else if (p.dma) {
+        } else if (p.dma && p.nrb == 1) {
             p.WM = TF_LM_DMA_WM;
-            p.NW = p.nrb == 1 ? TF_LM_DMA_NW_SINGLE : TF_LM_DMA_NW;
+            p.NW = TF_LM_DMA_NW_SINGLE;
+        } else if (p.dma) {
+            p.WM = TF_LM_DMA_MULTI_WM;
+            p.NW = TF_LM_DMA_NW;
         } else {
             p.WM = lm_wm(p.NT);
             p.NW = lm_nw(p.NT);

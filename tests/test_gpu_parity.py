@@ -81,10 +81,12 @@ def test_timed_entry_point_matches_and_times_the_lm_head():
     assert ev[0].elapsed_time(ev[1]) > 0.0
 
 
-def test_exact_ties_take_smaller_ids_and_use_the_slow_path():
+@pytest.mark.parametrize("d,dtype", [(64, "bf16"), (1040, "bf16"), (272, "f32")])
+def test_exact_ties_take_smaller_ids_and_use_the_slow_path(d, dtype):
     """Duplicated LM-head rows give exactly equal logits; the (value desc, id
-    asc) order must hold and the exact slow path must be exercised."""
-    w = W("bf16-ties", 1, 64, 2000, 3, 4, 24, 32, "bf16", 1.0, 14, 140)
+    asc) order must hold and the exact slow path must be exercised (d = 1040:
+    the re-evaluation's 512-element pieces end inside a column)."""
+    w = W(f"{dtype}-ties-d{d}", 1, d, 2000, 3, 4, 24, 32, dtype, 1.0, 14, 140)
     cpu = synth.make_inputs(w, "cpu", weight_std=0.1)
     # only five distinct output embeddings: token v uses row v % 5, so every
     # vocabulary slice holds many exactly equal logits
