@@ -286,7 +286,15 @@ def time_steps(w, copies, h, root, steps, warmup, context=None):
     torch.cuda.synchronize()
     names = ["stage1_lmhead_topk", "arapprox_mlp", "stage2_lmhead_topk", "tree"]
     us = {n: 1000.0 * sum(e[j].elapsed_time(e[j + 1]) for e in evs) / steps for j, n in enumerate(names)}
-    us["step"] = sum(us.values())
+    # whole steps with no event between the calls (each one idles the GPU briefly)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    us["step"] = 1000.0 * e0.elapsed_time(e1) / steps
     return us
 
 
