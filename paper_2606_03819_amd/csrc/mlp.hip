@@ -110,13 +110,16 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const uint16_t* 
         dst = et + (size_t)rr * npre * d + (size_t)which * d;
     }
     const int npc = d >> 3;   // 16-byte pieces
-    u32x4 v[MAXC];
+    u32x4 v[MAXC], gv[MAXC];
     float ss = 0.f;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
         const int pc = lane + 64 * c;
         if (pc < npc) {
             v[c] = *reinterpret_cast<const u32x4*>(src + 8 * pc);
+            // the gains travel with the vector: one round trip for both
+            gv[c] = gain != nullptr ? *reinterpret_cast<const u32x4*>(gain + 8 * pc)
+                                    : u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};   // bf16 ones
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu), hi = bf16_bits_to_f32(v[c][q] >> 16);
@@ -131,13 +134,11 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const uint16_t* 
     for (int c = 0; c < MAXC; ++c) {
         const int pc = lane + 64 * c;
         if (pc < npc) {
-            u32x4 gv = u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};   // bf16 ones
-            if (gain != nullptr) gv = *reinterpret_cast<const u32x4*>(gain + 8 * pc);
             u32x4 o;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu) * inv * bf16_bits_to_f32(gv[q] & 0xffffu);
-                const float hi = bf16_bits_to_f32(v[c][q] >> 16) * inv * bf16_bits_to_f32(gv[q] >> 16);
+                const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu) * inv * bf16_bits_to_f32(gv[c][q] & 0xffffu);
+                const float hi = bf16_bits_to_f32(v[c][q] >> 16) * inv * bf16_bits_to_f32(gv[c][q] >> 16);
                 o[q] = f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
             }
             *reinterpret_cast<u32x4*>(dst + 8 * pc) = o;
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict
 
 // ------------------------------------------------------------------ launcher
 
-template <int WM, int NT, int PIPE, bool WNT>
+template <int WM, int NT, int NW, int PIPE, bool WNT>
 static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                             const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
                             int ew, int I, const RowTable& rt, const GemmPlan& pg, const GemmPlan& pd,
@@ -250,13 +251,13 @@ static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_
     WRowsGateUp wgu{wg, wu, I, d + ew};
     XRowsConcat xc{ht, et, d, ew, rt};
     const GemmShape shg = pg.shape(rows, d + ew);
-    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(shg.G), dim3(64 * TF_NW), 0, st, wgu, xc,
+    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgu, xc,
                        shg, act, I, partial, counters);
     // the activation is [rows, 2I] bf16 hi/lo pairs
     WRowsPairedK wdn{wd, d, I};
     XRowsPlain xa{act, 2l * I};
     const GemmShape shd = pd.shape(rows, 2 * I);
-    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, TF_NW, PIPE, WNT>), dim3(shd.G), dim3(64 * TF_NW), 0, st, wdn, xa,
+    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shd.G), dim3(64 * NW), 0, st, wdn, xa,
                        shd, hp, h, d, rt, partial, counters + pg.counter_ints());
 }
 
@@ -311,19 +312,28 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
         const uint16_t* etb = static_cast<const uint16_t*>(et);
         uint16_t* actb = static_cast<uint16_t*>(act);
         uint16_t* hpb = static_cast<uint16_t*>(hp);
-        // both products of one call share the row blocking (same rows)
+        // both products of one call share the row blocking (same rows, so the
+        // same waves per workgroup)
+        constexpr bool kWnt = TF_MLP_WNT != 0;
         if (pg.NT == 1)
-            launch_mlp_bf16<2, 1, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew,
-                                                                       I, rt, pg, pd, mlp_partial, counters, stream);
+            launch_mlp_bf16<2, 1, TF_NW_SINGLE, TF_PIPE_DEFAULT, kWnt>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
+                                                                        ew, I, rt, pg, pd, mlp_partial, counters,
+                                                                        stream);
         else if (pg.NT == 2)
-            launch_mlp_bf16<1, 2, TF_PIPE_DEFAULT, (TF_MLP_WNT != 0)>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew,
-                                                                       I, rt, pg, pd, mlp_partial, counters, stream);
-        else if (pg.wnt)
-            launch_mlp_bf16<1, 4, TF_PIPE_SINGLE_NT4, true>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg,
-                                                            pd, mlp_partial, counters, stream);
+            launch_mlp_bf16<1, 2, TF_NW_SINGLE, TF_PIPE_DEFAULT, kWnt>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
+                                                                        ew, I, rt, pg, pd, mlp_partial, counters,
+                                                                        stream);
+        else if (pg.nrb == 1 && pg.wnt)
+            launch_mlp_bf16<1, 4, TF_NW_SINGLE, TF_PIPE_SINGLE_NT4, true>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
+                                                                           ew, I, rt, pg, pd, mlp_partial, counters,
+                                                                           stream);
+        else if (pg.nrb == 1)
+            launch_mlp_bf16<1, 4, TF_NW_SINGLE, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
+                                                                         ew, I, rt, pg, pd, mlp_partial, counters,
+                                                                         stream);
         else
-            launch_mlp_bf16<1, 4, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg,
-                                                          pd, mlp_partial, counters, stream);
+            launch_mlp_bf16<1, 4, TF_NW, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I,
+                                                                  rt, pg, pd, mlp_partial, counters, stream);
     } else {
         launch_norms<float>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
                             counters, 0, stream);
@@ -353,12 +363,16 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
         const GemmShape sh = pl.shape(rows, 2 * d);
         uint16_t* hpb = static_cast<uint16_t*>(hp);
         const uint16_t* hb = static_cast<const uint16_t*>(h);
+        constexpr int S = TF_NW_SINGLE;
         if (pl.NT == 1)
-            hipLaunchKernelGGL((linear_bf16_kernel<2, 1, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
-                               0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
+            hipLaunchKernelGGL((linear_bf16_kernel<2, 1, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
+                               stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
         else if (pl.NT == 2)
-            hipLaunchKernelGGL((linear_bf16_kernel<1, 2, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
-                               0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
+            hipLaunchKernelGGL((linear_bf16_kernel<1, 2, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
+                               stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
+        else if (pl.nrb == 1)
+            hipLaunchKernelGGL((linear_bf16_kernel<1, 4, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
+                               stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
         else
             hipLaunchKernelGGL((linear_bf16_kernel<1, 4, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
                                0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);

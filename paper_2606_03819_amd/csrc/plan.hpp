@@ -17,10 +17,16 @@ constexpr int kMaxTopk = 1024;         // longest top-k list the merge kernel so
 constexpr int kMaxBudget = 4095;       // tree nodes per sequence
 constexpr int kNumCUs = 256;           // compute units of an MI355X
 
-// Waves per workgroup of the bf16 streaming products; one such workgroup
-// fills a CU's register file at two waves per SIMD.
+// Waves per workgroup of the bf16 streaming products with several row
+// blocks; one such workgroup fills a CU's register file at two waves per
+// SIMD.  A single row block uses half the waves (two workgroups per CU): the
+// k-range is cut there, and a smaller workgroup leaves the last piece's
+// workgroup less partial sum to read back.
 #ifndef TF_NW
 #define TF_NW 8
+#endif
+#ifndef TF_NW_SINGLE
+#define TF_NW_SINGLE 4
 #endif
 // Tile ranges (workgroups) of the LM head when a single row block streams
 // the whole vocabulary.
@@ -32,10 +38,10 @@ constexpr int kNumCUs = 256;           // compute units of an MI355X
 // then cut; every cut adds a partial-sum round trip, so the smaller down
 // product uses fewer workgroups).
 #ifndef TF_MLP_WORKGROUPS
-#define TF_MLP_WORKGROUPS 256
+#define TF_MLP_WORKGROUPS 512
 #endif
 #ifndef TF_DOWN_WORKGROUPS
-#define TF_DOWN_WORKGROUPS 128
+#define TF_DOWN_WORKGROUPS 256
 #endif
 // Pipeline depth (k-chunks of loads in flight per wave) when a single row
 // block streams the weights once at NT = 4, and otherwise; the launchers pick
@@ -87,9 +93,9 @@ inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
     GemmPlan p;
     p.NT = plan_nt(rows);
     p.WM = plan_wm(p.NT);
-    p.NW = TF_NW;
-    p.chunk = p.NW * p.WM;
     p.nrb = cdiv(rows, 32 * p.NT);
+    p.NW = p.nrb == 1 ? TF_NW_SINGLE : TF_NW;
+    p.chunk = p.NW * p.WM;
     p.ntiles = ntiles;
     p.nchunks = cdiv(ntiles, p.chunk);
     p.nk = cdiv(K, 64);
