@@ -61,9 +61,10 @@ def kernel_source_digest() -> str:
 def lm_kernel_pattern(rows: int, d: int) -> str:
     """Regex for the bf16 LM-head kernel instance the plan picks for `rows` rows
     (template arguments: weight tiles per wave, activation tiles, waves, ...):
-    128-row tiles with d a multiple of 64 go to the LDS-DMA kernel."""
+    128-row tiles go to the LDS-DMA kernel when d is a multiple of its k step
+    (64 for one row block, 32 for several)."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
-    if nt == 4 and d % 64 == 0:
+    if nt == 4 and (d % 64 == 0 or (rows > 128 and d % 32 == 0)):
         return r"lmhead_dma_kernel<\d+, 4, "
     return rf"lmhead_bf16_kernel<\d+, {nt}, "
 

@@ -122,8 +122,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int WM, int NT, int NW, int KC, int S, bool WNT>
-__global__ __launch_bounds__(64 * NW, 1) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,
+template <int WM, int NT, int NW, int KC, int S, bool WNT, int MINB>
+__global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,
                                                                 const uint16_t* __restrict__ w, GemmShape sh,
                                                                 SliceMap map, int V, float sl2,
                                                                 float* __restrict__ part, int* __restrict__ diag) {
@@ -696,12 +696,12 @@ static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const
                        map, V, sl2, part, diag);
 }
 
-template <int WM, int NT, int NW, int KC, bool WNT>
+template <int WM, int NT, int NW, int KC, bool WNT, int MINB = 1>
 static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
                                 const SliceMap& map, int blocks, int V, float sl2, float* part, int* diag,
                                 hipStream_t st) {
     using T = DmaTraits<WM, NT, NW, KC, TF_LM_DMA_STAGES>;
-    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT>;
+    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT, MINB>;
     // dynamic LDS beyond the 64 KiB default
     const hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
@@ -723,8 +723,8 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
         if (p.wnt)   // a single row block
             return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb, V,
                                                                                            sl2, part, diag, st);
-        return launch_lm_dma<TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false>(x, ldx, w, sh, p.map, nb,
-                                                                                             V, sl2, part, diag, st);
+        return launch_lm_dma<TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false, TF_LM_DMA_MULTI_MINB>(
+            x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     }
     if (p.NT == 1)
         launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
