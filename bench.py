@@ -13,8 +13,9 @@ roofline of the dominant kernel (the stage-2 LM-head GEMM, timed alone with HIP
 events recorded around its launch), and the CPU oracle timed on a bounded
 sample on this host.
 
-Offline helpers (no GPU): --summarize-trace and --summarize-pmc turn
-rocprofv3 output into the text summaries kept under profiles/; the HBM traffic
+Offline helpers (no GPU): --summarize-trace, --summarize-pmc and
+--summarize-mfma turn rocprofv3 output into the text summaries kept under
+profiles/; the HBM traffic
 summary is read back into roofline.traffic while the kernel sources are
 unchanged since the counters were taken.
 """
@@ -41,6 +42,9 @@ from paper_2606_03819_amd import binding, synth  # noqa: E402
 METRIC = "draft trees/sec (+ conditional rows/sec) at Qwen3-8B shape; HBM GB/s or MFMA % of peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+NOMINAL_GHZ = 2.4              # the clock the MFMA peak is rated at
+XCDS = 8                       # accelerator dies (GRBM counters sum over them)
+SIMDS = 1024                   # 256 CUs x 4 SIMDs
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector/MFMA
 RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
 PROFILES = os.path.join(ROOT, "profiles")
@@ -101,6 +105,8 @@ def parse():
                     help="after timing, copy 1 GiB three times (torch.neg, read 1 GiB + write 1 GiB) "
                          "for counter calibration")
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a kernel-trace summary of a rocprofv3 run")
+    ap.add_argument("--summarize-mfma", metavar="DIR", help="print the MFMA use of the stage-2 LM-head kernel "
+                    "from a rocprofv3 run with SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the HBM traffic summary from FETCH_SIZE and WRITE_SIZE rocprofv3 runs")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
@@ -224,6 +230,47 @@ def summarize_pmc(args):
     print("```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
+def summarize_mfma(args):
+    """MFMA busy cycles and the clock of the stage-2 LM-head kernel (the longest
+    dispatches of its instance), against the FLOP rate they imply."""
+    w = synth.get_workload(args.workload)
+    pattern = lm_kernel_pattern(w.rows * w.b, w.d)
+    cur = _db(args.summarize_mfma).cursor()
+    per = {}
+    for name, c, disp, v, dur in cur.execute("select name, counter_name, dispatch_id, sum(counter_value), "
+                                             "avg(duration) from pmc_events group by name, counter_name, "
+                                             "dispatch_id"):
+        if re.search(pattern, name):
+            per.setdefault(disp, {"name": name.split("(")[0], "dur_ns": dur})[c] = v
+    if not per:
+        raise SystemExit("kernel not found in the counter run")
+    longest = max(d["dur_ns"] for d in per.values())
+    picks = [d for d in per.values() if d["dur_ns"] > 0.5 * longest]   # stage 2 (stage 1 has fewer rows)
+    flops = 2.0 * w.rows * w.b * w.V * w.d
+    rows_out = []
+    for d in picks:
+        t = d["dur_ns"] * 1e-9
+        clock = d["GRBM_GUI_ACTIVE"] / XCDS / t
+        busy = d["SQ_VALU_MFMA_BUSY_CYCLES"] / (clock * t * SIMDS)
+        rows_out.append((d["dur_ns"] / 1e3, clock / 1e9, busy, flops / t / 1e12))
+    n = len(rows_out)
+    avg = [sum(r[i] for r in rows_out) / n for i in range(4)]
+    print(f"# MFMA use of the stage-2 LM-head kernel, {w.name}\n")
+    print(f"One rocprofv3 counter run of the bench command; `SQ_VALU_MFMA_BUSY_CYCLES` summed over the "
+          f"{SIMDS} SIMDs, the clock from `GRBM_GUI_ACTIVE` (summed over {XCDS} XCDs) over the dispatch "
+          f"duration.  {w.rows * w.b} rows x V = {w.V} x d = {w.d}: {flops / 1e12:.3f} TFLOP per launch.\n")
+    print(f"Command (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
+    print("| dispatch | us | clock GHz | MFMA busy | TFLOP/s | of 2.5 PF | of peak at this clock |")
+    print("|---|---|---|---|---|---|---|")
+    for i, (us, ghz, busy, tf) in enumerate(rows_out):
+        print(f"| {i} | {us:.0f} | {ghz:.3f} | {busy:.3f} | {tf:.0f} | {tf / BF16_PEAK_TFLOPS:.3f} | "
+              f"{tf / (BF16_PEAK_TFLOPS * ghz / NOMINAL_GHZ):.3f} |")
+    print(f"\nKernel `{picks[0]['name']}`; mean over {n} dispatches: {avg[0]:.0f} us at {avg[1]:.3f} GHz, MFMA "
+          f"busy {avg[2]:.3f} of SIMD cycles, {avg[3]:.0f} TFLOP/s = {avg[3] / BF16_PEAK_TFLOPS:.3f} of the "
+          f"2.5 PF peak (rated at {NOMINAL_GHZ} GHz).  The busy fraction exceeds the FLOP fraction at the "
+          f"measured clock by the padded rows ({-(-(w.rows * w.b) // 128) * 128} computed for {w.rows * w.b}).")
+
+
 def make_drafter(w, weights):
     """The drafter of the workload's approximator (its buffers and workspace)."""
     cls = binding.Drafter2Prev if w.approximator == "2prev" else binding.Drafter
@@ -321,6 +368,9 @@ def main():
     args = parse()
     if args.summarize_trace:
         summarize_trace(args)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args)
         return
     if args.summarize_pmc:
         summarize_pmc(args)
