@@ -4,12 +4,21 @@
 namespace tf {
 
 // Entries each (row, vocabulary slice) partial keeps, and the partial layout:
-// [max, sum, bound, count, val[kKeep], idx[kKeep]] (raw, unscaled logits).
+// [max, sum, bound, count, val[keep], idx[keep]] (raw, unscaled logits).
+// Long lists (kKeepLong per slice, kLaneMfmaLong per lane and row in the
+// MFMA epilogue) serve top-k lists of at least kLongListK entries: with
+// short ones a row's best logits overflow a slice's or a lane's list often
+// enough there that the exact re-evaluation dominates.
 constexpr int kKeep = 4;
+constexpr int kKeepLong = 8;
 constexpr int kPartStride = 4 + 2 * kKeep;
+constexpr int kPartStrideLong = 4 + 2 * kKeepLong;
+constexpr int kLongListK = 64;
+constexpr int part_stride(int keep) { return 4 + 2 * keep; }
 // Per-thread running list lengths inside the LM-head epilogues (SIMT fp32
 // kernel, MFMA bf16 kernel).
 constexpr int kLane = 4;
 constexpr int kLaneMfma = 2;
+constexpr int kLaneMfmaLong = 3;
 
 }  // namespace tf

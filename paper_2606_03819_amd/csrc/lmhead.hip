@@ -14,14 +14,14 @@ namespace tf {
 
 // One workgroup per (tile range, row block): the range's rounds in turn, each
 // a full pass over K reduced to a (row, slice) partial.
-template <int WM, int NT, int NW, int PIPE, bool WNT>
+template <int WM, int NT, int NW, int PIPE, bool WNT, bool LONG>
 __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t* __restrict__ x, long ldx,
                                                                                const uint16_t* __restrict__ w,
                                                                                GemmShape sh, SliceMap map, int V,
                                                                                float sl2, float* __restrict__ part,
                                                                                int* __restrict__ diag) {
     using Tr = GemmTraits<WM, NT, NW>;
-    using E = EpiLmHead<WM, NT, NW>;
+    using E = EpiLmHead<WM, NT, NW, LONG>;
     constexpr int SMEM = Tr::SMEM_BYTES > E::MERGE_BYTES ? Tr::SMEM_BYTES : E::MERGE_BYTES;
     __shared__ __align__(16) unsigned char smem[SMEM];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
@@ -47,7 +47,7 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
         if (seg.t0 == seg.t1) {   // empty slice: a partial the merge skips
             const int t = threadIdx.x;
             if (t < Tr::TR && seg.row0 + t < sh.R) {
-                float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * kPartStride;
+                float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * part_stride(E::KEEP);
                 o[0] = neg_inf();
                 o[1] = 0.f;
                 o[2] = neg_inf();
@@ -122,13 +122,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int WM, int NT, int NW, int KC, int S, bool WNT, int MINB>
+template <int WM, int NT, int NW, int KC, int S, bool WNT, int MINB, bool LONG>
 __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,
                                                                 const uint16_t* __restrict__ w, GemmShape sh,
                                                                 SliceMap map, int V, float sl2,
                                                                 float* __restrict__ part, int* __restrict__ diag) {
     using T = DmaTraits<WM, NT, NW, KC, S>;
-    using E = EpiLmHead<WM, NT, NW>;
+    using E = EpiLmHead<WM, NT, NW, LONG>;
     static_assert(E::MERGE_BYTES <= T::RING, "the epilogue reuses the rings");
     extern __shared__ __align__(16) unsigned char dyn[];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
         if (seg.t0 == seg.t1) {   // empty slice: a partial the merge skips
             const int t = threadIdx.x;
             if (t < 32 * NT && seg.row0 + t < sh.R) {
-                float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * kPartStride;
+                float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * part_stride(E::KEEP);
                 o[0] = neg_inf();
                 o[1] = 0.f;
                 o[2] = neg_inf();
@@ -496,7 +496,9 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
     return v;
 }
 
-constexpr int kMergeCap = kMaxSplits * kKeep;   // candidate buffer: every slice entry fits
+// candidate buffer: every slice entry fits (long lists: at most kMaxSplitsLong slices)
+constexpr int kMergeCap = kMaxSplits * kKeep;
+static_assert(kMaxSplitsLong * kKeepLong <= kMergeCap, "long-list slices fit the candidate buffer");
 
 // One workgroup per row.
 //  1. log-sum-exp of the row from the slices' (max, sum) pairs;
@@ -508,8 +510,9 @@ constexpr int kMergeCap = kMaxSplits * kKeep;   // candidate buffer: every slice
 //  4. a slice whose bound (everything it dropped is <= bound) reaches the k-th
 //     value is re-evaluated exactly from memory, so the result is the exact
 //     top-k of the row for any data, ties included.
-template <class T>
+template <class T, int KEEP>
 __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
+    constexpr int PS = part_stride(KEEP);
     __shared__ float red[4];
     __shared__ float s_bound[4];
     __shared__ int s_count, s_nflag, s_ncand;
@@ -521,17 +524,17 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     const int row = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int K = a.K;
-    const float* P = a.part + (size_t)row * a.nsplit * kPartStride;
+    const float* P = a.part + (size_t)row * a.nsplit * PS;
 
     float M = neg_inf();
-    for (int s = tid; s < a.nsplit; s += 256) M = fmaxf(M, P[s * kPartStride]);
+    for (int s = tid; s < a.nsplit; s += 256) M = fmaxf(M, P[s * PS]);
     M = block_max(M, red);
     float S = 0.f;
     float head = neg_inf();
     for (int s = tid; s < a.nsplit; s += 256) {
-        const float ms = P[s * kPartStride];
-        if (ms != neg_inf()) S += P[s * kPartStride + 1] * exp2f((ms - M) * a.sl2);
-        if (__float_as_int(P[s * kPartStride + 3]) > 0) head = fmaxf(head, P[s * kPartStride + 4]);
+        const float ms = P[s * PS];
+        if (ms != neg_inf()) S += P[s * PS + 1] * exp2f((ms - M) * a.sl2);
+        if (__float_as_int(P[s * PS + 3]) > 0) head = fmaxf(head, P[s * PS + 4]);
     }
     S = block_sum(S, red);
     const float logS = logf(S);
@@ -548,14 +551,14 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     const float t0 = fmaxf(fmaxf(s_bound[0], s_bound[1]), fmaxf(s_bound[2], s_bound[3]));
 
     for (int s = tid; s < a.nsplit; s += 256) {
-        const float* ps = P + s * kPartStride;
+        const float* ps = P + s * PS;
         const int n = __float_as_int(ps[3]);
         for (int e = 0; e < n; ++e) {
             const float v = ps[4 + e];
             if (!(v >= t0)) break;   // lists are sorted
             const int pos = atomicAdd(&s_count, 1);
             cand_v[pos] = v;
-            cand_i[pos] = __float_as_int(ps[4 + kKeep + e]);
+            cand_i[pos] = __float_as_int(ps[4 + KEEP + e]);
         }
     }
     __syncthreads();
@@ -592,7 +595,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 
     const float tval = cnt == K ? sel_v[K - 1] : neg_inf();
     for (int s = tid; s < a.nsplit; s += 256) {
-        const float U = P[s * kPartStride + 2];
+        const float U = P[s * PS + 2];
         if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = s;
     }
     __syncthreads();
@@ -689,19 +692,19 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 
 // ------------------------------------------------------------------ launchers
 
-template <int WM, int NT, int NW, int PIPE, bool WNT>
+template <bool LONG, int WM, int NT, int NW, int PIPE, bool WNT>
 static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh, const SliceMap& map,
                            int blocks, int V, float sl2, float* part, int* diag, hipStream_t st) {
-    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(blocks), dim3(64 * NW), 0, st, x, ldx, w, sh,
-                       map, V, sl2, part, diag);
+    hipLaunchKernelGGL((lmhead_bf16_kernel<WM, NT, NW, PIPE, WNT, LONG>), dim3(blocks), dim3(64 * NW), 0, st, x, ldx,
+                       w, sh, map, V, sl2, part, diag);
 }
 
-template <int WM, int NT, int NW, int KC, bool WNT, int MINB = 1>
+template <bool LONG, int WM, int NT, int NW, int KC, bool WNT, int MINB = 1>
 static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
                                 const SliceMap& map, int blocks, int V, float sl2, float* part, int* diag,
                                 hipStream_t st) {
     using T = DmaTraits<WM, NT, NW, KC, TF_LM_DMA_STAGES>;
-    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT, MINB>;
+    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT, MINB, LONG>;
     // dynamic LDS beyond the 64 KiB default
     const hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
@@ -711,32 +714,34 @@ static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, 
 }
 
 // tile shape and pipeline variants the plans can ask for
+template <bool LONG>
 static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx, const uint16_t* w,
                                    const GemmShape& sh, int V, float sl2, float* part, int* diag, hipStream_t st) {
     const int nb = p.blocks();
     if (p.dma) {   // the shapes the plans use (see lm_plan)
 #if TF_LM_DMA_NT1
         if (p.NT == 1)
-            return launch_lm_dma<TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb,
+            return launch_lm_dma<LONG, TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb,
                                                                                             V, sl2, part, diag, st);
 #endif
         if (p.wnt)   // a single row block
-            return launch_lm_dma<TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb, V,
+            return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb, V,
                                                                                            sl2, part, diag, st);
-        return launch_lm_dma<TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false, TF_LM_DMA_MULTI_MINB>(
+        return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false,
+                             TF_LM_DMA_MULTI_MINB>(
             x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
     }
     if (p.NT == 1)
-        launch_lm_bf16<TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+        launch_lm_bf16<LONG, TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
                                                                            diag, st);
     else if (p.NT == 2)
-        launch_lm_bf16<TF_LM_WM_NT2, 2, TF_LM_NW_NT2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+        launch_lm_bf16<LONG, TF_LM_WM_NT2, 2, TF_LM_NW_NT2, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,
                                                                            diag, st);
     else if (p.wnt)
-        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, p.map, nb, V, sl2,
+        launch_lm_bf16<LONG, TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_SINGLE_NT4, true>(x, ldx, w, sh, p.map, nb, V, sl2,
                                                                               part, diag, st);
     else
-        launch_lm_bf16<TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, p.map, nb, V, sl2, part,
+        launch_lm_bf16<LONG, TF_LM_WM_NT4, 4, TF_LM_NW_NT4, TF_PIPE_DEFAULT, false>(x, ldx, w, sh, p.map, nb, V, sl2, part,
                                                                             diag, st);
     return hipSuccess;
 }
@@ -752,9 +757,13 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
     const GemmShape sh{rows, d, p.ntiles, p.map.G, p.nrb, p.nk, p.blocks()};
     const float sl2 = inv_t * kLog2e;
     if (ev_begin != nullptr && hipEventRecord(ev_begin, stream) != hipSuccess) return hipErrorInvalidHandle;
+    const bool longl = lm_long_lists(p, bf16, K);
     if (bf16) {
-        const hipError_t de = dispatch_lm_bf16(p, static_cast<const uint16_t*>(x), ldx,
-                                               static_cast<const uint16_t*>(w), sh, V, sl2, part, diag, stream);
+        const hipError_t de =
+            longl ? dispatch_lm_bf16<true>(p, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
+                                           sh, V, sl2, part, diag, stream)
+                  : dispatch_lm_bf16<false>(p, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
+                                            sh, V, sl2, part, diag, stream);
         if (de != hipSuccess) return de;
     } else
         hipLaunchKernelGGL(lmhead_f32_kernel, dim3(p.blocks()), dim3(256), 0, stream, static_cast<const float*>(x),
@@ -763,10 +772,12 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
     if (e != hipSuccess) return e;
     if (ev_end != nullptr && hipEventRecord(ev_end, stream) != hipSuccess) return hipErrorInvalidHandle;
     MergeArgs ma{part, p.nsplit(), p.map, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
-    if (bf16)
-        hipLaunchKernelGGL(merge_topk_kernel<uint16_t>, dim3(rows), dim3(256), 0, stream, ma);
+    if (bf16 && longl)
+        hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeepLong>), dim3(rows), dim3(256), 0, stream, ma);
+    else if (bf16)
+        hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep>), dim3(rows), dim3(256), 0, stream, ma);
     else
-        hipLaunchKernelGGL(merge_topk_kernel<float>, dim3(rows), dim3(256), 0, stream, ma);
+        hipLaunchKernelGGL((merge_topk_kernel<float, kKeep>), dim3(rows), dim3(256), 0, stream, ma);
     return hipGetLastError();
 }
 

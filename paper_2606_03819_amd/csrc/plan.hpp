@@ -13,6 +13,7 @@
 namespace tf {
 
 constexpr int kMaxSplits = 2048;       // vocabulary slices (partials per row); kMaxSplits*kKeep <= merge capacity
+constexpr int kMaxSplitsLong = 1024;   // slices up to which a launch may keep long lists
 constexpr int kMaxTopk = 1024;         // longest top-k list the merge kernel sorts
 constexpr int kMaxBudget = 4095;       // tree nodes per sequence
 constexpr int kNumCUs = 256;           // compute units of an MI355X
@@ -251,10 +252,18 @@ inline GemmPlan linear_plan(int rows, int d) { return mlp_plan(rows, cdiv(d, 32)
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// LM-head scratch: the (row, slice) partials.
+// Long (row, slice) lists for top-k lists of at least kLongListK entries
+// (bf16 kernels, while the merge's candidate buffer holds every entry).
+inline bool lm_long_lists(const LmPlan& p, bool bf16, int K) {
+    return bf16 && K >= kLongListK && p.nsplit() <= kMaxSplitsLong;
+}
+
+// LM-head scratch: the (row, slice) partials, sized for the long lists
+// whenever a launch could keep them.
 inline size_t lm_scratch_bytes(int rows, int V, int d, bool bf16) {
     const LmPlan p = lm_plan(rows, V, d, bf16);
-    return align256((size_t)rows * p.nsplit() * kPartStride * 4);
+    const int stride = bf16 && p.nsplit() <= kMaxSplitsLong ? kPartStrideLong : kPartStride;
+    return align256((size_t)rows * p.nsplit() * stride * 4);
 }
 
 struct Workspace {

@@ -377,8 +377,8 @@ struct XRowsConcat {
 // Merge the NC contributor lists of each activation row (written to `cm` as
 // [rows][NC][3 + 2*KL] = max, sum, bound, KL values, KL ids; `bound` is at
 // least every value the contributor saw but did not list) into the row's
-// (row, slice) partial.  One thread per row.
-template <int NC, int KL>
+// (row, slice) partial of KEEP entries.  One thread per row.
+template <int NC, int KL, int KEEP = kKeep>
 __device__ inline void lm_merge_contributors(const float* cm, int rstride, int rows, int row0, int split, int nsplit,
                                              int R, float sl2, float* part) {
     constexpr int W = 3 + 2 * KL;
@@ -399,12 +399,12 @@ __device__ inline void lm_merge_contributors(const float* cm, int rstride, int r
         const float mp = c[p * W + 0];
         S += (mp == neg_inf()) ? 0.f : c[p * W + 1] * exp2f((mp - M) * sl2);
     }
-    float* out = part + ((size_t)grow * nsplit + split) * kPartStride;
+    float* out = part + ((size_t)grow * nsplit + split) * part_stride(KEEP);
     int ptr[NC];
 #pragma unroll
     for (int p = 0; p < NC; ++p) ptr[p] = 0;
     int cnt = 0;
-    for (int e = 0; e <= kKeep; ++e) {
+    for (int e = 0; e <= KEEP; ++e) {
         float bv = neg_inf();
         int bi = -1, bp = -1;
 #pragma unroll
@@ -420,19 +420,19 @@ __device__ inline void lm_merge_contributors(const float* cm, int rstride, int r
             }
         }
         if (bp < 0) break;
-        if (e == kKeep) {
+        if (e == KEEP) {
             U = fmaxf(U, bv);
             break;
         }
 #pragma unroll
         for (int p = 0; p < NC; ++p) ptr[p] += (p == bp) ? 1 : 0;
         out[4 + e] = bv;
-        out[4 + kKeep + e] = __int_as_float(bi);
+        out[4 + KEEP + e] = __int_as_float(bi);
         ++cnt;
     }
-    for (int e = cnt; e < kKeep; ++e) {
+    for (int e = cnt; e < KEEP; ++e) {
         out[4 + e] = neg_inf();
-        out[4 + kKeep + e] = __int_as_float(-1);
+        out[4 + KEEP + e] = __int_as_float(-1);
     }
     out[0] = M;
     out[1] = S;
@@ -440,24 +440,27 @@ __device__ inline void lm_merge_contributors(const float* cm, int rstride, int r
     out[3] = __int_as_float(cnt);
 }
 
-// LM head: per lane and row, the maximum, the sum of exponentials, the two
+// LM head: per lane and row, the maximum, the sum of exponentials, the KL
 // best logits with their token ids and a bound on the rest (the largest logit
-// the lane drops); merged per workgroup into a (row, slice) partial of kKeep
-// entries, the slice being the workgroup's chunk of the vocabulary.
+// the lane drops); merged per workgroup into a (row, slice) partial of KEEP
+// entries, the slice being the workgroup's chunk of the vocabulary (LONG:
+// the long lists for large top-k).
 //
 // The partial's `bound` is an upper bound on every logit of the slice that is
 // not in its list: a lane drops only values no larger than its bound, and the
 // workgroup merge drops only values no larger than the (kKeep+1)-th entry of
 // the union.  The merge kernel uses it to prove the global top-k exact, or to
-// re-evaluate the slice when it cannot.  Two entries per lane keep this pass
-// cheap (it runs on the vector ALUs after every item); a slice is re-evaluated
-// only if one lane holds three of the row's best k logits.
-template <int WM, int NT, int NW>
+// re-evaluate the slice when it cannot.  Short lists (two entries per lane)
+// keep this pass cheap (it runs on the vector ALUs after every item); a
+// slice is re-evaluated only if one lane holds KL + 1 of the row's best k
+// logits or the slice KEEP + 1 of them.
+template <int WM, int NT, int NW, bool LONG = false>
 struct EpiLmHead {
-    float* part;     // [R, nchunks, kPartStride]
+    float* part;     // [R, nchunks, part_stride(KEEP)]
     int V;
     float sl2;       // inv_temperature * log2(e)
-    static constexpr int KL = kLaneMfma;
+    static constexpr int KL = LONG ? kLaneMfmaLong : kLaneMfma;
+    static constexpr int KEEP = LONG ? kKeepLong : kKeep;
     static constexpr int NC = 2 * NW;             // contributor lists per row
     static constexpr int MERGE_WORDS = 3 + 2 * KL;
     // odd row stride: the lanes of a wave (consecutive rows) hit distinct banks
@@ -483,9 +486,16 @@ struct EpiLmHead {
             for (int j = 0; j < 16; ++j) m = fmaxf(m, x[mt][j]);
         const float ms = m * sl2;
         float s = 0.f;
-        float l0 = neg_inf(), l1 = neg_inf(), rest = neg_inf();
-        int i0 = -1, i1 = -1;
-        // visited in increasing token id, so a tie keeps the smaller id first
+        float lv[KL], rest = neg_inf();
+        int li[KL];
+#pragma unroll
+        for (int q = 0; q < KL; ++q) {
+            lv[q] = neg_inf();
+            li[q] = -1;
+        }
+        // visited in increasing token id, so a tie keeps the smaller id first:
+        // a logit enters the list only past a strictly smaller one, and the
+        // entries below its place move down one
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
@@ -493,27 +503,34 @@ struct EpiLmHead {
                 const float xv = x[mt][j];
                 const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
                 s += exp2f(fmaf(xv, sl2, -ms));
-                const bool c0 = xv > l0, c1 = xv > l1;
-                rest = fmaxf(rest, c1 ? l1 : xv);
-                const float nl1 = c0 ? l0 : (c1 ? xv : l1);
-                const int ni1 = c0 ? i0 : (c1 ? v : i1);
-                l0 = c0 ? xv : l0;
-                i0 = c0 ? v : i0;
-                l1 = nl1;
-                i1 = ni1;
+                rest = fmaxf(rest, xv > lv[KL - 1] ? lv[KL - 1] : xv);
+                bool ins = false;
+                float cv = xv;
+                int ci = v;
+#pragma unroll
+                for (int q = 0; q < KL; ++q) {
+                    const bool sw = ins || cv > lv[q];
+                    const float tv = sw ? lv[q] : cv;
+                    const int ti = sw ? li[q] : ci;
+                    lv[q] = sw ? cv : lv[q];
+                    li[q] = sw ? ci : li[q];
+                    cv = tv;
+                    ci = ti;
+                    ins = sw;
+                }
             }
         c[0] = m;
         c[1] = m == neg_inf() ? 0.f : s;
         c[2] = rest;
-        c[3] = l0;
-        c[4] = l1;
-        c[5] = __int_as_float(i0);
-        c[6] = __int_as_float(i1);
+#pragma unroll
+        for (int q = 0; q < KL; ++q) {
+            c[3 + q] = lv[q];
+            c[3 + KL + q] = __int_as_float(li[q]);
+        }
     }
 
     __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char* smem,
                                           const GemmShape& sh) {
-        static_assert(KL == 2, "lane lists hold two entries");
         const int lane = threadIdx.x & 63;
         const int wave = threadIdx.x >> 6;
         float* cm = reinterpret_cast<float*>(smem);   // [32*NT rows, stride RSTRIDE][NC contributors][MERGE_WORDS]
@@ -526,7 +543,7 @@ struct EpiLmHead {
         for (int nt = 0; nt < NT; ++nt)
             lane_row(acc, nt, vbase, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
         __syncthreads();
-        lm_merge_contributors<NC, KL>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
+        lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
 };
 

@@ -81,12 +81,13 @@ def test_timed_entry_point_matches_and_times_the_lm_head():
     assert ev[0].elapsed_time(ev[1]) > 0.0
 
 
-@pytest.mark.parametrize("d,dtype", [(64, "bf16"), (1040, "bf16"), (272, "f32")])
-def test_exact_ties_take_smaller_ids_and_use_the_slow_path(d, dtype):
+@pytest.mark.parametrize("d,dtype,B", [(64, "bf16", 24), (1040, "bf16", 24), (272, "f32", 24), (64, "bf16", 80)])
+def test_exact_ties_take_smaller_ids_and_use_the_slow_path(d, dtype, B):
     """Duplicated LM-head rows give exactly equal logits; the (value desc, id
     asc) order must hold and the exact slow path must be exercised (d = 1040:
-    the re-evaluation's 512-element pieces end inside a column)."""
-    w = W(f"{dtype}-ties-d{d}", 1, d, 2000, 3, 4, 24, 32, dtype, 1.0, 14, 140)
+    the re-evaluation's 512-element pieces end inside a column; B = 80: the
+    80-entry stage-2 lists use the long per-slice lists)."""
+    w = W(f"{dtype}-ties-d{d}-B{B}", 1, d, 2000, 3, 4, B, 32, dtype, 1.0, 14, 140)
     cpu = synth.make_inputs(w, "cpu", weight_std=0.1)
     # only five distinct output embeddings: token v uses row v % 5, so every
     # vocabulary slice holds many exactly equal logits
