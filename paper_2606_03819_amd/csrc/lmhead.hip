@@ -496,6 +496,45 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
     return v;
 }
 
+// (value, id) pairs of a wave sorted in the (value desc, id asc) order, lane
+// 0 first: a bitonic network over __shfl_xor (ids are distinct, so the
+// order is total; padding pairs are equal and stay put).
+__device__ __forceinline__ void wave_sort_pairs(float& v, int& i, int lane) {
+    for (int k = 2; k <= 64; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const float ov = __shfl_xor(v, j);
+            const int oi = __shfl_xor(i, j);
+            const bool keep_better = ((lane & j) == 0) == ((lane & k) == 0);
+            const bool ob = better(ov, oi, v, i);
+            if (keep_better == ob) {
+                v = ov;
+                i = oi;
+            }
+        }
+}
+
+// The best 64 of two sorted wave lists (a, b), sorted: the better of a[l] and
+// b[63 - l] per lane is a bitonic sequence holding them, and half-cleaners
+// sort it.
+__device__ __forceinline__ void wave_merge_pairs(float& v, int& i, float bv, int bi, int lane) {
+    const float rv = __shfl(bv, 63 - lane);
+    const int ri = __shfl(bi, 63 - lane);
+    if (better(rv, ri, v, i)) {
+        v = rv;
+        i = ri;
+    }
+    for (int j = 32; j > 0; j >>= 1) {
+        const float ov = __shfl_xor(v, j);
+        const int oi = __shfl_xor(i, j);
+        const bool keep_better = (lane & j) == 0;
+        const bool ob = better(ov, oi, v, i);
+        if (keep_better == ob) {
+            v = ov;
+            i = oi;
+        }
+    }
+}
+
 // candidate buffer: every slice entry fits (long lists: at most kMaxSplitsLong slices)
 constexpr int kMergeCap = kMaxSplits * kKeep;
 static_assert(kMaxSplitsLong * kKeepLong <= kMergeCap, "long-list slices fit the candidate buffer");
@@ -526,15 +565,33 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     const int K = a.K;
     const float* P = a.part + (size_t)row * a.nsplit * PS;
 
+    // every slice's max, sum, bound, count and best logit, read once (the
+    // slices of a thread are tid, tid + 256, ...)
+    constexpr int SPT = kMaxSplits / 256;
+    f32x4 q[SPT];
+    float v0[SPT];
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const int s = tid + 256 * j;
+        if (s < a.nsplit) {
+            q[j] = *reinterpret_cast<const f32x4*>(P + s * PS);
+            v0[j] = P[s * PS + 4];
+        } else {
+            q[j] = f32x4{neg_inf(), 0.f, neg_inf(), 0.f};   // count 0
+            v0[j] = neg_inf();
+        }
+    }
     float M = neg_inf();
-    for (int s = tid; s < a.nsplit; s += 256) M = fmaxf(M, P[s * PS]);
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) M = fmaxf(M, q[j][0]);
     M = block_max(M, red);
     float S = 0.f;
     float head = neg_inf();
-    for (int s = tid; s < a.nsplit; s += 256) {
-        const float ms = P[s * PS];
-        if (ms != neg_inf()) S += P[s * PS + 1] * exp2f((ms - M) * a.sl2);
-        if (__float_as_int(P[s * PS + 3]) > 0) head = fmaxf(head, P[s * PS + 4]);
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const float ms = q[j][0];
+        if (ms != neg_inf()) S += q[j][1] * exp2f((ms - M) * a.sl2);
+        if (__float_as_int(q[j][3]) > 0) head = fmaxf(head, v0[j]);
     }
     S = block_sum(S, red);
     const float logS = logf(S);
@@ -550,19 +607,43 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     __syncthreads();
     const float t0 = fmaxf(fmaxf(s_bound[0], s_bound[1]), fmaxf(s_bound[2], s_bound[3]));
 
-    for (int s = tid; s < a.nsplit; s += 256) {
-        const float* ps = P + s * PS;
-        const int n = __float_as_int(ps[3]);
-        for (int e = 0; e < n; ++e) {
-            const float v = ps[4 + e];
-            if (!(v >= t0)) break;   // lists are sorted
-            const int pos = atomicAdd(&s_count, 1);
-            cand_v[pos] = v;
-            cand_i[pos] = __float_as_int(ps[4 + KEEP + e]);
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const int n = __float_as_int(q[j][3]);
+        if (n > 0 && v0[j] >= t0) {   // lists are sorted: the rest only if the best qualifies
+            const float* ps = P + (tid + 256 * j) * PS;
+            for (int e = 0; e < n; ++e) {
+                const float v = e == 0 ? v0[j] : ps[4 + e];
+                if (!(v >= t0)) break;
+                const int pos = atomicAdd(&s_count, 1);
+                cand_v[pos] = v;
+                cand_i[pos] = __float_as_int(ps[4 + KEEP + e]);
+            }
         }
     }
     __syncthreads();
     const int c = s_count;
+    if (K <= 64 && c <= 256) {
+        // each wave sorts 64 candidates in registers, wave 0 merges the four
+        // lists: the best 64 land sorted at the front of the buffer
+        const int e = 64 * wave + lane;
+        float v = e < c ? cand_v[e] : neg_inf();
+        int i = e < c ? cand_i[e] : 0x7fffffff;
+        wave_sort_pairs(v, i, lane);
+        cand_v[e] = v;
+        cand_i[e] = i;
+        __syncthreads();
+        if (wave == 0) {
+            float v1 = cand_v[64 + lane], v2 = cand_v[128 + lane], v3 = cand_v[192 + lane];
+            int i1 = cand_i[64 + lane], i2 = cand_i[128 + lane], i3 = cand_i[192 + lane];
+            wave_merge_pairs(v, i, v1, i1, lane);
+            wave_merge_pairs(v2, i2, v3, i3, lane);
+            wave_merge_pairs(v, i, v2, i2, lane);
+            cand_v[lane] = v;
+            cand_i[lane] = i;
+        }
+        __syncthreads();
+    } else {
     int pw = 1;
     while (pw < c) pw <<= 1;
     for (int i = c + tid; i < pw; i += 256) {
@@ -589,14 +670,16 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
             __syncthreads();
         }
     }
+    }
     int cnt = min(c, K);
     float* sel_v = cand_v;   // the best cnt entries, sorted
     int* sel_i = cand_i;
 
     const float tval = cnt == K ? sel_v[K - 1] : neg_inf();
-    for (int s = tid; s < a.nsplit; s += 256) {
-        const float U = P[s * PS + 2];
-        if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = s;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const float U = q[j][2];
+        if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = tid + 256 * j;
     }
     __syncthreads();
 
