@@ -209,7 +209,10 @@ __device__ __forceinline__ Cand wave_best(Cand best, const TreeLds& t) {
 }
 
 // Frontier in registers: slot s = lane + 64*j, j < FS (B + 1 <= 64*FS).
-template <int FS>
+// ALL: every rank of every row is cached (P = K2), so the row reads are LDS
+// reads only (a read that may go to either memory compiles to a flat load,
+// whose latency is that of the vector-memory path).
+template <int FS, bool ALL>
 __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a) {
     extern __shared__ __align__(16) unsigned char dyn[];
     const TreeLds t = tree_lds(dyn, a);
@@ -221,9 +224,11 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a
     __syncthreads();
     if (threadIdx.x >= 64) return;
     auto get_lp = [&](int r, int c) -> float {
+        if constexpr (ALL) return t.c_lp[r * a.P + c];
         return c < a.P ? t.c_lp[r * a.P + c] : rlp[(size_t)r * a.K2 + c];
     };
     auto get_idx = [&](int r, int c) -> int {
+        if constexpr (ALL) return t.c_idx[r * a.P + c];
         return c < a.P ? t.c_idx[r * a.P + c] : ridx[(size_t)r * a.K2 + c];
     };
     float f_score[FS], f_pscore[FS];
@@ -409,16 +414,22 @@ hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, cons
     TreeArgs a{cond_idx, cond_lp, topk_idx, gamma, M, topk2, B, Rs, P, mode,
                node_token, node_parent, node_depth, node_score, node_child_row};
     const void* fn;
+    const bool all = P >= topk2;
     if (B + 1 <= 64)
-        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<1>);
+        fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<1, true>)
+                 : reinterpret_cast<const void*>(build_tree_reg_kernel<1, false>);
     else if (B + 1 <= 128)
-        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<2>);
+        fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<2, true>)
+                 : reinterpret_cast<const void*>(build_tree_reg_kernel<2, false>);
     else if (B + 1 <= 256)
-        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<4>);
+        fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<4, true>)
+                 : reinterpret_cast<const void*>(build_tree_reg_kernel<4, false>);
     else if (B + 1 <= 512)
-        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<8>);
+        fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<8, true>)
+                 : reinterpret_cast<const void*>(build_tree_reg_kernel<8, false>);
     else if (B + 1 <= 64 * kTreeRegSlots)
-        fn = reinterpret_cast<const void*>(build_tree_reg_kernel<kTreeRegSlots>);
+        fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<kTreeRegSlots, true>)
+                 : reinterpret_cast<const void*>(build_tree_reg_kernel<kTreeRegSlots, false>);
     else
         fn = reinterpret_cast<const void*>(build_tree_kernel);
     // dynamic LDS beyond the 64 KiB default
