@@ -244,21 +244,53 @@ __global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict
 // ------------------------------------------------------------------ launcher
 
 template <int WM, int NT, int NW, int PIPE, bool WNT>
+static void launch_gateup(const uint16_t* wg, const uint16_t* wu, const uint16_t* ht, const uint16_t* et,
+                          uint16_t* act, int rows, int d, int ew, int I, const RowTable& rt, const GemmPlan& pg,
+                          float* partial, int* counters, hipStream_t st) {
+    WRowsGateUp wgu{wg, wu, I, d + ew};
+    XRowsConcat xc{ht, et, d, ew, rt};
+    const GemmShape shg = pg.shape(rows, d + ew);
+    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgu, xc, shg,
+                       act, I, partial, counters);
+}
+
+// the activation is [rows, 2I] bf16 hi/lo pairs
+template <int WM, int NT, int NW, int PIPE, bool WNT>
+static void launch_down(const uint16_t* h, const uint16_t* wd, const uint16_t* act, uint16_t* hp, int rows, int d,
+                        int I, const RowTable& rt, const GemmPlan& pd, float* partial, int* counters,
+                        hipStream_t st) {
+    WRowsPairedK wdn{wd, d, I};
+    XRowsPlain xa{act, 2l * I};
+    const GemmShape shd = pd.shape(rows, 2 * I);
+    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shd.G), dim3(64 * NW), 0, st, wdn, xa, shd,
+                       hp, h, d, rt, partial, counters);
+}
+
+// Both products share the row blocking (same rows); each plan picks its own
+// waves per workgroup.  The pipeline depth and the non-temporal weight loads
+// follow the plan's single-row-block choice.
+template <int WM, int NT>
 static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                             const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
                             int ew, int I, const RowTable& rt, const GemmPlan& pg, const GemmPlan& pd,
                             float* partial, int* counters, hipStream_t st) {
-    WRowsGateUp wgu{wg, wu, I, d + ew};
-    XRowsConcat xc{ht, et, d, ew, rt};
-    const GemmShape shg = pg.shape(rows, d + ew);
-    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgu, xc,
-                       shg, act, I, partial, counters);
-    // the activation is [rows, 2I] bf16 hi/lo pairs
-    WRowsPairedK wdn{wd, d, I};
-    XRowsPlain xa{act, 2l * I};
-    const GemmShape shd = pd.shape(rows, 2 * I);
-    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shd.G), dim3(64 * NW), 0, st, wdn, xa,
-                       shd, hp, h, d, rt, partial, counters + pg.counter_ints());
+    constexpr int S = TF_NW_SINGLE;
+    constexpr int PS = NT == 4 ? TF_PIPE_SINGLE_NT4 : TF_PIPE_DEFAULT;
+    if (pg.NW != S)
+        launch_gateup<WM, NT, TF_NW, TF_PIPE_DEFAULT, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial,
+                                                             counters, st);
+    else if (pg.wnt)
+        launch_gateup<WM, NT, S, PS, true>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial, counters, st);
+    else
+        launch_gateup<WM, NT, S, TF_PIPE_DEFAULT, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial,
+                                                         counters, st);
+    int* cd = counters + pg.counter_ints();
+    if (pd.NW != S)
+        launch_down<WM, NT, TF_NW, TF_PIPE_DEFAULT, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
+    else if (pd.wnt)
+        launch_down<WM, NT, S, PS, true>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
+    else
+        launch_down<WM, NT, S, TF_PIPE_DEFAULT, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
 }
 
 static bool aligned16p(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -312,28 +344,15 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
         const uint16_t* etb = static_cast<const uint16_t*>(et);
         uint16_t* actb = static_cast<uint16_t*>(act);
         uint16_t* hpb = static_cast<uint16_t*>(hp);
-        // both products of one call share the row blocking (same rows, so the
-        // same waves per workgroup)
-        constexpr bool kWnt = TF_MLP_WNT != 0;
         if (pg.NT == 1)
-            launch_mlp_bf16<2, 1, TF_NW_SINGLE, TF_PIPE_DEFAULT, kWnt>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
-                                                                        ew, I, rt, pg, pd, mlp_partial, counters,
-                                                                        stream);
+            launch_mlp_bf16<2, 1>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg, pd, mlp_partial,
+                                  counters, stream);
         else if (pg.NT == 2)
-            launch_mlp_bf16<1, 2, TF_NW_SINGLE, TF_PIPE_DEFAULT, kWnt>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
-                                                                        ew, I, rt, pg, pd, mlp_partial, counters,
-                                                                        stream);
-        else if (pg.nrb == 1 && pg.wnt)
-            launch_mlp_bf16<1, 4, TF_NW_SINGLE, TF_PIPE_SINGLE_NT4, true>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
-                                                                           ew, I, rt, pg, pd, mlp_partial, counters,
-                                                                           stream);
-        else if (pg.nrb == 1)
-            launch_mlp_bf16<1, 4, TF_NW_SINGLE, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d,
-                                                                         ew, I, rt, pg, pd, mlp_partial, counters,
-                                                                         stream);
+            launch_mlp_bf16<1, 2>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg, pd, mlp_partial,
+                                  counters, stream);
         else
-            launch_mlp_bf16<1, 4, TF_NW, TF_PIPE_DEFAULT, false>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I,
-                                                                  rt, pg, pd, mlp_partial, counters, stream);
+            launch_mlp_bf16<1, 4>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg, pd, mlp_partial,
+                                  counters, stream);
     } else {
         launch_norms<float>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
                             counters, 0, stream);
@@ -370,7 +389,7 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
         else if (pl.NT == 2)
             hipLaunchKernelGGL((linear_bf16_kernel<1, 2, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
                                stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
-        else if (pl.nrb == 1)
+        else if (pl.NW == S)
             hipLaunchKernelGGL((linear_bf16_kernel<1, 4, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
                                stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
         else

@@ -87,22 +87,26 @@ inline int plan_nt(int rows) { return rows <= 32 ? 1 : (rows <= 64 ? 2 : 4); }
 inline int plan_wm(int NT) { return NT == 1 ? 2 : 1; }
 
 // bf16 product of `rows` activation rows with `ntiles` weight tiles over K.
-// One row block: the units are cut evenly over `wg_single` workgroups.
-// Several row blocks: one item per workgroup, the row blocks of a chunk on
-// consecutive workgroups so that they share the chunk through L2.
+// Enough (chunk, row block) items of eight-wave workgroups to give every CU
+// one: one item per workgroup, the row blocks of a chunk on consecutive
+// workgroups so that they share the chunk through L2.  Fewer (one row block,
+// or a few): four-wave workgroups, the units cut evenly over `wg_single`
+// workgroups.
 inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
     GemmPlan p;
     p.NT = plan_nt(rows);
     p.WM = plan_wm(p.NT);
     p.nrb = cdiv(rows, 32 * p.NT);
-    p.NW = p.nrb == 1 ? TF_NW_SINGLE : TF_NW;
+    const bool whole = p.nrb > 1 && (long long)cdiv(ntiles, TF_NW * p.WM) * p.nrb >= kNumCUs;
+    p.NW = whole ? TF_NW : TF_NW_SINGLE;
     p.chunk = p.NW * p.WM;
     p.ntiles = ntiles;
     p.nchunks = cdiv(ntiles, p.chunk);
     p.nk = cdiv(K, 64);
-    if (p.nrb == 1) {
-        const long long units = (long long)p.nchunks * p.nk;
+    if (!whole) {
+        const long long units = (long long)p.items() * p.nk;
         p.G = (int)(units < wg_single ? units : wg_single);
+        if (p.G < p.items()) p.G = p.items();
     } else {
         p.G = p.items();
     }
