@@ -468,17 +468,27 @@ struct EpiLmHead {
     static constexpr int MERGE_BYTES = 32 * NT * RSTRIDE * 4;
 
     // One row (accumulator column nt) of this lane; tokens past the
-    // vocabulary count as -inf.
+    // vocabulary count as -inf (`inside`, uniform per wave: none of this
+    // wave's tokens is).  The exponentials use the hardware exp2, whose
+    // results below 2^-126 flush to zero: the sum starts at the row
+    // maximum's term, 1.
     __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NT], int nt, const int (&vbase)[WM],
-                                             float* c) const {
+                                             bool inside, float* c) const {
         float x[WM][16];
+        if (inside) {
 #pragma unroll
-        for (int mt = 0; mt < WM; ++mt)
+            for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
-                x[mt][j] = v < V ? acc[mt][nt][j] : neg_inf();
-            }
+                for (int j = 0; j < 16; ++j) x[mt][j] = acc[mt][nt][j];
+        } else {
+#pragma unroll
+            for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
+                    x[mt][j] = v < V ? acc[mt][nt][j] : neg_inf();
+                }
+        }
         float m = neg_inf();
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
@@ -502,7 +512,7 @@ struct EpiLmHead {
             for (int j = 0; j < 16; ++j) {
                 const float xv = x[mt][j];
                 const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
-                s += exp2f(fmaf(xv, sl2, -ms));
+                s += __builtin_amdgcn_exp2f(fmaf(xv, sl2, -ms));
                 rest = fmaxf(rest, xv > lv[KL - 1] ? lv[KL - 1] : xv);
                 bool ins = false;
                 float cv = xv;
@@ -539,9 +549,11 @@ struct EpiLmHead {
         int vbase[WM];
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt) vbase[mt] = (tw + mt < it.t1 ? tw + mt : 0x3fffffff / 32) * 32 + 4 * (lane >> 5);
+        // every token of this wave's tiles lies in the slice and the vocabulary
+        const bool inside = tw + WM <= it.t1 && (tw + WM) * 32 <= V;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
-            lane_row(acc, nt, vbase, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
+            lane_row(acc, nt, vbase, inside, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
         __syncthreads();
         lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
