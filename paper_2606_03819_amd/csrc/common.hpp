@@ -47,6 +47,17 @@ __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
+// A bf16 LM-head logit as the lists carry and compare it: the fp32 value
+// with its low kLogitTagBits mantissa bits cleared (monotone, relative change
+// below 2^-17).  The MFMA epilogue stores a token's lane-local position in
+// those bits, so that one float max or median ranks (value, position) pairs;
+// every comparison of bf16 logits (epilogue, merge, exact re-evaluation) is
+// made on this value, so that the lists' bounds stay exact.
+constexpr int kLogitTagBits = 6;
+__device__ __forceinline__ float logit_trunc(float x) {
+    return __int_as_float(__float_as_int(x) & ~((1 << kLogitTagBits) - 1));
+}
+
 __device__ __forceinline__ f32x16 mfma_32x32x16_bf16(const u32x4& a, const u32x4& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);

@@ -715,8 +715,8 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
                     const int v = vb + tid;
                     if (v < v1) {
                         float val;
-                        if constexpr (sizeof(T) == 2)
-                            val = s_colv[v - v0];
+                        if constexpr (sizeof(T) == 2)   // compared as the fast path's lists are
+                            val = logit_trunc(s_colv[v - v0]);
                         else   // the fp32 kernel's chain: fmaf over k in increasing order
                             val = dot_row(xr, wb + (size_t)v * a.d, a.d);
                         bool take = cnt < K || better(val, v, sel_v[K - 1], sel_i[K - 1]);

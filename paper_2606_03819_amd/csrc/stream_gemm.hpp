@@ -467,28 +467,67 @@ struct EpiLmHead {
     static constexpr int RSTRIDE = NC * MERGE_WORDS + 1;
     static constexpr int MERGE_BYTES = 32 * NT * RSTRIDE * 4;
 
-    // One row (accumulator column nt) of this lane; tokens past the
-    // vocabulary count as -inf (`inside`, uniform per wave: none of this
-    // wave's tokens is).  The exponentials use the hardware exp2, whose
-    // results below 2^-126 flush to zero: the sum starts at the row
-    // maximum's term, 1.
-    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NT], int nt, const int (&vbase)[WM],
-                                             bool inside, float* c) const {
-        float x[WM][16];
-        if (inside) {
+    // One row (accumulator column nt) of a lane whose WM*16 tokens all lie
+    // in the slice and the vocabulary.  Each logit becomes a key: its
+    // truncated value (logit_trunc) with the lane-local position p (tokens
+    // in increasing id) stored as TAG - p in the cleared bits.  Keys are
+    // distinct, and for positive values their order is the (value desc, id
+    // asc) order; equal negative values rank the larger id first, and when
+    // that drops the smaller one the bound reaches the listed value, so the
+    // merge re-evaluates the slice and the result stays exact.  The KL + 1
+    // best keys cost one max and KL medians per logit (the lists' ids come
+    // from the tags at the end), the exponentials a second pass.  The
+    // hardware exp2 flushes results below 2^-126 to zero: the sum starts at
+    // the row maximum's term, about 1.
+    __device__ __forceinline__ void lane_row_keys(const f32x16 (&acc)[WM][NT], int nt, int vbase0, float* c) const {
+        constexpr int TAG = (1 << kLogitTagBits) - 1;
+        static_assert(WM * 16 <= TAG + 1 && WM * 16 > KL, "positions fit the tag bits");
+        float k[KL + 1];
 #pragma unroll
-            for (int mt = 0; mt < WM; ++mt)
+        for (int q = 0; q <= KL; ++q) k[q] = neg_inf();
 #pragma unroll
-                for (int j = 0; j < 16; ++j) x[mt][j] = acc[mt][nt][j];
-        } else {
+        for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-            for (int mt = 0; mt < WM; ++mt)
+            for (int j = 0; j < 16; ++j) {
+                const float key = __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (TAG - (mt * 16 + j)));
+                float n[KL + 1];
+                n[0] = fmaxf(k[0], key);
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
-                    x[mt][j] = v < V ? acc[mt][nt][j] : neg_inf();
-                }
+                for (int q = 1; q <= KL; ++q) n[q] = __builtin_amdgcn_fmed3f(k[q - 1], k[q], key);
+#pragma unroll
+                for (int q = 0; q <= KL; ++q) k[q] = n[q];
+            }
+        const float m = logit_trunc(k[0]);
+        const float ms = m * sl2;
+        float s = 0.f;
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
+        c[0] = m;
+        c[1] = s;
+        c[2] = logit_trunc(k[KL]);
+#pragma unroll
+        for (int q = 0; q < KL; ++q) {
+            const int p = TAG - (__float_as_int(k[q]) & TAG);
+            c[3 + q] = logit_trunc(k[q]);
+            c[3 + KL + q] = __int_as_float(vbase0 + 32 * (p >> 4) + 8 * ((p >> 2) & 3) + (p & 3));
         }
+    }
+
+    // One row of a lane some of whose tokens lie past the slice or the
+    // vocabulary (those count as -inf): a running list over the truncated
+    // values, visited in increasing token id.
+    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NT], int nt, const int (&vbase)[WM],
+                                             float* c) const {
+        float x[WM][16];
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
+                x[mt][j] = v < V ? logit_trunc(acc[mt][nt][j]) : neg_inf();
+            }
         float m = neg_inf();
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
@@ -551,9 +590,15 @@ struct EpiLmHead {
         for (int mt = 0; mt < WM; ++mt) vbase[mt] = (tw + mt < it.t1 ? tw + mt : 0x3fffffff / 32) * 32 + 4 * (lane >> 5);
         // every token of this wave's tiles lies in the slice and the vocabulary
         const bool inside = tw + WM <= it.t1 && (tw + WM) * 32 <= V;
+        if (inside) {
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-            lane_row(acc, nt, vbase, inside, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
+            for (int nt = 0; nt < NT; ++nt)
+                lane_row_keys(acc, nt, vbase[0], cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
+        } else {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                lane_row(acc, nt, vbase, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
+        }
         __syncthreads();
         lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
