@@ -49,11 +49,11 @@ __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
 // A bf16 LM-head logit as the lists carry and compare it: the fp32 value
 // with its low kLogitTagBits mantissa bits cleared (monotone, relative change
-// below 2^-17).  The MFMA epilogue stores a token's lane-local position in
+// below 2^-16).  The MFMA epilogue stores a token's lane-local position in
 // those bits, so that one float max or median ranks (value, position) pairs;
 // every comparison of bf16 logits (epilogue, merge, exact re-evaluation) is
 // made on this value, so that the lists' bounds stay exact.
-constexpr int kLogitTagBits = 6;
+constexpr int kLogitTagBits = 7;
 __device__ __forceinline__ float logit_trunc(float x) {
     return __int_as_float(__float_as_int(x) & ~((1 << kLogitTagBits) - 1));
 }

@@ -16,9 +16,13 @@ constexpr int kPartStrideLong = 4 + 2 * kKeepLong;
 constexpr int kLongListK = 64;
 constexpr int part_stride(int keep) { return 4 + 2 * keep; }
 // Per-thread running list lengths inside the LM-head epilogues (SIMT fp32
-// kernel, MFMA bf16 kernel).
+// kernel, MFMA bf16 kernel; "wide": a lane holds more than 64 logits of a
+// row, so it more often holds several of the row's best and needs a longer
+// list for the same rate of overflowing lanes).
 constexpr int kLane = 4;
 constexpr int kLaneMfma = 2;
 constexpr int kLaneMfmaLong = 3;
+constexpr int kLaneMfmaWide = 3;
+constexpr int kLaneMfmaWideLong = 5;
 
 }  // namespace tf

@@ -86,19 +86,23 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 constexpr int kCpolNt = 2;
 typedef __attribute__((address_space(1))) void global_void_t;
 
-template <int WM, int NT, int NW, int KC, int S>
+template <int WM, int NT, int NW, int KC, int S, int WB = 1>
 struct DmaTraits {
+    static constexpr int WA = NW / WB;                        // waves along the weight tiles
+    static constexpr int NTW = NT / WB;                       // activation tiles per wave
     static constexpr int ROWB = KC * 2;                       // bytes of one tile row in one stage
     static constexpr int SLOTS = KC / 8;                      // 16-byte slots per row
     static constexpr int RPI = 1024 / ROWB;                   // rows per DMA instruction
     static constexpr int WTILE = 32 * ROWB;                   // one weight tile of one stage
     static constexpr int WINSTR = 32 / RPI;                   // DMA instructions per weight tile
-    static constexpr int WSTAGE = NW * WM * WTILE;            // all waves' weight tiles of one stage
+    static constexpr int WSTAGE = WA * WM * WTILE;            // all waves' weight tiles of one stage
     static constexpr int XSTAGE = 32 * NT * ROWB;             // the activation tile of one stage
     static constexpr int XINSTR = XSTAGE / 1024;              // its DMA instructions, spread over the waves
     static constexpr int XOFF = S * WSTAGE;                   // activation ring after the weight ring
     static constexpr int RING = S * WSTAGE + 2 * XSTAGE;
-    static constexpr int WPS = WINSTR * WM;                   // weight DMA instructions per wave per step
+    static constexpr int WPI = WINSTR / WB;                   // DMA instructions of a shared tile per wave
+    static constexpr int WPS = WPI * WM;                      // weight DMA instructions per wave per step
+    static_assert(NW % WB == 0 && NT % WB == 0 && WINSTR % WB == 0, "wave grid");
     static_assert(KC == 32 || KC == 64, "k step");
     // S >= 3: weight step j is issued at step j - S + 1 <= j - 2, before the
     // activation step j (issued at step j - 1), so waiting for the latter retires it
@@ -122,18 +126,22 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int WM, int NT, int NW, int KC, int S, bool WNT, int MINB, bool LONG>
+template <int WM, int NT, int NW, int KC, int S, bool WNT, int MINB, bool LONG, int WB>
 __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,
                                                                 const uint16_t* __restrict__ w, GemmShape sh,
                                                                 SliceMap map, int V, float sl2,
                                                                 float* __restrict__ part, int* __restrict__ diag) {
-    using T = DmaTraits<WM, NT, NW, KC, S>;
-    using E = EpiLmHead<WM, NT, NW, LONG>;
+    using T = DmaTraits<WM, NT, NW, KC, S, WB>;
+    using E = EpiLmHead<WM, NT, NW, LONG, WB>;
+    constexpr int NTW = T::NTW;
     static_assert(E::MERGE_BYTES <= T::RING, "the epilogue reuses the rings");
     extern __shared__ __align__(16) unsigned char dyn[];
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // wave grid: WA waves along the weight tiles times WB along the activation
+    // tiles; the WB waves of one weight column share its tiles' copies
+    const int wa = wave % T::WA, wb = wave / T::WA;
     E epi{part, V, sl2};
     const int L = xcd_logical_id(blockIdx.x, gridDim.x);
     const int rb = L % sh.nrb;
@@ -175,16 +183,16 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
         // anyway: a per-tile branch in the k loop costs more in MFMA-bound
         // launches, whose slices are all full, than the spare products cost
         // in the memory-bound ones.)
-        const int tw = seg.t0 + wave * WM;
-        const uint16_t* wsrc[WM][T::WINSTR];
+        const int tw = seg.t0 + wa * WM;
+        const uint16_t* wsrc[WM][T::WPI];
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-            for (int hb = 0; hb < T::WINSTR; ++hb) {
-                const int row = T::RPI * hb + lrow;
+            for (int hi = 0; hi < T::WPI; ++hi) {
+                const int row = T::RPI * (wb * T::WPI + hi) + lrow;
                 const int tile = min(tw + mt, seg.t1 - 1);
                 const int v = min(tile * 32 + row, V - 1);
-                wsrc[mt][hb] = w + (size_t)v * sh.K + (T::slot(row, lphys) - row * T::ROWB) / 2;
+                wsrc[mt][hi] = w + (size_t)v * sh.K + (T::slot(row, lphys) - row * T::ROWB) / 2;
             }
         constexpr int XPW = (T::XINSTR + NW - 1) / NW;   // activation instructions of this wave (at most)
         const uint16_t* xsrc[XPW];
@@ -201,10 +209,11 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
 #pragma unroll
             for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-                for (int hb = 0; hb < T::WINSTR; ++hb)
-                    __builtin_amdgcn_global_load_lds((global_void_t*)(wsrc[mt][hb] + k0),
-                                                     (lds_void_t*)(st + (wave * WM + mt) * T::WTILE + hb * 1024), 16,
-                                                     0, WNT ? kCpolNt : 0);
+                for (int hi = 0; hi < T::WPI; ++hi)
+                    __builtin_amdgcn_global_load_lds(
+                        (global_void_t*)(wsrc[mt][hi] + k0),
+                        (lds_void_t*)(st + (wa * WM + mt) * T::WTILE + (wb * T::WPI + hi) * 1024), 16, 0,
+                        WNT ? kCpolNt : 0);
         };
         auto issue_x = [&](int step) {
             unsigned char* st = dyn + T::XOFF + (step & 1) * T::XSTAGE;
@@ -215,11 +224,11 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
                     __builtin_amdgcn_global_load_lds((global_void_t*)(xsrc[i] + k0),
                                                      (lds_void_t*)(st + (wave + NW * i) * 1024), 16, 0, 0);
         };
-        f32x16 acc[WM][NT];
+        f32x16 acc[WM][NTW];
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
+            for (int nt = 0; nt < NTW; ++nt)
 #pragma unroll
                 for (int j = 0; j < 16; ++j) acc[mt][nt][j] = 0.f;
 
@@ -241,22 +250,22 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
             // the stages read in step j - 1 are free now
             if (j + 1 < nsteps) issue_x(j + 1);
             if (j + S - 1 < nsteps) issue_w(j + S - 1);
-            const unsigned char* wt = dyn + (j % S) * T::WSTAGE + wave * WM * T::WTILE;
-            const unsigned char* xt = dyn + T::XOFF + (j & 1) * T::XSTAGE;
+            const unsigned char* wt = dyn + (j % S) * T::WSTAGE + wa * WM * T::WTILE;
+            const unsigned char* xt = dyn + T::XOFF + (j & 1) * T::XSTAGE + wb * NTW * 32 * T::ROWB;
 #pragma unroll
             for (int ks = 0; ks < KC / 16; ++ks) {
                 const int ls = 2 * ks + (lane >> 5);
-                u32x4 afr[WM], bfr[NT];
+                u32x4 afr[WM], bfr[NTW];
 #pragma unroll
                 for (int mt = 0; mt < WM; ++mt)
                     afr[mt] = *reinterpret_cast<const u32x4*>(wt + mt * T::WTILE + T::slot(lane & 31, ls));
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
+                for (int nt = 0; nt < NTW; ++nt)
                     bfr[nt] = *reinterpret_cast<const u32x4*>(xt + T::slot(nt * 32 + (lane & 31), ls));
 #pragma unroll
                 for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_32x32x16_bf16(afr[mt], bfr[nt], acc[mt][nt]);
+                    for (int nt = 0; nt < NTW; ++nt) acc[mt][nt] = mfma_32x32x16_bf16(afr[mt], bfr[nt], acc[mt][nt]);
             }
         }
         __syncthreads();  // ring reads done before the epilogue reuses the LDS
@@ -782,12 +791,12 @@ static void launch_lm_bf16(const uint16_t* x, long ldx, const uint16_t* w, const
                        w, sh, map, V, sl2, part, diag);
 }
 
-template <bool LONG, int WM, int NT, int NW, int KC, bool WNT, int MINB = 1>
+template <bool LONG, int WM, int NT, int NW, int KC, bool WNT, int MINB = 1, int WB = 1>
 static hipError_t launch_lm_dma(const uint16_t* x, long ldx, const uint16_t* w, const GemmShape& sh,
                                 const SliceMap& map, int blocks, int V, float sl2, float* part, int* diag,
                                 hipStream_t st) {
-    using T = DmaTraits<WM, NT, NW, KC, TF_LM_DMA_STAGES>;
-    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT, MINB, LONG>;
+    using T = DmaTraits<WM, NT, NW, KC, TF_LM_DMA_STAGES, WB>;
+    auto kern = lmhead_dma_kernel<WM, NT, NW, KC, TF_LM_DMA_STAGES, WNT, MINB, LONG, WB>;
     // dynamic LDS beyond the 64 KiB default
     const hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::RING);
@@ -808,8 +817,8 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
                                                                                             V, sl2, part, diag, st);
 #endif
         if (p.wnt)   // a single row block
-            return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb, V,
-                                                                                           sl2, part, diag, st);
+            return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true, 1, TF_LM_DMA_SINGLE_WB>(
+                x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
         return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false,
                              TF_LM_DMA_MULTI_MINB>(
             x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);

@@ -123,6 +123,7 @@ inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
 // and at most 8 tiles (256 tokens) per workgroup.
 struct LmPlan {
     int NT, WM, NW, chunk, nrb, ntiles, nk;
+    int WB = 1;   // waves along the activation tiles (a grid of NW / WB x WB waves)
     SliceMap map;
     bool wnt;
     bool dma;   // the LDS-DMA kernel (TF_LM_DMA_NW waves of TF_LM_DMA_WM tiles, k in steps of 32)
@@ -151,16 +152,22 @@ struct LmPlan {
 #ifndef TF_LM_WM_NT4
 #define TF_LM_WM_NT4 1
 #endif
+// A single row block: four waves, one per SIMD, in a 2 x 2 grid (two along
+// the weight tiles, two along the activation tiles), each with 5 weight
+// tiles x 2 activation tiles: ten tiles per round, so the 256 ranges of the
+// Qwen vocabularies take two rounds, and every SIMD issues the same MFMAs
+// and fragment reads (five waves of 2 x 4 tiles left one SIMD with two
+// waves' work, which set the pace of every k step).
 #ifndef TF_LM_DMA_WM
-#define TF_LM_DMA_WM 2
+#define TF_LM_DMA_WM 5
 #endif
-// waves of the DMA kernel: five for a single row block (ten tiles per round,
-// so the 256 ranges of the Qwen vocabularies take two rounds instead of three;
-// memory-bound, the fifth wave's SIMD does twice the MFMA work unnoticed),
-// four for several row blocks (MFMA-bound: one wave per SIMD)
 #ifndef TF_LM_DMA_NW_SINGLE
-#define TF_LM_DMA_NW_SINGLE 5
+#define TF_LM_DMA_NW_SINGLE 4
 #endif
+#ifndef TF_LM_DMA_SINGLE_WB
+#define TF_LM_DMA_SINGLE_WB 2
+#endif
+// waves of the DMA kernel for several row blocks (MFMA-bound: one wave per SIMD)
 #ifndef TF_LM_DMA_NW
 #define TF_LM_DMA_NW 4
 #endif
@@ -217,6 +224,7 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
         } else if (p.dma && p.nrb == 1) {
             p.WM = TF_LM_DMA_WM;
             p.NW = TF_LM_DMA_NW_SINGLE;
+            p.WB = TF_LM_DMA_SINGLE_WB;
         } else if (p.dma) {
             p.WM = TF_LM_DMA_MULTI_WM;
             p.NW = TF_LM_DMA_NW;
@@ -224,7 +232,7 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
             p.WM = lm_wm(p.NT);
             p.NW = lm_nw(p.NT);
         }
-        p.chunk = p.NW * p.WM;
+        p.chunk = p.NW / p.WB * p.WM;
         const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)
                                  : cdiv(p.ntiles, p.chunk);
         p.map = make_slice_map(p.ntiles, G, p.chunk);

@@ -444,7 +444,10 @@ __device__ inline void lm_merge_contributors(const float* cm, int rstride, int r
 // best logits with their token ids and a bound on the rest (the largest logit
 // the lane drops); merged per workgroup into a (row, slice) partial of KEEP
 // entries, the slice being the workgroup's chunk of the vocabulary (LONG:
-// the long lists for large top-k).
+// the long lists for large top-k).  WB > 1: the waves form a grid of
+// NW / WB waves along the weight tiles times WB along the activation tiles,
+// each wave holding NT / WB activation tiles, so a row has 2 * NW / WB
+// contributor lists.
 //
 // The partial's `bound` is an upper bound on every logit of the slice that is
 // not in its list: a lane drops only values no larger than its bound, and the
@@ -454,23 +457,27 @@ __device__ inline void lm_merge_contributors(const float* cm, int rstride, int r
 // keep this pass cheap (it runs on the vector ALUs after every item); a
 // slice is re-evaluated only if one lane holds KL + 1 of the row's best k
 // logits or the slice KEEP + 1 of them.
-template <int WM, int NT, int NW, bool LONG = false>
+template <int WM, int NT, int NW, bool LONG = false, int WB = 1>
 struct EpiLmHead {
+    static constexpr int WA = NW / WB;            // waves along the weight tiles
+    static constexpr int NTW = NT / WB;           // activation tiles per wave
     float* part;     // [R, nchunks, part_stride(KEEP)]
     int V;
     float sl2;       // inv_temperature * log2(e)
-    static constexpr int KL = LONG ? kLaneMfmaLong : kLaneMfma;
+    static constexpr bool WIDE = WM * 16 > 64;
+    static constexpr int KL = LONG ? (WIDE ? kLaneMfmaWideLong : kLaneMfmaLong) : (WIDE ? kLaneMfmaWide : kLaneMfma);
     static constexpr int KEEP = LONG ? kKeepLong : kKeep;
-    static constexpr int NC = 2 * NW;             // contributor lists per row
+    static constexpr int NC = 2 * WA;             // contributor lists per row
     static constexpr int MERGE_WORDS = 3 + 2 * KL;
     // odd row stride: the lanes of a wave (consecutive rows) hit distinct banks
     static constexpr int RSTRIDE = NC * MERGE_WORDS + 1;
     static constexpr int MERGE_BYTES = 32 * NT * RSTRIDE * 4;
 
-    // One row (accumulator column nt) of a lane whose WM*16 tokens all lie
-    // in the slice and the vocabulary.  Each logit becomes a key: its
-    // truncated value (logit_trunc) with the lane-local position p (tokens
-    // in increasing id) stored as TAG - p in the cleared bits.  Keys are
+    // One row (accumulator column nt) of this lane: the tiles [tw, tw + WM)
+    // of which those before t1 lie in the slice (a wave-uniform test) and
+    // tokens from V on are left out.  Each logit becomes a key: its truncated
+    // value (logit_trunc) with the lane-local position p (tokens in
+    // increasing id) stored as TAG - p in the cleared bits.  Keys are
     // distinct, and for positive values their order is the (value desc, id
     // asc) order; equal negative values rank the larger id first, and when
     // that drops the smaller one the bound reaches the listed value, so the
@@ -479,126 +486,81 @@ struct EpiLmHead {
     // from the tags at the end), the exponentials a second pass.  The
     // hardware exp2 flushes results below 2^-126 to zero: the sum starts at
     // the row maximum's term, about 1.
-    __device__ __forceinline__ void lane_row_keys(const f32x16 (&acc)[WM][NT], int nt, int vbase0, float* c) const {
+    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NTW], int nt, int vbase0, int tw, int t1,
+                                             float* c) const {
         constexpr int TAG = (1 << kLogitTagBits) - 1;
-        static_assert(WM * 16 <= TAG + 1 && WM * 16 > KL, "positions fit the tag bits");
+        static_assert(WM * 16 <= TAG + 1 && 16 > KL, "positions fit the tag bits; one tile fills a list");
         float k[KL + 1];
 #pragma unroll
         for (int q = 0; q <= KL; ++q) k[q] = neg_inf();
+        auto insert = [&](float key) {
+            float n[KL + 1];
+            n[0] = fmaxf(k[0], key);
 #pragma unroll
-        for (int mt = 0; mt < WM; ++mt)
+            for (int q = 1; q <= KL; ++q) n[q] = __builtin_amdgcn_fmed3f(k[q - 1], k[q], key);
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const float key = __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (TAG - (mt * 16 + j)));
-                float n[KL + 1];
-                n[0] = fmaxf(k[0], key);
+            for (int q = 0; q <= KL; ++q) k[q] = n[q];
+        };
+        auto key_of = [&](int mt, int j) {
+            return __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (TAG - (mt * 16 + j)));
+        };
+        // wave-uniform branches: a tile past the slice is skipped, only a tile
+        // reaching past the vocabulary pays for the per-token test
 #pragma unroll
-                for (int q = 1; q <= KL; ++q) n[q] = __builtin_amdgcn_fmed3f(k[q - 1], k[q], key);
+        for (int mt = 0; mt < WM; ++mt) {
+            if (tw + mt >= t1) continue;
+            if ((tw + mt + 1) * 32 <= V) {
 #pragma unroll
-                for (int q = 0; q <= KL; ++q) k[q] = n[q];
+                for (int j = 0; j < 16; ++j) insert(key_of(mt, j));
+            } else {
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    insert(vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V ? key_of(mt, j) : neg_inf());
             }
+        }
         const float m = logit_trunc(k[0]);
-        const float ms = m * sl2;
         float s = 0.f;
+        if (m != neg_inf()) {
+            const float ms = m * sl2;
 #pragma unroll
-        for (int mt = 0; mt < WM; ++mt)
+            for (int mt = 0; mt < WM; ++mt) {
+                if (tw + mt >= t1) continue;
+                if ((tw + mt + 1) * 32 <= V) {
 #pragma unroll
-            for (int j = 0; j < 16; ++j) s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
+                    for (int j = 0; j < 16; ++j) s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 16; ++j)
+                        if (vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V)
+                            s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
+                }
+            }
+        }
         c[0] = m;
         c[1] = s;
         c[2] = logit_trunc(k[KL]);
 #pragma unroll
         for (int q = 0; q < KL; ++q) {
+            const bool ok = k[q] != neg_inf();
             const int p = TAG - (__float_as_int(k[q]) & TAG);
-            c[3 + q] = logit_trunc(k[q]);
-            c[3 + KL + q] = __int_as_float(vbase0 + 32 * (p >> 4) + 8 * ((p >> 2) & 3) + (p & 3));
+            c[3 + q] = ok ? logit_trunc(k[q]) : neg_inf();
+            c[3 + KL + q] = __int_as_float(ok ? vbase0 + 32 * (p >> 4) + 8 * ((p >> 2) & 3) + (p & 3) : -1);
         }
     }
 
-    // One row of a lane some of whose tokens lie past the slice or the
-    // vocabulary (those count as -inf): a running list over the truncated
-    // values, visited in increasing token id.
-    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NT], int nt, const int (&vbase)[WM],
-                                             float* c) const {
-        float x[WM][16];
-#pragma unroll
-        for (int mt = 0; mt < WM; ++mt)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
-                x[mt][j] = v < V ? logit_trunc(acc[mt][nt][j]) : neg_inf();
-            }
-        float m = neg_inf();
-#pragma unroll
-        for (int mt = 0; mt < WM; ++mt)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) m = fmaxf(m, x[mt][j]);
-        const float ms = m * sl2;
-        float s = 0.f;
-        float lv[KL], rest = neg_inf();
-        int li[KL];
-#pragma unroll
-        for (int q = 0; q < KL; ++q) {
-            lv[q] = neg_inf();
-            li[q] = -1;
-        }
-        // visited in increasing token id, so a tie keeps the smaller id first:
-        // a logit enters the list only past a strictly smaller one, and the
-        // entries below its place move down one
-#pragma unroll
-        for (int mt = 0; mt < WM; ++mt)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const float xv = x[mt][j];
-                const int v = vbase[mt] + 8 * (j >> 2) + (j & 3);
-                s += __builtin_amdgcn_exp2f(fmaf(xv, sl2, -ms));
-                rest = fmaxf(rest, xv > lv[KL - 1] ? lv[KL - 1] : xv);
-                bool ins = false;
-                float cv = xv;
-                int ci = v;
-#pragma unroll
-                for (int q = 0; q < KL; ++q) {
-                    const bool sw = ins || cv > lv[q];
-                    const float tv = sw ? lv[q] : cv;
-                    const int ti = sw ? li[q] : ci;
-                    lv[q] = sw ? cv : lv[q];
-                    li[q] = sw ? ci : li[q];
-                    cv = tv;
-                    ci = ti;
-                    ins = sw;
-                }
-            }
-        c[0] = m;
-        c[1] = m == neg_inf() ? 0.f : s;
-        c[2] = rest;
-#pragma unroll
-        for (int q = 0; q < KL; ++q) {
-            c[3 + q] = lv[q];
-            c[3 + KL + q] = __int_as_float(li[q]);
-        }
-    }
-
-    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char* smem,
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NTW], const Segment& it, unsigned char* smem,
                                           const GemmShape& sh) {
         const int lane = threadIdx.x & 63;
         const int wave = threadIdx.x >> 6;
+        const int wa = wave % WA, wb = wave / WA;
         float* cm = reinterpret_cast<float*>(smem);   // [32*NT rows, stride RSTRIDE][NC contributors][MERGE_WORDS]
-        const int q = wave * 2 + (lane >> 5);
-        const int tw = it.t0 + wave * WM;            // this wave's first tile
-        int vbase[WM];
+        const int q = wa * 2 + (lane >> 5);
+        // this lane's row of accumulator column 0
+        float* crow = cm + (wb * NTW * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS;
+        const int tw = it.t0 + wa * WM;              // this wave's first tile
+        const int vbase0 = tw * 32 + 4 * (lane >> 5);
 #pragma unroll
-        for (int mt = 0; mt < WM; ++mt) vbase[mt] = (tw + mt < it.t1 ? tw + mt : 0x3fffffff / 32) * 32 + 4 * (lane >> 5);
-        // every token of this wave's tiles lies in the slice and the vocabulary
-        const bool inside = tw + WM <= it.t1 && (tw + WM) * 32 <= V;
-        if (inside) {
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                lane_row_keys(acc, nt, vbase[0], cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
-        } else {
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                lane_row(acc, nt, vbase, cm + (nt * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS);
-        }
+        for (int nt = 0; nt < NTW; ++nt) lane_row(acc, nt, vbase0, tw, it.t1, crow + nt * 32 * RSTRIDE);
         __syncthreads();
         lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
