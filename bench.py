@@ -68,8 +68,8 @@ def lm_kernel_pattern(rows: int, d: int) -> str:
     128-row tiles go to the LDS-DMA kernel when d is a multiple of its k step
     (64 for one row block, 32 for several)."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
-    if nt == 4 and (d % 64 == 0 or (rows > 128 and d % 32 == 0)):
-        return r"lmhead_dma_kernel<\d+, 4, "
+    if nt >= 2 and (d % 64 == 0 or (rows > 128 and d % 32 == 0)):
+        return rf"lmhead_dma_kernel<\d+, {nt}, "
     return rf"lmhead_bf16_kernel<\d+, {nt}, "
 
 

@@ -104,9 +104,13 @@ struct DmaTraits {
     static constexpr int WPS = WPI * WM;                      // weight DMA instructions per wave per step
     static_assert(NW % WB == 0 && NT % WB == 0 && WINSTR % WB == 0, "wave grid");
     static_assert(KC == 32 || KC == 64, "k step");
-    // S >= 3: weight step j is issued at step j - S + 1 <= j - 2, before the
-    // activation step j (issued at step j - 1), so waiting for the latter retires it
-    static_assert(S >= 3 && WPS < 64, "ring depth, vmcnt range");
+    // activation DMA instructions every wave issues (a wave may issue one more)
+    static constexpr int XMIN = XINSTR / NW;
+    // Copies are issued in the order w(0) .. w(S-3), x(0), w(S-2), then per
+    // step j: x(j+1), w(j+S-1).  S >= 3 puts w(j) before x(j); after x(j)
+    // come w(j+S-2), x(j+1) and w(j+S-1): at most WAIT_J loads.
+    static constexpr int WAIT_J = 2 * WPS + XMIN;
+    static_assert(S >= 3 && WAIT_J < 64, "ring depth, vmcnt range");
     // byte offset of 16-byte logical slot `ls` of row `r`
     __device__ static __forceinline__ int slot(int r, int ls) {
         const int sw = KC == 32 ? ((r >> 2) & 3) : ((r >> 1) & 7);
@@ -232,24 +236,25 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
 #pragma unroll
                 for (int j = 0; j < 16; ++j) acc[mt][nt][j] = 0.f;
 
-        // prologue: the first S - 1 weight steps, then activation step 0
-        // (waiting for it then retires them all)
+        // prologue: weight steps 0 .. S-3, activation step 0, weight step S-2
 #pragma unroll
-        for (int p = 0; p < S - 1; ++p)
+        for (int p = 0; p < S - 2; ++p)
             if (p < nsteps) issue_w(p);
         issue_x(0);
+        if (S - 2 < nsteps) issue_w(S - 2);
         for (int j = 0; j < nsteps; ++j) {
-            // this wave's copies of step j have landed (issued in order, only
-            // weight step j + S - 2 may still be out); the other waves' too
+            // every wave is done with the stages of step j - 1: refill them
+            // before waiting for step j, so that up to S steps are in flight
+            block_barrier();
+            if (j + 1 < nsteps) issue_x(j + 1);
+            if (j + S - 1 < nsteps) issue_w(j + S - 1);
+            // this wave's copies of step j have landed; the other waves' too
             // after the barrier
-            if (j >= 1 && j + S - 2 < nsteps)
-                wait_vmcnt<T::WPS>();
+            if (j + S - 1 < nsteps)
+                wait_vmcnt<T::WAIT_J>();
             else
                 wait_vmcnt<0>();
             block_barrier();
-            // the stages read in step j - 1 are free now
-            if (j + 1 < nsteps) issue_x(j + 1);
-            if (j + S - 1 < nsteps) issue_w(j + S - 1);
             const unsigned char* wt = dyn + (j % S) * T::WSTAGE + wa * WM * T::WTILE;
             const unsigned char* xt = dyn + T::XOFF + (j & 1) * T::XSTAGE + wb * NTW * 32 * T::ROWB;
 #pragma unroll
@@ -816,6 +821,9 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
             return launch_lm_dma<LONG, TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb,
                                                                                             V, sl2, part, diag, st);
 #endif
+        if (p.NT == 2)   // 33..64 rows: one activation tile per wave of the grid
+            return launch_lm_dma<LONG, TF_LM_DMA_WM, 2, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true, 1, TF_LM_DMA_SINGLE_WB>(
+                x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
         if (p.wnt)   // a single row block
             return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true, 1, TF_LM_DMA_SINGLE_WB>(
                 x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);

@@ -214,10 +214,10 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     p.dma = false;
     if (bf16) {
         p.NT = plan_nt(rows);
-        // 128-row activation tiles with k in whole 32-wide steps: the DMA kernel
+        // 64- and 128-row activation tiles with k in whole steps: the DMA kernel
         p.nrb = cdiv(rows, 32 * p.NT);
         const int kc = p.NT == 4 && p.nrb > 1 ? TF_LM_DMA_MULTI_KC : TF_LM_DMA_KC;
-        p.dma = TF_LM_DMA && (p.NT == 4 || (TF_LM_DMA_NT1 && p.NT == 1)) && d % kc == 0;
+        p.dma = TF_LM_DMA && (p.NT >= 2 || (TF_LM_DMA_NT1 && p.NT == 1)) && d % kc == 0;
         if (p.dma && p.NT == 1) {
             p.WM = TF_LM_DMA_NT1_WM;
             p.NW = TF_LM_DMA_NT1_NW;
