@@ -510,6 +510,17 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
     return v;
 }
 
+// The best 64 of two descending wave lists, descending: the larger of a[l]
+// and b[63 - l] per lane form a bitonic sequence, and half-cleaners sort it.
+__device__ __forceinline__ float wave_merge_desc(float a, float b, int lane) {
+    float v = fmaxf(a, __shfl(b, 63 - lane));
+    for (int j = 32; j > 0; j >>= 1) {
+        const float o = __shfl_xor(v, j);
+        v = (lane & j) == 0 ? fmaxf(v, o) : fminf(v, o);
+    }
+    return v;
+}
+
 // (value, id) pairs of a wave sorted in the (value desc, id asc) order, lane
 // 0 first: a bitonic network over __shfl_xor (ids are distinct, so the
 // order is total; padding pairs are equal and stay put).
@@ -555,11 +566,13 @@ static_assert(kMaxSplitsLong * kKeepLong <= kMergeCap, "long-list slices fit the
 
 // One workgroup per row.
 //  1. log-sum-exp of the row from the slices' (max, sum) pairs;
-//  2. a lower bound t0 on the row's k-th best value: within a wave, sort the
-//     lanes' best slice heads; k distinct slices reach the k-th of them, so
-//     at least k candidates are >= it (k <= 64; otherwise t0 = -inf);
-//  3. every slice entry >= t0 goes to LDS, is bitonic-sorted, and the first k
-//     are the row's top-k among the candidates;
+//  2. a lower bound t0 on the row's k-th best value: the k-th best of the
+//     threads' heads (a thread's head is the best entry of its slices); k
+//     threads, so k distinct slices, reach it, so at least k candidates are
+//     >= it (k <= 64; otherwise t0 = -inf);
+//  3. every slice entry >= t0 goes to LDS and is sorted (in registers when
+//     k <= 64 and at most 256 entries qualify), and the first k are the
+//     row's top-k among the candidates;
 //  4. a slice whose bound (everything it dropped is <= bound) reaches the k-th
 //     value is re-evaluated exactly from memory, so the result is the exact
 //     top-k of the row for any data, ties included.
@@ -568,6 +581,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     constexpr int PS = part_stride(KEEP);
     __shared__ float red[4];
     __shared__ float s_bound[4];
+    __shared__ float s_heads[256];
     __shared__ int s_count, s_nflag, s_ncand;
     __shared__ float cand_v[kMergeCap];
     __shared__ int cand_i[kMergeCap];
@@ -610,16 +624,25 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     S = block_sum(S, red);
     const float logS = logf(S);
 
-    // lower bound on the k-th best value
+    // lower bound on the k-th best value: the k-th best of the 256 thread
+    // heads (each wave sorts its 64, wave 0 merges the four sorted lists)
     const float sorted = wave_sort_desc(head, lane);
-    const float wb = K <= 64 ? __shfl(sorted, K - 1) : neg_inf();
-    if (lane == 0) s_bound[wave] = wb;
+    s_heads[tid] = sorted;
     if (tid == 0) {
         s_count = 0;
         s_nflag = 0;
     }
     __syncthreads();
-    const float t0 = fmaxf(fmaxf(s_bound[0], s_bound[1]), fmaxf(s_bound[2], s_bound[3]));
+    if (wave == 0) {
+        float v = sorted;
+        v = wave_merge_desc(v, s_heads[64 + lane], lane);
+        const float v23 = wave_merge_desc(s_heads[128 + lane], s_heads[192 + lane], lane);
+        v = wave_merge_desc(v, v23, lane);
+        const float kth = __shfl(v, (K <= 64 ? K : 64) - 1);
+        if (lane == 0) s_bound[0] = K <= 64 ? kth : neg_inf();
+    }
+    __syncthreads();
+    const float t0 = s_bound[0];
 
 #pragma unroll
     for (int j = 0; j < SPT; ++j) {
