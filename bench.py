@@ -65,8 +65,8 @@ def kernel_source_digest() -> str:
 def lm_kernel_pattern(rows: int, d: int) -> str:
     """Regex for the bf16 LM-head kernel instance the plan picks for `rows` rows
     (template arguments: weight tiles per wave, activation tiles, waves, ...):
-    128-row tiles go to the LDS-DMA kernel when d is a multiple of its k step
-    (64 for one row block, 32 for several)."""
+    64- and 128-row tiles go to the LDS-DMA kernel when d is a multiple of its k
+    step (64 up to two row blocks, 32 beyond)."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
     if nt >= 2 and (d % 64 == 0 or (rows > 128 and d % 32 == 0)):
         return rf"lmhead_dma_kernel<\d+, {nt}, "

@@ -844,11 +844,14 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
             return launch_lm_dma<LONG, TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb,
                                                                                             V, sl2, part, diag, st);
 #endif
-        if (p.NT == 2)   // 33..64 rows: one activation tile per wave of the grid
+        if (p.grid && p.NT == 2)   // 33..64 rows: one activation tile per wave of the grid
             return launch_lm_dma<LONG, TF_LM_DMA_WM, 2, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true, 1, TF_LM_DMA_SINGLE_WB>(
                 x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
-        if (p.wnt)   // a single row block
+        if (p.grid && p.wnt)   // a single row block
             return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true, 1, TF_LM_DMA_SINGLE_WB>(
+                x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        if (p.grid)   // a few row blocks sharing each range's weights through L2
+            return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, false, 1, TF_LM_DMA_SINGLE_WB>(
                 x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
         return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false,
                              TF_LM_DMA_MULTI_MINB>(

@@ -124,6 +124,7 @@ inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
 struct LmPlan {
     int NT, WM, NW, chunk, nrb, ntiles, nk;
     int WB = 1;   // waves along the activation tiles (a grid of NW / WB x WB waves)
+    bool grid = false;   // the DMA kernel's 2 x 2 wave grid
     SliceMap map;
     bool wnt;
     bool dma;   // the LDS-DMA kernel (TF_LM_DMA_NW waves of TF_LM_DMA_WM tiles, k in steps of 32)
@@ -166,6 +167,13 @@ struct LmPlan {
 #endif
 #ifndef TF_LM_DMA_SINGLE_WB
 #define TF_LM_DMA_SINGLE_WB 2
+#endif
+// Row blocks up to which the grid shape serves the LM head: the row blocks
+// of a tile range run on consecutive workgroups (one XCD), so the second
+// reads the weights the first brought into L2 (plain loads, not
+// non-temporal).
+#ifndef TF_LM_GRID_NRB
+#define TF_LM_GRID_NRB 2
 #endif
 // waves of the DMA kernel for several row blocks (MFMA-bound: one wave per SIMD)
 #ifndef TF_LM_DMA_NW
@@ -214,14 +222,17 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     p.dma = false;
     if (bf16) {
         p.NT = plan_nt(rows);
-        // 64- and 128-row activation tiles with k in whole steps: the DMA kernel
+        // 64- and 128-row activation tiles with k in whole steps: the DMA
+        // kernel, as the 2 x 2 wave grid up to TF_LM_GRID_NRB row blocks
+        // (64-wide k steps), else with two workgroups per CU (32-wide)
         p.nrb = cdiv(rows, 32 * p.NT);
-        const int kc = p.NT == 4 && p.nrb > 1 ? TF_LM_DMA_MULTI_KC : TF_LM_DMA_KC;
-        p.dma = TF_LM_DMA && (p.NT >= 2 || (TF_LM_DMA_NT1 && p.NT == 1)) && d % kc == 0;
+        p.grid = TF_LM_DMA && p.NT >= 2 && p.nrb <= TF_LM_GRID_NRB && d % TF_LM_DMA_KC == 0;
+        const bool multi = TF_LM_DMA && p.NT == 4 && p.nrb > 1 && !p.grid && d % TF_LM_DMA_MULTI_KC == 0;
+        p.dma = p.grid || multi || (TF_LM_DMA && TF_LM_DMA_NT1 && p.NT == 1 && d % TF_LM_DMA_KC == 0);
         if (p.dma && p.NT == 1) {
             p.WM = TF_LM_DMA_NT1_WM;
             p.NW = TF_LM_DMA_NT1_NW;
-        } else if (p.dma && p.nrb == 1) {
+        } else if (p.grid) {
             p.WM = TF_LM_DMA_WM;
             p.NW = TF_LM_DMA_NW_SINGLE;
             p.WB = TF_LM_DMA_SINGLE_WB;
@@ -233,8 +244,10 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
             p.NW = lm_nw(p.NT);
         }
         p.chunk = p.NW / p.WB * p.WM;
-        const int G = p.nrb == 1 ? (p.ntiles < TF_LM_WORKGROUPS ? p.ntiles : TF_LM_WORKGROUPS)
-                                 : cdiv(p.ntiles, p.chunk);
+        // one row block, or the grid kernel: TF_LM_WORKGROUPS workgroups in
+        // all, the row blocks of a tile range on consecutive ones
+        const int gw = TF_LM_WORKGROUPS / p.nrb;
+        const int G = p.nrb == 1 || p.grid ? (p.ntiles < gw ? p.ntiles : gw) : cdiv(p.ntiles, p.chunk);
         p.map = make_slice_map(p.ntiles, G, p.chunk);
         p.wnt = p.nrb == 1;
     } else {
