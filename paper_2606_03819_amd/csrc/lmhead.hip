@@ -104,13 +104,10 @@ struct DmaTraits {
     static constexpr int WPS = WPI * WM;                      // weight DMA instructions per wave per step
     static_assert(NW % WB == 0 && NT % WB == 0 && WINSTR % WB == 0, "wave grid");
     static_assert(KC == 32 || KC == 64, "k step");
-    // activation DMA instructions every wave issues (a wave may issue one more)
-    static constexpr int XMIN = XINSTR / NW;
-    // Copies are issued in the order w(0) .. w(S-3), x(0), w(S-2), then per
-    // step j: x(j+1), w(j+S-1).  S >= 3 puts w(j) before x(j); after x(j)
-    // come w(j+S-2), x(j+1) and w(j+S-1): at most WAIT_J loads.
-    static constexpr int WAIT_J = 2 * WPS + XMIN;
-    static_assert(S >= 3 && WAIT_J < 64, "ring depth, vmcnt range");
+    // Copies are issued in the order w(0) .. w(S-3), x(0), w(S-2), then
+    // during step j: x(j+1), w(j+S-1).  S >= 3 puts w(j) before x(j), and
+    // after x(j) come only the WPS copies of w(j+S-2).
+    static_assert(S >= 3 && WPS < 64, "ring depth, vmcnt range");
     // byte offset of 16-byte logical slot `ls` of row `r`
     __device__ static __forceinline__ int slot(int r, int ls) {
         const int sw = KC == 32 ? ((r >> 2) & 3) : ((r >> 1) & 7);
@@ -219,6 +216,20 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
                         (lds_void_t*)(st + (wa * WM + mt) * T::WTILE + (wb * T::WPI + hi) * 1024), 16, 0,
                         WNT ? kCpolNt : 0);
         };
+        // the weight copies q = mt * WPI + hi of step `step` with q % (KC / 16) == part
+        auto issue_w_part = [&](int step, int part) {
+            unsigned char* st = dyn + (step % S) * T::WSTAGE;
+            const int k0 = step * KC;
+#pragma unroll
+            for (int mt = 0; mt < WM; ++mt)
+#pragma unroll
+                for (int hi = 0; hi < T::WPI; ++hi)
+                    if ((mt * T::WPI + hi) % (KC / 16) == part)
+                        __builtin_amdgcn_global_load_lds(
+                            (global_void_t*)(wsrc[mt][hi] + k0),
+                            (lds_void_t*)(st + (wa * WM + mt) * T::WTILE + (wb * T::WPI + hi) * 1024), 16, 0,
+                            WNT ? kCpolNt : 0);
+        };
         auto issue_x = [&](int step) {
             unsigned char* st = dyn + T::XOFF + (step & 1) * T::XSTAGE;
             const int k0 = step * KC;
@@ -243,15 +254,11 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
         issue_x(0);
         if (S - 2 < nsteps) issue_w(S - 2);
         for (int j = 0; j < nsteps; ++j) {
-            // every wave is done with the stages of step j - 1: refill them
-            // before waiting for step j, so that up to S steps are in flight
-            block_barrier();
-            if (j + 1 < nsteps) issue_x(j + 1);
-            if (j + S - 1 < nsteps) issue_w(j + S - 1);
-            // this wave's copies of step j have landed; the other waves' too
-            // after the barrier
-            if (j + S - 1 < nsteps)
-                wait_vmcnt<T::WAIT_J>();
+            // this wave's copies of step j have landed (only w(j+S-2) may
+            // still be out); the other waves' too after the barrier, which
+            // also frees the stages read in step j - 1
+            if (j + S - 2 < nsteps)
+                wait_vmcnt<T::WPS>();
             else
                 wait_vmcnt<0>();
             block_barrier();
@@ -261,6 +268,11 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
             for (int ks = 0; ks < KC / 16; ++ks) {
                 const int ls = 2 * ks + (lane >> 5);
                 u32x4 afr[WM], bfr[NTW];
+                // refill the freed stages between the MFMAs: the activation
+                // step first, the weight copies spread over the k sub-steps
+                // (issued in one burst they held the wave off its MFMAs)
+                if (ks == 0 && j + 1 < nsteps) issue_x(j + 1);
+                if (j + S - 1 < nsteps) issue_w_part(j + S - 1, ks);
 #pragma unroll
                 for (int mt = 0; mt < WM; ++mt)
                     afr[mt] = *reinterpret_cast<const u32x4*>(wt + mt * T::WTILE + T::slot(lane & 31, ls));
