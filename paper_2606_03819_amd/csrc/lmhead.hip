@@ -533,6 +533,63 @@ __device__ __forceinline__ float wave_merge_desc(float a, float b, int lane) {
     return v;
 }
 
+// Order-preserving unsigned image of a float: a larger float has a larger
+// image, and -0 shares +0's (they compare equal).
+__device__ __forceinline__ unsigned ord_bits(float v) {
+    const unsigned b = v == 0.f ? 0u : __float_as_uint(v);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// ord_bits of the K-th largest of vals[0, n) (1 <= K <= n), found by a radix
+// select over four 8-bit digits from the top: each pass counts, in LDS, the
+// values that match the digits found so far by their next digit, and wave 0
+// locates the digit holding the wanted rank.  Called by all 256 threads.
+__device__ unsigned kth_largest_ord(const float* vals, int n, int K, int* hist, int* sel) {
+    const int tid = threadIdx.x;
+    unsigned prefix = 0, mask = 0;
+    int need = K;   // rank wanted among the values that match the prefix
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        hist[tid] = 0;
+        __syncthreads();
+        for (int i = tid; i < n; i += 256) {
+            const unsigned u = ord_bits(vals[i]);
+            if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
+        }
+        __syncthreads();
+        if (tid < 64) {
+            // lane l holds digits 255 - 4l .. 252 - 4l, largest first
+            int h[4], tot = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                h[q] = hist[255 - (4 * tid + q)];
+                tot += h[q];
+            }
+            int incl = tot;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int t = __shfl_up(incl, o);
+                if (tid >= o) incl += t;
+            }
+            int acc = incl - tot;
+            if (acc < need && need <= incl) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (acc < need && need <= acc + h[q]) {
+                        sel[0] = 255 - (4 * tid + q);
+                        sel[1] = need - acc;
+                    }
+                    acc += h[q];
+                }
+            }
+        }
+        __syncthreads();
+        prefix |= (unsigned)sel[0] << shift;
+        mask |= 255u << shift;
+        need = sel[1];
+        __syncthreads();   // sel and hist are rewritten by the next pass
+    }
+    return prefix;
+}
+
 // (value, id) pairs of a wave sorted in the (value desc, id asc) order, lane
 // 0 first: a bitonic network over __shfl_xor (ids are distinct, so the
 // order is total; padding pairs are equal and stay put).
@@ -582,9 +639,11 @@ static_assert(kMaxSplitsLong * kKeepLong <= kMergeCap, "long-list slices fit the
 //     threads' heads (a thread's head is the best entry of its slices); k
 //     threads, so k distinct slices, reach it, so at least k candidates are
 //     >= it (k <= 64; otherwise t0 = -inf);
-//  3. every slice entry >= t0 goes to LDS and is sorted (in registers when
-//     k <= 64 and at most 256 entries qualify), and the first k are the
-//     row's top-k among the candidates;
+//  3. every slice entry >= t0 goes to LDS; when more than 2k qualify and
+//     they would not fit the register sort, a radix select finds the exact
+//     k-th largest of them and only those at or above it stay; the rest is
+//     sorted (in registers when k <= 64 and at most 256 remain), and the
+//     first k are the row's top-k among the candidates;
 //  4. a slice whose bound (everything it dropped is <= bound) reaches the k-th
 //     value is re-evaluated exactly from memory, so the result is the exact
 //     top-k of the row for any data, ties included.
@@ -594,6 +653,8 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     __shared__ float red[4];
     __shared__ float s_bound[4];
     __shared__ float s_heads[256];
+    __shared__ int s_hist[256];
+    __shared__ int s_sel[2];
     __shared__ int s_count, s_nflag, s_ncand;
     __shared__ float cand_v[kMergeCap];
     __shared__ int cand_i[kMergeCap];
@@ -671,7 +732,34 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
         }
     }
     __syncthreads();
-    const int c = s_count;
+    int c = s_count;
+    if ((K > 64 || c > 256) && c > 2 * K) {
+        // many candidates: keep those at or above the exact K-th largest
+        // value (at least K of them; more only with ties)
+        const unsigned tk = kth_largest_ord(cand_v, c, K, s_hist, s_sel);
+        constexpr int CPT = kMergeCap / 256;
+        float rv[CPT];
+        int ri[CPT];
+#pragma unroll
+        for (int m = 0; m < CPT; ++m) {
+            const int i = tid + 256 * m;
+            rv[m] = i < c ? cand_v[i] : neg_inf();
+            ri[m] = i < c ? cand_i[i] : 0;
+        }
+        if (tid == 0) s_count = 0;
+        __syncthreads();   // every candidate read before any is moved
+#pragma unroll
+        for (int m = 0; m < CPT; ++m) {
+            const int i = tid + 256 * m;
+            if (i < c && ord_bits(rv[m]) >= tk) {
+                const int pos = atomicAdd(&s_count, 1);
+                cand_v[pos] = rv[m];
+                cand_i[pos] = ri[m];
+            }
+        }
+        __syncthreads();
+        c = s_count;
+    }
     if (K <= 64 && c <= 256) {
         // each wave sorts 64 candidates in registers, wave 0 merges the four
         // lists: the best 64 land sorted at the front of the buffer
