@@ -953,6 +953,11 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
         if (p.grid)   // a few row blocks sharing each range's weights through L2
             return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, false, 1, TF_LM_DMA_SINGLE_WB>(
                 x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+#if TF_LM_MULTI_NT8
+        if (p.NT == 8)
+            return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 8, 8, TF_LM_DMA_MULTI_KC, false, 1, 2>(
+                x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+#endif
         return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false,
                              TF_LM_DMA_MULTI_MINB>(
             x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
