@@ -66,11 +66,11 @@ def lm_kernel_pattern(rows: int, d: int) -> str:
     """Regex for the bf16 LM-head kernel instance the plan picks for `rows` rows
     (template arguments: weight tiles per wave, activation tiles, waves, ...):
     64- and 128-row tiles go to the LDS-DMA kernel when d is a multiple of its k
-    step (64 up to two row blocks, 32 beyond, in 256-row blocks)."""
+    step (64; beyond two row blocks in 256-row blocks)."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
     if nt >= 2 and rows <= 256 and d % 64 == 0:   # the wave grid, up to two row blocks
         return rf"lmhead_dma_kernel<\d+, {nt}, "
-    if nt == 4 and rows > 128 and d % 32 == 0:    # 256-row blocks
+    if nt == 4 and rows > 128 and d % 64 == 0:    # 256-row blocks
         return r"lmhead_dma_kernel<\d+, 8, "
     return rf"lmhead_bf16_kernel<\d+, {nt}, "
 

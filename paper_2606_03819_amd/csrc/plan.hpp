@@ -179,27 +179,30 @@ struct LmPlan {
 #ifndef TF_LM_DMA_NW
 #define TF_LM_DMA_NW 4
 #endif
-// Several row blocks (MFMA-bound): weight tiles per wave, k step, and
-// workgroups per CU the registers must allow.  32-wide k steps make the
-// rings 64 KiB, so two workgroups share a CU and one's barrier and fragment
-// waits hide behind the other's MFMAs (-8% at 1936 rows against one
-// workgroup of 64-wide steps).
+// Several row blocks (MFMA-bound).  Default: 256-row blocks of eight waves
+// in a 4 x 2 grid, one workgroup per CU.  Each copied weight tile then meets
+// 256 activation rows and each copied activation tile 8 weight tiles: 0.5
+// KiB of copies per 32 x 32 tile pair of MFMA work against 0.75 KiB with
+// 128-row blocks (+6% on the 1936-row batched step); 64-wide k steps fill
+// the 160 KiB of LDS (+1.5% against 32-wide).  With TF_LM_MULTI_NT8 = 0:
+// 128-row blocks of four waves at 32-wide steps (64 KiB rings), two
+// workgroups per CU, so one's barrier and fragment waits hide behind the
+// other's MFMAs.
+#ifndef TF_LM_MULTI_NT8
+#define TF_LM_MULTI_NT8 1
+#endif
 #ifndef TF_LM_DMA_MULTI_WM
 #define TF_LM_DMA_MULTI_WM 2
 #endif
 #ifndef TF_LM_DMA_MULTI_KC
+#if TF_LM_MULTI_NT8
+#define TF_LM_DMA_MULTI_KC 64
+#else
 #define TF_LM_DMA_MULTI_KC 32
+#endif
 #endif
 #ifndef TF_LM_DMA_MULTI_MINB
 #define TF_LM_DMA_MULTI_MINB 2
-#endif
-// Several row blocks: 256-row blocks of eight waves, one workgroup per CU.
-// Each copied weight tile then meets 256 activation rows, each copied
-// activation tile 8 weight tiles: 0.5 KiB of copies per 32 x 32 tile pair
-// of MFMA work against 0.75 KiB with 128-row blocks (+6% on the 1936-row
-// batched step).
-#ifndef TF_LM_MULTI_NT8
-#define TF_LM_MULTI_NT8 1
 #endif
 #ifndef TF_LM_DMA_KC
 #define TF_LM_DMA_KC 64

@@ -30,12 +30,13 @@ CASES = [
     (W("bf16-long-lists", 1, 64, 3000, 3, 4, 300, 32, "bf16", 1.0, 13, 130), 0.15),
     # long per-slice lists (K2 >= 64) on the other LM-head shapes: 49 rows
     # (two activation tiles, DMA kernel), 164 rows with d = 80 (register-staged
-    # kernel, two row blocks) and with d = 96 (DMA kernel, two row blocks)
+    # kernel, two row blocks) and 287 rows with d = 128 (DMA kernel, 256-row
+    # blocks)
     (W("bf16-nt2-long", 1, 128, 3000, 5, 12, 72, 64, "bf16", 1.0, 16, 160), 0.12),
     # 49 rows with d = 80: the register-staged kernel's two-tile shape
     (W("bf16-reg-nt2", 1, 80, 3000, 5, 12, 32, 64, "bf16", 1.0, 19, 190), 0.12),
     (W("bf16-reg-multi-long", 4, 80, 2500, 6, 8, 80, 64, "bf16", 1.0, 17, 170), 0.12),
-    (W("bf16-dma-multi-long", 4, 96, 2500, 6, 8, 80, 64, "bf16", 1.0, 18, 180), 0.12),
+    (W("bf16-dma-multi-long", 7, 128, 2500, 6, 8, 80, 64, "bf16", 1.0, 18, 180), 0.12),
     (W("f32-ragged-vocab", 2, 96, 1000, 5, 3, 12, 64, "f32", 1.0, 7, 70), 0.15),
 ]
 
