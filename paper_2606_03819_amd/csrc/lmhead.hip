@@ -67,14 +67,16 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
 //
 // The same vocabulary slices with the weight and activation tiles copied
 // from memory straight into LDS (global_load_lds_dwordx4, no register
-// staging), so that the registers go to accumulators: NW waves of WM weight
-// tiles each (WNT: the weight copies carry the non-temporal hint).  k
-// advances KC at a time.  The weight tiles ([32 rows][KC] per
-// tile, each wave its own WM) go through a ring of S stages, copied S - 1
-// steps ahead; the activation tile ([32*NT rows][KC], shared) through a ring
-// of two, copied one step ahead from L2.  Each step a wave issues its
-// activation copies first, so waiting for them (all but the step's weight
-// copies retired, in issue order) also retires the older weight copies.  One
+// staging), so that the registers go to accumulators.  The NW waves form a
+// grid of NW / WB along the weight tiles (WM each) times WB along the
+// activation tiles (NT / WB each); the WB waves of a weight column split its
+// copies (WNT: they carry the non-temporal hint).  k advances KC at a time.
+// The weight tiles ([32 rows][KC] per tile) go through a ring of S stages,
+// copied S - 1 steps ahead; the activation tile ([32*NT rows][KC]) through a
+// ring of two, copied one step ahead from L2.  After the step's barrier a
+// wave issues the next activation copies, then spreads the weight copies of
+// step j + S - 1 over its MFMA sub-steps; waiting for the activation copies
+// (issue order) also retires the older weight copies.  One
 // DMA instruction fills 1 KiB: 1024 / (2 KC) whole rows, lane l taking
 // 16-byte slot l % (KC / 8) of row l / (KC / 8).  Slots are XOR-swizzled per
 // row so that the 16 rows one quarter-wave reads at one logical slot cover

@@ -116,18 +116,19 @@ inline GemmPlan gemm_plan(int rows, int ntiles, int K, int wg_single) {
 }
 
 // LM head over [rows, d] x [V, d]: vocabulary slices (see SliceMap), one
-// workgroup per (tile range, row block).  A single row block spreads the
-// tiles over TF_LM_WORKGROUPS ranges; several row blocks use one chunk per
-// range, the row blocks of a range on consecutive workgroups so that they
-// share its tiles through L2.  fp32 (small workloads, SIMT kernel): 32 rows
-// and at most 8 tiles (256 tokens) per workgroup.
+// workgroup per (tile range, row block), the row blocks of a range on
+// consecutive workgroups so that they share its tiles through L2.  One row
+// block, or up to TF_LM_GRID_NRB on the DMA kernel's wave grid: the tiles
+// spread over TF_LM_WORKGROUPS workgroups in all; more row blocks: one
+// chunk per range.  fp32 (small workloads, SIMT kernel): 32 rows and at most
+// 8 tiles (256 tokens) per workgroup.
 struct LmPlan {
     int NT, WM, NW, chunk, nrb, ntiles, nk;
     int WB = 1;   // waves along the activation tiles (a grid of NW / WB x WB waves)
-    bool grid = false;   // the DMA kernel's 2 x 2 wave grid
+    bool grid = false;   // the DMA kernel's 2 x 2 wave grid (up to TF_LM_GRID_NRB row blocks)
     SliceMap map;
     bool wnt;
-    bool dma;   // the LDS-DMA kernel (TF_LM_DMA_NW waves of TF_LM_DMA_WM tiles, k in steps of 32)
+    bool dma;   // the LDS-DMA kernel (the grid, or 256-row blocks; NT = 1 only with TF_LM_DMA_NT1)
     int nsplit() const { return map.G * map.rmax; }
     int blocks() const { return map.G * nrb; }
 };

@@ -453,10 +453,11 @@ __device__ inline void lm_merge_contributors(const float* cm, int rstride, int r
 // not in its list: a lane drops only values no larger than its bound, and the
 // workgroup merge drops only values no larger than the (kKeep+1)-th entry of
 // the union.  The merge kernel uses it to prove the global top-k exact, or to
-// re-evaluate the slice when it cannot.  Short lists (two entries per lane)
-// keep this pass cheap (it runs on the vector ALUs after every item); a
-// slice is re-evaluated only if one lane holds KL + 1 of the row's best k
-// logits or the slice KEEP + 1 of them.
+// re-evaluate the slice when it cannot.  Short lists (two or three entries
+// per lane, by how many logits of a row a lane holds) keep this pass cheap
+// (it runs on the vector ALUs after every item); a slice is re-evaluated
+// only if one lane holds KL + 1 of the row's best k logits or the slice
+// KEEP + 1 of them.
 template <int WM, int NT, int NW, bool LONG = false, int WB = 1>
 struct EpiLmHead {
     static constexpr int WA = NW / WB;            // waves along the weight tiles
