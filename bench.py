@@ -65,10 +65,11 @@ def kernel_source_digest() -> str:
 def lm_kernel_pattern(rows: int, d: int) -> str:
     """Regex for the bf16 LM-head kernel instance the plan picks for `rows` rows
     (template arguments: weight tiles per wave, activation tiles, waves, ...):
-    64- and 128-row tiles go to the LDS-DMA kernel when d is a multiple of its k
-    step (64; beyond two row blocks in 256-row blocks)."""
+    every tile shape goes to the LDS-DMA kernel when d is a multiple of its k
+    step (64; beyond two row blocks in 256-row blocks), else to the
+    register-staged kernel."""
     nt = 1 if rows <= 32 else (2 if rows <= 64 else 4)
-    if nt >= 2 and rows <= 256 and d % 64 == 0:   # the wave grid, up to two row blocks
+    if rows <= 256 and d % 64 == 0:   # 32-row tiles, or the wave grid up to two row blocks
         return rf"lmhead_dma_kernel<\d+, {nt}, "
     if nt == 4 and rows > 128 and d % 64 == 0:    # 256-row blocks
         return r"lmhead_dma_kernel<\d+, 8, "
