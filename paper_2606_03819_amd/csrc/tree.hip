@@ -280,7 +280,11 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a
             }
         const int row = __builtin_amdgcn_readlane(my_row, owner);
         const float pscore = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_ps), owner));
+        // both reads of the popped row together, so that ranks past the LDS
+        // cache cost one memory round trip per pop rather than two
         const int tok = get_idx(row, rank);
+        const bool more = rank + 1 < a.K2;
+        const float next_lp = more ? get_lp(row, rank + 1) : 0.f;
         const int child_row = tree_child_row(a, t, depth, tok, row, lane);
         if (lane == 0) {
             t.n_tok[n] = tok;
@@ -291,8 +295,6 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a
             t.n_crow[n] = child_row;
         }
         // the popped slot moves to its next sibling (owner lane)
-        const bool more = rank + 1 < a.K2;
-        const float next_lp = more ? get_lp(row, rank + 1) : 0.f;
         if (lane == owner) {
 #pragma unroll
             for (int j = 0; j < FS; ++j)
@@ -364,7 +366,9 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
         if (depth == 0) break;   // frontier exhausted (excluded by argument checks)
         const int slot = c_slot(best.meta), rank = c_rank(best.meta);
         const int row = t.f_row[slot];
+        // both reads of the popped row together (one round trip past the cache)
         const int tok = get_idx(row, rank);
+        const float next_lp = rank + 1 < a.K2 ? get_lp(row, rank + 1) : 0.f;
         const int child_row = tree_child_row(a, t, depth, tok, row, lane);
         wave_lds_sync();   // every lane has read the frontier before it changes
         if (lane == 0) {
@@ -376,7 +380,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
             t.n_crow[n] = child_row;
             if (rank + 1 < a.K2) {
                 t.f_rank[slot] = rank + 1;
-                t.f_score[slot] = t.f_pscore[slot] + get_lp(row, rank + 1);
+                t.f_score[slot] = t.f_pscore[slot] + next_lp;
             } else {
                 t.f_depth[slot] = 0;
             }
