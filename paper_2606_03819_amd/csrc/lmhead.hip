@@ -773,11 +773,19 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
         cand_i[e] = i;
         __syncthreads();
         if (wave == 0) {
-            float v1 = cand_v[64 + lane], v2 = cand_v[128 + lane], v3 = cand_v[192 + lane];
-            int i1 = cand_i[64 + lane], i2 = cand_i[128 + lane], i3 = cand_i[192 + lane];
-            wave_merge_pairs(v, i, v1, i1, lane);
-            wave_merge_pairs(v2, i2, v3, i3, lane);
-            wave_merge_pairs(v, i, v2, i2, lane);
+            // a wave whose 64 slots all lie past c holds padding only, which
+            // no merge takes over a candidate: merge only the waves in use
+            if (c > 64) {
+                float v1 = cand_v[64 + lane];
+                int i1 = cand_i[64 + lane];
+                if (c > 128) {
+                    float v2 = cand_v[128 + lane];
+                    int i2 = cand_i[128 + lane];
+                    if (c > 192) wave_merge_pairs(v2, i2, cand_v[192 + lane], cand_i[192 + lane], lane);
+                    wave_merge_pairs(v1, i1, v2, i2, lane);
+                }
+                wave_merge_pairs(v, i, v1, i1, lane);
+            }
             cand_v[lane] = v;
             cand_i[lane] = i;
         }
