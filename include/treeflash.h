@@ -78,6 +78,9 @@ size_t treeflash_workspace_bytes(int b, int gamma, int d, int I, int V, int k, i
  *   topk_idx      out [b, gamma, k] int32: the k best ids per depth (logit desc, id asc)
  *   topk_logprob  out [b, gamma, k] fp32 log-softmax values of those ids; may be NULL
  *   lse           out [b, gamma] fp32 log-sum-exp of the scaled logits; may be NULL
+ * bf16: the order and the listed log-probs use each logit with its 7 lowest
+ * mantissa bits cleared (a monotone change below 2^-16 relative), so logits
+ * that close rank by id; the log-sum-exp uses the full values.
  * The [b*gamma, V] logits are never written to memory.  The operation is the
  * same for any set of rows: called on h' viewed as [b, R, d] with k = topk2 it
  * is the LM-head half of the conditional stage (here `gamma` only counts rows
