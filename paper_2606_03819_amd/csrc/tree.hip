@@ -242,7 +242,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a
         const float first = get_lp(0, 0);
         if (lane == 0) {
             f_depth[0] = 1;
-            f_score[0] = first;
+            f_score[0] = 0.f + first;   // a -0.0 log-prob scores +0.0, as in the LDS kernel
         }
     }
 
@@ -256,9 +256,10 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_reg_kernel(TreeArgs a
                              ((uint32_t)f_depth[j] << 24) | ((uint32_t)(lane + 64 * j) << 12) | (uint32_t)f_rank[j]};
                 if (cand_before(c, lb, t)) lb = c;
             }
-        const uint32_t key = c_depth(lb.meta) != 0 ? f32_key(lb.score) : 0u;
+        // keys on score + 0: -0.0 and +0.0 tie here as they do in cand_before
+        const uint32_t key = c_depth(lb.meta) != 0 ? f32_key(lb.score + 0.f) : 0u;
         const uint32_t mx = wave_max_u32(key);
-        if (mx == 0u) break;   // frontier exhausted (excluded by argument checks)
+        if (mx == 0u) break;   // frontier exhausted: rows too short for B nodes; the rest stay -1
         const unsigned long long tied = __ballot(key == mx);
         Cand best;
         if (__popcll(tied) == 1) {
@@ -363,7 +364,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
         }
         best = wave_best(best, t);
         const int depth = c_depth(best.meta);
-        if (depth == 0) break;   // frontier exhausted (excluded by argument checks)
+        if (depth == 0) break;   // frontier exhausted: rows too short for B nodes; the rest stay -1
         const int slot = c_slot(best.meta), rank = c_rank(best.meta);
         const int row = t.f_row[slot];
         // both reads of the popped row together (one round trip past the cache)

@@ -29,3 +29,15 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    # worst parity errors per checked workload (collected by tests/parity.py)
+    try:
+        import parity
+    except Exception:
+        return
+    if parity.SUMMARY:
+        terminalreporter.write_sep("-", "parity against the oracle")
+        for line in parity.SUMMARY:
+            terminalreporter.write_line(line)
