@@ -39,6 +39,8 @@ Arithmetic is float64 throughout, with the following readings where the paper
 is silent (each is listed in DESIGN.md):
   * "normalized" is RMSNorm with its own gain, eps = 1e-6;
   * SwiGLU(x) = W_down (silu(W_gate x) * (W_up x)), no biases, x = [h~ ; e~];
+    without W_up, the plain two-layer SiLU MLP W_down silu(W_gate x) on the
+    same input and residual (a side mode);
   * the LM head is a plain product with the [V, d] output embedding; logits are
     multiplied by the inverse drafter temperature before the softmax;
   * for bf16 workloads the oracle rounds to bf16 exactly where a bf16 operand
@@ -169,13 +171,16 @@ def previous_tokens(root: int, topk_idx_seq: np.ndarray, gamma: int, M: int) -> 
 
 def ar_approximator(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
                     emb: np.ndarray, norm_h_gain: np.ndarray, norm_e_gain: np.ndarray,
-                    w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
+                    w_gate: np.ndarray, w_up: Optional[np.ndarray], w_down: np.ndarray,
                     eps: float = RMS_EPS, mirror_bf16: bool = False) -> np.ndarray:
     """Eq. 1 for every conditional row of one sequence.
 
     h_seq: [gamma, d] drafter states; prev/depth: [R] from row_table.
     h'_r = h_{depth_r} + W_down( silu(W_gate x_r) * (W_up x_r) ),
     x_r = [ rms(h_{depth_r}) ; rms(Embd(prev_r)) ].
+    With w_up None the gate is dropped: the plain two-layer SiLU MLP
+    h'_r = h_{depth_r} + W_down silu(W_gate x_r) on the same input and
+    residual (a side mode; Eq. 1 names the gated form).
     With mirror_bf16, x and h' are rounded to bf16 (the activation is not).
     """
     hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
@@ -184,8 +189,9 @@ def ar_approximator(h_seq: np.ndarray, prev: np.ndarray, depth: np.ndarray,
     if mirror_bf16:
         x = bf16_round(x)
     g = x @ np.asarray(w_gate, dtype=np.float64).T
-    u = x @ np.asarray(w_up, dtype=np.float64).T
-    a = silu(g) * u
+    a = silu(g)
+    if w_up is not None:
+        a = a * (x @ np.asarray(w_up, dtype=np.float64).T)
     hp = hd + a @ np.asarray(w_down, dtype=np.float64).T
     if mirror_bf16:
         hp = bf16_round(hp)
@@ -354,7 +360,8 @@ def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
 
     ``inputs`` holds float64/int64 numpy arrays: h [b, gamma, d], root [b],
     lm_head, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down (or w_lin
-    for the w/ Linear ablation, which then replaces Eq. 1's SwiGLU).
+    for the w/ Linear ablation, which then replaces Eq. 1's SwiGLU; without
+    w_up the plain SiLU MLP).
     ``sequences`` restricts the work to a subset of the batch (the sequences
     are independent).
     """
@@ -375,7 +382,7 @@ def draft(inputs: Dict[str, np.ndarray], gamma: int, k: int, B: int,
                                         mirror_bf16=mirror_bf16)
         else:
             hp = ar_approximator(h[s], prev, depth, inputs["emb"], inputs["norm_h_gain"],
-                                 inputs["norm_e_gain"], inputs["w_gate"], inputs["w_up"],
+                                 inputs["norm_e_gain"], inputs["w_gate"], inputs.get("w_up"),
                                  inputs["w_down"], eps=eps, mirror_bf16=mirror_bf16)
         rows = conditional_stage(hp, inputs["lm_head"], K2, inv_temperature, keep_full=keep_full)
         tree = build_tree(rows["cond_idx"], rows["cond_logprob"], st1["topk_idx"], gamma, k, B)

@@ -166,7 +166,7 @@ def treeflash_marginal_topk(h: torch.Tensor, lm_head: torch.Tensor, k: int, inv_
 def treeflash_arapprox_hidden(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up, w_down,
                               rms_eps: float = 1e-6, workspace: Optional[torch.Tensor] = None,
                               hprime: Optional[torch.Tensor] = None, V: Optional[int] = None):
-    """Eq. 1 for every conditional row: h' [b, R, d]."""
+    """Eq. 1 for every conditional row: h' [b, R, d] (w_up None: the plain SiLU MLP)."""
     b, gamma, d = h.shape
     k = topk_idx.shape[2]
     V = emb.shape[0] if V is None else V
@@ -258,7 +258,8 @@ def treeflash_arapprox_expand(h, root_token, topk_idx, emb, norm_h_gain, norm_e_
                               lm_head, topk2: int, inv_temperature: float = 1.0, rms_eps: float = 1e-6,
                               workspace: Optional[torch.Tensor] = None, cond_idx=None, cond_logprob=None,
                               cond_lse=None, want_lse: bool = True):
-    """Stage 2: Eq. 1 on every conditional row, LM head, log-softmax, top-topk2."""
+    """Stage 2: Eq. 1 on every conditional row (w_up None: the plain SiLU MLP),
+    LM head, log-softmax, top-topk2."""
     b, gamma, d = h.shape
     k = topk_idx.shape[2]
     V = lm_head.shape[0]
@@ -465,7 +466,7 @@ class Drafter:
             return self.cond_idx, self.cond_lp, self.cond_lse
         return treeflash_arapprox_expand(
             h, root, self.topk_idx if topk_idx is None else topk_idx, w["emb"], w["norm_h_gain"],
-            w["norm_e_gain"], w["w_gate"], w["w_up"], w["w_down"], w["lm_head"], self.topk2, self.inv_t,
+            w["norm_e_gain"], w["w_gate"], w.get("w_up"), w["w_down"], w["lm_head"], self.topk2, self.inv_t,
             self.eps, self.workspace, self.cond_idx, self.cond_lp, self.cond_lse)
 
     def tree_build(self, cond_idx=None, cond_lp=None, topk_idx=None):

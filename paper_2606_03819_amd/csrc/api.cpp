@@ -3,6 +3,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <initializer_list>
+
 #include "../../include/treeflash.h"
 #include "launch.hpp"
 #include "plan.hpp"
@@ -13,22 +15,49 @@ using namespace tf;
 
 constexpr long long kMaxRows = 1 << 20;
 
-// Operands read with 16-byte vector loads (activations, weights, h', the
-// workspace) must be 16-byte aligned; every other array only needs the
-// alignment of its 4-byte elements.
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+// Alignment.  An array not aligned to its element size is an invalid
+// argument.  Operands read with 16-byte vector loads (h, h', the weights, the
+// LM head) must also be 16-byte aligned; an element-aligned pointer that is
+// not is a valid request this build does not implement (TF_ERR_UNSUPPORTED).
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool dtype_ok(tf_dtype_t dt) { return dt == TF_F32 || dt == TF_BF16; }
+size_t elem_bytes(tf_dtype_t dt) { return dt == TF_BF16 ? 2 : 4; }
+bool elem_aligned(const void* p, tf_dtype_t dt) { return (reinterpret_cast<uintptr_t>(p) % elem_bytes(dt)) == 0; }
+// a vector-loaded operand of type dt (non-null)
+tf_status_t vec_status(const void* p, tf_dtype_t dt) {
+    if (!elem_aligned(p, dt)) return TF_ERR_INVALID_ARG;
+    return aligned16(p) ? TF_OK : TF_ERR_UNSUPPORTED;
+}
+// the first non-OK status of a list of vector-loaded operands, invalid before unsupported
+tf_status_t vec_status_all(std::initializer_list<const void*> ps, tf_dtype_t dt) {
+    tf_status_t worst = TF_OK;
+    for (const void* p : ps) {
+        const tf_status_t st = vec_status(p, dt);
+        if (st == TF_ERR_INVALID_ARG) return st;
+        if (st != TF_OK) worst = st;
+    }
+    return worst;
+}
+
+// Widths: d (and I) must be positive; the kernels step through them 16 at a
+// time (the MFMA's k), so other values are unsupported.
+tf_status_t width_status(int w) {
+    if (w < 1) return TF_ERR_INVALID_ARG;
+    return w % 16 == 0 ? TF_OK : TF_ERR_UNSUPPORTED;
+}
 
 // `gamma` is a draft depth (at most 255) unless `rows_only`, where it only
 // counts rows per sequence (the LM-head call on h' viewed as [b, R, d]).
-bool common_shapes_ok(int b, int gamma, int d, int V, int k, bool rows_only = false) {
-    if (b < 1 || gamma < 1 || (!rows_only && gamma > 255) || V < 1 || k < 1 || k > V || k > kMaxTopk) return false;
-    if (d < 16 || d % 16 != 0) return false;
-    if ((long long)b * gamma > kMaxRows) return false;
-    if (!rows_only && (long long)b * (1 + (long long)(gamma - 1) * k) > kMaxRows) return false;
-    if ((long long)V * d >= (1ll << 40)) return false;
-    return true;
+tf_status_t common_shapes(int b, int gamma, int d, int V, int k, bool rows_only = false) {
+    if (b < 1 || gamma < 1 || (!rows_only && gamma > 255) || V < 1 || k < 1 || k > V || k > kMaxTopk)
+        return TF_ERR_INVALID_ARG;
+    const tf_status_t wd = width_status(d);
+    if (wd != TF_OK) return wd;
+    if ((long long)b * gamma > kMaxRows) return TF_ERR_INVALID_ARG;
+    if (!rows_only && (long long)b * (1 + (long long)(gamma - 1) * k) > kMaxRows) return TF_ERR_INVALID_ARG;
+    if ((long long)V * d >= (1ll << 40)) return TF_ERR_INVALID_ARG;
+    return TF_OK;
 }
 
 size_t stage1_bytes(int b, int gamma, int d, int V, bool bf16) {
@@ -40,8 +69,8 @@ size_t stage1_bytes(int b, int gamma, int d, int V, bool bf16) {
 extern "C" {
 
 size_t treeflash_workspace_bytes(int b, int gamma, int d, int I, int V, int k, int topk2, tf_dtype_t dt) {
-    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k)) return 0;
-    if (I < 16 || I % 16 != 0 || topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return 0;
+    if (!dtype_ok(dt) || common_shapes(b, gamma, d, V, k) != TF_OK) return 0;
+    if (width_status(I) != TF_OK || topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return 0;
     return workspace_layout(b, gamma, d, I, V, k, dt == TF_BF16).total;
 }
 
@@ -50,11 +79,14 @@ static tf_status_t marginal_topk(const void* h, const void* lm_head, int b, int 
                                  float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
                                  hipEvent_t ev_begin, hipEvent_t ev_end) {
     if (h == nullptr || lm_head == nullptr || topk_idx == nullptr) return TF_ERR_INVALID_ARG;
-    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k, true)) return TF_ERR_INVALID_ARG;
+    if (!dtype_ok(dt)) return TF_ERR_INVALID_ARG;
+    const tf_status_t shp = common_shapes(b, gamma, d, V, k, true);
+    if (shp != TF_OK) return shp;
     if (!(inv_temperature > 0.f) || !isfinite(inv_temperature)) return TF_ERR_INVALID_ARG;
-    if (!aligned16(h) || !aligned16(lm_head) || !aligned4(topk_idx) ||
-        (topk_logprob != nullptr && !aligned4(topk_logprob)) || (lse != nullptr && !aligned4(lse)))
+    if (!aligned4(topk_idx) || (topk_logprob != nullptr && !aligned4(topk_logprob)) || (lse != nullptr && !aligned4(lse)))
         return TF_ERR_INVALID_ARG;
+    const tf_status_t al = vec_status_all({h, lm_head}, dt);
+    if (al != TF_OK) return al;
     const bool bf16 = dt == TF_BF16;
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < stage1_bytes(b, gamma, d, V, bf16))
         return TF_ERR_WORKSPACE;
@@ -86,23 +118,24 @@ tf_status_t treeflash_marginal_topk_timed(const void* h, const void* lm_head, in
 
 namespace {
 
+// w_up may be null (the plain SiLU MLP) when `up_optional`.
 tf_status_t check_hidden_args(const void* h, const int32_t* root_token, const int32_t* topk_idx, const void* emb,
                               const void* norm_h_gain, const void* norm_e_gain, const void* w_gate,
                               const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
-                              float rms_eps, tf_dtype_t dt) {
+                              float rms_eps, tf_dtype_t dt, bool up_optional = false) {
     if (h == nullptr || root_token == nullptr || topk_idx == nullptr || emb == nullptr || w_gate == nullptr ||
-        w_up == nullptr || w_down == nullptr)
+        (w_up == nullptr && !up_optional) || w_down == nullptr)
         return TF_ERR_INVALID_ARG;
-    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k)) return TF_ERR_INVALID_ARG;
-    if (I < 16 || I % 16 != 0) return TF_ERR_INVALID_ARG;
+    if (!dtype_ok(dt)) return TF_ERR_INVALID_ARG;
+    tf_status_t st = common_shapes(b, gamma, d, V, k);
+    if (st != TF_OK) return st;
+    if ((st = width_status(I)) != TF_OK) return st;
     if (!(rms_eps >= 0.f) || !isfinite(rms_eps)) return TF_ERR_INVALID_ARG;
-    const void* vec[] = {h, w_gate, w_up, w_down};
-    for (const void* p : vec)
-        if (!aligned16(p)) return TF_ERR_INVALID_ARG;
-    if (!aligned4(root_token) || !aligned4(topk_idx) || !aligned4(emb)) return TF_ERR_INVALID_ARG;
-    if ((norm_h_gain != nullptr && !aligned4(norm_h_gain)) || (norm_e_gain != nullptr && !aligned4(norm_e_gain)))
+    if (!aligned4(root_token) || !aligned4(topk_idx) || !elem_aligned(emb, dt)) return TF_ERR_INVALID_ARG;
+    if ((norm_h_gain != nullptr && !elem_aligned(norm_h_gain, dt)) ||
+        (norm_e_gain != nullptr && !elem_aligned(norm_e_gain, dt)))
         return TF_ERR_INVALID_ARG;
-    return TF_OK;
+    return vec_status_all({h, w_gate, w_up != nullptr ? w_up : w_gate, w_down}, dt);
 }
 
 }  // namespace
@@ -115,9 +148,10 @@ tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, 
                                       int d, int I, int V, int k, float rms_eps, tf_dtype_t dt, void* hprime,
                                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
     const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
-                                              w_down, b, gamma, d, I, V, k, rms_eps, dt);
+                                              w_down, b, gamma, d, I, V, k, rms_eps, dt, true);
     if (chk != TF_OK) return chk;
-    if (hprime == nullptr || !aligned16(hprime)) return TF_ERR_INVALID_ARG;
+    if (hprime == nullptr) return TF_ERR_INVALID_ARG;
+    if (vec_status(hprime, dt) != TF_OK) return vec_status(hprime, dt);
     const bool bf16 = dt == TF_BF16;
     const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16);
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
@@ -131,8 +165,8 @@ tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, 
 }
 
 size_t treeflash_workspace_bytes_2prev(int b, int gamma, int d, int I, int V, int k, int topk2, tf_dtype_t dt) {
-    if (!dtype_ok(dt) || !common_shapes_ok(b, gamma, d, V, k)) return 0;
-    if (I < 16 || I % 16 != 0 || topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return 0;
+    if (!dtype_ok(dt) || common_shapes(b, gamma, d, V, k) != TF_OK) return 0;
+    if (width_status(I) != TF_OK || topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return 0;
     if ((long long)b * cond_rows(gamma, k, 1) > kMaxRows) return 0;
     return workspace_layout(b, gamma, d, I, V, k, dt == TF_BF16, true).total;
 }
@@ -148,7 +182,8 @@ tf_status_t treeflash_arapprox_2prev_hidden(const void* h, const int32_t* contex
     if (chk != TF_OK) return chk;
     if (context_token == nullptr || !aligned4(context_token)) return TF_ERR_INVALID_ARG;
     if ((long long)b * cond_rows(gamma, k, 1) > kMaxRows) return TF_ERR_INVALID_ARG;
-    if (hprime == nullptr || !aligned16(hprime)) return TF_ERR_INVALID_ARG;
+    if (hprime == nullptr) return TF_ERR_INVALID_ARG;
+    if (vec_status(hprime, dt) != TF_OK) return vec_status(hprime, dt);
     const bool bf16 = dt == TF_BF16;
     const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16, true);
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
@@ -171,7 +206,8 @@ tf_status_t treeflash_arapprox_linear_hidden(const void* h, const int32_t* root_
     const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_lin, w_lin,
                                               w_lin, b, gamma, d, 16, V, k, rms_eps, dt);
     if (chk != TF_OK) return chk;
-    if (hprime == nullptr || !aligned16(hprime)) return TF_ERR_INVALID_ARG;
+    if (hprime == nullptr) return TF_ERR_INVALID_ARG;
+    if (vec_status(hprime, dt) != TF_OK) return vec_status(hprime, dt);
     const bool bf16 = dt == TF_BF16;
     const Workspace lay = workspace_layout(b, gamma, d, 16, V, k, bf16);
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;
@@ -192,14 +228,14 @@ tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, 
                                       float* cond_logprob, float* cond_lse, void* workspace,
                                       size_t workspace_bytes, hipStream_t stream) {
     const tf_status_t chk = check_hidden_args(h, root_token, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate, w_up,
-                                              w_down, b, gamma, d, I, V, k, rms_eps, dt);
+                                              w_down, b, gamma, d, I, V, k, rms_eps, dt, true);
     if (chk != TF_OK) return chk;
     if (lm_head == nullptr || cond_idx == nullptr || cond_logprob == nullptr) return TF_ERR_INVALID_ARG;
     if (topk2 < 1 || topk2 > V || topk2 > kMaxTopk) return TF_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.f) || !isfinite(inv_temperature)) return TF_ERR_INVALID_ARG;
-    if (!aligned16(lm_head) || !aligned4(cond_idx) || !aligned4(cond_logprob) ||
-        (cond_lse != nullptr && !aligned4(cond_lse)))
+    if (!aligned4(cond_idx) || !aligned4(cond_logprob) || (cond_lse != nullptr && !aligned4(cond_lse)))
         return TF_ERR_INVALID_ARG;
+    if (vec_status(lm_head, dt) != TF_OK) return vec_status(lm_head, dt);
     const bool bf16 = dt == TF_BF16;
     const Workspace lay = workspace_layout(b, gamma, d, I, V, k, bf16);
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < lay.total) return TF_ERR_WORKSPACE;

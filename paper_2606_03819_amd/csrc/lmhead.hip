@@ -4,6 +4,7 @@
 // partial, and one merge workgroup per row turns the partials into the row's
 // log-sum-exp and exact top-k.
 #include "common.hpp"
+#include "dma.hpp"
 #include "launch.hpp"
 #include "plan.hpp"
 #include "stream_gemm.hpp"
@@ -81,12 +82,6 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
 // 16-byte slot l % (KC / 8) of row l / (KC / 8).  Slots are XOR-swizzled per
 // row so that the 16 rows one quarter-wave reads at one logical slot cover
 // all 64 banks.
-typedef __attribute__((address_space(3))) void lds_void_t;
-// cache-policy bit of a non-temporal load (weights that one workgroup alone
-// streams: a single activation row block); several row blocks share each
-// weight tile through L2 and load it normally
-constexpr int kCpolNt = 2;
-typedef __attribute__((address_space(1))) void global_void_t;
 
 template <int WM, int NT, int NW, int KC, int S, int WB = 1>
 struct DmaTraits {
@@ -117,17 +112,6 @@ struct DmaTraits {
     }
 };
 
-// wait until at most N of this wave's memory loads are outstanding (also a
-// compiler barrier for memory operations)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-    asm volatile("" ::: "memory");
-}
-
-__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <int WM, int NT, int NW, int KC, int S, bool WNT, int MINB, bool LONG, int WB>
 __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_t* __restrict__ x, long ldx,

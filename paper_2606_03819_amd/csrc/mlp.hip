@@ -6,6 +6,7 @@
 // prev_r (Ablations, Model Design).  Rows follow the tables in rows.hpp.
 #include "common.hpp"
 #include "launch.hpp"
+#include "mlp_dma.hpp"
 #include "plan.hpp"
 #include "rows.hpp"
 #include "stream_gemm.hpp"
@@ -157,6 +158,17 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void gateup_bf16_kernel(W
     stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
+// the plain SiLU MLP's input projection: tiles of 32 gate rows
+template <int WM, int NT, int NW, int PIPE, bool WNT>
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void silu_gate_bf16_kernel(WRowsPlain ws, XRowsConcat xs,
+                                                                                  GemmShape sh,
+                                                                                  uint16_t* __restrict__ act, int I,
+                                                                                  float* partial, int* counter) {
+    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
+    EpiFixup<WM, NT, NW, EpiSiLU<WM, NT>> epi{EpiSiLU<WM, NT>{act, I}, partial, counter};
+    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
+}
+
 template <int WM, int NT, int NW, int PIPE, bool WNT>
 __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void down_bf16_kernel(WRowsPairedK ws, XRowsPlain xs, GemmShape sh,
                                                                uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
@@ -182,7 +194,7 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void linear_bf16_kernel(W
 // ------------------------------------------------------------------ fp32
 
 // x_r = [ht(depth) ; et(r)] is K = d + ew wide.
-__global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ wg, const float* __restrict__ wu,
+__global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ wg, const float* wu,
                                                          const float* __restrict__ ht, const float* __restrict__ et,
                                                          int rows, int d, int ew, int I, RowTable rt,
                                                          float* __restrict__ act) {
@@ -195,17 +207,18 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict
     const float* hr = ht + (size_t)(s * rt.gamma + rt.depth(rl) - 1) * d;
     const float* er = et + (size_t)r * ew;
     const float* g_row = wg + (size_t)i * K;
-    const float* u_row = wu + (size_t)i * K;
-    float g = 0.f, u = 0.f;
-    for (int k = 0; k < d; ++k) {
-        g = fmaf(hr[k], g_row[k], g);
-        u = fmaf(hr[k], u_row[k], u);
+    float g = 0.f;
+    for (int k = 0; k < d; ++k) g = fmaf(hr[k], g_row[k], g);
+    for (int k = 0; k < ew; ++k) g = fmaf(er[k], g_row[d + k], g);
+    float a = g / (1.0f + expf(-g));
+    if (wu != nullptr) {   // SwiGLU; without it the plain SiLU MLP
+        const float* u_row = wu + (size_t)i * K;
+        float u = 0.f;
+        for (int k = 0; k < d; ++k) u = fmaf(hr[k], u_row[k], u);
+        for (int k = 0; k < ew; ++k) u = fmaf(er[k], u_row[d + k], u);
+        a *= u;
     }
-    for (int k = 0; k < ew; ++k) {
-        g = fmaf(er[k], g_row[d + k], g);
-        u = fmaf(er[k], u_row[d + k], u);
-    }
-    act[(size_t)r * I + i] = g / (1.0f + expf(-g)) * u;
+    act[(size_t)r * I + i] = a;
 }
 
 __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__ wd, const float* __restrict__ act,
@@ -243,15 +256,22 @@ __global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict
 
 // ------------------------------------------------------------------ launcher
 
+// SwiGLU gate/up, or the gate alone when wu is null (plain SiLU MLP)
 template <int WM, int NT, int NW, int PIPE, bool WNT>
 static void launch_gateup(const uint16_t* wg, const uint16_t* wu, const uint16_t* ht, const uint16_t* et,
                           uint16_t* act, int rows, int d, int ew, int I, const RowTable& rt, const GemmPlan& pg,
                           float* partial, int* counters, hipStream_t st) {
-    WRowsGateUp wgu{wg, wu, I, d + ew};
     XRowsConcat xc{ht, et, d, ew, rt};
     const GemmShape shg = pg.shape(rows, d + ew);
-    hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgu, xc, shg,
-                       act, I, partial, counters);
+    if (wu != nullptr) {
+        WRowsGateUp wgu{wg, wu, I, d + ew};
+        hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgu, xc,
+                           shg, act, I, partial, counters);
+    } else {
+        WRowsPlain wgp{wg, I, d + ew};
+        hipLaunchKernelGGL((silu_gate_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgp,
+                           xc, shg, act, I, partial, counters);
+    }
 }
 
 // the activation is [rows, 2I] bf16 hi/lo pairs
@@ -321,6 +341,56 @@ static void launch_norms(const void* h, const int32_t* root, const int32_t* cont
                        diag, counters, ncounters);
 }
 
+// ------------------------------------------------ one row block (mlp_dma.hpp)
+
+// Ring depths: 40-70 KiB of weights in flight (SW - 1 stages of TG tiles,
+// 4 KiB each), and two activation chunks; the down projection's 256-byte
+// activation rows leave room for fewer weight stages.
+template <int TG, bool PAIRED>
+constexpr int mlp_dma_sw() {
+    return PAIRED ? (TG == 2 ? 6 : 4) : (TG == 2 ? 10 : 5);
+}
+constexpr int kMlpDmaSX = 3;
+
+template <int TG, int NTE, bool PAIRED, int WMAP, int EPI>
+static hipError_t launch_mlp_dma_nte(const MlpDmaArgs& a, hipStream_t st) {
+    constexpr int SW = mlp_dma_sw<TG, PAIRED>(), SX = kMlpDmaSX;
+    using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
+    static_assert(T::SMEM <= 152 * 1024, "LDS of one workgroup");
+    auto kern = mlp_dma_kernel<TG, NTE, PAIRED, SW, SX, WMAP, EPI>;
+    const hipError_t e =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::SMEM);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(a.G), dim3(256), T::SMEM, st, a);
+    return hipGetLastError();
+}
+
+template <bool PAIRED, int WMAP, int EPI>
+static hipError_t launch_mlp_dma(const MlpDmaArgs& a, const MlpDmaPlan& p, hipStream_t st) {
+    constexpr int TG = PAIRED ? TF_MLP_DMA_TG_DOWN : TF_MLP_DMA_TG_IN;
+    if (p.TG != TG) return hipErrorInvalidValue;
+    if (p.NTE == 1) return launch_mlp_dma_nte<TG, 1, PAIRED, WMAP, EPI>(a, st);
+    if (p.NTE == 2) return launch_mlp_dma_nte<TG, 2, PAIRED, WMAP, EPI>(a, st);
+    return launch_mlp_dma_nte<TG, 4, PAIRED, WMAP, EPI>(a, st);
+}
+
+static MlpDmaArgs mlp_dma_args(const MlpDmaPlan& p, const uint16_t* w, const uint16_t* wu, int N, int Kw,
+                               const uint16_t* xh, const uint16_t* xe, long lde, int Rh, int Re, uint16_t* out,
+                               int Nout, const uint16_t* h, const RowTable& rt, float* partial, int* counter) {
+    return MlpDmaArgs{w,      wu,     N,       Kw,    xh,   xe,   lde,  Rh, Re,      p.ntiles, p.items,
+                      p.nkh,  p.nke,  p.G,     out,   Nout, h,    rt,   partial, counter};
+}
+
+// Eq. 1 (or the plain SiLU MLP when w_up is null) for at most 128 rows and
+// 32 drafter states: gate/up with the h~ half once per drafter state, then
+// the down projection with the residual.
+static hipError_t launch_arapprox_dma(const void* h, const int32_t* root, const int32_t* context,
+                                      const int32_t* topk_idx, const void* emb, const void* gain_h,
+                                      const void* gain_e, const void* w_gate, const void* w_up, const void* w_down,
+                                      int b, int d, int I, int V, const RowTable& rt, int npre, float eps, void* ht,
+                                      void* et, void* act, void* hp, float* partial, int* counters, int* diag,
+                                      hipStream_t stream);
+
 hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* context, const int32_t* topk_idx,
                            const void* emb, const void* gain_h, const void* gain_e, const void* w_gate,
                            const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
@@ -331,7 +401,10 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
     const int ew = npre * d;
     const int rows = b * rt.Rs;
     if (bf16) {
-        const GemmPlan pg = gateup_plan(rows, d + ew, I);
+        if (mlp_dma_applies(true, b, gamma, rt.Rs, d, I, ew))
+            return launch_arapprox_dma(h, root, context, topk_idx, emb, gain_h, gain_e, w_gate, w_up, w_down, b, d,
+                                       I, V, rt, npre, eps, ht, et, act, hp, mlp_partial, counters, diag, stream);
+        const GemmPlan pg = w_up != nullptr ? gateup_plan(rows, d + ew, I) : silu_gate_plan(rows, d + ew, I);
         const GemmPlan pd = down_plan(rows, d, I);
         const int ncounters = (int)(pg.counter_ints() + pd.counter_ints());
         launch_norms<uint16_t>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
@@ -373,6 +446,18 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
                                   float* mlp_partial, int* counters, int* diag, hipStream_t stream) {
     const RowTable rt = make_row_table(gamma, k, 0);
     const int rows = b * rt.Rs;
+    if (mlp_dma_applies(bf16, b, gamma, rt.Rs, d, 64, d)) {
+        // one row block: the h~ half once per drafter state, residual epilogue
+        const MlpDmaPlan pl = mlp_dma_linear_plan(rows, d);
+        launch_norms<uint16_t>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
+                               counters, pl.items, stream);
+        const uint16_t* hb = static_cast<const uint16_t*>(h);
+        const MlpDmaArgs al = mlp_dma_args(pl, static_cast<const uint16_t*>(w_lin), nullptr, d, 2 * d,
+                                           static_cast<const uint16_t*>(ht), static_cast<const uint16_t*>(et), d,
+                                           b * gamma, rows, static_cast<uint16_t*>(hp), d, hb, rt, mlp_partial,
+                                           counters);
+        return launch_mlp_dma<false, kMlpWPlain, kMlpEpiResidual>(al, pl, stream);
+    }
     if (bf16) {
         const GemmPlan pl = linear_plan(rows, d);
         launch_norms<uint16_t>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
@@ -404,6 +489,33 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
                            static_cast<float*>(hp));
     }
     return hipGetLastError();
+}
+
+static hipError_t launch_arapprox_dma(const void* h, const int32_t* root, const int32_t* context,
+                                      const int32_t* topk_idx, const void* emb, const void* gain_h,
+                                      const void* gain_e, const void* w_gate, const void* w_up, const void* w_down,
+                                      int b, int d, int I, int V, const RowTable& rt, int npre, float eps, void* ht,
+                                      void* et, void* act, void* hp, float* partial, int* counters, int* diag,
+                                      hipStream_t stream) {
+    const int ew = npre * d;
+    const int rows = b * rt.Rs;
+    const bool swiglu = w_up != nullptr;
+    const MlpDmaPlan pg = mlp_dma_gate_plan(rows, d, ew, I, swiglu);
+    const MlpDmaPlan pd = mlp_dma_down_plan(rows, d, I);
+    launch_norms<uint16_t>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
+                           counters, pg.items + pd.items, stream);
+    const uint16_t* hb = static_cast<const uint16_t*>(h);
+    const uint16_t* htb = static_cast<const uint16_t*>(ht);
+    const uint16_t* etb = static_cast<const uint16_t*>(et);
+    uint16_t* actb = static_cast<uint16_t*>(act);
+    const MlpDmaArgs ag = mlp_dma_args(pg, static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
+                                       I, d + ew, htb, etb, ew, b * rt.gamma, rows, actb, I, hb, rt, partial, counters);
+    hipError_t e = swiglu ? launch_mlp_dma<false, kMlpWGateUp, kMlpEpiSwiGLU>(ag, pg, stream)
+                          : launch_mlp_dma<false, kMlpWPlain, kMlpEpiSiLU>(ag, pg, stream);
+    if (e != hipSuccess) return e;
+    const MlpDmaArgs ad = mlp_dma_args(pd, static_cast<const uint16_t*>(w_down), nullptr, d, I, nullptr, actb, 2l * I,
+                                       0, rows, static_cast<uint16_t*>(hp), d, hb, rt, partial, counters + pg.items);
+    return launch_mlp_dma<true, kMlpWPlain, kMlpEpiResidual>(ad, pd, stream);
 }
 
 }  // namespace tf

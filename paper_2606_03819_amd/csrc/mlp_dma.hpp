@@ -1,0 +1,524 @@
+// The AR approximator's products when one activation row block holds every
+// conditional row (at most 128 rows, at most 32 drafter states): the batch-1
+// drafting step.
+//
+// Every product streams a weight matrix once against few activation rows, so
+// it is bound by HBM.  An item is TG weight tiles of 32 rows over the whole
+// reduction range; the range runs in 64-column chunks ("units"), and the
+// units of all items are dealt out in contiguous ranges to G workgroups, so
+// every workgroup streams the same weight bytes.  An item cut by a range
+// boundary is computed in pieces whose accumulators the last piece to arrive
+// sums in workgroup order (the same device-coherent hand-off as the SwiGLU
+// products of several row blocks).
+//
+// The reduction range has up to two phases (Eq. 1, x = [h~ ; e~]):
+//   h phase  columns 0..d-1 of W_gate / W_up / W_lin against the b*gamma
+//            normalised drafter states h~: every row of depth i of a
+//            sequence shares h~_i, so this half is computed once per
+//            (sequence, depth) on one 32-row activation tile;
+//   e phase  the remaining columns against the rows' own inputs: the
+//            normalised previous-token embeddings e~ (gate/up, SiLU, linear)
+//            or the SwiGLU activation as bf16 hi/lo pairs (down projection).
+// The epilogue adds the h-phase sum of a row's (sequence, depth) state to its
+// e-phase sum, so the result is the full product over x.
+//
+// Copies go from memory straight into LDS (global_load_lds): a weight ring of
+// SW stages (each TG tiles x 64 columns) fed far ahead, since one item has
+// few weight bytes per chunk, and an activation ring of SX stages (the chunk's
+// activation tile, re-read from L2 by every workgroup).  Four waves: in the e
+// phase wave w holds activation tile w % NTE and the k sub-steps of group
+// w / NTE; in the h phase wave w holds the single tile and sub-steps w (mod
+// 4).  Waves that share a tile sum their accumulators in wave order after the
+// loop.
+#pragma once
+
+#include "common.hpp"
+#include "dma.hpp"
+#include "rows.hpp"
+#include "stream_gemm.hpp"
+#include "work.hpp"
+
+namespace tf {
+
+// weight rows of a tile: gate rows 16t.. then the up rows with the same
+// indices (SwiGLU), or 32 consecutive rows (every other product)
+constexpr int kMlpWGateUp = 0;
+constexpr int kMlpWPlain = 1;
+// epilogues
+constexpr int kMlpEpiSwiGLU = 0;    // a = silu(g) * u as bf16 hi/lo pairs
+constexpr int kMlpEpiSiLU = 1;      // a = silu(g) as bf16 hi/lo pairs (no up projection)
+constexpr int kMlpEpiResidual = 2;  // h' = bf16(h + y)
+
+struct MlpDmaArgs {
+    const uint16_t* w;    // plain weights [N, Kw], or the gate rows (gate/up)
+    const uint16_t* wu;   // the up rows [N, Kw] (gate/up)
+    int N;                // rows of w (and wu)
+    int Kw;               // weight columns
+    const uint16_t* xh;   // h phase: [Rh, d] normalised drafter states
+    const uint16_t* xe;   // e phase: [Re, lde]
+    long lde;
+    int Rh, Re;
+    int ntiles, items, nkh, nke, G;
+    uint16_t* out;        // [Re, 2 * Nout] hi/lo pairs, or [Re, Nout] (residual)
+    int Nout;             // output width: I (activations) or d (residual)
+    const uint16_t* h;    // residual source [b * gamma, d] (raw drafter states)
+    RowTable rt;
+    float* partial;       // [2G][PF] pieces of cut items
+    int* counter;         // [items] arrival counters, zero before the launch
+};
+
+template <int TG, int NTE, bool PAIRED, int SW, int SX>
+struct MlpDmaTraits {
+    static constexpr int NTHREADS = 256;
+    static constexpr int WTILE = 32 * 128;                  // one weight tile of one stage (64 columns)
+    static constexpr int WSTAGE = TG * WTILE;
+    static constexpr int XROWB = PAIRED ? 256 : 128;        // bytes of an activation row in one stage
+    static constexpr int XRPI = 1024 / XROWB;               // activation rows per DMA instruction
+    static constexpr int XSTAGE_E = 32 * NTE * XROWB;
+    static constexpr int XSTAGE_H = 32 * 128;
+    static constexpr int XSTAGE = XSTAGE_E > XSTAGE_H ? XSTAGE_E : XSTAGE_H;
+    static constexpr int XOFF = SW * WSTAGE;
+    static constexpr int RING = SW * WSTAGE + SX * XSTAGE;
+    static constexpr int QS = PAIRED ? 8 : 4;               // MFMA k sub-steps per chunk (e phase)
+    // two waves copy the weights, two the activations
+    static constexpr int WPW = 2 * TG;                      // weight DMA instructions per copier per chunk
+    static constexpr int XPW_H = 2;                         // activation DMA instructions per copier (h phase)
+    static constexpr int XPW_E = XSTAGE_E / 1024 / 2;       // ... (e phase)
+    static_assert(WPW * (SW - 2) <= 62 && XPW_E <= 62, "vmcnt range");
+    // 2 x 2 wave grid: two waves along the weight tiles (TW each), two
+    // along the activation tiles (NTW each, or both on the single tile of
+    // the h phase / of NTE = 1, splitting its k sub-steps)
+    static constexpr int TW = TG / 2;
+    static constexpr int NTW = NTE >= 2 ? NTE / 2 : 1;
+    // after the loop: the waves' accumulators, then (in the same LDS) the summed ones
+    static constexpr int TILE_F = 1024;                     // floats of one 32x32 accumulator
+    static constexpr int PF = TG * TILE_F * (1 + NTE);      // floats of one item's sums (h, then e)
+    static constexpr int SCR_W = 4 * TW * (1 + NTW) * TILE_F * 4;
+    static constexpr int SCR_C = PF * 4;
+    static constexpr int SMEM = RING > SCR_W ? (RING > SCR_C ? RING : SCR_C) : (SCR_W > SCR_C ? SCR_W : SCR_C);
+    static constexpr int HC = 4 * TG;                       // summed h floats per thread
+    static constexpr int EC = 4 * TG * NTE;                 // summed e floats per thread
+    static_assert(TG % 2 == 0, "weight tiles split over two waves");
+    static_assert(NTE == 1 || NTE == 2 || NTE == 4, "activation tiles");
+    static_assert(XPW_E >= 1 && XSTAGE_E % 2048 == 0, "whole DMA instructions per copier");
+    static_assert(SW > SX && SX >= 2, "ring depths: a chunk's weights are copied before its activations");
+    // 16-byte slot swizzles: 128-byte rows (weights, plain activations) and
+    // 256-byte rows (paired activations) keep a quarter-wave's 16 fragment
+    // reads at one logical slot on 16 distinct bank groups
+    __device__ static __forceinline__ int swz128(int r) { return (r >> 1) & 7; }
+    __device__ static __forceinline__ int swz256(int r) { return r & 15; }
+};
+
+// The item's outputs from its summed accumulators (hs: [TG][1024] h phase,
+// es: [TG][NTE][1024] e phase, both in MFMA register order: value j of lane
+// L is weight row 8(j/4) + 4(L/32) + j%4, activation row L%32).  Row r of
+// sequence s at depth i adds the h-phase sum of drafter state s*gamma+i-1.
+// One thread per (row, tile, group of 8 outputs).
+template <int TG, int NTE, int EPI>
+__device__ __forceinline__ void mlp_dma_epilogue(const MlpDmaArgs& a, int item, const float* hs, const float* es) {
+    constexpr int GPT = EPI == kMlpEpiSwiGLU ? 2 : 4;   // groups of 8 outputs per tile
+    const bool has_h = a.nkh > 0;
+    for (int e = threadIdx.x; e < 32 * NTE * TG * GPT; e += 256) {
+        const int r = e % (32 * NTE);
+        const int tg = e / (32 * NTE);
+        const int t = tg / GPT, q = tg - t * GPT;
+        const int tile = item * TG + t;
+        if (r >= a.Re || tile >= a.ntiles) continue;
+        const int n = r >> 5, c = r & 31;
+        const int sq = r / a.rt.Rs;
+        const int hr = sq * a.rt.gamma + a.rt.depth(r - sq * a.rt.Rs) - 1;
+        const float* E = es + (t * NTE + n) * 1024;
+        const float* H = hs + t * 1024;
+        // value e2 (0..7) of group q sits in register 4q + e2 % 4 of lane c + 32 (e2 / 4)
+        auto sum = [&](int jbase, int e2) {
+            const int j = jbase + (e2 & 3), hi = 32 * (e2 >> 2);
+            return E[j * 64 + c + hi] + (has_h ? H[j * 64 + hr + hi] : 0.f);
+        };
+        if constexpr (EPI == kMlpEpiResidual) {
+            const int n0 = tile * 32 + 8 * q;
+            if (n0 >= a.Nout) continue;
+            const u32x4 hv = *reinterpret_cast<const u32x4*>(a.h + (size_t)hr * a.Nout + n0);
+            u32x4 o;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const float y0 = bf16_bits_to_f32(hv[p] & 0xffffu) + sum(4 * q, 2 * p);
+                const float y1 = bf16_bits_to_f32(hv[p] >> 16) + sum(4 * q, 2 * p + 1);
+                o[p] = f32_to_bf16_bits(y0) | (f32_to_bf16_bits(y1) << 16);
+            }
+            *reinterpret_cast<u32x4*>(a.out + (size_t)r * a.Nout + n0) = o;
+        } else {
+            // activation i0..i0+7 as bf16 hi/lo pairs interleaved by 8
+            const int i0 = EPI == kMlpEpiSwiGLU ? tile * 16 + 8 * q : tile * 32 + 8 * q;
+            if (i0 >= a.Nout) continue;
+            u32x4 hi4, lo4;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                uint32_t hb[2], lb[2];
+#pragma unroll
+                for (int z = 0; z < 2; ++z) {
+                    const int e2 = 2 * p + z;
+                    const float gv = sum(4 * q, e2);
+                    float av = gv / (1.0f + __expf(-gv));
+                    if constexpr (EPI == kMlpEpiSwiGLU) av *= sum(4 * q + 8, e2);   // up rows 16.. of the tile
+                    hb[z] = f32_to_bf16_bits(av);
+                    lb[z] = f32_to_bf16_bits(av - bf16_bits_to_f32(hb[z]));
+                }
+                hi4[p] = hb[0] | (hb[1] << 16);
+                lo4[p] = lb[0] | (lb[1] << 16);
+            }
+            uint16_t* o = a.out + (size_t)r * 2 * a.Nout + (size_t)(i0 >> 3) * 16;
+            *reinterpret_cast<u32x4*>(o) = hi4;
+            *reinterpret_cast<u32x4*>(o + 8) = lo4;
+        }
+    }
+}
+
+// wait until at most STEP * k of this wave's loads are outstanding, k < 16
+// (uniform), for the last chunks of a segment where fewer copies follow
+template <int STEP, int K = 0>
+__device__ __forceinline__ void wait_vmcnt_mult(int k) {
+    if constexpr (STEP * K <= 62 && K < 16) {
+        if (k == K) {
+            wait_vmcnt<STEP * K>();
+            return;
+        }
+        wait_vmcnt_mult<STEP, K + 1>(k);
+    } else {
+        wait_vmcnt<0>();
+    }
+}
+
+// Copy cursors of one segment: the next chunk (segment-relative) each copier
+// stream fills and its ring stage, and the stages the next chunk is read from.
+struct MlpCursor {
+    int wnext, wstage, xnext, xstage, rw, rx;
+};
+
+// One chunk of weights: copier cw's rows of every tile of the item.  One
+// workgroup alone reads a weight tile, so the copies are non-temporal (they
+// do not displace the activation rows every workgroup re-reads from L2).
+template <int TG>
+__device__ __forceinline__ void mlp_copy_w(const uint16_t* const (&wsrc)[TG][2], int chunk, unsigned char* st,
+                                           int wtile) {
+#pragma unroll
+    for (int t = 0; t < TG; ++t)
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) dma16(wsrc[t][hb] + 64 * chunk, st + t * wtile + hb * 1024, kCpolNt);
+}
+
+// One chunk of activations: h~ rows in the h phase, else the e-phase rows.
+template <int XPW_E, bool PAIRED>
+__device__ __forceinline__ void mlp_copy_x(const uint16_t* const (&hsrc)[2], const uint16_t* const (&esrc)[XPW_E],
+                                           bool hphase, int chunk, unsigned char* st) {
+    if (hphase) {
+#pragma unroll
+        for (int v = 0; v < 2; ++v) dma16(hsrc[v] + 64 * chunk, st + 2 * v * 1024, 0);
+    } else {
+#pragma unroll
+        for (int v = 0; v < XPW_E; ++v) dma16(esrc[v] + (long)(PAIRED ? 128 : 64) * chunk, st + 2 * v * 1024, 0);
+    }
+}
+
+// The start of step s: wait for this wave's copies of chunk s (a weight
+// copier has copied up to min(s + SW - 2, nsteps - 1), an activation
+// copier up to s + 1), meet the barrier, refill the stages chunk s - 1 freed.
+template <class T, int SW, int SX, bool PAIRED, int TG = T::TW * 2>
+__device__ __forceinline__ void mlp_step_begin(MlpCursor& cur, bool wcopier, int s, int nsteps, int c0, int nkh,
+                                               const uint16_t* const (&wsrc)[TG][2],
+                                               const uint16_t* const (&hsrc)[2],
+                                               const uint16_t* const (&esrc)[T::XPW_E], unsigned char* wbase,
+                                               unsigned char* xbase) {
+    if (wcopier) {
+        const int ahead = nsteps - 1 - s;
+        if (ahead >= SW - 2)
+            wait_vmcnt<T::WPW * (SW - 2)>();
+        else
+            wait_vmcnt_mult<T::WPW>(ahead);
+    } else if (s + 1 < nsteps) {
+        if (c0 + s + 1 < nkh)
+            wait_vmcnt<T::XPW_H>();
+        else
+            wait_vmcnt<T::XPW_E>();
+    } else {
+        wait_vmcnt<0>();
+    }
+    block_barrier();
+    if (wcopier) {
+        if (cur.wnext < nsteps) {
+            mlp_copy_w<TG>(wsrc, cur.wnext, wbase + cur.wstage * T::WSTAGE, T::WTILE);
+            ++cur.wnext;
+            cur.wstage = cur.wstage + 1 == SW ? 0 : cur.wstage + 1;
+        }
+    } else if (cur.xnext < nsteps) {
+        mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < nkh, cur.xnext, xbase + cur.xstage * T::XSTAGE);
+        ++cur.xnext;
+        cur.xstage = cur.xstage + 1 == SX ? 0 : cur.xstage + 1;
+    }
+}
+
+template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP, int EPI>
+__global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
+    using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
+    constexpr int TW = T::TW, NTW = T::NTW;
+    static_assert(SX == 3, "two activation chunks in flight");
+    extern __shared__ __align__(16) unsigned char dyn[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int nk = a.nkh + a.nke;
+    const GemmShape sh{a.Re, nk * 64, a.ntiles, a.items, 1, nk, a.G};
+    const int g = xcd_logical_id(blockIdx.x, gridDim.x);
+    const long long u_end = unit_start(sh, g + 1);
+    long long u = unit_start(sh, g);
+    // this lane's row and physical slot in a 1 KiB DMA block of 128-byte rows
+    const int lrow = lane >> 3, lslot = lane & 7;
+    // Waves 0-1 copy the weights, waves 2-3 the activations: a wave waits
+    // on its own copies only (s_waitcnt counts a wave's loads in issue
+    // order), so the activation waits, two chunks out, never hold up the
+    // weight stream, which runs SW - 1 chunks ahead.
+    const bool wcopier = wave < 2;
+    const int cw = wcopier ? wave : wave - 2;   // index among the copiers of its stream
+    // the wave's place in the 2 x 2 grid: weight tiles wa*TW.., activation tiles wb*NTW..
+    const int wa = wave & 1, wb = wave >> 1;
+    const int fr = lane & 31;
+
+    while (u < u_end) {
+        const int item = (int)(u / nk);
+        const int c0 = (int)(u - (long long)item * nk);
+        const int c1 = (int)min((long long)nk, u_end - (long long)item * nk);
+        const int nsteps = c1 - c0;
+
+        // ---- this lane's DMA sources, at chunk c0 of the segment
+        // weights: copier cw copies rows 16cw..16cw+15 of every tile (two 8-row blocks)
+        const uint16_t* wsrc[TG][2];
+#pragma unroll
+        for (int t = 0; t < TG; ++t)
+#pragma unroll
+            for (int hb = 0; hb < 2; ++hb) {
+                const int row = 16 * cw + 8 * hb + lrow;
+                const int tile = min(item * TG + t, a.ntiles - 1);
+                const uint16_t* base;
+                if constexpr (WMAP == kMlpWGateUp) {
+                    const int i = min(tile * 16 + (row & 15), a.N - 1);
+                    base = (row < 16 ? a.w : a.wu) + (size_t)i * a.Kw;
+                } else {
+                    base = a.w + (size_t)min(tile * 32 + row, a.N - 1) * a.Kw;
+                }
+                wsrc[t][hb] = base + 8 * (lslot ^ T::swz128(row)) + 64 * c0;
+            }
+        // h phase: 32 rows of h~ in four 8-row blocks, blocks cw and cw + 2
+        const uint16_t* hsrc[2];
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            const int row = 8 * (cw + 2 * v) + lrow;
+            hsrc[v] = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) +
+                                            8 * (lslot ^ T::swz128(row)) + 64 * c0
+                                      : nullptr;
+        }
+        // e phase: DMA instruction q = cw + 2v covers rows XRPI*q ..
+        const uint16_t* esrc[T::XPW_E];
+        const int ce0 = c0 - a.nkh;   // e chunk of the segment's first chunk (negative in the h phase)
+#pragma unroll
+        for (int v = 0; v < T::XPW_E; ++v) {
+            const int q = cw + 2 * v;
+            int row, ps;
+            if constexpr (PAIRED) {
+                row = 4 * q + (lane >> 4);
+                ps = (lane & 15) ^ T::swz256(row);
+            } else {
+                row = 8 * q + lrow;
+                ps = lslot ^ T::swz128(row);
+            }
+            esrc[v] = a.xe + (size_t)min(row, a.Re - 1) * a.lde + 8 * ps + (long)(PAIRED ? 128 : 64) * ce0;
+        }
+
+        // ---- copies: weights SW - 1 chunks ahead, activations SX - 1
+        MlpCursor cur{0, 0, 0, 0, 0, 0};
+        unsigned char* const wbase = dyn + (2 * cw) * 1024;
+        unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
+
+        f32x16 acc_h[TW], acc_e[TW][NTW];
+#pragma unroll
+        for (int t = 0; t < TW; ++t)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                acc_h[t][j] = 0.f;
+#pragma unroll
+                for (int n = 0; n < NTW; ++n) acc_e[t][n][j] = 0.f;
+            }
+
+        // prologue: weights of chunks 0 .. SW-2, activations of chunks 0 .. SX-2
+        if (wcopier) {
+            for (; cur.wnext < SW - 1 && cur.wnext < nsteps; ++cur.wnext)
+                mlp_copy_w<TG>(wsrc, cur.wnext, wbase + cur.wnext * T::WSTAGE, T::WTILE);
+            cur.wstage = cur.wnext % SW;
+        } else {
+            for (; cur.xnext < SX - 1 && cur.xnext < nsteps; ++cur.xnext)
+                mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < a.nkh, cur.xnext,
+                                             xbase + cur.xnext * T::XSTAGE);
+            cur.xstage = cur.xnext % SX;
+        }
+
+        // The two phases run in loops of their own: each updates only its own
+        // accumulators, so none of them is copied between iterations.  A step
+        // first waits for this wave's copies of chunk s and meets the barrier
+        // (every wave's copies of chunk s have landed; the stages of chunk
+        // s - 1 are free), then refills the freed stages.
+        const int nh = max(0, min(nsteps, a.nkh - c0));   // h-phase chunks of the segment
+        for (int s = 0; s < nh; ++s) {
+            mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
+            const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
+            const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
+            cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
+            cur.rx = cur.rx + 1 == SX ? 0 : cur.rx + 1;
+            // the single activation tile, sub-steps wb and wb + 2
+#pragma unroll
+            for (int qq = 0; qq < 2; ++qq) {
+                const int ls = 2 * (wb + 2 * qq) + (lane >> 5);
+                const u32x4 b = *reinterpret_cast<const u32x4*>(xt + fr * 128 + ((ls ^ T::swz128(fr)) << 4));
+#pragma unroll
+                for (int t = 0; t < TW; ++t) {
+                    const u32x4 af = *reinterpret_cast<const u32x4*>(wt + t * T::WTILE + fr * 128 +
+                                                                     ((ls ^ T::swz128(fr)) << 4));
+                    acc_h[t] = mfma_32x32x16_bf16(af, b, acc_h[t]);
+                }
+            }
+        }
+        for (int s = nh; s < nsteps; ++s) {
+            mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
+            const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
+            const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
+            cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
+            cur.rx = cur.rx + 1 == SX ? 0 : cur.rx + 1;
+            // activation tiles wb*NTW.. over every sub-step (NTE = 1: the
+            // single tile, sub-steps of parity wb)
+            constexpr int QSTEP = NTE >= 2 ? 1 : 2;
+#pragma unroll
+            for (int qq = 0; qq < T::QS / QSTEP; ++qq) {
+                const int q = NTE >= 2 ? qq : wb + 2 * qq;
+                u32x4 b[NTW], af[TW];
+#pragma unroll
+                for (int n = 0; n < NTW; ++n) {
+                    const int xr = 32 * (NTE >= 2 ? wb * NTW + n : 0) + fr;
+                    const int ls = 2 * q + (lane >> 5);
+                    if constexpr (PAIRED)
+                        b[n] = *reinterpret_cast<const u32x4*>(xt + xr * 256 + ((ls ^ T::swz256(xr)) << 4));
+                    else
+                        b[n] = *reinterpret_cast<const u32x4*>(xt + xr * 128 + ((ls ^ T::swz128(xr)) << 4));
+                }
+#pragma unroll
+                for (int t = 0; t < TW; ++t) {
+                    // paired: sub-step q takes hi (lanes 0-31) and lo (32-63) of weight slot q
+                    const int lw = PAIRED ? q : 2 * q + (lane >> 5);
+                    af[t] = *reinterpret_cast<const u32x4*>(wt + t * T::WTILE + fr * 128 + ((lw ^ T::swz128(fr)) << 4));
+                }
+#pragma unroll
+                for (int t = 0; t < TW; ++t)
+#pragma unroll
+                    for (int n = 0; n < NTW; ++n) acc_e[t][n] = mfma_32x32x16_bf16(af[t], b[n], acc_e[t][n]);
+            }
+        }
+        __syncthreads();   // every copy has landed and every ring read is done
+
+        // ---- the item's sums (tile t of wave grid column t / TW; waves that
+        // share a tile, along the activation tiles, add in wave order)
+        float* wsc = reinterpret_cast<float*>(dyn);   // [wave][TW][1 + NTW][1024]
+#pragma unroll
+        for (int t = 0; t < TW; ++t)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                wsc[((wave * TW + t) * (1 + NTW)) * 1024 + j * 64 + lane] = acc_h[t][j];
+#pragma unroll
+                for (int n = 0; n < NTW; ++n) wsc[((wave * TW + t) * (1 + NTW) + 1 + n) * 1024 + j * 64 + lane] = acc_e[t][n][j];
+            }
+        __syncthreads();
+        auto wslot = [&](int w, int tl, int part) { return wsc + ((w * TW + tl) * (1 + NTW) + part) * 1024; };
+        float hc[T::HC], ec[T::EC];
+#pragma unroll
+        for (int i = 0; i < T::HC; ++i) {
+            const int e = tid + 256 * i;   // [TG][1024]
+            const int t = e >> 10, f = e & 1023;
+            const int col = t / TW, tl = t % TW;
+            hc[i] = wslot(col, tl, 0)[f] + wslot(2 + col, tl, 0)[f];
+        }
+#pragma unroll
+        for (int i = 0; i < T::EC; ++i) {
+            const int e = tid + 256 * i;   // [TG][NTE][1024]
+            const int t = e / (NTE * 1024), n = (e >> 10) % NTE, f = e & 1023;
+            const int col = t / TW, tl = t % TW;
+            if constexpr (NTE >= 2)
+                ec[i] = wslot((n / NTW) * 2 + col, tl, 1 + n % NTW)[f];
+            else
+                ec[i] = wslot(col, tl, 1)[f] + wslot(2 + col, tl, 1)[f];
+        }
+        __syncthreads();   // the per-wave sums are read; their LDS takes the item's sums below
+
+        // ---- a cut item: store this piece (its phases only); the last to arrive sums them
+        const int gfirst = unit_owner(sh, (long long)item * nk);
+        const int npieces = unit_owner(sh, (long long)item * nk + nk - 1) - gfirst + 1;
+        float* csc = reinterpret_cast<float*>(dyn);   // [TG][1024] h, then [TG][NTE][1024] e
+        bool last = true;
+        if (npieces > 1) {
+            float* mine = a.partial + (size_t)piece_slot(sh, g, item) * T::PF;
+            if (c0 < a.nkh) {
+#pragma unroll
+                for (int i = 0; i < T::HC; ++i) store_coherent(mine + tid + 256 * i, hc[i]);
+            }
+            if (c1 > a.nkh) {
+#pragma unroll
+                for (int i = 0; i < T::EC; ++i) store_coherent(mine + T::HC * 256 + tid + 256 * i, ec[i]);
+            }
+            wait_memory();
+            __syncthreads();   // every thread's piece is stored
+            int* flag = reinterpret_cast<int*>(csc);
+            if (tid == 0)
+                flag[0] = __hip_atomic_fetch_add(a.counter + item, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                                  npieces - 1
+                              ? 1
+                              : 0;
+            __syncthreads();
+            last = flag[0] != 0;
+            __syncthreads();
+            if (last) {
+#pragma unroll
+                for (int i = 0; i < T::HC; ++i) hc[i] = 0.f;
+#pragma unroll
+                for (int i = 0; i < T::EC; ++i) ec[i] = 0.f;
+                const long long ib = (long long)item * nk;
+                for (int pc = 0; pc < npieces; ++pc) {
+                    // chunks [p0, p1) of the item held by piece pc
+                    const int gp = gfirst + pc;
+                    const int p0 = (int)max(0ll, unit_start(sh, gp) - ib);
+                    const int p1 = (int)min((long long)nk, unit_start(sh, gp + 1) - ib);
+                    const float* src = a.partial + (size_t)piece_slot(sh, gp, item) * T::PF;
+                    if (p0 < a.nkh) {
+                        float v[T::HC];
+#pragma unroll
+                        for (int i = 0; i < T::HC; ++i) v[i] = load_coherent(src + tid + 256 * i);
+#pragma unroll
+                        for (int i = 0; i < T::HC; ++i) hc[i] += v[i];
+                    }
+                    if (p1 > a.nkh) {
+                        float v[T::EC];
+#pragma unroll
+                        for (int i = 0; i < T::EC; ++i) v[i] = load_coherent(src + T::HC * 256 + tid + 256 * i);
+#pragma unroll
+                        for (int i = 0; i < T::EC; ++i) ec[i] += v[i];
+                    }
+                }
+            }
+        }
+        if (last) {
+#pragma unroll
+            for (int i = 0; i < T::HC; ++i) csc[tid + 256 * i] = hc[i];
+#pragma unroll
+            for (int i = 0; i < T::EC; ++i) csc[T::HC * 256 + tid + 256 * i] = ec[i];
+            __syncthreads();
+            mlp_dma_epilogue<TG, NTE, EPI>(a, item, csc, csc + T::HC * 256);
+        }
+        u = (long long)(item + 1) * nk;
+        if (u < u_end) __syncthreads();   // the epilogue's LDS use ends before the next item's copies land
+    }
+}
+
+}  // namespace tf

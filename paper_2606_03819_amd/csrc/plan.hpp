@@ -292,12 +292,71 @@ inline GemmPlan mlp_plan(int rows, int ntiles, int K, int wg_single) {
 }
 // gate/up over x = [h~ ; e~], K = 2d (3d for the bigram rows)
 inline GemmPlan gateup_plan(int rows, int K, int I) { return mlp_plan(rows, cdiv(I, 16), K, TF_MLP_WORKGROUPS); }
+// the gate alone (plain SiLU MLP): tiles of 32 gate rows
+inline GemmPlan silu_gate_plan(int rows, int K, int I) { return mlp_plan(rows, cdiv(I, 32), K, TF_MLP_WORKGROUPS); }
 // down projection over the activation's bf16 hi/lo pairs: K = 2I
 inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d, 32), 2 * I, TF_DOWN_WORKGROUPS); }
 // the linear approximator: [rows, 2d] x [d, 2d]^T
 inline GemmPlan linear_plan(int rows, int d) { return mlp_plan(rows, cdiv(d, 32), 2 * d, TF_DOWN_WORKGROUPS); }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The products of the AR approximator when one row block holds every
+// conditional row (mlp_dma.hpp): items of TG weight tiles over their whole
+// reduction range (an h phase of nkh and an e phase of nke 64-column
+// chunks), dealt out to G workgroups of at least kMlpDmaMinUnits chunks.
+// The input projections take four tiles per item, the down projection (its
+// activation rows twice as long: bf16 hi/lo pairs) two, so that one chunk
+// carries 16 MFMAs per wave and 8-16 KiB of weights: fewer, fatter chunks
+// than with one tile, whose per-chunk barrier and latencies otherwise set
+// the pace.
+#ifndef TF_MLP_DMA_TG_IN
+#define TF_MLP_DMA_TG_IN 4
+#endif
+#ifndef TF_MLP_DMA_TG_DOWN
+#define TF_MLP_DMA_TG_DOWN 2
+#endif
+constexpr int kMlpDmaMinUnits = 12;
+constexpr int kMlpDmaMaxRows = 128;    // conditional rows (four activation tiles)
+constexpr int kMlpDmaMaxStates = 32;   // drafter states (one activation tile)
+struct MlpDmaPlan {
+    int TG;       // weight tiles per item
+    int NTE;      // 32-row activation tiles of the e phase (1, 2 or 4)
+    int ntiles;   // 32-row weight tiles
+    int items, nkh, nke, G;
+    size_t part_floats() const { return (size_t)2 * G * TG * 1024 * (1 + NTE); }
+};
+inline bool mlp_dma_applies(bool bf16, int b, int gamma, int R, int d, int I, int ew) {
+    return bf16 && (long long)b * gamma <= kMlpDmaMaxStates && (long long)b * R <= kMlpDmaMaxRows && d % 64 == 0 &&
+           I % 64 == 0 && ew % 64 == 0;
+}
+inline MlpDmaPlan mlp_dma_plan(int rows, int ntiles, int nkh, int nke, int TG) {
+    MlpDmaPlan p;
+    p.TG = TG;
+    p.NTE = rows <= 32 ? 1 : (rows <= 64 ? 2 : 4);
+    p.ntiles = ntiles;
+    p.items = cdiv(ntiles, TG);
+    p.nkh = nkh;
+    p.nke = nke;
+    const long long U = (long long)p.items * (nkh + nke);
+    long long G = U / kMlpDmaMinUnits;
+    G = G < kNumCUs ? G : kNumCUs;
+    p.G = (int)(G < 1 ? 1 : G);
+    return p;
+}
+// gate/up (SwiGLU: tiles of 16 gate + 16 up rows) or the gate alone (the
+// plain SiLU MLP: tiles of 32 gate rows) over [h~ ; e~], e~ ew wide
+inline MlpDmaPlan mlp_dma_gate_plan(int rows, int d, int ew, int I, bool swiglu) {
+    return mlp_dma_plan(rows, swiglu ? cdiv(I, 16) : cdiv(I, 32), d / 64, ew / 64, TF_MLP_DMA_TG_IN);
+}
+// down projection over the activation's hi/lo pairs (no h phase)
+inline MlpDmaPlan mlp_dma_down_plan(int rows, int d, int I) {
+    return mlp_dma_plan(rows, cdiv(d, 32), 0, I / 64, TF_MLP_DMA_TG_DOWN);
+}
+// the linear approximator W_lin [d, 2d] over [h~ ; e~]
+inline MlpDmaPlan mlp_dma_linear_plan(int rows, int d) {
+    return mlp_dma_plan(rows, cdiv(d, 32), d / 64, d / 64, TF_MLP_DMA_TG_IN);
+}
 
 // Long (row, slice) lists for top-k lists of at least kLongListK entries
 // (bf16 kernels, while the merge's candidate buffer holds every entry).
@@ -346,12 +405,27 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     w.ncounters = 0;
     if (bf16) {
         const GemmPlan pg = gateup_plan(rows2, (1 + npre) * d, I), pd = down_plan(rows2, d, I),
-                       pl = linear_plan(rows2, d);
-        const size_t a = pg.fix_floats(), c = pd.fix_floats(), l = pl.fix_floats();
+                       pl = linear_plan(rows2, d), ps = silu_gate_plan(rows2, (1 + npre) * d, I);
+        const size_t a = pg.fix_floats(), c = pd.fix_floats(), l = pl.fix_floats(), sf = ps.fix_floats();
         mp = a > c ? a : c;
         mp = mp > l ? mp : l;
-        const size_t nc = pg.counter_ints() + pd.counter_ints();
-        w.ncounters = (int)(nc > pl.counter_ints() ? nc : pl.counter_ints());
+        mp = mp > sf ? mp : sf;
+        size_t nc = pg.counter_ints() + pd.counter_ints();
+        nc = nc > ps.counter_ints() + pd.counter_ints() ? nc : ps.counter_ints() + pd.counter_ints();
+        nc = nc > pl.counter_ints() ? nc : pl.counter_ints();
+        if (mlp_dma_applies(bf16, b, gamma, R, d, I, npre * d)) {
+            // either the SwiGLU or the SiLU gate plan (the SwiGLU one has more
+            // items), the down projection, the linear approximator
+            const MlpDmaPlan qg = mlp_dma_gate_plan(rows2, d, npre * d, I, true),
+                             qs = mlp_dma_gate_plan(rows2, d, npre * d, I, false), qd = mlp_dma_down_plan(rows2, d, I),
+                             ql = mlp_dma_linear_plan(rows2, d);
+            const size_t pf[] = {qg.part_floats(), qs.part_floats(), qd.part_floats(), ql.part_floats()};
+            for (size_t x : pf) mp = mp > x ? mp : x;
+            const size_t qc = (size_t)qg.items + qd.items;
+            nc = nc > qc ? nc : qc;
+            nc = nc > (size_t)ql.items ? nc : (size_t)ql.items;
+        }
+        w.ncounters = (int)nc;
     }
     w.mlp_part = off;
     off += align256(mp * 4);

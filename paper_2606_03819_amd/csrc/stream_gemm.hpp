@@ -709,6 +709,51 @@ struct EpiSwiGLU {
     }
 };
 
+// Plain SiLU activation (no up projection): a[r, i] = silu(g) for tiles of
+// 32 gate rows, written as bf16 hi/lo pairs interleaved by 8 like EpiSwiGLU.
+template <int WM, int NT>
+struct EpiSiLU {
+    uint16_t* out;   // [R, 2I]
+    int I;
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char*,
+                                          const GemmShape& sh) {
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt) {
+            const int tile = it.t0 + wave * WM + mt;
+            if (tile >= it.t1) continue;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int r = it.row0 + nt * 32 + (lane & 31);
+                if (r >= sh.R) continue;
+#pragma unroll
+                for (int jg = 0; jg < 4; ++jg) {
+                    const int i = tile * 32 + 8 * jg + 4 * (lane >> 5);
+                    if (i >= I) continue;
+                    uint32_t hi2[2], lo2[2];
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        uint32_t h[2], l[2];
+#pragma unroll
+                        for (int e = 0; e < 2; ++e) {
+                            const float g = acc[mt][nt][4 * jg + 2 * q + e];
+                            const float a = g / (1.0f + __expf(-g));
+                            h[e] = f32_to_bf16_bits(a);
+                            l[e] = f32_to_bf16_bits(a - bf16_bits_to_f32(h[e]));
+                        }
+                        hi2[q] = h[0] | (h[1] << 16);
+                        lo2[q] = l[0] | (l[1] << 16);
+                    }
+                    uint16_t* o = out + (size_t)r * 2 * I + (size_t)(i >> 3) * 16 + (i & 7);
+                    *reinterpret_cast<uint2*>(o) = uint2{hi2[0], hi2[1]};
+                    *reinterpret_cast<uint2*>(o + 8) = uint2{lo2[0], lo2[1]};
+                }
+            }
+        }
+    }
+};
+
 // Residual: h'[r, n] = bf16( h[seq, depth-1, n] + y[r, n] ).
 template <int WM, int NT>
 struct EpiResidual {

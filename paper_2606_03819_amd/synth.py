@@ -62,8 +62,9 @@ class Workload:
     weight_seed: int
     state_seed: int       # per-sequence seed = state_seed + s when b > 1
     description: str = ""
-    # "swiglu" (Eq. 1), "linear" (the w/ Linear ablation) or "2prev" (the
-    # w/ 2-prev ablation: SwiGLU on [h~; e~(prev1); e~(prev2)])
+    # "swiglu" (Eq. 1), "silu" (the plain two-layer SiLU MLP: no up
+    # projection), "linear" (the w/ Linear ablation) or "2prev" (the w/
+    # 2-prev ablation: SwiGLU on [h~; e~(prev1); e~(prev2)])
     approximator: str = "swiglu"
 
     @property
@@ -117,6 +118,9 @@ WORKLOADS: Dict[str, Workload] = {
                  "Qwen3-8B-shaped bf16, w/ 2-prev approximator (905 bigram rows)", "2prev"),
         Workload("qwen3-8b-shape-linear", 1, 4096, 151936, 16, 8, 32, 0, "bf16", 1.0, 3, 13,
                  "Qwen3-8B-shaped bf16, w/ Linear approximator", "linear"),
+        # the plain two-layer SiLU MLP (no up projection) in place of the SwiGLU
+        Workload("qwen3-8b-shape-silu", 1, 4096, 151936, 16, 8, 32, 4096, "bf16", 1.0, 3, 13,
+                 "Qwen3-8B-shaped bf16, plain SiLU MLP approximator", "silu"),
     ]
 }
 
@@ -143,8 +147,9 @@ def _normal(shape, std, g, device, dtype):
 
 
 def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> Dict[str, torch.Tensor]:
-    """Weights in draw order: LM head, embedding, gate, up, down (or, for the
-    linear approximator, W_lin [d, 2d] in their place), then gains.
+    """Weights in draw order: LM head, embedding, gate, up, down (no up for
+    the plain SiLU MLP; for the linear approximator, W_lin [d, 2d] in their
+    place), then gains.
 
     ``weight_std`` other than 0.02 is only used by tests that want sharper
     distributions on small shapes.
@@ -160,7 +165,8 @@ def make_weights(w: Workload, device="cpu", weight_std: float = WEIGHT_STD) -> D
     else:
         kin = 3 * w.d if w.approximator == "2prev" else 2 * w.d
         out["w_gate"] = _normal((w.I, kin), weight_std, g, device, dt)
-        out["w_up"] = _normal((w.I, kin), weight_std, g, device, dt)
+        if w.approximator != "silu":
+            out["w_up"] = _normal((w.I, kin), weight_std, g, device, dt)
         out["w_down"] = _normal((w.d, w.I), weight_std, g, device, dt)
     out["norm_h_gain"] = torch.ones(w.d, device=device, dtype=dt)
     out["norm_e_gain"] = torch.ones(w.d, device=device, dtype=dt)

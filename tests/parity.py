@@ -160,7 +160,7 @@ def _oracle_rows(o_in, w, topk_seq, s):
                                            o_in["norm_e_gain"], o_in["w_lin"], mirror_bf16=(w.dtype == "bf16"))
     else:
         hp = oracle.ar_approximator(o_in["h"][s], prev, depth, o_in["emb"], o_in["norm_h_gain"],
-                                    o_in["norm_e_gain"], o_in["w_gate"], o_in["w_up"], o_in["w_down"],
+                                    o_in["norm_e_gain"], o_in["w_gate"], o_in.get("w_up"), o_in["w_down"],
                                     mirror_bf16=(w.dtype == "bf16"))
     return oracle.conditional_stage(hp, o_in["lm_head"], w.topk2, w.inv_temperature, keep_full=True)
 

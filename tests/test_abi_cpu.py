@@ -67,11 +67,11 @@ def _marginal(timed=False, **over):
 
 @pytest.mark.parametrize("over,code", [
     (dict(h=None), INVALID), (dict(w=None), INVALID), (dict(idx=None), INVALID),
-    (dict(b=0), INVALID), (dict(gamma=0), INVALID), (dict(d=4090), INVALID), (dict(d=0), INVALID),
+    (dict(b=0), INVALID), (dict(gamma=0), INVALID), (dict(d=4090), UNSUPPORTED), (dict(d=0), INVALID),
     (dict(k=0), INVALID), (dict(k=151937), INVALID), (dict(k=2000), INVALID), (dict(V=0), INVALID),
     (dict(it=0.0), INVALID), (dict(it=-1.0), INVALID), (dict(it=float("inf")), INVALID),
-    (dict(it=float("nan")), INVALID), (dict(dt=5), INVALID), (dict(h=FAKE + 4), INVALID),
-    (dict(lp=FAKE + 2), INVALID), (dict(lse=FAKE + 1), INVALID), (dict(w=FAKE + 4), INVALID),
+    (dict(it=float("nan")), INVALID), (dict(dt=5), INVALID), (dict(h=FAKE + 4), UNSUPPORTED), (dict(h=FAKE + 1), INVALID),
+    (dict(lp=FAKE + 2), INVALID), (dict(lse=FAKE + 1), INVALID), (dict(w=FAKE + 4), UNSUPPORTED),
     (dict(ws=None), WORKSPACE), (dict(ws=FAKE + 8), WORKSPACE),
     (dict(wsb=1024), WORKSPACE),
 ])
@@ -93,13 +93,16 @@ def _expand(**over):
 
 @pytest.mark.parametrize("over,code", [
     (dict(h=None), INVALID), (dict(root=None), INVALID), (dict(topk=None), INVALID), (dict(emb=None), INVALID),
-    (dict(wg=None), INVALID), (dict(wu=None), INVALID), (dict(wd=None), INVALID), (dict(lm=None), INVALID),
-    (dict(ci=None), INVALID), (dict(cl=None), INVALID), (dict(I=0), INVALID), (dict(I=100), INVALID),
+    (dict(wg=None), INVALID), (dict(wd=None), INVALID), (dict(lm=None), INVALID),
+    (dict(ci=None), INVALID), (dict(cl=None), INVALID), (dict(I=0), INVALID), (dict(I=100), UNSUPPORTED),
     (dict(topk2=0), INVALID), (dict(topk2=151937), INVALID), (dict(topk2=2048), INVALID),
     (dict(eps=-1.0), INVALID), (dict(eps=float("nan")), INVALID), (dict(it=0.0), INVALID),
-    (dict(gh=FAKE + 2), INVALID), (dict(lse=FAKE + 2), INVALID), (dict(gamma=300), INVALID),
-    (dict(wd=FAKE + 4), INVALID), (dict(lm=FAKE + 8), INVALID), (dict(ci=FAKE + 1), INVALID),
+    (dict(gh=FAKE + 1), INVALID), (dict(lse=FAKE + 2), INVALID), (dict(gamma=300), INVALID),
+    (dict(wd=FAKE + 4), UNSUPPORTED), (dict(lm=FAKE + 8), UNSUPPORTED), (dict(ci=FAKE + 1), INVALID),
+    (dict(wd=FAKE + 1), INVALID), (dict(d=4090), UNSUPPORTED),
     (dict(ws=None), WORKSPACE), (dict(wsb=4096), WORKSPACE),
+    # no up projection (the plain SiLU MLP) is a valid request: the workspace check comes next
+    (dict(wu=None, wsb=4096), WORKSPACE), (dict(wu=None, wg=None), INVALID),
 ])
 def test_arapprox_expand_rejects(over, code):
     assert _expand(**over) == code
@@ -117,9 +120,10 @@ def _hidden(**over):
 
 @pytest.mark.parametrize("over,code", [
     (dict(h=None), INVALID), (dict(root=None), INVALID), (dict(topk=None), INVALID), (dict(emb=None), INVALID),
-    (dict(wg=None), INVALID), (dict(wu=None), INVALID), (dict(wd=None), INVALID), (dict(hp=None), INVALID),
-    (dict(hp=FAKE2 + 2), INVALID), (dict(I=24), INVALID), (dict(eps=float("inf")), INVALID),
-    (dict(k=0), INVALID), (dict(ws=None), WORKSPACE), (dict(wsb=100), WORKSPACE),
+    (dict(wg=None), INVALID), (dict(wd=None), INVALID), (dict(hp=None), INVALID),
+    (dict(hp=FAKE2 + 2), UNSUPPORTED), (dict(hp=FAKE2 + 1), INVALID), (dict(I=24), UNSUPPORTED),
+    (dict(eps=float("inf")), INVALID), (dict(k=0), INVALID), (dict(ws=None), WORKSPACE), (dict(wsb=100), WORKSPACE),
+    (dict(wu=None, wsb=100), WORKSPACE), (dict(wu=FAKE + 4), UNSUPPORTED), (dict(dt=F32, wu=FAKE + 2), INVALID),
 ])
 def test_arapprox_hidden_rejects(over, code):
     assert _hidden(**over) == code
@@ -136,9 +140,10 @@ def _linear(**over):
 
 @pytest.mark.parametrize("over,code", [
     (dict(h=None), INVALID), (dict(root=None), INVALID), (dict(topk=None), INVALID), (dict(emb=None), INVALID),
-    (dict(wl=None), INVALID), (dict(wl=FAKE + 8), INVALID), (dict(hp=None), INVALID), (dict(hp=FAKE2 + 2), INVALID),
-    (dict(d=24), INVALID), (dict(eps=float("inf")), INVALID), (dict(k=0), INVALID), (dict(k=2000), INVALID),
-    (dict(gamma=300), INVALID), (dict(dt=7), INVALID), (dict(gh=FAKE + 2), INVALID),
+    (dict(wl=None), INVALID), (dict(wl=FAKE + 8), UNSUPPORTED), (dict(hp=None), INVALID),
+    (dict(hp=FAKE2 + 2), UNSUPPORTED), (dict(d=24), UNSUPPORTED), (dict(d=-16), INVALID),
+    (dict(eps=float("inf")), INVALID), (dict(k=0), INVALID), (dict(k=2000), INVALID),
+    (dict(gamma=300), INVALID), (dict(dt=7), INVALID), (dict(gh=FAKE + 1), INVALID),
     (dict(ws=None), WORKSPACE), (dict(ws=FAKE + 8), WORKSPACE), (dict(wsb=100), WORKSPACE),
 ])
 def test_arapprox_linear_hidden_rejects(over, code):
@@ -168,8 +173,9 @@ def _hidden2(**over):
 
 @pytest.mark.parametrize("over,code", [
     (dict(h=None), INVALID), (dict(ctx=None), INVALID), (dict(ctx=FAKE + 2), INVALID), (dict(root=None), INVALID),
-    (dict(topk=None), INVALID), (dict(emb=None), INVALID), (dict(wg=None), INVALID), (dict(wu=FAKE + 8), INVALID),
-    (dict(hp=None), INVALID), (dict(I=24), INVALID), (dict(k=0), INVALID), (dict(gamma=256), INVALID),
+    (dict(topk=None), INVALID), (dict(emb=None), INVALID), (dict(wg=None), INVALID), (dict(wu=FAKE + 8), UNSUPPORTED),
+    (dict(wu=None), INVALID), (dict(hp=None), INVALID), (dict(I=24), UNSUPPORTED), (dict(k=0), INVALID),
+    (dict(gamma=256), INVALID),
     # 32 * (1 + 64 + 14 * 64 * 64) bigram rows exceed the 2^20 row limit
     (dict(b=32, k=64), INVALID),
     (dict(ws=None), WORKSPACE), (dict(wsb=4096), WORKSPACE),

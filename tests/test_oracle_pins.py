@@ -118,6 +118,41 @@ def pin_ar_closed_form(rng, d=12, mirror=False):
     return ok and bool(np.allclose(got, want.numpy(), rtol=1e-13, atol=1e-13 + tol))
 
 
+def pin_silu_mlp_closed_form(rng, d=20, mirror=False):
+    """Without W_up (the plain SiLU MLP side mode): with W_gate = [P | c I]
+    (P a permutation) and a diagonal W_down = diag(s), every row is
+    h' = h + s * silu(P h~ + c e~); checked against torch's rms_norm and
+    silu, also with the bf16 rounding points."""
+    V, gamma, M = 11, 4, 2
+    perm = rng.permutation(d)
+    c = 0.75
+    w_gate = np.concatenate([_perm_matrix(perm), c * np.eye(d)], axis=1)
+    sc = rng.uniform(-1.5, 1.5, d)
+    w_down = np.diag(sc)
+    h = rng.standard_normal((gamma, d)) * 1.5
+    emb = rng.standard_normal((V, d)) * 0.05
+    gh = rng.uniform(0.5, 1.5, d)
+    ge = rng.uniform(0.5, 1.5, d)
+    if mirror:
+        h = oracle.bf16_round(h)
+    topk = np.array([[3, 9], [10, 0], [6, 2], [1, 4]])
+    depth, _ = oracle.row_table(gamma, M)
+    prev = oracle.previous_tokens(8, topk, gamma, M)
+    got = oracle.ar_approximator(h, prev, depth, emb, gh, ge, w_gate, None, w_down, eps=1e-6, mirror_bf16=mirror)
+    th = torch.from_numpy(h[depth - 1])
+    hn = F.rms_norm(th, (d,), torch.from_numpy(gh), eps=1e-6)
+    en = F.rms_norm(torch.from_numpy(emb[prev]), (d,), torch.from_numpy(ge), eps=1e-6)
+    if mirror:
+        hn = hn.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+        en = en.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    want = th + F.silu(hn[:, perm] + c * en) * torch.from_numpy(sc)
+    if mirror:
+        want = want.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+        ulp = np.abs(want.numpy()) * 2.0 ** -7 + 1e-30
+        return bool(np.all(np.abs(got - want.numpy()) <= ulp))
+    return bool(np.allclose(got, want.numpy(), rtol=1e-13, atol=1e-13))
+
+
 def pin_zero_down(rng, mirror=True):
     """Zero-initialised AR approximator reproduces the drafter (Training paragraph)."""
     V, d, gamma, M = 30, 16, 4, 3
@@ -165,7 +200,7 @@ def pin_uniform_head(rng):
 
 
 ALL_PINS = [pin_uniform_head, pin_bf16_round, pin_rms_norm, pin_silu, pin_marginal_permuted_identity,
-            pin_ar_closed_form, pin_zero_down, pin_row_table, pin_rows_sum_to_one]
+            pin_ar_closed_form, pin_silu_mlp_closed_form, pin_zero_down, pin_row_table, pin_rows_sum_to_one]
 
 
 # ------------------------------------------------------------------- tests
@@ -183,6 +218,22 @@ def test_bf16_round_known_values():
 
 def test_ar_closed_form_mirror():
     assert pin_ar_closed_form(np.random.default_rng(7), mirror=True)
+
+
+def test_silu_mlp_closed_form_mirror():
+    assert pin_silu_mlp_closed_form(np.random.default_rng(8), mirror=True)
+
+
+def test_silu_mlp_zero_down_keeps_the_state():
+    rng = np.random.default_rng(9)
+    V, d, gamma, M = 25, 16, 3, 2
+    h = oracle.bf16_round(rng.standard_normal((gamma, d)))
+    topk = np.stack([rng.permutation(V)[:M] for _ in range(gamma)])
+    depth, _ = oracle.row_table(gamma, M)
+    prev = oracle.previous_tokens(4, topk, gamma, M)
+    hp = oracle.ar_approximator(h, prev, depth, rng.standard_normal((V, d)), np.ones(d), np.ones(d),
+                                rng.standard_normal((d, 2 * d)), None, np.zeros((d, d)), mirror_bf16=True)
+    assert np.array_equal(hp, h[depth - 1])
 
 
 def test_topk_tie_rule():
@@ -272,7 +323,21 @@ def _marginal_transposed(h, lm_head, k, inv_temperature=1.0):
             "topk_logprob": np.take_along_axis(lp, idx, axis=-1)}
 
 
+def _ar_silu_gate_squared(h_seq, prev, depth, emb, gh, ge, wg, wu, wd, eps=1e-6, mirror_bf16=False):
+    # without an up projection, multiplies the activation by the gate again
+    hd = np.asarray(h_seq, dtype=np.float64)[np.asarray(depth) - 1]
+    e = np.asarray(emb, dtype=np.float64)[np.asarray(prev)]
+    x = np.concatenate([ot.rms_norm(hd, gh, eps), ot.rms_norm(e, ge, eps)], axis=-1)
+    if mirror_bf16:
+        x = ot.bf16_round(x)
+    g = x @ np.asarray(wg).T
+    a = ot.silu(g) * (x @ np.asarray(wu).T if wu is not None else g)
+    out = hd + a @ np.asarray(wd).T
+    return ot.bf16_round(out) if mirror_bf16 else out
+
+
 MUTATIONS.update({
+    "silu_mode_gate_squared": ("ar_approximator", _ar_silu_gate_squared),
     "prev_from_same_depth": ("previous_tokens", _prev_wrong_depth),
     "concat_halves_swapped": ("ar_approximator", _ar_swapped_halves),
     "residual_dropped": ("ar_approximator", _ar_no_residual),
