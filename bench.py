@@ -103,6 +103,8 @@ def parse():
     ap.add_argument("--workload", default="qwen3-8b-shape", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--copies", type=int, default=4, help="independent weight copies rotated per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time only the headline workload (not the other four benchmark workloads)")
     ap.add_argument("--cpu-seconds", type=float, default=30.0, help="rough cap on the CPU baseline's work")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, copy 1 GiB three times (torch.neg, read 1 GiB + write 1 GiB) "
@@ -131,25 +133,49 @@ def make_copies(w, n):
     return copies, {k: v.to(dev) for k, v in states.items()}
 
 
-def cpu_baseline(w, weights, states, budget_s):
-    """The oracle, untuned, on one sequence's full step (one draft tree)."""
+def host_cpu():
+    """(usable host cores, CPU model name)."""
+    cores = len(os.sched_getaffinity(0))
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, model
+
+
+def cpu_baseline(w, weights, states, budget_s, repeats=3):
+    """The oracle, untuned, on one sequence's full step (one draft tree), with
+    BLAS threads = every usable host core; the median of `repeats` runs (fewer
+    when one run takes more than a third of `budget_s`)."""
     import numpy as np
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
     import oracle
 
+    cores, model = host_cpu()
     inputs = {k: synth.to_numpy64(v) for k, v in weights.items()}
     inputs["h"] = synth.to_numpy64(states["h"][:1])
     inputs["root"] = synth.to_numpy64(states["root"][:1])
     inputs["context"] = synth.to_numpy64(states["context"][:1])
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     draft = oracle.draft_2prev if w.approximator == "2prev" else oracle.draft
-    t0 = time.perf_counter()
-    draft(inputs, w.gamma, w.k, w.B, w.inv_temperature, mirror_bf16=(w.dtype == "bf16"))
-    dt = time.perf_counter() - t0
+    times = []
+    with threadpool_limits(limits=cores):
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        for _ in range(repeats):
+            t0 = time.perf_counter()
+            draft(inputs, w.gamma, w.k, w.B, w.inv_temperature, mirror_bf16=(w.dtype == "bf16"))
+            times.append(time.perf_counter() - t0)
+            if sum(times) > budget_s or times[0] > budget_s / 3:
+                break
+    dt = sorted(times)[len(times) // 2]
     return {"value": 1.0 / dt, "unit": "trees/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"one sequence's full drafting step (stage 1, {w.rows} conditional rows, tree); "
-                      f"{dt:.2f} s in NumPy float64 on this host",
-            "seconds": dt}
+            "sample": f"one sequence's full drafting step (stage 1, {w.rows} conditional rows, tree) of "
+                      f"{w.name}; median of {len(times)} run(s), {dt:.2f} s each in NumPy float64",
+            "seconds": dt, "runs": len(times), "host_cores": cores, "cpu_model": model}
 
 
 def _db(path):
@@ -281,8 +307,9 @@ def make_drafter(w, weights):
 
 
 def approx_hidden(wt, h, root, context, topk_idx, workspace, hp, V):
-    """Stage 2's first half: Eq. 1's SwiGLU, the w/ Linear layer when the weights
-    hold one, or the w/ 2-prev SwiGLU when gate/up read three d-blocks."""
+    """Stage 2's first half: Eq. 1's SwiGLU (the plain SiLU MLP without an up
+    projection), the w/ Linear layer when the weights hold one, or the w/
+    2-prev SwiGLU when gate/up read three d-blocks."""
     d = h.shape[2]
     if "w_lin" in wt:
         binding.treeflash_arapprox_linear_hidden(h, root, topk_idx, wt["emb"], wt["norm_h_gain"],
@@ -293,7 +320,7 @@ def approx_hidden(wt, h, root, context, topk_idx, workspace, hp, V):
                                                 workspace, hp, V)
     else:
         binding.treeflash_arapprox_hidden(h, root, topk_idx, wt["emb"], wt["norm_h_gain"], wt["norm_e_gain"],
-                                          wt["w_gate"], wt["w_up"], wt["w_down"], 1e-6, workspace, hp, V)
+                                          wt["w_gate"], wt.get("w_up"), wt["w_down"], 1e-6, workspace, hp, V)
 
 
 def build_tree(w, dr):
@@ -367,31 +394,77 @@ def sweep(args):
           flush=True)
 
 
-def main():
-    args = parse()
-    if args.summarize_trace:
-        summarize_trace(args)
-        return
-    if args.summarize_mfma:
-        summarize_mfma(args)
-        return
-    if args.summarize_pmc:
-        summarize_pmc(args)
-        return
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
-    if not torch.cuda.is_available():
-        print(json.dumps({"error": "no GPU visible"}))
-        sys.exit(2)
-    torch.cuda.set_device(0)
-    binding.lib()
-    if args.sweep:
-        sweep(args)
-        return
-    w = synth.get_workload(args.workload)
-    copies, st = make_copies(w, max(1, args.copies))
+def mlp_weight_bytes(w):
+    """Bytes of the AR approximator's weights (read once per step)."""
+    es = 2 if w.dtype == "bf16" else 4
+    d, I = w.d, w.I
+    kin = 3 * d if w.approximator == "2prev" else 2 * d
+    if w.approximator == "linear":
+        return 2 * d * d * es
+    nin = 1 if w.approximator == "silu" else 2      # gate (and up) projections
+    return (nin * I * kin + d * I) * es
+
+
+def mlp_flops(w):
+    """Algorithmic FLOPs of the AR approximator: the h~ half of the input
+    projections once per drafter state (b * gamma), the rest per conditional row."""
+    d, I = w.d, w.I
+    states, rows = w.b * w.gamma, w.b * w.rows
+    ew = 2 * d if w.approximator == "2prev" else d
+    if w.approximator == "linear":
+        return 2.0 * d * d * states + 2.0 * d * d * rows
+    nin = 1 if w.approximator == "silu" else 2
+    return 2.0 * nin * I * (d * states + ew * rows) + 2.0 * d * I * rows
+
+
+def stage_roofline(w, stage_us):
+    """The treeflash_arapprox_expand stage (gather + norms, the approximator,
+    the stage-2 LM head with log-softmax and top-K2): algorithmic bytes and
+    FLOPs against its measured time (the evented pass: AR approximator +
+    stage-2 LM head and merge)."""
+    es = 2 if w.dtype == "bf16" else 4
+    rows = w.b * w.rows
+    npre = 2 if w.approximator == "2prev" else 1
+    nbytes = (mlp_weight_bytes(w) + rows * npre * w.d * es + w.b * w.gamma * w.d * es
+              + w.V * w.d * es + rows * w.d * es)
+    flops = mlp_flops(w) + 2.0 * rows * w.V * w.d
+    t = (stage_us["arapprox_mlp"] + stage_us["stage2_lmhead_topk"]) * 1e-6
+    peak_f = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
+    t_ideal = max(nbytes / (HBM_PEAK_GBS * 1e9), flops / (peak_f * 1e12))
+    return {"us": t * 1e6, "alg_bytes": nbytes, "alg_flops": flops,
+            "hbm_frac": nbytes / t / 1e9 / HBM_PEAK_GBS, "mfma_frac": flops / t / 1e12 / peak_f,
+            "frac": t_ideal / t, "bound": "hbm" if nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (peak_f * 1e12) else "mfma"}
+
+
+def lm_roofline(w, gemm):
+    """Roofline of the dominant kernel, the stage-2 LM-head GEMM (the per-row
+    merge is a separate kernel); algorithmic bytes per launch: lm_head [V, d]
+    once plus the activation rows h' [rows, d]."""
+    es = 2 if w.dtype == "bf16" else 4
+    rows, V, d = w.b * w.rows, w.V, w.d
+    t_lm = gemm["mean"] * 1e-6
+    alg_bytes = V * d * es + rows * d * es
+    alg_flops = 2.0 * rows * V * d
+    if w.dtype == "bf16" and rows > RIDGE:
+        roof = {"bound": "mfma", "achieved": alg_flops / t_lm / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = read_traffic(w.name)
+    roof["kernel"] = ("stage-2 LM head on h': " + lm_kernel_pattern(rows, d).split("<")[0]) if w.dtype == "bf16" \
+        else "stage-2 LM head on h': lmhead_f32_kernel"
+    roof["kernel_us"] = gemm
+    roof["alg_bytes_per_launch"] = alg_bytes
+    roof["alg_flops_per_launch"] = alg_flops
+    roof["hbm_frac"] = alg_bytes / t_lm / 1e9 / HBM_PEAK_GBS
+    roof["mfma_frac"] = alg_flops / t_lm / 1e12 / BF16_PEAK_TFLOPS
+    return roof
+
+
+def measure(w, copies, st, steps, warmup, copy_calibration=False):
+    """Timed drafting steps of workload w (only the two events around the
+    stage-2 LM-head kernel inside the timed region), then an untimed pass with
+    events between the calls for the per-stage split."""
     dev = torch.device("cuda", 0)
     d, V, R, b = w.d, w.V, w.rows, w.b
     dr = make_drafter(w, copies[0])
@@ -421,21 +494,21 @@ def main():
     def make_events():
         # events 0..4 bracket the four calls; 5, 6 bracket the stage-2 LM-head GEMM kernel
         # (recorded inside the library on this stream); recording once creates them
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
         for e in evs:
             for x in e:
                 x.record()
         torch.cuda.synchronize()
         return evs
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     # timed steps: only the two events around the stage-2 LM-head kernel (an event
     # on the stream leaves a few microseconds of idle GPU), for its live duration
     evs = make_events()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         step(i, evs[i])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -443,18 +516,14 @@ def main():
 
     # per-stage split from a second, untimed pass with events between the calls
     sevs = make_events()
-    for i in range(args.steps):
+    for i in range(steps):
         step(i, sevs[i], stages=True)
     torch.cuda.synchronize()
-    stage_ms = {"stage1_lmhead_topk": 0.0, "arapprox_mlp": 0.0, "stage2_lmhead_topk": 0.0, "tree": 0.0}
-    names = list(stage_ms)
-    for e in sevs:
-        for j, n in enumerate(names):
-            stage_ms[n] += e[j].elapsed_time(e[j + 1])
-    stage_us = {n: 1000.0 * v / args.steps for n, v in stage_ms.items()}
+    names = ["stage1_lmhead_topk", "arapprox_mlp", "stage2_lmhead_topk", "tree"]
+    stage_us = {n: 1000.0 * sum(e[j].elapsed_time(e[j + 1]) for e in sevs) / steps for j, n in enumerate(names)}
     gemm = {"mean": sum(gemm_us) / len(gemm_us), "median": gemm_us[len(gemm_us) // 2],
             "p10": gemm_us[len(gemm_us) // 10], "p90": gemm_us[(9 * len(gemm_us)) // 10]}
-    if args.copy_calibration:
+    if copy_calibration:
         # an elementwise kernel that reads COPY_BYTES and writes COPY_BYTES (torch's
         # same-dtype copy_ goes to the runtime's blit kernel, shared with other copies)
         a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -463,9 +532,74 @@ def main():
             torch.neg(a, out=c)
         torch.cuda.synchronize()
         del a, c
+    return {"elapsed_s": elapsed, "stage_us": stage_us, "lm_kernel_us": gemm, "drafter": dr}
+
+
+# The other workloads of the benchmark's five (the headline one is timed above).
+OTHER_CONFIGS = ["tiny-f32", "qwen3-4b-shape", "qwen3-8b-shape-k16-b64", "qwen3-8b-shape-batch16"]
+
+
+def other_configs(headline, args):
+    """Throughput, the dominant kernel's roofline and the a2-a4 stage fraction of
+    every other workload (fewer steps: the headline line is the one the metric
+    is quoted on)."""
+    out = {}
+    steps, warmup = max(5, args.steps // 2), max(2, args.warmup // 2)
+    for name in OTHER_CONFIGS:
+        if name == headline:
+            continue
+        w = synth.get_workload(name)
+        copies, st = make_copies(w, max(1, args.copies))
+        m = measure(w, copies, st, steps, warmup)
+        roof = lm_roofline(w, m["lm_kernel_us"])
+        out[name] = {"trees_per_s": w.b * steps / m["elapsed_s"],
+                     "rows_per_s": w.b * w.rows * steps / m["elapsed_s"],
+                     "ms_per_step": 1000.0 * m["elapsed_s"] / steps, "steps": steps, "warmup": warmup,
+                     "stage_us": m["stage_us"],
+                     "stage2_lm_kernel": {k: roof[k] for k in ("bound", "achieved", "peak", "unit", "frac",
+                                                               "hbm_frac", "mfma_frac", "kernel_us")},
+                     "arapprox_expand_stage": stage_roofline(w, m["stage_us"])}
+        del m, copies, st
+        torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    args = parse()
+    if args.summarize_trace:
+        summarize_trace(args)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    binding.lib()
+    if args.sweep:
+        sweep(args)
+        return
+    w = synth.get_workload(args.workload)
+    copies, st = make_copies(w, max(1, args.copies))
+    dev = torch.device("cuda", 0)
+    d, V, R, b = w.d, w.V, w.rows, w.b
+    h, root, context = st["h"], st["root"], st["context"]
+    m = measure(w, copies, st, args.steps, args.warmup, args.copy_calibration)
+    dr = m.pop("drafter")
+    elapsed = m["elapsed_s"]
     ms_per_step = 1000.0 * elapsed / args.steps
     trees_per_s = b * args.steps / elapsed
     rows = b * R
+    stage_us = m["stage_us"]
+    gemm = m["lm_kernel_us"]
 
     # verification hand-off on the last step's trees: tree-attention inputs and the
     # acceptance walk for a synthetic verifier that agrees with the drafter's best
@@ -516,30 +650,9 @@ def main():
               "K": md.K, "what": "stage 1 with K = min(B, V) entries per depth + marginal OPT-Tree"}
     del md
 
-    # dominant kernel: the stage-2 LM-head GEMM (the per-row merge is a separate kernel);
-    # algorithmic bytes per launch: lm_head [V, d] once plus the activation rows h' [rows, d]
+    roof = lm_roofline(w, gemm)
     es = 2 if w.dtype == "bf16" else 4
-    t_lm = gemm["mean"] * 1e-6
-    alg_bytes = V * d * es + rows * d * es
-    alg_flops = 2.0 * rows * V * d
-    if w.dtype == "bf16" and rows > RIDGE:
-        roof = {"bound": "mfma", "achieved": alg_flops / t_lm / 1e12, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": alg_bytes / t_lm / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = read_traffic(w.name)
-    roof["kernel"] = ("stage-2 LM head on h': " + lm_kernel_pattern(rows, d).split("<")[0]) if w.dtype == "bf16" \
-        else "stage-2 LM head on h': lmhead_f32_kernel"
-    roof["kernel_us"] = gemm
-    roof["alg_bytes_per_launch"] = alg_bytes
-    roof["alg_flops_per_launch"] = alg_flops
-    roof["hbm_frac"] = alg_bytes / t_lm / 1e9 / HBM_PEAK_GBS
-    roof["mfma_frac"] = alg_flops / t_lm / 1e12 / BF16_PEAK_TFLOPS
-
-    # whole-step roofline context
-    kin = 3 * d if w.approximator == "2prev" else 2 * d
-    mlp_bytes = (2 * d * d if w.approximator == "linear" else 2 * w.I * kin + d * w.I) * es
-    step_bytes = 2 * V * d * es + mlp_bytes
+    step_bytes = 2 * V * d * es + mlp_weight_bytes(w)
     out = {
         "metric": METRIC, "value": trees_per_s, "unit": "trees/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
@@ -551,11 +664,15 @@ def main():
         "stage_us": stage_us,
         "step_hbm_frac": step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": roof,
+        "arapprox_expand_stage": stage_roofline(w, stage_us),
         "ddtree_baseline": ddtree,
         "verify_handoff": handoff,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, copies[0], st, args.cpu_seconds)
+    del dr, copies, st
+    if not args.no_configs:
+        out["configs"] = other_configs(w.name, args)
     print(json.dumps(out), flush=True)
 
 

@@ -5,7 +5,7 @@
 
 #include <initializer_list>
 
-#include "../../include/treeflash.h"
+#include "treeflash.h"
 #include "launch.hpp"
 #include "plan.hpp"
 

@@ -933,11 +933,9 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
                                    const GemmShape& sh, int V, float sl2, float* part, int* diag, hipStream_t st) {
     const int nb = p.blocks();
     if (p.dma) {   // the shapes the plans use (see lm_plan)
-#if TF_LM_DMA_NT1
         if (p.NT == 1)
             return launch_lm_dma<LONG, TF_LM_DMA_NT1_WM, 1, TF_LM_DMA_NT1_NW, TF_LM_DMA_KC, true>(x, ldx, w, sh, p.map, nb,
                                                                                             V, sl2, part, diag, st);
-#endif
         if (p.grid && p.NT == 2)   // 33..64 rows: one activation tile per wave of the grid
             return launch_lm_dma<LONG, TF_LM_DMA_WM, 2, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, true, 1, TF_LM_DMA_SINGLE_WB>(
                 x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
@@ -947,14 +945,9 @@ static hipError_t dispatch_lm_bf16(const LmPlan& p, const uint16_t* x, long ldx,
         if (p.grid)   // a few row blocks sharing each range's weights through L2
             return launch_lm_dma<LONG, TF_LM_DMA_WM, 4, TF_LM_DMA_NW_SINGLE, TF_LM_DMA_KC, false, 1, TF_LM_DMA_SINGLE_WB>(
                 x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
-#if TF_LM_MULTI_NT8
-        if (p.NT == 8)
-            return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 8, 8, TF_LM_DMA_MULTI_KC, false, 1, 2>(
-                x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
-#endif
-        return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 4, TF_LM_DMA_NW, TF_LM_DMA_MULTI_KC, false,
-                             TF_LM_DMA_MULTI_MINB>(
-            x, ldx, w, sh, p.map, nb, V, sl2, part, diag, st);
+        // several row blocks: 256-row blocks (lm_plan)
+        return launch_lm_dma<LONG, TF_LM_DMA_MULTI_WM, 8, 8, TF_LM_DMA_KC, false, 1, 2>(x, ldx, w, sh, p.map, nb, V,
+                                                                                    sl2, part, diag, st);
     }
     if (p.NT == 1)
         launch_lm_bf16<LONG, TF_LM_WM_NT1, 1, TF_LM_NW_NT1, TF_PIPE_DEFAULT, true>(x, ldx, w, sh, p.map, nb, V, sl2, part,

@@ -287,30 +287,22 @@ static void launch_down(const uint16_t* h, const uint16_t* wd, const uint16_t* a
 }
 
 // Both products share the row blocking (same rows); each plan picks its own
-// waves per workgroup.  The pipeline depth and the non-temporal weight loads
-// follow the plan's single-row-block choice.
+// waves per workgroup.
 template <int WM, int NT>
 static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
                             const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
                             int ew, int I, const RowTable& rt, const GemmPlan& pg, const GemmPlan& pd,
                             float* partial, int* counters, hipStream_t st) {
-    constexpr int S = TF_NW_SINGLE;
-    constexpr int PS = NT == 4 ? TF_PIPE_SINGLE_NT4 : TF_PIPE_DEFAULT;
+    constexpr int S = TF_NW_SINGLE, P = TF_PIPE_DEFAULT;
     if (pg.NW != S)
-        launch_gateup<WM, NT, TF_NW, TF_PIPE_DEFAULT, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial,
-                                                             counters, st);
-    else if (pg.wnt)
-        launch_gateup<WM, NT, S, PS, true>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial, counters, st);
+        launch_gateup<WM, NT, TF_NW, P, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial, counters, st);
     else
-        launch_gateup<WM, NT, S, TF_PIPE_DEFAULT, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial,
-                                                         counters, st);
+        launch_gateup<WM, NT, S, P, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial, counters, st);
     int* cd = counters + pg.counter_ints();
     if (pd.NW != S)
-        launch_down<WM, NT, TF_NW, TF_PIPE_DEFAULT, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
-    else if (pd.wnt)
-        launch_down<WM, NT, S, PS, true>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
+        launch_down<WM, NT, TF_NW, P, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
     else
-        launch_down<WM, NT, S, TF_PIPE_DEFAULT, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
+        launch_down<WM, NT, S, P, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
 }
 
 static bool aligned16p(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }

@@ -53,9 +53,6 @@ constexpr int kNumCUs = 256;           // compute units of an MI355X
 #ifndef TF_PIPE_DEFAULT
 #define TF_PIPE_DEFAULT 2
 #endif
-#ifndef TF_MLP_WNT
-#define TF_MLP_WNT 0
-#endif
 
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
@@ -176,34 +173,15 @@ struct LmPlan {
 #ifndef TF_LM_GRID_NRB
 #define TF_LM_GRID_NRB 2
 #endif
-// waves of the DMA kernel for several row blocks (MFMA-bound: one wave per SIMD)
-#ifndef TF_LM_DMA_NW
-#define TF_LM_DMA_NW 4
-#endif
-// Several row blocks (MFMA-bound).  Default: 256-row blocks of eight waves
-// in a 4 x 2 grid, one workgroup per CU.  Each copied weight tile then meets
-// 256 activation rows and each copied activation tile 8 weight tiles: 0.5
-// KiB of copies per 32 x 32 tile pair of MFMA work against 0.75 KiB with
-// 128-row blocks (+6% on the 1936-row batched step); 64-wide k steps fill
-// the 160 KiB of LDS (+1.5% against 32-wide).  With TF_LM_MULTI_NT8 = 0:
-// 128-row blocks of four waves at 32-wide steps (64 KiB rings), two
-// workgroups per CU, so one's barrier and fragment waits hide behind the
-// other's MFMAs.
-#ifndef TF_LM_MULTI_NT8
-#define TF_LM_MULTI_NT8 1
-#endif
+// Several row blocks (MFMA-bound): 256-row blocks of eight waves in a 4 x 2
+// grid (2 weight x 4 activation tiles each), one workgroup per CU.  Each
+// copied weight tile then meets 256 activation rows and each copied
+// activation tile 8 weight tiles: 0.5 KiB of copies per 32 x 32 tile pair of
+// MFMA work against 0.75 KiB with 128-row blocks of four waves (+6% on the
+// 1936-row batched step); 64-wide k steps fill the 160 KiB of LDS (+1.5%
+// against 32-wide).
 #ifndef TF_LM_DMA_MULTI_WM
 #define TF_LM_DMA_MULTI_WM 2
-#endif
-#ifndef TF_LM_DMA_MULTI_KC
-#if TF_LM_MULTI_NT8
-#define TF_LM_DMA_MULTI_KC 64
-#else
-#define TF_LM_DMA_MULTI_KC 32
-#endif
-#endif
-#ifndef TF_LM_DMA_MULTI_MINB
-#define TF_LM_DMA_MULTI_MINB 2
 #endif
 #ifndef TF_LM_DMA_KC
 #define TF_LM_DMA_KC 64
@@ -211,15 +189,9 @@ struct LmPlan {
 #ifndef TF_LM_DMA_STAGES
 #define TF_LM_DMA_STAGES 3
 #endif
-#ifndef TF_LM_DMA
-#define TF_LM_DMA 1
-#endif
-// the DMA kernel for 32-row tiles too (stage 1): four waves of three tiles
-// (twelve per round, two rounds per range, 152 KiB of rings), about 1% faster
-// per step than the register-staged kernel at the 8B shape
-#ifndef TF_LM_DMA_NT1
-#define TF_LM_DMA_NT1 1
-#endif
+// 32-row tiles (stage 1): four waves of three tiles (twelve per round, two
+// rounds per range, 152 KiB of rings), about 1% faster per step than the
+// register-staged kernel at the 8B shape
 #ifndef TF_LM_DMA_NT1_WM
 #define TF_LM_DMA_NT1_WM 3
 #endif
@@ -236,13 +208,12 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
     p.dma = false;
     if (bf16) {
         p.NT = plan_nt(rows);
-        // 64- and 128-row activation tiles with k in whole steps: the DMA
-        // kernel, as the 2 x 2 wave grid up to TF_LM_GRID_NRB row blocks
-        // (64-wide k steps), else with two workgroups per CU (32-wide)
+        // k in whole 64-wide steps: the DMA kernel -- 32-row tiles, the 2 x 2
+        // wave grid up to TF_LM_GRID_NRB row blocks, else 256-row blocks
         p.nrb = cdiv(rows, 32 * p.NT);
-        p.grid = TF_LM_DMA && p.NT >= 2 && p.nrb <= TF_LM_GRID_NRB && d % TF_LM_DMA_KC == 0;
-        const bool multi = TF_LM_DMA && p.NT == 4 && p.nrb > 1 && !p.grid && d % TF_LM_DMA_MULTI_KC == 0;
-        p.dma = p.grid || multi || (TF_LM_DMA && TF_LM_DMA_NT1 && p.NT == 1 && d % TF_LM_DMA_KC == 0);
+        p.grid = p.NT >= 2 && p.nrb <= TF_LM_GRID_NRB && d % TF_LM_DMA_KC == 0;
+        const bool multi = p.NT == 4 && p.nrb > 1 && !p.grid && d % TF_LM_DMA_KC == 0;
+        p.dma = p.grid || multi || (p.NT == 1 && d % TF_LM_DMA_KC == 0);
         if (p.dma && p.NT == 1) {
             p.WM = TF_LM_DMA_NT1_WM;
             p.NW = TF_LM_DMA_NT1_NW;
@@ -250,7 +221,7 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
             p.WM = TF_LM_DMA_WM;
             p.NW = TF_LM_DMA_NW_SINGLE;
             p.WB = TF_LM_DMA_SINGLE_WB;
-        } else if (p.dma && TF_LM_MULTI_NT8) {
+        } else if (p.dma) {
             // 256-row blocks: eight waves in a 4 x 2 grid of 2 weight x 4
             // activation tiles, one workgroup per CU
             p.NT = 8;
@@ -258,9 +229,6 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
             p.WM = TF_LM_DMA_MULTI_WM;
             p.NW = 8;
             p.WB = 2;
-        } else if (p.dma) {
-            p.WM = TF_LM_DMA_MULTI_WM;
-            p.NW = TF_LM_DMA_NW;
         } else {
             p.WM = lm_wm(p.NT);
             p.NW = lm_nw(p.NT);
@@ -287,7 +255,7 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
 // SwiGLU products (bf16).
 inline GemmPlan mlp_plan(int rows, int ntiles, int K, int wg_single) {
     GemmPlan p = gemm_plan(rows, ntiles, K, wg_single);
-    p.wnt = TF_MLP_WNT && p.nrb == 1;
+    p.wnt = false;   // every workgroup of a row block re-reads its weights from L2
     return p;
 }
 // gate/up over x = [h~ ; e~], K = 2d (3d for the bigram rows)
