@@ -107,6 +107,25 @@ tf_status_t treeflash_marginal_topk_timed(const void *h, const void *lm_head,
                                           hipStream_t stream, hipEvent_t ev_begin,
                                           hipEvent_t ev_end);
 
+/* treeflash_marginal_topk for callers that cannot allocate memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid it):
+ * the same computation and outputs, with its scratch taken from a device
+ * array the library owns instead of a caller workspace.  The array holds
+ * treeflash_static_scratch_bytes() bytes (16 MiB: stage 1 of up to 16
+ * sequences at the Qwen3-8B shape, or one sequence's conditional rows); a
+ * call that needs more returns TF_ERR_WORKSPACE and launches nothing.  It
+ * calls no allocator.  Each GPU holds one copy of the array until the process
+ * ends, shared by every call on that GPU: calls that overlap in time on one
+ * GPU (several streams or host threads) race and must be serialised by the
+ * caller.  The first call on a GPU resolves the array's device address
+ * (TF_ERR_HIP if the runtime cannot). */
+tf_status_t treeflash_marginal_topk_static(const void *h, const void *lm_head,
+                                           int b, int gamma, int d, int V, int k,
+                                           float inv_temperature, tf_dtype_t dt,
+                                           int32_t *topk_idx, float *topk_logprob, float *lse,
+                                           hipStream_t stream);
+size_t treeflash_static_scratch_bytes(void);
+
 /* Part 1, stage 2, first half (Method, Eq. 1): the AR-approximated hidden
  * state of every conditional row,
  *   h'_r = h_{depth(r)} + W_down( silu(W_gate x_r) * (W_up x_r) ),

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(HERE, "libtreeflash.so")
 TF_F32, TF_BF16 = 0, 1
 STATUS = {0: "TF_OK", 1: "TF_ERR_INVALID_ARG", 2: "TF_ERR_UNSUPPORTED", 3: "TF_ERR_WORKSPACE", 4: "TF_ERR_HIP"}
 EXPORTED = ("treeflash_workspace_bytes", "treeflash_marginal_topk", "treeflash_marginal_topk_timed",
+            "treeflash_marginal_topk_static", "treeflash_static_scratch_bytes",
             "treeflash_arapprox_hidden", "treeflash_arapprox_linear_hidden", "treeflash_arapprox_expand",
             "treeflash_build_tree",
             "treeflash_build_tree_marginal", "treeflash_tree_attention_inputs", "treeflash_accept",
@@ -50,6 +51,10 @@ def lib() -> ctypes.CDLL:
     L.treeflash_marginal_topk.restype = I
     L.treeflash_marginal_topk_timed.argtypes = [P, P, I, I, I, I, I, F, I, P, P, P, P, S, P, P, P]
     L.treeflash_marginal_topk_timed.restype = I
+    L.treeflash_marginal_topk_static.argtypes = [P, P, I, I, I, I, I, F, I, P, P, P, P]
+    L.treeflash_marginal_topk_static.restype = I
+    L.treeflash_static_scratch_bytes.argtypes = []
+    L.treeflash_static_scratch_bytes.restype = S
     L.treeflash_arapprox_hidden.argtypes = [P, P, P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, P, S, P]
     L.treeflash_arapprox_hidden.restype = I
     L.treeflash_arapprox_linear_hidden.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, I, P, P, S, P]
@@ -160,6 +165,27 @@ def treeflash_marginal_topk(h: torch.Tensor, lm_head: torch.Tensor, k: int, inv_
         _check("treeflash_marginal_topk", lib().treeflash_marginal_topk(*args))
     else:
         _check("treeflash_marginal_topk_timed", lib().treeflash_marginal_topk_timed(*args, events[0], events[1]))
+    return topk_idx, topk_logprob
+
+
+def treeflash_marginal_topk_static(h: torch.Tensor, lm_head: torch.Tensor, k: int, inv_temperature: float = 1.0,
+                                   topk_idx: Optional[torch.Tensor] = None,
+                                   topk_logprob: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None):
+    """treeflash_marginal_topk with the library's own device scratch (no workspace)."""
+    b, gamma, d = h.shape
+    V = lm_head.shape[0]
+    dev = h.device
+    dt = _dtype_code(h)
+    if lm_head.shape != (V, d):
+        raise ValueError("lm_head must be [V, d]")
+    if topk_idx is None:
+        topk_idx = torch.empty((b, gamma, k), dtype=torch.int32, device=dev)
+    if topk_logprob is None:
+        topk_logprob = torch.empty((b, gamma, k), dtype=torch.float32, device=dev)
+    _check("treeflash_marginal_topk_static", lib().treeflash_marginal_topk_static(
+        _ptr(h, "h", device=dev), _ptr(lm_head, "lm_head", h.dtype, dev), b, gamma, d, V, k,
+        float(inv_temperature), dt, _ptr(topk_idx, "topk_idx", torch.int32, dev),
+        _ptr(topk_logprob, "topk_logprob", torch.float32, dev), _ptr(lse, "lse", torch.float32, dev), _stream(dev)))
     return topk_idx, topk_logprob
 
 

@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include <initializer_list>
+#include <mutex>
 
 #include "treeflash.h"
 #include "launch.hpp"
@@ -74,10 +75,10 @@ size_t treeflash_workspace_bytes(int b, int gamma, int d, int I, int V, int k, i
     return workspace_layout(b, gamma, d, I, V, k, dt == TF_BF16).total;
 }
 
-static tf_status_t marginal_topk(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
-                                 float inv_temperature, tf_dtype_t dt, int32_t* topk_idx, float* topk_logprob,
-                                 float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
-                                 hipEvent_t ev_begin, hipEvent_t ev_end) {
+// Every argument of the LM-head call but its workspace.
+static tf_status_t check_marginal_args(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
+                                       float inv_temperature, tf_dtype_t dt, const int32_t* topk_idx,
+                                       const float* topk_logprob, const float* lse) {
     if (h == nullptr || lm_head == nullptr || topk_idx == nullptr) return TF_ERR_INVALID_ARG;
     if (!dtype_ok(dt)) return TF_ERR_INVALID_ARG;
     const tf_status_t shp = common_shapes(b, gamma, d, V, k, true);
@@ -85,8 +86,16 @@ static tf_status_t marginal_topk(const void* h, const void* lm_head, int b, int 
     if (!(inv_temperature > 0.f) || !isfinite(inv_temperature)) return TF_ERR_INVALID_ARG;
     if (!aligned4(topk_idx) || (topk_logprob != nullptr && !aligned4(topk_logprob)) || (lse != nullptr && !aligned4(lse)))
         return TF_ERR_INVALID_ARG;
-    const tf_status_t al = vec_status_all({h, lm_head}, dt);
-    if (al != TF_OK) return al;
+    return vec_status_all({h, lm_head}, dt);
+}
+
+static tf_status_t marginal_topk(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
+                                 float inv_temperature, tf_dtype_t dt, int32_t* topk_idx, float* topk_logprob,
+                                 float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 hipEvent_t ev_begin, hipEvent_t ev_end) {
+    const tf_status_t chk =
+        check_marginal_args(h, lm_head, b, gamma, d, V, k, inv_temperature, dt, topk_idx, topk_logprob, lse);
+    if (chk != TF_OK) return chk;
     const bool bf16 = dt == TF_BF16;
     if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < stage1_bytes(b, gamma, d, V, bf16))
         return TF_ERR_WORKSPACE;
@@ -104,6 +113,60 @@ tf_status_t treeflash_marginal_topk(const void* h, const void* lm_head, int b, i
     return marginal_topk(h, lm_head, b, gamma, d, V, k, inv_temperature, dt, topk_idx, topk_logprob, lse, workspace,
                          workspace_bytes, stream, nullptr, nullptr);
 }
+
+}  // extern "C"
+
+// ------------------------------------------- the allocation-free variant
+//
+// treeflash_marginal_topk_static draws its scratch (the diagnostic counter
+// and the (row, vocabulary slice) partials) from a device array of
+// kStaticScratchBytes owned by the library, not from a caller workspace.
+// Every call on a GPU shares that GPU's copy of the array, so calls that
+// overlap in time on one GPU (other streams, other host threads) race.  The
+// LM-head kernel zeroes the diagnostic counter itself and writes every
+// partial the merge reads, so nothing left by an earlier call is read.
+namespace {
+
+constexpr size_t kStaticScratchBytes = 16u << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// This device's address of `scratch`, resolved once per device (each GPU
+// holds its own copy of the array); nullptr when the runtime cannot.
+void* device_scratch() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+tf_status_t treeflash_marginal_topk_static(const void* h, const void* lm_head, int b, int gamma, int d, int V,
+                                           int k, float inv_temperature, tf_dtype_t dt, int32_t* topk_idx,
+                                           float* topk_logprob, float* lse, hipStream_t stream) {
+    // every argument and the scratch size before any HIP call
+    const tf_status_t chk =
+        check_marginal_args(h, lm_head, b, gamma, d, V, k, inv_temperature, dt, topk_idx, topk_logprob, lse);
+    if (chk != TF_OK) return chk;
+    if (stage1_bytes(b, gamma, d, V, dt == TF_BF16) > kStaticScratchBytes) return TF_ERR_WORKSPACE;
+    void* ws = device_scratch();
+    if (ws == nullptr) return TF_ERR_HIP;
+    return marginal_topk(h, lm_head, b, gamma, d, V, k, inv_temperature, dt, topk_idx, topk_logprob, lse, ws,
+                         kStaticScratchBytes, stream, nullptr, nullptr);
+}
+
+size_t treeflash_static_scratch_bytes(void) { return kStaticScratchBytes; }
 
 tf_status_t treeflash_marginal_topk_timed(const void* h, const void* lm_head, int b, int gamma, int d, int V, int k,
                                           float inv_temperature, tf_dtype_t dt, int32_t* topk_idx,

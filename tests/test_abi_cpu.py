@@ -305,3 +305,26 @@ def _accept(**over):
 ])
 def test_accept_rejects(over, code):
     assert _accept(**over) == code
+
+
+def _static(**over):
+    a = dict(h=FAKE, w=FAKE, b=1, gamma=16, d=4096, V=151936, k=8, it=1.0, dt=BF16, idx=FAKE2, lp=None,
+             lse=None, st=None)
+    a.update(over)
+    return binding.lib().treeflash_marginal_topk_static(a["h"], a["w"], a["b"], a["gamma"], a["d"], a["V"], a["k"],
+                                                        a["it"], a["dt"], a["idx"], a["lp"], a["lse"], a["st"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(h=None), INVALID), (dict(w=None), INVALID), (dict(idx=None), INVALID), (dict(b=0), INVALID),
+    (dict(d=4090), UNSUPPORTED), (dict(k=0), INVALID), (dict(it=0.0), INVALID), (dict(dt=3), INVALID),
+    (dict(h=FAKE + 4), UNSUPPORTED), (dict(lp=FAKE + 2), INVALID),
+    # 16 sequences x 121 rows need more scratch than the library's array holds
+    (dict(b=16, gamma=121, k=32), WORKSPACE),
+])
+def test_marginal_topk_static_rejects(over, code):
+    assert _static(**over) == code
+
+
+def test_static_scratch_size():
+    assert binding.lib().treeflash_static_scratch_bytes() == 16 << 20
