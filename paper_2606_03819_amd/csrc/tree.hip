@@ -13,7 +13,9 @@
 // Up to 1024 slots the frontier lives in registers (slot s in lane s % 64)
 // and the argmax is a DPP maximum of the lanes' score keys; only an exact
 // score tie between lanes runs the full comparison.  Larger budgets keep the
-// frontier in LDS.
+// frontier in LDS.  Below 128 slots, with every row in LDS, the stage-1
+// candidates and the rows' first log-probs sit in registers too and runs of
+// siblings from one slot are popped in one step (see the lane-table kernel).
 //
 // Candidate order: path score (fp32 running sum) desc, depth asc, then the
 // lexicographic order of the rank paths (ranks of the nodes in their parents'
@@ -398,6 +400,358 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
     tree_store(a, t, seq, n, lane);
 }
 
+// ------------------------------------------------ lane tables and sibling runs
+//
+// For budgets below 128 with every rank of every row in LDS, the selecting
+// wave also keeps in registers the stage-1 candidates (flat index
+// (depth-1)*M + m in lane index % 64 of register index / 64) and the first
+// log-prob of every row (row r in lane r % 64 of register r / 64).  Each
+// frontier slot holds its candidate's key, parent score, depth and rank,
+// entry index and the first row of its entries' children (single rows:
+// 1 + (depth-1)*M; bigram rows: 1 + M + (depth-2)*M^2 + m2*M, m2 the
+// parent's candidate index; marginal: the next depth's row).  At the top of
+// every pop each lane reads its slots' tokens and next log-probs from LDS,
+// so that the read overlaps the wave maximum; the popped node's child row is
+// then a ballot of the candidate registers against its token and the first
+// log-prob of that row a readlane.
+//
+// Sibling runs.  When a pop comes from the same slot as the one before, the
+// best key of the other slots (a second wave maximum) bounds what may come
+// next: the slot's following siblings are popped in order for as long as
+// each beats that bound and every child opened by the siblings popped before
+// it (ties stop the run; the next pop then takes the full order).  All 64
+// lanes evaluate the next 64 siblings at once (score, child row, child key),
+// a prefix maximum over the lanes gives the run's length, and the run is
+// committed in one step: its nodes written by their lanes, its children
+// moved into their slots by a lane permutation.  Nodes go to the outputs as
+// they are popped; LDS keeps only their parents and ranks, which the full
+// order reads on ties.  Rows whose leading entries
+// dominate the frontier (flat conditional distributions make star-shaped
+// trees) then cost one step instead of one pop per node.
+//
+// A node's score is the key's float: scores are sums of a +0.0 root score
+// and log-probs, never -0.0, so the key (which folds -0.0 into +0.0) loses
+// nothing.
+constexpr int kLaneSlotsMax = 2;   // frontier slots per lane (B + 1 <= 128)
+constexpr int kLaneTabMax = 4;     // table registers (rows and candidates <= 256)
+
+__host__ __device__ inline size_t tree_lane_lds_bytes(int B, int Rs, int K2) {
+    return (size_t)8 * B + (size_t)8 * Rs * K2;
+}
+
+// Key of a candidate score: -0.0 keys as +0.0, as cand_before compares.
+__device__ __forceinline__ uint32_t score_key(float s) {
+    const int u = __float_as_int(s + 0.f);
+    return (uint32_t)(u ^ ((u >> 31) | (int)0x80000000));   // f32_key
+}
+
+// Inclusive prefix maximum over the wave's lanes (0 is the identity).
+__device__ __forceinline__ uint32_t wave_prefix_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true));   // row_shr:1
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true));   // row_shr:2
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true));   // row_shr:4
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true));   // row_shr:8
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));  // row_bcast:15
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));  // row_bcast:31
+    return v;
+}
+
+template <int FS, int T>
+__global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs a) {
+    extern __shared__ __align__(16) unsigned char dyn[];
+    TreeLds t{};   // parents and ranks of the nodes (for ties), and the rows
+    {
+        int32_t* p = reinterpret_cast<int32_t*>(dyn);
+        t.n_par = p; p += a.B;
+        t.n_rank = p; p += a.B;
+        t.c_lp = reinterpret_cast<float*>(p); p += a.Rs * a.K2;
+        t.c_idx = p;
+    }
+    const int nent = a.Rs * a.K2;
+    const int seq = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int32_t* ridx = a.cond_idx + (size_t)seq * nent;
+    const float* rlp = a.cond_lp + (size_t)seq * nent;
+    // outputs of this sequence, written as the nodes are popped
+    int32_t* o_tok = a.tok + (size_t)seq * a.B;
+    int32_t* o_par = a.par + (size_t)seq * a.B;
+    int32_t* o_dep = a.dep + (size_t)seq * a.B;
+    float* o_score = a.score + (size_t)seq * a.B;
+    int32_t* o_crow = a.crow != nullptr ? a.crow + (size_t)seq * a.B : nullptr;
+    const bool marginal = a.mode == kTreeMarginal;
+    const int nflat = marginal ? 0 : a.gamma * a.M;
+    // first child row of the entries of a slot opened by a node of depth d
+    // and candidate index m: c0 + c1*d + c2*m
+    const int c0 = a.mode == kTreeBigram ? 1 + a.M - a.M * a.M : 1;
+    const int c1 = a.mode == kTreeSingle ? a.M : a.mode == kTreeBigram ? a.M * a.M : 1;
+    const int c2 = a.mode == kTreeBigram ? a.M : 0;
+
+    // the selecting wave's tables, loaded beside the rows
+    int tkr[T], tkd[T];
+    float rfr[T];
+    if (tid < 64) {
+#pragma unroll
+        for (int r = 0; r < T; ++r) {
+            const int f = 64 * r + lane;
+            tkr[r] = f < nflat ? a.topk[(size_t)seq * nflat + f] : -1;
+            tkd[r] = f < nflat ? f / a.M + 1 : 0;
+            rfr[r] = rlp[(size_t)min(f, a.Rs - 1) * a.K2];
+        }
+    }
+    for (int e0 = tid; e0 < nent; e0 += 4 * kTreeThreads) {
+        float lp[4];
+        int ix[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = min(e0 + u * kTreeThreads, nent - 1);
+            lp[u] = rlp[e];
+            ix[u] = ridx[e];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * kTreeThreads;
+            if (e < nent) {
+                t.c_lp[e] = lp[u];
+                t.c_idx[e] = ix[u];
+            }
+        }
+    }
+    __syncthreads();
+    if (tid >= 64) return;
+
+    // frontier: slot s = lane + 64*j; key 0 = empty
+    uint32_t skey[FS];
+    float sps[FS];
+    int sdr[FS], sea[FS], scb[FS];   // sdr = depth << 16 | rank; sea = entry index row*K2 + rank
+#pragma unroll
+    for (int j = 0; j < FS; ++j) {
+        skey[j] = 0u;
+        sps[j] = 0.f;
+        sdr[j] = sea[j] = scb[j] = 0;
+    }
+    {
+        const float first = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(rfr[0])));
+        if (lane == 0) {
+            skey[0] = score_key(0.f + first);
+            sdr[0] = 1 << 16;
+            scb[0] = 1;   // depth-1 entries expand into rows 1 + m (marginal: row 1)
+        }
+    }
+
+    int n = 0, prev = -1;
+    while (n < a.B) {
+        // every slot's token and next log-prob, read while the maximum runs
+        int tokv[FS];
+        float nlpv[FS];
+#pragma unroll
+        for (int j = 0; j < FS; ++j) {
+            tokv[j] = t.c_idx[sea[j]];
+            nlpv[j] = t.c_lp[min(sea[j] + 1, nent - 1)];
+        }
+        asm volatile("" ::: "memory");   // keep the reads above the maximum
+        uint32_t lk = skey[0];
+        int lj = 0, ldup = 0;
+#pragma unroll
+        for (int j = 1; j < FS; ++j) {
+            if (skey[j] > lk) {
+                lk = skey[j];
+                lj = j;
+                ldup = 0;
+            } else if (skey[j] == lk) {
+                ldup = 1;
+            }
+        }
+        const uint32_t mx = wave_max_u32(lk);
+        if (mx == 0u) break;   // frontier exhausted: rows too short for B nodes; the rest stay -1
+        const unsigned long long tied = __ballot(lk == mx);
+        int wl, js;
+        if (__builtin_expect(__popcll(tied) == 1 &&
+                                 (FS == 1 || __builtin_amdgcn_readlane(ldup, __ffsll((long long)tied) - 1) == 0),
+                             1)) {
+            wl = __ffsll((long long)tied) - 1;
+            js = FS == 1 ? 0 : __builtin_amdgcn_readlane(lj, wl);
+        } else {   // exact score tie: the full order decides (rank paths from the node table)
+            Cand lb{0.f, 0u};
+#pragma unroll
+            for (int j = 0; j < FS; ++j)
+                if (skey[j] == mx) {
+                    const Cand c{key_f32(skey[j]), ((uint32_t)(sdr[j] >> 16) << 24) |
+                                                       ((uint32_t)(lane + 64 * j) << 12) | (uint32_t)(sdr[j] & 0xffff)};
+                    if (cand_before(c, lb, t)) lb = c;
+                }
+            const Cand best = wave_best(lb, t);
+            wl = __builtin_amdgcn_readfirstlane(c_slot(best.meta) & 63);
+            js = __builtin_amdgcn_readfirstlane(c_slot(best.meta) >> 6);
+        }
+        // the winning slot's fields
+        float g_ps = sps[0], g_nl = nlpv[0];
+        int g_dr = sdr[0], g_cb = scb[0], g_tok = tokv[0], g_ea = sea[0];
+#pragma unroll
+        for (int j = 1; j < FS; ++j)
+            if (j == js) {
+                g_ps = sps[j];
+                g_nl = nlpv[j];
+                g_dr = sdr[j];
+                g_cb = scb[j];
+                g_tok = tokv[j];
+                g_ea = sea[j];
+            }
+        const float score = key_f32(mx);
+        const int dr = __builtin_amdgcn_readlane(g_dr, wl);
+        const int cb = __builtin_amdgcn_readlane(g_cb, wl);
+        const int tok = __builtin_amdgcn_readlane(g_tok, wl);
+        const int depth = dr >> 16, rank = dr & 0xffff;
+        const int slot = wl + 64 * js;
+        const bool more = rank + 1 < a.K2;
+        // child row: the node's token among the candidates of its depth
+        int f = -1;
+#pragma unroll
+        for (int r = T - 1; r >= 0; --r) {
+            const unsigned long long hit = __ballot(((tkr[r] ^ tok) | (tkd[r] ^ depth)) == 0);
+            if (hit != 0ull) f = 64 * r + __ffsll((long long)hit) - 1;
+        }
+        const int m = marginal ? 0 : f - (depth - 1) * a.M;
+        const int child_row = depth < a.gamma && (marginal || f >= 0) ? cb + m : -1;
+        float cfirst = 0.f;
+        if (child_row >= 0) {
+            cfirst = rfr[0];
+#pragma unroll
+            for (int r = 1; r < T; ++r)
+                if (r == (child_row >> 6)) cfirst = rfr[r];
+            cfirst = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cfirst), child_row & 63));
+        }
+        const float cs = score + cfirst;
+        const uint32_t ck = child_row >= 0 ? score_key(cs) : 0u;
+
+        // a second pop in a row from this slot: try a sibling run
+        int L = 1;
+        if (slot == prev && more && n + 1 < a.B) {
+            uint32_t lo = 0u;
+#pragma unroll
+            for (int j = 0; j < FS; ++j) lo = max(lo, lane + 64 * j == slot ? 0u : skey[j]);
+            const uint32_t k2 = wave_max_u32(lo);
+            const float ps = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g_ps), wl));
+            const float nl = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g_nl), wl));
+            const uint32_t ka = score_key(ps + nl);
+            if (ka > k2 && ka > ck) {
+                const int ea = __builtin_amdgcn_readlane(g_ea, wl);
+                // sibling i of this pop in lane i
+                const bool valid = rank + lane < a.K2;
+                const int e = min(ea + lane, nent - 1);
+                const float lpi = t.c_lp[e];
+                const int toki = t.c_idx[e];
+                const float si = ps + lpi;
+                const uint32_t ki = valid ? score_key(si) : 0u;
+                int mi = -1;
+                if (depth < a.gamma) {
+                    if (marginal) {
+                        mi = 0;
+                    } else {
+                        for (int q = 0; q < a.M; ++q) {
+                            const int fq = (depth - 1) * a.M + q;
+                            int cand = tkr[0];
+#pragma unroll
+                            for (int r = 1; r < T; ++r)
+                                if (r == (fq >> 6)) cand = tkr[r];
+                            cand = __builtin_amdgcn_readlane(cand, fq & 63);
+                            mi = mi < 0 && toki == cand ? q : mi;
+                        }
+                    }
+                }
+                const int crowi = mi >= 0 ? cb + mi : -1;
+                const float cfi = t.c_lp[max(crowi, 0) * a.K2];
+                const uint32_t cki = crowi >= 0 && valid ? score_key(si + cfi) : 0u;
+                // a sibling is popped if it beats the other slots and every child opened before it
+                const uint32_t before = (uint32_t)__builtin_amdgcn_update_dpp(
+                    0, (int)wave_prefix_max_u32(cki), 0x138, 0xF, 0xF, true);   // wave_shr:1
+                const bool ok = lane == 0 || (ki > max(k2, before) && lane < a.B - n);
+                const unsigned long long bad = ~__ballot(ok);
+                L = bad == 0ull ? 63 : min(__ffsll((long long)bad) - 1, 63);
+                // the run's nodes
+                if (lane < L) {
+                    t.n_par[n + lane] = slot - 1;
+                    t.n_rank[n + lane] = rank + lane;
+                    o_tok[n + lane] = toki;
+                    o_par[n + lane] = slot - 1;
+                    o_dep[n + lane] = depth;
+                    o_score[n + lane] = si;
+                    if (o_crow != nullptr) o_crow[n + lane] = crowi;
+                }
+                // their children into slots n + 1 + i
+                const int ncbi = c0 + c1 * depth + c2 * mi;
+#pragma unroll
+                for (int j = 0; j < FS; ++j) {
+                    const int s = lane + 64 * j;
+                    const int src = ((s - n - 1) & 63) << 2;
+                    const uint32_t pk = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)cki);
+                    const float pps = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(si)));
+                    const int pea = __builtin_amdgcn_ds_bpermute(src, max(crowi, 0) * a.K2);
+                    const int pcb = __builtin_amdgcn_ds_bpermute(src, ncbi);
+                    const bool in = s >= n + 1 && s <= n + L;
+                    skey[j] = in ? pk : skey[j];
+                    sps[j] = in ? pps : sps[j];
+                    sdr[j] = in ? (depth + 1) << 16 : sdr[j];
+                    sea[j] = in ? pea : sea[j];
+                    scb[j] = in ? pcb : scb[j];
+                }
+                // the slot moves past the run
+                const uint32_t kl = (uint32_t)__builtin_amdgcn_readlane((int)ki, L);
+#pragma unroll
+                for (int j = 0; j < FS; ++j) {
+                    const bool own = lane + 64 * j == slot;
+                    skey[j] = own ? kl : skey[j];
+                    sdr[j] = own ? sdr[j] + L : sdr[j];
+                    sea[j] = own ? sea[j] + L : sea[j];
+                }
+            }
+        }
+        if (L == 1) {
+            if (lane == 0) {
+                t.n_par[n] = slot - 1;
+                t.n_rank[n] = rank;
+                o_tok[n] = tok;
+                o_par[n] = slot - 1;
+                o_dep[n] = depth;
+                o_score[n] = score;
+                if (o_crow != nullptr) o_crow[n] = child_row;
+            }
+            // the popped slot moves to its next sibling (its lane has read that entry's log-prob)
+#pragma unroll
+            for (int j = 0; j < FS; ++j) {
+                const bool own = lane + 64 * j == slot;
+                const float ns = sps[j] + nlpv[j];
+                skey[j] = own ? (more ? score_key(ns) : 0u) : skey[j];
+                sdr[j] = own ? sdr[j] + 1 : sdr[j];
+                sea[j] = own ? sea[j] + (more ? 1 : 0) : sea[j];
+            }
+            // an expandable node opens slot n + 1 on the first entry of its row
+            if (child_row >= 0) {
+                const int ncb = c0 + c1 * depth + c2 * m;
+#pragma unroll
+                for (int j = 0; j < FS; ++j) {
+                    const bool ch = lane + 64 * j == n + 1;
+                    skey[j] = ch ? ck : skey[j];
+                    sps[j] = ch ? score : sps[j];
+                    sdr[j] = ch ? (depth + 1) << 16 : sdr[j];
+                    sea[j] = ch ? child_row * a.K2 : sea[j];
+                    scb[j] = ch ? ncb : scb[j];
+                }
+            }
+        }
+        prev = slot;
+        n += L;
+    }
+    // slots past the last pop get the empty values
+    for (int i = n + lane; i < a.B; i += 64) {
+        o_tok[i] = -1;
+        o_par[i] = -1;
+        o_dep[i] = 0;
+        o_score[i] = neg_inf();
+        if (o_crow != nullptr) o_crow[i] = -1;
+    }
+}
+
 size_t tree_lds_bytes(int B, int gamma, int M, int Rs, int K2, int* cached_ranks) {
     const size_t fixed = tree_fixed_bytes(B, gamma, M);
     if (fixed > (size_t)kTreeLdsBudget) return 0;
@@ -420,7 +774,19 @@ hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, cons
                node_token, node_parent, node_depth, node_score, node_child_row};
     const void* fn;
     const bool all = P >= topk2;
-    if (B + 1 <= 64)
+    size_t lds_used = lds;
+    const int tab = std::max(Rs, mode == kTreeMarginal ? 0 : gamma * M);
+    const size_t lane_lds = tree_lane_lds_bytes(B, Rs, topk2);
+    if (lane_lds <= (size_t)kTreeLdsBudget && B + 1 <= 64 * kLaneSlotsMax && tab <= 64 * kLaneTabMax) {
+        // frontier, candidates and first log-probs in registers
+        lds_used = lane_lds;
+        if (B + 1 <= 64)
+            fn = tab <= 128 ? reinterpret_cast<const void*>(build_tree_lane_kernel<1, 2>)
+                            : reinterpret_cast<const void*>(build_tree_lane_kernel<1, 4>);
+        else
+            fn = tab <= 128 ? reinterpret_cast<const void*>(build_tree_lane_kernel<2, 2>)
+                            : reinterpret_cast<const void*>(build_tree_lane_kernel<2, 4>);
+    } else if (B + 1 <= 64)
         fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<1, true>)
                  : reinterpret_cast<const void*>(build_tree_reg_kernel<1, false>);
     else if (B + 1 <= 128)
@@ -441,7 +807,7 @@ hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, cons
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kTreeLdsBudget) != hipSuccess)
         return hipErrorInvalidValue;
     void* args[] = {&a};
-    const hipError_t e = hipLaunchKernel(fn, dim3(b), dim3(kTreeThreads), args, lds, stream);
+    const hipError_t e = hipLaunchKernel(fn, dim3(b), dim3(kTreeThreads), args, lds_used, stream);
     if (e != hipSuccess) return e;
     return hipGetLastError();
 }
