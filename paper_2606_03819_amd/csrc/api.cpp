@@ -222,8 +222,8 @@ tf_status_t treeflash_arapprox_hidden(const void* h, const int32_t* root_token, 
     const hipError_t e = launch_arapprox(h, root_token, nullptr, topk_idx, emb, norm_h_gain, norm_e_gain, w_gate,
                                          w_up, w_down, b, gamma, d, I, V, k, false, rms_eps, bf16, ws + lay.ht, ws + lay.et,
                                          ws + lay.act, hprime, reinterpret_cast<float*>(ws + lay.mlp_part),
-                                         reinterpret_cast<int*>(ws + lay.counters), reinterpret_cast<int*>(ws + lay.diag),
-                                         stream);
+                                         reinterpret_cast<int*>(ws + lay.counters), reinterpret_cast<float*>(ws + lay.hh),
+                                         reinterpret_cast<int*>(ws + lay.diag), stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
@@ -256,7 +256,8 @@ tf_status_t treeflash_arapprox_2prev_hidden(const void* h, const int32_t* contex
                                          ws + lay.ht, ws + lay.et, ws + lay.act, hprime,
                                          reinterpret_cast<float*>(ws + lay.mlp_part),
                                          reinterpret_cast<int*>(ws + lay.counters),
-                                         reinterpret_cast<int*>(ws + lay.diag), stream);
+                                         reinterpret_cast<float*>(ws + lay.hh), reinterpret_cast<int*>(ws + lay.diag),
+                                         stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
 
@@ -279,6 +280,7 @@ tf_status_t treeflash_arapprox_linear_hidden(const void* h, const int32_t* root_
                                                 gamma, d, V, k, rms_eps, bf16, ws + lay.ht, ws + lay.et, hprime,
                                                 reinterpret_cast<float*>(ws + lay.mlp_part),
                                                 reinterpret_cast<int*>(ws + lay.counters),
+                                                reinterpret_cast<float*>(ws + lay.hh),
                                                 reinterpret_cast<int*>(ws + lay.diag), stream);
     return e == hipSuccess ? TF_OK : TF_ERR_HIP;
 }
@@ -308,7 +310,8 @@ tf_status_t treeflash_arapprox_expand(const void* h, const int32_t* root_token, 
                                    w_down, b, gamma, d, I, V, k, false, rms_eps, bf16, ws + lay.ht, ws + lay.et,
                                    ws + lay.act,
                                    ws + lay.hp, reinterpret_cast<float*>(ws + lay.mlp_part),
-                                   reinterpret_cast<int*>(ws + lay.counters), diag, stream);
+                                   reinterpret_cast<int*>(ws + lay.counters), reinterpret_cast<float*>(ws + lay.hh), diag,
+                                   stream);
     if (e != hipSuccess) return TF_ERR_HIP;
     const int rows = b * (1 + (gamma - 1) * k);
     e = launch_lmhead_topk(ws + lay.hp, d, lm_head, rows, d, V, topk2, inv_temperature, bf16, ws + lay.lm,

@@ -22,14 +22,14 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
                            const void* emb, const void* gain_h, const void* gain_e, const void* w_gate,
                            const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
                            bool bigram, float eps, bool bf16, void* ht, void* et, void* act, void* hp,
-                           float* mlp_partial, int* counters, int* diag, hipStream_t stream);
+                           float* mlp_partial, int* counters, float* hh, int* diag, hipStream_t stream);
 
 // The "w/ Linear" approximator for every conditional row: RMSNorm of h and
 // of the previous token's embedding, h' = h + W_lin [h~ ; e~].
 hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
                                   const void* gain_h, const void* gain_e, const void* w_lin, int b, int gamma, int d,
                                   int V, int k, float eps, bool bf16, void* ht, void* et, void* hp,
-                                  float* mlp_partial, int* counters, int* diag, hipStream_t stream);
+                                  float* mlp_partial, int* counters, float* hh, int* diag, hipStream_t stream);
 
 // Best-first tree selection, one workgroup per sequence.  `mode` 0: the
 // single-token rows; 1: the rows are the gamma marginal rows [b, gamma,

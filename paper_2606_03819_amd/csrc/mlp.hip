@@ -149,45 +149,12 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const uint16_t* 
 
 // ------------------------------------------------------------------ bf16
 
-template <int WM, int NT, int NW, int PIPE, bool WNT>
-__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void gateup_bf16_kernel(WRowsGateUp ws, XRowsConcat xs, GemmShape sh,
-                                                                 uint16_t* __restrict__ act, int I, float* partial,
-                                                                 int* counter) {
+// Any product of the approximator over several row blocks: `ws` weight rows
+// against `xs` activation rows, the epilogue behind the split-k fix-up.
+template <int WM, int NT, int NW, int PIPE, bool WNT, class WSrc, class XSrc, class Epi>
+__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void product_bf16_kernel(WSrc ws, XSrc xs, GemmShape sh,
+                                                                              Epi epi) {
     __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
-    EpiFixup<WM, NT, NW, EpiSwiGLU<WM, NT>> epi{EpiSwiGLU<WM, NT>{act, I}, partial, counter};
-    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
-}
-
-// the plain SiLU MLP's input projection: tiles of 32 gate rows
-template <int WM, int NT, int NW, int PIPE, bool WNT>
-__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void silu_gate_bf16_kernel(WRowsPlain ws, XRowsConcat xs,
-                                                                                  GemmShape sh,
-                                                                                  uint16_t* __restrict__ act, int I,
-                                                                                  float* partial, int* counter) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
-    EpiFixup<WM, NT, NW, EpiSiLU<WM, NT>> epi{EpiSiLU<WM, NT>{act, I}, partial, counter};
-    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
-}
-
-template <int WM, int NT, int NW, int PIPE, bool WNT>
-__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void down_bf16_kernel(WRowsPairedK ws, XRowsPlain xs, GemmShape sh,
-                                                               uint16_t* __restrict__ hp, const uint16_t* __restrict__ h,
-                                                               int d, RowTable rt, float* partial, int* counter) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
-    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, rt}, partial, counter};
-    stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
-}
-
-// The linear approximator: h' = h + W_lin [h~ ; e~].
-template <int WM, int NT, int NW, int PIPE, bool WNT>
-__global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void linear_bf16_kernel(WRowsPlain ws, XRowsConcat xs,
-                                                                              GemmShape sh,
-                                                                              uint16_t* __restrict__ hp,
-                                                                              const uint16_t* __restrict__ h, int d,
-                                                                              RowTable rt, float* partial,
-                                                                              int* counter) {
-    __shared__ __align__(16) unsigned char smem[GemmTraits<WM, NT, NW>::SMEM_BYTES];
-    EpiFixup<WM, NT, NW, EpiResidual<WM, NT>> epi{EpiResidual<WM, NT>{hp, h, d, rt}, partial, counter};
     stream_gemm<WM, NT, NW, PIPE, WNT>(ws, xs, epi, sh, smem);
 }
 
@@ -256,53 +223,83 @@ __global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict
 
 // ------------------------------------------------------------------ launcher
 
-// SwiGLU gate/up, or the gate alone when wu is null (plain SiLU MLP)
-template <int WM, int NT, int NW, int PIPE, bool WNT>
-static void launch_gateup(const uint16_t* wg, const uint16_t* wu, const uint16_t* ht, const uint16_t* et,
-                          uint16_t* act, int rows, int d, int ew, int I, const RowTable& rt, const GemmPlan& pg,
-                          float* partial, int* counters, hipStream_t st) {
-    XRowsConcat xc{ht, et, d, ew, rt};
-    const GemmShape shg = pg.shape(rows, d + ew);
-    if (wu != nullptr) {
-        WRowsGateUp wgu{wg, wu, I, d + ew};
-        hipLaunchKernelGGL((gateup_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgu, xc,
-                           shg, act, I, partial, counters);
+// Epilogue makers: each product's epilogue for the (WM, NT) its plan picks.
+struct MakeStoreH {   // the h~ half: fp32 table, one row per drafter state
+    float* out;
+    int ldo;
+    template <int WM, int NT>
+    EpiStoreF32<WM, NT> make() const { return EpiStoreF32<WM, NT>{out, ldo}; }
+};
+struct MakeSwiGLUH {   // the e~ half of gate/up: + h~ half, SwiGLU
+    uint16_t* act;
+    int I;
+    const float* hh;
+    int ldh;
+    RowTable rt;
+    template <int WM, int NT>
+    EpiAddH<WM, NT, EpiSwiGLU<WM, NT>> make() const {
+        return EpiAddH<WM, NT, EpiSwiGLU<WM, NT>>{EpiSwiGLU<WM, NT>{act, I}, hh, ldh, rt};
+    }
+};
+struct MakeSiLUH {   // the e~ half of the plain SiLU gate
+    uint16_t* act;
+    int I;
+    const float* hh;
+    int ldh;
+    RowTable rt;
+    template <int WM, int NT>
+    EpiAddH<WM, NT, EpiSiLU<WM, NT>> make() const {
+        return EpiAddH<WM, NT, EpiSiLU<WM, NT>>{EpiSiLU<WM, NT>{act, I}, hh, ldh, rt};
+    }
+};
+struct MakeResidual {   // the down projection: + h
+    uint16_t* hp;
+    const uint16_t* h;
+    int d;
+    RowTable rt;
+    template <int WM, int NT>
+    EpiResidual<WM, NT> make() const { return EpiResidual<WM, NT>{hp, h, d, rt}; }
+};
+struct MakeResidualH {   // the e~ half of the linear layer: + h~ half, + h
+    uint16_t* hp;
+    const uint16_t* h;
+    int d;
+    RowTable rt;
+    const float* hh;
+    int ldh;
+    template <int WM, int NT>
+    EpiAddH<WM, NT, EpiResidual<WM, NT>> make() const {
+        return EpiAddH<WM, NT, EpiResidual<WM, NT>>{EpiResidual<WM, NT>{hp, h, d, rt}, hh, ldh, rt};
+    }
+};
+
+template <int WM, int NT, class WSrc, class XSrc, class Maker>
+static void run_product_nt(const GemmPlan& p, const WSrc& ws, const XSrc& xs, int rows, int K, const Maker& mk,
+                           float* partial, int* counters, hipStream_t st) {
+    constexpr int S = TF_NW_SINGLE, P = TF_PIPE_DEFAULT;
+    using Inner = decltype(mk.template make<WM, NT>());
+    const GemmShape sh = p.shape(rows, K);
+    if (p.NW != S) {
+        using E = EpiFixup<WM, NT, TF_NW, Inner>;
+        hipLaunchKernelGGL((product_bf16_kernel<WM, NT, TF_NW, P, false, WSrc, XSrc, E>), dim3(sh.G),
+                           dim3(64 * TF_NW), 0, st, ws, xs, sh, E{mk.template make<WM, NT>(), partial, counters});
     } else {
-        WRowsPlain wgp{wg, I, d + ew};
-        hipLaunchKernelGGL((silu_gate_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shg.G), dim3(64 * NW), 0, st, wgp,
-                           xc, shg, act, I, partial, counters);
+        using E = EpiFixup<WM, NT, S, Inner>;
+        hipLaunchKernelGGL((product_bf16_kernel<WM, NT, S, P, false, WSrc, XSrc, E>), dim3(sh.G), dim3(64 * S), 0,
+                           st, ws, xs, sh, E{mk.template make<WM, NT>(), partial, counters});
     }
 }
 
-// the activation is [rows, 2I] bf16 hi/lo pairs
-template <int WM, int NT, int NW, int PIPE, bool WNT>
-static void launch_down(const uint16_t* h, const uint16_t* wd, const uint16_t* act, uint16_t* hp, int rows, int d,
-                        int I, const RowTable& rt, const GemmPlan& pd, float* partial, int* counters,
-                        hipStream_t st) {
-    WRowsPairedK wdn{wd, d, I};
-    XRowsPlain xa{act, 2l * I};
-    const GemmShape shd = pd.shape(rows, 2 * I);
-    hipLaunchKernelGGL((down_bf16_kernel<WM, NT, NW, PIPE, WNT>), dim3(shd.G), dim3(64 * NW), 0, st, wdn, xa, shd,
-                       hp, h, d, rt, partial, counters);
-}
-
-// Both products share the row blocking (same rows); each plan picks its own
-// waves per workgroup.
-template <int WM, int NT>
-static void launch_mlp_bf16(const uint16_t* h, const uint16_t* wg, const uint16_t* wu, const uint16_t* wd,
-                            const uint16_t* ht, const uint16_t* et, uint16_t* act, uint16_t* hp, int rows, int d,
-                            int ew, int I, const RowTable& rt, const GemmPlan& pg, const GemmPlan& pd,
-                            float* partial, int* counters, hipStream_t st) {
-    constexpr int S = TF_NW_SINGLE, P = TF_PIPE_DEFAULT;
-    if (pg.NW != S)
-        launch_gateup<WM, NT, TF_NW, P, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial, counters, st);
+// One product with the tile shape its plan picks (plan_nt / plan_wm).
+template <class WSrc, class XSrc, class Maker>
+static void run_product(const GemmPlan& p, const WSrc& ws, const XSrc& xs, int rows, int K, const Maker& mk,
+                        float* partial, int* counters, hipStream_t st) {
+    if (p.NT == 1)
+        run_product_nt<2, 1>(p, ws, xs, rows, K, mk, partial, counters, st);
+    else if (p.NT == 2)
+        run_product_nt<1, 2>(p, ws, xs, rows, K, mk, partial, counters, st);
     else
-        launch_gateup<WM, NT, S, P, false>(wg, wu, ht, et, act, rows, d, ew, I, rt, pg, partial, counters, st);
-    int* cd = counters + pg.counter_ints();
-    if (pd.NW != S)
-        launch_down<WM, NT, TF_NW, P, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
-    else
-        launch_down<WM, NT, S, P, false>(h, wd, act, hp, rows, d, I, rt, pd, partial, cd, st);
+        run_product_nt<1, 4>(p, ws, xs, rows, K, mk, partial, counters, st);
 }
 
 static bool aligned16p(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -387,7 +384,7 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
                            const void* emb, const void* gain_h, const void* gain_e, const void* w_gate,
                            const void* w_up, const void* w_down, int b, int gamma, int d, int I, int V, int k,
                            bool bigram, float eps, bool bf16, void* ht, void* et, void* act, void* hp,
-                           float* mlp_partial, int* counters, int* diag, hipStream_t stream) {
+                           float* mlp_partial, int* counters, float* hh, int* diag, hipStream_t stream) {
     const RowTable rt = make_row_table(gamma, k, bigram ? 1 : 0);
     const int npre = bigram ? 2 : 1;
     const int ew = npre * d;
@@ -396,28 +393,35 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
         if (mlp_dma_applies(true, b, gamma, rt.Rs, d, I, ew))
             return launch_arapprox_dma(h, root, context, topk_idx, emb, gain_h, gain_e, w_gate, w_up, w_down, b, d,
                                        I, V, rt, npre, eps, ht, et, act, hp, mlp_partial, counters, diag, stream);
-        const GemmPlan pg = w_up != nullptr ? gateup_plan(rows, d + ew, I) : silu_gate_plan(rows, d + ew, I);
+        // several row blocks: the input projection split at the h~ / e~ boundary
+        // (the h~ half once per drafter state), then the down projection
+        const bool swiglu = w_up != nullptr;
+        const int states = b * rt.gamma;
+        const SplitPlans sp = split_plans(swiglu ? 0 : 1, states, rows, d, ew, I);
         const GemmPlan pd = down_plan(rows, d, I);
-        const int ncounters = (int)(pg.counter_ints() + pd.counter_ints());
         launch_norms<uint16_t>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
-                               counters, ncounters, stream);
+                               counters, (int)(sp.counter_ints() + pd.counter_ints()), stream);
         const uint16_t* hb = static_cast<const uint16_t*>(h);
         const uint16_t* wg = static_cast<const uint16_t*>(w_gate);
         const uint16_t* wu = static_cast<const uint16_t*>(w_up);
-        const uint16_t* wd = static_cast<const uint16_t*>(w_down);
-        const uint16_t* htb = static_cast<const uint16_t*>(ht);
-        const uint16_t* etb = static_cast<const uint16_t*>(et);
+        const XRowsPlain xh{static_cast<const uint16_t*>(ht), d};
+        const XRowsPlain xe{static_cast<const uint16_t*>(et), ew};
         uint16_t* actb = static_cast<uint16_t*>(act);
-        uint16_t* hpb = static_cast<uint16_t*>(hp);
-        if (pg.NT == 1)
-            launch_mlp_bf16<2, 1>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg, pd, mlp_partial,
-                                  counters, stream);
-        else if (pg.NT == 2)
-            launch_mlp_bf16<1, 2>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg, pd, mlp_partial,
-                                  counters, stream);
-        else
-            launch_mlp_bf16<1, 4>(hb, wg, wu, wd, htb, etb, actb, hpb, rows, d, ew, I, rt, pg, pd, mlp_partial,
-                                  counters, stream);
+        int* ce = counters + sp.ph.counter_ints();
+        int* cd = ce + sp.pe.counter_ints();
+        if (swiglu) {
+            run_product(sp.ph, WRowsGateUp{wg, wu, I, d + ew}, xh, states, d, MakeStoreH{hh, sp.ldh()}, mlp_partial,
+                        counters, stream);
+            run_product(sp.pe, WRowsGateUp{wg + d, wu + d, I, d + ew}, xe, rows, ew,
+                        MakeSwiGLUH{actb, I, hh, sp.ldh(), rt}, mlp_partial, ce, stream);
+        } else {
+            run_product(sp.ph, WRowsPlain{wg, I, d + ew}, xh, states, d, MakeStoreH{hh, sp.ldh()}, mlp_partial,
+                        counters, stream);
+            run_product(sp.pe, WRowsPlain{wg + d, I, d + ew}, xe, rows, ew, MakeSiLUH{actb, I, hh, sp.ldh(), rt},
+                        mlp_partial, ce, stream);
+        }
+        run_product(pd, WRowsPairedK{static_cast<const uint16_t*>(w_down), d, I}, XRowsPlain{actb, 2l * I}, rows,
+                    2 * I, MakeResidual{static_cast<uint16_t*>(hp), hb, d, rt}, mlp_partial, cd, stream);
     } else {
         launch_norms<float>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
                             counters, 0, stream);
@@ -435,7 +439,7 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
 hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int32_t* topk_idx, const void* emb,
                                   const void* gain_h, const void* gain_e, const void* w_lin, int b, int gamma, int d,
                                   int V, int k, float eps, bool bf16, void* ht, void* et, void* hp,
-                                  float* mlp_partial, int* counters, int* diag, hipStream_t stream) {
+                                  float* mlp_partial, int* counters, float* hh, int* diag, hipStream_t stream) {
     const RowTable rt = make_row_table(gamma, k, 0);
     const int rows = b * rt.Rs;
     if (mlp_dma_applies(bf16, b, gamma, rt.Rs, d, 64, d)) {
@@ -451,27 +455,17 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
         return launch_mlp_dma<false, kMlpWPlain, kMlpEpiResidual>(al, pl, stream);
     }
     if (bf16) {
-        const GemmPlan pl = linear_plan(rows, d);
+        // several row blocks: the h~ half once per drafter state, then the e~ half with the residual
+        const int states = b * gamma;
+        const SplitPlans sp = split_plans(2, states, rows, d, d, d);
         launch_norms<uint16_t>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
-                               counters, (int)pl.counter_ints(), stream);
-        WRowsPlain wr{static_cast<const uint16_t*>(w_lin), d, 2 * d};
-        XRowsConcat xc{static_cast<const uint16_t*>(ht), static_cast<const uint16_t*>(et), d, d, rt};
-        const GemmShape sh = pl.shape(rows, 2 * d);
-        uint16_t* hpb = static_cast<uint16_t*>(hp);
-        const uint16_t* hb = static_cast<const uint16_t*>(h);
-        constexpr int S = TF_NW_SINGLE;
-        if (pl.NT == 1)
-            hipLaunchKernelGGL((linear_bf16_kernel<2, 1, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
-                               stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
-        else if (pl.NT == 2)
-            hipLaunchKernelGGL((linear_bf16_kernel<1, 2, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
-                               stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
-        else if (pl.NW == S)
-            hipLaunchKernelGGL((linear_bf16_kernel<1, 4, S, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * S), 0,
-                               stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
-        else
-            hipLaunchKernelGGL((linear_bf16_kernel<1, 4, TF_NW, TF_PIPE_DEFAULT, false>), dim3(sh.G), dim3(64 * TF_NW),
-                               0, stream, wr, xc, sh, hpb, hb, d, rt, mlp_partial, counters);
+                               counters, (int)sp.counter_ints(), stream);
+        const uint16_t* wl = static_cast<const uint16_t*>(w_lin);
+        run_product(sp.ph, WRowsPlain{wl, d, 2 * d}, XRowsPlain{static_cast<const uint16_t*>(ht), d}, states, d,
+                    MakeStoreH{hh, sp.ldh()}, mlp_partial, counters, stream);
+        run_product(sp.pe, WRowsPlain{wl + d, d, 2 * d}, XRowsPlain{static_cast<const uint16_t*>(et), d}, rows, d,
+                    MakeResidualH{static_cast<uint16_t*>(hp), static_cast<const uint16_t*>(h), d, rt, hh, sp.ldh()},
+                    mlp_partial, counters + sp.ph.counter_ints(), stream);
     } else {
         launch_norms<float>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
                             counters, 0, stream);

@@ -266,6 +266,25 @@ inline GemmPlan silu_gate_plan(int rows, int K, int I) { return mlp_plan(rows, c
 inline GemmPlan down_plan(int rows, int d, int I) { return mlp_plan(rows, cdiv(d, 32), 2 * I, TF_DOWN_WORKGROUPS); }
 // the linear approximator: [rows, 2d] x [d, 2d]^T
 inline GemmPlan linear_plan(int rows, int d) { return mlp_plan(rows, cdiv(d, 32), 2 * d, TF_DOWN_WORKGROUPS); }
+// one half (h~ or e~) of the linear layer's input: [rows, d] x [d, d]^T
+inline GemmPlan linear_half_plan(int rows, int d) { return mlp_plan(rows, cdiv(d, 32), d, TF_DOWN_WORKGROUPS); }
+
+// The input projections over several activation row blocks, split at the
+// h~ / e~ boundary of x (Eq. 1): the h~ half once per drafter state
+// ([b*gamma, d] into an fp32 table of ldh() columns), the e~ half for every
+// row (K = ew), whose epilogue adds its state's entry of the table.
+struct SplitPlans {
+    GemmPlan ph, pe;
+    int ldh() const { return ph.ntiles * 32; }
+    size_t fix_floats() const { return ph.fix_floats() > pe.fix_floats() ? ph.fix_floats() : pe.fix_floats(); }
+    size_t counter_ints() const { return ph.counter_ints() + pe.counter_ints(); }
+};
+// kind 0: SwiGLU gate/up, 1: the plain SiLU gate, 2: the linear layer
+inline SplitPlans split_plans(int kind, int states, int rows, int d, int ew, int I) {
+    if (kind == 0) return SplitPlans{gateup_plan(states, d, I), gateup_plan(rows, ew, I)};
+    if (kind == 1) return SplitPlans{silu_gate_plan(states, d, I), silu_gate_plan(rows, ew, I)};
+    return SplitPlans{linear_half_plan(states, d), linear_half_plan(rows, d)};
+}
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -341,14 +360,15 @@ inline size_t lm_scratch_bytes(int rows, int V, int d, bool bf16) {
 }
 
 struct Workspace {
-    size_t diag, lm, ht, et, act, hp, mlp_part, counters, total;
+    size_t diag, lm, ht, et, act, hp, mlp_part, counters, hh, total;
     int ncounters;
 };
 
 // Layout: [diag counters | LM-head scratch (stage 1 or stage 2) | normalised
 // h | normalised embeddings | SwiGLU activation | h' | SwiGLU partial sums |
-// SwiGLU arrival counters].  Stage 1 uses the first two only.  `bigram`
-// sizes the w/ 2-prev rows (two embeddings per row, a 3d-wide input).
+// SwiGLU arrival counters | h~-half table of the split input projections].
+// Stage 1 uses the first two only.  `bigram` sizes the w/ 2-prev rows (two
+// embeddings per row, a 3d-wide input).
 inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, bool bf16, bool bigram = false) {
     const int R = (int)cond_rows(gamma, k, bigram ? 1 : 0);
     const int npre = bigram ? 2 : 1;
@@ -371,16 +391,18 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     off += align256((size_t)rows2 * d * es);
     size_t mp = 0;
     w.ncounters = 0;
+    size_t hhf = 0;
     if (bf16) {
-        const GemmPlan pg = gateup_plan(rows2, (1 + npre) * d, I), pd = down_plan(rows2, d, I),
-                       pl = linear_plan(rows2, d), ps = silu_gate_plan(rows2, (1 + npre) * d, I);
-        const size_t a = pg.fix_floats(), c = pd.fix_floats(), l = pl.fix_floats(), sf = ps.fix_floats();
-        mp = a > c ? a : c;
-        mp = mp > l ? mp : l;
-        mp = mp > sf ? mp : sf;
-        size_t nc = pg.counter_ints() + pd.counter_ints();
-        nc = nc > ps.counter_ints() + pd.counter_ints() ? nc : ps.counter_ints() + pd.counter_ints();
-        nc = nc > pl.counter_ints() ? nc : pl.counter_ints();
+        const SplitPlans sg = split_plans(0, rows1, rows2, d, npre * d, I), ss = split_plans(1, rows1, rows2, d, npre * d, I),
+                         sl = split_plans(2, rows1, rows2, d, d, I);
+        const GemmPlan pd = down_plan(rows2, d, I);
+        const size_t fx[] = {sg.fix_floats(), ss.fix_floats(), sl.fix_floats(), pd.fix_floats()};
+        for (size_t x : fx) mp = mp > x ? mp : x;
+        size_t nc = sg.counter_ints() + pd.counter_ints();
+        nc = nc > ss.counter_ints() + pd.counter_ints() ? nc : ss.counter_ints() + pd.counter_ints();
+        nc = nc > sl.counter_ints() ? nc : sl.counter_ints();
+        const int ldh[] = {sg.ldh(), ss.ldh(), sl.ldh()};
+        for (int x : ldh) hhf = hhf > (size_t)rows1 * x ? hhf : (size_t)rows1 * x;
         if (mlp_dma_applies(bf16, b, gamma, R, d, I, npre * d)) {
             // either the SwiGLU or the SiLU gate plan (the SwiGLU one has more
             // items), the down projection, the linear approximator
@@ -399,6 +421,8 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
     off += align256(mp * 4);
     w.counters = off;
     off += align256((size_t)w.ncounters * 4);
+    w.hh = off;
+    off += align256(hhf * 4);
     w.total = off;
     return w;
 }

@@ -754,6 +754,72 @@ struct EpiSiLU {
     }
 };
 
+// fp32 store of the product: out[r, tile*32 + row of the tile] (the h~
+// half of an input projection, one row per drafter state).
+template <int WM, int NT>
+struct EpiStoreF32 {
+    float* out;
+    int ldo;
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char*,
+                                          const GemmShape& sh) {
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int mt = 0; mt < WM; ++mt) {
+            const int tile = it.t0 + wave * WM + mt;
+            if (tile >= it.t1) continue;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int r = it.row0 + nt * 32 + (lane & 31);
+                if (r >= sh.R) continue;
+#pragma unroll
+                for (int jg = 0; jg < 4; ++jg) {
+                    const int n = tile * 32 + 8 * jg + 4 * (lane >> 5);
+                    *reinterpret_cast<f32x4*>(out + (size_t)r * ldo + n) =
+                        f32x4{acc[mt][nt][4 * jg], acc[mt][nt][4 * jg + 1], acc[mt][nt][4 * jg + 2],
+                              acc[mt][nt][4 * jg + 3]};
+                }
+            }
+        }
+    }
+};
+
+// Adds to every row's product the h~-half product of its drafter state
+// (EpiStoreF32's layout, the same weight tiles), then runs `inner`: the
+// product over x = [h~ ; e~] (Eq. 1) with the h~ half computed once per
+// (sequence, depth).
+template <int WM, int NT, class Inner>
+struct EpiAddH {
+    Inner inner;
+    const float* H;   // [b*gamma, ldh]
+    int ldh;
+    RowTable t;
+    __device__ __forceinline__ void apply(f32x16 (&acc)[WM][NT], const Segment& it, unsigned char* smem,
+                                          const GemmShape& sh) {
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int r = it.row0 + nt * 32 + (lane & 31);
+            if (r >= sh.R) continue;
+            const int s = r / t.Rs;
+            const float* hrow = H + (size_t)(s * t.gamma + t.depth(r - s * t.Rs) - 1) * ldh;
+#pragma unroll
+            for (int mt = 0; mt < WM; ++mt) {
+                const int tile = it.t0 + wave * WM + mt;
+                if (tile >= it.t1) continue;
+#pragma unroll
+                for (int jg = 0; jg < 4; ++jg) {
+                    const f32x4 hv = *reinterpret_cast<const f32x4*>(hrow + tile * 32 + 8 * jg + 4 * (lane >> 5));
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) acc[mt][nt][4 * jg + q] += hv[q];
+                }
+            }
+        }
+        inner.apply(acc, it, smem, sh);
+    }
+};
+
 // Residual: h'[r, n] = bf16( h[seq, depth-1, n] + y[r, n] ).
 template <int WM, int NT>
 struct EpiResidual {
