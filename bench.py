@@ -114,6 +114,10 @@ def parse():
                     "from a rocprofv3 run with SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the HBM traffic summary from FETCH_SIZE and WRITE_SIZE rocprofv3 runs")
+    ap.add_argument("--summarize-mops", metavar="DIR", help="print the bf16 MFMA work per kernel from a rocprofv3 run "
+                    "with SQ_INSTS_VALU_MFMA_MOPS_BF16")
+    ap.add_argument("--summarize-mlp-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the HBM traffic summary of the AR approximator's kernels")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
     ap.add_argument("--sweep", action="store_true",
                     help="drafting cost over budgets B = 16..512 (M = 8) and branchings M = 4..64 (B = 32) "
@@ -257,6 +261,81 @@ def summarize_pmc(args):
     print(f"- traffic {rec['traffic_bytes'] / 1e6:.1f} MB per launch = {rec['traffic_over_algorithmic']:.3f} x the "
           f"algorithmic {alg / 1e6:.1f} MB (lm_head + activation rows)\n")
     print("```json\n" + json.dumps(rec, indent=1) + "\n```")
+
+
+def mlp_kernel_bytes(w):
+    """(regex, label, algorithmic bytes) of the AR approximator's kernels on the
+    one-row-block path: weights, inputs and outputs each counted once."""
+    es = 2 if w.dtype == "bf16" else 4
+    R, S, d, I = w.rows * w.b, w.gamma * w.b, w.d, w.I
+    ew = d
+    nproj = 1 if w.approximator == "silu" else 2
+    gate = nproj * I * (d + ew) * es + (S * d + R * ew) * es + R * 2 * I * es
+    down = d * I * es + R * 2 * I * es + S * d * es + R * d * es
+    norm = S * d * es + R * ew * es + 2 * d * es + (S * d + R * ew) * es
+    return [(r"mlp_dma_kernel<\d+, \d+, false,", "gate/up (or gate) projection: `mlp_dma_kernel<..., false, ...>`", gate),
+            (r"mlp_dma_kernel<\d+, \d+, true,", "down projection: `mlp_dma_kernel<..., true, ...>`", down),
+            (r"rmsnorm_rows", "gather + RMSNorm: `rmsnorm_rows_bf16_kernel`", norm)]
+
+
+def summarize_mlp_pmc(args):
+    """HBM traffic of the AR approximator's kernels, scaled like the LM head's."""
+    w = synth.get_workload(args.workload)
+
+    def per_kernel(path, counter):
+        cur = _db(path).cursor()
+        return {name: (v, n) for name, v, n in cur.execute(
+            "select name, avg(counter_value), count(*) from pmc_events where counter_name = ? group by name",
+            (counter,))}
+
+    fetch = per_kernel(args.summarize_mlp_pmc[0], "FETCH_SIZE")
+    write = per_kernel(args.summarize_mlp_pmc[1], "WRITE_SIZE")
+
+    def pick(d, pat):
+        hits = [(k, v) for k, v in d.items() if re.search(pat, k)]
+        if not hits:
+            raise SystemExit(f"kernel {pat} not found in the counter runs")
+        return max(hits, key=lambda kv: kv[1][0])
+
+    cp_f, cp_w = pick(fetch, "neg"), pick(write, "neg")
+    kib = COPY_BYTES / 1024.0
+    f_fac, w_fac = kib / cp_f[1][0], kib / cp_w[1][0]
+    recs = []
+    for pat, label, alg in mlp_kernel_bytes(w):
+        kf, kw = pick(fetch, pat), pick(write, pat)
+        rd, wr = kf[1][0] * 1024.0 * f_fac, kw[1][0] * 1024.0 * w_fac
+        recs.append({"kernel": kf[0].split("(")[0], "what": label, "dispatches": kf[1][1],
+                     "fetch_size_kib": kf[1][0], "write_size_kib": kw[1][0], "read_bytes": rd, "write_bytes": wr,
+                     "traffic_bytes": rd + wr, "algorithmic_bytes": alg, "traffic_over_algorithmic": (rd + wr) / alg})
+    print(f"# HBM traffic of the AR approximator's kernels, {w.name}\n")
+    print("Two rocprofv3 counter runs of the same bench command, one counter each; the 1 GiB copy "
+          "(torch.neg over float32) that `--copy-calibration` adds gives the factor that turns each counter "
+          "into bytes.  Algorithmic bytes: weights, input rows and outputs, each once (the gate/up activation "
+          "as bf16 hi/lo pairs).\n")
+    print(f"Commands (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
+    print(f"- copy of {COPY_BYTES} B: factors {f_fac:.3f} (read), {w_fac:.3f} (write)")
+    for r in recs:
+        print(f"- {r['what']}: FETCH_SIZE {r['fetch_size_kib']:.0f} KiB, WRITE_SIZE {r['write_size_kib']:.0f} KiB per "
+              f"dispatch ({r['dispatches']} dispatches) -> {r['traffic_bytes'] / 1e6:.1f} MB = "
+              f"{r['traffic_over_algorithmic']:.3f} x the algorithmic {r['algorithmic_bytes'] / 1e6:.1f} MB")
+    print("\n```json\n" + json.dumps({"workload": w.name, "fetch_factor": f_fac, "write_factor": w_fac,
+                                        "kernels": recs}, indent=1) + "\n```")
+
+
+def summarize_mops(args):
+    """bf16 MFMA work per dispatch of every library kernel (SQ_INSTS_VALU_MFMA_MOPS_BF16,
+    512 FLOP per MOP, summed over the counter's instances of a dispatch)."""
+    cur = _db(args.summarize_mops).cursor()
+    per = {}
+    for name, disp, v in cur.execute("select name, dispatch_id, sum(counter_value) from pmc_events "
+                                     "where counter_name = 'SQ_INSTS_VALU_MFMA_MOPS_BF16' group by name, dispatch_id"):
+        if "tf::" in name and v > 0:
+            per.setdefault(name.split("(")[0], []).append(v * 512.0)
+    print(f"# bf16 MFMA work per kernel, {args.workload}\n")
+    print(f"Command (repository root, `cd /tmp && export TMPDIR=/tmp` first):\n\n```\n{args.command}\n```\n")
+    print("| kernel | dispatches | GFLOP per dispatch (median) |\n|---|---|---|")
+    for k, v in sorted(per.items(), key=lambda kv: -sorted(kv[1])[len(kv[1]) // 2]):
+        print(f"| `{k}` | {len(v)} | {sorted(v)[len(v) // 2] / 1e9:.1f} |")
 
 
 def summarize_mfma(args):
@@ -574,6 +653,12 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(args)
+        return
+    if args.summarize_mlp_pmc:
+        summarize_mlp_pmc(args)
+        return
+    if args.summarize_mops:
+        summarize_mops(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
