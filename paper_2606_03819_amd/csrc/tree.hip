@@ -432,11 +432,19 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_kernel(TreeArgs a) {
 // A node's score is the key's float: scores are sums of a +0.0 root score
 // and log-probs, never -0.0, so the key (which folds -0.0 into +0.0) loses
 // nothing.
-constexpr int kLaneSlotsMax = 2;   // frontier slots per lane (B + 1 <= 128)
+constexpr int kLaneSlotsMax = 8;   // frontier slots per lane (B <= 512)
 constexpr int kLaneTabMax = 4;     // table registers (rows and candidates <= 256)
 
-__host__ __device__ inline size_t tree_lane_lds_bytes(int B, int Rs, int K2) {
-    return (size_t)8 * B + (size_t)8 * Rs * K2;
+// LDS of the lane-table kernel: the nodes' parents and ranks, then the
+// leading P ranks of every row (ids and log-probs), P as many as fit.
+__host__ __device__ inline int tree_lane_ranks(int B, int Rs, int K2) {
+    const long long room = (long long)kTreeLdsBudget - 8ll * B;
+    if (room < 8ll * Rs) return 0;
+    const long long P = room / (8ll * Rs);
+    return (int)(P < K2 ? P : K2);
+}
+__host__ __device__ inline size_t tree_lane_lds_bytes(int B, int Rs, int P) {
+    return (size_t)8 * B + (size_t)8 * Rs * P;
 }
 
 // Key of a candidate score: -0.0 keys as +0.0, as cand_before compares.
@@ -456,18 +464,24 @@ __device__ __forceinline__ uint32_t wave_prefix_max_u32(uint32_t v) {
     return v;
 }
 
-template <int FS, int T>
+// FS frontier slots per lane (B <= 64 * FS: a child slot past the last one,
+// opened by the B-th pop, is never popped and is dropped), T table
+// registers; ALL: every rank of every
+// row is in LDS (a.P == a.K2), else ranks from a.P on are read from memory
+// (only when some lane needs one: a ballot guards those loads).
+template <int FS, int T, bool ALL>
 __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs a) {
     extern __shared__ __align__(16) unsigned char dyn[];
-    TreeLds t{};   // parents and ranks of the nodes (for ties), and the rows
+    TreeLds t{};   // parents and ranks of the nodes (for ties), and the rows' leading ranks
     {
         int32_t* p = reinterpret_cast<int32_t*>(dyn);
         t.n_par = p; p += a.B;
         t.n_rank = p; p += a.B;
-        t.c_lp = reinterpret_cast<float*>(p); p += a.Rs * a.K2;
+        t.c_lp = reinterpret_cast<float*>(p); p += a.Rs * a.P;
         t.c_idx = p;
     }
-    const int nent = a.Rs * a.K2;
+    const int nent = a.Rs * a.K2;   // entries in memory
+    const int ncache = a.Rs * a.P;  // entries in LDS
     const int seq = blockIdx.x;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -499,19 +513,24 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
             rfr[r] = rlp[(size_t)min(f, a.Rs - 1) * a.K2];
         }
     }
-    for (int e0 = tid; e0 < nent; e0 += 4 * kTreeThreads) {
+    for (int e0 = tid; e0 < ncache; e0 += 4 * kTreeThreads) {
         float lp[4];
         int ix[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int e = min(e0 + u * kTreeThreads, nent - 1);
-            lp[u] = rlp[e];
-            ix[u] = ridx[e];
+            const int e = min(e0 + u * kTreeThreads, ncache - 1);
+            int ge = e;
+            if constexpr (!ALL) {
+                const int r = e / a.P;
+                ge = r * a.K2 + (e - r * a.P);
+            }
+            lp[u] = rlp[ge];
+            ix[u] = ridx[ge];
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int e = e0 + u * kTreeThreads;
-            if (e < nent) {
+            if (e < ncache) {
                 t.c_lp[e] = lp[u];
                 t.c_idx[e] = ix[u];
             }
@@ -523,12 +542,12 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
     // frontier: slot s = lane + 64*j; key 0 = empty
     uint32_t skey[FS];
     float sps[FS];
-    int sdr[FS], sea[FS], scb[FS];   // sdr = depth << 16 | rank; sea = entry index row*K2 + rank
+    int sdr[FS], sea[FS], slc[FS], scb[FS];   // sdr = depth << 16 | rank; sea / slc = entry index in memory / LDS
 #pragma unroll
     for (int j = 0; j < FS; ++j) {
         skey[j] = 0u;
         sps[j] = 0.f;
-        sdr[j] = sea[j] = scb[j] = 0;
+        sdr[j] = sea[j] = slc[j] = scb[j] = 0;
     }
     {
         const float first = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(rfr[0])));
@@ -546,8 +565,22 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
         float nlpv[FS];
 #pragma unroll
         for (int j = 0; j < FS; ++j) {
-            tokv[j] = t.c_idx[sea[j]];
-            nlpv[j] = t.c_lp[min(sea[j] + 1, nent - 1)];
+            tokv[j] = t.c_idx[min(slc[j], ncache - 1)];
+            nlpv[j] = t.c_lp[min(slc[j] + 1, ncache - 1)];
+        }
+        if constexpr (!ALL) {
+            // ranks past the LDS copy come from memory (a slot at rank P - 1 needs its next log-prob)
+            bool far = false;
+#pragma unroll
+            for (int j = 0; j < FS; ++j) far = far || (skey[j] != 0u && (sdr[j] & 0xffff) + 1 >= a.P);
+            if (__ballot(far) != 0ull) {
+#pragma unroll
+                for (int j = 0; j < FS; ++j) {
+                    const int rk = sdr[j] & 0xffff;
+                    if (skey[j] != 0u && rk >= a.P) tokv[j] = ridx[sea[j]];
+                    if (skey[j] != 0u && rk + 1 >= a.P) nlpv[j] = rlp[min(sea[j] + 1, nent - 1)];
+                }
+            }
         }
         asm volatile("" ::: "memory");   // keep the reads above the maximum
         uint32_t lk = skey[0];
@@ -586,7 +619,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
         }
         // the winning slot's fields
         float g_ps = sps[0], g_nl = nlpv[0];
-        int g_dr = sdr[0], g_cb = scb[0], g_tok = tokv[0], g_ea = sea[0];
+        int g_dr = sdr[0], g_cb = scb[0], g_tok = tokv[0], g_ea = sea[0], g_lc = slc[0];
 #pragma unroll
         for (int j = 1; j < FS; ++j)
             if (j == js) {
@@ -596,6 +629,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
                 g_cb = scb[j];
                 g_tok = tokv[j];
                 g_ea = sea[j];
+                g_lc = slc[j];
             }
         const float score = key_f32(mx);
         const int dr = __builtin_amdgcn_readlane(g_dr, wl);
@@ -636,11 +670,25 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
             const uint32_t ka = score_key(ps + nl);
             if (ka > k2 && ka > ck) {
                 const int ea = __builtin_amdgcn_readlane(g_ea, wl);
+                const int lc = __builtin_amdgcn_readlane(g_lc, wl);
                 // sibling i of this pop in lane i
                 const bool valid = rank + lane < a.K2;
-                const int e = min(ea + lane, nent - 1);
-                const float lpi = t.c_lp[e];
-                const int toki = t.c_idx[e];
+                float lpi;
+                int toki;
+                if (ALL || rank + 63 < a.P) {
+                    const int e = min(lc + lane, ncache - 1);
+                    lpi = t.c_lp[e];
+                    toki = t.c_idx[e];
+                } else {
+                    const int e = min(ea + lane, nent - 1);
+                    const int c = min(lc + lane, ncache - 1);
+                    lpi = t.c_lp[c];
+                    toki = t.c_idx[c];
+                    if (rank + lane >= a.P) {   // past the LDS copy
+                        lpi = rlp[e];
+                        toki = ridx[e];
+                    }
+                }
                 const float si = ps + lpi;
                 const uint32_t ki = valid ? score_key(si) : 0u;
                 int mi = -1;
@@ -660,7 +708,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
                     }
                 }
                 const int crowi = mi >= 0 ? cb + mi : -1;
-                const float cfi = t.c_lp[max(crowi, 0) * a.K2];
+                const float cfi = t.c_lp[max(crowi, 0) * a.P];   // rank 0 of a row is always in LDS
                 const uint32_t cki = crowi >= 0 && valid ? score_key(si + cfi) : 0u;
                 // a sibling is popped if it beats the other slots and every child opened before it
                 const uint32_t before = (uint32_t)__builtin_amdgcn_update_dpp(
@@ -680,19 +728,23 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
                 }
                 // their children into slots n + 1 + i
                 const int ncbi = c0 + c1 * depth + c2 * mi;
+                const int srci_ea = max(crowi, 0) * a.K2, srci_lc = max(crowi, 0) * a.P;
 #pragma unroll
                 for (int j = 0; j < FS; ++j) {
+                    if (64 * j + 63 < n + 1 || 64 * j > n + L) continue;   // no slot of this register changes
                     const int s = lane + 64 * j;
                     const int src = ((s - n - 1) & 63) << 2;
                     const uint32_t pk = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)cki);
                     const float pps = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(si)));
-                    const int pea = __builtin_amdgcn_ds_bpermute(src, max(crowi, 0) * a.K2);
+                    const int pea = __builtin_amdgcn_ds_bpermute(src, srci_ea);
+                    const int plc = __builtin_amdgcn_ds_bpermute(src, srci_lc);
                     const int pcb = __builtin_amdgcn_ds_bpermute(src, ncbi);
                     const bool in = s >= n + 1 && s <= n + L;
                     skey[j] = in ? pk : skey[j];
                     sps[j] = in ? pps : sps[j];
                     sdr[j] = in ? (depth + 1) << 16 : sdr[j];
                     sea[j] = in ? pea : sea[j];
+                    slc[j] = in ? plc : slc[j];
                     scb[j] = in ? pcb : scb[j];
                 }
                 // the slot moves past the run
@@ -703,6 +755,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
                     skey[j] = own ? kl : skey[j];
                     sdr[j] = own ? sdr[j] + L : sdr[j];
                     sea[j] = own ? sea[j] + L : sea[j];
+                    slc[j] = own ? slc[j] + L : slc[j];
                 }
             }
         }
@@ -724,6 +777,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
                 skey[j] = own ? (more ? score_key(ns) : 0u) : skey[j];
                 sdr[j] = own ? sdr[j] + 1 : sdr[j];
                 sea[j] = own ? sea[j] + (more ? 1 : 0) : sea[j];
+                slc[j] = own ? slc[j] + (more ? 1 : 0) : slc[j];
             }
             // an expandable node opens slot n + 1 on the first entry of its row
             if (child_row >= 0) {
@@ -735,6 +789,7 @@ __global__ __launch_bounds__(kTreeThreads) void build_tree_lane_kernel(TreeArgs 
                     sps[j] = ch ? score : sps[j];
                     sdr[j] = ch ? (depth + 1) << 16 : sdr[j];
                     sea[j] = ch ? child_row * a.K2 : sea[j];
+                    slc[j] = ch ? child_row * a.P : slc[j];
                     scb[j] = ch ? ncb : scb[j];
                 }
             }
@@ -776,16 +831,20 @@ hipError_t launch_build_tree(const int32_t* cond_idx, const float* cond_lp, cons
     const bool all = P >= topk2;
     size_t lds_used = lds;
     const int tab = std::max(Rs, mode == kTreeMarginal ? 0 : gamma * M);
-    const size_t lane_lds = tree_lane_lds_bytes(B, Rs, topk2);
-    if (lane_lds <= (size_t)kTreeLdsBudget && B + 1 <= 64 * kLaneSlotsMax && tab <= 64 * kLaneTabMax) {
-        // frontier, candidates and first log-probs in registers
-        lds_used = lane_lds;
-        if (B + 1 <= 64)
-            fn = tab <= 128 ? reinterpret_cast<const void*>(build_tree_lane_kernel<1, 2>)
-                            : reinterpret_cast<const void*>(build_tree_lane_kernel<1, 4>);
-        else
-            fn = tab <= 128 ? reinterpret_cast<const void*>(build_tree_lane_kernel<2, 2>)
-                            : reinterpret_cast<const void*>(build_tree_lane_kernel<2, 4>);
+    const int PL = tree_lane_ranks(B, Rs, topk2);
+    // B slots suffice: the slot the last pop opens is never popped
+    if (PL >= 1 && B <= 64 * kLaneSlotsMax && tab <= 64 * kLaneTabMax) {
+        // frontier, candidates and first log-probs in registers; sibling runs
+        lds_used = tree_lane_lds_bytes(B, Rs, PL);
+        a.P = PL;
+        const bool lall = PL >= topk2, t2 = tab <= 128;
+        const int fs = B <= 64 ? 1 : B <= 128 ? 2 : B <= 256 ? 4 : 8;
+#define TF_LANE(FSV, TV, AV) reinterpret_cast<const void*>(build_tree_lane_kernel<FSV, TV, AV>)
+#define TF_LANE_FS(FSV) (lall ? (t2 ? TF_LANE(FSV, 2, true) : TF_LANE(FSV, 4, true)) \
+                              : (t2 ? TF_LANE(FSV, 2, false) : TF_LANE(FSV, 4, false)))
+        fn = fs == 1 ? TF_LANE_FS(1) : fs == 2 ? TF_LANE_FS(2) : fs == 4 ? TF_LANE_FS(4) : TF_LANE_FS(8);
+#undef TF_LANE_FS
+#undef TF_LANE
     } else if (B + 1 <= 64)
         fn = all ? reinterpret_cast<const void*>(build_tree_reg_kernel<1, true>)
                  : reinterpret_cast<const void*>(build_tree_reg_kernel<1, false>);

@@ -8,12 +8,12 @@ stage-1 candidates of every other sequence drawn from the leading tokens of
 their depth's rows so that the trees run deep.  Each tree must equal the
 oracle's field by field.
 
-The budgets cover every launch shape: the lane-table kernel with one and two
-frontier slots per lane (each at both ends of its range; peaked rows, whose
-trees run deep, and flat rows, whose star-shaped trees are popped in sibling
-runs), the register frontier with four, eight and sixteen slots, the
-LDS-cached rows when the rows do not fit, the LDS frontier, the bigram rows
-of the w/ 2-prev approximator and the marginal rows.  Rows shorter than the budget whose expansions run out
+The budgets cover every launch shape: the lane-table kernel with one, two,
+four and eight frontier slots per lane (each at both ends of its range;
+peaked rows, whose trees run deep, and flat rows, whose star-shaped trees
+are popped in sibling runs), with every row in LDS and with rows longer than
+the LDS copy, the register frontier with sixteen slots, the LDS frontier,
+the bigram rows of the w/ 2-prev approximator and the marginal rows.  Rows shorter than the budget whose expansions run out
 leave the tail of the tree empty (token and parent -1, depth 0, score -inf).
 """
 import numpy as np
@@ -138,7 +138,14 @@ ROW_CASES = [
     ("single", 5, 4, 100, 100, 104, 2, 20, 3.0),
     ("single", 4, 4, 127, 127, 131, 2, 21, 0.5),
     ("bigram", 4, 3, 60, 60, 64, 2, 22, 2.0),
-    ("single", 3, 2, 200, 200, 204, 1, 23, 3.0),   # beyond the run kernel: register frontier
+    ("single", 3, 2, 200, 200, 204, 1, 23, 3.0),
+    # rows longer than the LDS copy (ranks past it read from memory), deep and star-shaped
+    ("single", 16, 8, 200, 200, 210, 1, 24),
+    ("single", 16, 8, 300, 300, 304, 1, 25, 3.0),
+    ("single", 16, 8, 511, 511, 520, 1, 26, 3.0),
+    ("single", 16, 8, 512, 512, 520, 1, 27, 3.0),   # B = 64 * 8: the last pop's child slot is dropped
+    ("single", 4, 3, 64, 64, 70, 2, 28, 0.5),       # B = 64 on one slot per lane
+    ("single", 4, 3, 128, 128, 135, 2, 29, 1.0),
 ]
 
 
