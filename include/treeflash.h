@@ -209,7 +209,12 @@ tf_status_t treeflash_arapprox_expand(const void *h, const int32_t *root_token,
  *   node_child_row  row (0..R-1) holding this node's children, -1 if it is not
  *                   expandable (depth gamma, or not a stage-1 candidate); may be NULL
  * Ties in path score go to the shallower node, then to the lexicographically
- * smaller path of row ranks (rank = position in the parent's sorted row). */
+ * smaller path of row ranks (rank = position in the parent's sorted row).
+ * Rows shorter than the vocabulary (topk2 < B) may hold fewer admissible
+ * nodes than B when they omit a depth's candidates: the selection then stops
+ * when its frontier is empty and the remaining entries read token and parent
+ * -1, depth 0, score -inf, child_row -1 (the count of real nodes is the
+ * number of entries with depth > 0). */
 tf_status_t treeflash_build_tree(const int32_t *cond_idx, const float *cond_logprob,
                                  const int32_t *topk_idx,
                                  int b, int gamma, int k, int topk2, int B,
