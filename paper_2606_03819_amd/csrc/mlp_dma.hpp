@@ -7,9 +7,9 @@
 // reduction range; the range runs in 64-column chunks ("units"), and the
 // units of all items are dealt out in contiguous ranges to G workgroups, so
 // every workgroup streams the same weight bytes.  An item cut by a range
-// boundary is computed in pieces whose accumulators the last piece to arrive
-// sums in workgroup order (the same device-coherent hand-off as the SwiGLU
-// products of several row blocks).
+// boundary is computed in pieces whose sums the last piece to arrive adds
+// in piece order (the same device-coherent hand-off as the SwiGLU products
+// of several row blocks).
 //
 // The reduction range has up to two phases (Eq. 1, x = [h~ ; e~]):
 //   h phase  columns 0..d-1 of W_gate / W_up / W_lin against the b*gamma
@@ -67,6 +67,9 @@ struct MlpDmaArgs {
     int* counter;         // [items] arrival counters, zero before the launch
 };
 
+// 16-byte slot swizzle of 128-byte rows (below)
+__device__ __forceinline__ int mlp_swz128(int r) { return (r >> 1) & 7; }
+
 template <int TG, int NTE, bool PAIRED, int SW, int SX>
 struct MlpDmaTraits {
     static constexpr int NTHREADS = 256;
@@ -105,51 +108,143 @@ struct MlpDmaTraits {
     // 16-byte slot swizzles: 128-byte rows (weights, plain activations) and
     // 256-byte rows (paired activations) keep a quarter-wave's 16 fragment
     // reads at one logical slot on 16 distinct bank groups
-    __device__ static __forceinline__ int swz128(int r) { return (r >> 1) & 7; }
+    __device__ static __forceinline__ int swz128(int r) { return mlp_swz128(r); }
     __device__ static __forceinline__ int swz256(int r) { return r & 15; }
 };
 
-// The item's outputs from its summed accumulators (hs: [TG][1024] h phase,
-// es: [TG][NTE][1024] e phase, both in MFMA register order: value j of lane
-// L is weight row 8(j/4) + 4(L/32) + j%4, activation row L%32).  Row r of
-// sequence s at depth i adds the h-phase sum of drafter state s*gamma+i-1.
-// One thread per (row, tile, group of 8 outputs).
-template <int TG, int NTE, int EPI>
-__device__ __forceinline__ void mlp_dma_epilogue(const MlpDmaArgs& a, int item, const float* hs, const float* es) {
-    constexpr int GPT = EPI == kMlpEpiSwiGLU ? 2 : 4;   // groups of 8 outputs per tile
-    const bool has_h = a.nkh > 0;
-    for (int e = threadIdx.x; e < 32 * NTE * TG * GPT; e += 256) {
-        const int r = e % (32 * NTE);
-        const int tg = e / (32 * NTE);
-        const int t = tg / GPT, q = tg - t * GPT;
-        const int tile = item * TG + t;
-        if (r >= a.Re || tile >= a.ntiles) continue;
-        const int n = r >> 5, c = r & 31;
-        const int sq = r / a.rt.Rs;
-        const int hr = sq * a.rt.gamma + a.rt.depth(r - sq * a.rt.Rs) - 1;
-        const float* E = es + (t * NTE + n) * 1024;
-        const float* H = hs + t * 1024;
-        // value e2 (0..7) of group q sits in register 4q + e2 % 4 of lane c + 32 (e2 / 4)
-        auto sum = [&](int jbase, int e2) {
+// ------------------------------------------------------------------ outputs
+//
+// An item's sums are in MFMA register order: value j of lane L of a 32 x 32
+// tile is weight row 8(j/4) + 4(L/32) + j%4, activation row L%32.  The
+// epilogue walks an item in units of (row, weight tile, group of 8 outputs);
+// a group's 8 sums sit in registers jbase + e2 % 4 of lanes c + 32 (e2 / 4),
+// e2 = 0..7.  Row r of sequence s at depth i adds the h-phase sum of drafter
+// state s*gamma + i - 1.
+
+// An item's sums in LDS: hs [TG][1024] (h phase), es [TG][NTE][1024] (e phase).
+struct MlpLdsSums {
+    const float* hs;
+    const float* es;
+    template <int TG, int NTE, bool HASH>
+    __device__ __forceinline__ void get(int t, int n, int c, int hr, int jbase, float (&v)[8]) const {
+#pragma unroll
+        for (int e2 = 0; e2 < 8; ++e2) {
             const int j = jbase + (e2 & 3), hi = 32 * (e2 >> 2);
-            return E[j * 64 + c + hi] + (has_h ? H[j * 64 + hr + hi] : 0.f);
-        };
-        if constexpr (EPI == kMlpEpiResidual) {
-            const int n0 = tile * 32 + 8 * q;
-            if (n0 >= a.Nout) continue;
-            const u32x4 hv = *reinterpret_cast<const u32x4*>(a.h + (size_t)hr * a.Nout + n0);
+            float x = es[(t * NTE + n) * 1024 + j * 64 + c + hi];
+            if constexpr (HASH) x += hs[t * 1024 + j * 64 + hr + hi];
+            v[e2] = x;
+        }
+    }
+};
+
+// A cut item's sums from its pieces' partial sums in memory (a slot of PF
+// floats: [TG][1024] h phase, then [TG][NTE][1024] e phase), each phase
+// added over the pieces in piece order, then the two phases.  info[p] (LDS)
+// is piece p's slot << 2 | (it covers e chunks) | (it covers h chunks) << 1.
+// The loads of four pieces are in flight together.
+template <int PF>
+struct MlpPieceSums {
+    const float* partial;
+    const int* info;
+    int npieces;
+    template <int TG, int NTE, bool HASH>
+    __device__ __forceinline__ void get(int t, int n, int c, int hr, int jbase, float (&v)[8]) const {
+        float es[8], hs[8];
+#pragma unroll
+        for (int e2 = 0; e2 < 8; ++e2) es[e2] = hs[e2] = 0.f;
+        for (int p0 = 0; p0 < npieces; p0 += 4) {
+            float le[4][8], lh[4][8];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+#pragma unroll
+                for (int e2 = 0; e2 < 8; ++e2) le[k][e2] = lh[k][e2] = 0.f;
+                if (p0 + k < npieces) {
+                    const int f = info[p0 + k];
+                    const float* src = partial + (size_t)(f >> 2) * PF;
+                    if (f & 1) {
+#pragma unroll
+                        for (int e2 = 0; e2 < 8; ++e2)
+                            le[k][e2] = load_coherent(src + TG * 1024 + (t * NTE + n) * 1024 +
+                                                      (jbase + (e2 & 3)) * 64 + c + 32 * (e2 >> 2));
+                    }
+                    if (HASH && (f & 2)) {
+#pragma unroll
+                        for (int e2 = 0; e2 < 8; ++e2)
+                            lh[k][e2] = load_coherent(src + t * 1024 + (jbase + (e2 & 3)) * 64 + hr + 32 * (e2 >> 2));
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int e2 = 0; e2 < 8; ++e2) {
+                    es[e2] += le[k][e2];
+                    hs[e2] += lh[k][e2];
+                }
+        }
+#pragma unroll
+        for (int e2 = 0; e2 < 8; ++e2) v[e2] = HASH ? es[e2] + hs[e2] : es[e2];
+    }
+};
+
+// Outputs of the epilogue units [e0, e1) of `item` (unit e: row e % (32 NTE),
+// tile and group e / (32 NTE)), one unit per thread at a time, from `src`.
+// The residual rows are read before any sum, the sums of a unit are all
+// loaded before the arithmetic.
+template <int TG, int NTE, int EPI, bool HASH, class Src>
+__device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, int e0, int e1, const Src& src) {
+    constexpr int GPT = EPI == kMlpEpiSwiGLU ? 2 : 4;   // groups of 8 outputs per tile
+    constexpr int NIT = (32 * NTE * TG * GPT + 255) / 256;
+    struct Unit {
+        int r, t, q, tile, hr;
+        bool ok;
+    };
+    auto unit = [&](int e) {
+        Unit u;
+        u.r = e % (32 * NTE);
+        const int tg = e / (32 * NTE);
+        u.t = tg / GPT;
+        u.q = tg - u.t * GPT;
+        u.tile = item * TG + u.t;
+        const int o0 = EPI == kMlpEpiSwiGLU ? u.tile * 16 + 8 * u.q : u.tile * 32 + 8 * u.q;
+        u.ok = e < e1 && u.r < a.Re && u.tile < a.ntiles && o0 < a.Nout;
+        const int sq = u.r / a.rt.Rs;
+        u.hr = sq * a.rt.gamma + a.rt.depth(u.r - sq * a.rt.Rs) - 1;
+        return u;
+    };
+    if constexpr (EPI == kMlpEpiResidual) {
+        u32x4 hv[NIT];
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const Unit u = unit(e0 + threadIdx.x + 256 * it);
+            if (u.ok) hv[it] = *reinterpret_cast<const u32x4*>(a.h + (size_t)u.hr * a.Nout + u.tile * 32 + 8 * u.q);
+        }
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const Unit u = unit(e0 + threadIdx.x + 256 * it);
+            if (!u.ok) continue;
+            float v[8];
+            src.template get<TG, NTE, HASH>(u.t, u.r >> 5, u.r & 31, u.hr, 4 * u.q, v);
             u32x4 o;
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                const float y0 = bf16_bits_to_f32(hv[p] & 0xffffu) + sum(4 * q, 2 * p);
-                const float y1 = bf16_bits_to_f32(hv[p] >> 16) + sum(4 * q, 2 * p + 1);
+                const float y0 = bf16_bits_to_f32(hv[it][p] & 0xffffu) + v[2 * p];
+                const float y1 = bf16_bits_to_f32(hv[it][p] >> 16) + v[2 * p + 1];
                 o[p] = f32_to_bf16_bits(y0) | (f32_to_bf16_bits(y1) << 16);
             }
-            *reinterpret_cast<u32x4*>(a.out + (size_t)r * a.Nout + n0) = o;
-        } else {
+            *reinterpret_cast<u32x4*>(a.out + (size_t)u.r * a.Nout + u.tile * 32 + 8 * u.q) = o;
+        }
+    } else {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const Unit u = unit(e0 + threadIdx.x + 256 * it);
+            if (!u.ok) continue;
             // activation i0..i0+7 as bf16 hi/lo pairs interleaved by 8
-            const int i0 = EPI == kMlpEpiSwiGLU ? tile * 16 + 8 * q : tile * 32 + 8 * q;
-            if (i0 >= a.Nout) continue;
+            const int i0 = EPI == kMlpEpiSwiGLU ? u.tile * 16 + 8 * u.q : u.tile * 32 + 8 * u.q;
+            float gv[8], uv[8];
+            src.template get<TG, NTE, HASH>(u.t, u.r >> 5, u.r & 31, u.hr, 4 * u.q, gv);
+            if constexpr (EPI == kMlpEpiSwiGLU)   // up rows 16.. of the tile
+                src.template get<TG, NTE, HASH>(u.t, u.r >> 5, u.r & 31, u.hr, 4 * u.q + 8, uv);
             u32x4 hi4, lo4;
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
@@ -157,16 +252,15 @@ __device__ __forceinline__ void mlp_dma_epilogue(const MlpDmaArgs& a, int item, 
 #pragma unroll
                 for (int z = 0; z < 2; ++z) {
                     const int e2 = 2 * p + z;
-                    const float gv = sum(4 * q, e2);
-                    float av = gv / (1.0f + __expf(-gv));
-                    if constexpr (EPI == kMlpEpiSwiGLU) av *= sum(4 * q + 8, e2);   // up rows 16.. of the tile
+                    float av = gv[e2] / (1.0f + __expf(-gv[e2]));
+                    if constexpr (EPI == kMlpEpiSwiGLU) av *= uv[e2];
                     hb[z] = f32_to_bf16_bits(av);
                     lb[z] = f32_to_bf16_bits(av - bf16_bits_to_f32(hb[z]));
                 }
                 hi4[p] = hb[0] | (hb[1] << 16);
                 lo4[p] = lb[0] | (lb[1] << 16);
             }
-            uint16_t* o = a.out + (size_t)r * 2 * a.Nout + (size_t)(i0 >> 3) * 16;
+            uint16_t* o = a.out + (size_t)u.r * 2 * a.Nout + (size_t)(i0 >> 3) * 16;
             *reinterpret_cast<u32x4*>(o) = hi4;
             *reinterpret_cast<u32x4*>(o + 8) = lo4;
         }
@@ -256,20 +350,59 @@ __device__ __forceinline__ void mlp_step_begin(MlpCursor& cur, bool wcopier, int
     }
 }
 
-template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP, int EPI>
-__global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
+// Piece placement of a cut item: the pieces are workgroups gfirst ..
+// gfirst + npieces - 1.
+struct MlpPieces {
+    int gfirst, npieces;
+};
+__device__ __forceinline__ MlpPieces mlp_pieces(const GemmShape& sh, int item) {
+    const int gfirst = unit_owner(sh, (long long)item * sh.nk);
+    return MlpPieces{gfirst, unit_owner(sh, (long long)item * sh.nk + sh.nk - 1) - gfirst + 1};
+}
+
+__device__ __forceinline__ GemmShape mlp_shape(const MlpDmaArgs& a) {
+    const int nk = a.nkh + a.nke;
+    return GemmShape{a.Re, nk * 64, a.ntiles, a.items, 1, nk, a.G};
+}
+
+// Weight DMA sources of copier cw (rows 16cw..16cw+15 of every tile, two
+// 8-row blocks) at chunk c0 of `item`.
+template <int TG, int WMAP>
+__device__ __forceinline__ void mlp_weight_sources(const MlpDmaArgs& a, int item, int c0, int cw, int lane,
+                                                   const uint16_t* (&wsrc)[TG][2]) {
+    const int lrow = lane >> 3, lslot = lane & 7;
+#pragma unroll
+    for (int t = 0; t < TG; ++t)
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+            const int row = 16 * cw + 8 * hb + lrow;
+            const int tile = min(item * TG + t, a.ntiles - 1);
+            const uint16_t* base;
+            if constexpr (WMAP == kMlpWGateUp) {
+                const int i = min(tile * 16 + (row & 15), a.N - 1);
+                base = (row < 16 ? a.w : a.wu) + (size_t)i * a.Kw;
+            } else {
+                base = a.w + (size_t)min(tile * 32 + row, a.N - 1) * a.Kw;
+            }
+            wsrc[t][hb] = base + 8 * (lslot ^ mlp_swz128(row)) + 64 * c0;
+        }
+}
+
+// One item piece, chunks [c0, c1) of `item`, streamed through the rings in
+// `dyn`.  On return every copy has landed, the LDS is free, and hc / ec hold
+// this thread's part of the piece's sums, the waves' accumulators added in
+// wave order: hc[i] is element tid + 256 i of [TG][1024] (h phase), ec[i]
+// element tid + 256 i of [TG][NTE][1024] (e phase).
+template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP>
+__device__ __forceinline__ void mlp_piece(const MlpDmaArgs& a, int item, int c0, int c1, unsigned char* dyn,
+                                          float (&hc)[4 * TG], float (&ec)[4 * TG * NTE]) {
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
     constexpr int TW = T::TW, NTW = T::NTW;
     static_assert(SX == 3, "two activation chunks in flight");
-    extern __shared__ __align__(16) unsigned char dyn[];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nk = a.nkh + a.nke;
-    const GemmShape sh{a.Re, nk * 64, a.ntiles, a.items, 1, nk, a.G};
-    const int g = xcd_logical_id(blockIdx.x, gridDim.x);
-    const long long u_end = unit_start(sh, g + 1);
-    long long u = unit_start(sh, g);
+    const int nsteps = c1 - c0;
     // this lane's row and physical slot in a 1 KiB DMA block of 128-byte rows
     const int lrow = lane >> 3, lslot = lane & 7;
     // Waves 0-1 copy the weights, waves 2-3 the activations: a wave waits
@@ -282,239 +415,231 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
     const int wa = wave & 1, wb = wave >> 1;
     const int fr = lane & 31;
 
+    // ---- this lane's DMA sources, at chunk c0 of the segment
+    const uint16_t* wsrc[TG][2];
+    mlp_weight_sources<TG, WMAP>(a, item, c0, cw, lane, wsrc);
+    // h phase: 32 rows of h~ in four 8-row blocks, blocks cw and cw + 2
+    const uint16_t* hsrc[2];
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+        const int row = 8 * (cw + 2 * v) + lrow;
+        hsrc[v] = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) + 8 * (lslot ^ T::swz128(row)) +
+                                        64 * c0
+                                  : nullptr;
+    }
+    // e phase: DMA instruction q = cw + 2v covers rows XRPI*q ..
+    const uint16_t* esrc[T::XPW_E];
+    const int ce0 = c0 - a.nkh;   // e chunk of the segment's first chunk (negative in the h phase)
+#pragma unroll
+    for (int v = 0; v < T::XPW_E; ++v) {
+        const int q = cw + 2 * v;
+        int row, ps;
+        if constexpr (PAIRED) {
+            row = 4 * q + (lane >> 4);
+            ps = (lane & 15) ^ T::swz256(row);
+        } else {
+            row = 8 * q + lrow;
+            ps = lslot ^ T::swz128(row);
+        }
+        esrc[v] = a.xe + (size_t)min(row, a.Re - 1) * a.lde + 8 * ps + (long)(PAIRED ? 128 : 64) * ce0;
+    }
+
+    // ---- copies: weights SW - 1 chunks ahead, activations SX - 1
+    MlpCursor cur{0, 0, 0, 0, 0, 0};
+    unsigned char* const wbase = dyn + (2 * cw) * 1024;
+    unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
+
+    f32x16 acc_h[TW], acc_e[TW][NTW];
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            acc_h[t][j] = 0.f;
+#pragma unroll
+            for (int n = 0; n < NTW; ++n) acc_e[t][n][j] = 0.f;
+        }
+
+    // prologue: weights of chunks 0 .. SW-2, activations of chunks 0 .. SX-2
+    if (wcopier) {
+        for (; cur.wnext < SW - 1 && cur.wnext < nsteps; ++cur.wnext)
+            mlp_copy_w<TG>(wsrc, cur.wnext, wbase + cur.wnext * T::WSTAGE, T::WTILE);
+        cur.wstage = cur.wnext % SW;
+    } else {
+        for (; cur.xnext < SX - 1 && cur.xnext < nsteps; ++cur.xnext)
+            mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < a.nkh, cur.xnext, xbase + cur.xnext * T::XSTAGE);
+        cur.xstage = cur.xnext % SX;
+    }
+
+    // The two phases run in loops of their own: each updates only its own
+    // accumulators, so none of them is copied between iterations.  A step
+    // first waits for this wave's copies of chunk s and meets the barrier
+    // (every wave's copies of chunk s have landed; the stages of chunk
+    // s - 1 are free), then refills the freed stages.
+    const int nh = max(0, min(nsteps, a.nkh - c0));   // h-phase chunks of the segment
+    for (int s = 0; s < nh; ++s) {
+        mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
+        const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
+        const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
+        cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
+        cur.rx = cur.rx + 1 == SX ? 0 : cur.rx + 1;
+        // the single activation tile, sub-steps wb and wb + 2
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq) {
+            const int ls = 2 * (wb + 2 * qq) + (lane >> 5);
+            const u32x4 b = *reinterpret_cast<const u32x4*>(xt + fr * 128 + ((ls ^ T::swz128(fr)) << 4));
+#pragma unroll
+            for (int t = 0; t < TW; ++t) {
+                const u32x4 af =
+                    *reinterpret_cast<const u32x4*>(wt + t * T::WTILE + fr * 128 + ((ls ^ T::swz128(fr)) << 4));
+                acc_h[t] = mfma_32x32x16_bf16(af, b, acc_h[t]);
+            }
+        }
+    }
+    for (int s = nh; s < nsteps; ++s) {
+        mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
+        const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
+        const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
+        cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
+        cur.rx = cur.rx + 1 == SX ? 0 : cur.rx + 1;
+        // activation tiles wb*NTW.. over every sub-step (NTE = 1: the
+        // single tile, sub-steps of parity wb)
+        constexpr int QSTEP = NTE >= 2 ? 1 : 2;
+#pragma unroll
+        for (int qq = 0; qq < T::QS / QSTEP; ++qq) {
+            const int q = NTE >= 2 ? qq : wb + 2 * qq;
+            u32x4 b[NTW], af[TW];
+#pragma unroll
+            for (int n = 0; n < NTW; ++n) {
+                const int xr = 32 * (NTE >= 2 ? wb * NTW + n : 0) + fr;
+                const int ls = 2 * q + (lane >> 5);
+                if constexpr (PAIRED)
+                    b[n] = *reinterpret_cast<const u32x4*>(xt + xr * 256 + ((ls ^ T::swz256(xr)) << 4));
+                else
+                    b[n] = *reinterpret_cast<const u32x4*>(xt + xr * 128 + ((ls ^ T::swz128(xr)) << 4));
+            }
+#pragma unroll
+            for (int t = 0; t < TW; ++t) {
+                // paired: sub-step q takes hi (lanes 0-31) and lo (32-63) of weight slot q
+                const int lw = PAIRED ? q : 2 * q + (lane >> 5);
+                af[t] = *reinterpret_cast<const u32x4*>(wt + t * T::WTILE + fr * 128 + ((lw ^ T::swz128(fr)) << 4));
+            }
+#pragma unroll
+            for (int t = 0; t < TW; ++t)
+#pragma unroll
+                for (int n = 0; n < NTW; ++n) acc_e[t][n] = mfma_32x32x16_bf16(af[t], b[n], acc_e[t][n]);
+        }
+    }
+    __syncthreads();   // every copy has landed and every ring read is done
+
+    // ---- the piece's sums (tile t of wave grid column t / TW; waves that
+    // share a tile, along the activation tiles, add in wave order)
+    float* wsc = reinterpret_cast<float*>(dyn);   // [wave][TW][1 + NTW][1024]
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            wsc[((wave * TW + t) * (1 + NTW)) * 1024 + j * 64 + lane] = acc_h[t][j];
+#pragma unroll
+            for (int n = 0; n < NTW; ++n)
+                wsc[((wave * TW + t) * (1 + NTW) + 1 + n) * 1024 + j * 64 + lane] = acc_e[t][n][j];
+        }
+    __syncthreads();
+    auto wslot = [&](int w, int tl, int part) { return wsc + ((w * TW + tl) * (1 + NTW) + part) * 1024; };
+#pragma unroll
+    for (int i = 0; i < T::HC; ++i) {
+        const int e = tid + 256 * i;   // [TG][1024]
+        const int t = e >> 10, f = e & 1023;
+        const int col = t / TW, tl = t % TW;
+        hc[i] = wslot(col, tl, 0)[f] + wslot(2 + col, tl, 0)[f];
+    }
+#pragma unroll
+    for (int i = 0; i < T::EC; ++i) {
+        const int e = tid + 256 * i;   // [TG][NTE][1024]
+        const int t = e / (NTE * 1024), n = (e >> 10) % NTE, f = e & 1023;
+        const int col = t / TW, tl = t % TW;
+        if constexpr (NTE >= 2)
+            ec[i] = wslot((n / NTW) * 2 + col, tl, 1 + n % NTW)[f];
+        else
+            ec[i] = wslot(col, tl, 1)[f] + wslot(2 + col, tl, 1)[f];
+    }
+    __syncthreads();   // the per-wave sums are read; the LDS is free
+}
+
+// A cut item's piece: store its sums (the phases it covers) in its slot and
+// count its arrival.
+template <int TG, int NTE>
+__device__ __forceinline__ void mlp_store_piece(float* slot, bool has_h, bool has_e, const float (&hc)[4 * TG],
+                                                const float (&ec)[4 * TG * NTE]) {
+    const int tid = threadIdx.x;
+    if (has_h) {
+#pragma unroll
+        for (int i = 0; i < 4 * TG; ++i) store_coherent(slot + tid + 256 * i, hc[i]);
+    }
+    if (has_e) {
+#pragma unroll
+        for (int i = 0; i < 4 * TG * NTE; ++i) store_coherent(slot + TG * 1024 + tid + 256 * i, ec[i]);
+    }
+}
+
+// Every item piece of this workgroup's range; a cut item is summed by its
+// last piece to arrive, in piece order, then written by the epilogue.
+template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP, int EPI>
+__global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
+    using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
+    constexpr int NE = 32 * NTE * TG * (EPI == kMlpEpiSwiGLU ? 2 : 4);
+    constexpr bool HASH = !PAIRED;   // the down projection alone has no h phase
+    extern __shared__ __align__(16) unsigned char dyn[];
+    const int tid = threadIdx.x;
+    const GemmShape sh = mlp_shape(a);
+    const int nk = sh.nk;
+    const int g = xcd_logical_id(blockIdx.x, gridDim.x);
+    const long long u_end = unit_start(sh, g + 1);
+    long long u = unit_start(sh, g);
     while (u < u_end) {
         const int item = (int)(u / nk);
         const int c0 = (int)(u - (long long)item * nk);
         const int c1 = (int)min((long long)nk, u_end - (long long)item * nk);
-        const int nsteps = c1 - c0;
-
-        // ---- this lane's DMA sources, at chunk c0 of the segment
-        // weights: copier cw copies rows 16cw..16cw+15 of every tile (two 8-row blocks)
-        const uint16_t* wsrc[TG][2];
-#pragma unroll
-        for (int t = 0; t < TG; ++t)
-#pragma unroll
-            for (int hb = 0; hb < 2; ++hb) {
-                const int row = 16 * cw + 8 * hb + lrow;
-                const int tile = min(item * TG + t, a.ntiles - 1);
-                const uint16_t* base;
-                if constexpr (WMAP == kMlpWGateUp) {
-                    const int i = min(tile * 16 + (row & 15), a.N - 1);
-                    base = (row < 16 ? a.w : a.wu) + (size_t)i * a.Kw;
-                } else {
-                    base = a.w + (size_t)min(tile * 32 + row, a.N - 1) * a.Kw;
-                }
-                wsrc[t][hb] = base + 8 * (lslot ^ T::swz128(row)) + 64 * c0;
-            }
-        // h phase: 32 rows of h~ in four 8-row blocks, blocks cw and cw + 2
-        const uint16_t* hsrc[2];
-#pragma unroll
-        for (int v = 0; v < 2; ++v) {
-            const int row = 8 * (cw + 2 * v) + lrow;
-            hsrc[v] = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) +
-                                            8 * (lslot ^ T::swz128(row)) + 64 * c0
-                                      : nullptr;
-        }
-        // e phase: DMA instruction q = cw + 2v covers rows XRPI*q ..
-        const uint16_t* esrc[T::XPW_E];
-        const int ce0 = c0 - a.nkh;   // e chunk of the segment's first chunk (negative in the h phase)
-#pragma unroll
-        for (int v = 0; v < T::XPW_E; ++v) {
-            const int q = cw + 2 * v;
-            int row, ps;
-            if constexpr (PAIRED) {
-                row = 4 * q + (lane >> 4);
-                ps = (lane & 15) ^ T::swz256(row);
-            } else {
-                row = 8 * q + lrow;
-                ps = lslot ^ T::swz128(row);
-            }
-            esrc[v] = a.xe + (size_t)min(row, a.Re - 1) * a.lde + 8 * ps + (long)(PAIRED ? 128 : 64) * ce0;
-        }
-
-        // ---- copies: weights SW - 1 chunks ahead, activations SX - 1
-        MlpCursor cur{0, 0, 0, 0, 0, 0};
-        unsigned char* const wbase = dyn + (2 * cw) * 1024;
-        unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
-
-        f32x16 acc_h[TW], acc_e[TW][NTW];
-#pragma unroll
-        for (int t = 0; t < TW; ++t)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                acc_h[t][j] = 0.f;
-#pragma unroll
-                for (int n = 0; n < NTW; ++n) acc_e[t][n][j] = 0.f;
-            }
-
-        // prologue: weights of chunks 0 .. SW-2, activations of chunks 0 .. SX-2
-        if (wcopier) {
-            for (; cur.wnext < SW - 1 && cur.wnext < nsteps; ++cur.wnext)
-                mlp_copy_w<TG>(wsrc, cur.wnext, wbase + cur.wnext * T::WSTAGE, T::WTILE);
-            cur.wstage = cur.wnext % SW;
-        } else {
-            for (; cur.xnext < SX - 1 && cur.xnext < nsteps; ++cur.xnext)
-                mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < a.nkh, cur.xnext,
-                                             xbase + cur.xnext * T::XSTAGE);
-            cur.xstage = cur.xnext % SX;
-        }
-
-        // The two phases run in loops of their own: each updates only its own
-        // accumulators, so none of them is copied between iterations.  A step
-        // first waits for this wave's copies of chunk s and meets the barrier
-        // (every wave's copies of chunk s have landed; the stages of chunk
-        // s - 1 are free), then refills the freed stages.
-        const int nh = max(0, min(nsteps, a.nkh - c0));   // h-phase chunks of the segment
-        for (int s = 0; s < nh; ++s) {
-            mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
-            const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
-            const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
-            cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
-            cur.rx = cur.rx + 1 == SX ? 0 : cur.rx + 1;
-            // the single activation tile, sub-steps wb and wb + 2
-#pragma unroll
-            for (int qq = 0; qq < 2; ++qq) {
-                const int ls = 2 * (wb + 2 * qq) + (lane >> 5);
-                const u32x4 b = *reinterpret_cast<const u32x4*>(xt + fr * 128 + ((ls ^ T::swz128(fr)) << 4));
-#pragma unroll
-                for (int t = 0; t < TW; ++t) {
-                    const u32x4 af = *reinterpret_cast<const u32x4*>(wt + t * T::WTILE + fr * 128 +
-                                                                     ((ls ^ T::swz128(fr)) << 4));
-                    acc_h[t] = mfma_32x32x16_bf16(af, b, acc_h[t]);
-                }
-            }
-        }
-        for (int s = nh; s < nsteps; ++s) {
-            mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
-            const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
-            const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
-            cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
-            cur.rx = cur.rx + 1 == SX ? 0 : cur.rx + 1;
-            // activation tiles wb*NTW.. over every sub-step (NTE = 1: the
-            // single tile, sub-steps of parity wb)
-            constexpr int QSTEP = NTE >= 2 ? 1 : 2;
-#pragma unroll
-            for (int qq = 0; qq < T::QS / QSTEP; ++qq) {
-                const int q = NTE >= 2 ? qq : wb + 2 * qq;
-                u32x4 b[NTW], af[TW];
-#pragma unroll
-                for (int n = 0; n < NTW; ++n) {
-                    const int xr = 32 * (NTE >= 2 ? wb * NTW + n : 0) + fr;
-                    const int ls = 2 * q + (lane >> 5);
-                    if constexpr (PAIRED)
-                        b[n] = *reinterpret_cast<const u32x4*>(xt + xr * 256 + ((ls ^ T::swz256(xr)) << 4));
-                    else
-                        b[n] = *reinterpret_cast<const u32x4*>(xt + xr * 128 + ((ls ^ T::swz128(xr)) << 4));
-                }
-#pragma unroll
-                for (int t = 0; t < TW; ++t) {
-                    // paired: sub-step q takes hi (lanes 0-31) and lo (32-63) of weight slot q
-                    const int lw = PAIRED ? q : 2 * q + (lane >> 5);
-                    af[t] = *reinterpret_cast<const u32x4*>(wt + t * T::WTILE + fr * 128 + ((lw ^ T::swz128(fr)) << 4));
-                }
-#pragma unroll
-                for (int t = 0; t < TW; ++t)
-#pragma unroll
-                    for (int n = 0; n < NTW; ++n) acc_e[t][n] = mfma_32x32x16_bf16(af[t], b[n], acc_e[t][n]);
-            }
-        }
-        __syncthreads();   // every copy has landed and every ring read is done
-
-        // ---- the item's sums (tile t of wave grid column t / TW; waves that
-        // share a tile, along the activation tiles, add in wave order)
-        float* wsc = reinterpret_cast<float*>(dyn);   // [wave][TW][1 + NTW][1024]
-#pragma unroll
-        for (int t = 0; t < TW; ++t)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                wsc[((wave * TW + t) * (1 + NTW)) * 1024 + j * 64 + lane] = acc_h[t][j];
-#pragma unroll
-                for (int n = 0; n < NTW; ++n) wsc[((wave * TW + t) * (1 + NTW) + 1 + n) * 1024 + j * 64 + lane] = acc_e[t][n][j];
-            }
-        __syncthreads();
-        auto wslot = [&](int w, int tl, int part) { return wsc + ((w * TW + tl) * (1 + NTW) + part) * 1024; };
         float hc[T::HC], ec[T::EC];
-#pragma unroll
-        for (int i = 0; i < T::HC; ++i) {
-            const int e = tid + 256 * i;   // [TG][1024]
-            const int t = e >> 10, f = e & 1023;
-            const int col = t / TW, tl = t % TW;
-            hc[i] = wslot(col, tl, 0)[f] + wslot(2 + col, tl, 0)[f];
-        }
-#pragma unroll
-        for (int i = 0; i < T::EC; ++i) {
-            const int e = tid + 256 * i;   // [TG][NTE][1024]
-            const int t = e / (NTE * 1024), n = (e >> 10) % NTE, f = e & 1023;
-            const int col = t / TW, tl = t % TW;
-            if constexpr (NTE >= 2)
-                ec[i] = wslot((n / NTW) * 2 + col, tl, 1 + n % NTW)[f];
-            else
-                ec[i] = wslot(col, tl, 1)[f] + wslot(2 + col, tl, 1)[f];
-        }
-        __syncthreads();   // the per-wave sums are read; their LDS takes the item's sums below
+        mlp_piece<TG, NTE, PAIRED, SW, SX, WMAP>(a, item, c0, c1, dyn, hc, ec);
 
-        // ---- a cut item: store this piece (its phases only); the last to arrive sums them
-        const int gfirst = unit_owner(sh, (long long)item * nk);
-        const int npieces = unit_owner(sh, (long long)item * nk + nk - 1) - gfirst + 1;
+        // ---- a cut item: store this piece; the last to arrive sums them
+        const MlpPieces pcs = mlp_pieces(sh, item);
         float* csc = reinterpret_cast<float*>(dyn);   // [TG][1024] h, then [TG][NTE][1024] e
         bool last = true;
-        if (npieces > 1) {
-            float* mine = a.partial + (size_t)piece_slot(sh, g, item) * T::PF;
-            if (c0 < a.nkh) {
-#pragma unroll
-                for (int i = 0; i < T::HC; ++i) store_coherent(mine + tid + 256 * i, hc[i]);
-            }
-            if (c1 > a.nkh) {
-#pragma unroll
-                for (int i = 0; i < T::EC; ++i) store_coherent(mine + T::HC * 256 + tid + 256 * i, ec[i]);
-            }
+        if (pcs.npieces > 1) {
+            mlp_store_piece<TG, NTE>(a.partial + (size_t)piece_slot(sh, g, item) * T::PF, c0 < a.nkh, c1 > a.nkh, hc,
+                                     ec);
             wait_memory();
             __syncthreads();   // every thread's piece is stored
             int* flag = reinterpret_cast<int*>(csc);
             if (tid == 0)
                 flag[0] = __hip_atomic_fetch_add(a.counter + item, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                                  npieces - 1
+                                  pcs.npieces - 1
                               ? 1
                               : 0;
             __syncthreads();
             last = flag[0] != 0;
             __syncthreads();
             if (last) {
-#pragma unroll
-                for (int i = 0; i < T::HC; ++i) hc[i] = 0.f;
-#pragma unroll
-                for (int i = 0; i < T::EC; ++i) ec[i] = 0.f;
+                // this piece's info, then the epilogue over the pieces' sums
+                int* info = reinterpret_cast<int*>(csc);
                 const long long ib = (long long)item * nk;
-                for (int pc = 0; pc < npieces; ++pc) {
-                    // chunks [p0, p1) of the item held by piece pc
-                    const int gp = gfirst + pc;
+                if (tid < pcs.npieces) {
+                    const int gp = pcs.gfirst + tid;
                     const int p0 = (int)max(0ll, unit_start(sh, gp) - ib);
                     const int p1 = (int)min((long long)nk, unit_start(sh, gp + 1) - ib);
-                    const float* src = a.partial + (size_t)piece_slot(sh, gp, item) * T::PF;
-                    if (p0 < a.nkh) {
-                        float v[T::HC];
-#pragma unroll
-                        for (int i = 0; i < T::HC; ++i) v[i] = load_coherent(src + tid + 256 * i);
-#pragma unroll
-                        for (int i = 0; i < T::HC; ++i) hc[i] += v[i];
-                    }
-                    if (p1 > a.nkh) {
-                        float v[T::EC];
-#pragma unroll
-                        for (int i = 0; i < T::EC; ++i) v[i] = load_coherent(src + T::HC * 256 + tid + 256 * i);
-#pragma unroll
-                        for (int i = 0; i < T::EC; ++i) ec[i] += v[i];
-                    }
+                    info[tid] = (piece_slot(sh, gp, item) << 2) | (p1 > a.nkh ? 1 : 0) | (p0 < a.nkh ? 2 : 0);
                 }
+                __syncthreads();
+                mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpPieceSums<T::PF>{a.partial, info, pcs.npieces});
             }
-        }
-        if (last) {
+        } else {
 #pragma unroll
             for (int i = 0; i < T::HC; ++i) csc[tid + 256 * i] = hc[i];
 #pragma unroll
             for (int i = 0; i < T::EC; ++i) csc[T::HC * 256 + tid + 256 * i] = ec[i];
             __syncthreads();
-            mlp_dma_epilogue<TG, NTE, EPI>(a, item, csc, csc + T::HC * 256);
+            mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
         }
         u = (long long)(item + 1) * nk;
         if (u < u_end) __syncthreads();   // the epilogue's LDS use ends before the next item's copies land

@@ -4,7 +4,9 @@ MLP without an up projection) on every launch path:
 * one row block (at most 128 conditional rows, 32 drafter states, widths a
   multiple of 64): the LDS-DMA kernels, with the h~ half of W_gate/W_up
   computed once per drafter state -- one, two and four activation tiles,
-  items cut between workgroups and several whole items per workgroup;
+  items cut between workgroups and several whole items per workgroup; the
+  inputs normalised by whole 16-byte pieces, or element by element when the
+  embedding or a gain is not 16-byte aligned;
 * several row blocks, or widths that are not a multiple of 64: the
   register-staged products;
 * fp32.
@@ -109,6 +111,29 @@ def test_hprime_matches_oracle(w, std):
     # a second call on the same workspace (arrival counters reset by the call)
     ratio2 = check_hprime(w, g, o_in, seeded_candidates(w, w.state_seed + 1))
     print(f"[mlp] {w.name}: worst error / bound {max(ratio, ratio2):.3f}", flush=True)
+
+
+def misaligned(t):
+    """A copy of `t` at an address 2 bytes past a 16-byte boundary (element aligned only)."""
+    flat = torch.empty(t.numel() + 8, dtype=t.dtype, device=t.device)
+    view = flat[1:1 + t.numel()].view(t.shape)
+    view.copy_(t)
+    assert view.data_ptr() % 16 == 2
+    return view
+
+
+@pytest.mark.parametrize("which", ["emb", "norm_e_gain"])
+def test_hprime_misaligned_inputs(which):
+    """An embedding table or gain that is element aligned only: the normalisation reads them element by
+    element."""
+    w, std = CASES[0]
+    print(f"[mlp] h' case={w.name} with {which} misaligned", flush=True)
+    cpu = synth.make_inputs(w, "cpu", weight_std=std)
+    g = {k: v.cuda() for k, v in cpu.items()}
+    g[which] = misaligned(g[which])
+    o_in = oracle_inputs(cpu)
+    ratio = check_hprime(w, g, o_in, seeded_candidates(w, w.state_seed + 2))
+    print(f"[mlp] {w.name} ({which} misaligned): worst error / bound {ratio:.3f}", flush=True)
 
 
 SILU_DRAFTS = [c for c in CASES if c[0].approximator == "silu"]
