@@ -56,4 +56,5 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+
 }  // namespace tf

@@ -273,7 +273,7 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
         }
         __syncthreads();  // ring reads done before the epilogue reuses the LDS
         epi.apply(acc, seg, dyn, se);
-        __syncthreads();  // the epilogue's LDS use ends before the next round's copies land
+        lds_barrier();  // the epilogue's LDS use ends before the next round's copies land
     }
 }
 

@@ -300,7 +300,7 @@ __device__ __forceinline__ void stream_gemm(const WSrc& wsrc, const XSrc& xsrc, 
         __syncthreads();  // LDS tiles no longer needed
         epi.apply(acc, seg, smem, sh);
         u = (long long)(seg.item + 1) * sh.nk;
-        if (u < u_end) __syncthreads();  // the epilogue's LDS use ends before the next tiles land
+        if (u < u_end) lds_barrier();  // the epilogue's LDS use ends before the next tiles land
     }
 }
 
@@ -379,7 +379,8 @@ struct XRowsConcat {
 // least every value the contributor saw but did not list) into the row's
 // (row, slice) partial of KEEP entries.  One thread per row.
 template <int NC, int KL, int KEEP = kKeep>
-__device__ inline void lm_merge_contributors(const float* cm, int rstride, int rows, int row0, int split, int nsplit,
+__device__ __forceinline__ void lm_merge_contributors(const float* cm, int rstride, int rows, int row0, int split,
+                                                      int nsplit,
                                              int R, float sl2, float* part) {
     constexpr int W = 3 + 2 * KL;
     const int tid = threadIdx.x;
@@ -562,7 +563,7 @@ struct EpiLmHead {
         const int vbase0 = tw * 32 + 4 * (lane >> 5);
 #pragma unroll
         for (int nt = 0; nt < NTW; ++nt) lane_row(acc, nt, vbase0, tw, it.t1, crow + nt * 32 * RSTRIDE);
-        __syncthreads();
+        lds_barrier();
         lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
 };
