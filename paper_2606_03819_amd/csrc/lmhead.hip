@@ -60,7 +60,7 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
         gemm_segment<WM, NT, NW, PIPE, WNT>(ws, xs, sh, seg, acc, smem);
         __syncthreads();  // LDS tiles no longer needed
         epi.apply(acc, seg, smem, se);
-        __syncthreads();  // the epilogue's LDS use ends before the next round's tiles land
+        lds_barrier();  // the epilogue's LDS use ends before the next round's tiles land
     }
 }
 
