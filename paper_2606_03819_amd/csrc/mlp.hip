@@ -160,65 +160,66 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void product_bf16_kernel(
 
 // ------------------------------------------------------------------ fp32
 
-// x_r = [ht(depth) ; et(r)] is K = d + ew wide.
-__global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ wg, const float* wu,
-                                                         const float* __restrict__ ht, const float* __restrict__ et,
-                                                         int rows, int d, int ew, int I, RowTable rt,
-                                                         float* __restrict__ act) {
-    const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
-    const int i = blockIdx.x * 64 + (threadIdx.x & 63);
-    if (r >= rows || i >= I) return;
-    const int s = r / rt.Rs;
-    const int rl = r - s * rt.Rs;
-    const int K = d + ew;
-    const float* hr = ht + (size_t)(s * rt.gamma + rt.depth(rl) - 1) * d;
-    const float* er = et + (size_t)r * ew;
-    const float* g_row = wg + (size_t)i * K;
-    float g = 0.f;
-    for (int k = 0; k < d; ++k) g = fmaf(hr[k], g_row[k], g);
-    for (int k = 0; k < ew; ++k) g = fmaf(er[k], g_row[d + k], g);
-    float a = g / (1.0f + expf(-g));
-    if (wu != nullptr) {   // SwiGLU; without it the plain SiLU MLP
-        const float* u_row = wu + (size_t)i * K;
-        float u = 0.f;
-        for (int k = 0; k < d; ++k) u = fmaf(hr[k], u_row[k], u);
-        for (int k = 0; k < ew; ++k) u = fmaf(er[k], u_row[d + k], u);
-        a *= u;
+// The approximator's fp32 products (small models): out[r, n] = epi( x_r . W[n] )
+// with x_r = [x0 row of r's drafter state (d0 wide) ; x1 row r (K - d0 wide)].
+// A workgroup holds 16 rows x 16 output columns; the reduction range streams
+// through LDS in 64-wide chunks (every thread copies four activation and four
+// weight values per chunk, consecutive threads consecutive k), and each
+// thread accumulates its output with one fmaf chain in k order.
+//   GATE:  act = silu(x . W_gate[n]) * (x . W_up[n])  (W_up null: silu alone)
+//   else:  out = h[r's drafter state, n] + x . W[n]   (down projection, linear)
+template <bool GATE>
+__global__ __launch_bounds__(256) void mlp_f32_kernel(const float* __restrict__ wa, const float* __restrict__ wb,
+                                                      int N, int K, const float* __restrict__ x0, int d0,
+                                                      const float* __restrict__ x1, int ld1, RowTable rt, int rows,
+                                                      const float* __restrict__ h, float* __restrict__ out,
+                                                      int ldo) {
+    __shared__ float xs[16][65];
+    __shared__ float ws[2][16][65];
+    const int tid = threadIdx.x;
+    const int n0 = blockIdx.x * 16, r0 = blockIdx.y * 16;
+    const int tx = tid & 15, ty = tid >> 4;
+    const bool two = GATE && wb != nullptr;
+    // the x0 row (drafter state) of each of the tile's rows
+    auto state_of = [&](int r) {
+        const int s = r / rt.Rs;
+        return s * rt.gamma + rt.depth(r - s * rt.Rs) - 1;
+    };
+    float acc_a = 0.f, acc_b = 0.f;
+    for (int k0 = 0; k0 < K; k0 += 64) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = tid + 256 * j;
+            const int rr = e >> 6, kk = e & 63, k = k0 + kk;
+            const int r = r0 + rr, n = n0 + rr;
+            float xv = 0.f, wv = 0.f, wv2 = 0.f;
+            if (r < rows && k < K) xv = k < d0 ? x0[(size_t)state_of(r) * d0 + k] : x1[(size_t)r * ld1 + (k - d0)];
+            if (n < N && k < K) {
+                wv = wa[(size_t)n * K + k];
+                if (two) wv2 = wb[(size_t)n * K + k];
+            }
+            xs[rr][kk] = xv;
+            ws[0][rr][kk] = wv;
+            ws[1][rr][kk] = wv2;
+        }
+        __syncthreads();
+        const int kn = min(64, K - k0);
+        for (int kk = 0; kk < kn; ++kk) {
+            const float xv = xs[ty][kk];
+            acc_a = fmaf(xv, ws[0][tx][kk], acc_a);
+            if (two) acc_b = fmaf(xv, ws[1][tx][kk], acc_b);
+        }
+        __syncthreads();
     }
-    act[(size_t)r * I + i] = a;
-}
-
-__global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__ wd, const float* __restrict__ act,
-                                                       const float* __restrict__ h, int rows, int d, int I,
-                                                       RowTable rt, float* __restrict__ hp) {
-    const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
-    const int n = blockIdx.x * 64 + (threadIdx.x & 63);
-    if (r >= rows || n >= d) return;
-    const int s = r / rt.Rs;
-    const int rl = r - s * rt.Rs;
-    const float* ar = act + (size_t)r * I;
-    const float* wr = wd + (size_t)n * I;
-    float y = 0.f;
-    for (int i = 0; i < I; ++i) y = fmaf(ar[i], wr[i], y);
-    hp[(size_t)r * d + n] = h[(size_t)(s * rt.gamma + rt.depth(rl) - 1) * d + n] + y;
-}
-
-__global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict__ wl, const float* __restrict__ ht,
-                                                         const float* __restrict__ et, const float* __restrict__ h,
-                                                         int rows, int d, RowTable rt, float* __restrict__ hp) {
-    const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
-    const int n = blockIdx.x * 64 + (threadIdx.x & 63);
-    if (r >= rows || n >= d) return;
-    const int s = r / rt.Rs;
-    const int rl = r - s * rt.Rs;
-    const int hrow = s * rt.gamma + rt.depth(rl) - 1;
-    const float* hr = ht + (size_t)hrow * d;
-    const float* er = et + (size_t)r * d;
-    const float* w = wl + (size_t)n * 2 * d;
-    float y = 0.f;
-    for (int k = 0; k < d; ++k) y = fmaf(hr[k], w[k], y);
-    for (int k = 0; k < d; ++k) y = fmaf(er[k], w[d + k], y);
-    hp[(size_t)r * d + n] = h[(size_t)hrow * d + n] + y;
+    const int r = r0 + ty, n = n0 + tx;
+    if (r >= rows || n >= N) return;
+    if constexpr (GATE) {
+        float a = acc_a / (1.0f + expf(-acc_a));
+        if (two) a *= acc_b;
+        out[(size_t)r * ldo + n] = a;
+    } else {
+        out[(size_t)r * ldo + n] = h[(size_t)state_of(r) * N + n] + acc_a;
+    }
 }
 
 // ------------------------------------------------------------------ launcher
@@ -425,13 +426,14 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
     } else {
         launch_norms<float>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et, diag,
                             counters, 0, stream);
-        hipLaunchKernelGGL(gateup_f32_kernel, dim3(cdiv(I, 64), cdiv(rows, 4)), dim3(256), 0, stream,
-                           static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
-                           static_cast<const float*>(ht), static_cast<const float*>(et), rows, d, ew, I, rt,
-                           static_cast<float*>(act));
-        hipLaunchKernelGGL(down_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
-                           static_cast<const float*>(w_down), static_cast<const float*>(act),
-                           static_cast<const float*>(h), rows, d, I, rt, static_cast<float*>(hp));
+        hipLaunchKernelGGL(mlp_f32_kernel<true>, dim3(cdiv(I, 16), cdiv(rows, 16)), dim3(256), 0, stream,
+                           static_cast<const float*>(w_gate), static_cast<const float*>(w_up), I, d + ew,
+                           static_cast<const float*>(ht), d, static_cast<const float*>(et), ew, rt, rows, nullptr,
+                           static_cast<float*>(act), I);
+        hipLaunchKernelGGL(mlp_f32_kernel<false>, dim3(cdiv(d, 16), cdiv(rows, 16)), dim3(256), 0, stream,
+                           static_cast<const float*>(w_down), nullptr, d, I, nullptr, 0,
+                           static_cast<const float*>(act), I, rt, rows, static_cast<const float*>(h),
+                           static_cast<float*>(hp), d);
     }
     return hipGetLastError();
 }
@@ -469,10 +471,10 @@ hipError_t launch_arapprox_linear(const void* h, const int32_t* root, const int3
     } else {
         launch_norms<float>(h, root, nullptr, topk_idx, emb, gain_h, gain_e, b, d, V, rt, 1, eps, ht, et, diag,
                             counters, 0, stream);
-        hipLaunchKernelGGL(linear_f32_kernel, dim3(cdiv(d, 64), cdiv(rows, 4)), dim3(256), 0, stream,
-                           static_cast<const float*>(w_lin), static_cast<const float*>(ht),
-                           static_cast<const float*>(et), static_cast<const float*>(h), rows, d, rt,
-                           static_cast<float*>(hp));
+        hipLaunchKernelGGL(mlp_f32_kernel<false>, dim3(cdiv(d, 16), cdiv(rows, 16)), dim3(256), 0, stream,
+                           static_cast<const float*>(w_lin), nullptr, d, 2 * d, static_cast<const float*>(ht), d,
+                           static_cast<const float*>(et), d, rt, rows, static_cast<const float*>(h),
+                           static_cast<float*>(hp), d);
     }
     return hipGetLastError();
 }
