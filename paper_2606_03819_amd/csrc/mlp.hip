@@ -164,8 +164,9 @@ __global__ __launch_bounds__(64 * NW, 512 / (64 * NW)) void product_bf16_kernel(
 // with x_r = [x0 row of r's drafter state (d0 wide) ; x1 row r (K - d0 wide)].
 // A workgroup holds 16 rows x 16 output columns; the reduction range streams
 // through LDS in 64-wide chunks (every thread copies four activation and four
-// weight values per chunk, consecutive threads consecutive k), and each
-// thread accumulates its output with one fmaf chain in k order.
+// weight values per chunk, consecutive threads consecutive k, the next
+// chunk's loads in flight while this one is multiplied), and each thread
+// accumulates its output with one fmaf chain in k order.
 //   GATE:  act = silu(x . W_gate[n]) * (x . W_up[n])  (W_up null: silu alone)
 //   else:  out = h[r's drafter state, n] + x . W[n]   (down projection, linear)
 template <bool GATE>
@@ -185,24 +186,40 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(const float* __restrict__ 
         const int s = r / rt.Rs;
         return s * rt.gamma + rt.depth(r - s * rt.Rs) - 1;
     };
+    // this thread's copies of a chunk: rows (and weight rows) e / 64, k e % 64, e = tid + 256 j
+    int xrow[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int r = r0 + ((tid + 256 * j) >> 6);
+        xrow[j] = r < rows ? state_of(r) : -1;
+    }
+    float px[4], pw[4], pw2[4];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = tid + 256 * j;
+            const int rr = e >> 6, k = k0 + (e & 63);
+            const int r = r0 + rr, n = n0 + rr;
+            px[j] = pw[j] = pw2[j] = 0.f;
+            if (xrow[j] >= 0 && k < K) px[j] = k < d0 ? x0[(size_t)xrow[j] * d0 + k] : x1[(size_t)r * ld1 + (k - d0)];
+            if (n < N && k < K) {
+                pw[j] = wa[(size_t)n * K + k];
+                if (two) pw2[j] = wb[(size_t)n * K + k];
+            }
+        }
+    };
     float acc_a = 0.f, acc_b = 0.f;
+    fetch(0);
     for (int k0 = 0; k0 < K; k0 += 64) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int e = tid + 256 * j;
-            const int rr = e >> 6, kk = e & 63, k = k0 + kk;
-            const int r = r0 + rr, n = n0 + rr;
-            float xv = 0.f, wv = 0.f, wv2 = 0.f;
-            if (r < rows && k < K) xv = k < d0 ? x0[(size_t)state_of(r) * d0 + k] : x1[(size_t)r * ld1 + (k - d0)];
-            if (n < N && k < K) {
-                wv = wa[(size_t)n * K + k];
-                if (two) wv2 = wb[(size_t)n * K + k];
-            }
-            xs[rr][kk] = xv;
-            ws[0][rr][kk] = wv;
-            ws[1][rr][kk] = wv2;
+            xs[e >> 6][e & 63] = px[j];
+            ws[0][e >> 6][e & 63] = pw[j];
+            ws[1][e >> 6][e & 63] = pw2[j];
         }
         __syncthreads();
+        if (k0 + 64 < K) fetch(k0 + 64);   // the next chunk's loads run under this chunk's products
         const int kn = min(64, K - k0);
         for (int kk = 0; kk < kn; ++kk) {
             const float xv = xs[ty][kk];
