@@ -380,60 +380,62 @@ struct XRowsConcat {
 // (row, slice) partial of KEEP entries.  One thread per row.
 template <int NC, int KL, int KEEP = kKeep>
 __device__ __forceinline__ void lm_merge_contributors(const float* cm, int rstride, int rows, int row0, int split,
-                                                      int nsplit,
-                                             int R, float sl2, float* part) {
+                                                      int nsplit, int R, float sl2, float* part) {
     constexpr int W = 3 + 2 * KL;
+    constexpr int NCAND = NC * KL;
     const int tid = threadIdx.x;
     if (tid >= rows) return;
     const int grow = row0 + tid;
     if (grow >= R) return;
+    // every contributor's words at once (one batch of LDS reads), then the
+    // selection in registers: the KEEP best of the lists' entries are the
+    // first KEEP picks of the best remaining entry by (value desc, id asc)
+    // (ids are distinct within a slice, so a pick is removed by its id)
     const float* c = cm + tid * rstride;
+    float cmax[NC], csum[NC], cbnd[NC], v[NCAND];
+    int id[NCAND];
+#pragma unroll
+    for (int p = 0; p < NC; ++p) {
+        cmax[p] = c[p * W + 0];
+        csum[p] = c[p * W + 1];
+        cbnd[p] = c[p * W + 2];
+#pragma unroll
+        for (int q = 0; q < KL; ++q) {
+            v[p * KL + q] = c[p * W + 3 + q];
+            id[p * KL + q] = __float_as_int(c[p * W + 3 + KL + q]);
+        }
+    }
     float M = neg_inf(), U = neg_inf();
 #pragma unroll
     for (int p = 0; p < NC; ++p) {
-        M = fmaxf(M, c[p * W + 0]);
-        U = fmaxf(U, c[p * W + 2]);
+        M = fmaxf(M, cmax[p]);
+        U = fmaxf(U, cbnd[p]);
     }
     float S = 0.f;
 #pragma unroll
-    for (int p = 0; p < NC; ++p) {
-        const float mp = c[p * W + 0];
-        S += (mp == neg_inf()) ? 0.f : c[p * W + 1] * exp2f((mp - M) * sl2);
-    }
+    for (int p = 0; p < NC; ++p) S += (cmax[p] == neg_inf()) ? 0.f : csum[p] * exp2f((cmax[p] - M) * sl2);
     float* out = part + ((size_t)grow * nsplit + split) * part_stride(KEEP);
-    int ptr[NC];
-#pragma unroll
-    for (int p = 0; p < NC; ++p) ptr[p] = 0;
     int cnt = 0;
+#pragma unroll
     for (int e = 0; e <= KEEP; ++e) {
         float bv = neg_inf();
-        int bi = -1, bp = -1;
+        int bi = -1;
 #pragma unroll
-        for (int p = 0; p < NC; ++p) {
-            if (ptr[p] < KL) {
-                const float v = c[p * W + 3 + ptr[p]];
-                const int i = __float_as_int(c[p * W + 3 + KL + ptr[p]]);
-                if (i >= 0 && (bp < 0 || better(v, i, bv, bi))) {
-                    bv = v;
-                    bi = i;
-                    bp = p;
-                }
-            }
+        for (int j = 0; j < NCAND; ++j) {
+            const bool take = id[j] >= 0 && (bi < 0 || better(v[j], id[j], bv, bi));
+            bv = take ? v[j] : bv;
+            bi = take ? id[j] : bi;
         }
-        if (bp < 0) break;
-        if (e == KEEP) {
-            U = fmaxf(U, bv);
-            break;
-        }
+        if (e < KEEP) {
+            // the e-th entry, or the empty entry once the lists are exhausted
+            out[4 + e] = bi >= 0 ? bv : neg_inf();
+            out[4 + KEEP + e] = __int_as_float(bi);
+            cnt += bi >= 0 ? 1 : 0;
 #pragma unroll
-        for (int p = 0; p < NC; ++p) ptr[p] += (p == bp) ? 1 : 0;
-        out[4 + e] = bv;
-        out[4 + KEEP + e] = __int_as_float(bi);
-        ++cnt;
-    }
-    for (int e = cnt; e < KEEP; ++e) {
-        out[4 + e] = neg_inf();
-        out[4 + KEEP + e] = __int_as_float(-1);
+            for (int j = 0; j < NCAND; ++j) id[j] = (bi >= 0 && id[j] == bi) ? -1 : id[j];
+        } else if (bi >= 0) {
+            U = fmaxf(U, bv);   // the best entry left out bounds the slice's other logits
+        }
     }
     out[0] = M;
     out[1] = S;
