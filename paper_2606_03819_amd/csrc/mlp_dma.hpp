@@ -32,6 +32,8 @@
 // loop.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "dma.hpp"
 #include "rows.hpp"
@@ -97,7 +99,7 @@ struct MlpDmaTraits {
     static constexpr int TILE_F = 1024;                     // floats of one 32x32 accumulator
     static constexpr int PF = TG * TILE_F * (1 + NTE);      // floats of one item's sums (h, then e)
     static constexpr int SCR_W = 4 * TW * (1 + NTW) * TILE_F * 4;
-    static constexpr int SCR_C = PF * 4;
+    static constexpr int SCR_C = PF * 4 + 8 * 256;   // the summed pieces, then two slot lists (at most 256)
     static constexpr int SMEM = RING > SCR_W ? (RING > SCR_C ? RING : SCR_C) : (SCR_W > SCR_C ? SCR_W : SCR_C);
     static constexpr int HC = 4 * TG;                       // summed h floats per thread
     static constexpr int EC = 4 * TG * NTE;                 // summed e floats per thread
@@ -134,56 +136,6 @@ struct MlpLdsSums {
             if constexpr (HASH) x += hs[t * 1024 + j * 64 + hr + hi];
             v[e2] = x;
         }
-    }
-};
-
-// A cut item's sums from its pieces' partial sums in memory (a slot of PF
-// floats: [TG][1024] h phase, then [TG][NTE][1024] e phase), each phase
-// added over the pieces in piece order, then the two phases.  info[p] (LDS)
-// is piece p's slot << 2 | (it covers e chunks) | (it covers h chunks) << 1.
-// The loads of four pieces are in flight together.
-template <int PF>
-struct MlpPieceSums {
-    const float* partial;
-    const int* info;
-    int npieces;
-    template <int TG, int NTE, bool HASH>
-    __device__ __forceinline__ void get(int t, int n, int c, int hr, int jbase, float (&v)[8]) const {
-        float es[8], hs[8];
-#pragma unroll
-        for (int e2 = 0; e2 < 8; ++e2) es[e2] = hs[e2] = 0.f;
-        for (int p0 = 0; p0 < npieces; p0 += 4) {
-            float le[4][8], lh[4][8];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-#pragma unroll
-                for (int e2 = 0; e2 < 8; ++e2) le[k][e2] = lh[k][e2] = 0.f;
-                if (p0 + k < npieces) {
-                    const int f = info[p0 + k];
-                    const float* src = partial + (size_t)(f >> 2) * PF;
-                    if (f & 1) {
-#pragma unroll
-                        for (int e2 = 0; e2 < 8; ++e2)
-                            le[k][e2] = load_coherent(src + TG * 1024 + (t * NTE + n) * 1024 +
-                                                      (jbase + (e2 & 3)) * 64 + c + 32 * (e2 >> 2));
-                    }
-                    if (HASH && (f & 2)) {
-#pragma unroll
-                        for (int e2 = 0; e2 < 8; ++e2)
-                            lh[k][e2] = load_coherent(src + t * 1024 + (jbase + (e2 & 3)) * 64 + hr + 32 * (e2 >> 2));
-                    }
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-#pragma unroll
-                for (int e2 = 0; e2 < 8; ++e2) {
-                    es[e2] += le[k][e2];
-                    hs[e2] += lh[k][e2];
-                }
-        }
-#pragma unroll
-        for (int e2 = 0; e2 < 8; ++e2) v[e2] = HASH ? es[e2] + hs[e2] : es[e2];
     }
 };
 
@@ -581,6 +533,63 @@ __device__ __forceinline__ void mlp_store_piece(float* slot, bool has_h, bool ha
     }
 }
 
+// The last piece of a cut item to arrive: the pieces' sums into csc ([TG][1024]
+// h phase, then [TG][NTE][1024] e phase), each phase added over its pieces in
+// piece order.  hs[0..nh) and es[0..ne) are the slots of the pieces that
+// cover h chunks and e chunks, in piece order.  The loads are 16 bytes per
+// lane and device-coherent (buffer loads with the sc1 bit the device-scope
+// atomic loads carry); one batch holds the h sums of two pieces and the e
+// sums of BE, so the usual item of two h and two e pieces takes a single
+// round trip.  Each thread owns the 16-byte groups tid + 256 i of a phase.
+template <int TG, int NTE, int PF, int BE>
+__device__ __forceinline__ void mlp_combine_pieces(const float* partial, const int* hs, int nh, const int* es, int ne,
+                                                   float* csc) {
+    constexpr int kSc1 = 16;   // cache-policy bits of a device-coherent load
+    constexpr int H4 = TG, E4 = TG * NTE;   // 16-byte groups per thread of each phase
+    constexpr int BH = 2;                   // pieces per batch of the h phase (BE: of the e phase)
+    const int tid = threadIdx.x;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(partial), (short)0, 0x7fffffff, 0x00020000);
+    auto ld = [&](int slot, int f) {
+        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (slot * PF + f) * 4, 0, kSc1));
+    };
+    const f32x4 zero{0.f, 0.f, 0.f, 0.f};
+    f32x4 sh[H4], se[E4];
+#pragma unroll
+    for (int i = 0; i < H4; ++i) sh[i] = zero;
+#pragma unroll
+    for (int i = 0; i < E4; ++i) se[i] = zero;
+    for (int ph = 0, pe = 0; ph < nh || pe < ne; ph += BH, pe += BE) {
+        f32x4 vh[BH][H4], ve[BE][E4];
+#pragma unroll
+        for (int k = 0; k < BH; ++k) {
+            const bool has = ph + k < nh;
+            const int slot = has ? hs[ph + k] : 0;
+#pragma unroll
+            for (int i = 0; i < H4; ++i) vh[k][i] = has ? ld(slot, 4 * tid + 1024 * i) : zero;
+        }
+#pragma unroll
+        for (int k = 0; k < BE; ++k) {
+            const bool has = pe + k < ne;
+            const int slot = has ? es[pe + k] : 0;
+#pragma unroll
+            for (int i = 0; i < E4; ++i) ve[k][i] = has ? ld(slot, TG * 1024 + 4 * tid + 1024 * i) : zero;
+        }
+#pragma unroll
+        for (int k = 0; k < BH; ++k)
+#pragma unroll
+            for (int i = 0; i < H4; ++i) sh[i] += vh[k][i];
+#pragma unroll
+        for (int k = 0; k < BE; ++k)
+#pragma unroll
+            for (int i = 0; i < E4; ++i) se[i] += ve[k][i];
+    }
+#pragma unroll
+    for (int i = 0; i < H4; ++i) *reinterpret_cast<f32x4*>(csc + 4 * tid + 1024 * i) = sh[i];
+#pragma unroll
+    for (int i = 0; i < E4; ++i) *reinterpret_cast<f32x4*>(csc + TG * 1024 + 4 * tid + 1024 * i) = se[i];
+}
+
 // Every item piece of this workgroup's range; a cut item is summed by its
 // last piece to arrive, in piece order, then written by the epilogue.
 template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP, int EPI>
@@ -621,17 +630,26 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
             last = flag[0] != 0;
             __syncthreads();
             if (last) {
-                // this piece's info, then the epilogue over the pieces' sums
-                int* info = reinterpret_cast<int*>(csc);
+                // the slots of the pieces covering each phase, in piece order (LDS after the
+                // sums: the pieces of an item are consecutive workgroups, those of a phase
+                // too, so each list is a range of them), the sums, then the epilogue
+                int* hs = reinterpret_cast<int*>(csc + T::PF);
+                int* es = hs + 256;
                 const long long ib = (long long)item * nk;
-                if (tid < pcs.npieces) {
-                    const int gp = pcs.gfirst + tid;
-                    const int p0 = (int)max(0ll, unit_start(sh, gp) - ib);
-                    const int p1 = (int)min((long long)nk, unit_start(sh, gp + 1) - ib);
-                    info[tid] = (piece_slot(sh, gp, item) << 2) | (p1 > a.nkh ? 1 : 0) | (p0 < a.nkh ? 2 : 0);
+                // pieces [0, ph1) cover h chunks, pieces [pe0, npieces) cover e chunks
+                const int ph1 = a.nkh > 0 ? unit_owner(sh, ib + min(a.nkh, nk) - 1) - pcs.gfirst + 1 : 0;
+                const int pe0 = a.nkh < nk ? unit_owner(sh, ib + a.nkh) - pcs.gfirst : pcs.npieces;
+                for (int i = tid; i < pcs.npieces; i += 256) {
+                    const int slot = piece_slot(sh, pcs.gfirst + i, item);
+                    if (i < ph1) hs[i] = slot;
+                    if (i >= pe0) es[i - pe0] = slot;
                 }
                 __syncthreads();
-                mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpPieceSums<T::PF>{a.partial, info, pcs.npieces});
+                // (the widest residual epilogue leaves room for one e piece per batch)
+                constexpr int BE = EPI == kMlpEpiResidual && HASH && NTE == 4 ? 1 : 2;
+                mlp_combine_pieces<TG, NTE, T::PF, BE>(a.partial, hs, ph1, es, pcs.npieces - pe0, csc);
+                __syncthreads();
+                mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
             }
         } else {
 #pragma unroll
