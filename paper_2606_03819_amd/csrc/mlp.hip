@@ -54,6 +54,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
         dst = et + (size_t)rr * npre * d + (size_t)which * d;
     }
     float ss = 0.f;
+#pragma unroll 4   // four loads in flight before the first use
     for (int k = threadIdx.x; k < d; k += 256) {
         const float x = load_elem(src, k);
         ss = fmaf(x, x, ss);
@@ -63,10 +64,12 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__
     __syncthreads();
     ss = (red[0] + red[1]) + (red[2] + red[3]);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-    for (int k = threadIdx.x; k < d; k += 256) {
-        float y = load_elem(src, k) * inv;
-        if (gain != nullptr) y *= load_elem(gain, k);
-        store_elem(dst, k, y);
+    if (gain != nullptr) {
+#pragma unroll 4
+        for (int k = threadIdx.x; k < d; k += 256) store_elem(dst, k, load_elem(src, k) * inv * load_elem(gain, k));
+    } else {
+#pragma unroll 4
+        for (int k = threadIdx.x; k < d; k += 256) store_elem(dst, k, load_elem(src, k) * inv);
     }
 }
 
@@ -112,15 +115,22 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const uint16_t* 
     }
     const int npc = d >> 3;   // 16-byte pieces
     u32x4 v[MAXC], gv[MAXC];
+    // Every load is issued before the first use: the branch per piece is
+    // uniform and a lane past the row re-reads its last piece (its values are
+    // dropped below), so the row and its gains take one round trip.
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        if (64 * c < npc) {
+            const int pc = min(lane + 64 * c, npc - 1);
+            v[c] = *reinterpret_cast<const u32x4*>(src + 8 * pc);
+            gv[c] = gain != nullptr ? *reinterpret_cast<const u32x4*>(gain + 8 * pc)
+                                    : u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};   // bf16 ones
+        }
+    }
     float ss = 0.f;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
-        const int pc = lane + 64 * c;
-        if (pc < npc) {
-            v[c] = *reinterpret_cast<const u32x4*>(src + 8 * pc);
-            // the gains travel with the vector: one round trip for both
-            gv[c] = gain != nullptr ? *reinterpret_cast<const u32x4*>(gain + 8 * pc)
-                                    : u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};   // bf16 ones
+        if (64 * c < npc && lane + 64 * c < npc) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu), hi = bf16_bits_to_f32(v[c][q] >> 16);
@@ -384,8 +394,8 @@ static hipError_t launch_mlp_dma(const MlpDmaArgs& a, const MlpDmaPlan& p, hipSt
 static MlpDmaArgs mlp_dma_args(const MlpDmaPlan& p, const uint16_t* w, const uint16_t* wu, int N, int Kw,
                                const uint16_t* xh, const uint16_t* xe, long lde, int Rh, int Re, uint16_t* out,
                                int Nout, const uint16_t* h, const RowTable& rt, float* partial, int* counter) {
-    return MlpDmaArgs{w,      wu,     N,       Kw,    xh,   xe,   lde,  Rh, Re,      p.ntiles, p.items,
-                      p.nkh,  p.nke,  p.G,     out,   Nout, h,    rt,   partial, counter};
+    return MlpDmaArgs{w,     wu,    N,   Kw,   xh,   xe,   lde, Rh,   Re,      p.ntiles, p.items, p.nkh,
+                      p.nke, p.G,   p.wh, p.we, out, Nout, h,  rt,   partial, counter};
 }
 
 // Eq. 1 (or the plain SiLU MLP when w_up is null) for at most 128 rows and

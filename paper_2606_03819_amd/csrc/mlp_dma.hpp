@@ -61,6 +61,7 @@ struct MlpDmaArgs {
     long lde;
     int Rh, Re;
     int ntiles, items, nkh, nke, G;
+    int wh, we;           // split costs of an h and an e chunk (CostSplit)
     uint16_t* out;        // [Re, 2 * Nout] hi/lo pairs, or [Re, Nout] (residual)
     int Nout;             // output width: I (activations) or d (residual)
     const uint16_t* h;    // residual source [b * gamma, d] (raw drafter states)
@@ -99,7 +100,7 @@ struct MlpDmaTraits {
     static constexpr int TILE_F = 1024;                     // floats of one 32x32 accumulator
     static constexpr int PF = TG * TILE_F * (1 + NTE);      // floats of one item's sums (h, then e)
     static constexpr int SCR_W = 4 * TW * (1 + NTW) * TILE_F * 4;
-    static constexpr int SCR_C = PF * 4 + 8 * 256;   // the summed pieces, then two slot lists (at most 256)
+    static constexpr int SCR_C = PF * 4;   // the summed pieces
     static constexpr int SMEM = RING > SCR_W ? (RING > SCR_C ? RING : SCR_C) : (SCR_W > SCR_C ? SCR_W : SCR_C);
     static constexpr int HC = 4 * TG;                       // summed h floats per thread
     static constexpr int EC = 4 * TG * NTE;                 // summed e floats per thread
@@ -302,19 +303,8 @@ __device__ __forceinline__ void mlp_step_begin(MlpCursor& cur, bool wcopier, int
     }
 }
 
-// Piece placement of a cut item: the pieces are workgroups gfirst ..
-// gfirst + npieces - 1.
-struct MlpPieces {
-    int gfirst, npieces;
-};
-__device__ __forceinline__ MlpPieces mlp_pieces(const GemmShape& sh, int item) {
-    const int gfirst = unit_owner(sh, (long long)item * sh.nk);
-    return MlpPieces{gfirst, unit_owner(sh, (long long)item * sh.nk + sh.nk - 1) - gfirst + 1};
-}
-
-__device__ __forceinline__ GemmShape mlp_shape(const MlpDmaArgs& a) {
-    const int nk = a.nkh + a.nke;
-    return GemmShape{a.Re, nk * 64, a.ntiles, a.items, 1, nk, a.G};
+__device__ __forceinline__ CostSplit mlp_shape(const MlpDmaArgs& a) {
+    return cost_split(a.items, a.nkh, a.nke, a.wh, a.we, a.G);
 }
 
 // Weight DMA sources of copier cw (rows 16cw..16cw+15 of every tile, two
@@ -534,22 +524,25 @@ __device__ __forceinline__ void mlp_store_piece(float* slot, bool has_h, bool ha
 }
 
 // The last piece of a cut item to arrive: the pieces' sums into csc ([TG][1024]
-// h phase, then [TG][NTE][1024] e phase), each phase added over its pieces in
-// piece order.  hs[0..nh) and es[0..ne) are the slots of the pieces that
-// cover h chunks and e chunks, in piece order.  The loads are 16 bytes per
-// lane and device-coherent (buffer loads with the sc1 bit the device-scope
-// atomic loads carry); one batch holds the h sums of two pieces and the e
-// sums of BE, so the usual item of two h and two e pieces takes a single
-// round trip.  Each thread owns the 16-byte groups tid + 256 i of a phase.
+// h phase, then [TG][NTE][1024] e phase), each phase added over the pieces
+// that cover it (pcs), in piece order.  The loads are 16 bytes per lane and
+// device-coherent (buffer loads with the sc1 bit the device-scope atomic
+// loads carry); one batch holds the h sums of two pieces and the e sums of
+// BE, so the usual item (two pieces with h chunks, up to BE with e chunks)
+// takes a single round trip.  Each thread owns the 16-byte groups
+// tid + 256 i of a phase.
 template <int TG, int NTE, int PF, int BE>
-__device__ __forceinline__ void mlp_combine_pieces(const float* partial, const int* hs, int nh, const int* es, int ne,
+__device__ __forceinline__ void mlp_combine_pieces(const float* partial, int nslots, const CutPieces& pcs,
                                                    float* csc) {
     constexpr int kSc1 = 16;   // cache-policy bits of a device-coherent load
     constexpr int H4 = TG, E4 = TG * NTE;   // 16-byte groups per thread of each phase
     constexpr int BH = 2;                   // pieces per batch of the h phase (BE: of the e phase)
     const int tid = threadIdx.x;
+    // The descriptor spans the nslots slots: a batch's missing pieces read
+    // slot nslots, past the range, which returns zeros without a memory
+    // access, so every load of a batch is issued unconditionally.
     const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(partial), (short)0, 0x7fffffff, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(partial), (short)0, nslots * PF * 4, 0x00020000);
     auto ld = [&](int slot, int f) {
         return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (slot * PF + f) * 4, 0, kSc1));
     };
@@ -559,21 +552,20 @@ __device__ __forceinline__ void mlp_combine_pieces(const float* partial, const i
     for (int i = 0; i < H4; ++i) sh[i] = zero;
 #pragma unroll
     for (int i = 0; i < E4; ++i) se[i] = zero;
+    const int nh = pcs.ph1, ne = pcs.npieces - pcs.pe0;
     for (int ph = 0, pe = 0; ph < nh || pe < ne; ph += BH, pe += BE) {
         f32x4 vh[BH][H4], ve[BE][E4];
 #pragma unroll
         for (int k = 0; k < BH; ++k) {
-            const bool has = ph + k < nh;
-            const int slot = has ? hs[ph + k] : 0;
+            const int slot = ph + k < nh ? pcs.slot(ph + k) : nslots;
 #pragma unroll
-            for (int i = 0; i < H4; ++i) vh[k][i] = has ? ld(slot, 4 * tid + 1024 * i) : zero;
+            for (int i = 0; i < H4; ++i) vh[k][i] = ld(slot, 4 * tid + 1024 * i);
         }
 #pragma unroll
         for (int k = 0; k < BE; ++k) {
-            const bool has = pe + k < ne;
-            const int slot = has ? es[pe + k] : 0;
+            const int slot = pe + k < ne ? pcs.slot(pcs.pe0 + pe + k) : nslots;
 #pragma unroll
-            for (int i = 0; i < E4; ++i) ve[k][i] = has ? ld(slot, TG * 1024 + 4 * tid + 1024 * i) : zero;
+            for (int i = 0; i < E4; ++i) ve[k][i] = ld(slot, TG * 1024 + 4 * tid + 1024 * i);
         }
 #pragma unroll
         for (int k = 0; k < BH; ++k)
@@ -599,25 +591,30 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
     constexpr bool HASH = !PAIRED;   // the down projection alone has no h phase
     extern __shared__ __align__(16) unsigned char dyn[];
     const int tid = threadIdx.x;
-    const GemmShape sh = mlp_shape(a);
+    const CostSplit sh = mlp_shape(a);
     const int nk = sh.nk;
     const int g = xcd_logical_id(blockIdx.x, gridDim.x);
-    const long long u_end = unit_start(sh, g + 1);
-    long long u = unit_start(sh, g);
+    const int u_end = unit_start(sh, g + 1);
+    int u = unit_start(sh, g);
     while (u < u_end) {
-        const int item = (int)(u / nk);
-        const int c0 = (int)(u - (long long)item * nk);
-        const int c1 = (int)min((long long)nk, u_end - (long long)item * nk);
+        const int item = u / nk;
+        const int c0 = u - item * nk;
+        const int c1 = min(nk, u_end - item * nk);
+        CutPieces pcs = cut_pieces(sh, item);   // uniform: kept in scalar registers
+        pcs.gfirst = __builtin_amdgcn_readfirstlane(pcs.gfirst);
+        pcs.npieces = __builtin_amdgcn_readfirstlane(pcs.npieces);
+        pcs.slot0 = __builtin_amdgcn_readfirstlane(pcs.slot0);
+        pcs.ph1 = __builtin_amdgcn_readfirstlane(pcs.ph1);
+        pcs.pe0 = __builtin_amdgcn_readfirstlane(pcs.pe0);
         float hc[T::HC], ec[T::EC];
         mlp_piece<TG, NTE, PAIRED, SW, SX, WMAP>(a, item, c0, c1, dyn, hc, ec);
 
         // ---- a cut item: store this piece; the last to arrive sums them
-        const MlpPieces pcs = mlp_pieces(sh, item);
         float* csc = reinterpret_cast<float*>(dyn);   // [TG][1024] h, then [TG][NTE][1024] e
         bool last = true;
         if (pcs.npieces > 1) {
-            mlp_store_piece<TG, NTE>(a.partial + (size_t)piece_slot(sh, g, item) * T::PF, c0 < a.nkh, c1 > a.nkh, hc,
-                                     ec);
+            mlp_store_piece<TG, NTE>(a.partial + (size_t)pcs.slot(g - pcs.gfirst) * T::PF, c0 < a.nkh, c1 > a.nkh,
+                                     hc, ec);
             wait_memory();
             __syncthreads();   // every thread's piece is stored
             int* flag = reinterpret_cast<int*>(csc);
@@ -630,24 +627,12 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
             last = flag[0] != 0;
             __syncthreads();
             if (last) {
-                // the slots of the pieces covering each phase, in piece order (LDS after the
-                // sums: the pieces of an item are consecutive workgroups, those of a phase
-                // too, so each list is a range of them), the sums, then the epilogue
-                int* hs = reinterpret_cast<int*>(csc + T::PF);
-                int* es = hs + 256;
-                const long long ib = (long long)item * nk;
-                // pieces [0, ph1) cover h chunks, pieces [pe0, npieces) cover e chunks
-                const int ph1 = a.nkh > 0 ? unit_owner(sh, ib + min(a.nkh, nk) - 1) - pcs.gfirst + 1 : 0;
-                const int pe0 = a.nkh < nk ? unit_owner(sh, ib + a.nkh) - pcs.gfirst : pcs.npieces;
-                for (int i = tid; i < pcs.npieces; i += 256) {
-                    const int slot = piece_slot(sh, pcs.gfirst + i, item);
-                    if (i < ph1) hs[i] = slot;
-                    if (i >= pe0) es[i - pe0] = slot;
-                }
-                __syncthreads();
-                // (the widest residual epilogue leaves room for one e piece per batch)
-                constexpr int BE = EPI == kMlpEpiResidual && HASH && NTE == 4 ? 1 : 2;
-                mlp_combine_pieces<TG, NTE, T::PF, BE>(a.partial, hs, ph1, es, pcs.npieces - pe0, csc);
+                // the pieces' sums in piece order, then the epilogue
+                // e pieces per batch: three for SwiGLU over four tiles (an item's
+                // e half usually spans three pieces), one for the widest residual
+                // epilogue (registers), else two
+                constexpr int BE = NTE == 4 ? (EPI == kMlpEpiSwiGLU ? 3 : (EPI == kMlpEpiResidual && HASH ? 1 : 2)) : 2;
+                mlp_combine_pieces<TG, NTE, T::PF, BE>(a.partial, 2 * a.G, pcs, csc);
                 __syncthreads();
                 mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
             }
@@ -659,7 +644,7 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
             __syncthreads();
             mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
         }
-        u = (long long)(item + 1) * nk;
+        u = (item + 1) * nk;
         if (u < u_end) __syncthreads();   // the epilogue's LDS use ends before the next item's copies land
     }
 }

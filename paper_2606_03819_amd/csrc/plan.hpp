@@ -311,12 +311,9 @@ struct MlpDmaPlan {
     int NTE;      // 32-row activation tiles of the e phase (1, 2 or 4)
     int ntiles;   // 32-row weight tiles
     int items, nkh, nke, G;
+    int wh, we;   // cost of an h chunk and of an e chunk in the split (work.hpp)
     size_t part_floats() const { return (size_t)2 * G * TG * 1024 * (1 + NTE); }
 };
-inline bool mlp_dma_applies(bool bf16, int b, int gamma, int R, int d, int I, int ew) {
-    return bf16 && (long long)b * gamma <= kMlpDmaMaxStates && (long long)b * R <= kMlpDmaMaxRows && d % 64 == 0 &&
-           I % 64 == 0 && ew % 64 == 0;
-}
 inline MlpDmaPlan mlp_dma_plan(int rows, int ntiles, int nkh, int nke, int TG) {
     MlpDmaPlan p;
     p.TG = TG;
@@ -329,7 +326,18 @@ inline MlpDmaPlan mlp_dma_plan(int rows, int ntiles, int nkh, int nke, int TG) {
     long long G = U / kMlpDmaMinUnits;
     G = G < kNumCUs ? G : kNumCUs;
     p.G = (int)(G < 1 ? 1 : G);
+    // An e chunk against four activation tiles streams its weights at about
+    // three fifths of an h chunk's rate (the activation copies from L2 share
+    // the CU's load path with the weight stream; 5:3 measured best against
+    // 3:2 and 9:5); two tiles take a ratio between that and 1, and one tile,
+    // like the h phase, costs the same.
+    p.wh = nkh > 0 && p.NTE == 4 ? 3 : (nkh > 0 && p.NTE == 2 ? 4 : 1);
+    p.we = nkh > 0 && p.NTE == 4 ? 5 : (nkh > 0 && p.NTE == 2 ? 5 : 1);
+    if (!cost_split_valid(p.items, nkh, nke, p.wh, p.we, p.G)) p.wh = p.we = 1;
     return p;
+}
+inline bool mlp_dma_plan_ok(const MlpDmaPlan& p) {
+    return cost_split_valid(p.items, p.nkh, p.nke, p.wh, p.we, p.G);
 }
 // gate/up (SwiGLU: tiles of 16 gate + 16 up rows) or the gate alone (the
 // plain SiLU MLP: tiles of 32 gate rows) over [h~ ; e~], e~ ew wide
@@ -343,6 +351,18 @@ inline MlpDmaPlan mlp_dma_down_plan(int rows, int d, int I) {
 // the linear approximator W_lin [d, 2d] over [h~ ; e~]
 inline MlpDmaPlan mlp_dma_linear_plan(int rows, int d) {
     return mlp_dma_plan(rows, cdiv(d, 32), d / 64, d / 64, TF_MLP_DMA_TG_IN);
+}
+// One row block holds every conditional row and each plan the path may
+// launch (either gate plan, the down projection, the linear layer) keeps its
+// split in 32-bit arithmetic.
+inline bool mlp_dma_applies(bool bf16, int b, int gamma, int R, int d, int I, int ew) {
+    if (!(bf16 && (long long)b * gamma <= kMlpDmaMaxStates && (long long)b * R <= kMlpDmaMaxRows && d % 64 == 0 &&
+          I % 64 == 0 && ew % 64 == 0))
+        return false;
+    const int rows = b * R;
+    return mlp_dma_plan_ok(mlp_dma_gate_plan(rows, d, ew, I, true)) &&
+           mlp_dma_plan_ok(mlp_dma_gate_plan(rows, d, ew, I, false)) && mlp_dma_plan_ok(mlp_dma_down_plan(rows, d, I)) &&
+           mlp_dma_plan_ok(mlp_dma_linear_plan(rows, d));
 }
 
 // Long (row, slice) lists for top-k lists of at least kLongListK entries

@@ -54,6 +54,79 @@ inline bool gemm_has_pieces(const GemmShape& s) {
     return false;
 }
 
+// One-row-block products (every activation row in one block): an item's k-
+// chunks come in two phases, first nkh chunks of the h~ half of x against the
+// drafter states' one row tile, then nke chunks against every row (the e~
+// half, or the whole input of a product without the split).  An e chunk costs
+// more than an h chunk (more activation tiles per weight byte), so the units
+// (item-major, as above) are dealt out by cost: an h chunk costs wh, an e
+// chunk we, and workgroup g owns the units whose cost offset falls in
+// [ceil(g*C/G), ceil((g+1)*C/G)), C the total.  Every workgroup then carries
+// the same work up to one chunk; the pieces of a cut item are consecutive
+// workgroups as before, and a workgroup holds at most two cut items.  Ranges
+// are never empty while C/G >= max(wh, we), and the arithmetic stays in 32
+// bits while C*G < 2^31 (cost_split_valid).
+struct CostSplit {
+    int nk, nkh, wh, we, G;
+    int citem, ctot;   // cost of one item, of all items
+};
+
+__host__ __device__ inline CostSplit cost_split(int items, int nkh, int nke, int wh, int we, int G) {
+    const int citem = nkh * wh + nke * we;
+    return CostSplit{nkh + nke, nkh, wh, we, G, citem, citem * items};
+}
+
+// cost offset of chunk c of `item` (the cost of every unit before it)
+__host__ __device__ inline int split_cost(const CostSplit& s, int item, int c) {
+    const int ch = c < s.nkh ? c : s.nkh;
+    return item * s.citem + ch * s.wh + (c - ch) * s.we;
+}
+
+// first unit of workgroup g (g = G gives the end of the last range): the
+// first unit whose cost offset reaches ceil(g*C/G)
+__host__ __device__ inline int unit_start(const CostSplit& s, int g) {
+    const int x = (g * s.ctot + s.G - 1) / s.G;
+    const int it = x / s.citem;
+    const int o = x - it * s.citem, oh = s.nkh * s.wh;
+    const int c = o <= oh ? (o + s.wh - 1) / s.wh : s.nkh + (o - oh + s.we - 1) / s.we;
+    return it * s.nk + c;
+}
+
+// workgroup whose range holds chunk c of `item`
+__host__ __device__ inline int unit_owner(const CostSplit& s, int item, int c) {
+    return split_cost(s, item, c) * s.G / s.ctot;
+}
+
+// partial-sum slot of workgroup g's piece of `item`: slot 2g for the item its
+// range starts in, 2g + 1 for the one it ends in (as piece_slot above)
+__host__ __device__ inline int piece_slot(const CostSplit& s, int g, int item) {
+    return 2 * g + (item != unit_start(s, g) / s.nk ? 1 : 0);
+}
+
+// The pieces of a cut item: workgroups gfirst .. gfirst + npieces - 1.  Piece
+// i > 0 starts its range inside the item (slot 2(gfirst + i)); the first may
+// have started in an earlier item (then slot 2 gfirst + 1).  Pieces [0, ph1)
+// cover h chunks, pieces [pe0, npieces) e chunks (one piece may do both).
+struct CutPieces {
+    int gfirst, npieces, slot0, ph1, pe0;
+    __host__ __device__ int slot(int i) const { return i == 0 ? slot0 : 2 * (gfirst + i); }
+};
+
+__host__ __device__ inline CutPieces cut_pieces(const CostSplit& s, int item) {
+    CutPieces p;
+    p.gfirst = unit_owner(s, item, 0);
+    p.npieces = unit_owner(s, item, s.nk - 1) - p.gfirst + 1;
+    p.slot0 = 2 * p.gfirst + (unit_start(s, p.gfirst) < item * s.nk ? 1 : 0);
+    p.ph1 = s.nkh > 0 ? unit_owner(s, item, (s.nkh < s.nk ? s.nkh : s.nk) - 1) - p.gfirst + 1 : 0;
+    p.pe0 = s.nkh < s.nk ? unit_owner(s, item, s.nkh) - p.gfirst : p.npieces;
+    return p;
+}
+
+inline bool cost_split_valid(int items, int nkh, int nke, int wh, int we, int G) {
+    const long long c = ((long long)nkh * wh + (long long)nke * we) * items;
+    return c > 0 && c * G < (1LL << 31) && c >= (long long)G * (wh > we ? wh : we);
+}
+
 // LM head (many weight tiles): the vocabulary is cut instead.
 //
 // Vocabulary slices of the LM head.  The T weight tiles are cut into G
