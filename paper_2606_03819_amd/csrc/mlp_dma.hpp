@@ -330,47 +330,49 @@ __device__ __forceinline__ void mlp_weight_sources(const MlpDmaArgs& a, int item
         }
 }
 
-// One item piece, chunks [c0, c1) of `item`, streamed through the rings in
-// `dyn`.  On return every copy has landed, the LDS is free, and hc / ec hold
-// this thread's part of the piece's sums, the waves' accumulators added in
-// wave order: hc[i] is element tid + 256 i of [TG][1024] (h phase), ec[i]
-// element tid + 256 i of [TG][NTE][1024] (e phase).
+// The copy state of one item piece, chunks [c0, c1) of `item`: this lane's
+// DMA sources at chunk c0 and the ring cursors.
+template <int TG, int XPW>
+struct MlpSegment {
+    const uint16_t* wsrc[TG][2];
+    const uint16_t* hsrc[2];
+    const uint16_t* esrc[XPW];
+    MlpCursor cur;
+    int c0, nsteps;
+};
+
+// Waves 0-1 copy the weights, waves 2-3 the activations: a wave waits on
+// its own copies only (s_waitcnt counts a wave's loads in issue order), so
+// the activation waits, two chunks out, never hold up the weight stream,
+// which runs SW - 1 chunks ahead.  cw: the wave's index among the copiers of
+// its stream.
+__device__ __forceinline__ int mlp_copier_index(int wave) { return wave < 2 ? wave : wave - 2; }
+
+// A piece's sources and the ring prologue (weights of chunks 0 .. SW-2,
+// activations of chunks 0 .. SX-2).  Issued apart from the piece's loop so
+// that a workgroup's first copies leave before any set-up of its own.
 template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP>
-__device__ __forceinline__ void mlp_piece(const MlpDmaArgs& a, int item, int c0, int c1, unsigned char* dyn,
-                                          float (&hc)[4 * TG], float (&ec)[4 * TG * NTE]) {
+__device__ __forceinline__ void mlp_piece_begin(const MlpDmaArgs& a, int item, int c0, int c1, unsigned char* dyn,
+                                                MlpSegment<TG, MlpDmaTraits<TG, NTE, PAIRED, SW, SX>::XPW_E>& sg) {
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
-    constexpr int TW = T::TW, NTW = T::NTW;
-    static_assert(SX == 3, "two activation chunks in flight");
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nsteps = c1 - c0;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const bool wcopier = wave < 2;
+    const int cw = mlp_copier_index(wave);
     // this lane's row and physical slot in a 1 KiB DMA block of 128-byte rows
     const int lrow = lane >> 3, lslot = lane & 7;
-    // Waves 0-1 copy the weights, waves 2-3 the activations: a wave waits
-    // on its own copies only (s_waitcnt counts a wave's loads in issue
-    // order), so the activation waits, two chunks out, never hold up the
-    // weight stream, which runs SW - 1 chunks ahead.
-    const bool wcopier = wave < 2;
-    const int cw = wcopier ? wave : wave - 2;   // index among the copiers of its stream
-    // the wave's place in the 2 x 2 grid: weight tiles wa*TW.., activation tiles wb*NTW..
-    const int wa = wave & 1, wb = wave >> 1;
-    const int fr = lane & 31;
-
-    // ---- this lane's DMA sources, at chunk c0 of the segment
-    const uint16_t* wsrc[TG][2];
-    mlp_weight_sources<TG, WMAP>(a, item, c0, cw, lane, wsrc);
+    sg.c0 = c0;
+    sg.nsteps = c1 - c0;
+    mlp_weight_sources<TG, WMAP>(a, item, c0, cw, lane, sg.wsrc);
     // h phase: 32 rows of h~ in four 8-row blocks, blocks cw and cw + 2
-    const uint16_t* hsrc[2];
 #pragma unroll
     for (int v = 0; v < 2; ++v) {
         const int row = 8 * (cw + 2 * v) + lrow;
-        hsrc[v] = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) + 8 * (lslot ^ T::swz128(row)) +
-                                        64 * c0
-                                  : nullptr;
+        sg.hsrc[v] = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) +
+                                           8 * (lslot ^ T::swz128(row)) + 64 * c0
+                                     : nullptr;
     }
     // e phase: DMA instruction q = cw + 2v covers rows XRPI*q ..
-    const uint16_t* esrc[T::XPW_E];
     const int ce0 = c0 - a.nkh;   // e chunk of the segment's first chunk (negative in the h phase)
 #pragma unroll
     for (int v = 0; v < T::XPW_E; ++v) {
@@ -383,11 +385,49 @@ __device__ __forceinline__ void mlp_piece(const MlpDmaArgs& a, int item, int c0,
             row = 8 * q + lrow;
             ps = lslot ^ T::swz128(row);
         }
-        esrc[v] = a.xe + (size_t)min(row, a.Re - 1) * a.lde + 8 * ps + (long)(PAIRED ? 128 : 64) * ce0;
+        sg.esrc[v] = a.xe + (size_t)min(row, a.Re - 1) * a.lde + 8 * ps + (long)(PAIRED ? 128 : 64) * ce0;
     }
-
-    // ---- copies: weights SW - 1 chunks ahead, activations SX - 1
     MlpCursor cur{0, 0, 0, 0, 0, 0};
+    unsigned char* const wbase = dyn + (2 * cw) * 1024;
+    unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
+    if (wcopier) {
+        for (; cur.wnext < SW - 1 && cur.wnext < sg.nsteps; ++cur.wnext)
+            mlp_copy_w<TG>(sg.wsrc, cur.wnext, wbase + cur.wnext * T::WSTAGE, T::WTILE);
+        cur.wstage = cur.wnext % SW;
+    } else {
+        for (; cur.xnext < SX - 1 && cur.xnext < sg.nsteps; ++cur.xnext)
+            mlp_copy_x<T::XPW_E, PAIRED>(sg.hsrc, sg.esrc, c0 + cur.xnext < a.nkh, cur.xnext,
+                                         xbase + cur.xnext * T::XSTAGE);
+        cur.xstage = cur.xnext % SX;
+    }
+    sg.cur = cur;
+}
+
+// The rest of the piece begun by mlp_piece_begin, streamed through the rings
+// in `dyn`.  On return every copy has landed, the LDS is free, and hc / ec
+// hold this thread's part of the piece's sums, the waves' accumulators added
+// in wave order: hc[i] is element tid + 256 i of [TG][1024] (h phase), ec[i]
+// element tid + 256 i of [TG][NTE][1024] (e phase).
+template <int TG, int NTE, bool PAIRED, int SW, int SX>
+__device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
+                                              MlpSegment<TG, MlpDmaTraits<TG, NTE, PAIRED, SW, SX>::XPW_E>& sg,
+                                              unsigned char* dyn, float (&hc)[4 * TG], float (&ec)[4 * TG * NTE]) {
+    using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
+    constexpr int TW = T::TW, NTW = T::NTW;
+    static_assert(SX == 3, "two activation chunks in flight");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool wcopier = wave < 2;
+    const int cw = mlp_copier_index(wave);
+    // the wave's place in the 2 x 2 grid: weight tiles wa*TW.., activation tiles wb*NTW..
+    const int wa = wave & 1, wb = wave >> 1;
+    const int fr = lane & 31;
+    const int c0 = sg.c0, nsteps = sg.nsteps;
+    const auto& wsrc = sg.wsrc;
+    const auto& hsrc = sg.hsrc;
+    const auto& esrc = sg.esrc;
+    MlpCursor& cur = sg.cur;
     unsigned char* const wbase = dyn + (2 * cw) * 1024;
     unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
 
@@ -400,17 +440,6 @@ __device__ __forceinline__ void mlp_piece(const MlpDmaArgs& a, int item, int c0,
 #pragma unroll
             for (int n = 0; n < NTW; ++n) acc_e[t][n][j] = 0.f;
         }
-
-    // prologue: weights of chunks 0 .. SW-2, activations of chunks 0 .. SX-2
-    if (wcopier) {
-        for (; cur.wnext < SW - 1 && cur.wnext < nsteps; ++cur.wnext)
-            mlp_copy_w<TG>(wsrc, cur.wnext, wbase + cur.wnext * T::WSTAGE, T::WTILE);
-        cur.wstage = cur.wnext % SW;
-    } else {
-        for (; cur.xnext < SX - 1 && cur.xnext < nsteps; ++cur.xnext)
-            mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < a.nkh, cur.xnext, xbase + cur.xnext * T::XSTAGE);
-        cur.xstage = cur.xnext % SX;
-    }
 
     // The two phases run in loops of their own: each updates only its own
     // accumulators, so none of them is copied between iterations.  A step
@@ -596,6 +625,8 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
     const int g = xcd_logical_id(blockIdx.x, gridDim.x);
     const int u_end = unit_start(sh, g + 1);
     int u = unit_start(sh, g);
+    MlpSegment<TG, T::XPW_E> sg;
+    if (u < u_end) mlp_piece_begin<TG, NTE, PAIRED, SW, SX, WMAP>(a, u / nk, u % nk, min(nk, u_end - u / nk * nk), dyn, sg);
     while (u < u_end) {
         const int item = u / nk;
         const int c0 = u - item * nk;
@@ -607,7 +638,7 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
         pcs.ph1 = __builtin_amdgcn_readfirstlane(pcs.ph1);
         pcs.pe0 = __builtin_amdgcn_readfirstlane(pcs.pe0);
         float hc[T::HC], ec[T::EC];
-        mlp_piece<TG, NTE, PAIRED, SW, SX, WMAP>(a, item, c0, c1, dyn, hc, ec);
+        mlp_piece_run<TG, NTE, PAIRED, SW, SX>(a, sg, dyn, hc, ec);
 
         // ---- a cut item: store this piece; the last to arrive sums them
         float* csc = reinterpret_cast<float*>(dyn);   // [TG][1024] h, then [TG][NTE][1024] e
@@ -645,7 +676,10 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
             mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
         }
         u = (item + 1) * nk;
-        if (u < u_end) __syncthreads();   // the epilogue's LDS use ends before the next item's copies land
+        if (u < u_end) {
+            __syncthreads();   // the epilogue's LDS use ends before the next item's copies land
+            mlp_piece_begin<TG, NTE, PAIRED, SW, SX, WMAP>(a, item + 1, 0, min(nk, u_end - u), dyn, sg);
+        }
     }
 }
 
