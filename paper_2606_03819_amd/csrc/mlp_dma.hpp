@@ -140,41 +140,48 @@ struct MlpLdsSums {
     }
 };
 
-// Outputs of the epilogue units [e0, e1) of `item` (unit e: row e % (32 NTE),
-// tile and group e / (32 NTE)), one unit per thread at a time, from `src`.
-// The residual rows are read before any sum, the sums of a unit are all
-// loaded before the arithmetic.
+// Outputs of `item`, one epilogue unit per thread at a time, from `src`:
+// unit e = tid + 256 it is row e % (32 NTE), tile and group e / (32 NTE);
+// 256 is a multiple of 32 NTE, so a thread keeps one row (and its drafter
+// state) for every unit.  The residual rows are read before any sum, the
+// sums of a unit are all loaded before the arithmetic.
 template <int TG, int NTE, int EPI, bool HASH, class Src>
-__device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, int e0, int e1, const Src& src) {
+__device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, const Src& src) {
     constexpr int GPT = EPI == kMlpEpiSwiGLU ? 2 : 4;   // groups of 8 outputs per tile
-    constexpr int NIT = (32 * NTE * TG * GPT + 255) / 256;
+    constexpr int NE = 32 * NTE * TG * GPT;             // units of the item
+    constexpr int NIT = (NE + 255) / 256;
+    constexpr int RPI = 32 * NTE;                       // rows of a unit row block
+    static_assert(256 % RPI == 0, "a thread keeps its row");
     struct Unit {
         int r, t, q, tile, hr;
         bool ok;
     };
-    auto unit = [&](int e) {
+    const int tid = threadIdx.x;
+    const int r = tid % RPI;
+    const int sq = r / a.rt.Rs;
+    const int hr = sq * a.rt.gamma + a.rt.depth(r - sq * a.rt.Rs) - 1;
+    auto unit = [&](int it) {
         Unit u;
-        u.r = e % (32 * NTE);
-        const int tg = e / (32 * NTE);
+        u.r = r;
+        const int tg = tid / RPI + it * (256 / RPI);
         u.t = tg / GPT;
         u.q = tg - u.t * GPT;
         u.tile = item * TG + u.t;
         const int o0 = EPI == kMlpEpiSwiGLU ? u.tile * 16 + 8 * u.q : u.tile * 32 + 8 * u.q;
-        u.ok = e < e1 && u.r < a.Re && u.tile < a.ntiles && o0 < a.Nout;
-        const int sq = u.r / a.rt.Rs;
-        u.hr = sq * a.rt.gamma + a.rt.depth(u.r - sq * a.rt.Rs) - 1;
+        u.ok = tg < NE / RPI && r < a.Re && u.tile < a.ntiles && o0 < a.Nout;
+        u.hr = hr;
         return u;
     };
     if constexpr (EPI == kMlpEpiResidual) {
         u32x4 hv[NIT];
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
-            const Unit u = unit(e0 + threadIdx.x + 256 * it);
+            const Unit u = unit(it);
             if (u.ok) hv[it] = *reinterpret_cast<const u32x4*>(a.h + (size_t)u.hr * a.Nout + u.tile * 32 + 8 * u.q);
         }
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
-            const Unit u = unit(e0 + threadIdx.x + 256 * it);
+            const Unit u = unit(it);
             if (!u.ok) continue;
             float v[8];
             src.template get<TG, NTE, HASH>(u.t, u.r >> 5, u.r & 31, u.hr, 4 * u.q, v);
@@ -190,7 +197,7 @@ __device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, int 
     } else {
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
-            const Unit u = unit(e0 + threadIdx.x + 256 * it);
+            const Unit u = unit(it);
             if (!u.ok) continue;
             // activation i0..i0+7 as bf16 hi/lo pairs interleaved by 8
             const int i0 = EPI == kMlpEpiSwiGLU ? u.tile * 16 + 8 * u.q : u.tile * 32 + 8 * u.q;
@@ -516,17 +523,16 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
         }
     __syncthreads();
     auto wslot = [&](int w, int tl, int part) { return wsc + ((w * TW + tl) * (1 + NTW) + part) * 1024; };
+    // element tid + 256 i: tile and offset are constants plus tid (tid < 256)
 #pragma unroll
     for (int i = 0; i < T::HC; ++i) {
-        const int e = tid + 256 * i;   // [TG][1024]
-        const int t = e >> 10, f = e & 1023;
+        const int t = i >> 2, f = ((i & 3) << 8) + tid;   // [TG][1024]
         const int col = t / TW, tl = t % TW;
         hc[i] = wslot(col, tl, 0)[f] + wslot(2 + col, tl, 0)[f];
     }
 #pragma unroll
     for (int i = 0; i < T::EC; ++i) {
-        const int e = tid + 256 * i;   // [TG][NTE][1024]
-        const int t = e / (NTE * 1024), n = (e >> 10) % NTE, f = e & 1023;
+        const int t = i / (4 * NTE), n = (i >> 2) % NTE, f = ((i & 3) << 8) + tid;   // [TG][NTE][1024]
         const int col = t / TW, tl = t % TW;
         if constexpr (NTE >= 2)
             ec[i] = wslot((n / NTW) * 2 + col, tl, 1 + n % NTW)[f];
@@ -616,7 +622,6 @@ __device__ __forceinline__ void mlp_combine_pieces(const float* partial, int nsl
 template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP, int EPI>
 __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
-    constexpr int NE = 32 * NTE * TG * (EPI == kMlpEpiSwiGLU ? 2 : 4);
     constexpr bool HASH = !PAIRED;   // the down projection alone has no h phase
     extern __shared__ __align__(16) unsigned char dyn[];
     const int tid = threadIdx.x;
@@ -665,7 +670,7 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
                 constexpr int BE = NTE == 4 ? (EPI == kMlpEpiSwiGLU ? 3 : (EPI == kMlpEpiResidual && HASH ? 1 : 2)) : 2;
                 mlp_combine_pieces<TG, NTE, T::PF, BE>(a.partial, 2 * a.G, pcs, csc);
                 __syncthreads();
-                mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
+                mlp_epilogue<TG, NTE, EPI, HASH>(a, item, MlpLdsSums{csc, csc + T::HC * 256});
             }
         } else {
 #pragma unroll
@@ -673,7 +678,7 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
 #pragma unroll
             for (int i = 0; i < T::EC; ++i) csc[T::HC * 256 + tid + 256 * i] = ec[i];
             __syncthreads();
-            mlp_epilogue<TG, NTE, EPI, HASH>(a, item, 0, NE, MlpLdsSums{csc, csc + T::HC * 256});
+            mlp_epilogue<TG, NTE, EPI, HASH>(a, item, MlpLdsSums{csc, csc + T::HC * 256});
         }
         u = (item + 1) * nk;
         if (u < u_end) {
