@@ -360,12 +360,16 @@ static void launch_norms(const void* h, const int32_t* root, const int32_t* cont
 
 // ------------------------------------------------ one row block (mlp_dma.hpp)
 
-// Ring depths: 40-70 KiB of weights in flight (SW - 1 stages of TG tiles,
-// 4 KiB each), and two activation chunks; the down projection's 256-byte
-// activation rows leave room for fewer weight stages.
+// Ring depths: SW - 1 weight stages in flight (TG tiles of 4 KiB each) and
+// two activation chunks.  Every copy of a workgroup fills LDS through the
+// same per-CU path (~45 GB/s measured for weights and activations alike), so
+// the down projection, whose 256-byte activation rows make the activation
+// four fifths of its bytes, keeps three weight stages in flight (measured
+// faster than four or five); the input projections are insensitive to
+// four to six.
 template <int TG, bool PAIRED>
 constexpr int mlp_dma_sw() {
-    return PAIRED ? (TG == 2 ? 6 : 4) : (TG == 2 ? 10 : 5);
+    return PAIRED ? (TG == 2 ? 4 : 4) : (TG == 2 ? 10 : 5);
 }
 constexpr int kMlpDmaSX = 3;
 
