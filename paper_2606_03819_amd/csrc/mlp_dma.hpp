@@ -86,11 +86,11 @@ struct MlpDmaTraits {
     static constexpr int XOFF = SW * WSTAGE;
     static constexpr int RING = SW * WSTAGE + SX * XSTAGE;
     static constexpr int QS = PAIRED ? 8 : 4;               // MFMA k sub-steps per chunk (e phase)
-    // two waves copy the weights, two the activations
-    static constexpr int WPW = 2 * TG;                      // weight DMA instructions per copier per chunk
-    static constexpr int XPW_H = 2;                         // activation DMA instructions per copier (h phase)
-    static constexpr int XPW_E = XSTAGE_E / 1024 / 2;       // ... (e phase)
-    static_assert(WPW * (SW - 2) <= 62 && XPW_E <= 62, "vmcnt range");
+    // every wave copies a quarter of each chunk (8-row blocks of 1 KiB)
+    static constexpr int WPW = TG;                          // weight DMA instructions per wave per chunk
+    static constexpr int XPW_H = 1;                         // activation DMA instructions per wave (h phase)
+    static constexpr int XPW_E = XSTAGE_E / 1024 / 4;       // ... (e phase)
+    static_assert((SW - 1) * WPW + (SX - 1) * XPW_E <= 62, "vmcnt range");
     // 2 x 2 wave grid: two waves along the weight tiles (TW each), two
     // along the activation tiles (NTW each, or both on the single tile of
     // the h phase / of NTE = 1, splitting its k sub-steps)
@@ -106,7 +106,7 @@ struct MlpDmaTraits {
     static constexpr int EC = 4 * TG * NTE;                 // summed e floats per thread
     static_assert(TG % 2 == 0, "weight tiles split over two waves");
     static_assert(NTE == 1 || NTE == 2 || NTE == 4, "activation tiles");
-    static_assert(XPW_E >= 1 && XSTAGE_E % 2048 == 0, "whole DMA instructions per copier");
+    static_assert(XPW_E >= 1 && XSTAGE_E % 4096 == 0, "whole DMA instructions per wave");
     static_assert(SW > SX && SX >= 2, "ring depths: a chunk's weights are copied before its activations");
     // 16-byte slot swizzles: 128-byte rows (weights, plain activations) and
     // 256-byte rows (paired activations) keep a quarter-wave's 16 fragment
@@ -227,163 +227,149 @@ __device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, cons
     }
 }
 
-// wait until at most STEP * k of this wave's loads are outstanding, k < 16
-// (uniform), for the last chunks of a segment where fewer copies follow
-template <int STEP, int K = 0>
-__device__ __forceinline__ void wait_vmcnt_mult(int k) {
-    if constexpr (STEP * K <= 62 && K < 16) {
-        if (k == K) {
-            wait_vmcnt<STEP * K>();
-            return;
-        }
-        wait_vmcnt_mult<STEP, K + 1>(k);
-    } else {
-        wait_vmcnt<0>();
-    }
-}
-
-// Copy cursors of one segment: the next chunk (segment-relative) each copier
-// stream fills and its ring stage, and the stages the next chunk is read from.
+// Copy cursors of one segment: the next chunk (segment-relative) of each
+// stream and its ring stage, and the stages the next chunk is read from.
 struct MlpCursor {
     int wnext, wstage, xnext, xstage, rw, rx;
 };
 
-// One chunk of weights: copier cw's rows of every tile of the item.  One
-// workgroup alone reads a weight tile, so the copies are non-temporal (they
-// do not displace the activation rows every workgroup re-reads from L2).
+// One chunk of weights: this wave's 8-row block c of every tile of the item.
+// One workgroup alone reads a weight tile, so the copies are non-temporal
+// (they do not displace the activation rows every workgroup re-reads from L2).
 template <int TG>
-__device__ __forceinline__ void mlp_copy_w(const uint16_t* const (&wsrc)[TG][2], int chunk, unsigned char* st,
-                                           int wtile) {
+__device__ __forceinline__ void mlp_copy_w(const uint16_t* const (&wsrc)[TG], int chunk, unsigned char* st, int wtile,
+                                           int c) {
 #pragma unroll
-    for (int t = 0; t < TG; ++t)
-#pragma unroll
-        for (int hb = 0; hb < 2; ++hb) dma16(wsrc[t][hb] + 64 * chunk, st + t * wtile + hb * 1024, kCpolNt);
+    for (int t = 0; t < TG; ++t) dma16(wsrc[t] + 64 * chunk, st + t * wtile + c * 1024, kCpolNt);
 }
 
-// One chunk of activations: h~ rows in the h phase, else the e-phase rows.
+// One chunk of activations: this wave's 8-row block of the h~ rows in the h
+// phase, else its DMA instructions q = c + 4v of the e-phase rows.
 template <int XPW_E, bool PAIRED>
-__device__ __forceinline__ void mlp_copy_x(const uint16_t* const (&hsrc)[2], const uint16_t* const (&esrc)[XPW_E],
-                                           bool hphase, int chunk, unsigned char* st) {
+__device__ __forceinline__ void mlp_copy_x(const uint16_t* hsrc, const uint16_t* const (&esrc)[XPW_E], bool hphase,
+                                           int chunk, unsigned char* st, int c) {
     if (hphase) {
-#pragma unroll
-        for (int v = 0; v < 2; ++v) dma16(hsrc[v] + 64 * chunk, st + 2 * v * 1024, 0);
+        dma16(hsrc + 64 * chunk, st + c * 1024, 0);
     } else {
 #pragma unroll
-        for (int v = 0; v < XPW_E; ++v) dma16(esrc[v] + (long)(PAIRED ? 128 : 64) * chunk, st + 2 * v * 1024, 0);
+        for (int v = 0; v < XPW_E; ++v)
+            dma16(esrc[v] + (long)(PAIRED ? 128 : 64) * chunk, st + (c + 4 * v) * 1024, 0);
     }
 }
 
-// The start of step s: wait for this wave's copies of chunk s (a weight
-// copier has copied up to min(s + SW - 2, nsteps - 1), an activation
-// copier up to s + 1), meet the barrier, refill the stages chunk s - 1 freed.
-template <class T, int SW, int SX, bool PAIRED, int TG = T::TW * 2>
-__device__ __forceinline__ void mlp_step_begin(MlpCursor& cur, bool wcopier, int s, int nsteps, int c0, int nkh,
-                                               const uint16_t* const (&wsrc)[TG][2],
-                                               const uint16_t* const (&hsrc)[2],
-                                               const uint16_t* const (&esrc)[T::XPW_E], unsigned char* wbase,
-                                               unsigned char* xbase) {
-    if (wcopier) {
-        const int ahead = nsteps - 1 - s;
-        if (ahead >= SW - 2)
-            wait_vmcnt<T::WPW * (SW - 2)>();
-        else
-            wait_vmcnt_mult<T::WPW>(ahead);
-    } else if (s + 1 < nsteps) {
-        if (c0 + s + 1 < nkh)
-            wait_vmcnt<T::XPW_H>();
-        else
-            wait_vmcnt<T::XPW_E>();
-    } else {
-        wait_vmcnt<0>();
+// Copy order.  Every wave copies its share of both streams; step s (after
+// its barrier) copies the activations of chunk s + SX - 1, then the weights
+// of chunk s + SW - 1, and the prologue issues the copies the steps
+// 1 - SW .. -1 would have, in the same order.  A wave's loads complete in
+// issue order, so at step s waiting for its activation copies of chunk s
+// (issued after those of the weights of chunk s, SW > SX) waits for both:
+// at most the copies issued after them may be outstanding, the weights of
+// chunk s + SW - SX and the activations and weights of the SX - 2 steps
+// between (chunks past the segment are never copied).
+template <class T, int SW, int SX>
+__device__ __forceinline__ int mlp_wait_count(int s, int nsteps, int c0, int nkh) {
+    int n = s + SW - SX < nsteps ? T::WPW : 0;
+#pragma unroll
+    for (int j = 1; j <= SX - 2; ++j) {
+        if (s + j < nsteps) n += c0 + s + j < nkh ? T::XPW_H : T::XPW_E;
+        if (s + j + SW - SX < nsteps) n += T::WPW;
     }
-    block_barrier();
-    if (wcopier) {
-        if (cur.wnext < nsteps) {
-            mlp_copy_w<TG>(wsrc, cur.wnext, wbase + cur.wstage * T::WSTAGE, T::WTILE);
-            ++cur.wnext;
-            cur.wstage = cur.wstage + 1 == SW ? 0 : cur.wstage + 1;
-        }
-    } else if (cur.xnext < nsteps) {
-        mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < nkh, cur.xnext, xbase + cur.xstage * T::XSTAGE);
+    return n;
+}
+
+// The copies of (emulated) step s: activations of chunk s + SX - 1 (when that
+// is a chunk of the segment), then weights of chunk s + SW - 1.
+template <class T, int SW, int SX, bool PAIRED, int TG = T::TW * 2>
+__device__ __forceinline__ void mlp_step_copies(MlpCursor& cur, int s, int nsteps, int c0, int nkh, int c,
+                                                const uint16_t* const (&wsrc)[TG], const uint16_t* hsrc,
+                                                const uint16_t* const (&esrc)[T::XPW_E], unsigned char* dyn) {
+    if (s + SX - 1 >= 0 && cur.xnext < nsteps) {
+        mlp_copy_x<T::XPW_E, PAIRED>(hsrc, esrc, c0 + cur.xnext < nkh, cur.xnext,
+                                     dyn + T::XOFF + cur.xstage * T::XSTAGE, c);
         ++cur.xnext;
         cur.xstage = cur.xstage + 1 == SX ? 0 : cur.xstage + 1;
     }
+    if (cur.wnext < nsteps) {
+        mlp_copy_w<TG>(wsrc, cur.wnext, dyn + cur.wstage * T::WSTAGE, T::WTILE, c);
+        ++cur.wnext;
+        cur.wstage = cur.wstage + 1 == SW ? 0 : cur.wstage + 1;
+    }
+}
+
+// The start of step s: wait for this wave's copies of chunk s, meet the
+// barrier (every wave's copies have landed; the stages chunk s - 1 used are
+// free), then copy into the freed stages.
+template <class T, int SW, int SX, bool PAIRED, int TG = T::TW * 2>
+__device__ __forceinline__ void mlp_step_begin(MlpCursor& cur, int s, int nsteps, int c0, int nkh, int c,
+                                               const uint16_t* const (&wsrc)[TG], const uint16_t* hsrc,
+                                               const uint16_t* const (&esrc)[T::XPW_E], unsigned char* dyn) {
+    wait_vmcnt_dyn(mlp_wait_count<T, SW, SX>(s, nsteps, c0, nkh));
+    block_barrier();
+    mlp_step_copies<T, SW, SX, PAIRED>(cur, s, nsteps, c0, nkh, c, wsrc, hsrc, esrc, dyn);
 }
 
 __device__ __forceinline__ CostSplit mlp_shape(const MlpDmaArgs& a) {
     return cost_split(a.items, a.nkh, a.nke, a.wh, a.we, a.G);
 }
 
-// Weight DMA sources of copier cw (rows 16cw..16cw+15 of every tile, two
-// 8-row blocks) at chunk c0 of `item`.
+// Weight DMA sources of wave c (rows 8c..8c+7 of every tile) at chunk c0 of
+// `item`.
 template <int TG, int WMAP>
-__device__ __forceinline__ void mlp_weight_sources(const MlpDmaArgs& a, int item, int c0, int cw, int lane,
-                                                   const uint16_t* (&wsrc)[TG][2]) {
+__device__ __forceinline__ void mlp_weight_sources(const MlpDmaArgs& a, int item, int c0, int c, int lane,
+                                                   const uint16_t* (&wsrc)[TG]) {
     const int lrow = lane >> 3, lslot = lane & 7;
+    const int row = 8 * c + lrow;
 #pragma unroll
-    for (int t = 0; t < TG; ++t)
-#pragma unroll
-        for (int hb = 0; hb < 2; ++hb) {
-            const int row = 16 * cw + 8 * hb + lrow;
-            const int tile = min(item * TG + t, a.ntiles - 1);
-            const uint16_t* base;
-            if constexpr (WMAP == kMlpWGateUp) {
-                const int i = min(tile * 16 + (row & 15), a.N - 1);
-                base = (row < 16 ? a.w : a.wu) + (size_t)i * a.Kw;
-            } else {
-                base = a.w + (size_t)min(tile * 32 + row, a.N - 1) * a.Kw;
-            }
-            wsrc[t][hb] = base + 8 * (lslot ^ mlp_swz128(row)) + 64 * c0;
+    for (int t = 0; t < TG; ++t) {
+        const int tile = min(item * TG + t, a.ntiles - 1);
+        const uint16_t* base;
+        if constexpr (WMAP == kMlpWGateUp) {
+            const int i = min(tile * 16 + (row & 15), a.N - 1);
+            base = (row < 16 ? a.w : a.wu) + (size_t)i * a.Kw;
+        } else {
+            base = a.w + (size_t)min(tile * 32 + row, a.N - 1) * a.Kw;
         }
+        wsrc[t] = base + 8 * (lslot ^ mlp_swz128(row)) + 64 * c0;
+    }
 }
 
 // The copy state of one item piece, chunks [c0, c1) of `item`: this lane's
 // DMA sources at chunk c0 and the ring cursors.
 template <int TG, int XPW>
 struct MlpSegment {
-    const uint16_t* wsrc[TG][2];
-    const uint16_t* hsrc[2];
+    const uint16_t* wsrc[TG];
+    const uint16_t* hsrc;
     const uint16_t* esrc[XPW];
     MlpCursor cur;
     int c0, nsteps;
 };
 
-// Waves 0-1 copy the weights, waves 2-3 the activations: a wave waits on
-// its own copies only (s_waitcnt counts a wave's loads in issue order), so
-// the activation waits, two chunks out, never hold up the weight stream,
-// which runs SW - 1 chunks ahead.  cw: the wave's index among the copiers of
-// its stream.
-__device__ __forceinline__ int mlp_copier_index(int wave) { return wave < 2 ? wave : wave - 2; }
-
-// A piece's sources and the ring prologue (weights of chunks 0 .. SW-2,
-// activations of chunks 0 .. SX-2).  Issued apart from the piece's loop so
-// that a workgroup's first copies leave before any set-up of its own.
+// A piece's sources and the ring prologue (the copies of the emulated steps
+// 1 - SW .. -1).  Issued apart from the piece's loop so that a workgroup's
+// first copies leave before any set-up of its own.
 template <int TG, int NTE, bool PAIRED, int SW, int SX, int WMAP>
 __device__ __forceinline__ void mlp_piece_begin(const MlpDmaArgs& a, int item, int c0, int c1, unsigned char* dyn,
                                                 MlpSegment<TG, MlpDmaTraits<TG, NTE, PAIRED, SW, SX>::XPW_E>& sg) {
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const bool wcopier = wave < 2;
-    const int cw = mlp_copier_index(wave);
+    const int c = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // this wave's quarter of every chunk
     // this lane's row and physical slot in a 1 KiB DMA block of 128-byte rows
     const int lrow = lane >> 3, lslot = lane & 7;
     sg.c0 = c0;
     sg.nsteps = c1 - c0;
-    mlp_weight_sources<TG, WMAP>(a, item, c0, cw, lane, sg.wsrc);
-    // h phase: 32 rows of h~ in four 8-row blocks, blocks cw and cw + 2
-#pragma unroll
-    for (int v = 0; v < 2; ++v) {
-        const int row = 8 * (cw + 2 * v) + lrow;
-        sg.hsrc[v] = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) +
-                                           8 * (lslot ^ T::swz128(row)) + 64 * c0
-                                     : nullptr;
+    mlp_weight_sources<TG, WMAP>(a, item, c0, c, lane, sg.wsrc);
+    // h phase: 32 rows of h~ in four 8-row blocks, block c
+    {
+        const int row = 8 * c + lrow;
+        sg.hsrc = a.xh != nullptr ? a.xh + (size_t)min(row, a.Rh - 1) * (a.nkh * 64) + 8 * (lslot ^ T::swz128(row)) +
+                                        64 * c0
+                                  : nullptr;
     }
-    // e phase: DMA instruction q = cw + 2v covers rows XRPI*q ..
+    // e phase: DMA instruction q = c + 4v covers rows XRPI*q ..
     const int ce0 = c0 - a.nkh;   // e chunk of the segment's first chunk (negative in the h phase)
 #pragma unroll
     for (int v = 0; v < T::XPW_E; ++v) {
-        const int q = cw + 2 * v;
+        const int q = c + 4 * v;
         int row, ps;
         if constexpr (PAIRED) {
             row = 4 * q + (lane >> 4);
@@ -394,20 +380,10 @@ __device__ __forceinline__ void mlp_piece_begin(const MlpDmaArgs& a, int item, i
         }
         sg.esrc[v] = a.xe + (size_t)min(row, a.Re - 1) * a.lde + 8 * ps + (long)(PAIRED ? 128 : 64) * ce0;
     }
-    MlpCursor cur{0, 0, 0, 0, 0, 0};
-    unsigned char* const wbase = dyn + (2 * cw) * 1024;
-    unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
-    if (wcopier) {
-        for (; cur.wnext < SW - 1 && cur.wnext < sg.nsteps; ++cur.wnext)
-            mlp_copy_w<TG>(sg.wsrc, cur.wnext, wbase + cur.wnext * T::WSTAGE, T::WTILE);
-        cur.wstage = cur.wnext % SW;
-    } else {
-        for (; cur.xnext < SX - 1 && cur.xnext < sg.nsteps; ++cur.xnext)
-            mlp_copy_x<T::XPW_E, PAIRED>(sg.hsrc, sg.esrc, c0 + cur.xnext < a.nkh, cur.xnext,
-                                         xbase + cur.xnext * T::XSTAGE);
-        cur.xstage = cur.xnext % SX;
-    }
-    sg.cur = cur;
+    sg.cur = MlpCursor{0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int s = 1 - SW; s < 0; ++s)
+        mlp_step_copies<T, SW, SX, PAIRED>(sg.cur, s, sg.nsteps, c0, a.nkh, c, sg.wsrc, sg.hsrc, sg.esrc, dyn);
 }
 
 // The rest of the piece begun by mlp_piece_begin, streamed through the rings
@@ -425,18 +401,13 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const bool wcopier = wave < 2;
-    const int cw = mlp_copier_index(wave);
     // the wave's place in the 2 x 2 grid: weight tiles wa*TW.., activation tiles wb*NTW..
     const int wa = wave & 1, wb = wave >> 1;
     const int fr = lane & 31;
     const int c0 = sg.c0, nsteps = sg.nsteps;
     const auto& wsrc = sg.wsrc;
-    const auto& hsrc = sg.hsrc;
     const auto& esrc = sg.esrc;
     MlpCursor& cur = sg.cur;
-    unsigned char* const wbase = dyn + (2 * cw) * 1024;
-    unsigned char* const xbase = dyn + T::XOFF + cw * 1024;
 
     f32x16 acc_h[TW], acc_e[TW][NTW];
 #pragma unroll
@@ -455,7 +426,7 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
     // s - 1 are free), then refills the freed stages.
     const int nh = max(0, min(nsteps, a.nkh - c0));   // h-phase chunks of the segment
     for (int s = 0; s < nh; ++s) {
-        mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
+        mlp_step_begin<T, SW, SX, PAIRED>(cur, s, nsteps, c0, a.nkh, wave, wsrc, sg.hsrc, esrc, dyn);
         const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
         const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
         cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
@@ -474,7 +445,7 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
         }
     }
     for (int s = nh; s < nsteps; ++s) {
-        mlp_step_begin<T, SW, SX, PAIRED>(cur, wcopier, s, nsteps, c0, a.nkh, wsrc, hsrc, esrc, wbase, xbase);
+        mlp_step_begin<T, SW, SX, PAIRED>(cur, s, nsteps, c0, a.nkh, wave, wsrc, sg.hsrc, esrc, dyn);
         const unsigned char* wt = dyn + cur.rw * T::WSTAGE + wa * TW * T::WTILE;
         const unsigned char* xt = dyn + T::XOFF + cur.rx * T::XSTAGE;
         cur.rw = cur.rw + 1 == SW ? 0 : cur.rw + 1;
