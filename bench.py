@@ -540,10 +540,14 @@ def lm_roofline(w, gemm):
     return roof
 
 
+EVENT_EVERY = 4   # timed steps per pair of events around the stage-2 LM-head kernel
+
+
 def measure(w, copies, st, steps, warmup, copy_calibration=False):
     """Timed drafting steps of workload w (only the two events around the
-    stage-2 LM-head kernel inside the timed region), then an untimed pass with
-    events between the calls for the per-stage split."""
+    stage-2 LM-head kernel inside the timed region, on every EVENT_EVERY-th
+    step), then an untimed pass with events between the calls for the
+    per-stage split."""
     dev = torch.device("cuda", 0)
     d, V, R, b = w.d, w.V, w.rows, w.b
     dr = make_drafter(w, copies[0])
@@ -583,15 +587,17 @@ def measure(w, copies, st, steps, warmup, copy_calibration=False):
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    # timed steps: only the two events around the stage-2 LM-head kernel (an event
-    # on the stream leaves a few microseconds of idle GPU), for its live duration
+    # timed steps: the two events around the stage-2 LM-head kernel, for its live
+    # duration, on every EVENT_EVERY-th step only (an event on the stream leaves
+    # a few microseconds of idle GPU: every step would carry ~6 us of it)
+    every = EVENT_EVERY if steps >= 4 * EVENT_EVERY else 1
     evs = make_events()
     t0 = time.perf_counter()
     for i in range(steps):
-        step(i, evs[i])
+        step(i, evs[i] if i % every == 0 else None)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    gemm_us = sorted(1000.0 * e[5].elapsed_time(e[6]) for e in evs)
+    gemm_us = sorted(1000.0 * e[5].elapsed_time(e[6]) for i, e in enumerate(evs) if i % every == 0)
 
     # per-stage split from a second, untimed pass with events between the calls
     sevs = make_events()
