@@ -30,6 +30,14 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
     return u >> 16;
 }
 
+// Two floats to bf16 with round-to-nearest-even in one instruction
+// (v_cvt_pk_bf16_f32): a in the low half, b in the high half.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2_bits(float a, float b) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){a, b}, b2));
+}
+
 // Monotone map float -> uint32 (larger float <=> larger key).
 __device__ __forceinline__ uint32_t f32_key(float f) {
     uint32_t u = __float_as_uint(f);

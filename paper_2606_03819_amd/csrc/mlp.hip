@@ -150,7 +150,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const uint16_t* 
             for (int q = 0; q < 4; ++q) {
                 const float lo = bf16_bits_to_f32(v[c][q] & 0xffffu) * inv * bf16_bits_to_f32(gv[c][q] & 0xffffu);
                 const float hi = bf16_bits_to_f32(v[c][q] >> 16) * inv * bf16_bits_to_f32(gv[c][q] >> 16);
-                o[q] = f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+                o[q] = f32x2_to_bf16x2_bits(lo, hi);
             }
             *reinterpret_cast<u32x4*>(dst + 8 * pc) = o;
         }

@@ -190,7 +190,7 @@ __device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, cons
             for (int p = 0; p < 4; ++p) {
                 const float y0 = bf16_bits_to_f32(hv[it][p] & 0xffffu) + v[2 * p];
                 const float y1 = bf16_bits_to_f32(hv[it][p] >> 16) + v[2 * p + 1];
-                o[p] = f32_to_bf16_bits(y0) | (f32_to_bf16_bits(y1) << 16);
+                o[p] = f32x2_to_bf16x2_bits(y0, y1);
             }
             *reinterpret_cast<u32x4*>(a.out + (size_t)u.r * a.Nout + u.tile * 32 + 8 * u.q) = o;
         }
@@ -208,17 +208,17 @@ __device__ __forceinline__ void mlp_epilogue(const MlpDmaArgs& a, int item, cons
             u32x4 hi4, lo4;
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                uint32_t hb[2], lb[2];
+                float av[2];
 #pragma unroll
                 for (int z = 0; z < 2; ++z) {
                     const int e2 = 2 * p + z;
-                    float av = gv[e2] / (1.0f + __expf(-gv[e2]));
-                    if constexpr (EPI == kMlpEpiSwiGLU) av *= uv[e2];
-                    hb[z] = f32_to_bf16_bits(av);
-                    lb[z] = f32_to_bf16_bits(av - bf16_bits_to_f32(hb[z]));
+                    // silu(g) = g / (1 + e^-g), the quotient by the hardware reciprocal
+                    av[z] = gv[e2] * __builtin_amdgcn_rcpf(1.0f + __expf(-gv[e2]));
+                    if constexpr (EPI == kMlpEpiSwiGLU) av[z] *= uv[e2];
                 }
-                hi4[p] = hb[0] | (hb[1] << 16);
-                lo4[p] = lb[0] | (lb[1] << 16);
+                hi4[p] = f32x2_to_bf16x2_bits(av[0], av[1]);
+                lo4[p] = f32x2_to_bf16x2_bits(av[0] - bf16_bits_to_f32(hi4[p] & 0xffffu),
+                                              av[1] - bf16_bits_to_f32(hi4[p] >> 16));
             }
             uint16_t* o = a.out + (size_t)u.r * 2 * a.Nout + (size_t)(i0 >> 3) * 16;
             *reinterpret_cast<u32x4*>(o) = hi4;
