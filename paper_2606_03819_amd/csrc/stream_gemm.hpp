@@ -691,17 +691,17 @@ struct EpiSwiGLU {
                     uint32_t hi2[2], lo2[2];
 #pragma unroll
                     for (int q = 0; q < 2; ++q) {
-                        uint32_t h[2], l[2];
+                        float a[2];
 #pragma unroll
                         for (int e = 0; e < 2; ++e) {
                             const float g = acc[mt][nt][4 * jg + 2 * q + e];
                             const float u = acc[mt][nt][4 * jg + 2 * q + e + 8];
-                            const float a = g / (1.0f + __expf(-g)) * u;
-                            h[e] = f32_to_bf16_bits(a);
-                            l[e] = f32_to_bf16_bits(a - bf16_bits_to_f32(h[e]));
+                            // silu(g) = g / (1 + e^-g), the quotient by the hardware reciprocal
+                            a[e] = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
                         }
-                        hi2[q] = h[0] | (h[1] << 16);
-                        lo2[q] = l[0] | (l[1] << 16);
+                        hi2[q] = f32x2_to_bf16x2_bits(a[0], a[1]);
+                        lo2[q] = f32x2_to_bf16x2_bits(a[0] - bf16_bits_to_f32(hi2[q] & 0xffffu),
+                                                      a[1] - bf16_bits_to_f32(hi2[q] >> 16));
                     }
                     uint16_t* o = out + (size_t)r * 2 * I + (size_t)(i >> 3) * 16 + (i & 7);
                     *reinterpret_cast<uint2*>(o) = uint2{hi2[0], hi2[1]};
@@ -737,16 +737,15 @@ struct EpiSiLU {
                     uint32_t hi2[2], lo2[2];
 #pragma unroll
                     for (int q = 0; q < 2; ++q) {
-                        uint32_t h[2], l[2];
+                        float a[2];
 #pragma unroll
                         for (int e = 0; e < 2; ++e) {
                             const float g = acc[mt][nt][4 * jg + 2 * q + e];
-                            const float a = g / (1.0f + __expf(-g));
-                            h[e] = f32_to_bf16_bits(a);
-                            l[e] = f32_to_bf16_bits(a - bf16_bits_to_f32(h[e]));
+                            a[e] = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
                         }
-                        hi2[q] = h[0] | (h[1] << 16);
-                        lo2[q] = l[0] | (l[1] << 16);
+                        hi2[q] = f32x2_to_bf16x2_bits(a[0], a[1]);
+                        lo2[q] = f32x2_to_bf16x2_bits(a[0] - bf16_bits_to_f32(hi2[q] & 0xffffu),
+                                                      a[1] - bf16_bits_to_f32(hi2[q] >> 16));
                     }
                     uint16_t* o = out + (size_t)r * 2 * I + (size_t)(i >> 3) * 16 + (i & 7);
                     *reinterpret_cast<uint2*>(o) = uint2{hi2[0], hi2[1]};
@@ -852,11 +851,9 @@ struct EpiResidual {
                     const uint2 hv = *reinterpret_cast<const uint2*>(hrow + n);
                     const float h0 = bf16_bits_to_f32(hv.x & 0xffffu), h1 = bf16_bits_to_f32(hv.x >> 16);
                     const float h2 = bf16_bits_to_f32(hv.y & 0xffffu), h3 = bf16_bits_to_f32(hv.y >> 16);
-                    const uint32_t o0 = f32_to_bf16_bits(h0 + acc[mt][nt][4 * jg + 0]);
-                    const uint32_t o1 = f32_to_bf16_bits(h1 + acc[mt][nt][4 * jg + 1]);
-                    const uint32_t o2 = f32_to_bf16_bits(h2 + acc[mt][nt][4 * jg + 2]);
-                    const uint32_t o3 = f32_to_bf16_bits(h3 + acc[mt][nt][4 * jg + 3]);
-                    *reinterpret_cast<uint2*>(out + (size_t)r * d + n) = uint2{o0 | (o1 << 16), o2 | (o3 << 16)};
+                    const uint32_t o01 = f32x2_to_bf16x2_bits(h0 + acc[mt][nt][4 * jg + 0], h1 + acc[mt][nt][4 * jg + 1]);
+                    const uint32_t o23 = f32x2_to_bf16x2_bits(h2 + acc[mt][nt][4 * jg + 2], h3 + acc[mt][nt][4 * jg + 3]);
+                    *reinterpret_cast<uint2*>(out + (size_t)r * d + n) = uint2{o01, o23};
                 }
             }
         }
