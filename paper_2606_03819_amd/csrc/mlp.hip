@@ -367,15 +367,19 @@ static void launch_norms(const void* h, const int32_t* root, const int32_t* cont
 // four fifths of its bytes, keeps three weight stages in flight (measured
 // faster than four or five); the input projections are insensitive to
 // four to six.
-template <int TG, bool PAIRED>
+template <int TG, bool PAIRED, int NTE>
 constexpr int mlp_dma_sw() {
-    return PAIRED ? (TG == 2 ? 4 : 4) : (TG == 2 ? 10 : 5);
+    return PAIRED ? 4 : (TG == 2 ? 10 : (NTE == 8 ? 4 : 5));
 }
-constexpr int kMlpDmaSX = 3;
+// activation stages: eight tiles' 32 KiB chunks leave room for one in flight
+template <int NTE>
+constexpr int mlp_dma_sx() {
+    return NTE == 8 ? 2 : 3;
+}
 
 template <int TG, int NTE, bool PAIRED, int WMAP, int EPI>
 static hipError_t launch_mlp_dma_nte(const MlpDmaArgs& a, hipStream_t st) {
-    constexpr int SW = mlp_dma_sw<TG, PAIRED>(), SX = kMlpDmaSX;
+    constexpr int SW = mlp_dma_sw<TG, PAIRED, NTE>(), SX = mlp_dma_sx<NTE>();
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
     static_assert(T::SMEM <= 152 * 1024, "LDS of one workgroup");
     auto kern = mlp_dma_kernel<TG, NTE, PAIRED, SW, SX, WMAP, EPI>;
@@ -392,6 +396,10 @@ static hipError_t launch_mlp_dma(const MlpDmaArgs& a, const MlpDmaPlan& p, hipSt
     if (p.TG != TG) return hipErrorInvalidValue;
     if (p.NTE == 1) return launch_mlp_dma_nte<TG, 1, PAIRED, WMAP, EPI>(a, st);
     if (p.NTE == 2) return launch_mlp_dma_nte<TG, 2, PAIRED, WMAP, EPI>(a, st);
+    if constexpr (!PAIRED && EPI != kMlpEpiResidual) {   // eight tiles: the input projections only
+        if (p.NTE == 8) return launch_mlp_dma_nte<TG, 8, PAIRED, WMAP, EPI>(a, st);
+    }
+    if (p.NTE != 4) return hipErrorInvalidValue;
     return launch_mlp_dma_nte<TG, 4, PAIRED, WMAP, EPI>(a, st);
 }
 
@@ -425,6 +433,28 @@ hipError_t launch_arapprox(const void* h, const int32_t* root, const int32_t* co
         if (mlp_dma_applies(true, b, gamma, rt.Rs, d, I, ew))
             return launch_arapprox_dma(h, root, context, topk_idx, emb, gain_h, gain_e, w_gate, w_up, w_down, b, d,
                                        I, V, rt, npre, eps, ht, et, act, hp, mlp_partial, counters, diag, stream);
+        if (mlp_dma_gate_applies(true, b, gamma, rt.Rs, d, I, ew)) {
+            // 129-256 rows: the input projections on the one-row-block kernel
+            // (eight activation tiles), the down projection over several row blocks
+            const bool swiglu = w_up != nullptr;
+            const MlpDmaPlan pg = mlp_dma_gate_plan(rows, d, ew, I, swiglu);
+            const GemmPlan pd = down_plan(rows, d, I);
+            launch_norms<uint16_t>(h, root, context, topk_idx, emb, gain_h, gain_e, b, d, V, rt, npre, eps, ht, et,
+                                   diag, counters, (int)(pg.items + pd.counter_ints()), stream);
+            const uint16_t* hb = static_cast<const uint16_t*>(h);
+            uint16_t* actb = static_cast<uint16_t*>(act);
+            const MlpDmaArgs ag = mlp_dma_args(pg, static_cast<const uint16_t*>(w_gate),
+                                               static_cast<const uint16_t*>(w_up), I, d + ew,
+                                               static_cast<const uint16_t*>(ht), static_cast<const uint16_t*>(et),
+                                               ew, b * rt.gamma, rows, actb, I, hb, rt, mlp_partial, counters);
+            const hipError_t e = swiglu ? launch_mlp_dma<false, kMlpWGateUp, kMlpEpiSwiGLU>(ag, pg, stream)
+                                        : launch_mlp_dma<false, kMlpWPlain, kMlpEpiSiLU>(ag, pg, stream);
+            if (e != hipSuccess) return e;
+            run_product(pd, WRowsPairedK{static_cast<const uint16_t*>(w_down), d, I}, XRowsPlain{actb, 2l * I},
+                        rows, 2 * I, MakeResidual{static_cast<uint16_t*>(hp), hb, d, rt}, mlp_partial,
+                        counters + pg.items, stream);
+            return hipGetLastError();
+        }
         // several row blocks: the input projection split at the h~ / e~ boundary
         // (the h~ half once per drafter state), then the down projection
         const bool swiglu = w_up != nullptr;

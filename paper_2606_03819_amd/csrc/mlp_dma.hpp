@@ -96,16 +96,15 @@ struct MlpDmaTraits {
     // the h phase / of NTE = 1, splitting its k sub-steps)
     static constexpr int TW = TG / 2;
     static constexpr int NTW = NTE >= 2 ? NTE / 2 : 1;
-    // after the loop: the waves' accumulators, then (in the same LDS) the summed ones
+    // after the loop the piece's sums (PF floats) reuse the ring's LDS
     static constexpr int TILE_F = 1024;                     // floats of one 32x32 accumulator
     static constexpr int PF = TG * TILE_F * (1 + NTE);      // floats of one item's sums (h, then e)
-    static constexpr int SCR_W = 4 * TW * (1 + NTW) * TILE_F * 4;
-    static constexpr int SCR_C = PF * 4;   // the summed pieces
-    static constexpr int SMEM = RING > SCR_W ? (RING > SCR_C ? RING : SCR_C) : (SCR_W > SCR_C ? SCR_W : SCR_C);
+    static constexpr int SCR_C = PF * 4;
+    static constexpr int SMEM = RING > SCR_C ? RING : SCR_C;
     static constexpr int HC = 4 * TG;                       // summed h floats per thread
     static constexpr int EC = 4 * TG * NTE;                 // summed e floats per thread
     static_assert(TG % 2 == 0, "weight tiles split over two waves");
-    static_assert(NTE == 1 || NTE == 2 || NTE == 4, "activation tiles");
+    static_assert(NTE == 1 || NTE == 2 || NTE == 4 || NTE == 8, "activation tiles");
     static_assert(XPW_E >= 1 && XSTAGE_E % 4096 == 0, "whole DMA instructions per wave");
     static_assert(SW > SX && SX >= 2, "ring depths: a chunk's weights are copied before its activations");
     // 16-byte slot swizzles: 128-byte rows (weights, plain activations) and
@@ -397,7 +396,7 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
                                               unsigned char* dyn, float (&hc)[4 * TG], float (&ec)[4 * TG * NTE]) {
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
     constexpr int TW = T::TW, NTW = T::NTW;
-    static_assert(SX == 3, "two activation chunks in flight");
+    static_assert(SX == 2 || SX == 3, "one or two activation chunks in flight");
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -480,36 +479,52 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
     }
     __syncthreads();   // every copy has landed and every ring read is done
 
-    // ---- the piece's sums (tile t of wave grid column t / TW; waves that
-    // share a tile, along the activation tiles, add in wave order)
-    float* wsc = reinterpret_cast<float*>(dyn);   // [wave][TW][1 + NTW][1024]
+    // ---- the piece's sums, in LDS in their final layout (fs: [TG][1024] h,
+    // then [TG][NTE][1024] e; element j * 64 + lane of a tile is the MFMA
+    // register order).  With NTE >= 2 every (weight tile, activation tile)
+    // of the e phase belongs to one wave, which writes it in place; the h
+    // tile (and NTE = 1's e tile) is split over the two waves of a grid
+    // column (k sub-steps), so the second writes and the first adds its own.
+    float* fs = reinterpret_cast<float*>(dyn);
+    float* const fe = fs + TG * 1024;
+    if constexpr (NTE >= 2) {
 #pragma unroll
-    for (int t = 0; t < TW; ++t)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            wsc[((wave * TW + t) * (1 + NTW)) * 1024 + j * 64 + lane] = acc_h[t][j];
+        for (int t = 0; t < TW; ++t)
 #pragma unroll
             for (int n = 0; n < NTW; ++n)
-                wsc[((wave * TW + t) * (1 + NTW) + 1 + n) * 1024 + j * 64 + lane] = acc_e[t][n][j];
-        }
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    fe[((wa * TW + t) * NTE + wb * NTW + n) * 1024 + j * 64 + lane] = acc_e[t][n][j];
+    }
+    if (wb == 1) {
+#pragma unroll
+        for (int t = 0; t < TW; ++t)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                fs[(wa * TW + t) * 1024 + j * 64 + lane] = acc_h[t][j];
+                if constexpr (NTE == 1) fe[(wa * TW + t) * 1024 + j * 64 + lane] = acc_e[t][0][j];
+            }
+    }
     __syncthreads();
-    auto wslot = [&](int w, int tl, int part) { return wsc + ((w * TW + tl) * (1 + NTW) + part) * 1024; };
-    // element tid + 256 i: tile and offset are constants plus tid (tid < 256)
+    if (wb == 0) {
 #pragma unroll
-    for (int i = 0; i < T::HC; ++i) {
-        const int t = i >> 2, f = ((i & 3) << 8) + tid;   // [TG][1024]
-        const int col = t / TW, tl = t % TW;
-        hc[i] = wslot(col, tl, 0)[f] + wslot(2 + col, tl, 0)[f];
-    }
+        for (int t = 0; t < TW; ++t)
 #pragma unroll
-    for (int i = 0; i < T::EC; ++i) {
-        const int t = i / (4 * NTE), n = (i >> 2) % NTE, f = ((i & 3) << 8) + tid;   // [TG][NTE][1024]
-        const int col = t / TW, tl = t % TW;
-        if constexpr (NTE >= 2)
-            ec[i] = wslot((n / NTW) * 2 + col, tl, 1 + n % NTW)[f];
-        else
-            ec[i] = wslot(col, tl, 1)[f] + wslot(2 + col, tl, 1)[f];
+            for (int j = 0; j < 16; ++j) {
+                float* ph = fs + (wa * TW + t) * 1024 + j * 64 + lane;
+                *ph = acc_h[t][j] + *ph;
+                if constexpr (NTE == 1) {
+                    float* pe = fe + (wa * TW + t) * 1024 + j * 64 + lane;
+                    *pe = acc_e[t][0][j] + *pe;
+                }
+            }
     }
+    __syncthreads();
+    // element tid + 256 i of each phase
+#pragma unroll
+    for (int i = 0; i < T::HC; ++i) hc[i] = fs[tid + 256 * i];
+#pragma unroll
+    for (int i = 0; i < T::EC; ++i) ec[i] = fe[tid + 256 * i];
     __syncthreads();   // the per-wave sums are read; the LDS is free
 }
 
@@ -637,18 +652,14 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
                 // the pieces' sums in piece order, then the epilogue
                 // e pieces per batch: three for SwiGLU over four tiles (an item's
                 // e half usually spans three pieces), one for the widest residual
-                // epilogue (registers), else two
-                constexpr int BE = NTE == 4 ? (EPI == kMlpEpiSwiGLU ? 3 : (EPI == kMlpEpiResidual && HASH ? 1 : 2)) : 2;
+                // epilogue and for eight tiles (registers), else two
+                constexpr int BE = NTE == 8 ? 1 : (NTE == 4 ? (EPI == kMlpEpiSwiGLU ? 3 : (EPI == kMlpEpiResidual && HASH ? 1 : 2)) : 2);
                 mlp_combine_pieces<TG, NTE, T::PF, BE>(a.partial, 2 * a.G, pcs, csc);
                 __syncthreads();
                 mlp_epilogue<TG, NTE, EPI, HASH>(a, item, MlpLdsSums{csc, csc + T::HC * 256});
             }
         } else {
-#pragma unroll
-            for (int i = 0; i < T::HC; ++i) csc[tid + 256 * i] = hc[i];
-#pragma unroll
-            for (int i = 0; i < T::EC; ++i) csc[T::HC * 256 + tid + 256 * i] = ec[i];
-            __syncthreads();
+            // a whole item: its sums are in LDS as the piece left them
             mlp_epilogue<TG, NTE, EPI, HASH>(a, item, MlpLdsSums{csc, csc + T::HC * 256});
         }
         u = (item + 1) * nk;

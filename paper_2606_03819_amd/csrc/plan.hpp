@@ -305,6 +305,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 #endif
 constexpr int kMlpDmaMinUnits = 12;
 constexpr int kMlpDmaMaxRows = 128;    // conditional rows (four activation tiles)
+constexpr int kMlpDmaMaxGateRows = 256; // the input projections alone (eight activation tiles)
 constexpr int kMlpDmaMaxStates = 32;   // drafter states (one activation tile)
 struct MlpDmaPlan {
     int TG;       // weight tiles per item
@@ -317,7 +318,7 @@ struct MlpDmaPlan {
 inline MlpDmaPlan mlp_dma_plan(int rows, int ntiles, int nkh, int nke, int TG) {
     MlpDmaPlan p;
     p.TG = TG;
-    p.NTE = rows <= 32 ? 1 : (rows <= 64 ? 2 : 4);
+    p.NTE = rows <= 32 ? 1 : (rows <= 64 ? 2 : (rows <= 128 ? 4 : 8));
     p.ntiles = ntiles;
     p.items = cdiv(ntiles, TG);
     p.nkh = nkh;
@@ -330,9 +331,10 @@ inline MlpDmaPlan mlp_dma_plan(int rows, int ntiles, int nkh, int nke, int TG) {
     // three fifths of an h chunk's rate (the activation copies from L2 share
     // the CU's load path with the weight stream; 5:3 measured best against
     // 3:2 and 9:5); two tiles take a ratio between that and 1, and one tile,
-    // like the h phase, costs the same.
-    p.wh = nkh > 0 && p.NTE == 4 ? 3 : (nkh > 0 && p.NTE == 2 ? 4 : 1);
-    p.we = nkh > 0 && p.NTE == 4 ? 5 : (nkh > 0 && p.NTE == 2 ? 5 : 1);
+    // like the h phase, costs the same; eight tiles (the input
+    // projections of 129-256 rows) 5:2.
+    p.wh = nkh == 0 ? 1 : (p.NTE == 8 ? 2 : (p.NTE == 4 ? 3 : (p.NTE == 2 ? 4 : 1)));
+    p.we = nkh == 0 ? 1 : (p.NTE == 8 ? 5 : (p.NTE == 4 ? 5 : (p.NTE == 2 ? 5 : 1)));
     if (!cost_split_valid(p.items, nkh, nke, p.wh, p.we, p.G)) p.wh = p.we = 1;
     return p;
 }
@@ -355,6 +357,17 @@ inline MlpDmaPlan mlp_dma_linear_plan(int rows, int d) {
 // One row block holds every conditional row and each plan the path may
 // launch (either gate plan, the down projection, the linear layer) keeps its
 // split in 32-bit arithmetic.
+// 129-256 conditional rows: the input projections on the one-row-block kernel
+// (eight activation tiles), the down projection on the kernel for several
+// row blocks (its activation pairs for eight tiles do not fit the LDS).
+inline bool mlp_dma_gate_applies(bool bf16, int b, int gamma, int R, int d, int I, int ew) {
+    if (!(bf16 && (long long)b * gamma <= kMlpDmaMaxStates && (long long)b * R > kMlpDmaMaxRows &&
+          (long long)b * R <= kMlpDmaMaxGateRows && d % 64 == 0 && I % 64 == 0 && ew % 64 == 0))
+        return false;
+    const int rows = b * R;
+    return mlp_dma_plan_ok(mlp_dma_gate_plan(rows, d, ew, I, true)) &&
+           mlp_dma_plan_ok(mlp_dma_gate_plan(rows, d, ew, I, false));
+}
 inline bool mlp_dma_applies(bool bf16, int b, int gamma, int R, int d, int I, int ew) {
     if (!(bf16 && (long long)b * gamma <= kMlpDmaMaxStates && (long long)b * R <= kMlpDmaMaxRows && d % 64 == 0 &&
           I % 64 == 0 && ew % 64 == 0))
@@ -434,6 +447,16 @@ inline Workspace workspace_layout(int b, int gamma, int d, int I, int V, int k, 
             const size_t qc = (size_t)qg.items + qd.items;
             nc = nc > qc ? nc : qc;
             nc = nc > (size_t)ql.items ? nc : (size_t)ql.items;
+        }
+        if (mlp_dma_gate_applies(bf16, b, gamma, R, d, I, npre * d)) {
+            // either gate plan on the one-row-block kernel, then the down
+            // projection of several row blocks
+            const MlpDmaPlan qg = mlp_dma_gate_plan(rows2, d, npre * d, I, true),
+                             qs = mlp_dma_gate_plan(rows2, d, npre * d, I, false);
+            mp = mp > qg.part_floats() ? mp : qg.part_floats();
+            mp = mp > qs.part_floats() ? mp : qs.part_floats();
+            const size_t qc = (size_t)qg.items + pd.counter_ints();
+            nc = nc > qc ? nc : qc;
         }
         w.ncounters = (int)nc;
     }

@@ -82,7 +82,7 @@ int main() {
     long long nplans = 0, nitems = 0;
     const int ds[] = {64, 192, 640, 1024, 1088, 2048, 2560, 4096, 5120, 8192, 16384};
     const int Is[] = {64, 256, 1088, 1536, 3072, 4096, 6144, 9728, 12288, 28672};
-    const int rowsv[] = {1, 16, 31, 32, 33, 61, 64, 65, 100, 121, 128};
+    const int rowsv[] = {1, 16, 31, 32, 33, 61, 64, 65, 100, 121, 128, 129, 200, 241, 256};
     for (int d : ds)
         for (int I : Is)
             for (int rows : rowsv)

@@ -7,8 +7,10 @@ MLP without an up projection) on every launch path:
   items cut between workgroups and several whole items per workgroup; the
   inputs normalised by whole 16-byte pieces, or element by element when the
   embedding or a gain is not 16-byte aligned;
-* several row blocks, or widths that are not a multiple of 64: the
-  register-staged products;
+* 129-256 rows: the input projections on the LDS-DMA kernel with eight
+  activation tiles, the down projection register-staged;
+* more rows, or widths that are not a multiple of 64: the register-staged
+  products;
 * fp32.
 
 h' is compared element by element with ``oracle.ar_approximator``: fp32
@@ -47,11 +49,15 @@ CASES = [
     (W("mlp-dma-wide-silu", 1, 64, 1500, 6, 5, 16, 8192, "bf16", 1.0, 65, 75, "", "silu"), 0.05),
     # 32 drafter states, the most one activation tile holds
     (W("mlp-dma-32-states", 4, 128, 1200, 8, 3, 12, 128, "bf16", 1.0, 66, 76), 0.1),
+    # eight activation tiles for the input projections (241 rows; 171 rows of three sequences)
+    (W("mlp-dma-nte8", 1, 256, 3000, 16, 16, 24, 256, "bf16", 1.0, 60, 70), 0.08),
+    (W("mlp-dma-nte8-silu", 1, 256, 3000, 16, 16, 24, 256, "bf16", 1.0, 60, 70, "", "silu"), 0.08),
+    (W("mlp-dma-nte8-b3", 3, 128, 2048, 8, 8, 20, 128, "bf16", 1.0, 68, 78), 0.1),
     # register-staged products: a width that is not a multiple of 64; more rows than one block
     (W("mlp-reg-d96", 2, 96, 1000, 5, 3, 12, 96, "bf16", 1.0, 67, 77), 0.15),
     (W("mlp-reg-d96-silu", 2, 96, 1000, 5, 3, 12, 96, "bf16", 1.0, 67, 77, "", "silu"), 0.15),
-    (W("mlp-reg-rows", 3, 128, 2048, 8, 8, 20, 128, "bf16", 1.0, 68, 78), 0.1),
-    (W("mlp-reg-rows-silu", 3, 128, 2048, 8, 8, 20, 128, "bf16", 1.0, 68, 78, "", "silu"), 0.1),
+    (W("mlp-reg-rows", 5, 128, 2048, 8, 8, 20, 128, "bf16", 1.0, 68, 78), 0.1),
+    (W("mlp-reg-rows-silu", 5, 128, 2048, 8, 8, 20, 128, "bf16", 1.0, 68, 78, "", "silu"), 0.1),
     (W("mlp-f32-silu", 2, 96, 1000, 5, 3, 12, 64, "f32", 1.0, 69, 79, "", "silu"), 0.15),
 ]
 
