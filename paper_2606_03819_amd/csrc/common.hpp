@@ -52,6 +52,11 @@ __device__ __forceinline__ float key_f32(uint32_t k) {
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
     return va > vb || (va == vb && ia < ib);
 }
+// The same order with the three comparisons combined as lane masks, so that
+// a wave evaluates it without branches.
+__device__ __forceinline__ bool better_masks(float va, int ia, float vb, int ib) {
+    return (va > vb) | ((va == vb) & (ia < ib));
+}
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
@@ -75,13 +80,65 @@ __device__ __forceinline__ f32x16 mfma_32x32x16_bf16(const u32x4& a, const u32x4
 // (the column is lane % 32).
 __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
 
+// The value that lane (lane ^ J) of this wave holds, J a power of two below
+// 64, without a trip through the LDS crossbar: DPP quad permutes (J = 1, 2),
+// rotations within a 16-lane row (J = 4, 8), and the row and half-wave swaps
+// of gfx950 (J = 16, 32).  Every lane must be active.
+template <int J>
+__device__ __forceinline__ int lane_xor(int v) {
+    static_assert(J == 1 || J == 2 || J == 4 || J == 8 || J == 16 || J == 32, "xor distance");
+    if constexpr (J == 1) {
+        return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+    } else if constexpr (J == 2) {
+        return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+    } else if constexpr (J == 4) {
+        const int up = __builtin_amdgcn_mov_dpp(v, 0x12C, 0xF, 0xF, false);   // row_ror:12, lane + 4
+        const int dn = __builtin_amdgcn_mov_dpp(v, 0x124, 0xF, 0xF, false);   // row_ror:4, lane - 4
+        return (threadIdx.x & 4) ? dn : up;
+    } else if constexpr (J == 8) {
+        return __builtin_amdgcn_mov_dpp(v, 0x128, 0xF, 0xF, false);   // row_ror:8
+    } else if constexpr (J == 16) {
+        // odd rows of the first copy trade places with even rows of the second
+        const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (threadIdx.x & 16) ? (int)p[0] : (int)p[1];
+    } else {
+        // the upper half of the first copy trades places with the lower half of the second
+        const auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return (threadIdx.x & 32) ? (int)p[0] : (int)p[1];
+    }
+}
+template <int J>
+__device__ __forceinline__ float lane_xor(float v) {
+    return __int_as_float(lane_xor<J>(__float_as_int(v)));
+}
+// lane_xor with a distance known once the caller's loops are unrolled
+template <class T>
+__device__ __forceinline__ T lane_xor_n(T v, int j) {
+    switch (j) {
+        case 1: return lane_xor<1>(v);
+        case 2: return lane_xor<2>(v);
+        case 4: return lane_xor<4>(v);
+        case 8: return lane_xor<8>(v);
+        case 16: return lane_xor<16>(v);
+        default: return lane_xor<32>(v);
+    }
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
+    v = fmaxf(v, lane_xor<32>(v));
+    v = fmaxf(v, lane_xor<16>(v));
+    v = fmaxf(v, lane_xor<8>(v));
+    v = fmaxf(v, lane_xor<4>(v));
+    v = fmaxf(v, lane_xor<2>(v));
+    return fmaxf(v, lane_xor<1>(v));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    v += lane_xor<32>(v);
+    v += lane_xor<16>(v);
+    v += lane_xor<8>(v);
+    v += lane_xor<4>(v);
+    v += lane_xor<2>(v);
+    return v + lane_xor<1>(v);
 }
 
 }  // namespace tf

@@ -482,39 +482,29 @@ __device__ __forceinline__ float dot_row(const float* a, const float* b, int d) 
     return acc;
 }
 
-__device__ __forceinline__ float block_max(float v, float* red) {
-    v = wave_max(v);
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-    __syncthreads();
-    return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-}
-__device__ __forceinline__ float block_sum(float v, float* red) {
-    v = wave_sum(v);
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-    __syncthreads();
-    return (red[0] + red[1]) + (red[2] + red[3]);
-}
-
 // Descending bitonic sort of one value per lane across a wave.
 __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
+#pragma unroll
     for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
-            const float o = __shfl_xor(v, j);
+            const float o = lane_xor_n(v, j);
             const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
             v = keep_max ? fmaxf(v, o) : fminf(v, o);
         }
     return v;
 }
 
-// The best 64 of two descending wave lists, descending: the larger of a[l]
-// and b[63 - l] per lane form a bitonic sequence, and half-cleaners sort it.
-__device__ __forceinline__ float wave_merge_desc(float a, float b, int lane) {
-    float v = fmaxf(a, __shfl(b, 63 - lane));
+// The best 64 of two wave lists sorted in opposite directions, sorted
+// descending (DESC) or ascending: the larger of a[l] and b[l] per lane form a
+// bitonic sequence holding them, and half-cleaners sort it.
+template <bool DESC>
+__device__ __forceinline__ float wave_merge(float a, float b, int lane) {
+    float v = fmaxf(a, b);
+#pragma unroll
     for (int j = 32; j > 0; j >>= 1) {
-        const float o = __shfl_xor(v, j);
-        v = (lane & j) == 0 ? fmaxf(v, o) : fminf(v, o);
+        const float o = lane_xor_n(v, j);
+        v = ((lane & j) == 0) == DESC ? fmaxf(v, o) : fminf(v, o);
     }
     return v;
 }
@@ -577,15 +567,17 @@ __device__ unsigned kth_largest_ord(const float* vals, int n, int K, int* hist, 
 }
 
 // (value, id) pairs of a wave sorted in the (value desc, id asc) order, lane
-// 0 first: a bitonic network over __shfl_xor (ids are distinct, so the
-// order is total; padding pairs are equal and stay put).
+// 0 first: a bitonic network (ids are distinct, so the order is total;
+// padding pairs are equal and stay put).
 __device__ __forceinline__ void wave_sort_pairs(float& v, int& i, int lane) {
+#pragma unroll
     for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
-            const float ov = __shfl_xor(v, j);
-            const int oi = __shfl_xor(i, j);
+            const float ov = lane_xor_n(v, j);
+            const int oi = lane_xor_n(i, j);
             const bool keep_better = ((lane & j) == 0) == ((lane & k) == 0);
-            const bool ob = better(ov, oi, v, i);
+            const bool ob = better_masks(ov, oi, v, i);
             if (keep_better == ob) {
                 v = ov;
                 i = oi;
@@ -593,21 +585,21 @@ __device__ __forceinline__ void wave_sort_pairs(float& v, int& i, int lane) {
         }
 }
 
-// The best 64 of two sorted wave lists (a, b), sorted: the better of a[l] and
-// b[63 - l] per lane is a bitonic sequence holding them, and half-cleaners
-// sort it.
+// The best 64 of two pair lists sorted in opposite orders, in the (value
+// desc, id asc) order (DESC) or its reverse: the better of a[l] and b[l] per
+// lane form a bitonic sequence holding them, and half-cleaners sort it.
+template <bool DESC>
 __device__ __forceinline__ void wave_merge_pairs(float& v, int& i, float bv, int bi, int lane) {
-    const float rv = __shfl(bv, 63 - lane);
-    const int ri = __shfl(bi, 63 - lane);
-    if (better(rv, ri, v, i)) {
-        v = rv;
-        i = ri;
+    if (better_masks(bv, bi, v, i)) {
+        v = bv;
+        i = bi;
     }
+#pragma unroll
     for (int j = 32; j > 0; j >>= 1) {
-        const float ov = __shfl_xor(v, j);
-        const int oi = __shfl_xor(i, j);
-        const bool keep_better = (lane & j) == 0;
-        const bool ob = better(ov, oi, v, i);
+        const float ov = lane_xor_n(v, j);
+        const int oi = lane_xor_n(i, j);
+        const bool keep_better = ((lane & j) == 0) == DESC;
+        const bool ob = better_masks(ov, oi, v, i);
         if (keep_better == ob) {
             v = ov;
             i = oi;
@@ -633,17 +625,21 @@ static_assert(kMaxSplitsLong * kKeepLong <= kMergeCap, "long-list slices fit the
 //  4. a slice whose bound (everything it dropped is <= bound) reaches the k-th
 //     value is re-evaluated exactly from memory, so the result is the exact
 //     top-k of the row for any data, ties included.
-template <class T, int KEEP>
+// SPT: slices per thread (nsplit <= 256 * SPT), so that a launch with few
+// slices keeps no idle slice slots in its registers.
+template <class T, int KEEP, int SPT>
 __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     constexpr int PS = part_stride(KEEP);
-    __shared__ float red[4];
+    constexpr int NQ = PS / 4;   // 16-byte words of one partial
+    static_assert(PS % 4 == 0, "partials are whole 16-byte words");
+    __shared__ float s_max[4], s_sum[4];
     __shared__ float s_bound[4];
     __shared__ float s_heads[256];
     __shared__ int s_hist[256];
     __shared__ int s_sel[2];
     __shared__ int s_count, s_nflag, s_ncand;
-    __shared__ float cand_v[kMergeCap];
-    __shared__ int cand_i[kMergeCap];
+    __shared__ float cand_v[kMergeCap + 1];   // the last slot takes discarded stores
+    __shared__ int cand_i[kMergeCap + 1];
     __shared__ int s_flag[kMaxSplits];
     __shared__ float s_colv[512];   // logits of a re-evaluated group of 16 tiles (bf16)
 
@@ -652,71 +648,92 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     const int K = a.K;
     const float* P = a.part + (size_t)row * a.nsplit * PS;
 
-    // every slice's max, sum, bound, count and best logit, read once (the
-    // slices of a thread are tid, tid + 256, ...)
-    constexpr int SPT = kMaxSplits / 256;
-    f32x4 q[SPT];
-    float v0[SPT];
+    // every slice's whole partial (max, sum, bound, count, values, ids), read
+    // in one batch (the slices of a thread are tid, tid + 256, ...)
+    static_assert(256 * SPT <= (KEEP == kKeep ? kMaxSplits : kMaxSplitsLong), "slices per thread");
+    f32x4 rec[SPT][NQ];
 #pragma unroll
     for (int j = 0; j < SPT; ++j) {
         const int s = tid + 256 * j;
         if (s < a.nsplit) {
-            q[j] = *reinterpret_cast<const f32x4*>(P + s * PS);
-            v0[j] = P[s * PS + 4];
+#pragma unroll
+            for (int w = 0; w < NQ; ++w) rec[j][w] = *reinterpret_cast<const f32x4*>(P + s * PS + 4 * w);
         } else {
-            q[j] = f32x4{neg_inf(), 0.f, neg_inf(), 0.f};   // count 0
-            v0[j] = neg_inf();
+            rec[j][0] = f32x4{neg_inf(), 0.f, neg_inf(), 0.f};   // count 0
+#pragma unroll
+            for (int w = 1; w < NQ; ++w) rec[j][w] = f32x4{neg_inf(), neg_inf(), neg_inf(), neg_inf()};
         }
     }
-    float M = neg_inf();
-#pragma unroll
-    for (int j = 0; j < SPT; ++j) M = fmaxf(M, q[j][0]);
-    M = block_max(M, red);
-    float S = 0.f;
-    float head = neg_inf();
-#pragma unroll
-    for (int j = 0; j < SPT; ++j) {
-        const float ms = q[j][0];
-        if (ms != neg_inf()) S += q[j][1] * exp2f((ms - M) * a.sl2);
-        if (__float_as_int(q[j][3]) > 0) head = fmaxf(head, v0[j]);
-    }
-    S = block_sum(S, red);
-    const float logS = logf(S);
-
-    // lower bound on the k-th best value: the k-th best of the 256 thread
-    // heads (each wave sorts its 64, wave 0 merges the four sorted lists)
-    const float sorted = wave_sort_desc(head, lane);
-    s_heads[tid] = sorted;
+    auto field = [&](int j, int f) { return rec[j][f >> 2][f & 3]; };   // f a constant after unrolling
     if (tid == 0) {
         s_count = 0;
         s_nflag = 0;
     }
+    float M = neg_inf(), head = neg_inf();
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        M = fmaxf(M, field(j, 0));
+        if (__float_as_int(field(j, 3)) > 0) head = fmaxf(head, field(j, 4));
+    }
+    // lower bound on the k-th best value: the k-th best of the 256 thread
+    // heads (each wave sorts its 64, wave 0 merges the four sorted lists)
+    const float sorted = wave_sort_desc(head, lane);
+    s_heads[tid] = sorted;
+    M = wave_max(M);
+    if (lane == 0) s_max[wave] = M;
     __syncthreads();
+    M = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
+    float S = 0.f;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const float ms = field(j, 0);
+        if (ms != neg_inf()) S += field(j, 1) * exp2f((ms - M) * a.sl2);
+    }
+    S = wave_sum(S);
+    if (lane == 0) s_sum[wave] = S;
     if (wave == 0) {
-        float v = sorted;
-        v = wave_merge_desc(v, s_heads[64 + lane], lane);
-        const float v23 = wave_merge_desc(s_heads[128 + lane], s_heads[192 + lane], lane);
-        v = wave_merge_desc(v, v23, lane);
-        const float kth = __shfl(v, (K <= 64 ? K : 64) - 1);
+        // lists 0 and 1 into one descending list, 2 and 3 into an ascending
+        // one (each second list read back to front), then those two
+        float v = wave_merge<true>(sorted, s_heads[64 + 63 - lane], lane);
+        const float v23 = wave_merge<false>(s_heads[128 + lane], s_heads[192 + 63 - lane], lane);
+        v = wave_merge<true>(v, v23, lane);
+        const float kth = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), (K <= 64 ? K : 64) - 1));
         if (lane == 0) s_bound[0] = K <= 64 ? kth : neg_inf();
     }
     __syncthreads();
+    S = (s_sum[0] + s_sum[1]) + (s_sum[2] + s_sum[3]);
+    const float logS = logf(S);
     const float t0 = s_bound[0];
 
+    // every entry >= t0 to LDS (lists are sorted: an entry qualifies only if
+    // the ones before it do), one slot reservation per thread; an entry past
+    // its slice's count (whose slot may hold stale words) reads as NaN, which
+    // never qualifies, and the stores of the entries that do not qualify go
+    // to a dump slot, so the pass runs without branches
+    int nq[SPT], ntot = 0;
 #pragma unroll
     for (int j = 0; j < SPT; ++j) {
-        const int n = __float_as_int(q[j][3]);
-        if (n > 0 && v0[j] >= t0) {   // lists are sorted: the rest only if the best qualifies
-            const float* ps = P + (tid + 256 * j) * PS;
-            for (int e = 0; e < n; ++e) {
-                const float v = e == 0 ? v0[j] : ps[4 + e];
-                if (!(v >= t0)) break;
-                const int pos = atomicAdd(&s_count, 1);
-                cand_v[pos] = v;
-                cand_i[pos] = __float_as_int(ps[4 + KEEP + e]);
-            }
+        const int n = __float_as_int(field(j, 3));
+        int m = 0;
+#pragma unroll
+        for (int e = 0; e < KEEP; ++e) {
+            const float v = e < n ? field(j, 4 + e) : __builtin_nanf("");
+            m += v >= t0 ? 1 : 0;
         }
+        nq[j] = m;
+        ntot += m;
     }
+    int pos = ntot > 0 ? atomicAdd(&s_count, ntot) : 0;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j)
+#pragma unroll
+        for (int e = 0; e < KEEP; ++e) {
+            const bool q = e < nq[j];
+            const int dst = q ? pos : kMergeCap;
+            cand_v[dst] = field(j, 4 + e);
+            cand_i[dst] = __float_as_int(field(j, 4 + KEEP + e));
+            pos += q ? 1 : 0;
+        }
     __syncthreads();
     int c = s_count;
     if ((K > 64 || c > 256) && c > 2 * K) {
@@ -758,17 +775,17 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
         __syncthreads();
         if (wave == 0) {
             // a wave whose 64 slots all lie past c holds padding only, which
-            // no merge takes over a candidate: merge only the waves in use
-            if (c > 64) {
-                float v1 = cand_v[64 + lane];
-                int i1 = cand_i[64 + lane];
-                if (c > 128) {
-                    float v2 = cand_v[128 + lane];
-                    int i2 = cand_i[128 + lane];
-                    if (c > 192) wave_merge_pairs(v2, i2, cand_v[192 + lane], cand_i[192 + lane], lane);
-                    wave_merge_pairs(v1, i1, v2, i2, lane);
-                }
-                wave_merge_pairs(v, i, v1, i1, lane);
+            // no merge takes over a candidate: merge only the waves in use.
+            // Lists 0 and 1 into one sorted list, 2 and 3 into a reversed
+            // one (each second list read back to front), then those two.
+            if (c > 128) {
+                float v2 = cand_v[128 + lane];
+                int i2 = cand_i[128 + lane];
+                wave_merge_pairs<false>(v2, i2, cand_v[192 + 63 - lane], cand_i[192 + 63 - lane], lane);
+                wave_merge_pairs<true>(v, i, cand_v[64 + 63 - lane], cand_i[64 + 63 - lane], lane);
+                wave_merge_pairs<true>(v, i, v2, i2, lane);
+            } else if (c > 64) {
+                wave_merge_pairs<true>(v, i, cand_v[64 + 63 - lane], cand_i[64 + 63 - lane], lane);
             }
             cand_v[lane] = v;
             cand_i[lane] = i;
@@ -809,7 +826,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     const float tval = cnt == K ? sel_v[K - 1] : neg_inf();
 #pragma unroll
     for (int j = 0; j < SPT; ++j) {
-        const float U = q[j][2];
+        const float U = field(j, 2);
         if (U != neg_inf() && U >= tval) s_flag[atomicAdd(&s_nflag, 1)] = tid + 256 * j;
     }
     __syncthreads();
@@ -990,12 +1007,22 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
     if (e != hipSuccess) return e;
     if (ev_end != nullptr && hipEventRecord(ev_end, stream) != hipSuccess) return hipErrorInvalidHandle;
     MergeArgs ma{part, p.nsplit(), p.map, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
-    if (bf16 && longl)
-        hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeepLong>), dim3(rows), dim3(256), 0, stream, ma);
-    else if (bf16)
-        hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep>), dim3(rows), dim3(256), 0, stream, ma);
-    else
-        hipLaunchKernelGGL((merge_topk_kernel<float, kKeep>), dim3(rows), dim3(256), 0, stream, ma);
+    const bool two = p.nsplit() <= 512;   // two slices per thread, else the most a launch may have
+    if (bf16 && longl) {
+        if (two)
+            hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeepLong, 2>), dim3(rows), dim3(256), 0, stream, ma);
+        else
+            hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeepLong, kMaxSplitsLong / 256>), dim3(rows), dim3(256),
+                               0, stream, ma);
+    } else if (bf16) {
+        if (two)
+            hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep, 2>), dim3(rows), dim3(256), 0, stream, ma);
+        else
+            hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep, kMaxSplits / 256>), dim3(rows), dim3(256), 0,
+                               stream, ma);
+    } else {
+        hipLaunchKernelGGL((merge_topk_kernel<float, kKeep, kMaxSplits / 256>), dim3(rows), dim3(256), 0, stream, ma);
+    }
     return hipGetLastError();
 }
 
