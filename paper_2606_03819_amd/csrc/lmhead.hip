@@ -28,7 +28,7 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
     if (diag != nullptr && blockIdx.x == 0 && threadIdx.x == 0) diag[0] = 0;
     WRowsPlain ws{w, V, sh.K};
     XRowsPlain xs{x, ldx};
-    E epi{part, sl2};
+    E epi{part, V, sl2};
     const int L = xcd_logical_id(blockIdx.x, gridDim.x);
     const int rb = L % sh.nrb;
     const int g = L / sh.nrb;
@@ -39,15 +39,13 @@ __global__ __launch_bounds__(64 * NW, 1) void lmhead_bf16_kernel(const uint16_t*
         seg.g = L;
         seg.item = seg.chunk = g * map.rmax + r;
         seg.rb = rb;
-        slice_rows(map, seg.chunk, seg.v0, seg.v1);   // whole tiles (the plans give this kernel 32-row units)
-        seg.t0 = seg.v0 / 32;
-        seg.t1 = (seg.v1 + 31) / 32;
+        slice_tiles(map, seg.chunk, seg.t0, seg.t1);
         seg.kc0 = 0;
         seg.kc1 = sh.nk;
         seg.row0 = rb * Tr::TR;
         seg.gfirst = L;
         seg.npieces = 1;
-        if (seg.v0 == seg.v1) {   // empty slice: a partial the merge skips
+        if (seg.t0 == seg.t1) {   // empty slice: a partial the merge skips
             const int t = threadIdx.x;
             if (t < Tr::TR && seg.row0 + t < sh.R) {
                 float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * part_stride(E::KEEP);
@@ -131,7 +129,7 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
     // wave grid: WA waves along the weight tiles times WB along the activation
     // tiles; the WB waves of one weight column share its tiles' copies
     const int wa = wave % T::WA, wb = wave / T::WA;
-    E epi{part, sl2};
+    E epi{part, V, sl2};
     const int L = xcd_logical_id(blockIdx.x, gridDim.x);
     const int rb = L % sh.nrb;
     const int g = L / sh.nrb;
@@ -147,13 +145,13 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
         seg.g = L;
         seg.item = seg.chunk = g * map.rmax + r;
         seg.rb = rb;
-        slice_rows(map, seg.chunk, seg.v0, seg.v1);
+        slice_tiles(map, seg.chunk, seg.t0, seg.t1);
         seg.kc0 = 0;
         seg.kc1 = sh.nk;
         seg.row0 = rb * 32 * NT;
         seg.gfirst = L;
         seg.npieces = 1;
-        if (seg.v0 == seg.v1) {   // empty slice: a partial the merge skips
+        if (seg.t0 == seg.t1) {   // empty slice: a partial the merge skips
             const int t = threadIdx.x;
             if (t < 32 * NT && seg.row0 + t < sh.R) {
                 float* o = part + ((size_t)(seg.row0 + t) * se.nchunks + seg.chunk) * part_stride(E::KEEP);
@@ -166,21 +164,21 @@ __global__ __launch_bounds__(64 * NW, MINB) void lmhead_dma_kernel(const uint16_
         }
         // global sources of this lane's DMA pieces (k offset added per step):
         // the piece landing at physical slot lphys of row `row` is logical
-        // slot lphys ^ swizzle(row).  The slice's tiles start at its first
-        // row; rows past the slice (in its last tile, or in tiles wholly past
-        // it) repeat its last row, so every load stays inside the slice; the
-        // epilogue masks those products.  (They are computed anyway: a
-        // per-tile branch in the k loop costs more in MFMA-bound launches,
-        // whose slices are all full, than the spare products cost in the
-        // memory-bound ones.)
-        const int vt = seg.v0 + 32 * wa * WM;   // first row of this wave's tiles
+        // slot lphys ^ swizzle(row).  Tiles past the slice repeat its last
+        // tile and vocabulary rows past V repeat row V-1, so every load stays
+        // inside w; the epilogue masks those products.  (They are computed
+        // anyway: a per-tile branch in the k loop costs more in MFMA-bound
+        // launches, whose slices are all full, than the spare products cost
+        // in the memory-bound ones.)
+        const int tw = seg.t0 + wa * WM;
         const uint16_t* wsrc[WM][T::WPI];
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt)
 #pragma unroll
             for (int hi = 0; hi < T::WPI; ++hi) {
                 const int row = T::RPI * (wb * T::WPI + hi) + lrow;
-                const int v = min(vt + 32 * mt + row, seg.v1 - 1);
+                const int tile = min(tw + mt, seg.t1 - 1);
+                const int v = min(tile * 32 + row, V - 1);
                 wsrc[mt][hi] = w + (size_t)v * sh.K + (T::slot(row, lphys) - row * T::ROWB) / 2;
             }
         constexpr int XPW = (T::XINSTR + NW - 1) / NW;   // activation instructions of this wave (at most)
@@ -297,10 +295,9 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
     const int split = L / sh.nrb;   // one tile range of at most 8 tiles, one slice (rmax = 1)
     const int rb = L - split * sh.nrb;
     const int row0 = rb * 32;
-    int v0, v1;
-    slice_rows(map, split, v0, v1);   // whole tiles (the plans give this kernel 32-row units)
-    const int t0 = v0 / 32, t1 = (v1 + 31) / 32;
-    const int vend = v1;
+    int t0, t1;
+    slice_tiles(map, split, t0, t1);
+    const int vend = min(V, t1 * 32);
     const int srow = tid >> 3, sub = tid & 7;
 
     float m = neg_inf(), s = 0.f;
@@ -410,25 +407,25 @@ struct MergeArgs {
     int* diag;
 };
 
-// Exact logits of one activation row with the 32 vocabulary rows from each of
-// NTL row bases rb (rows from vend on repeat row vend - 1), computed as the
+// Exact logits of one activation row with the 32 vocabulary rows of each of
+// NTL tiles (ids 32t .. 32t+31; ids past V repeat row V-1), computed as the
 // bf16 LM-head kernels compute them: one chain per logit, an MFMA 32x32x16
 // per 16-wide k block in increasing k from zero, the weights as the A
 // operand and the activation as B, so that every value is bit for bit the
 // one the fast path saw (exact ties order the same way on both paths).  The
 // row fills all 32 B columns, so every lane holds the logits of ids
-// rb + acc_row(j, lane) in acc[j].  Loads go in batches of P k blocks, two
+// 32t + acc_row(j, lane) in acc[j].  Loads go in batches of P k blocks, two
 // batches in flight: one lands while the other feeds the MFMAs (a batch
 // reaching past d re-reads the last block and is not used).
 template <int NTL, int P>
-__device__ __forceinline__ void tile_logits_mfma(const uint16_t* xr, const uint16_t* w, int d, int vend,
-                                                 const int (&rb)[NTL], f32x16 (&acc)[NTL]) {
+__device__ __forceinline__ void tile_logits_mfma(const uint16_t* xr, const uint16_t* w, int d, int V,
+                                                 const int (&t)[NTL], f32x16 (&acc)[NTL]) {
     const int lane = threadIdx.x & 63;
     const int h8 = 8 * (lane >> 5);
     const uint16_t* wp[NTL];
 #pragma unroll
     for (int i = 0; i < NTL; ++i) {
-        wp[i] = w + (size_t)min(rb[i] + (lane & 31), vend - 1) * d + h8;
+        wp[i] = w + (size_t)min(t[i] * 32 + (lane & 31), V - 1) * d + h8;
 #pragma unroll
         for (int j = 0; j < 16; ++j) acc[i][j] = 0.f;
     }
@@ -460,19 +457,18 @@ __device__ __forceinline__ void tile_logits_mfma(const uint16_t* xr, const uint1
     }
 }
 
-// Logits of rows [vg, vend) (at most 16 tiles of 32 rows from vg) into
-// colv[v - vg]: wave w takes tiles w + 4i, i < NTL; a slot past the last
-// tile repeats it and is not read.
+// Logits of tiles [tg, tend) (at most 16) into colv[(t - tg) * 32 + m]: wave
+// w takes tiles tg + w + 4i, i < NTL; a slot past tend repeats the last tile
+// and is not read.
 template <int NTL>
-__device__ __forceinline__ void slice_logits(const uint16_t* xr, const uint16_t* w, int d, int vg, int vend,
+__device__ __forceinline__ void slice_logits(const uint16_t* xr, const uint16_t* w, int d, int V, int tg, int tend,
                                              float* colv) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int ntile = (vend - vg + 31) / 32;
-    int rb[NTL];
+    int tl[NTL];
 #pragma unroll
-    for (int i = 0; i < NTL; ++i) rb[i] = vg + 32 * min(wave + 4 * i, ntile - 1);
+    for (int i = 0; i < NTL; ++i) tl[i] = min(tg + wave + 4 * i, tend - 1);
     f32x16 lg[NTL];
-    tile_logits_mfma<NTL, (NTL >= 4 ? 2 : 3)>(xr, w, d, vend, rb, lg);
+    tile_logits_mfma<NTL, (NTL >= 4 ? 2 : 3)>(xr, w, d, V, tl, lg);
     if ((lane & 31) == 0)
 #pragma unroll
         for (int i = 0; i < NTL; ++i)
@@ -844,22 +840,22 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
         const T* wb = reinterpret_cast<const T*>(a.w);
         for (int f = 0; f < nflag; ++f) {
             const int s = s_flag[f];
-            int vs0, vs1;
-            slice_rows(a.map, s, vs0, vs1);
-            // groups of 16 tiles from the slice's first row (every slice the
-            // plans make is one group)
-            for (int v0 = vs0; v0 < vs1; v0 += 512) {
-                const int v1 = min(vs1, v0 + 512);
+            int t0s, t1s;
+            slice_tiles(a.map, s, t0s, t1s);
+            // groups of 16 tiles (every slice the plans make is one group)
+            for (int tg = t0s; tg < t1s; tg += 16) {
+                const int tend = min(t1s, tg + 16);
+                const int v0 = tg * 32, v1 = min(a.V, tend * 32);
                 if constexpr (sizeof(T) == 2) {
-                    const int ntl = ((v1 - v0 + 31) / 32 + 3) / 4;   // tiles per wave
+                    const int ntl = (tend - tg + 3) / 4;   // tiles per wave
                     if (ntl == 1)
-                        slice_logits<1>(xr, wb, a.d, v0, v1, s_colv);
+                        slice_logits<1>(xr, wb, a.d, a.V, tg, tend, s_colv);
                     else if (ntl == 2)
-                        slice_logits<2>(xr, wb, a.d, v0, v1, s_colv);
+                        slice_logits<2>(xr, wb, a.d, a.V, tg, tend, s_colv);
                     else if (ntl == 3)
-                        slice_logits<3>(xr, wb, a.d, v0, v1, s_colv);
+                        slice_logits<3>(xr, wb, a.d, a.V, tg, tend, s_colv);
                     else
-                        slice_logits<4>(xr, wb, a.d, v0, v1, s_colv);
+                        slice_logits<4>(xr, wb, a.d, a.V, tg, tend, s_colv);
                 }
                 for (int vb = v0; vb < v1; vb += 256) {
                     if (tid == 0) s_ncand = 0;

@@ -238,14 +238,7 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
         // all, the row blocks of a tile range on consecutive ones
         const int gw = TF_LM_WORKGROUPS / p.nrb;
         const int G = p.nrb == 1 || p.grid ? (p.ntiles < gw ? p.ntiles : gw) : cdiv(p.ntiles, p.chunk);
-        // the grid kernel on one row block cuts the vocabulary by rows, so
-        // that every workgroup streams the same bytes (the launch's time
-        // follows the workgroup with the most rows): 2% faster at 121 rows.
-        // Launches of several row blocks, which lean on their MFMAs, keep
-        // whole tiles (a slice of rows costs a partial tile's products per
-        // round: 5% slower at 241 rows), and so does the 32-row kernel (1%
-        // slower by rows at 16 rows, within the spread of boxes)
-        p.map = p.grid && p.nrb == 1 ? make_slice_map_rows(V, G, p.chunk) : make_slice_map(V, G, p.chunk);
+        p.map = make_slice_map(p.ntiles, G, p.chunk);
         p.wnt = p.nrb == 1;
     } else {
         p.NT = 1;
@@ -253,7 +246,7 @@ inline LmPlan lm_plan(int rows, int V, int d, bool bf16) {
         p.NW = 4;
         p.chunk = 8;
         p.nrb = cdiv(rows, 32);
-        p.map = make_slice_map(V, cdiv(p.ntiles, p.chunk), p.chunk);
+        p.map = make_slice_map(p.ntiles, cdiv(p.ntiles, p.chunk), p.chunk);
         p.wnt = false;
     }
     return p;

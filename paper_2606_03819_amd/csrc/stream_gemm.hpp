@@ -42,7 +42,6 @@ struct Segment {
     int g;         // workgroup (logical id)
     int item, chunk, rb;
     int t0, t1;    // weight tiles [t0, t1)
-    int v0, v1;    // vocabulary rows [v0, v1) of an LM-head slice
     int kc0, kc1;  // 64-wide k-chunks [kc0, kc1)
     int row0;      // first activation row
     int gfirst;    // first workgroup holding a piece of the item
@@ -467,6 +466,7 @@ struct EpiLmHead {
     static constexpr int WA = NW / WB;            // waves along the weight tiles
     static constexpr int NTW = NT / WB;           // activation tiles per wave
     float* part;     // [R, nchunks, part_stride(KEEP)]
+    int V;
     float sl2;       // inv_temperature * log2(e)
     static constexpr bool WIDE = WM * 16 > 64;
     static constexpr int KL = LONG ? (WIDE ? kLaneMfmaWideLong : kLaneMfmaLong) : (WIDE ? kLaneMfmaWide : kLaneMfma);
@@ -477,9 +477,9 @@ struct EpiLmHead {
     static constexpr int RSTRIDE = NC * MERGE_WORDS + 1;
     static constexpr int MERGE_BYTES = 32 * NT * RSTRIDE * 4;
 
-    // One row (accumulator column nt) of this lane: the WM tiles of 32 rows
-    // from row vt, of which those starting before v1 reach into the slice (a
-    // wave-uniform test) and tokens from v1 on are left out.  Each logit becomes a key: its truncated
+    // One row (accumulator column nt) of this lane: the tiles [tw, tw + WM)
+    // of which those before t1 lie in the slice (a wave-uniform test) and
+    // tokens from V on are left out.  Each logit becomes a key: its truncated
     // value (logit_trunc) with the lane-local position p (tokens in
     // increasing id) stored as TAG - p in the cleared bits.  Keys are
     // distinct, and for positive values their order is the (value desc, id
@@ -490,7 +490,7 @@ struct EpiLmHead {
     // from the tags at the end), the exponentials a second pass.  The
     // hardware exp2 flushes results below 2^-126 to zero: the sum starts at
     // the row maximum's term, about 1.
-    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NTW], int nt, int vbase0, int vt, int v1,
+    __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NTW], int nt, int vbase0, int tw, int t1,
                                              float* c) const {
         constexpr int TAG = (1 << kLogitTagBits) - 1;
         static_assert(WM * 16 <= TAG + 1 && 16 > KL, "positions fit the tag bits; one tile fills a list");
@@ -509,17 +509,17 @@ struct EpiLmHead {
             return __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (TAG - (mt * 16 + j)));
         };
         // wave-uniform branches: a tile past the slice is skipped, only a tile
-        // reaching past its end pays for the per-token test
+        // reaching past the vocabulary pays for the per-token test
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt) {
-            if (vt + 32 * mt >= v1) continue;
-            if (vt + 32 * (mt + 1) <= v1) {
+            if (tw + mt >= t1) continue;
+            if ((tw + mt + 1) * 32 <= V) {
 #pragma unroll
                 for (int j = 0; j < 16; ++j) insert(key_of(mt, j));
             } else {
 #pragma unroll
                 for (int j = 0; j < 16; ++j)
-                    insert(vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < v1 ? key_of(mt, j) : neg_inf());
+                    insert(vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V ? key_of(mt, j) : neg_inf());
             }
         }
         const float m = logit_trunc(k[0]);
@@ -528,14 +528,14 @@ struct EpiLmHead {
             const float ms = m * sl2;
 #pragma unroll
             for (int mt = 0; mt < WM; ++mt) {
-                if (vt + 32 * mt >= v1) continue;
-                if (vt + 32 * (mt + 1) <= v1) {
+                if (tw + mt >= t1) continue;
+                if ((tw + mt + 1) * 32 <= V) {
 #pragma unroll
                     for (int j = 0; j < 16; ++j) s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
                 } else {
 #pragma unroll
                     for (int j = 0; j < 16; ++j)
-                        if (vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < v1)
+                        if (vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V)
                             s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
                 }
             }
@@ -561,10 +561,10 @@ struct EpiLmHead {
         const int q = wa * 2 + (lane >> 5);
         // this lane's row of accumulator column 0
         float* crow = cm + (wb * NTW * 32 + (lane & 31)) * RSTRIDE + q * MERGE_WORDS;
-        const int vt = it.v0 + 32 * wa * WM;         // first row of this wave's tiles
-        const int vbase0 = vt + 4 * (lane >> 5);
+        const int tw = it.t0 + wa * WM;              // this wave's first tile
+        const int vbase0 = tw * 32 + 4 * (lane >> 5);
 #pragma unroll
-        for (int nt = 0; nt < NTW; ++nt) lane_row(acc, nt, vbase0, vt, it.v1, crow + nt * 32 * RSTRIDE);
+        for (int nt = 0; nt < NTW; ++nt) lane_row(acc, nt, vbase0, tw, it.t1, crow + nt * 32 * RSTRIDE);
         lds_barrier();
         lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }

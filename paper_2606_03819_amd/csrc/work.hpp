@@ -129,61 +129,41 @@ inline bool cost_split_valid(int items, int nkh, int nke, int wh, int we, int G)
 
 // LM head (many weight tiles): the vocabulary is cut instead.
 //
-// Vocabulary slices of the LM head.  The vocabulary is dealt out in units of
-// `unit` rows (a whole 32-row weight tile, or a single row): the N units are
-// cut into G contiguous ranges of floor(N/G) or ceil(N/G) units (one per
-// workgroup column), and range g is streamed in rounds(g) = ceil(tiles_g /
-// chunk) near-equal rounds of at most `chunk` tiles of 32 rows (tiles_g =
-// the range's rows over 32, rounded up), each a full pass over K.  Slice
-// g*rmax + r is round r of range g and is empty when r >= rounds(g).  Every
-// workgroup thus streams the same number of rows (up to one unit), and no
-// slice needs partial sums from another workgroup.  With single-row units a
-// slice's tiles start at its first row, the last one reaching past the
-// slice; the kernels clamp those rows' loads into the slice and leave their
-// products out.
+// Vocabulary slices of the LM head.  The T weight tiles are cut into G
+// contiguous ranges of floor(T/G) or ceil(T/G) tiles (one per workgroup
+// column); range g is streamed in rounds(g) = ceil(n_g / chunk) near-equal
+// rounds of at most `chunk` tiles, each a full pass over K.  Slice g*rmax + r
+// is round r of range g and is empty when r >= rounds(g).  Every workgroup
+// thus streams the same number of weight tiles (up to one), and no slice
+// needs partial sums from another workgroup.
 struct SliceMap {
-    int N;       // units
-    int unit;    // vocabulary rows per unit (32 or 1)
-    int V;       // vocabulary rows
-    int G;       // ranges
+    int T;       // weight tiles
+    int G;       // tile ranges
     int chunk;   // most tiles per round
     int rmax;    // slices per range
 };
 
 __host__ __device__ inline int slice_range_begin(const SliceMap& m, int g) {
-    return (int)((long long)g * m.N / m.G);
+    return (int)((long long)g * m.T / m.G);
 }
 
-// vocabulary rows [v0, v1) of slice s (v0 == v1 for an empty slice)
-__host__ __device__ inline void slice_rows(const SliceMap& m, int s, int& v0, int& v1) {
+// tiles [t0, t1) of slice s (t0 == t1 for an empty slice)
+__host__ __device__ inline void slice_tiles(const SliceMap& m, int s, int& t0, int& t1) {
     const int g = s / m.rmax, r = s - g * m.rmax;
     const int a = slice_range_begin(m, g);
     const int n = slice_range_begin(m, g + 1) - a;
-    const int tiles = (int)(((long long)n * m.unit + 31) / 32);
-    const int rounds = (tiles + m.chunk - 1) / m.chunk;
+    const int rounds = (n + m.chunk - 1) / m.chunk;
     if (r >= rounds) {
-        v0 = v1 = a * m.unit;
+        t0 = t1 = a;
         return;
     }
-    const int u0 = a + (int)((long long)r * n / rounds);
-    const int u1 = a + (int)((long long)(r + 1) * n / rounds);
-    v0 = u0 * m.unit;
-    v1 = u1 * m.unit < m.V ? u1 * m.unit : m.V;
+    t0 = a + (int)((long long)r * n / rounds);
+    t1 = a + (int)((long long)(r + 1) * n / rounds);
 }
 
-// Slices of whole 32-row tiles (the tiles of V rows).
-inline SliceMap make_slice_map(int V, int G, int chunk) {
-    const int T = (V + 31) / 32;
+inline SliceMap make_slice_map(int T, int G, int chunk) {
     const int per = (T + G - 1) / G;
-    return SliceMap{T, 32, V, G, chunk, (per + chunk - 1) / chunk};
-}
-
-// Slices of single rows: every range holds the same number of rows (up to
-// one), whatever V / 32 / G leaves over.
-inline SliceMap make_slice_map_rows(int V, int G, int chunk) {
-    const int per = (V + G - 1) / G;
-    const int tiles = (per + 31) / 32;
-    return SliceMap{V, 1, V, G, chunk, (tiles + chunk - 1) / chunk};
+    return SliceMap{T, G, chunk, (per + chunk - 1) / chunk};
 }
 
 }  // namespace tf
