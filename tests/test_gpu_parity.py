@@ -90,13 +90,17 @@ def test_timed_entry_point_matches_and_times_the_lm_head():
     assert ev[0].elapsed_time(ev[1]) > 0.0
 
 
-@pytest.mark.parametrize("d,dtype,B", [(64, "bf16", 24), (1040, "bf16", 24), (272, "f32", 24), (64, "bf16", 80)])
-def test_exact_ties_take_smaller_ids_and_use_the_slow_path(d, dtype, B):
+@pytest.mark.parametrize("d,dtype,B,gamma,k", [(64, "bf16", 24, 3, 4), (1040, "bf16", 24, 3, 4), (272, "f32", 24, 3, 4),
+                                               (64, "bf16", 80, 3, 4), (128, "bf16", 24, 5, 12)])
+def test_exact_ties_take_smaller_ids_and_use_the_slow_path(d, dtype, B, gamma, k):
     """Duplicated LM-head rows give exactly equal logits; the (value desc, id
-    asc) order must hold and the exact slow path must be exercised (d = 1040:
-    the re-evaluation's 512-element pieces end inside a column; B = 80: the
-    80-entry stage-2 lists use the long per-slice lists)."""
-    w = W(f"{dtype}-ties-d{d}-B{B}", 1, d, 2000, 3, 4, B, 32, dtype, 1.0, 14, 140)
+    asc) order must hold and the exact slow path must be exercised in both
+    stages (d = 1040: the re-evaluation's 512-element pieces end inside a
+    column; B = 80: the 80-entry stage-2 lists use the long per-slice lists;
+    gamma = 5, k = 12: 49 conditional rows, one row block of the wave grid,
+    which streams its rounds and k steps last to first, so the
+    re-evaluation replays that order)."""
+    w = W(f"{dtype}-ties-d{d}-B{B}-g{gamma}-k{k}", 1, d, 2000, gamma, k, B, 32, dtype, 1.0, 14, 140)
     cpu = synth.make_inputs(w, "cpu", weight_std=0.1)
     # only five distinct output embeddings: token v uses row v % 5, so every
     # vocabulary slice holds many exactly equal logits
@@ -109,6 +113,7 @@ def test_exact_ties_take_smaller_ids_and_use_the_slow_path(d, dtype, B):
     st1 = oracle.marginal_stage(o_in["h"], o_in["lm_head"], w.k, 1.0)
     assert np.array_equal(idx.cpu().numpy(), st1["topk_idx"])   # ties at the boundary go to smaller ids
     dr.stage2(g["h"], g["root"])
+    assert dr.diagnostics() > 0
     st = _oracle_rows(o_in, w, st1["topk_idx"][0], 0)
     check_topk(dr.cond_idx.cpu().numpy()[0], dr.cond_lp.cpu().numpy()[0], st["logprob"], 2e-2, "ties stage 2")
 
