@@ -416,24 +416,26 @@ __device__ __forceinline__ void lm_merge_contributors(const float* cm, int rstri
     for (int p = 0; p < NC; ++p) S += (cmax[p] == neg_inf()) ? 0.f : csum[p] * exp2f((cmax[p] - M) * sl2);
     float* out = part + ((size_t)grow * nsplit + split) * part_stride(KEEP);
     int cnt = 0;
+    // each pick: the largest value, then the smallest id holding it (an
+    // empty or picked entry holds -inf, and listed logits are finite), by
+    // maxima, minima and selects alone -- no per-entry branch or mask logic
 #pragma unroll
     for (int e = 0; e <= KEEP; ++e) {
         float bv = neg_inf();
-        int bi = -1;
 #pragma unroll
-        for (int j = 0; j < NCAND; ++j) {
-            const bool take = id[j] >= 0 && (bi < 0 || better(v[j], id[j], bv, bi));
-            bv = take ? v[j] : bv;
-            bi = take ? id[j] : bi;
-        }
+        for (int j = 0; j < NCAND; ++j) bv = fmaxf(bv, v[j]);
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int j = 0; j < NCAND; ++j) bi = min(bi, v[j] == bv ? id[j] : 0x7fffffff);
+        const bool any = bv != neg_inf();
         if (e < KEEP) {
             // the e-th entry, or the empty entry once the lists are exhausted
-            out[4 + e] = bi >= 0 ? bv : neg_inf();
-            out[4 + KEEP + e] = __int_as_float(bi);
-            cnt += bi >= 0 ? 1 : 0;
+            out[4 + e] = bv;
+            out[4 + KEEP + e] = __int_as_float(any ? bi : -1);
+            cnt += any ? 1 : 0;
 #pragma unroll
-            for (int j = 0; j < NCAND; ++j) id[j] = (bi >= 0 && id[j] == bi) ? -1 : id[j];
-        } else if (bi >= 0) {
+            for (int j = 0; j < NCAND; ++j) v[j] = id[j] == bi ? neg_inf() : v[j];
+        } else if (any) {
             U = fmaxf(U, bv);   // the best entry left out bounds the slice's other logits
         }
     }
