@@ -387,7 +387,7 @@ __global__ __launch_bounds__(256) void lmhead_f32_kernel(const float* __restrict
         c[3 + kLane + e] = __int_as_float(li[e]);
     }
     __syncthreads();
-    lm_merge_contributors<8, kLane>(cmrg, 8 * W, 32, row0, split, sh.nchunks, sh.R, sl2, part);
+    lm_merge_contributors<8, kLane, kKeep, 8>(cmrg, 8 * W, 32, row0, split, sh.nchunks, sh.R, sl2, part);
 }
 
 // ------------------------------------------------------------------ merge

@@ -377,25 +377,31 @@ struct XRowsConcat {
 // Merge the NC contributor lists of each activation row (written to `cm` as
 // [rows][NC][3 + 2*KL] = max, sum, bound, KL values, KL ids; `bound` is at
 // least every value the contributor saw but did not list) into the row's
-// (row, slice) partial of KEEP entries.  One thread per row.
-template <int NC, int KL, int KEEP = kKeep>
+// (row, slice) partial of KEEP entries.  T consecutive lanes per row, each
+// taking NC / T contributors: a lane picks the KEEP + 1 best of its own
+// entries by (value desc, id asc), then the row's picks are the heads' best,
+// found by maxima and minima across the T lanes (DPP), the winning lane
+// moving to its next entry.  The (KEEP + 1)-th pick bounds every entry a lane
+// left out (that lane still holds an unpicked entry at least as large), so
+// it and the contributors' bounds bound the slice's unlisted logits.
+template <int NC, int KL, int KEEP = kKeep, int T = 1>
 __device__ __forceinline__ void lm_merge_contributors(const float* cm, int rstride, int rows, int row0, int split,
                                                       int nsplit, int R, float sl2, float* part) {
+    static_assert(NC % T == 0 && (T == 1 || T == 2 || T == 4 || T == 8), "lanes per row");
     constexpr int W = 3 + 2 * KL;
-    constexpr int NCAND = NC * KL;
-    const int tid = threadIdx.x;
-    if (tid >= rows) return;
-    const int grow = row0 + tid;
+    constexpr int NCT = NC / T;          // contributors of one lane
+    constexpr int NCAND = NCT * KL;
+    constexpr int NL = KEEP + 1;         // a lane's picks: KEEP to list, one to bound the rest
+    const int r = threadIdx.x / T, t = threadIdx.x % T;
+    if (r >= rows) return;               // whole groups of T lanes leave together
+    const int grow = row0 + r;
     if (grow >= R) return;
-    // every contributor's words at once (one batch of LDS reads), then the
-    // selection in registers: the KEEP best of the lists' entries are the
-    // first KEEP picks of the best remaining entry by (value desc, id asc)
-    // (ids are distinct within a slice, so a pick is removed by its id)
-    const float* c = cm + tid * rstride;
-    float cmax[NC], csum[NC], cbnd[NC], v[NCAND];
+    // this lane's contributors' words at once (one batch of LDS reads)
+    const float* c = cm + r * rstride + t * NCT * W;
+    float cmax[NCT], csum[NCT], cbnd[NCT], v[NCAND];
     int id[NCAND];
 #pragma unroll
-    for (int p = 0; p < NC; ++p) {
+    for (int p = 0; p < NCT; ++p) {
         cmax[p] = c[p * W + 0];
         csum[p] = c[p * W + 1];
         cbnd[p] = c[p * W + 2];
@@ -407,42 +413,87 @@ __device__ __forceinline__ void lm_merge_contributors(const float* cm, int rstri
     }
     float M = neg_inf(), U = neg_inf();
 #pragma unroll
-    for (int p = 0; p < NC; ++p) {
+    for (int p = 0; p < NCT; ++p) {
         M = fmaxf(M, cmax[p]);
         U = fmaxf(U, cbnd[p]);
     }
+#pragma unroll
+    for (int o = 1; o < T; o <<= 1) {
+        M = fmaxf(M, lane_xor_n(M, o));
+        U = fmaxf(U, lane_xor_n(U, o));
+    }
     float S = 0.f;
 #pragma unroll
-    for (int p = 0; p < NC; ++p) S += (cmax[p] == neg_inf()) ? 0.f : csum[p] * exp2f((cmax[p] - M) * sl2);
-    float* out = part + ((size_t)grow * nsplit + split) * part_stride(KEEP);
-    int cnt = 0;
-    // each pick: the largest value, then the smallest id holding it (an
-    // empty or picked entry holds -inf, and listed logits are finite), by
-    // maxima, minima and selects alone -- no per-entry branch or mask logic
+    for (int p = 0; p < NCT; ++p) S += (cmax[p] == neg_inf()) ? 0.f : csum[p] * exp2f((cmax[p] - M) * sl2);
 #pragma unroll
-    for (int e = 0; e <= KEEP; ++e) {
+    for (int o = 1; o < T; o <<= 1) S += lane_xor_n(S, o);
+    // this lane's picks, in order: the largest value, then the smallest id
+    // holding it (an empty or picked entry holds -inf, and listed logits are
+    // finite), by maxima, minima and selects alone
+    float lv[NL];
+    int li[NL];
+#pragma unroll
+    for (int e = 0; e < NL; ++e) {
         float bv = neg_inf();
 #pragma unroll
         for (int j = 0; j < NCAND; ++j) bv = fmaxf(bv, v[j]);
         int bi = 0x7fffffff;
 #pragma unroll
         for (int j = 0; j < NCAND; ++j) bi = min(bi, v[j] == bv ? id[j] : 0x7fffffff);
+        lv[e] = bv;
+        li[e] = bi;
+        if (e + 1 < NL) {
+#pragma unroll
+            for (int j = 0; j < NCAND; ++j) v[j] = id[j] == bi ? neg_inf() : v[j];
+        }
+    }
+    float* out = part + ((size_t)grow * nsplit + split) * part_stride(KEEP);
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < NL; ++e) {
+        float bv = lv[0];
+        int bi = li[0];
+        if constexpr (T > 1) {
+#pragma unroll
+            for (int o = 1; o < T; o <<= 1) bv = fmaxf(bv, lane_xor_n(bv, o));
+            bi = lv[0] == bv ? li[0] : 0x7fffffff;
+#pragma unroll
+            for (int o = 1; o < T; o <<= 1) bi = min(bi, lane_xor_n(bi, o));
+            if (e + 1 < NL) {
+                // the winning lane moves to its next pick (ids are distinct in a slice)
+                const bool mine = lv[0] == bv && li[0] == bi;
+#pragma unroll
+                for (int q = 0; q + 1 < NL; ++q) {
+                    lv[q] = mine ? lv[q + 1] : lv[q];
+                    li[q] = mine ? li[q + 1] : li[q];
+                }
+                lv[NL - 1] = mine ? neg_inf() : lv[NL - 1];
+            }
+        } else if (e + 1 < NL) {
+#pragma unroll
+            for (int q = 0; q + 1 < NL; ++q) {
+                lv[q] = lv[q + 1];
+                li[q] = li[q + 1];
+            }
+        }
         const bool any = bv != neg_inf();
         if (e < KEEP) {
             // the e-th entry, or the empty entry once the lists are exhausted
-            out[4 + e] = bv;
-            out[4 + KEEP + e] = __int_as_float(any ? bi : -1);
+            if (t == 0) {
+                out[4 + e] = bv;
+                out[4 + KEEP + e] = __int_as_float(any ? bi : -1);
+            }
             cnt += any ? 1 : 0;
-#pragma unroll
-            for (int j = 0; j < NCAND; ++j) v[j] = id[j] == bi ? neg_inf() : v[j];
         } else if (any) {
             U = fmaxf(U, bv);   // the best entry left out bounds the slice's other logits
         }
     }
-    out[0] = M;
-    out[1] = S;
-    out[2] = U;
-    out[3] = __int_as_float(cnt);
+    if (t == 0) {
+        out[0] = M;
+        out[1] = S;
+        out[2] = U;
+        out[3] = __int_as_float(cnt);
+    }
 }
 
 // LM head: per lane and row, the maximum, the sum of exponentials, the KL
@@ -478,6 +529,10 @@ struct EpiLmHead {
     // odd row stride: the lanes of a wave (consecutive rows) hit distinct banks
     static constexpr int RSTRIDE = NC * MERGE_WORDS + 1;
     static constexpr int MERGE_BYTES = 32 * NT * RSTRIDE * 4;
+    // lanes per row in the merge: the workgroup's threads over the rows, at
+    // most one contributor each
+    static constexpr int MT_ALL = (64 * NW) / (32 * NT);
+    static constexpr int MT = MT_ALL >= NC ? NC : (MT_ALL >= 1 ? MT_ALL : 1);
 
     // One row (accumulator column nt) of this lane: the tiles [tw, tw + WM)
     // of which those before t1 lie in the slice (a wave-uniform test) and
@@ -568,7 +623,7 @@ struct EpiLmHead {
 #pragma unroll
         for (int nt = 0; nt < NTW; ++nt) lane_row(acc, nt, vbase0, tw, it.t1, crow + nt * 32 * RSTRIDE);
         lds_barrier();
-        lm_merge_contributors<NC, KL, KEEP>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
+        lm_merge_contributors<NC, KL, KEEP, MT>(cm, RSTRIDE, 32 * NT, it.row0, it.chunk, sh.nchunks, sh.R, sl2, part);
     }
 };
 
