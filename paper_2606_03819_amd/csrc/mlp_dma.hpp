@@ -388,12 +388,12 @@ __device__ __forceinline__ void mlp_piece_begin(const MlpDmaArgs& a, int item, i
 // The rest of the piece begun by mlp_piece_begin, streamed through the rings
 // in `dyn`.  On return every copy has landed, the LDS is free, and hc / ec
 // hold this thread's part of the piece's sums, the waves' accumulators added
-// in wave order: hc[i] is element tid + 256 i of [TG][1024] (h phase), ec[i]
-// element tid + 256 i of [TG][NTE][1024] (e phase).
+// in wave order: hc[i] is the 16-byte group 4 tid + 1024 i of [TG][1024] (h
+// phase), ec[i] that of [TG][NTE][1024] (e phase).
 template <int TG, int NTE, bool PAIRED, int SW, int SX>
 __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
                                               MlpSegment<TG, MlpDmaTraits<TG, NTE, PAIRED, SW, SX>::XPW_E>& sg,
-                                              unsigned char* dyn, float (&hc)[4 * TG], float (&ec)[4 * TG * NTE]) {
+                                              unsigned char* dyn, f32x4 (&hc)[TG], f32x4 (&ec)[TG * NTE]) {
     using T = MlpDmaTraits<TG, NTE, PAIRED, SW, SX>;
     constexpr int TW = T::TW, NTW = T::NTW;
     static_assert(SX == 2 || SX == 3, "one or two activation chunks in flight");
@@ -520,27 +520,35 @@ __device__ __forceinline__ void mlp_piece_run(const MlpDmaArgs& a,
             }
     }
     __syncthreads();
-    // element tid + 256 i of each phase
+    // 16-byte group tid + 256 i of each phase
 #pragma unroll
-    for (int i = 0; i < T::HC; ++i) hc[i] = fs[tid + 256 * i];
+    for (int i = 0; i < TG; ++i) hc[i] = *reinterpret_cast<const f32x4*>(fs + 4 * tid + 1024 * i);
 #pragma unroll
-    for (int i = 0; i < T::EC; ++i) ec[i] = fe[tid + 256 * i];
+    for (int i = 0; i < TG * NTE; ++i) ec[i] = *reinterpret_cast<const f32x4*>(fe + 4 * tid + 1024 * i);
     __syncthreads();   // the per-wave sums are read; the LDS is free
 }
 
-// A cut item's piece: store its sums (the phases it covers) in its slot and
-// count its arrival.
-template <int TG, int NTE>
-__device__ __forceinline__ void mlp_store_piece(float* slot, bool has_h, bool has_e, const float (&hc)[4 * TG],
-                                                const float (&ec)[4 * TG * NTE]) {
+// A cut item's piece: store its sums (the phases it covers) in its slot of
+// PF floats, 16 bytes per lane with the cache-policy bit of a device-scope
+// store (written through to memory, where the last piece's device-coherent
+// loads find them on any XCD).
+template <int TG, int NTE, int PF>
+__device__ __forceinline__ void mlp_store_piece(float* slot, bool has_h, bool has_e, const f32x4 (&hc)[TG],
+                                                const f32x4 (&ec)[TG * NTE]) {
+    constexpr int kSc1 = 16;   // cache-policy bits of a device-coherent store
     const int tid = threadIdx.x;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, PF * 4, 0x00020000);
     if (has_h) {
 #pragma unroll
-        for (int i = 0; i < 4 * TG; ++i) store_coherent(slot + tid + 256 * i, hc[i]);
+        for (int i = 0; i < TG; ++i)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, hc[i]), rs, (4 * tid + 1024 * i) * 4, 0,
+                                                   kSc1);
     }
     if (has_e) {
 #pragma unroll
-        for (int i = 0; i < 4 * TG * NTE; ++i) store_coherent(slot + TG * 1024 + tid + 256 * i, ec[i]);
+        for (int i = 0; i < TG * NTE; ++i)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, ec[i]), rs,
+                                                   (TG * 1024 + 4 * tid + 1024 * i) * 4, 0, kSc1);
     }
 }
 
@@ -628,15 +636,15 @@ __global__ __launch_bounds__(256, 1) void mlp_dma_kernel(MlpDmaArgs a) {
         pcs.slot0 = __builtin_amdgcn_readfirstlane(pcs.slot0);
         pcs.ph1 = __builtin_amdgcn_readfirstlane(pcs.ph1);
         pcs.pe0 = __builtin_amdgcn_readfirstlane(pcs.pe0);
-        float hc[T::HC], ec[T::EC];
+        f32x4 hc[TG], ec[TG * NTE];
         mlp_piece_run<TG, NTE, PAIRED, SW, SX>(a, sg, dyn, hc, ec);
 
         // ---- a cut item: store this piece; the last to arrive sums them
         float* csc = reinterpret_cast<float*>(dyn);   // [TG][1024] h, then [TG][NTE][1024] e
         bool last = true;
         if (pcs.npieces > 1) {
-            mlp_store_piece<TG, NTE>(a.partial + (size_t)pcs.slot(g - pcs.gfirst) * T::PF, c0 < a.nkh, c1 > a.nkh,
-                                     hc, ec);
+            mlp_store_piece<TG, NTE, T::PF>(a.partial + (size_t)pcs.slot(g - pcs.gfirst) * T::PF, c0 < a.nkh,
+                                            c1 > a.nkh, hc, ec);
             wait_memory();
             __syncthreads();   // every thread's piece is stored
             int* flag = reinterpret_cast<int*>(csc);
