@@ -638,9 +638,14 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     __shared__ int s_hist[256];
     __shared__ int s_sel[2];
     __shared__ int s_count, s_nflag, s_ncand;
-    __shared__ float cand_v[kMergeCap + 1];   // the last slot takes discarded stores
-    __shared__ int cand_i[kMergeCap + 1];
-    __shared__ int s_flag[kMaxSplits];
+    // candidate buffer: every entry of the launch's slices fits (the last
+    // slot takes discarded stores); sized by SPT so that launches with few
+    // slices keep more workgroups per CU
+    constexpr int CAP = 256 * SPT * KEEP;
+    static_assert(CAP >= kMaxTopk + 256 && CAP <= kMergeCap, "sorted head and slow-path scratch fit");
+    __shared__ float cand_v[CAP + 1];
+    __shared__ int cand_i[CAP + 1];
+    __shared__ int s_flag[256 * SPT];
     __shared__ float s_colv[512];   // logits of a re-evaluated group of 16 tiles (bf16)
 
     const int row = blockIdx.x;
@@ -729,7 +734,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
 #pragma unroll
         for (int e = 0; e < KEEP; ++e) {
             const bool q = e < nq[j];
-            const int dst = q ? pos : kMergeCap;
+            const int dst = q ? pos : CAP;
             cand_v[dst] = field(j, 4 + e);
             cand_i[dst] = __float_as_int(field(j, 4 + KEEP + e));
             pos += q ? 1 : 0;
@@ -740,7 +745,7 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
         // many candidates: keep those at or above the exact K-th largest
         // value (at least K of them; more only with ties)
         const unsigned tk = kth_largest_ord(cand_v, c, K, s_hist, s_sel);
-        constexpr int CPT = kMergeCap / 256;
+        constexpr int CPT = CAP / 256;
         float rv[CPT];
         int ri[CPT];
 #pragma unroll
@@ -834,8 +839,8 @@ __global__ __launch_bounds__(256) void merge_topk_kernel(MergeArgs a) {
     // exact slow path for slices that may hide a qualifying logit
     const int nflag = s_nflag;
     if (nflag > 0) {
-        float* buf_v = cand_v + kMergeCap - 256;   // scratch past the sorted head (K <= kMaxTopk)
-        int* buf_i = cand_i + kMergeCap - 256;
+        float* buf_v = cand_v + CAP - 256;   // scratch past the sorted head (K <= kMaxTopk)
+        int* buf_i = cand_i + CAP - 256;
         const T* xr = reinterpret_cast<const T*>(a.x) + (size_t)row * a.ldx;
         const T* wb = reinterpret_cast<const T*>(a.w);
         for (int f = 0; f < nflag; ++f) {
@@ -1007,16 +1012,19 @@ hipError_t launch_lmhead_topk(const void* x, long ldx, const void* w, int rows, 
     if (e != hipSuccess) return e;
     if (ev_end != nullptr && hipEventRecord(ev_end, stream) != hipSuccess) return hipErrorInvalidHandle;
     MergeArgs ma{part, p.nsplit(), p.map, K, V, d, inv_t, sl2, out_idx, out_lp, out_lse, x, ldx, w, diag};
-    const bool two = p.nsplit() <= 512;   // two slices per thread, else the most a launch may have
+    // slices per thread: two, four or the most a launch may have
+    const int ns = p.nsplit();
     if (bf16 && longl) {
-        if (two)
+        if (ns <= 512)
             hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeepLong, 2>), dim3(rows), dim3(256), 0, stream, ma);
         else
             hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeepLong, kMaxSplitsLong / 256>), dim3(rows), dim3(256),
                                0, stream, ma);
     } else if (bf16) {
-        if (two)
+        if (ns <= 512)
             hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep, 2>), dim3(rows), dim3(256), 0, stream, ma);
+        else if (ns <= 1024)
+            hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep, 4>), dim3(rows), dim3(256), 0, stream, ma);
         else
             hipLaunchKernelGGL((merge_topk_kernel<uint16_t, kKeep, kMaxSplits / 256>), dim3(rows), dim3(256), 0,
                                stream, ma);
