@@ -21,6 +21,10 @@ constexpr int part_stride(int keep) { return 4 + 2 * keep; }
 // list for the same rate of overflowing lanes).
 constexpr int kLane = 4;
 constexpr int kLaneMfma = 2;
+// 256-row blocks (the batched steps: thousands of rows, so a lane holding
+// three of a row's best 32 logits, which a two-entry list flags for the
+// exact slow path, turns up in a sizeable share of launches)
+constexpr int kLaneMfmaMulti = 3;
 constexpr int kLaneMfmaLong = 3;
 constexpr int kLaneMfmaWide = 3;
 constexpr int kLaneMfmaWideLong = 5;

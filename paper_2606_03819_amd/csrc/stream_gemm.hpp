@@ -522,7 +522,8 @@ struct EpiLmHead {
     int V;
     float sl2;       // inv_temperature * log2(e)
     static constexpr bool WIDE = WM * 16 > 64;
-    static constexpr int KL = LONG ? (WIDE ? kLaneMfmaWideLong : kLaneMfmaLong) : (WIDE ? kLaneMfmaWide : kLaneMfma);
+    static constexpr int KL = LONG ? (WIDE ? kLaneMfmaWideLong : kLaneMfmaLong)
+                                   : (WIDE ? kLaneMfmaWide : (NT >= 8 ? kLaneMfmaMulti : kLaneMfma));
     static constexpr int KEEP = LONG ? kKeepLong : kKeep;
     static constexpr int NC = 2 * WA;             // contributor lists per row
     static constexpr int MERGE_WORDS = 3 + 2 * KL;
