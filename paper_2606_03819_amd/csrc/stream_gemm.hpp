@@ -539,32 +539,40 @@ struct EpiLmHead {
     // of which those before t1 lie in the slice (a wave-uniform test) and
     // tokens from V on are left out.  Each logit becomes a key: its truncated
     // value (logit_trunc) with the lane-local position p (tokens in
-    // increasing id) stored as TAG - p in the cleared bits.  Keys are
+    // increasing id) stored as PB - p in the cleared bits, PB the last
+    // position (so most tags are inline constants of the and-or that forms
+    // the key, one instruction instead of two).  Keys are
     // distinct, and for positive values their order is the (value desc, id
     // asc) order; equal negative values rank the larger id first, and when
     // that drops the smaller one the bound reaches the listed value, so the
     // merge re-evaluates the slice and the result stays exact.  The KL + 1
-    // best keys cost one max and KL medians per logit (the lists' ids come
-    // from the tags at the end), the exponentials a second pass.  The
+    // best keys cost KL + 1 medians per logit (the maximum as a median with
+    // +inf, held in a scalar register the compiler cannot see through: as a
+    // max it would first quiet each key, one more instruction per logit), the
+    // lists' ids coming from the tags at the end; the exponentials take a
+    // second pass.  The
     // hardware exp2 flushes results below 2^-126 to zero: the sum starts at
     // the row maximum's term, about 1.
     __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NTW], int nt, int vbase0, int tw, int t1,
                                              float* c) const {
         constexpr int TAG = (1 << kLogitTagBits) - 1;
-        static_assert(WM * 16 <= TAG + 1 && 16 > KL, "positions fit the tag bits; one tile fills a list");
+        constexpr int PB = WM * 16 - 1;   // last lane-local position
+        static_assert(PB <= TAG && 16 > KL, "positions fit the tag bits; one tile fills a list");
         float k[KL + 1];
 #pragma unroll
         for (int q = 0; q <= KL; ++q) k[q] = neg_inf();
+        float pinf;
+        asm("s_mov_b32 %0, 0x7f800000" : "=s"(pinf));
         auto insert = [&](float key) {
             float n[KL + 1];
-            n[0] = fmaxf(k[0], key);
+            n[0] = __builtin_amdgcn_fmed3f(k[0], key, pinf);
 #pragma unroll
             for (int q = 1; q <= KL; ++q) n[q] = __builtin_amdgcn_fmed3f(k[q - 1], k[q], key);
 #pragma unroll
             for (int q = 0; q <= KL; ++q) k[q] = n[q];
         };
         auto key_of = [&](int mt, int j) {
-            return __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (TAG - (mt * 16 + j)));
+            return __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (PB - (mt * 16 + j)));
         };
         // wave-uniform branches: a tile past the slice is skipped, only a tile
         // reaching past the vocabulary pays for the per-token test
@@ -604,7 +612,7 @@ struct EpiLmHead {
 #pragma unroll
         for (int q = 0; q < KL; ++q) {
             const bool ok = k[q] != neg_inf();
-            const int p = TAG - (__float_as_int(k[q]) & TAG);
+            const int p = PB - (__float_as_int(k[q]) & TAG);
             c[3 + q] = ok ? logit_trunc(k[q]) : neg_inf();
             c[3 + KL + q] = __int_as_float(ok ? vbase0 + 32 * (p >> 4) + 8 * ((p >> 2) & 3) + (p & 3) : -1);
         }
