@@ -571,39 +571,41 @@ struct EpiLmHead {
 #pragma unroll
             for (int q = 0; q <= KL; ++q) k[q] = n[q];
         };
-        auto key_of = [&](int mt, int j) {
-            return __int_as_float((__float_as_int(acc[mt][nt][j]) & ~TAG) | (PB - (mt * 16 + j)));
-        };
-        // wave-uniform branches: a tile past the slice is skipped, only a tile
-        // reaching past the vocabulary pays for the per-token test
+        // one pass: a tile's logits are read once, ranked, then summed as
+        // exponentials relative to the running maximum (the truncated best
+        // key so far), the sum so far rescaled when the maximum grows; the
+        // hardware exp2 flushes terms below 2^-126 of the maximum's to zero
+        float m = neg_inf(), s = 0.f;
 #pragma unroll
         for (int mt = 0; mt < WM; ++mt) {
-            if (tw + mt >= t1) continue;
-            if ((tw + mt + 1) * 32 <= V) {
+            if (tw + mt >= t1) continue;   // wave-uniform: a tile past the slice
+            const bool full = (tw + mt + 1) * 32 <= V;   // wave-uniform: else the per-token test
+            float xv[16];
 #pragma unroll
-                for (int j = 0; j < 16; ++j) insert(key_of(mt, j));
+            for (int j = 0; j < 16; ++j) xv[j] = acc[mt][nt][j];
+            auto key = [&](int j) { return __int_as_float((__float_as_int(xv[j]) & ~TAG) | (PB - (mt * 16 + j))); };
+            auto valid = [&](int j) { return vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V; };
+            if (full) {
+#pragma unroll
+                for (int j = 0; j < 16; ++j) insert(key(j));
             } else {
 #pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    insert(vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V ? key_of(mt, j) : neg_inf());
+                for (int j = 0; j < 16; ++j) insert(valid(j) ? key(j) : neg_inf());
             }
-        }
-        const float m = logit_trunc(k[0]);
-        float s = 0.f;
-        if (m != neg_inf()) {
-            const float ms = m * sl2;
+            const float mn = logit_trunc(k[0]);
+            if (mn != neg_inf()) {
+                const float ms = mn * sl2;
+                float t = 0.f;
+                if (full) {
 #pragma unroll
-            for (int mt = 0; mt < WM; ++mt) {
-                if (tw + mt >= t1) continue;
-                if ((tw + mt + 1) * 32 <= V) {
-#pragma unroll
-                    for (int j = 0; j < 16; ++j) s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
+                    for (int j = 0; j < 16; ++j) t += __builtin_amdgcn_exp2f(fmaf(xv[j], sl2, -ms));
                 } else {
 #pragma unroll
                     for (int j = 0; j < 16; ++j)
-                        if (vbase0 + 32 * mt + 8 * (j >> 2) + (j & 3) < V)
-                            s += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][j], sl2, -ms));
+                        if (valid(j)) t += __builtin_amdgcn_exp2f(fmaf(xv[j], sl2, -ms));
                 }
+                s = s * __builtin_amdgcn_exp2f((m - mn) * sl2) + t;   // m = -inf: s is still 0
+                m = mn;
             }
         }
         c[0] = m;
