@@ -549,10 +549,8 @@ struct EpiLmHead {
     // best keys cost KL + 1 medians per logit (the maximum as a median with
     // +inf, held in a scalar register the compiler cannot see through: as a
     // max it would first quiet each key, one more instruction per logit), the
-    // lists' ids coming from the tags at the end; the exponentials take a
-    // second pass.  The
-    // hardware exp2 flushes results below 2^-126 to zero: the sum starts at
-    // the row maximum's term, about 1.
+    // lists' ids coming from the tags at the end; the exponentials follow in
+    // the same pass, tile by tile (below).
     __device__ __forceinline__ void lane_row(const f32x16 (&acc)[WM][NTW], int nt, int vbase0, int tw, int t1,
                                              float* c) const {
         constexpr int TAG = (1 << kLogitTagBits) - 1;
